@@ -1,0 +1,453 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix (no GPU).
+
+Each check is independent of the oracle's own formulas: hand-worked fixtures under tests/golden/, closed forms
+(exact singular values of generated low-rank matrices, Eckart-Young), an independent library routine (LAPACK's
+symmetric eigensolver instead of the oracle's SVD, torch's float32->bfloat16 cast), brute force with pure-Python
+loops on tiny inputs, and invariants (rank-0 identity, permuted block tables).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import kvc_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _num(x):
+    if isinstance(x, str):
+        return -0.0 if x == "-0" else float(eval(x, {"sqrt": math.sqrt}))
+    return float(x)
+
+
+def _arr(rows):
+    return np.array([[_num(v) for v in r] for r in rows], dtype=np.float64)
+
+
+def _bf16_torch(x32: np.ndarray) -> np.ndarray:
+    t = torch.from_numpy(np.ascontiguousarray(x32, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+# ------------------------------------------------------------------------------------------------ storage rounding
+
+def test_bf16_decode_roundtrip_all_patterns():
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    vals = O.bf16_bits_to_f64(bits)
+    ok = ~np.isnan(vals)
+    assert np.array_equal(O.f64_to_bf16_bits(vals[ok]), bits[ok])
+    assert np.all(np.isnan(O.bf16_bits_to_f64(O.f64_to_bf16_bits(vals[~ok]))))
+
+
+def test_bf16_rounding_matches_torch_on_binary32_inputs():
+    rng = np.random.default_rng(5)
+    raw = rng.integers(0, 1 << 32, size=200000, dtype=np.uint64).astype(np.uint32)
+    x32 = raw.view(np.float32)
+    x32 = x32[np.isfinite(x32)]
+    extra = np.array([0.0, -0.0, 1.0, -1.0, 3.0e38, -3.0e38, 1e-40, -1e-40, 1.00390625, 1.01171875],
+                     dtype=np.float32)
+    x32 = np.concatenate([x32, extra, rng.standard_normal(100000).astype(np.float32)])
+    assert np.array_equal(O.f64_to_bf16_bits(x32.astype(np.float64)), _bf16_torch(x32))
+
+
+def test_bf16_rounding_is_single_rounding_from_binary64():
+    # 1 + 2^-8 is the midpoint between bfloat16 1.0 (0x3F80) and 1 + 2^-7 (0x3F81).  A value just above it must go
+    # up even though rounding it to binary32 first would land exactly on the midpoint and then tie to even.
+    half = 2.0 ** -8
+    cases = {
+        1.0 + half + 2.0 ** -40: 0x3F81,
+        1.0 + half - 2.0 ** -40: 0x3F80,
+        1.0 + half: 0x3F80,                 # tie -> even
+        1.0 + 3 * half: 0x3F82,             # tie -> even
+        -(1.0 + half + 2.0 ** -40): 0xBF81,
+        float("inf"): 0x7F80,
+        -float("inf"): 0xFF80,
+        -0.0: 0x8000,
+        1e39: 0x7F80,                       # beyond the largest bfloat16
+    }
+    got = O.f64_to_bf16_bits(np.array(list(cases.keys())))
+    assert [int(g) for g in got] == list(cases.values())
+    nan_bits = O.f64_to_bf16_bits(np.array([float("nan")]))
+    assert np.isnan(O.bf16_bits_to_f64(nan_bits))[0]
+
+
+def test_f32_rounding_is_ieee():
+    x = np.array([1.0 + 2.0 ** -24, 1.0 + 2.0 ** -24 + 2.0 ** -50, 1.0 + 3 * 2.0 ** -24])
+    assert O.f64_to_f32(x).view(np.uint32).tolist() == [0x3F800000, 0x3F800001, 0x3F800002]
+
+
+# ------------------------------------------------------------------------------------------------ apply
+
+def _golden_cache(g, dtype):
+    nb, bs, H, d = g["num_blocks"], g["block_size"], g["num_kv_heads"], g["head_dim"]
+    pool = np.full((nb, bs, H, d), 99.0)
+    src = _arr(g["src_rows"])
+    for (blk, slot), row in zip(g["src_locations"], src):
+        pool[blk, slot, 0] = row
+    stored = O.to_storage(pool, dtype)
+    return O.Cache(dtype, bs, [stored], [stored.copy()])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_apply_worked_example(dtype):
+    g = _load("apply_worked_example.json")
+    cache = _golden_cache(g, dtype)
+    coef = _arr(g["coef"])
+    basis = _arr(g["basis"])
+    T, Ts = g["num_tokens"], g["state_tokens"]
+    st = O.State(O.to_storage(coef[None, None, None].repeat(2, axis=1), dtype),
+                 basis[None, None, None].repeat(2, axis=1).astype(np.float32), None, dtype)
+    item = O.Item(T, g["src_offset"], g["dst_offset"], np.array(g["src_table"]), np.array(g["dst_table"]), st)
+    assert st.num_tokens == Ts
+    out = O.apply(cache, [item])
+    exp = _arr(g["expected_rows"])
+    for kv in range(2):
+        for (blk, slot), row in zip(g["dst_locations"], exp):
+            got = out.pool(0, kv)[blk, slot, 0]
+            assert np.array_equal(O.to_f64(got, dtype), row)
+            # signed zeros: the copied -0 stays -0; the corrected 0.5 + (-0.5) is +0
+            assert np.array_equal(np.signbit(O.to_f64(got, dtype)), np.signbit(row))
+        # the source rows are untouched
+        for (blk, slot), row in zip(g["src_locations"], _arr(g["src_rows"])):
+            assert np.array_equal(O.to_f64(out.pool(0, kv)[blk, slot, 0], dtype), row)
+
+
+def _brute_apply_rows(src, coef, basis):
+    """Pure-Python loops: out[t][j] = src[t][j] + sum_k coef[t][k] * basis[k][j] for covered rows."""
+    out = [list(map(float, r)) for r in src]
+    for t in range(len(coef)):
+        for j in range(len(basis[0])):
+            acc = float(src[t][j])
+            for k in range(len(basis)):
+                acc += float(coef[t][k]) * float(basis[k][j])
+            out[t][j] = acc
+    return np.array(out)
+
+
+def test_apply_matches_brute_force_loops():
+    rng = np.random.default_rng(3)
+    T, Ts, r, d = 9, 7, 3, 5
+    src = rng.standard_normal((T, d)).astype(np.float32)
+    coef = rng.standard_normal((Ts, r))
+    basis = rng.standard_normal((r, d))
+    got = O.correct_rows(src, coef, basis, "f32")
+    ref = _brute_apply_rows(src.astype(np.float64), coef, basis)
+    assert np.allclose(got.astype(np.float64), ref, rtol=2 ** -23, atol=1e-12)
+    assert np.array_equal(got[Ts:], src[Ts:])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_apply_rank0_and_zero_coverage_are_bit_copies(dtype):
+    rng = np.random.default_rng(11)
+    T, d = 37, 8
+    vals = rng.standard_normal((T, d))
+    vals[0, 0] = -0.0
+    src = O.to_storage(vals, dtype)
+    if dtype == "bf16":
+        src[1, 1] = 0x7FC1       # a NaN payload survives a copy
+    for coef, basis in [(np.zeros((T, 0)), np.zeros((0, d))), (np.zeros((0, 4)), rng.standard_normal((4, d)))]:
+        out = O.correct_rows(src, coef, basis, dtype)
+        assert out.tobytes() == src.tobytes()
+
+
+def test_apply_through_permuted_tables_equals_contiguous():
+    rng = np.random.default_rng(4)
+    bs, H, d, T, r = 4, 2, 8, 13, 3
+    nblk_seq = -(-T // bs)
+    vals = rng.standard_normal((T, H, d))
+    coef = rng.standard_normal((1, 2, H, T, r))
+    basis = rng.standard_normal((1, 2, H, r, d)).astype(np.float32)
+    st = O.State(coef.astype(np.float32), basis, None, "f32")
+
+    # contiguous: src in blocks [0, nblk_seq), dst in [nblk_seq, 2 nblk_seq)
+    pool = np.zeros((2 * nblk_seq, bs, H, d), dtype=np.float32)
+    pool.reshape(-1, H, d)[:T] = vals
+    c1 = O.Cache("f32", bs, [pool], [pool.copy()])
+    o1 = O.apply(c1, [O.Item(T, 0, nblk_seq * bs, None, None, st)])
+    ref = o1.k[0].reshape(-1, H, d)[nblk_seq * bs: nblk_seq * bs + T]
+
+    # paged: the same rows behind a shuffled table, misaligned offsets on both sides
+    nb = 3 * nblk_seq + 2
+    perm = rng.permutation(nb)
+    src_tab, dst_tab = perm[:nblk_seq + 1], perm[nblk_seq + 1: 2 * nblk_seq + 2]
+    pool2 = np.zeros((nb, bs, H, d), dtype=np.float32)
+    c2 = O.Cache("f32", bs, [pool2], [pool2.copy()])
+    for kv in range(2):
+        for h in range(H):
+            O.write_rows(c2, 0, kv, h, src_tab, 3, vals[:, h].astype(np.float32))
+    o2 = O.apply(c2, [O.Item(T, 3, 1, src_tab, dst_tab, st)])
+    for h in range(H):
+        got = O.read_rows(o2, 0, 0, h, dst_tab, 1, T)
+        assert np.array_equal(got, ref[:, h])
+
+
+# ------------------------------------------------------------------------------------------------ fit (Eq. 7)
+
+def test_svd_worked_examples():
+    g = _load("svd_worked_examples.json")
+    for case in g["cases"]:
+        z = _arr(case["z"])
+        r = z.shape[1]
+        a, b, s = O.truncated_svd(z, r)
+        assert np.allclose(s, [_num(v) for v in case["sigma"]], atol=1e-14)
+        assert np.allclose(a, _arr(case["A"]), atol=1e-14)
+        assert np.allclose(b, _arr(case["B"]), atol=1e-14)
+        a1, b1, _ = O.truncated_svd(z, 1)
+        assert math.isclose(np.sum((z - a1 @ b1) ** 2), case["rank1_residual_sq"], rel_tol=1e-13)
+
+
+def _lowrank(rng, T, d, r, s):
+    u, _ = np.linalg.qr(rng.standard_normal((T, r)))
+    v, _ = np.linalg.qr(rng.standard_normal((d, r)))
+    return (u * s) @ v.T
+
+
+@pytest.mark.parametrize("T,d,r", [(64, 16, 4), (40, 32, 8), (16, 16, 16)])
+def test_fit_exact_rank_recovers_generator_singular_values(T, d, r):
+    rng = np.random.default_rng(T * d + r)
+    s = np.sort(rng.uniform(0.1, 1.0, r))[::-1]
+    z = _lowrank(rng, T, d, r, s)
+    a, b, sig = O.truncated_svd(z, r)
+    assert np.allclose(sig, s, rtol=1e-12, atol=1e-13)
+    assert np.allclose(a @ b, z, atol=1e-12)
+    assert np.allclose(b @ b.T, np.eye(r), atol=1e-12)                # B = R_r^T has orthonormal rows
+    assert np.allclose(a.T @ a, np.diag(sig ** 2), atol=1e-12)         # A = U_r Sigma_r
+
+
+def test_fit_eckart_young_against_independent_eigensolver():
+    rng = np.random.default_rng(8)
+    T, d = 50, 12
+    z = rng.standard_normal((T, d))
+    lam = np.sort(np.linalg.eigvalsh(z.T @ z))[::-1]                    # LAPACK dsyevd, not the SVD
+    for r in range(0, d + 1):
+        a, b, s = O.truncated_svd(z, r)
+        assert np.allclose(s, np.sqrt(lam[:r]), rtol=1e-10)
+        resid = np.sum((z - a @ b) ** 2)
+        assert math.isclose(resid, lam[r:].sum(), rel_tol=1e-9, abs_tol=1e-9)
+        # the product equals the projection on the top-r eigenvectors of Z^T Z
+        w, vecs = np.linalg.eigh(z.T @ z)
+        top = vecs[:, np.argsort(w)[::-1][:r]]
+        assert np.allclose(a @ b, z @ top @ top.T, atol=1e-9)
+
+
+def _power_top_pair(z, iters=2000):
+    """Pure-Python power iteration on Z^T Z for the leading singular triplet."""
+    n, d = len(z), len(z[0])
+    v = [1.0 / math.sqrt(d)] * d
+    for _ in range(iters):
+        zv = [sum(z[i][j] * v[j] for j in range(d)) for i in range(n)]
+        w = [sum(z[i][j] * zv[i] for i in range(n)) for j in range(d)]
+        nrm = math.sqrt(sum(x * x for x in w))
+        v = [x / nrm for x in w]
+    zv = [sum(z[i][j] * v[j] for j in range(d)) for i in range(n)]
+    return math.sqrt(sum(x * x for x in zv)), v
+
+
+def test_fit_top_triplet_matches_brute_force_power_iteration():
+    rng = np.random.default_rng(9)
+    z = rng.standard_normal((7, 4)) + np.outer(rng.standard_normal(7), [3.0, -1.0, 2.0, 0.5])
+    s1, v1 = _power_top_pair(z.tolist())
+    a, b, s = O.truncated_svd(z, 1)
+    assert math.isclose(s[0], s1, rel_tol=1e-10)
+    v1 = np.array(v1)
+    v1 = v1 if v1[np.argmax(np.abs(v1))] > 0 else -v1                 # canonical sign
+    assert np.allclose(b[0], v1, atol=1e-8)
+    assert np.allclose(a[:, 0], z @ v1, atol=1e-7)
+
+
+def test_fit_rank_above_data_rank_adds_zero_components():
+    rng = np.random.default_rng(10)
+    z = _lowrank(rng, 30, 10, 3, np.array([3.0, 2.0, 1.0]))
+    a, b, s = O.truncated_svd(z, 6)
+    assert np.allclose(s[3:], 0, atol=1e-12)
+    assert np.allclose(a @ b, z, atol=1e-12)
+    assert np.allclose(b @ b.T, np.eye(6), atol=1e-12)
+
+
+def test_canonical_sign_convention():
+    rng = np.random.default_rng(12)
+    z = rng.standard_normal((20, 6))
+    _, b, _ = O.truncated_svd(z, 6)
+    for row in b:
+        assert row[np.argmax(np.abs(row))] > 0
+    # exact ties: the first tied index is made positive
+    _, b, _ = O.truncated_svd(np.array([[2.0, 2.0], [1.0, -1.0]]), 2)
+    assert b[0, 0] > 0 and b[1, 0] > 0
+
+
+def _paired_cache(rng, dtype, T, H, d, L, bs, deviation):
+    """A two-sequence contiguous cache: src rows, then dst rows = src + deviation(layer, kv, head)."""
+    nb = 2 * (-(-T // bs))
+    pools = {}
+    for kv in range(2):
+        pools[kv] = []
+        for layer in range(L):
+            pool = np.zeros((nb, bs, H, d))
+            flat = pool.reshape(-1, H, d)
+            src = rng.standard_normal((T, H, d))
+            flat[:T] = src
+            for h in range(H):
+                flat[nb * bs // 2: nb * bs // 2 + T, h] = src[:, h] + deviation(layer, kv, h)
+            pools[kv].append(O.to_storage(pool, dtype))
+    return O.Cache(dtype, bs, pools[0], pools[1]), nb * bs // 2
+
+
+def test_fit_reads_dst_minus_src_through_pages():
+    rng = np.random.default_rng(13)
+    T, H, d, L, bs, r = 24, 2, 8, 2, 4, 3
+    devs = {}
+
+    def deviation(layer, kv, h):
+        devs[(layer, kv, h)] = _lowrank(rng, T, d, r, np.array([2.0, 1.0, 0.5]) * (1 + layer + kv + h))
+        return devs[(layer, kv, h)]
+
+    cache, dst_off = _paired_cache(rng, "f32", T, H, d, L, bs, deviation)
+    states, raw = O.fit(cache, [O.Item(T, 0, dst_off, None, None)], r)
+    coef, basis, sigma = raw[0]
+    for (layer, kv, h), dv in devs.items():
+        z = (O.read_rows(cache, layer, kv, h, None, dst_off, T).astype(np.float64)
+             - O.read_rows(cache, layer, kv, h, None, 0, T).astype(np.float64))
+        # float32 storage makes z rank 3 only up to rounding: compare with the projection of z on the top-3
+        # eigenvectors of z^T z (an independent LAPACK routine), and with z itself at storage precision
+        w, vecs = np.linalg.eigh(z.T @ z)
+        top = vecs[:, np.argsort(w)[::-1][:r]]
+        assert np.allclose(coef[layer, kv, h] @ basis[layer, kv, h], z @ top @ top.T, atol=1e-10)
+        assert np.allclose(coef[layer, kv, h] @ basis[layer, kv, h], z, atol=1e-5)
+        # the stored float32 deviation is the generated one up to float32 storage of both caches
+        assert np.allclose(z, dv, atol=1e-5)
+        assert np.allclose(sigma[layer, kv, h], np.array([2.0, 1.0, 0.5]) * (1 + layer + kv + h), rtol=1e-5)
+    # base mode factorises the dst cache itself
+    _, raw_base = O.fit(cache, [O.Item(T, 0, dst_off, None, None)], d, mode=O.MODE_BASE)
+    cb, bb, _ = raw_base[0]
+    assert np.allclose(cb[1, 0, 1] @ bb[1, 0, 1], O.read_rows(cache, 1, 0, 1, None, dst_off, T), atol=1e-12)
+
+
+def test_fit_prefix_coverage_uses_only_leading_rows():
+    rng = np.random.default_rng(14)
+    T, H, d, L, bs = 20, 1, 6, 1, 4
+    cache, dst_off = _paired_cache(rng, "f32", T, H, d, L, bs, lambda *a: rng.standard_normal((T, d)))
+    states, raw = O.fit(cache, [O.Item(T, 0, dst_off, None, None)], 2, state_tokens=[11])
+    z = (O.read_rows(cache, 0, 1, 0, None, dst_off, 11).astype(np.float64)
+         - O.read_rows(cache, 0, 1, 0, None, 0, 11).astype(np.float64))
+    a, b, s = O.truncated_svd(z, 2)
+    assert states[0].num_tokens == 11
+    assert np.allclose(raw[0][0][0, 1, 0] @ raw[0][1][0, 1, 0], a @ b, atol=1e-12)
+
+
+# ------------------------------------------------------------------------------------------------ chain (Eq. 6)
+
+def _state_from(a_list, b_list, dtype="f32"):
+    """One-layer, one-head state whose K and V units carry the same factors."""
+    a = np.asarray(a_list, dtype=np.float64)
+    b = np.asarray(b_list, dtype=np.float64)
+    coef = np.stack([a, a])[None, :, None]
+    basis = np.stack([b, b])[None, :, None].astype(np.float32)
+    return O.State(O.to_storage(coef, dtype), basis, None, dtype)
+
+
+def test_chain_worked_example():
+    g = _load("chain_worked_example.json")
+    s1 = _state_from(g["first"]["A"], g["first"]["B"])
+    s2 = _state_from(g["second"]["A"], g["second"]["B"])
+    for key, r in (("rank2", 2), ("rank1", 1)):
+        _, (coef, basis, sigma) = O.chain(s1, s2, r)
+        assert np.allclose(sigma[0, 0, 0], g[key]["sigma"], atol=1e-14)
+        assert np.allclose(coef[0, 0, 0], _arr(g[key]["A"]), atol=1e-14)
+        assert np.allclose(basis[0, 0, 0], _arr(g[key]["B"]), atol=1e-14)
+
+
+def test_chain_lossless_equals_sum_and_eq6_identity():
+    rng = np.random.default_rng(15)
+    T, d, r1, r2 = 40, 16, 3, 4
+    d1 = _lowrank(rng, T, d, r1, np.array([3.0, 2.0, 1.0]))
+    d2 = _lowrank(rng, T, d, r2, np.array([2.5, 1.5, 1.0, 0.5]))
+    a1, b1, _ = O.truncated_svd(d1, r1)
+    a2, b2, _ = O.truncated_svd(d2, r2)
+    s1, s2 = _state_from(a1, b1), _state_from(a2, b2)
+    # Eq. 6: the correction from agent i to agent k equals the sum of the two consecutive corrections
+    _, (coef, basis, sigma) = O.chain(s1, s2, r1 + r2)
+    c0 = rng.standard_normal((T, d))
+    c1 = c0 + d1
+    c2 = c1 + d2
+    prod = coef[0, 0, 0] @ basis[0, 0, 0]
+    assert np.allclose(prod, (a1 @ b1).astype(np.float32).astype(np.float64)
+                       + (a2 @ b2).astype(np.float32).astype(np.float64), atol=1e-5)
+    assert np.allclose(prod, c2 - c0, atol=1e-5)
+    # and equals a direct fit of the non-chained deviation C2 - C0 (Eq. 6, chained == non-chained when exact)
+    a02, b02, _ = O.truncated_svd(c2 - c0, r1 + r2)
+    assert np.allclose(prod, a02 @ b02, atol=1e-5)
+
+
+def test_chain_orthogonal_states_keep_union_of_singular_values():
+    rng = np.random.default_rng(16)
+    T, d = 30, 10
+    u, _ = np.linalg.qr(rng.standard_normal((T, 5)))
+    v, _ = np.linalg.qr(rng.standard_normal((d, 5)))
+    s_a, s_b = np.array([5.0, 3.0, 1.0]), np.array([4.0, 2.0])
+    a1, b1 = u[:, :3] * s_a, v[:, :3].T
+    a2, b2 = u[:, 3:] * s_b, v[:, 3:].T
+    s1, s2 = _state_from(a1, b1, "f32"), _state_from(a2, b2, "f32")
+    for r_out in range(1, 6):
+        _, (_, _, sigma) = O.chain(s1, s2, r_out)
+        assert np.allclose(sigma[0, 0, 0], [5, 4, 3, 2, 1][:r_out], atol=1e-5)
+
+
+def test_chain_shared_subspace_truncation_is_exact():
+    # both corrections live in one rank-3 row space (the long-context workload's structure)
+    rng = np.random.default_rng(17)
+    T, d, r = 25, 9, 3
+    v, _ = np.linalg.qr(rng.standard_normal((d, r)))
+    w1, w2 = rng.standard_normal((T, r)), rng.standard_normal((T, r))
+    s1, s2 = _state_from(w1, v.T), _state_from(w2, v.T)
+    _, (coef, basis, sigma) = O.chain(s1, s2, r)
+    ref = (w1.astype(np.float32).astype(np.float64) + w2.astype(np.float32).astype(np.float64)) \
+        @ v.T.astype(np.float32).astype(np.float64)
+    assert np.allclose(coef[0, 0, 0] @ basis[0, 0, 0], ref, atol=1e-10)
+
+
+def test_chain_pads_shorter_state_with_zero_rows():
+    rng = np.random.default_rng(18)
+    d = 6
+    a1, b1 = rng.standard_normal((10, 2)), np.linalg.qr(rng.standard_normal((d, 2)))[0].T
+    a2, b2 = rng.standard_normal((14, 2)), np.linalg.qr(rng.standard_normal((d, 2)))[0].T
+    s1, s2 = _state_from(a1, b1), _state_from(a2, b2)
+    st, (coef, basis, _) = O.chain(s1, s2, 4)
+    assert st.num_tokens == 14
+    m = np.zeros((14, d))
+    m[:10] += s1.coef_f64(0, 0, 0) @ s1.basis_f64(0, 0, 0)
+    m += s2.coef_f64(0, 0, 0) @ s2.basis_f64(0, 0, 0)
+    assert np.allclose(coef[0, 0, 0] @ basis[0, 0, 0], m, atol=1e-12)
+
+
+# ------------------------------------------------------------------------------------------------ metrics
+
+def test_memory_example_is_fifty_gib():
+    g = _load("memory_example.json")
+    got = O.full_dimensional_pool_bytes(g["num_anchors"], g["num_consumers"], g["num_layers"], g["num_kv_heads"],
+                                        g["head_dim"], g["num_tokens"], g["elem_bytes"])
+    assert got == g["expected_bytes"] == g["expected_gib"] * 2 ** 30
+
+
+def test_lowrank_state_bytes_closed_form():
+    # Section 3.3: O(VNr(L+D)) per pool; per unit r (T + d) numbers plus sigma
+    assert O.lowrank_state_bytes(1, 1, 128, 4096, 32, 2, with_sigma=False) == 2 * (32 * 4096 * 2 + 32 * 128 * 4)
+    assert O.lowrank_state_bytes(32, 8, 128, 32768, 32, 2) == 512 * (32768 * 32 * 2 + 32 * 128 * 4 + 32 * 4)
+
+
+def test_effective_rank_and_error_metric():
+    # energies 9, 4, 1, 0.25: 90 % of 14.25 needs the first two (13 / 14.25 = 0.912)
+    assert O.effective_rank(np.array([3.0, 2.0, 1.0, 0.5])) == 2
+    assert O.effective_rank(np.array([1.0, 1.0, 1.0, 1.0, 1.0, 1.0, 1.0, 1.0, 1.0, 1.0])) == 9
+    assert O.effective_rank(np.zeros(3)) == 0
+    c = np.array([[3.0, 4.0]])
+    assert math.isclose(O.normalized_frobenius_error(c + np.array([[0.0, 1.0]]), c), 0.2)
+    assert math.isclose(O.max_relative_error(np.array([1.0, -2.5]), np.array([1.0, -2.0])), 0.25)
