@@ -1,0 +1,161 @@
+/*
+ * kvc.h -- C ABI of libkvc: online low-rank KV-cache correction for shared context across agents (KVCMAS).
+ *
+ * Three operations on a paged K/V cache, all asynchronous on the caller's HIP stream:
+ *
+ *   kvc_fit_state  Eq. 12 then Eq. 7.  For each (layer, K/V, KV head) unit of an item, Z = C_dst - C_src over the
+ *                  first T_s rows (the observed transition after a dense prefill, with identity alignment), or
+ *                  Z = C_dst (a base cache, Section 3.3), and its rank-r truncated SVD Z ~ A B with A = U_r Sigma_r
+ *                  (T_s x r, "coef") and B = R_r^T (r x d, "basis", orthonormal rows), plus sigma.
+ *   kvc_apply      Eq. 4 with the source agent's materialised cache as the reference (Section 3.2, Eq. 6) and one
+ *                  state (Eq. 8 with a single anchor, w = 1): C_dst[t] = C_src[t] + A[t] B for t < T_s and
+ *                  C_dst[t] = C_src[t] (bit copy) for T_s <= t < T (Appendix A.3, "Variable Segment Lengths").
+ *   kvc_chain      Eq. 6 composed in low rank: from S1 = Delta_{j<-i} and S2 = Delta_{k<-j}, the rank-r_out truncated
+ *                  SVD of A1 B1 + A2 B2 (rows past a state's coverage are zero), without forming any T x d matrix.
+ *
+ * Layout.  One pool per layer for K and one for V.  Token slot s of physical block b of KV head h starts at element
+ *   b * block_stride + s * token_stride + h * head_stride
+ * of the layer's pool, and its head_dim elements are contiguous.  An item's token t sits at position p = offset + t of
+ * its block sequence: block = table[p / block_size] (or p / block_size when the table pointer is NULL, i.e.
+ * contiguous rows), slot = p % block_size.  A state's unit u = (layer, kv, head) with kv = 0 for K and 1 for V keeps
+ *   coef  [L][2][H][T_s][r]  (coef_dtype)      basis [L][2][H][r][d] (float32)      sigma [L][2][H][r] (float32)
+ *
+ * Ownership.  The caller allocates every buffer (pools, tables, states, workspaces, both copies of the item array);
+ * the library allocates nothing, keeps no pointer after a call returns, holds no global state and may be called
+ * from several threads.  Source rows are only read.
+ *
+ * Errors.  Every argument check runs on the host before anything is enqueued; on an error nothing is enqueued and
+ * the status says why.  A failed launch returns KVC_ERR_HIP (kvc_last_hip_error() gives the hipError_t of the
+ * calling thread).  Faults inside a kernel surface at the caller's next synchronisation.  Rows whose block-table
+ * entry lies outside [0, num_blocks) are neither read nor written.  NaN and Inf propagate.
+ */
+#ifndef KVC_H
+#define KVC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVC_VERSION 1
+#define KVC_MAX_RANK 128 /* largest r of a state */
+
+typedef enum kvc_status {
+  KVC_OK = 0,
+  KVC_ERR_NULL_ARG = 1,    /* a required pointer is NULL */
+  KVC_ERR_SHAPE = 2,       /* sizes inconsistent or out of range */
+  KVC_ERR_DTYPE = 3,       /* unknown dtype, or dtypes that do not go together */
+  KVC_ERR_ALIGN = 4,       /* a row or a coefficient array is not 16-byte aligned */
+  KVC_ERR_ALIAS = 5,       /* destination rows may overlap source rows */
+  KVC_ERR_WORKSPACE = 6,   /* workspace missing, misaligned or smaller than the query says */
+  KVC_ERR_UNSUPPORTED = 7, /* head_dim other than 64 or 128 */
+  KVC_ERR_HIP = 8          /* the HIP runtime refused a launch */
+} kvc_status;
+
+typedef enum kvc_dtype { KVC_F32 = 0, KVC_BF16 = 1 } kvc_dtype;
+
+typedef enum kvc_fit_mode {
+  KVC_FIT_DELTA = 0, /* Z = C_dst - C_src: the observed transition of Eq. 12 */
+  KVC_FIT_BASE = 1   /* Z = C_dst: a base cache (Z in {C, Delta}, Section 3.3); the src side is not read */
+} kvc_fit_mode;
+
+/* A paged K/V pool set.  k_layers / v_layers are HOST arrays of num_layers DEVICE pointers.  Strides are in
+ * elements; block_stride, token_stride and head_stride times the element size must be multiples of 16 bytes and
+ * every layer pointer 16-byte aligned.  head_dim is 64 or 128. */
+typedef struct kvc_cache {
+  kvc_dtype dtype;
+  int32_t num_layers;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t block_size;
+  int32_t num_blocks;
+  int64_t block_stride;
+  int64_t token_stride;
+  int64_t head_stride;
+  void* const* k_layers;
+  void* const* v_layers;
+} kvc_cache;
+
+/* Low-rank state of one sequence (Eq. 7): coef = A, basis = B per unit.  DEVICE pointers.  coef_dtype is the cache
+ * dtype for fit/apply (bf16 coefficients for bf16 caches, float32 for float32 caches).  0 <= rank <= min(head_dim,
+ * KVC_MAX_RANK); rank 0 makes apply a copy.  coef must be 16-byte aligned.  sigma may be NULL. */
+typedef struct kvc_state {
+  int32_t num_layers;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t num_tokens; /* T_s: coefficient rows per unit */
+  int32_t rank;
+  kvc_dtype coef_dtype;
+  void* coef;
+  float* basis;
+  float* sigma;
+} kvc_state;
+
+/* One shared segment of an agent edge.  apply reads `state`; fit writes it (its rank, num_tokens and pointers say
+ * what to produce: rows t < state.num_tokens are fitted).  state.num_tokens <= num_tokens. */
+typedef struct kvc_item {
+  int32_t num_tokens; /* T: rows of the segment */
+  int32_t src_offset; /* position of row 0 within the src block sequence */
+  int32_t dst_offset; /* position of row 0 within the dst block sequence */
+  int32_t reserved;   /* must be 0 */
+  kvc_state state;
+} kvc_item;
+
+/* A batch of independent items handled by one launch per kernel.  `items` is a HOST array used for checks and launch
+ * sizing; `items_dev` is a DEVICE array holding the same bytes, read by the kernels.  Tables are DEVICE int32 arrays
+ * [num_items][max_blocks] of physical block ids; NULL means the identity mapping (contiguous rows). */
+typedef struct kvc_batch {
+  int32_t num_items;
+  int32_t max_blocks;
+  const kvc_item* items;
+  const kvc_item* items_dev;
+  const int32_t* src_tables;
+  const int32_t* dst_tables;
+} kvc_batch;
+
+int32_t kvc_version(void);
+const char* kvc_status_str(kvc_status status);
+/* hipError_t of the last failed HIP call made by this thread inside the library (0 if none). */
+int32_t kvc_last_hip_error(void);
+
+/* Bytes of one low-rank state (coef + basis + sigma), the O(N r (L + D)) term of Section 3.3. */
+size_t kvc_state_bytes(int32_t num_layers, int32_t num_kv_heads, int32_t head_dim, int32_t num_tokens, int32_t rank,
+                       kvc_dtype coef_dtype);
+/* Bytes of the same segment kept full-dimensional (L x {K,V} x T x H d), the O(N L D) term of Section 3.1. */
+size_t kvc_dense_bytes(int32_t num_layers, int32_t num_kv_heads, int32_t head_dim, int32_t num_tokens,
+                       kvc_dtype dtype);
+
+/* Materialise each item's destination rows from its source rows and state, for layers [layer_begin, layer_end).
+ * One launch covers every item, layer, K/V and head of the call (a serving batch corrects a whole layer at once).
+ * Destination rows must not overlap any source row of the call; with NULL tables and equal pools the host checks the
+ * row ranges, with tables it rejects src_tables == dst_tables. */
+kvc_status kvc_apply(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
+                     hipStream_t stream);
+
+/* Workspace kvc_fit_state needs for this call (bytes, 256-byte aligned start required). */
+size_t kvc_fit_workspace_bytes(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin,
+                               int32_t layer_end);
+/* Fit each item's state for layers [layer_begin, layer_end); other layers of the state are left as they are.
+ * Sigma descending; each basis row has its largest-magnitude entry positive. */
+kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
+                         kvc_fit_mode mode, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace kvc_chain needs (bytes, 256-byte aligned start required). */
+size_t kvc_chain_workspace_bytes(const kvc_state* first, const kvc_state* second, const kvc_state* out,
+                                 int32_t layer_begin, int32_t layer_end);
+/* out = truncated SVD of first + second (Eq. 6), rank out->rank <= min(first->rank + second->rank, head_dim), for
+ * layers [layer_begin, layer_end).  out->num_tokens must equal max(first->num_tokens, second->num_tokens); all three
+ * share num_layers, num_kv_heads, head_dim and coef_dtype.  With out->rank = first->rank + second->rank <= head_dim
+ * the composition is lossless. */
+kvc_status kvc_chain(const kvc_state* first, const kvc_state* second, kvc_state* out, int32_t layer_begin,
+                     int32_t layer_end, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVC_H */

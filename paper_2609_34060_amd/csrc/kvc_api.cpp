@@ -1,0 +1,189 @@
+// Host entry points of libkvc: argument checks, launch sizing and dispatch.  Every check runs before anything is
+// enqueued; on an error nothing is enqueued.
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+
+#include "kvc.h"
+#include "kvc_launch.h"
+
+namespace {
+
+thread_local int32_t g_last_hip_error = 0;
+
+kvc_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return KVC_OK;
+  g_last_hip_error = static_cast<int32_t>(e);
+  return KVC_ERR_HIP;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t dtype_size(kvc_dtype t) { return t == KVC_BF16 ? 2 : 4; }
+
+bool valid_dtype(kvc_dtype t) { return t == KVC_F32 || t == KVC_BF16; }
+
+kvc_status check_cache(const kvc_cache* c, int32_t lb, int32_t le) {
+  if (!c) return KVC_ERR_NULL_ARG;
+  if (!valid_dtype(c->dtype)) return KVC_ERR_DTYPE;
+  if (c->head_dim != 64 && c->head_dim != 128) return KVC_ERR_UNSUPPORTED;
+  if (c->num_layers < 1 || c->num_kv_heads < 1 || c->block_size < 1 || c->num_blocks < 1) return KVC_ERR_SHAPE;
+  if (lb < 0 || le < lb || le > c->num_layers) return KVC_ERR_SHAPE;
+  if (c->block_stride < 1 || c->token_stride < 1 || c->head_stride < 1) return KVC_ERR_SHAPE;
+  const int64_t es = static_cast<int64_t>(dtype_size(c->dtype));
+  if ((c->block_stride * es) % 16 || (c->token_stride * es) % 16 || (c->head_stride * es) % 16) return KVC_ERR_ALIGN;
+  // a row must fit between two token slots and two heads (head_dim contiguous elements)
+  if (c->head_stride < c->head_dim && c->num_kv_heads > 1) return KVC_ERR_SHAPE;
+  if (le > lb && (!c->k_layers || !c->v_layers)) return KVC_ERR_NULL_ARG;
+  for (int32_t l = lb; l < le; ++l) {
+    if (!c->k_layers[l] || !c->v_layers[l]) return KVC_ERR_NULL_ARG;
+    if (!aligned16(c->k_layers[l]) || !aligned16(c->v_layers[l])) return KVC_ERR_ALIGN;
+  }
+  return KVC_OK;
+}
+
+kvc_status check_state_shape(const kvc_state& s, int32_t L, int32_t H, int32_t d) {
+  if (s.num_layers != L || s.num_kv_heads != H || s.head_dim != d) return KVC_ERR_SHAPE;
+  if (!valid_dtype(s.coef_dtype)) return KVC_ERR_DTYPE;
+  if (s.rank < 0 || s.rank > std::min<int32_t>(d, KVC_MAX_RANK) || s.num_tokens < 0) return KVC_ERR_SHAPE;
+  if (s.rank > 0 && s.num_tokens > 0) {
+    if (!s.coef || !s.basis) return KVC_ERR_NULL_ARG;
+    if (!aligned16(s.coef) || !aligned16(s.basis)) return KVC_ERR_ALIGN;
+  }
+  return KVC_OK;
+}
+
+// Rows [off, off + T) of a block sequence must stay inside its table row (or the pool for the identity mapping).
+bool positions_fit(int64_t off, int64_t T, bool has_table, const kvc_batch* b, const kvc_cache* c) {
+  if (off < 0) return false;
+  const int64_t end = off + T;
+  if (end > INT32_MAX) return false;
+  const int64_t cap = has_table ? static_cast<int64_t>(b->max_blocks) * c->block_size
+                                : static_cast<int64_t>(c->num_blocks) * c->block_size;
+  return T == 0 || end <= cap;
+}
+
+kvc_status check_batch(const kvc_cache* c, const kvc_batch* b, bool needs_src) {
+  if (!b) return KVC_ERR_NULL_ARG;
+  if (b->num_items < 0 || b->max_blocks < 0) return KVC_ERR_SHAPE;
+  if (b->num_items == 0) return KVC_OK;
+  if (!b->items || !b->items_dev) return KVC_ERR_NULL_ARG;
+  if ((b->src_tables || b->dst_tables) && b->max_blocks < 1) return KVC_ERR_SHAPE;
+  for (int32_t i = 0; i < b->num_items; ++i) {
+    const kvc_item& it = b->items[i];
+    if (it.reserved != 0 || it.num_tokens < 0) return KVC_ERR_SHAPE;
+    if (!positions_fit(it.dst_offset, it.num_tokens, b->dst_tables != nullptr, b, c)) return KVC_ERR_SHAPE;
+    if (needs_src && !positions_fit(it.src_offset, it.num_tokens, b->src_tables != nullptr, b, c))
+      return KVC_ERR_SHAPE;
+    kvc_status s = check_state_shape(it.state, c->num_layers, c->num_kv_heads, c->head_dim);
+    if (s != KVC_OK) return s;
+    if (it.state.coef_dtype != c->dtype) return KVC_ERR_DTYPE;
+    if (it.state.num_tokens > it.num_tokens) return KVC_ERR_SHAPE;
+  }
+  return KVC_OK;
+}
+
+void fill_pool_view(const kvc_cache* c, kvc::PoolView& pv) {
+  pv.block_stride = c->block_stride;
+  pv.token_stride = c->token_stride;
+  pv.head_stride = c->head_stride;
+  pv.block_size = c->block_size;
+  pv.num_blocks = c->num_blocks;
+  pv.num_kv_heads = c->num_kv_heads;
+  pv.head_dim = c->head_dim;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t kvc_version(void) { return KVC_VERSION; }
+
+const char* kvc_status_str(kvc_status s) {
+  switch (s) {
+    case KVC_OK: return "ok";
+    case KVC_ERR_NULL_ARG: return "null argument";
+    case KVC_ERR_SHAPE: return "inconsistent or out-of-range sizes";
+    case KVC_ERR_DTYPE: return "unsupported or mismatched dtype";
+    case KVC_ERR_ALIGN: return "pointer or stride not 16-byte aligned";
+    case KVC_ERR_ALIAS: return "destination rows may overlap source rows";
+    case KVC_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case KVC_ERR_UNSUPPORTED: return "unsupported head_dim (64 or 128)";
+    case KVC_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+int32_t kvc_last_hip_error(void) { return g_last_hip_error; }
+
+size_t kvc_state_bytes(int32_t L, int32_t H, int32_t d, int32_t T, int32_t r, kvc_dtype coef_dtype) {
+  if (L < 0 || H < 0 || d < 0 || T < 0 || r < 0 || !valid_dtype(coef_dtype)) return 0;
+  const size_t units = static_cast<size_t>(L) * 2 * H;
+  return units * (static_cast<size_t>(T) * r * dtype_size(coef_dtype) + static_cast<size_t>(r) * d * 4 +
+                  static_cast<size_t>(r) * 4);
+}
+
+size_t kvc_dense_bytes(int32_t L, int32_t H, int32_t d, int32_t T, kvc_dtype dtype) {
+  if (L < 0 || H < 0 || d < 0 || T < 0 || !valid_dtype(dtype)) return 0;
+  return static_cast<size_t>(L) * 2 * H * static_cast<size_t>(T) * d * dtype_size(dtype);
+}
+
+kvc_status kvc_apply(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
+                     hipStream_t stream) {
+  kvc_status s = check_cache(cache, layer_begin, layer_end);
+  if (s != KVC_OK) return s;
+  s = check_batch(cache, batch, true);
+  if (s != KVC_OK) return s;
+  if (batch->src_tables && batch->src_tables == batch->dst_tables) return KVC_ERR_ALIAS;
+  int max_tokens = 0, max_rank = 0;
+  for (int32_t i = 0; i < batch->num_items; ++i) {
+    const kvc_item& it = batch->items[i];
+    max_tokens = std::max(max_tokens, it.num_tokens);
+    max_rank = std::max(max_rank, it.state.rank);
+    if (!batch->src_tables && !batch->dst_tables && it.num_tokens > 0) {
+      const int64_t a0 = it.src_offset, a1 = a0 + it.num_tokens, b0 = it.dst_offset, b1 = b0 + it.num_tokens;
+      if (a0 < b1 && b0 < a1) return KVC_ERR_ALIAS;
+    }
+  }
+  if (batch->num_items == 0 || layer_end == layer_begin || max_tokens == 0) return KVC_OK;
+  kvc::ApplyArgs a;
+  std::memset(&a, 0, sizeof(a));
+  fill_pool_view(cache, a.pv);
+  a.items = batch->items_dev;
+  a.src_tables = batch->src_tables;
+  a.dst_tables = batch->dst_tables;
+  a.max_blocks = batch->max_blocks;
+  for (int32_t l0 = layer_begin; l0 < layer_end; l0 += kvc::kMaxLayersPerLaunch) {
+    const int32_t l1 = std::min(layer_end, l0 + kvc::kMaxLayersPerLaunch);
+    a.layer_begin = l0;
+    a.num_layers = l1 - l0;
+    for (int32_t l = l0; l < l1; ++l) {
+      a.layers.k[l - l0] = cache->k_layers[l];
+      a.layers.v[l - l0] = cache->v_layers[l];
+    }
+    // grid.z = items x layers must stay below 65536
+    const int32_t per_launch_items = std::max<int32_t>(1, 65535 / a.num_layers);
+    for (int32_t i0 = 0; i0 < batch->num_items; i0 += per_launch_items) {
+      const int32_t n = std::min(per_launch_items, batch->num_items - i0);
+      kvc::ApplyArgs ai = a;
+      ai.items = batch->items_dev + i0;
+      ai.src_tables = batch->src_tables ? batch->src_tables + static_cast<int64_t>(i0) * batch->max_blocks : nullptr;
+      ai.dst_tables = batch->dst_tables ? batch->dst_tables + static_cast<int64_t>(i0) * batch->max_blocks : nullptr;
+      s = hip_status(kvc::launch_apply(ai, cache->dtype, max_rank, max_tokens, n, stream));
+      if (s != KVC_OK) return s;
+    }
+  }
+  return KVC_OK;
+}
+
+size_t kvc_fit_workspace_bytes(const kvc_cache*, const kvc_batch*, int32_t, int32_t) { return 0; }
+kvc_status kvc_fit_state(const kvc_cache*, const kvc_batch*, int32_t, int32_t, kvc_fit_mode, void*, size_t,
+                         hipStream_t) {
+  return KVC_ERR_UNSUPPORTED;
+}
+size_t kvc_chain_workspace_bytes(const kvc_state*, const kvc_state*, const kvc_state*, int32_t, int32_t) { return 0; }
+kvc_status kvc_chain(const kvc_state*, const kvc_state*, kvc_state*, int32_t, int32_t, void*, size_t, hipStream_t) {
+  return KVC_ERR_UNSUPPORTED;
+}
+
+}  // extern "C"

@@ -1,0 +1,270 @@
+// kvc_apply kernels: C_dst[t] = C_src[t] + A[t] B for t < T_s, bit copy for T_s <= t < T (Eq. 4 with the source
+// agent's cache as reference, Eq. 8 with one state, prefix coverage of Appendix A.3).
+//
+// bf16 caches: one workgroup = 4 wave64s over one (item, layer, K/V, head) unit and a chunk of 512 tokens.  The
+// correction of a 16-token tile is the MFMA contraction  D^T = B^T A^T + C^T  with M = feature (16 per tile), N =
+// token, K = rank (32 per v_mfma_f32_16x16x32_bf16), and the accumulator C initialised with the source rows in fp32.
+// B is staged once per workgroup in LDS as a bf16 hi/lo pair (about 16 significant bits of the fp32 basis) and
+// held in registers as MFMA A-fragments; the bf16 coefficients are the MFMA B-operand, loaded straight from the
+// coefficient rows (one 16-byte load per lane and 32 ranks).  The M index of each tile is permuted so that the
+// four lanes holding one token own 64 contiguous bytes of the row per 16-byte load: every global load and store of
+// a cache row is 128-bit and a row is touched by whole 64-byte segments.
+//
+// float32 caches: a VALU kernel with the basis in LDS (float32 throughout, for the 1e-5 storage tolerance).
+#include "kvc_device.h"
+#include "kvc_launch.h"
+
+namespace kvc {
+
+constexpr int kApplyWaves = 4;
+constexpr int kApplyThreads = kApplyWaves * kWave;
+constexpr int kApplyTilesPerWave = 8;
+constexpr int kApplyChunk = kApplyWaves * kApplyTilesPerWave * 16;  // tokens per workgroup
+
+int apply_chunk_tokens() { return kApplyChunk; }
+
+// Feature held by MFMA row m of M-tile mt: the lanes of token-group g = m / 4 own features 32 q + 8 g + [0, 8) of
+// 16-byte load q = mt / 2, the first four in M-tile 2q and the last four in 2q + 1.
+__device__ __forceinline__ int apply_feature(int mt, int m) {
+  return 32 * (mt >> 1) + 8 * (m >> 2) + 4 * (mt & 1) + (m & 3);
+}
+
+template <int D, int KS>
+__global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
+  constexpr int MT = D / 16;  // M-tiles per row
+  constexpr int NQ = D / 32;  // 16-byte loads per lane per row
+  constexpr int KP = KS * 32; // padded rank
+  __shared__ __attribute__((aligned(16))) uint16_t s_hi[D * KP];
+  __shared__ __attribute__((aligned(16))) uint16_t s_lo[D * KP];
+
+  const int nl = a.num_layers;
+  const int item_id = blockIdx.z / nl;
+  const int lrel = blockIdx.z - item_id * nl;
+  const int layer = a.layer_begin + lrel;
+  const int H = a.pv.num_kv_heads;
+  const int kv = blockIdx.y / H;
+  const int head = blockIdx.y - kv * H;
+
+  const kvc_item* itp = a.items + item_id;
+  const int T = itp->num_tokens;
+  const int t_begin = blockIdx.x * kApplyChunk;
+  if (t_begin >= T) return;
+  const int r = itp->state.rank;
+  const int Tdecl = itp->state.num_tokens;
+  const int Ts = r > 0 ? min(Tdecl, T) : 0;
+  const int src_off = itp->src_offset, dst_off = itp->dst_offset;
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)item_id * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)item_id * a.max_blocks : nullptr;
+  const int64_t unit = unit_index(layer, kv, head, H);
+  const uint16_t* coef = static_cast<const uint16_t*>(itp->state.coef) + unit * (int64_t)Tdecl * r;
+  const float* basis = itp->state.basis + unit * (int64_t)r * D;
+  const uint16_t* src_pool = static_cast<const uint16_t*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
+  uint16_t* dst_pool = static_cast<uint16_t*>(const_cast<void*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]));
+
+  const int wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const int g = lane >> 4;
+  const int n = lane & 15;
+  const bool correct = t_begin < Ts;  // uniform over the workgroup
+
+  // Up to 64 ranks the A-fragments stay in registers for the whole chunk; beyond that they are re-read from LDS.
+  constexpr bool kRegFrags = KS <= 2;
+  constexpr int FM = kRegFrags ? MT : 1, FK = kRegFrags ? KS : 1;
+  bf16x8 ahi[FM][FK], alo[FM][FK];
+  if (correct) {
+    // Stage B^T as bf16 hi/lo, zero-padded to KP ranks: s[f * KP + k] = split(B[k][f]).
+    for (int e = threadIdx.x; e < D * KP; e += kApplyThreads) {
+      const int k = e / D, f = e - k * D;
+      const float x = k < r ? basis[k * D + f] : 0.0f;
+      uint32_t hb, lb;
+      split_bf16(x, hb, lb);
+      s_hi[f * KP + k] = (uint16_t)hb;
+      s_lo[f * KP + k] = (uint16_t)lb;
+    }
+    __syncthreads();
+    if constexpr (kRegFrags) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int f = apply_feature(mt, n);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const int k0 = ks * 32 + 8 * g;
+          ahi[mt][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[f * KP + k0]));
+          alo[mt][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[f * KP + k0]));
+        }
+      }
+    }
+  }
+  const bool coef_vec = (r & 7) == 0;
+
+  for (int j = 0; j < kApplyTilesPerWave; ++j) {
+    const int t0 = t_begin + (j * kApplyWaves + wave) * 16;
+    if (t0 >= T) break;
+    const int t = t0 + n;
+    const bool valid = t < T;
+    const int64_t so = valid ? row_offset(a.pv, src_tab, src_off, t, head) : -1;
+    const int64_t dof = valid ? row_offset(a.pv, dst_tab, dst_off, t, head) : -1;
+    u32x4 raw[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      raw[q] = so >= 0 ? *reinterpret_cast<const u32x4*>(src_pool + so + 32 * q + 8 * g) : u32x4{0, 0, 0, 0};
+    }
+    u32x4 outw[NQ];
+    if (t0 < Ts) {
+      bf16x8 cb[KS];
+      const bool crow = t < Ts;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int k0 = ks * 32 + 8 * g;
+        u32x4 w = {0, 0, 0, 0};
+        if (crow) {
+          const uint16_t* cp = coef + (int64_t)t * r + k0;
+          if (coef_vec && k0 + 8 <= r) {
+            w = *reinterpret_cast<const u32x4*>(cp);
+          } else {
+            uint32_t e[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) e[i] = (k0 + i < r) ? cp[i] : 0u;
+            w = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16)};
+          }
+        }
+        cb[ks] = as_bf16x8(w);
+      }
+      f32x4 acc[MT];
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        acc[2 * q] = f32x4{bf16_lo_to_f32(raw[q][0]), bf16_hi_to_f32(raw[q][0]), bf16_lo_to_f32(raw[q][1]),
+                           bf16_hi_to_f32(raw[q][1])};
+        acc[2 * q + 1] = f32x4{bf16_lo_to_f32(raw[q][2]), bf16_hi_to_f32(raw[q][2]), bf16_lo_to_f32(raw[q][3]),
+                               bf16_hi_to_f32(raw[q][3])};
+      }
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          if constexpr (kRegFrags) {
+            acc[mt] = mfma16x16x32(alo[mt][ks], cb[ks], acc[mt]);
+            acc[mt] = mfma16x16x32(ahi[mt][ks], cb[ks], acc[mt]);
+          } else {
+            const int fo = apply_feature(mt, n) * KP + ks * 32 + 8 * g;
+            const bf16x8 fl = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[fo]));
+            const bf16x8 fh = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[fo]));
+            acc[mt] = mfma16x16x32(fl, cb[ks], acc[mt]);
+            acc[mt] = mfma16x16x32(fh, cb[ks], acc[mt]);
+          }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const f32x4 x = acc[2 * q], y = acc[2 * q + 1];
+        const u32x4 c = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(y[0], y[1]),
+                         pack_bf16x2(y[2], y[3])};
+        outw[q] = crow ? c : raw[q];
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) outw[q] = raw[q];
+    }
+    if (dof >= 0) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) *reinterpret_cast<u32x4*>(dst_pool + dof + 32 * q + 8 * g) = outw[q];
+    }
+  }
+}
+
+// float32 caches: each thread owns 4 features of one token; the rank loop runs over B in LDS.
+template <int D>
+__global__ __launch_bounds__(kApplyThreads) void apply_f32_valu(ApplyArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float s_b[];  // [r][D]
+  constexpr int LPT = D / 4;                                   // lanes per token
+  constexpr int TPP = kApplyThreads / LPT;                     // tokens per pass
+
+  const int nl = a.num_layers;
+  const int item_id = blockIdx.z / nl;
+  const int lrel = blockIdx.z - item_id * nl;
+  const int layer = a.layer_begin + lrel;
+  const int H = a.pv.num_kv_heads;
+  const int kv = blockIdx.y / H;
+  const int head = blockIdx.y - kv * H;
+
+  const kvc_item* itp = a.items + item_id;
+  const int T = itp->num_tokens;
+  const int t_begin = blockIdx.x * kApplyChunk;
+  if (t_begin >= T) return;
+  const int r = itp->state.rank;
+  const int Tdecl = itp->state.num_tokens;
+  const int Ts = r > 0 ? min(Tdecl, T) : 0;
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)item_id * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)item_id * a.max_blocks : nullptr;
+  const int64_t unit = unit_index(layer, kv, head, H);
+  const float* coef = static_cast<const float*>(itp->state.coef) + unit * (int64_t)Tdecl * r;
+  const float* basis = itp->state.basis + unit * (int64_t)r * D;
+  const float* src_pool = static_cast<const float*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
+  float* dst_pool = static_cast<float*>(const_cast<void*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]));
+
+  const bool correct = t_begin < Ts;
+  if (correct) {
+    for (int e = threadIdx.x; e < r * D; e += kApplyThreads) s_b[e] = basis[e];
+    __syncthreads();
+  }
+  const int sub = threadIdx.x / LPT;
+  const int f0 = 4 * (threadIdx.x % LPT);
+  const int t_end = min(T, t_begin + kApplyChunk);
+  for (int t = t_begin + sub; t < t_end; t += TPP) {
+    const int64_t so = row_offset(a.pv, src_tab, itp->src_offset, t, head);
+    const int64_t dof = row_offset(a.pv, dst_tab, itp->dst_offset, t, head);
+    if (so < 0 || dof < 0) continue;
+    const f32x4 s = *reinterpret_cast<const f32x4*>(src_pool + so + f0);
+    f32x4 o = s;
+    if (t < Ts) {
+      const float* crow = coef + (int64_t)t * r;
+      for (int k = 0; k < r; ++k) {
+        const float c = crow[k];
+        const f32x4 b = *reinterpret_cast<const f32x4*>(&s_b[k * D + f0]);
+        o[0] = fmaf(c, b[0], o[0]);
+        o[1] = fmaf(c, b[1], o[1]);
+        o[2] = fmaf(c, b[2], o[2]);
+        o[3] = fmaf(c, b[3], o[3]);
+      }
+    }
+    *reinterpret_cast<f32x4*>(dst_pool + dof + f0) = o;
+  }
+}
+
+template <int D, int KS>
+static hipError_t launch_bf16(const ApplyArgs& a, dim3 grid, hipStream_t stream) {
+  hipLaunchKernelGGL((apply_bf16_mfma<D, KS>), grid, dim3(kApplyThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_bf16_ks(const ApplyArgs& a, int ks, dim3 grid, hipStream_t stream) {
+  switch (ks) {
+    case 0:
+    case 1: return launch_bf16<D, 1>(a, grid, stream);
+    case 2: return launch_bf16<D, 2>(a, grid, stream);
+    case 3: return launch_bf16<D, 3>(a, grid, stream);
+    default: return launch_bf16<D, 4>(a, grid, stream);
+  }
+}
+
+hipError_t launch_apply(const ApplyArgs& a, kvc_dtype dtype, int max_rank, int max_tokens, int num_items,
+                        hipStream_t stream) {
+  const int chunks = (max_tokens + kApplyChunk - 1) / kApplyChunk;
+  if (chunks == 0 || num_items == 0 || a.num_layers == 0) return hipSuccess;
+  dim3 grid(chunks, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+  const int D = a.pv.head_dim;
+  if (dtype == KVC_BF16) {
+    const int ks = (max_rank + 31) / 32;
+    return D == 64 ? launch_bf16_ks<64>(a, ks, grid, stream) : launch_bf16_ks<128>(a, ks, grid, stream);
+  }
+  const size_t lds = (size_t)max_rank * D * sizeof(float);
+  if (D == 64) {
+    hipLaunchKernelGGL(apply_f32_valu<64>, grid, dim3(kApplyThreads), lds, stream, a);
+  } else {
+    hipLaunchKernelGGL(apply_f32_valu<128>, grid, dim3(kApplyThreads), lds, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace kvc

@@ -1,0 +1,76 @@
+// Device helpers shared by the libkvc kernels (gfx950 / CDNA4, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kvc.h"
+
+namespace kvc {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// Per-launch description of the pools of one cache (device-side view of kvc_cache).
+struct PoolView {
+  int64_t block_stride, token_stride, head_stride;  // elements
+  int32_t block_size, num_blocks, num_kv_heads, head_dim;
+};
+
+// Layer pointer tables travel in the kernel arguments (up to this many layers per launch).
+constexpr int kMaxLayersPerLaunch = 128;
+struct LayerPtrs {
+  const void* k[kMaxLayersPerLaunch];
+  const void* v[kMaxLayersPerLaunch];
+};
+
+// ---- bf16 <-> f32 ----------------------------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_lo_to_f32(uint32_t packed) { return __uint_as_float(packed << 16); }
+__device__ __forceinline__ float bf16_hi_to_f32(uint32_t packed) { return __uint_as_float(packed & 0xffff0000u); }
+
+// Round-to-nearest-even float -> bf16 bits; NaN stays a quiet NaN with its sign.
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+// x = hi + lo + O(2^-17 |x|) with hi = bf16(x) and lo = bf16(x - hi): the two-term split that lets bf16 MFMA carry
+// about 16 significant bits of an fp32 operand.
+__device__ __forceinline__ void split_bf16(float x, uint32_t& hi_bits, uint32_t& lo_bits) {
+  hi_bits = f32_to_bf16_bits(x);
+  float hi = __uint_as_float(hi_bits << 16);
+  lo_bits = f32_to_bf16_bits(x - hi);
+}
+
+// ---- paged row addressing --------------------------------------------------------------------------------------
+// Token t of a block sequence with row offset `off`: position p = off + t, block = table[p / bs] (identity when
+// table is null), slot = p % bs.  Returns the element offset of the row, or -1 when the block id is out of range.
+__device__ __forceinline__ int64_t row_offset(const PoolView& pv, const int32_t* __restrict__ table, int32_t off,
+                                              int32_t t, int32_t head) {
+  const int32_t p = off + t;
+  const int32_t lb = p / pv.block_size;
+  const int32_t slot = p - lb * pv.block_size;
+  const int32_t blk = table ? table[lb] : lb;
+  if (blk < 0 || blk >= pv.num_blocks) return -1;
+  return (int64_t)blk * pv.block_stride + (int64_t)slot * pv.token_stride + (int64_t)head * pv.head_stride;
+}
+
+__device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Offset of unit (layer, kv, head) in a state's per-unit arrays.
+__device__ __forceinline__ int64_t unit_index(int32_t layer, int32_t kv, int32_t head, int32_t num_kv_heads) {
+  return ((int64_t)layer * 2 + kv) * num_kv_heads + head;
+}
+
+}  // namespace kvc

@@ -1,0 +1,260 @@
+"""Python binding of libkvc (ctypes): argument marshalling only.
+
+The names mirror the C ABI in include/kvc.h: kvc_fit_state, kvc_apply, kvc_chain and the size queries.  Every step
+of the correction runs in the library's HIP kernels; torch only provides device memory and the stream.  Loading
+fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvc.so")
+
+KVC_OK, KVC_ERR_NULL_ARG, KVC_ERR_SHAPE, KVC_ERR_DTYPE, KVC_ERR_ALIGN = 0, 1, 2, 3, 4
+KVC_ERR_ALIAS, KVC_ERR_WORKSPACE, KVC_ERR_UNSUPPORTED, KVC_ERR_HIP = 5, 6, 7, 8
+KVC_F32, KVC_BF16 = 0, 1
+KVC_FIT_DELTA, KVC_FIT_BASE = 0, 1
+KVC_MAX_RANK = 128
+
+EXPORTED = ["kvc_version", "kvc_status_str", "kvc_last_hip_error", "kvc_state_bytes", "kvc_dense_bytes",
+            "kvc_apply", "kvc_fit_workspace_bytes", "kvc_fit_state", "kvc_chain_workspace_bytes", "kvc_chain"]
+
+
+class KvcError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_str(status)} (status {status})")
+        self.status = status
+
+
+class kvc_cache(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int), ("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32), ("num_blocks", ctypes.c_int32),
+                ("block_stride", ctypes.c_int64), ("token_stride", ctypes.c_int64), ("head_stride", ctypes.c_int64),
+                ("k_layers", ctypes.POINTER(ctypes.c_void_p)), ("v_layers", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class kvc_state(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("num_tokens", ctypes.c_int32), ("rank", ctypes.c_int32), ("coef_dtype", ctypes.c_int),
+                ("coef", ctypes.c_void_p), ("basis", ctypes.c_void_p), ("sigma", ctypes.c_void_p)]
+
+
+class kvc_item(ctypes.Structure):
+    _fields_ = [("num_tokens", ctypes.c_int32), ("src_offset", ctypes.c_int32), ("dst_offset", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("state", kvc_state)]
+
+
+class kvc_batch(ctypes.Structure):
+    _fields_ = [("num_items", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
+                ("items", ctypes.POINTER(kvc_item)), ("items_dev", ctypes.c_void_p),
+                ("src_tables", ctypes.c_void_p), ("dst_tables", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libkvc.so (built by build.py).  Raises if it is missing: there is no fallback path."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2609_34060_amd/build.py (hipcc, gfx950)")
+    lib = ctypes.CDLL(path)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    lib.kvc_version.restype = i32
+    lib.kvc_status_str.restype = ctypes.c_char_p
+    lib.kvc_status_str.argtypes = [ctypes.c_int]
+    lib.kvc_last_hip_error.restype = i32
+    lib.kvc_state_bytes.restype = sz
+    lib.kvc_state_bytes.argtypes = [i32, i32, i32, i32, i32, ctypes.c_int]
+    lib.kvc_dense_bytes.restype = sz
+    lib.kvc_dense_bytes.argtypes = [i32, i32, i32, i32, ctypes.c_int]
+    lib.kvc_apply.restype = ctypes.c_int
+    lib.kvc_apply.argtypes = [ctypes.POINTER(kvc_cache), ctypes.POINTER(kvc_batch), i32, i32, vp]
+    lib.kvc_fit_workspace_bytes.restype = sz
+    lib.kvc_fit_workspace_bytes.argtypes = [ctypes.POINTER(kvc_cache), ctypes.POINTER(kvc_batch), i32, i32]
+    lib.kvc_fit_state.restype = ctypes.c_int
+    lib.kvc_fit_state.argtypes = [ctypes.POINTER(kvc_cache), ctypes.POINTER(kvc_batch), i32, i32, ctypes.c_int,
+                                  vp, sz, vp]
+    lib.kvc_chain_workspace_bytes.restype = sz
+    lib.kvc_chain_workspace_bytes.argtypes = [ctypes.POINTER(kvc_state)] * 3 + [i32, i32]
+    lib.kvc_chain.restype = ctypes.c_int
+    lib.kvc_chain.argtypes = [ctypes.POINTER(kvc_state)] * 3 + [i32, i32, vp, sz, vp]
+    _lib = lib
+    return lib
+
+
+def status_str(status: int) -> str:
+    return load().kvc_status_str(status).decode()
+
+
+def _check(status: int, what: str) -> None:
+    if status != KVC_OK:
+        raise KvcError(status, what)
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return KVC_BF16
+    if dt == torch.float32:
+        return KVC_F32
+    raise ValueError(f"unsupported dtype {dt}")
+
+
+def _stream_handle(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+# ------------------------------------------------------------------------------------------------------------------
+# Python-side holders (keep the tensors and ctypes arrays alive for the duration of a call)
+# ------------------------------------------------------------------------------------------------------------------
+
+class Cache:
+    """kvc_cache over per-layer pools [num_blocks, block_size, num_kv_heads, head_dim] (or any strided view whose
+    head_dim is contiguous)."""
+
+    def __init__(self, k_pools: Sequence[torch.Tensor], v_pools: Sequence[torch.Tensor],
+                 strides: Optional[Sequence[int]] = None):
+        assert len(k_pools) == len(v_pools) and len(k_pools) > 0
+        p0 = k_pools[0]
+        self.k_pools, self.v_pools = list(k_pools), list(v_pools)
+        nb, bs, H, d = p0.shape
+        if strides is None:
+            strides = (p0.stride(0), p0.stride(1), p0.stride(2))
+        n = len(k_pools)
+        self._k = (ctypes.c_void_p * n)(*[p.data_ptr() for p in k_pools])
+        self._v = (ctypes.c_void_p * n)(*[p.data_ptr() for p in v_pools])
+        self.c = kvc_cache(_dtype_code(p0.dtype), n, H, d, bs, nb, strides[0], strides[1], strides[2],
+                           ctypes.cast(self._k, ctypes.POINTER(ctypes.c_void_p)),
+                           ctypes.cast(self._v, ctypes.POINTER(ctypes.c_void_p)))
+
+    @property
+    def num_layers(self):
+        return self.c.num_layers
+
+
+class State:
+    """Low-rank state tensors: coef [L, 2, H, T, r], basis [L, 2, H, r, d] float32, sigma [L, 2, H, r] float32."""
+
+    def __init__(self, coef: torch.Tensor, basis: torch.Tensor, sigma: Optional[torch.Tensor] = None):
+        self.coef, self.basis, self.sigma = coef, basis, sigma
+        L, two, H, T, r = coef.shape
+        assert two == 2 and basis.shape[:4] == (L, 2, H, r)
+        self.s = kvc_state(L, H, basis.shape[-1], T, r, _dtype_code(coef.dtype),
+                           coef.data_ptr() if coef.numel() else None,
+                           basis.data_ptr() if basis.numel() else None,
+                           sigma.data_ptr() if (sigma is not None and sigma.numel()) else None)
+
+    @staticmethod
+    def empty(L: int, H: int, d: int, T: int, rank: int, coef_dtype: torch.dtype, device) -> "State":
+        return State(torch.zeros(L, 2, H, T, rank, dtype=coef_dtype, device=device),
+                     torch.zeros(L, 2, H, rank, d, dtype=torch.float32, device=device),
+                     torch.zeros(L, 2, H, rank, dtype=torch.float32, device=device))
+
+    @property
+    def num_tokens(self) -> int:
+        return self.s.num_tokens
+
+    @property
+    def rank(self) -> int:
+        return self.s.rank
+
+
+class Batch:
+    """kvc_batch: host items, their device copy and the block tables (device int32 [n, max_blocks] or None)."""
+
+    def __init__(self, num_tokens: Sequence[int], src_offsets: Sequence[int], dst_offsets: Sequence[int],
+                 states: Sequence[State], src_tables: Optional[torch.Tensor] = None,
+                 dst_tables: Optional[torch.Tensor] = None, device=None):
+        n = len(num_tokens)
+        self.states = list(states)
+        arr = (kvc_item * max(n, 1))()
+        for i in range(n):
+            arr[i].num_tokens = int(num_tokens[i])
+            arr[i].src_offset = int(src_offsets[i])
+            arr[i].dst_offset = int(dst_offsets[i])
+            arr[i].reserved = 0
+            arr[i].state = states[i].s
+        self._items = arr
+        device = device if device is not None else (states[0].basis.device if n else "cuda")
+        raw = bytes(memoryview(arr).cast("B"))[: n * ctypes.sizeof(kvc_item)]
+        self.items_dev = torch.frombuffer(bytearray(raw), dtype=torch.uint8).to(device) if n else None
+        self.src_tables = None if src_tables is None else src_tables.to(torch.int32).contiguous()
+        self.dst_tables = None if dst_tables is None else dst_tables.to(torch.int32).contiguous()
+        max_blocks = 0
+        for t in (self.src_tables, self.dst_tables):
+            if t is not None:
+                assert t.shape[0] == n
+                max_blocks = max(max_blocks, t.shape[1])
+        if self.src_tables is not None and self.dst_tables is not None:
+            assert self.src_tables.shape[1] == self.dst_tables.shape[1]
+        self.b = kvc_batch(n, max_blocks, ctypes.cast(arr, ctypes.POINTER(kvc_item)),
+                           self.items_dev.data_ptr() if n else None,
+                           None if self.src_tables is None else self.src_tables.data_ptr(),
+                           None if self.dst_tables is None else self.dst_tables.data_ptr())
+
+
+# ------------------------------------------------------------------------------------------------------------------
+# Entry points (same names as the C ABI)
+# ------------------------------------------------------------------------------------------------------------------
+
+def kvc_version() -> int:
+    return load().kvc_version()
+
+
+def kvc_state_bytes(L: int, H: int, d: int, T: int, rank: int, coef_dtype: int) -> int:
+    return load().kvc_state_bytes(L, H, d, T, rank, coef_dtype)
+
+
+def kvc_dense_bytes(L: int, H: int, d: int, T: int, dtype: int) -> int:
+    return load().kvc_dense_bytes(L, H, d, T, dtype)
+
+
+def kvc_apply(cache: Cache, batch: Batch, layer_begin: int = 0, layer_end: Optional[int] = None,
+              stream=None) -> None:
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    st = load().kvc_apply(ctypes.byref(cache.c), ctypes.byref(batch.b), layer_begin, layer_end,
+                          _stream_handle(stream))
+    _check(st, "kvc_apply")
+
+
+def kvc_fit_workspace_bytes(cache: Cache, batch: Batch, layer_begin: int = 0, layer_end: Optional[int] = None) -> int:
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    return load().kvc_fit_workspace_bytes(ctypes.byref(cache.c), ctypes.byref(batch.b), layer_begin, layer_end)
+
+
+def kvc_fit_state(cache: Cache, batch: Batch, layer_begin: int = 0, layer_end: Optional[int] = None,
+                  mode: int = KVC_FIT_DELTA, workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    need = kvc_fit_workspace_bytes(cache, batch, layer_begin, layer_end)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=cache.k_pools[0].device)
+    st = load().kvc_fit_state(ctypes.byref(cache.c), ctypes.byref(batch.b), layer_begin, layer_end, mode,
+                              ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream_handle(stream))
+    _check(st, "kvc_fit_state")
+
+
+def kvc_chain_workspace_bytes(first: State, second: State, out: State, layer_begin: int = 0,
+                              layer_end: Optional[int] = None) -> int:
+    layer_end = first.s.num_layers if layer_end is None else layer_end
+    return load().kvc_chain_workspace_bytes(ctypes.byref(first.s), ctypes.byref(second.s), ctypes.byref(out.s),
+                                            layer_begin, layer_end)
+
+
+def kvc_chain(first: State, second: State, out: State, layer_begin: int = 0, layer_end: Optional[int] = None,
+              workspace: Optional[torch.Tensor] = None, stream=None) -> None:
+    layer_end = first.s.num_layers if layer_end is None else layer_end
+    need = kvc_chain_workspace_bytes(first, second, out, layer_begin, layer_end)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=first.basis.device)
+    st = load().kvc_chain(ctypes.byref(first.s), ctypes.byref(second.s), ctypes.byref(out.s), layer_begin,
+                          layer_end, ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
+                          _stream_handle(stream))
+    _check(st, "kvc_chain")

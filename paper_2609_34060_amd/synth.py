@@ -292,12 +292,14 @@ def build_paged(w: Workload, device="cpu", layers: Optional[Sequence[int]] = Non
 # ---------------------------------------------------------------------------------------------------------------
 
 def random_state(L: int, H: int, d: int, T: int, rank: int, coef_dtype: torch.dtype, device, *keys: int,
-                 coef_scale: float = 0.25):
-    """A state with orthonormal basis rows and Gaussian coefficients.
+                 coef_scale: Optional[float] = None):
+    """A state with orthonormal basis rows and Gaussian coefficients (default scale: RMS of A B equal to 0.25).
 
     Returns (coef [L, 2, H, T, rank] coef_dtype, basis [L, 2, H, rank, d] float32, sigma [L, 2, H, rank] float32);
     sigma is the column norm of coef (descriptive only)."""
     g = torch_generator(device, 77, L, H, d, T, rank, *keys)
+    if coef_scale is None:
+        coef_scale = 0.25 * math.sqrt(d / max(rank, 1))
     coef = (torch.randn(L, 2, H, T, rank, generator=g, device=device) * coef_scale).to(coef_dtype)
     if rank > 0:
         basis = orthonormal_columns(torch.randn(L * 2 * H, d, rank, generator=g, device=device))

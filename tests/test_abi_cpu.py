@@ -1,0 +1,180 @@
+"""The C ABI without a GPU: the library loads, exports every declared symbol, and rejects bad arguments on the host
+before any launch (fake device addresses are never dereferenced: each case fails a host-side check)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import kvc_oracle as O
+from paper_2609_34060_amd import kvc
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "kvc.h")
+FAKE = 0x7F0000001000        # a 4 KiB-aligned address that is only compared, never dereferenced
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvc_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = kvc.load()
+    declared = _declared_functions()
+    assert set(declared) == set(kvc.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert lib.kvc_version() == 1
+
+
+def test_status_strings():
+    for st in range(9):
+        assert kvc.status_str(st)
+    assert kvc.status_str(0) == "ok"
+
+
+def test_memory_accounting_matches_oracle_and_paper_example():
+    for (L, H, d, T, r, dt, eb) in [(32, 8, 128, 32768, 32, kvc.KVC_BF16, 2), (2, 4, 64, 256, 8, kvc.KVC_F32, 4),
+                                    (28, 4, 128, 3328, 0, kvc.KVC_BF16, 2)]:
+        assert kvc.kvc_state_bytes(L, H, d, T, r, dt) == O.lowrank_state_bytes(L, H, d, T, r, eb)
+        assert kvc.kvc_dense_bytes(L, H, d, T, dt) == O.dense_segment_bytes(L, H, d, T, eb)
+    # Section 3.1: 20 anchors x (1 base + 4 corrections) of a 4K-token Llama-3.1-8B segment in BF16 = 50 GiB
+    assert 20 * (1 + 4) * kvc.kvc_dense_bytes(32, 8, 128, 4096, kvc.KVC_BF16) == 50 * 2 ** 30
+
+
+class Fixture:
+    """A valid-looking bf16 cache/batch description made of fake device addresses."""
+
+    def __init__(self, L=2, H=2, d=128, bs=16, nb=64, T=100, rank=16, n=1):
+        self.ptrs_k = (ctypes.c_void_p * L)(*[FAKE + 0x100000 * i for i in range(L)])
+        self.ptrs_v = (ctypes.c_void_p * L)(*[FAKE + 0x800000 + 0x100000 * i for i in range(L)])
+        self.cache = kvc.kvc_cache(kvc.KVC_BF16, L, H, d, bs, nb, bs * H * d, H * d, d,
+                                   ctypes.cast(self.ptrs_k, ctypes.POINTER(ctypes.c_void_p)),
+                                   ctypes.cast(self.ptrs_v, ctypes.POINTER(ctypes.c_void_p)))
+        self.items = (kvc.kvc_item * n)()
+        for i in range(n):
+            self.items[i].num_tokens = T
+            self.items[i].src_offset = 0
+            self.items[i].dst_offset = 512
+            self.items[i].state = kvc.kvc_state(L, H, d, T, rank, kvc.KVC_BF16, FAKE + 0x4000000, FAKE + 0x8000000,
+                                                None)
+        self.batch = kvc.kvc_batch(n, 0, ctypes.cast(self.items, ctypes.POINTER(kvc.kvc_item)), FAKE + 0xC000000,
+                                   None, None)
+
+    def apply(self, lb=0, le=None):
+        le = self.cache.num_layers if le is None else le
+        return kvc.load().kvc_apply(ctypes.byref(self.cache), ctypes.byref(self.batch), lb, le, None)
+
+
+def _cases():
+    def null_cache(f):
+        return kvc.load().kvc_apply(None, ctypes.byref(f.batch), 0, 1, None), kvc.KVC_ERR_NULL_ARG
+
+    def null_batch(f):
+        return kvc.load().kvc_apply(ctypes.byref(f.cache), None, 0, 1, None), kvc.KVC_ERR_NULL_ARG
+
+    def head_dim(f):
+        f.cache.head_dim = 96
+        return f.apply(), kvc.KVC_ERR_UNSUPPORTED
+
+    def dtype(f):
+        f.cache.dtype = 7
+        return f.apply(), kvc.KVC_ERR_DTYPE
+
+    def layer_range(f):
+        return f.apply(1, 3), kvc.KVC_ERR_SHAPE
+
+    def stride_align(f):
+        f.cache.token_stride = 4          # 8 bytes
+        return f.apply(), kvc.KVC_ERR_ALIGN
+
+    def layer_ptr_align(f):
+        f.ptrs_v[1] = FAKE + 8
+        return f.apply(), kvc.KVC_ERR_ALIGN
+
+    def null_layer(f):
+        f.ptrs_k[0] = None
+        return f.apply(), kvc.KVC_ERR_NULL_ARG
+
+    def rank_gt_d(f):
+        f.cache.head_dim = 64
+        for i in range(f.batch.num_items):
+            f.items[i].state.head_dim = 64
+            f.items[i].state.rank = 65
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def rank_gt_max(f):
+        f.items[0].state.rank = 129
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def state_tokens(f):
+        f.items[0].state.num_tokens = f.items[0].num_tokens + 1
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def state_shape(f):
+        f.items[0].state.num_kv_heads = 3
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def coef_dtype(f):
+        f.items[0].state.coef_dtype = kvc.KVC_F32
+        return f.apply(), kvc.KVC_ERR_DTYPE
+
+    def coef_align(f):
+        f.items[0].state.coef = FAKE + 2
+        return f.apply(), kvc.KVC_ERR_ALIGN
+
+    def null_coef(f):
+        f.items[0].state.coef = None
+        return f.apply(), kvc.KVC_ERR_NULL_ARG
+
+    def beyond_pool(f):
+        f.items[0].dst_offset = 64 * 16 - 10
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def beyond_table(f):
+        f.batch.src_tables = FAKE
+        f.batch.dst_tables = FAKE + 0x1000
+        f.batch.max_blocks = 6             # 96 rows < 100
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def same_tables(f):
+        f.items[0].dst_offset = 0
+        f.batch.src_tables = FAKE
+        f.batch.dst_tables = FAKE
+        f.batch.max_blocks = 8
+        return f.apply(), kvc.KVC_ERR_ALIAS
+
+    def overlap_rows(f):
+        f.items[0].dst_offset = 50
+        return f.apply(), kvc.KVC_ERR_ALIAS
+
+    def null_items_dev(f):
+        f.batch.items_dev = None
+        return f.apply(), kvc.KVC_ERR_NULL_ARG
+
+    def reserved(f):
+        f.items[0].reserved = 1
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def negative_offset(f):
+        f.items[0].src_offset = -1
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    return [null_cache, null_batch, head_dim, dtype, layer_range, stride_align, layer_ptr_align, null_layer,
+            rank_gt_d, rank_gt_max, state_tokens, state_shape, coef_dtype, coef_align, null_coef, beyond_pool,
+            beyond_table, same_tables, overlap_rows, null_items_dev, reserved, negative_offset]
+
+
+@pytest.mark.parametrize("case", _cases(), ids=lambda c: c.__name__)
+def test_apply_rejects_bad_arguments_before_launch(case):
+    got, expected = case(Fixture())
+    assert got == expected, (kvc.status_str(got), kvc.status_str(expected))
+
+
+def test_apply_empty_batch_is_a_noop():
+    f = Fixture()
+    f.batch.num_items = 0
+    assert f.apply() == kvc.KVC_OK
+    f = Fixture()
+    assert f.apply(1, 1) == kvc.KVC_OK           # an empty layer range is valid (nothing to launch)
