@@ -83,6 +83,45 @@ kvc_status check_batch(const kvc_cache* c, const kvc_batch* b, bool needs_src) {
   return KVC_OK;
 }
 
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+// Workspace layout and launch grouping of a fit call.  Units are processed in groups of at most 128 layers and as
+// many items as keep items x layers below 65536; the workspace holds one group.  A unit's Gram is split into
+// max_parts partials of part_tokens rows so that one call launches about 4096 Gram workgroups.
+struct FitPlan {
+  int32_t layers_per_group = 1, items_per_group = 1, part_tokens = 256, max_parts = 1;
+  size_t units = 0, off_partials = 0, off_reflect = 0, off_beta = 0, off_vecs = 0, total = 0;
+};
+
+FitPlan plan_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int32_t le) {
+  FitPlan p;
+  const int32_t nl = le - lb;
+  if (nl <= 0 || b->num_items <= 0) return p;
+  p.layers_per_group = std::min<int32_t>(nl, kvc::kMaxLayersPerLaunch);
+  p.items_per_group = std::max<int32_t>(1, std::min<int32_t>(b->num_items, 65535 / p.layers_per_group));
+  int32_t tmax = 0;
+  for (int32_t i = 0; i < b->num_items; ++i)
+    if (b->items[i].state.rank > 0) tmax = std::max(tmax, b->items[i].state.num_tokens);
+  const int64_t d = c->head_dim;
+  p.units = static_cast<size_t>(p.items_per_group) * p.layers_per_group * 2 * c->num_kv_heads;
+  const int64_t want_parts = std::max<int64_t>(1, (4096 + static_cast<int64_t>(p.units) - 1) / p.units);
+  int64_t part = (std::max<int32_t>(tmax, 1) + want_parts - 1) / want_parts;
+  part = std::max<int64_t>(256, (part + 31) / 32 * 32);
+  p.part_tokens = static_cast<int32_t>(part);
+  p.max_parts = static_cast<int32_t>(std::max<int64_t>(1, (tmax + part - 1) / part));
+  size_t off = 0;
+  p.off_partials = off;
+  off = align256(off + p.units * p.max_parts * d * d * sizeof(float));
+  p.off_reflect = off;
+  off = align256(off + p.units * d * d * sizeof(double));
+  p.off_beta = off;
+  off = align256(off + p.units * d * sizeof(double));
+  p.off_vecs = off;
+  off = align256(off + p.units * KVC_MAX_RANK * d * sizeof(double));
+  p.total = off;
+  return p;
+}
+
 void fill_pool_view(const kvc_cache* c, kvc::PoolView& pv) {
   pv.block_stride = c->block_stride;
   pv.token_stride = c->token_stride;
@@ -176,10 +215,76 @@ kvc_status kvc_apply(const kvc_cache* cache, const kvc_batch* batch, int32_t lay
   return KVC_OK;
 }
 
-size_t kvc_fit_workspace_bytes(const kvc_cache*, const kvc_batch*, int32_t, int32_t) { return 0; }
-kvc_status kvc_fit_state(const kvc_cache*, const kvc_batch*, int32_t, int32_t, kvc_fit_mode, void*, size_t,
-                         hipStream_t) {
-  return KVC_ERR_UNSUPPORTED;
+size_t kvc_fit_workspace_bytes(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin,
+                               int32_t layer_end) {
+  if (check_cache(cache, layer_begin, layer_end) != KVC_OK || !batch || batch->num_items < 0) return 0;
+  if (batch->num_items > 0 && !batch->items) return 0;
+  return plan_fit(cache, batch, layer_begin, layer_end).total;
+}
+
+kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
+                         kvc_fit_mode mode, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  kvc_status s = check_cache(cache, layer_begin, layer_end);
+  if (s != KVC_OK) return s;
+  if (mode != KVC_FIT_DELTA && mode != KVC_FIT_BASE) return KVC_ERR_SHAPE;
+  s = check_batch(cache, batch, mode == KVC_FIT_DELTA);
+  if (s != KVC_OK) return s;
+  int max_rank = 0, max_tokens = 0;
+  for (int32_t i = 0; i < batch->num_items; ++i) {
+    const kvc_state& st = batch->items[i].state;
+    // Eq. 7 keeps at most min(T_s, d) singular triplets
+    if (st.rank > st.num_tokens) return KVC_ERR_SHAPE;
+    max_rank = std::max(max_rank, st.rank);
+    if (st.rank > 0) max_tokens = std::max(max_tokens, st.num_tokens);
+  }
+  if (batch->num_items == 0 || layer_end == layer_begin || max_rank == 0) return KVC_OK;
+  const FitPlan p = plan_fit(cache, batch, layer_begin, layer_end);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < p.total)
+    return KVC_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+
+  kvc::FitArgs fa;
+  std::memset(&fa, 0, sizeof(fa));
+  fill_pool_view(cache, fa.pv);
+  fa.max_blocks = batch->max_blocks;
+  fa.mode = mode;
+  fa.partials = reinterpret_cast<float*>(ws + p.off_partials);
+  fa.max_parts = p.max_parts;
+  fa.part_tokens = p.part_tokens;
+  kvc::EigArgs ea;
+  std::memset(&ea, 0, sizeof(ea));
+  ea.n = cache->head_dim;
+  ea.partials = fa.partials;
+  ea.max_parts = p.max_parts;
+  ea.part_tokens = p.part_tokens;
+  ea.num_kv_heads = cache->num_kv_heads;
+  ea.reflect = reinterpret_cast<double*>(ws + p.off_reflect);
+  ea.reflect_beta = reinterpret_cast<double*>(ws + p.off_beta);
+  ea.vecs = reinterpret_cast<double*>(ws + p.off_vecs);
+  ea.seed = 0x5EEDu;
+  for (int32_t l0 = layer_begin; l0 < layer_end; l0 += p.layers_per_group) {
+    const int32_t l1 = std::min(layer_end, l0 + p.layers_per_group);
+    fa.layer_begin = ea.layer_begin = l0;
+    fa.num_layers = ea.num_layers = l1 - l0;
+    for (int32_t l = l0; l < l1; ++l) {
+      fa.layers.k[l - l0] = cache->k_layers[l];
+      fa.layers.v[l - l0] = cache->v_layers[l];
+    }
+    for (int32_t i0 = 0; i0 < batch->num_items; i0 += p.items_per_group) {
+      const int32_t n = std::min(p.items_per_group, batch->num_items - i0);
+      fa.items = ea.items = batch->items_dev + i0;
+      fa.src_tables = batch->src_tables ? batch->src_tables + static_cast<int64_t>(i0) * batch->max_blocks : nullptr;
+      fa.dst_tables = batch->dst_tables ? batch->dst_tables + static_cast<int64_t>(i0) * batch->max_blocks : nullptr;
+      ea.num_units = n * fa.num_layers * 2 * cache->num_kv_heads;
+      s = hip_status(kvc::launch_fit_gram(fa, cache->dtype, n, stream));
+      if (s != KVC_OK) return s;
+      s = hip_status(kvc::launch_eig(ea, stream));
+      if (s != KVC_OK) return s;
+      s = hip_status(kvc::launch_fit_proj(fa, cache->dtype, n, max_tokens, max_rank, stream));
+      if (s != KVC_OK) return s;
+    }
+  }
+  return KVC_OK;
 }
 size_t kvc_chain_workspace_bytes(const kvc_state*, const kvc_state*, const kvc_state*, int32_t, int32_t) { return 0; }
 kvc_status kvc_chain(const kvc_state*, const kvc_state*, kvc_state*, int32_t, int32_t, void*, size_t, hipStream_t) {

@@ -29,11 +29,18 @@ __device__ __forceinline__ int apply_feature(int mt, int m) {
   return 32 * (mt >> 1) + 8 * (m >> 2) + 4 * (mt & 1) + (m & 3);
 }
 
-template <int D, int KS>
+// Tuning knobs of the bf16 kernel (chosen by measurement on MI355X; see the launcher).
+//   TPW   16-token tiles per wave per workgroup (a workgroup covers 4 * 16 * TPW tokens)
+//   REGF  A-fragments held in registers for the whole chunk (true) or re-read from LDS per tile (false)
+//   PF    software prefetch: the next tile's rows and coefficients are loaded before this tile's MFMAs
+//   NTL   non-temporal loads of the streamed source rows (read exactly once)
+//   NTS   non-temporal stores of the destination rows (written exactly once)
+template <int D, int KS, int TPW, bool REGF, bool PF, bool NTL, bool NTS>
 __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
   constexpr int MT = D / 16;  // M-tiles per row
   constexpr int NQ = D / 32;  // 16-byte loads per lane per row
   constexpr int KP = KS * 32; // padded rank
+  constexpr int CHUNK = kApplyWaves * TPW * 16;
   __shared__ __attribute__((aligned(16))) uint16_t s_hi[D * KP];
   __shared__ __attribute__((aligned(16))) uint16_t s_lo[D * KP];
 
@@ -47,7 +54,7 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
 
   const kvc_item* itp = a.items + item_id;
   const int T = itp->num_tokens;
-  const int t_begin = blockIdx.x * kApplyChunk;
+  const int t_begin = blockIdx.x * CHUNK;
   if (t_begin >= T) return;
   const int r = itp->state.rank;
   const int Tdecl = itp->state.num_tokens;
@@ -67,8 +74,7 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
   const int n = lane & 15;
   const bool correct = t_begin < Ts;  // uniform over the workgroup
 
-  // Up to 64 ranks the A-fragments stay in registers for the whole chunk; beyond that they are re-read from LDS.
-  constexpr bool kRegFrags = KS <= 2;
+  constexpr bool kRegFrags = REGF && KS <= 2;
   constexpr int FM = kRegFrags ? MT : 1, FK = kRegFrags ? KS : 1;
   bf16x8 ahi[FM][FK], alo[FM][FK];
   if (correct) {
@@ -97,77 +103,116 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
   }
   const bool coef_vec = (r & 7) == 0;
 
-  for (int j = 0; j < kApplyTilesPerWave; ++j) {
-    const int t0 = t_begin + (j * kApplyWaves + wave) * 16;
-    if (t0 >= T) break;
-    const int t = t0 + n;
+  struct Tile {
+    u32x4 raw[NQ];
+    u32x4 cw[KS];
+    int64_t dof;
+  };
+  // Issue the loads of tile j (rows through the block tables, coefficient rows); lanes past T load nothing.
+  auto load_tile = [&](int j, Tile& tl) {
+    const int t = t_begin + (j * kApplyWaves + wave) * 16 + n;
     const bool valid = t < T;
     const int64_t so = valid ? row_offset(a.pv, src_tab, src_off, t, head) : -1;
-    const int64_t dof = valid ? row_offset(a.pv, dst_tab, dst_off, t, head) : -1;
-    u32x4 raw[NQ];
+    tl.dof = valid ? row_offset(a.pv, dst_tab, dst_off, t, head) : -1;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      raw[q] = so >= 0 ? *reinterpret_cast<const u32x4*>(src_pool + so + 32 * q + 8 * g) : u32x4{0, 0, 0, 0};
+      const u32x4* p = reinterpret_cast<const u32x4*>(src_pool + so + 32 * q + 8 * g);
+      if (so >= 0) {
+        tl.raw[q] = NTL ? __builtin_nontemporal_load(p) : *p;
+      } else {
+        tl.raw[q] = u32x4{0, 0, 0, 0};
+      }
     }
+    const bool crow = t < Ts;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int k0 = ks * 32 + 8 * g;
+      u32x4 w = {0, 0, 0, 0};
+      if (crow) {
+        const uint16_t* cp = coef + (int64_t)t * r + k0;
+        if (coef_vec && k0 + 8 <= r) {
+          w = *reinterpret_cast<const u32x4*>(cp);
+        } else {
+          uint32_t e[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) e[i] = (k0 + i < r) ? cp[i] : 0u;
+          w = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16)};
+        }
+      }
+      tl.cw[ks] = w;
+    }
+  };
+  // Correct (rows t < Ts) or copy, then store through the destination table.
+  auto finish_tile = [&](int j, const Tile& tl) {
+    const int t0 = t_begin + (j * kApplyWaves + wave) * 16;
+    const int t = t0 + n;
     u32x4 outw[NQ];
     if (t0 < Ts) {
-      bf16x8 cb[KS];
-      const bool crow = t < Ts;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int k0 = ks * 32 + 8 * g;
-        u32x4 w = {0, 0, 0, 0};
-        if (crow) {
-          const uint16_t* cp = coef + (int64_t)t * r + k0;
-          if (coef_vec && k0 + 8 <= r) {
-            w = *reinterpret_cast<const u32x4*>(cp);
-          } else {
-            uint32_t e[8];
-#pragma unroll
-            for (int i = 0; i < 8; ++i) e[i] = (k0 + i < r) ? cp[i] : 0u;
-            w = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16), e[6] | (e[7] << 16)};
-          }
-        }
-        cb[ks] = as_bf16x8(w);
-      }
       f32x4 acc[MT];
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
-        acc[2 * q] = f32x4{bf16_lo_to_f32(raw[q][0]), bf16_hi_to_f32(raw[q][0]), bf16_lo_to_f32(raw[q][1]),
-                           bf16_hi_to_f32(raw[q][1])};
-        acc[2 * q + 1] = f32x4{bf16_lo_to_f32(raw[q][2]), bf16_hi_to_f32(raw[q][2]), bf16_lo_to_f32(raw[q][3]),
-                               bf16_hi_to_f32(raw[q][3])};
+        acc[2 * q] = f32x4{bf16_lo_to_f32(tl.raw[q][0]), bf16_hi_to_f32(tl.raw[q][0]),
+                           bf16_lo_to_f32(tl.raw[q][1]), bf16_hi_to_f32(tl.raw[q][1])};
+        acc[2 * q + 1] = f32x4{bf16_lo_to_f32(tl.raw[q][2]), bf16_hi_to_f32(tl.raw[q][2]),
+                               bf16_lo_to_f32(tl.raw[q][3]), bf16_hi_to_f32(tl.raw[q][3])};
       }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 cb = as_bf16x8(tl.cw[ks]);
           if constexpr (kRegFrags) {
-            acc[mt] = mfma16x16x32(alo[mt][ks], cb[ks], acc[mt]);
-            acc[mt] = mfma16x16x32(ahi[mt][ks], cb[ks], acc[mt]);
+            acc[mt] = mfma16x16x32(alo[mt][ks], cb, acc[mt]);
+            acc[mt] = mfma16x16x32(ahi[mt][ks], cb, acc[mt]);
           } else {
             const int fo = apply_feature(mt, n) * KP + ks * 32 + 8 * g;
             const bf16x8 fl = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[fo]));
             const bf16x8 fh = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[fo]));
-            acc[mt] = mfma16x16x32(fl, cb[ks], acc[mt]);
-            acc[mt] = mfma16x16x32(fh, cb[ks], acc[mt]);
+            acc[mt] = mfma16x16x32(fl, cb, acc[mt]);
+            acc[mt] = mfma16x16x32(fh, cb, acc[mt]);
           }
         }
       }
+      const bool crow = t < Ts;
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         const f32x4 x = acc[2 * q], y = acc[2 * q + 1];
         const u32x4 c = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(y[0], y[1]),
                          pack_bf16x2(y[2], y[3])};
-        outw[q] = crow ? c : raw[q];
+        outw[q] = crow ? c : tl.raw[q];
       }
     } else {
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) outw[q] = raw[q];
+      for (int q = 0; q < NQ; ++q) outw[q] = tl.raw[q];
     }
-    if (dof >= 0) {
+    if (tl.dof >= 0) {
 #pragma unroll
-      for (int q = 0; q < NQ; ++q) *reinterpret_cast<u32x4*>(dst_pool + dof + 32 * q + 8 * g) = outw[q];
+      for (int q = 0; q < NQ; ++q) {
+        u32x4* p = reinterpret_cast<u32x4*>(dst_pool + tl.dof + 32 * q + 8 * g);
+        if (NTS) {
+          __builtin_nontemporal_store(outw[q], p);
+        } else {
+          *p = outw[q];
+        }
+      }
+    }
+  };
+
+  if constexpr (PF) {
+    Tile cur, nxt;
+    load_tile(0, cur);
+    for (int j = 0; j < TPW; ++j) {
+      if (t_begin + (j * kApplyWaves + wave) * 16 >= T) break;
+      if (j + 1 < TPW && t_begin + ((j + 1) * kApplyWaves + wave) * 16 < T) load_tile(j + 1, nxt);
+      finish_tile(j, cur);
+      cur = nxt;
+    }
+  } else {
+    for (int j = 0; j < TPW; ++j) {
+      if (t_begin + (j * kApplyWaves + wave) * 16 >= T) break;
+      Tile cur;
+      load_tile(j, cur);
+      finish_tile(j, cur);
     }
   }
 }
@@ -231,9 +276,13 @@ __global__ __launch_bounds__(kApplyThreads) void apply_f32_valu(ApplyArgs a) {
   }
 }
 
+// Chosen configuration (tiles per wave, fragment placement, prefetch, non-temporal access).
+constexpr int kTPW = 16;
+constexpr bool kREGF = false, kPF = false, kNTL = false, kNTS = false;
+
 template <int D, int KS>
 static hipError_t launch_bf16(const ApplyArgs& a, dim3 grid, hipStream_t stream) {
-  hipLaunchKernelGGL((apply_bf16_mfma<D, KS>), grid, dim3(kApplyThreads), 0, stream, a);
+  hipLaunchKernelGGL((apply_bf16_mfma<D, KS, kTPW, kREGF, kPF, kNTL, kNTS>), grid, dim3(kApplyThreads), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -250,14 +299,15 @@ static hipError_t launch_bf16_ks(const ApplyArgs& a, int ks, dim3 grid, hipStrea
 
 hipError_t launch_apply(const ApplyArgs& a, kvc_dtype dtype, int max_rank, int max_tokens, int num_items,
                         hipStream_t stream) {
-  const int chunks = (max_tokens + kApplyChunk - 1) / kApplyChunk;
-  if (chunks == 0 || num_items == 0 || a.num_layers == 0) return hipSuccess;
-  dim3 grid(chunks, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+  if (max_tokens == 0 || num_items == 0 || a.num_layers == 0) return hipSuccess;
   const int D = a.pv.head_dim;
   if (dtype == KVC_BF16) {
+    const int chunk = kApplyWaves * kTPW * 16;
+    dim3 grid((max_tokens + chunk - 1) / chunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
     const int ks = (max_rank + 31) / 32;
     return D == 64 ? launch_bf16_ks<64>(a, ks, grid, stream) : launch_bf16_ks<128>(a, ks, grid, stream);
   }
+  dim3 grid((max_tokens + kApplyChunk - 1) / kApplyChunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
   const size_t lds = (size_t)max_rank * D * sizeof(float);
   if (D == 64) {
     hipLaunchKernelGGL(apply_f32_valu<64>, grid, dim3(kApplyThreads), lds, stream, a);

@@ -1,0 +1,484 @@
+// kvc_fit_state kernels: the observed transition Z = C_dst - C_src of Eq. 12 (or Z = C_dst for a base cache) and
+// its rank-r truncated SVD (Eq. 7) through the Gram matrix G = Z^T Z:
+//   gram   one workgroup per (unit, token chunk) writes the chunk's partial Gram (fp32, d x d); the eigensolver
+//          sums the partials of a unit in a fixed order in fp64, so the result does not depend on scheduling.
+//   proj   coef = Z R_r (= U_r Sigma_r), re-reading Z from the cache after the basis is known.
+//
+// bf16 caches: Z is formed in fp32 (the difference of two bf16 values is exact in fp32) and split into a bf16
+// hi/lo pair; every product is hi*hi + hi*lo + lo*hi on v_mfma_f32_16x16x32_bf16 with fp32 accumulation, about
+// 16 significant bits per operand.  In the Gram kernel Z goes through LDS transposed ([feature][token]) so that the
+// MFMA A and B fragments of a 16-feature tile are the same 16-byte LDS reads; only tiles on or above the diagonal
+// are computed and each is stored with its mirror.  In the projection the rows are read straight into the MFMA
+// B-operand layout (16 contiguous bytes per lane), the basis hi/lo is staged in LDS.
+// float32 caches use plain fp32 VALU kernels.
+#include <utility>
+
+#include "kvc_device.h"
+#include "kvc_launch.h"
+
+namespace kvc {
+
+constexpr int kFitThreads = 256;
+constexpr int kFitWaves = kFitThreads / kWave;
+
+struct FitUnit {
+  int item, lrel, layer, kv, head;
+  int64_t unit;  // index within the item's state
+};
+
+__device__ __forceinline__ FitUnit fit_unit(const FitArgs& a) {
+  FitUnit f;
+  const int H = a.pv.num_kv_heads;
+  f.item = blockIdx.z / a.num_layers;
+  f.lrel = blockIdx.z - f.item * a.num_layers;
+  f.layer = a.layer_begin + f.lrel;
+  f.kv = blockIdx.y / H;
+  f.head = blockIdx.y - f.kv * H;
+  f.unit = unit_index(f.layer, f.kv, f.head, H);
+  return f;
+}
+
+// Linear unit id shared with the eigensolver: ((item * num_layers + lrel) * 2 + kv) * H + head.
+__device__ __forceinline__ int64_t fit_linear_unit(const FitArgs& a, const FitUnit& f) {
+  return (((int64_t)f.item * a.num_layers + f.lrel) * 2 + f.kv) * a.pv.num_kv_heads + f.head;
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Gram, bf16 caches
+// ---------------------------------------------------------------------------------------------------------------
+
+// Tile idx of the upper triangle (row-major over fi <= fj) of an FT x FT grid of 16 x 16 tiles.
+constexpr int tile_fi(int idx, int FT) {
+  int fi = 0;
+  while (idx >= FT - fi) {
+    idx -= FT - fi;
+    ++fi;
+  }
+  return fi;
+}
+constexpr int tile_fj(int idx, int FT) {
+  int fi = 0;
+  while (idx >= FT - fi) {
+    idx -= FT - fi;
+    ++fi;
+  }
+  return fi + idx;
+}
+
+template <int D>
+struct GramShape {
+  static constexpr int FT = D / 16;                 // feature tiles
+  static constexpr int NTILES = FT * (FT + 1) / 2;  // tiles on or above the diagonal
+  static constexpr int TPWV = (NTILES + kFitWaves - 1) / kFitWaves;
+  static constexpr int STEP = 32;                   // tokens per MFMA K-step
+  static constexpr int LDT = STEP + 8;              // padded token stride of the transposed tile
+  static constexpr int SEGS = STEP * D / 8;         // 16-byte row segments per step
+  static constexpr int SPT = SEGS / kFitThreads;    // per thread
+};
+
+// Tile Q of wave W (tile index W + 4 Q): G[16 fi .., 16 fj ..] += Z_fi^T Z_fj with the hi/lo products.
+template <int D, int W, int Q>
+__device__ __forceinline__ void gram_tile(f32x4* acc, const bf16x8* fh, const bf16x8* fl) {
+  constexpr int idx = W + Q * kFitWaves;
+  if constexpr (idx < GramShape<D>::NTILES) {
+    constexpr int fi = tile_fi(idx, GramShape<D>::FT), fj = tile_fj(idx, GramShape<D>::FT);
+    acc[Q] = mfma16x16x32(fl[fi], fh[fj], acc[Q]);
+    acc[Q] = mfma16x16x32(fh[fi], fl[fj], acc[Q]);
+    acc[Q] = mfma16x16x32(fh[fi], fh[fj], acc[Q]);
+  }
+}
+template <int D, int W, int Q>
+__device__ __forceinline__ void gram_store(float* P, const f32x4* acc, int g, int n) {
+  constexpr int idx = W + Q * kFitWaves;
+  if constexpr (idx < GramShape<D>::NTILES) {
+    constexpr int fi = tile_fi(idx, GramShape<D>::FT), fj = tile_fj(idx, GramShape<D>::FT);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 16 * fi + 4 * g + i, col = 16 * fj + n;
+      P[row * D + col] = acc[Q][i];
+      P[col * D + row] = acc[Q][i];
+    }
+  }
+}
+template <int D, int W, int... Qs>
+__device__ __forceinline__ void gram_tiles(f32x4* acc, const bf16x8* fh, const bf16x8* fl,
+                                           std::integer_sequence<int, Qs...>) {
+  (gram_tile<D, W, Qs>(acc, fh, fl), ...);
+}
+template <int D, int W, int... Qs>
+__device__ __forceinline__ void gram_stores(float* P, const f32x4* acc, int g, int n,
+                                            std::integer_sequence<int, Qs...>) {
+  (gram_store<D, W, Qs>(P, acc, g, n), ...);
+}
+
+// Body of the bf16 Gram kernel for wave W (its tile list is known at compile time).
+template <int D, int W>
+__device__ __forceinline__ void gram_bf16_body(const FitArgs& a, const FitUnit& f, const kvc_item* itp,
+                                               int t_begin, int t_end, uint16_t* s_hi, uint16_t* s_lo) {
+  using S = GramShape<D>;
+  constexpr int LDT = S::LDT, SPT = S::SPT, FT = S::FT, TPWV = S::TPWV;
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const uint16_t* pool = static_cast<const uint16_t*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
+  const bool delta = a.mode == KVC_FIT_DELTA;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int g = lane >> 4, n = lane & 15;
+
+  f32x4 acc[TPWV];
+#pragma unroll
+  for (int q = 0; q < TPWV; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 rd[SPT], rs[SPT];
+  auto load_step = [&](int t0) {
+#pragma unroll
+    for (int q = 0; q < SPT; ++q) {
+      const int seg = tid + q * kFitThreads;
+      const int tk = seg / (D / 8), part = seg - tk * (D / 8);
+      const int t = t0 + tk;
+      rd[q] = u32x4{0, 0, 0, 0};
+      rs[q] = u32x4{0, 0, 0, 0};
+      if (t < t_end) {
+        const int64_t od = row_offset(a.pv, dst_tab, itp->dst_offset, t, f.head);
+        if (od >= 0) rd[q] = *reinterpret_cast<const u32x4*>(pool + od + 8 * part);
+        if (delta) {
+          const int64_t os = row_offset(a.pv, src_tab, itp->src_offset, t, f.head);
+          if (os >= 0) rs[q] = *reinterpret_cast<const u32x4*>(pool + os + 8 * part);
+        }
+      }
+    }
+  };
+  auto stage_step = [&]() {
+#pragma unroll
+    for (int q = 0; q < SPT; ++q) {
+      const int seg = tid + q * kFitThreads;
+      const int tk = seg / (D / 8), part = seg - tk * (D / 8);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float z0 = bf16_lo_to_f32(rd[q][w]) - bf16_lo_to_f32(rs[q][w]);
+        const float z1 = bf16_hi_to_f32(rd[q][w]) - bf16_hi_to_f32(rs[q][w]);
+        uint32_t h0, l0, h1, l1;
+        split_bf16(z0, h0, l0);
+        split_bf16(z1, h1, l1);
+        const int fe = 8 * part + 2 * w;
+        s_hi[fe * LDT + tk] = (uint16_t)h0;
+        s_lo[fe * LDT + tk] = (uint16_t)l0;
+        s_hi[(fe + 1) * LDT + tk] = (uint16_t)h1;
+        s_lo[(fe + 1) * LDT + tk] = (uint16_t)l1;
+      }
+    }
+  };
+
+  load_step(t_begin);
+  for (int t0 = t_begin; t0 < t_end; t0 += S::STEP) {
+    stage_step();
+    __syncthreads();
+    if (t0 + S::STEP < t_end) load_step(t0 + S::STEP);
+    bf16x8 fh[FT], fl[FT];
+#pragma unroll
+    for (int ft = 0; ft < FT; ++ft) {
+      fh[ft] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[(16 * ft + n) * LDT + 8 * g]));
+      fl[ft] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[(16 * ft + n) * LDT + 8 * g]));
+    }
+    gram_tiles<D, W>(acc, fh, fl, std::make_integer_sequence<int, TPWV>{});
+    __syncthreads();
+  }
+  const int64_t lu = fit_linear_unit(a, f);
+  float* P = a.partials + ((size_t)lu * a.max_parts + blockIdx.x) * D * D;
+  gram_stores<D, W>(P, acc, g, n, std::make_integer_sequence<int, TPWV>{});
+}
+
+template <int D>
+__global__ __launch_bounds__(kFitThreads) void gram_bf16_mfma(FitArgs a) {
+  using S = GramShape<D>;
+  static_assert(S::SEGS % kFitThreads == 0, "segments per thread");
+  __shared__ __attribute__((aligned(16))) uint16_t s_hi[D * S::LDT];
+  __shared__ __attribute__((aligned(16))) uint16_t s_lo[D * S::LDT];
+  const FitUnit f = fit_unit(a);
+  const kvc_item* itp = a.items + f.item;
+  const int r = itp->state.rank;
+  const int Ts = itp->state.num_tokens;
+  const int t_begin = blockIdx.x * a.part_tokens;
+  if (r == 0 || t_begin >= Ts) return;
+  const int t_end = min(Ts, t_begin + a.part_tokens);
+  switch (threadIdx.x >> 6) {
+    case 0: gram_bf16_body<D, 0>(a, f, itp, t_begin, t_end, s_hi, s_lo); break;
+    case 1: gram_bf16_body<D, 1>(a, f, itp, t_begin, t_end, s_hi, s_lo); break;
+    case 2: gram_bf16_body<D, 2>(a, f, itp, t_begin, t_end, s_hi, s_lo); break;
+    default: gram_bf16_body<D, 3>(a, f, itp, t_begin, t_end, s_hi, s_lo); break;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Gram, fp32 caches (VALU, fp32 accumulation)
+// ---------------------------------------------------------------------------------------------------------------
+
+template <int D>
+__global__ __launch_bounds__(kFitThreads) void gram_f32_valu(FitArgs a) {
+  constexpr int STEP = 32;
+  constexpr int NE = D * (D + 1) / 2;
+  constexpr int EPT = (NE + kFitThreads - 1) / kFitThreads;
+  __shared__ float s_z[STEP][D + 1];
+
+  const FitUnit f = fit_unit(a);
+  const kvc_item* itp = a.items + f.item;
+  const int r = itp->state.rank;
+  const int Ts = itp->state.num_tokens;
+  const int c = blockIdx.x;
+  const int t_begin = c * a.part_tokens;
+  if (r == 0 || t_begin >= Ts) return;
+  const int t_end = min(Ts, t_begin + a.part_tokens);
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const float* pool = static_cast<const float*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
+  const bool delta = a.mode == KVC_FIT_DELTA;
+  const int tid = threadIdx.x;
+
+  int ei[EPT], ej[EPT];
+  float acc[EPT];
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) {
+    int e = tid + q * kFitThreads;
+    acc[q] = 0.f;
+    ei[q] = -1;
+    ej[q] = 0;
+    if (e < NE) {
+      int i = 0;
+      while (e >= D - i) {
+        e -= D - i;
+        ++i;
+      }
+      ei[q] = i;
+      ej[q] = i + e;
+    }
+  }
+  for (int t0 = t_begin; t0 < t_end; t0 += STEP) {
+    for (int e = tid; e < STEP * D; e += kFitThreads) {
+      const int tk = e / D, fe = e - tk * D;
+      const int t = t0 + tk;
+      float z = 0.f;
+      if (t < t_end) {
+        const int64_t od = row_offset(a.pv, dst_tab, itp->dst_offset, t, f.head);
+        if (od >= 0) z = pool[od + fe];
+        if (delta) {
+          const int64_t os = row_offset(a.pv, src_tab, itp->src_offset, t, f.head);
+          if (os >= 0) z -= pool[os + fe];
+        }
+      }
+      s_z[tk][fe] = z;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < EPT; ++q) {
+      if (ei[q] < 0) continue;
+      float s = acc[q];
+      for (int tk = 0; tk < STEP; ++tk) s = fmaf(s_z[tk][ei[q]], s_z[tk][ej[q]], s);
+      acc[q] = s;
+    }
+    __syncthreads();
+  }
+  float* P = a.partials + ((size_t)fit_linear_unit(a, f) * a.max_parts + c) * D * D;
+#pragma unroll
+  for (int q = 0; q < EPT; ++q) {
+    if (ei[q] < 0) continue;
+    P[ei[q] * D + ej[q]] = acc[q];
+    P[ej[q] * D + ei[q]] = acc[q];
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Projection coef = Z R_r, bf16 caches
+// ---------------------------------------------------------------------------------------------------------------
+
+constexpr int kProjTilesPerWave = 16;
+constexpr int kProjChunk = kFitWaves * kProjTilesPerWave * 16;
+
+template <int D, int MTR>
+__global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
+  constexpr int KS = D / 32;          // K-steps over features
+  constexpr int RP = MTR * 16;        // padded rank
+  constexpr bool kRegFrags = MTR <= 2;
+  constexpr int FM = kRegFrags ? MTR : 1, FK = kRegFrags ? KS : 1;
+  __shared__ __attribute__((aligned(16))) uint16_t s_hi[RP * D];
+  __shared__ __attribute__((aligned(16))) uint16_t s_lo[RP * D];
+
+  const FitUnit f = fit_unit(a);
+  const kvc_item* itp = a.items + f.item;
+  const int r = itp->state.rank;
+  const int Ts = itp->state.num_tokens;
+  const int t_begin = blockIdx.x * kProjChunk;
+  if (r == 0 || t_begin >= Ts) return;
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const uint16_t* pool = static_cast<const uint16_t*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
+  const bool delta = a.mode == KVC_FIT_DELTA;
+  const float* basis = itp->state.basis + f.unit * (int64_t)r * D;
+  uint16_t* coef = static_cast<uint16_t*>(itp->state.coef) + f.unit * (int64_t)Ts * r;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, n = lane & 15;
+
+  for (int e = tid; e < RP * D; e += kFitThreads) {
+    const int k = e / D;
+    const float x = k < r ? basis[e] : 0.f;
+    uint32_t hb, lb;
+    split_bf16(x, hb, lb);
+    s_hi[e] = (uint16_t)hb;
+    s_lo[e] = (uint16_t)lb;
+  }
+  __syncthreads();
+  bf16x8 ah[FM][FK], al[FM][FK];
+  if constexpr (kRegFrags) {
+#pragma unroll
+    for (int mt = 0; mt < MTR; ++mt)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int o = (16 * mt + n) * D + 32 * ks + 8 * g;
+        ah[mt][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[o]));
+        al[mt][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[o]));
+      }
+  }
+
+  for (int j = 0; j < kProjTilesPerWave; ++j) {
+    const int t0 = t_begin + (j * kFitWaves + wave) * 16;
+    if (t0 >= Ts) break;
+    const int t = t0 + n;
+    const bool valid = t < Ts;
+    const int64_t od = valid ? row_offset(a.pv, dst_tab, itp->dst_offset, t, f.head) : -1;
+    const int64_t os = (valid && delta) ? row_offset(a.pv, src_tab, itp->src_offset, t, f.head) : -1;
+    bf16x8 zh[KS], zl[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const u32x4 d = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+      const u32x4 s = os >= 0 ? *reinterpret_cast<const u32x4*>(pool + os + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+      u32x4 hw, lw;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float z0 = bf16_lo_to_f32(d[w]) - bf16_lo_to_f32(s[w]);
+        const float z1 = bf16_hi_to_f32(d[w]) - bf16_hi_to_f32(s[w]);
+        uint32_t h0, l0, h1, l1;
+        split_bf16(z0, h0, l0);
+        split_bf16(z1, h1, l1);
+        hw[w] = h0 | (h1 << 16);
+        lw[w] = l0 | (l1 << 16);
+      }
+      zh[ks] = as_bf16x8(hw);
+      zl[ks] = as_bf16x8(lw);
+    }
+#pragma unroll
+    for (int mt = 0; mt < MTR; ++mt) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        bf16x8 fh, fl;
+        if constexpr (kRegFrags) {
+          fh = ah[mt][ks];
+          fl = al[mt][ks];
+        } else {
+          const int o = (16 * mt + n) * D + 32 * ks + 8 * g;
+          fh = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[o]));
+          fl = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[o]));
+        }
+        acc = mfma16x16x32(fl, zh[ks], acc);
+        acc = mfma16x16x32(fh, zl[ks], acc);
+        acc = mfma16x16x32(fh, zh[ks], acc);
+      }
+      // lane holds coef[t][16 mt + 4 g + i], i = 0..3
+      if (valid) {
+        const int k0 = 16 * mt + 4 * g;
+        uint16_t* cp = coef + (int64_t)t * r + k0;
+        if ((r & 3) == 0 && k0 + 4 <= r) {
+          uint2 w;
+          w.x = pack_bf16x2(acc[0], acc[1]);
+          w.y = pack_bf16x2(acc[2], acc[3]);
+          *reinterpret_cast<uint2*>(cp) = w;
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (k0 + i < r) cp[i] = (uint16_t)f32_to_bf16_bits(acc[i]);
+        }
+      }
+    }
+  }
+}
+
+// Projection, fp32 caches: one thread per (token, rank), fp32 FMAs over the features.
+template <int D>
+__global__ __launch_bounds__(kFitThreads) void proj_f32_valu(FitArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float s_b[];  // [r][D]
+  const FitUnit f = fit_unit(a);
+  const kvc_item* itp = a.items + f.item;
+  const int r = itp->state.rank;
+  const int Ts = itp->state.num_tokens;
+  const int t_begin = blockIdx.x * kProjChunk;
+  if (r == 0 || t_begin >= Ts) return;
+  const int t_end = min(Ts, t_begin + kProjChunk);
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const float* pool = static_cast<const float*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
+  const bool delta = a.mode == KVC_FIT_DELTA;
+  const float* basis = itp->state.basis + f.unit * (int64_t)r * D;
+  float* coef = static_cast<float*>(itp->state.coef) + f.unit * (int64_t)Ts * r;
+  for (int e = threadIdx.x; e < r * D; e += kFitThreads) s_b[e] = basis[e];
+  __syncthreads();
+  const int64_t total = (int64_t)(t_end - t_begin) * r;
+  for (int64_t e = threadIdx.x; e < total; e += kFitThreads) {
+    const int t = t_begin + (int)(e / r), k = (int)(e % r);
+    const int64_t od = row_offset(a.pv, dst_tab, itp->dst_offset, t, f.head);
+    const int64_t os = delta ? row_offset(a.pv, src_tab, itp->src_offset, t, f.head) : -1;
+    float s = 0.f;
+    for (int fe = 0; fe < D; ++fe) {
+      float z = od >= 0 ? pool[od + fe] : 0.f;
+      if (os >= 0) z -= pool[os + fe];
+      s = fmaf(z, s_b[k * D + fe], s);
+    }
+    coef[(int64_t)t * r + k] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------------------------------------------
+
+int proj_chunk_tokens() { return kProjChunk; }
+
+hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream) {
+  dim3 grid(a.max_parts, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+  const int D = a.pv.head_dim;
+  if (dtype == KVC_BF16) {
+    if (D == 64) hipLaunchKernelGGL(gram_bf16_mfma<64>, grid, dim3(kFitThreads), 0, stream, a);
+    else hipLaunchKernelGGL(gram_bf16_mfma<128>, grid, dim3(kFitThreads), 0, stream, a);
+  } else {
+    if (D == 64) hipLaunchKernelGGL(gram_f32_valu<64>, grid, dim3(kFitThreads), 0, stream, a);
+    else hipLaunchKernelGGL(gram_f32_valu<128>, grid, dim3(kFitThreads), 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_proj_bf16(const FitArgs& a, int mtr, dim3 grid, hipStream_t stream) {
+  switch (mtr) {
+    case 1: hipLaunchKernelGGL((proj_bf16_mfma<D, 1>), grid, dim3(kFitThreads), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((proj_bf16_mfma<D, 2>), grid, dim3(kFitThreads), 0, stream, a); break;
+    case 3:
+    case 4: hipLaunchKernelGGL((proj_bf16_mfma<D, 4>), grid, dim3(kFitThreads), 0, stream, a); break;
+    default: hipLaunchKernelGGL((proj_bf16_mfma<D, 8>), grid, dim3(kFitThreads), 0, stream, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fit_proj(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens, int max_rank,
+                           hipStream_t stream) {
+  if (max_rank == 0 || max_tokens == 0) return hipSuccess;
+  dim3 grid((max_tokens + kProjChunk - 1) / kProjChunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+  const int D = a.pv.head_dim;
+  if (dtype == KVC_BF16) {
+    const int mtr = (max_rank + 15) / 16;
+    return D == 64 ? launch_proj_bf16<64>(a, mtr, grid, stream) : launch_proj_bf16<128>(a, mtr, grid, stream);
+  }
+  const size_t lds = (size_t)max_rank * D * sizeof(float);
+  if (D == 64) hipLaunchKernelGGL(proj_f32_valu<64>, grid, dim3(kFitThreads), lds, stream, a);
+  else hipLaunchKernelGGL(proj_f32_valu<128>, grid, dim3(kFitThreads), lds, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace kvc

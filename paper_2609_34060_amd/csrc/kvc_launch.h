@@ -23,4 +23,46 @@ int apply_chunk_tokens();
 hipError_t launch_apply(const ApplyArgs& a, kvc_dtype dtype, int max_rank, int max_tokens, int num_items,
                         hipStream_t stream);
 
+// Fit (kvc_fit.hip): Gram partials, then projection after the eigensolver.
+struct FitArgs {
+  PoolView pv;
+  LayerPtrs layers;
+  const kvc_item* items;       // device; each item's state receives the fit
+  const int32_t* src_tables;
+  const int32_t* dst_tables;
+  int32_t max_blocks;
+  int32_t layer_begin;
+  int32_t num_layers;
+  int32_t mode;                // kvc_fit_mode
+  float* partials;             // workspace [unit][max_parts][d][d]
+  int32_t max_parts;
+  int32_t part_tokens;
+};
+int proj_chunk_tokens();
+hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream);
+hipError_t launch_fit_proj(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens, int max_rank,
+                           hipStream_t stream);
+
+// Top-r eigenpairs of per-unit Gram matrices (kvc_eig.hip).  Unit u enumerates (item, layer, K/V, head) with the
+// head fastest: u = ((item * num_layers + layer - layer_begin) * 2 + kv) * num_kv_heads + head.
+struct EigArgs {
+  int32_t n;                  // head_dim
+  int32_t num_units;
+  const float* partials;      // fp32 partial Grams [unit][max_parts][n][n], or null
+  int32_t max_parts;
+  int32_t part_tokens;        // tokens per partial: a unit with T_s rows has ceil(T_s / part_tokens) partials
+  const double* dense;        // fp64 Grams [unit][n][n] when partials is null
+  const kvc_item* items;      // device items whose states receive basis/sigma, or null
+  kvc_state state;            // the receiving state when items is null
+  int32_t layer_begin;
+  int32_t num_layers;
+  int32_t num_kv_heads;
+  double* reflect;            // workspace [unit][n][n]
+  double* reflect_beta;       // workspace [unit][n]
+  double* vecs;               // workspace [unit][KVC_MAX_RANK][n]
+  uint32_t seed;
+};
+size_t eig_lds_bytes(int n);
+hipError_t launch_eig(const EigArgs& a, hipStream_t stream);
+
 }  // namespace kvc
