@@ -122,6 +122,71 @@ FitPlan plan_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int32_t le)
   return p;
 }
 
+kvc_status check_chain(const kvc_state* a, const kvc_state* b, const kvc_state* o, int32_t lb, int32_t le) {
+  if (!a || !b || !o) return KVC_ERR_NULL_ARG;
+  const int32_t L = a->num_layers, H = a->num_kv_heads, d = a->head_dim;
+  if (d != 64 && d != 128) return KVC_ERR_UNSUPPORTED;
+  if (L < 1 || H < 1) return KVC_ERR_SHAPE;
+  for (const kvc_state* s : {a, b, o}) {
+    kvc_status st = check_state_shape(*s, L, H, d);
+    if (st != KVC_OK) return st;
+  }
+  if (b->coef_dtype != a->coef_dtype || o->coef_dtype != a->coef_dtype) return KVC_ERR_DTYPE;
+  if (lb < 0 || le < lb || le > L) return KVC_ERR_SHAPE;
+  if (o->num_tokens != std::max(a->num_tokens, b->num_tokens)) return KVC_ERR_SHAPE;
+  if (o->rank > std::min<int32_t>({a->rank + b->rank, d, o->num_tokens})) return KVC_ERR_SHAPE;
+  // the output must not overwrite an input
+  if (o->rank > 0 && o->num_tokens > 0) {
+    for (const kvc_state* s : {a, b}) {
+      if (s->rank > 0 && (o->coef == s->coef || o->basis == s->basis)) return KVC_ERR_ALIAS;
+    }
+  }
+  return KVC_OK;
+}
+
+// Chain workspace: H partials (chunks sized as in the fit), the fp64 intermediates of G = K H K^T, the eigensolver
+// scratch and Y.
+struct ChainPlan {
+  int32_t mp = 16, part_tokens = 256, max_parts = 1;
+  size_t units = 0, off_partials = 0, off_hsum = 0, off_pmat = 0, off_gram = 0, off_reflect = 0, off_beta = 0,
+         off_vecs = 0, off_ymat = 0, total = 0;
+};
+
+ChainPlan plan_chain(const kvc_state* a, const kvc_state* b, const kvc_state* o, int32_t lb, int32_t le) {
+  ChainPlan p;
+  const size_t d = a->head_dim;
+  const size_t m = static_cast<size_t>(a->rank) + b->rank;
+  p.mp = static_cast<int32_t>(std::max<size_t>(16, (m + 15) / 16 * 16));
+  p.units = static_cast<size_t>(le - lb) * 2 * a->num_kv_heads;
+  const int64_t T = std::max<int32_t>(o->num_tokens, 1);
+  const int64_t want_parts = std::max<int64_t>(1, (4096 + static_cast<int64_t>(p.units) - 1) /
+                                                      std::max<int64_t>(1, static_cast<int64_t>(p.units)));
+  int64_t part = (T + want_parts - 1) / want_parts;
+  part = std::max<int64_t>(256, (part + 31) / 32 * 32);
+  p.part_tokens = static_cast<int32_t>(part);
+  p.max_parts = static_cast<int32_t>((T + part - 1) / part);
+  const size_t U = p.units, mp = p.mp;
+  size_t off = 0;
+  p.off_partials = off;
+  off = align256(off + U * p.max_parts * mp * mp * sizeof(float));
+  p.off_hsum = off;
+  off = align256(off + U * m * m * sizeof(double));
+  p.off_pmat = off;
+  off = align256(off + U * m * d * sizeof(double));
+  p.off_gram = off;
+  off = align256(off + U * d * d * sizeof(double));
+  p.off_reflect = off;
+  off = align256(off + U * d * d * sizeof(double));
+  p.off_beta = off;
+  off = align256(off + U * d * sizeof(double));
+  p.off_vecs = off;
+  off = align256(off + U * KVC_MAX_RANK * d * sizeof(double));
+  p.off_ymat = off;
+  off = align256(off + U * m * static_cast<size_t>(o->rank) * sizeof(float));
+  p.total = off;
+  return p;
+}
+
 void fill_pool_view(const kvc_cache* c, kvc::PoolView& pv) {
   pv.block_stride = c->block_stride;
   pv.token_stride = c->token_stride;
@@ -286,9 +351,51 @@ kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t
   }
   return KVC_OK;
 }
-size_t kvc_chain_workspace_bytes(const kvc_state*, const kvc_state*, const kvc_state*, int32_t, int32_t) { return 0; }
-kvc_status kvc_chain(const kvc_state*, const kvc_state*, kvc_state*, int32_t, int32_t, void*, size_t, hipStream_t) {
-  return KVC_ERR_UNSUPPORTED;
+size_t kvc_chain_workspace_bytes(const kvc_state* first, const kvc_state* second, const kvc_state* out,
+                                 int32_t layer_begin, int32_t layer_end) {
+  if (check_chain(first, second, out, layer_begin, layer_end) != KVC_OK) return 0;
+  return plan_chain(first, second, out, layer_begin, layer_end).total;
+}
+
+kvc_status kvc_chain(const kvc_state* first, const kvc_state* second, kvc_state* out, int32_t layer_begin,
+                     int32_t layer_end, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  kvc_status s = check_chain(first, second, out, layer_begin, layer_end);
+  if (s != KVC_OK) return s;
+  if (layer_end == layer_begin || out->rank == 0 || out->num_tokens == 0) return KVC_OK;
+  const ChainPlan p = plan_chain(first, second, out, layer_begin, layer_end);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < p.total)
+    return KVC_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  kvc::ChainArgs ca;
+  std::memset(&ca, 0, sizeof(ca));
+  ca.first = *first;
+  ca.second = *second;
+  ca.out = *out;
+  ca.layer_begin = layer_begin;
+  ca.num_layers = layer_end - layer_begin;
+  ca.num_units = static_cast<int32_t>(p.units);
+  ca.mp = p.mp;
+  ca.partials = reinterpret_cast<float*>(ws + p.off_partials);
+  ca.max_parts = p.max_parts;
+  ca.part_tokens = p.part_tokens;
+  ca.hsum = reinterpret_cast<double*>(ws + p.off_hsum);
+  ca.pmat = reinterpret_cast<double*>(ws + p.off_pmat);
+  ca.gram = reinterpret_cast<double*>(ws + p.off_gram);
+  ca.ymat = reinterpret_cast<float*>(ws + p.off_ymat);
+  kvc::EigArgs ea;
+  std::memset(&ea, 0, sizeof(ea));
+  ea.n = first->head_dim;
+  ea.num_units = ca.num_units;
+  ea.dense = ca.gram;
+  ea.state = *out;
+  ea.layer_begin = layer_begin;
+  ea.num_layers = ca.num_layers;
+  ea.num_kv_heads = first->num_kv_heads;
+  ea.reflect = reinterpret_cast<double*>(ws + p.off_reflect);
+  ea.reflect_beta = reinterpret_cast<double*>(ws + p.off_beta);
+  ea.vecs = reinterpret_cast<double*>(ws + p.off_vecs);
+  ea.seed = 0xC4A1u;
+  return hip_status(kvc::launch_chain(ca, ea, stream));
 }
 
 }  // extern "C"

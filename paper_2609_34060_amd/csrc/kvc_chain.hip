@@ -1,0 +1,352 @@
+// kvc_chain kernels: compose S1 = (A1, B1) = Delta_{j<-i} and S2 = (A2, B2) = Delta_{k<-j} into the rank-r_out
+// truncated SVD of M = A1 B1 + A2 B2 (Eq. 6 then Eq. 7) without forming M.  With A = [A1 A2] (T x m, m = r1 + r2)
+// and K = [B1; B2]^T (d x m), M = A K^T and M^T M = K (A^T A) K^T, so
+//   cgram     H = A^T A from the coefficient rows (one pass over T; rows past a state's T are zero), partial per
+//             token chunk.  bf16 coefficients are exact MFMA operands; fp32 ones use the bf16 hi/lo split.
+//   assemble  G = K H K^T in fp64 (d x d), the Gram of M.
+//   eig       the shared eigensolver: top r_out eigenvectors R of G, sigma = sqrt(lambda) -> out.basis, out.sigma.
+//   ymat      Y = K^T R (m x r_out), so that the new coefficients are M R = A Y.
+//   cproj     A_out = A Y, a second pass over the coefficient rows on MFMA (Y as a bf16 hi/lo pair).
+#include <utility>
+
+#include "kvc_device.h"
+#include "kvc_launch.h"
+
+namespace kvc {
+
+constexpr int kChainThreads = 256;
+constexpr int kChainWaves = kChainThreads / kWave;
+
+struct ChainUnit {
+  int lrel, layer, kv, head;
+  int64_t idx;  // unit index within the states
+};
+
+__device__ __forceinline__ ChainUnit chain_unit(const ChainArgs& a, int u) {
+  ChainUnit c;
+  const int H = a.first.num_kv_heads;
+  c.lrel = u / (2 * H);
+  int rem = u - c.lrel * 2 * H;
+  c.kv = rem / H;
+  c.head = rem - c.kv * H;
+  c.layer = a.layer_begin + c.lrel;
+  c.idx = unit_index(c.layer, c.kv, c.head, H);
+  return c;
+}
+
+// Concatenated coefficient [A1 A2][t][l] as a float (0 outside either state's rows).
+template <bool F32>
+__device__ __forceinline__ float cat_coef(const ChainArgs& a, const void* A1, const void* A2, int t, int l) {
+  const int r1 = a.first.rank, r2 = a.second.rank;
+  if (l < r1) {
+    if (t >= a.first.num_tokens) return 0.f;
+    return F32 ? static_cast<const float*>(A1)[(int64_t)t * r1 + l]
+               : bf16_lo_to_f32(static_cast<const uint16_t*>(A1)[(int64_t)t * r1 + l]);
+  }
+  l -= r1;
+  if (l >= r2 || t >= a.second.num_tokens) return 0.f;
+  return F32 ? static_cast<const float*>(A2)[(int64_t)t * r2 + l]
+             : bf16_lo_to_f32(static_cast<const uint16_t*>(A2)[(int64_t)t * r2 + l]);
+}
+
+__device__ __forceinline__ float cat_basis(const ChainArgs& a, int64_t idx, int l, int f) {
+  const int r1 = a.first.rank, d = a.first.head_dim;
+  if (l < r1) return a.first.basis[(idx * r1 + l) * d + f];
+  return a.second.basis[(idx * a.second.rank + (l - r1)) * d + f];
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// cgram: partial H over a token chunk, tiles on or above the diagonal
+// ---------------------------------------------------------------------------------------------------------------
+
+template <int FT, bool F32>
+__global__ __launch_bounds__(kChainThreads) void chain_gram(ChainArgs a) {
+  constexpr int MP = FT * 16;
+  constexpr int NT = FT * (FT + 1) / 2;
+  constexpr int TPWV = (NT + kChainWaves - 1) / kChainWaves;
+  constexpr int STEP = 32, LDT = STEP + 8;
+  __shared__ __attribute__((aligned(16))) uint16_t s_hi[MP * LDT];
+  __shared__ __attribute__((aligned(16))) uint16_t s_lo[F32 ? MP * LDT : 8];
+
+  const int u = blockIdx.y;
+  const ChainUnit cu = chain_unit(a, u);
+  const int T = a.out.num_tokens;
+  const int t_begin = blockIdx.x * a.part_tokens;
+  if (t_begin >= T) return;
+  const int t_end = min(T, t_begin + a.part_tokens);
+  const int esz = F32 ? 4 : 2;
+  const void* A1 = static_cast<const char*>(a.first.coef) + cu.idx * (int64_t)a.first.num_tokens * a.first.rank * esz;
+  const void* A2 =
+      static_cast<const char*>(a.second.coef) + cu.idx * (int64_t)a.second.num_tokens * a.second.rank * esz;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, n = lane & 15;
+
+  f32x4 acc[TPWV];
+#pragma unroll
+  for (int q = 0; q < TPWV; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int t0 = t_begin; t0 < t_end; t0 += STEP) {
+    for (int e = tid; e < STEP * MP; e += kChainThreads) {
+      const int tk = e / MP, l = e - tk * MP;
+      const int t = t0 + tk;
+      const float x = (t < t_end) ? cat_coef<F32>(a, A1, A2, t, l) : 0.f;
+      if (F32) {
+        uint32_t hb, lb;
+        split_bf16(x, hb, lb);
+        s_hi[l * LDT + tk] = (uint16_t)hb;
+        s_lo[l * LDT + tk] = (uint16_t)lb;
+      } else {
+        s_hi[l * LDT + tk] = (uint16_t)(__float_as_uint(x) >> 16);  // exact: x came from a bf16
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < TPWV; ++q) {
+      const int idx = wave + q * kChainWaves;
+      if (idx < NT) {
+        int fi = 0, rem = idx;
+        while (rem >= FT - fi) {
+          rem -= FT - fi;
+          ++fi;
+        }
+        const int fj = fi + rem;
+        const int oa = (16 * fi + n) * LDT + 8 * g, ob = (16 * fj + n) * LDT + 8 * g;
+        const bf16x8 ah = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[oa]));
+        const bf16x8 bh = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[ob]));
+        if constexpr (F32) {
+          const bf16x8 al = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[oa]));
+          const bf16x8 bl = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[ob]));
+          acc[q] = mfma16x16x32(al, bh, acc[q]);
+          acc[q] = mfma16x16x32(ah, bl, acc[q]);
+        }
+        acc[q] = mfma16x16x32(ah, bh, acc[q]);
+      }
+    }
+    __syncthreads();
+  }
+  float* P = a.partials + ((size_t)u * a.max_parts + blockIdx.x) * MP * MP;
+#pragma unroll
+  for (int q = 0; q < TPWV; ++q) {
+    const int idx = wave + q * kChainWaves;
+    if (idx < NT) {
+      int fi = 0, rem = idx;
+      while (rem >= FT - fi) {
+        rem -= FT - fi;
+        ++fi;
+      }
+      const int fj = fi + rem;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 16 * fi + 4 * g + i, col = 16 * fj + n;
+        P[row * MP + col] = acc[q][i];
+        P[col * MP + row] = acc[q][i];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// assemble: H = sum of partials (fp64), P = H K^T (m x d), G = K P (d x d)
+// ---------------------------------------------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kChainThreads) void chain_assemble(ChainArgs a) {
+  const int u = blockIdx.x;
+  const ChainUnit cu = chain_unit(a, u);
+  const int m = a.first.rank + a.second.rank, MP = a.mp, d = a.first.head_dim;
+  const int T = a.out.num_tokens;
+  const int parts = (T + a.part_tokens - 1) / a.part_tokens;
+  const float* PP = a.partials + (size_t)u * a.max_parts * MP * MP;
+  double* Hs = a.hsum + (size_t)u * m * m;
+  double* Pm = a.pmat + (size_t)u * m * d;
+  double* G = a.gram + (size_t)u * d * d;
+  for (int e = threadIdx.x; e < m * m; e += kChainThreads) {
+    const int i = e / m, j = e - i * m;
+    double s = 0.0;
+    for (int c = 0; c < parts; ++c) s += (double)PP[(size_t)c * MP * MP + i * MP + j];
+    Hs[e] = s;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < m * d; e += kChainThreads) {
+    const int l = e / d, f = e - l * d;
+    double s = 0.0;
+    for (int k = 0; k < m; ++k) s += Hs[l * m + k] * (double)cat_basis(a, cu.idx, k, f);
+    Pm[e] = s;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < d * d; e += kChainThreads) {
+    const int i = e / d, j = e - i * d;
+    if (j < i) continue;
+    double s = 0.0;
+    for (int l = 0; l < m; ++l) s += (double)cat_basis(a, cu.idx, l, i) * Pm[l * d + j];
+    G[i * d + j] = s;
+    G[j * d + i] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// ymat: Y = K^T R with R = out.basis^T (fp64 accumulation, stored fp32)
+// ---------------------------------------------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kChainThreads) void chain_ymat(ChainArgs a) {
+  const int u = blockIdx.x;
+  const ChainUnit cu = chain_unit(a, u);
+  const int m = a.first.rank + a.second.rank, ro = a.out.rank, d = a.first.head_dim;
+  const float* Bo = a.out.basis + cu.idx * (int64_t)ro * d;
+  float* Y = a.ymat + (size_t)u * m * ro;
+  for (int e = threadIdx.x; e < m * ro; e += kChainThreads) {
+    const int l = e / ro, k = e - l * ro;
+    double s = 0.0;
+    for (int f = 0; f < d; ++f) s += (double)cat_basis(a, cu.idx, l, f) * (double)Bo[k * d + f];
+    Y[e] = (float)s;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// cproj: A_out = [A1 A2] Y on MFMA.  M = output rank (16 per tile), N = token (16), K = concatenated rank (32 per
+// step).  Y^T is staged in LDS as a bf16 hi/lo pair; the coefficient rows are the B operand.
+// ---------------------------------------------------------------------------------------------------------------
+
+constexpr int kCprojTilesPerWave = 8;
+constexpr int kCprojChunk = kChainWaves * kCprojTilesPerWave * 16;
+
+template <int MTR, bool F32>
+__global__ __launch_bounds__(kChainThreads) void chain_proj(ChainArgs a) {
+  extern __shared__ __attribute__((aligned(16))) uint16_t s_y[];  // hi [MTR*16][KP], lo [MTR*16][KP]
+  const int u = blockIdx.y;
+  const ChainUnit cu = chain_unit(a, u);
+  const int T = a.out.num_tokens;
+  const int t_begin = blockIdx.x * kCprojChunk;
+  if (t_begin >= T) return;
+  const int m = a.first.rank + a.second.rank, ro = a.out.rank;
+  const int KSC = (m + 31) / 32, KP = KSC * 32;
+  uint16_t* s_hi = s_y;
+  uint16_t* s_lo = s_y + MTR * 16 * KP;
+  const float* Y = a.ymat + (size_t)u * m * ro;
+  for (int e = threadIdx.x; e < MTR * 16 * KP; e += kChainThreads) {
+    const int k = e / KP, l = e - k * KP;
+    const float y = (k < ro && l < m) ? Y[l * ro + k] : 0.f;
+    uint32_t hb, lb;
+    split_bf16(y, hb, lb);
+    s_hi[e] = (uint16_t)hb;
+    s_lo[e] = (uint16_t)lb;
+  }
+  __syncthreads();
+  const int esz = F32 ? 4 : 2;
+  const void* A1 = static_cast<const char*>(a.first.coef) + cu.idx * (int64_t)a.first.num_tokens * a.first.rank * esz;
+  const void* A2 =
+      static_cast<const char*>(a.second.coef) + cu.idx * (int64_t)a.second.num_tokens * a.second.rank * esz;
+  void* Co = static_cast<char*>(a.out.coef) + cu.idx * (int64_t)T * ro * esz;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, n = lane & 15;
+
+  for (int j = 0; j < kCprojTilesPerWave; ++j) {
+    const int t0 = t_begin + (j * kChainWaves + wave) * 16;
+    if (t0 >= T) break;
+    const int t = t0 + n;
+    f32x4 acc[MTR];
+#pragma unroll
+    for (int mt = 0; mt < MTR; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < KSC; ++ks) {
+      uint32_t ch[4], cl[4];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int l = 32 * ks + 8 * g + 2 * w;
+        const float x0 = (t < T) ? cat_coef<F32>(a, A1, A2, t, l) : 0.f;
+        const float x1 = (t < T) ? cat_coef<F32>(a, A1, A2, t, l + 1) : 0.f;
+        if (F32) {
+          uint32_t h0, l0, h1, l1;
+          split_bf16(x0, h0, l0);
+          split_bf16(x1, h1, l1);
+          ch[w] = h0 | (h1 << 16);
+          cl[w] = l0 | (l1 << 16);
+        } else {
+          ch[w] = (__float_as_uint(x0) >> 16) | (__float_as_uint(x1) & 0xffff0000u);
+          cl[w] = 0;
+        }
+      }
+      const bf16x8 bh = as_bf16x8(u32x4{ch[0], ch[1], ch[2], ch[3]});
+      const bf16x8 bl = as_bf16x8(u32x4{cl[0], cl[1], cl[2], cl[3]});
+#pragma unroll
+      for (int mt = 0; mt < MTR; ++mt) {
+        const int o = (16 * mt + n) * KP + 32 * ks + 8 * g;
+        const bf16x8 yh = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[o]));
+        const bf16x8 yl = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[o]));
+        acc[mt] = mfma16x16x32(yl, bh, acc[mt]);
+        if constexpr (F32) acc[mt] = mfma16x16x32(yh, bl, acc[mt]);
+        acc[mt] = mfma16x16x32(yh, bh, acc[mt]);
+      }
+    }
+    if (t < T) {
+#pragma unroll
+      for (int mt = 0; mt < MTR; ++mt) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int k = 16 * mt + 4 * g + i;
+          if (k < ro) {
+            if (F32) static_cast<float*>(Co)[(int64_t)t * ro + k] = acc[mt][i];
+            else static_cast<uint16_t*>(Co)[(int64_t)t * ro + k] = (uint16_t)f32_to_bf16_bits(acc[mt][i]);
+          }
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------------------------------------------
+
+template <int FT, bool F32>
+static void launch_cgram_one(dim3 grid, hipStream_t stream, const ChainArgs& a) {
+  hipLaunchKernelGGL((chain_gram<FT, F32>), grid, dim3(kChainThreads), 0, stream, a);
+}
+
+template <bool F32, int... FTs>
+static void launch_cgram_ft(int ft, dim3 grid, hipStream_t stream, const ChainArgs& a,
+                            std::integer_sequence<int, FTs...>) {
+  ((ft == FTs + 1 ? launch_cgram_one<FTs + 1, F32>(grid, stream, a) : void()), ...);
+}
+
+template <bool F32>
+static void launch_cproj_mtr(int mtr, dim3 grid, size_t lds, hipStream_t stream, const ChainArgs& a) {
+  switch (mtr) {
+    case 1: hipLaunchKernelGGL((chain_proj<1, F32>), grid, dim3(kChainThreads), lds, stream, a); break;
+    case 2: hipLaunchKernelGGL((chain_proj<2, F32>), grid, dim3(kChainThreads), lds, stream, a); break;
+    case 3:
+    case 4: hipLaunchKernelGGL((chain_proj<4, F32>), grid, dim3(kChainThreads), lds, stream, a); break;
+    default: hipLaunchKernelGGL((chain_proj<8, F32>), grid, dim3(kChainThreads), lds, stream, a); break;
+  }
+}
+
+hipError_t launch_chain(const ChainArgs& a, const EigArgs& ea, hipStream_t stream) {
+  const bool f32 = a.first.coef_dtype == KVC_F32;
+  const int ft = a.mp / 16;
+  const int T = a.out.num_tokens;
+  dim3 ggrid(a.max_parts, a.num_units);
+  if (f32) launch_cgram_ft<true>(ft, ggrid, stream, a, std::make_integer_sequence<int, 16>{});
+  else launch_cgram_ft<false>(ft, ggrid, stream, a, std::make_integer_sequence<int, 16>{});
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(chain_assemble, dim3(a.num_units), dim3(kChainThreads), 0, stream, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if ((e = launch_eig(ea, stream)) != hipSuccess) return e;
+  hipLaunchKernelGGL(chain_ymat, dim3(a.num_units), dim3(kChainThreads), 0, stream, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int mtr = (a.out.rank + 15) / 16;
+  const int mtr_inst = mtr <= 2 ? mtr : (mtr <= 4 ? 4 : 8);
+  const int m = a.first.rank + a.second.rank;
+  const size_t lds = (size_t)mtr_inst * 16 * ((m + 31) / 32 * 32) * 2 * sizeof(uint16_t);
+  dim3 pgrid((T + kCprojChunk - 1) / kCprojChunk, a.num_units);
+  if (f32) {
+    e = hipFuncSetAttribute((const void*)chain_proj<8, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    launch_cproj_mtr<true>(mtr, pgrid, lds, stream, a);
+  } else {
+    e = hipFuncSetAttribute((const void*)chain_proj<8, false>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds);
+    if (e != hipSuccess) return e;
+    launch_cproj_mtr<false>(mtr, pgrid, lds, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace kvc

@@ -65,4 +65,21 @@ struct EigArgs {
 size_t eig_lds_bytes(int n);
 hipError_t launch_eig(const EigArgs& a, hipStream_t stream);
 
+// Chain (kvc_chain.hip).  Unit u = (layer - layer_begin) * 2 H + kv * H + head.
+struct ChainArgs {
+  kvc_state first, second, out;
+  int32_t layer_begin;
+  int32_t num_layers;
+  int32_t num_units;
+  int32_t mp;                  // r1 + r2 rounded up to a multiple of 16
+  float* partials;             // workspace [unit][max_parts][mp][mp]
+  int32_t max_parts;
+  int32_t part_tokens;
+  double* hsum;                // [unit][m][m]
+  double* pmat;                // [unit][m][d]
+  double* gram;                // [unit][d][d]
+  float* ymat;                 // [unit][m][r_out]
+};
+hipError_t launch_chain(const ChainArgs& a, const EigArgs& ea, hipStream_t stream);
+
 }  // namespace kvc
