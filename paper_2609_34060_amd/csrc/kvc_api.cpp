@@ -87,7 +87,7 @@ size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 // Workspace layout and launch grouping of a fit call.  Units are processed in groups of at most 128 layers and as
 // many items as keep items x layers below 65536; the workspace holds one group.  A unit's Gram is split into
-// max_parts partials of part_tokens rows so that one call launches about 4096 Gram workgroups.
+// max_parts partials of part_tokens rows (one Gram wave each).
 struct FitPlan {
   int32_t layers_per_group = 1, items_per_group = 1, part_tokens = 256, max_parts = 1;
   size_t units = 0, off_partials = 0, off_reflect = 0, off_beta = 0, off_vecs = 0, total = 0;
@@ -104,11 +104,13 @@ FitPlan plan_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int32_t le)
     if (b->items[i].state.rank > 0) tmax = std::max(tmax, b->items[i].state.num_tokens);
   const int64_t d = c->head_dim;
   p.units = static_cast<size_t>(p.items_per_group) * p.layers_per_group * 2 * c->num_kv_heads;
-  const int64_t want_parts = std::max<int64_t>(1, (4096 + static_cast<int64_t>(p.units) - 1) / p.units);
+  // one partial per Gram wave; about 2048 waves per call (two per SIMD of the chip), a multiple of 4 per unit
+  const int64_t want_parts = std::max<int64_t>(1, (2048 + static_cast<int64_t>(p.units) - 1) / p.units);
   int64_t part = (std::max<int32_t>(tmax, 1) + want_parts - 1) / want_parts;
   part = std::max<int64_t>(256, (part + 31) / 32 * 32);
   p.part_tokens = static_cast<int32_t>(part);
   p.max_parts = static_cast<int32_t>(std::max<int64_t>(1, (tmax + part - 1) / part));
+  p.max_parts = (p.max_parts + 3) / 4 * 4;
   size_t off = 0;
   p.off_partials = off;
   off = align256(off + p.units * p.max_parts * d * d * sizeof(float));
@@ -195,6 +197,9 @@ void fill_pool_view(const kvc_cache* c, kvc::PoolView& pv) {
   pv.num_blocks = c->num_blocks;
   pv.num_kv_heads = c->num_kv_heads;
   pv.head_dim = c->head_dim;
+  pv.block_shift = -1;
+  for (int32_t sh = 0; sh < 31; ++sh)
+    if ((int32_t{1} << sh) == c->block_size) pv.block_shift = sh;
 }
 
 }  // namespace

@@ -18,6 +18,7 @@ constexpr int kWave = 64;
 struct PoolView {
   int64_t block_stride, token_stride, head_stride;  // elements
   int32_t block_size, num_blocks, num_kv_heads, head_dim;
+  int32_t block_shift;                               // log2(block_size) when it is a power of two, else -1
 };
 
 // Layer pointer tables travel in the kernel arguments (up to this many layers per launch).
@@ -32,21 +33,26 @@ struct LayerPtrs {
 __device__ __forceinline__ float bf16_lo_to_f32(uint32_t packed) { return __uint_as_float(packed << 16); }
 __device__ __forceinline__ float bf16_hi_to_f32(uint32_t packed) { return __uint_as_float(packed & 0xffff0000u); }
 
-// Round-to-nearest-even float -> bf16 bits; NaN stays a quiet NaN with its sign.
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float x) {
-  uint32_t u = __float_as_uint(x);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> packed bf16 pair, round to nearest even (one v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float x) { return pack_bf16x2(x, 0.0f) & 0xffffu; }
+
 // x = hi + lo + O(2^-17 |x|) with hi = bf16(x) and lo = bf16(x - hi): the two-term split that lets bf16 MFMA carry
-// about 16 significant bits of an fp32 operand.
+// about 16 significant bits of an fp32 operand.  Pairs of values, packed.
+__device__ __forceinline__ void split_bf16x2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  hi = pack_bf16x2(x0, x1);
+  lo = pack_bf16x2(x0 - __uint_as_float(hi << 16), x1 - __uint_as_float(hi & 0xffff0000u));
+}
 __device__ __forceinline__ void split_bf16(float x, uint32_t& hi_bits, uint32_t& lo_bits) {
-  hi_bits = f32_to_bf16_bits(x);
-  float hi = __uint_as_float(hi_bits << 16);
-  lo_bits = f32_to_bf16_bits(x - hi);
+  uint32_t h, l;
+  split_bf16x2(x, 0.0f, h, l);
+  hi_bits = h & 0xffffu;
+  lo_bits = l & 0xffffu;
 }
 
 // ---- paged row addressing --------------------------------------------------------------------------------------
@@ -55,7 +61,7 @@ __device__ __forceinline__ void split_bf16(float x, uint32_t& hi_bits, uint32_t&
 __device__ __forceinline__ int64_t row_offset(const PoolView& pv, const int32_t* __restrict__ table, int32_t off,
                                               int32_t t, int32_t head) {
   const int32_t p = off + t;
-  const int32_t lb = p / pv.block_size;
+  const int32_t lb = pv.block_shift >= 0 ? p >> pv.block_shift : p / pv.block_size;
   const int32_t slot = p - lb * pv.block_size;
   const int32_t blk = table ? table[lb] : lb;
   if (blk < 0 || blk >= pv.num_blocks) return -1;

@@ -18,6 +18,7 @@ namespace kvc {
 
 constexpr int kEigThreads = 1024;
 constexpr int kEigWaves = kEigThreads / kWave;
+constexpr int kReflChunk = 16;  // reflectors staged in LDS per back-transformation chunk
 
 __device__ __forceinline__ double wave_sum(double x) {
 #pragma unroll
@@ -65,8 +66,14 @@ __device__ __forceinline__ uint32_t hash3(uint32_t a, uint32_t b, uint32_t c) {
   return h;
 }
 
+// 1 / q from the hardware reciprocal and one Newton step (relative error about 2^-52).
+__device__ __forceinline__ double recip(double q) {
+  const double r0 = __builtin_amdgcn_rcp(q);
+  return fma(r0, fma(-q, r0, 1.0), r0);
+}
+
 // Number of eigenvalues of T below x (ratio form of the Sturm sequence; pivots smaller than pivmin are replaced
-// by -pivmin).
+// by -pivmin, so that b^2 / q stays finite).
 template <int N>
 __device__ __forceinline__ int sturm_count(const double* sa, const double* sb2, double x, double pivmin) {
   double q = sa[0] - x;
@@ -74,7 +81,7 @@ __device__ __forceinline__ int sturm_count(const double* sa, const double* sb2, 
   int c = q < 0.0;
 #pragma unroll 4
   for (int i = 1; i < N; ++i) {
-    q = (sa[i] - x) - sb2[i - 1] / q;
+    q = (sa[i] - x) - sb2[i - 1] * recip(q);
     if (fabs(q) < pivmin) q = -pivmin;
     c += q < 0.0;
   }
@@ -95,6 +102,8 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
   double* s_v = s_lam + KVC_MAX_RANK;   // current reflector
   double* s_p = s_v + N;                // p / w
   double* s_misc = s_p + N;             // scalars
+  double* s_rb = s_misc + 8;            // a chunk of reflectors for the back-transformation [kReflChunk][N]
+  double* s_rbeta = s_rb + kReflChunk * N;
 
   const int u = blockIdx.x;
   const UnitTarget tg = eig_target(a, u);
@@ -178,11 +187,13 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
     }
     __syncthreads();
     // A22 -= v w^T + w v^T, with the same rounding for (i, j) and (j, i) to keep A exactly symmetric
-    for (int e = tid; e < m * m; e += kEigThreads) {
-      const int i = e / m, j = e - i * m;
-      const double t = __dadd_rn(__dmul_rn(s_v[i], s_p[j]), __dmul_rn(s_p[i], s_v[j]));
-      double* p = &A[(k + 1 + i) * LD + k + 1 + j];
-      *p = __dsub_rn(*p, t);
+    for (int i = tid >> 5; i < m; i += kEigThreads >> 5) {
+      const double vi = s_v[i], wi = s_p[i];
+      double* row = &A[(k + 1 + i) * LD + k + 1];
+      for (int j = tid & 31; j < m; j += 32) {
+        const double t = __dadd_rn(__dmul_rn(vi, s_p[j]), __dmul_rn(wi, s_v[j]));
+        row[j] = __dsub_rn(row[j], t);
+      }
     }
     __syncthreads();
   }
@@ -219,7 +230,8 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
     {
       int rp = 1;
       while (rp < r) rp <<= 1;
-      const int P = min(kWave, kEigThreads / rp);   // lanes per eigenvalue (a power of two dividing 64)
+      // lanes per eigenvalue (a power of two dividing 64); 16 trades latency (iterations) against the fp64 work
+      const int P = min(16, kEigThreads / rp);
       int bits = 0;
       while ((2 << bits) <= P + 1) ++bits;          // floor(log2(P + 1))
       const int iters = 66 / bits + 1;
@@ -321,21 +333,33 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
     }
 
     // ---- 5. back-transformation X <- H_0 H_1 ... H_{N-3} X ---------------------------------------------
-    for (int k = N - 3; k >= 0; --k) {
-      const int m = N - k - 1;
-      for (int i = tid; i < m; i += kEigThreads) s_v[i] = refl[k * N + i];
+    // Reflectors are staged kReflChunk at a time; each wave owns whole columns of X, so the steps inside a chunk
+    // need no barrier.
+    for (int kc = N - 3; kc >= 0; kc -= kReflChunk) {
+      const int nk = min(kReflChunk, kc + 1);
       __syncthreads();
-      const double beta = refl_beta[k];
-      if (beta != 0.0) {
+      for (int e = tid; e < nk * N; e += kEigThreads) {
+        const int c = e / N, i = e - c * N;
+        const int k = kc - c;
+        s_rb[c * N + i] = i < N - k - 1 ? refl[k * N + i] : 0.0;
+      }
+      for (int c = tid; c < nk; c += kEigThreads) s_rbeta[c] = refl_beta[kc - c];
+      __syncthreads();
+      for (int c = 0; c < nk; ++c) {
+        const int k = kc - c;
+        const int m = N - k - 1;
+        const double beta = s_rbeta[c];
+        if (beta == 0.0) continue;
+        const double* v = &s_rb[c * N];
         for (int j = wave; j < r; j += kEigWaves) {
           double s = 0.0;
-          for (int i = lane; i < m; i += kWave) s += s_v[i] * A[j * N + k + 1 + i];
+          for (int i = lane; i < m; i += kWave) s += v[i] * A[j * N + k + 1 + i];
           s = wave_sum(s) * beta;
-          for (int i = lane; i < m; i += kWave) A[j * N + k + 1 + i] -= s * s_v[i];
+          for (int i = lane; i < m; i += kWave) A[j * N + k + 1 + i] -= s * v[i];
         }
       }
-      __syncthreads();
     }
+    __syncthreads();
   }
 
   // ---- canonical sign and output ----------------------------------------------------------------------------
@@ -361,7 +385,7 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
 
 size_t eig_lds_bytes(int n) {
   const size_t areg = std::max((size_t)n * (n + 1), (size_t)2 * n * kWave);
-  return (areg + 5 * (size_t)n + KVC_MAX_RANK + 8) * sizeof(double);
+  return (areg + 5 * (size_t)n + KVC_MAX_RANK + 8 + (size_t)kReflChunk * (n + 1)) * sizeof(double);
 }
 
 hipError_t launch_eig(const EigArgs& a, hipStream_t stream) {

@@ -1,13 +1,13 @@
 // kvc_fit_state kernels: the observed transition Z = C_dst - C_src of Eq. 12 (or Z = C_dst for a base cache) and
 // its rank-r truncated SVD (Eq. 7) through the Gram matrix G = Z^T Z:
-//   gram   one workgroup per (unit, token chunk) writes the chunk's partial Gram (fp32, d x d); the eigensolver
-//          sums the partials of a unit in a fixed order in fp64, so the result does not depend on scheduling.
+//   gram   one wave per (unit, token range) writes that range's partial Gram (fp32, d x d); the eigensolver sums
+//          the partials of a unit in a fixed order in fp64, so the result does not depend on scheduling.
 //   proj   coef = Z R_r (= U_r Sigma_r), re-reading Z from the cache after the basis is known.
 //
 // bf16 caches: Z is formed in fp32 (the difference of two bf16 values is exact in fp32) and split into a bf16
 // hi/lo pair; every product is hi*hi + hi*lo + lo*hi on v_mfma_f32_16x16x32_bf16 with fp32 accumulation, about
-// 16 significant bits per operand.  In the Gram kernel Z goes through LDS transposed ([feature][token]) so that the
-// MFMA A and B fragments of a 16-feature tile are the same 16-byte LDS reads; only tiles on or above the diagonal
+// 16 significant bits per operand.  The Gram keeps the token index in the MFMA K slot by a permuted feature order
+// (see GramSeg) so that its operands come straight from coalesced row loads; only tiles on or above the diagonal
 // are computed and each is stored with its mirror.  In the projection the rows are read straight into the MFMA
 // B-operand layout (16 contiguous bytes per lane), the basis hi/lo is staged in LDS.
 // float32 caches use plain fp32 VALU kernels.
@@ -67,145 +67,190 @@ constexpr int tile_fj(int idx, int FT) {
 
 template <int D>
 struct GramShape {
-  static constexpr int FT = D / 16;                 // feature tiles
+  static constexpr int FT = D / 16;                 // 16 x 16 output tiles per side
   static constexpr int NTILES = FT * (FT + 1) / 2;  // tiles on or above the diagonal
-  static constexpr int TPWV = (NTILES + kFitWaves - 1) / kFitWaves;
-  static constexpr int STEP = 32;                   // tokens per MFMA K-step
-  static constexpr int LDT = STEP + 8;              // padded token stride of the transposed tile
-  static constexpr int SEGS = STEP * D / 8;         // 16-byte row segments per step
-  static constexpr int SPT = SEGS / kFitThreads;    // per thread
 };
 
-// Tile Q of wave W (tile index W + 4 Q): G[16 fi .., 16 fj ..] += Z_fi^T Z_fj with the hi/lo products.
+// The Gram is computed in a permuted feature order: output tile (fi, fj) holds G[FT m + fi][FT n + fj] for
+// m, n in [0, 16).  Lane (g, m) of a wave then needs, for its 8 tokens 8 g + j, the FT contiguous features
+// FT m .. FT m + FT - 1 of each row (one 2 FT-byte read per token), and the MFMA fragment of tile row fi is
+// element fi of those 8 segments, gathered with byte permutes.
+template <int FT>
+struct GramSeg;
+template <>
+struct GramSeg<8> {
+  using T = u32x4;
+};
+template <>
+struct GramSeg<4> {
+  using T = uint2;
+};
+
+template <int FT>
+__device__ __forceinline__ uint32_t seg_dword(const typename GramSeg<FT>::T& s, int w) {
+  if constexpr (FT == 8) return s[w];
+  else return w == 0 ? s.x : s.y;
+}
+
+// Fragment of tile row fi: bf16 element fi of each of the 8 token segments (tokens 8 g + 0 .. 7).
+template <int FT, int FI>
+__device__ __forceinline__ bf16x8 gram_fragment(const typename GramSeg<FT>::T* seg) {
+  constexpr uint32_t sel = (FI & 1) ? 0x07060302u : 0x05040100u;
+  u32x4 f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w)
+    f[w] = __builtin_amdgcn_perm(seg_dword<FT>(seg[2 * w + 1], FI >> 1), seg_dword<FT>(seg[2 * w], FI >> 1), sel);
+  return as_bf16x8(f);
+}
+
+// Tile Q of wave W (tile index W + 4 Q): acc += Z_fi^T Z_fj with the hi/lo products.
 template <int D, int W, int Q>
-__device__ __forceinline__ void gram_tile(f32x4* acc, const bf16x8* fh, const bf16x8* fl) {
+__device__ __forceinline__ void gram_tile(f32x4* acc, const typename GramSeg<D / 16>::T* sh,
+                                          const typename GramSeg<D / 16>::T* sl) {
+  constexpr int FT = D / 16;
   constexpr int idx = W + Q * kFitWaves;
   if constexpr (idx < GramShape<D>::NTILES) {
-    constexpr int fi = tile_fi(idx, GramShape<D>::FT), fj = tile_fj(idx, GramShape<D>::FT);
-    acc[Q] = mfma16x16x32(fl[fi], fh[fj], acc[Q]);
-    acc[Q] = mfma16x16x32(fh[fi], fl[fj], acc[Q]);
-    acc[Q] = mfma16x16x32(fh[fi], fh[fj], acc[Q]);
+    constexpr int fi = tile_fi(idx, FT), fj = tile_fj(idx, FT);
+    const bf16x8 ah = gram_fragment<FT, fi>(sh), al = gram_fragment<FT, fi>(sl);
+    const bf16x8 bh = gram_fragment<FT, fj>(sh), bl = gram_fragment<FT, fj>(sl);
+    acc[Q] = mfma16x16x32(al, bh, acc[Q]);
+    acc[Q] = mfma16x16x32(ah, bl, acc[Q]);
+    acc[Q] = mfma16x16x32(ah, bh, acc[Q]);
   }
 }
 template <int D, int W, int Q>
 __device__ __forceinline__ void gram_store(float* P, const f32x4* acc, int g, int n) {
+  constexpr int FT = D / 16;
   constexpr int idx = W + Q * kFitWaves;
   if constexpr (idx < GramShape<D>::NTILES) {
-    constexpr int fi = tile_fi(idx, GramShape<D>::FT), fj = tile_fj(idx, GramShape<D>::FT);
+    constexpr int fi = tile_fi(idx, FT), fj = tile_fj(idx, FT);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = 16 * fi + 4 * g + i, col = 16 * fj + n;
+      const int row = FT * (4 * g + i) + fi, col = FT * n + fj;
       P[row * D + col] = acc[Q][i];
       P[col * D + row] = acc[Q][i];
     }
   }
 }
-template <int D, int W, int... Qs>
-__device__ __forceinline__ void gram_tiles(f32x4* acc, const bf16x8* fh, const bf16x8* fl,
-                                           std::integer_sequence<int, Qs...>) {
-  (gram_tile<D, W, Qs>(acc, fh, fl), ...);
+// All tiles of the upper triangle for one wave: acc[idx] += Z_fi^T Z_fj (hi/lo products).
+template <int D, int... Is>
+__device__ __forceinline__ void gram_all_tiles(f32x4* acc, const typename GramSeg<D / 16>::T* sh,
+                                               const typename GramSeg<D / 16>::T* sl, std::integer_sequence<int, Is...>) {
+  (gram_tile<D, Is, 0>(acc + Is, sh, sl), ...);
 }
-template <int D, int W, int... Qs>
-__device__ __forceinline__ void gram_stores(float* P, const f32x4* acc, int g, int n,
-                                            std::integer_sequence<int, Qs...>) {
-  (gram_store<D, W, Qs>(P, acc, g, n), ...);
+template <int D, int... Is>
+__device__ __forceinline__ void gram_all_stores(float* P, const f32x4* acc, int g, int n,
+                                                std::integer_sequence<int, Is...>) {
+  (gram_store<D, Is, 0>(P, acc + Is, g, n), ...);
 }
 
-// Body of the bf16 Gram kernel for wave W (its tile list is known at compile time).
-template <int D, int W>
-__device__ __forceinline__ void gram_bf16_body(const FitArgs& a, const FitUnit& f, const kvc_item* itp,
-                                               int t_begin, int t_end, uint16_t* s_hi, uint16_t* s_lo) {
-  using S = GramShape<D>;
-  constexpr int LDT = S::LDT, SPT = S::SPT, FT = S::FT, TPWV = S::TPWV;
-  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
-  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)f.item * a.max_blocks : nullptr;
-  const uint16_t* pool = static_cast<const uint16_t*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
-  const bool delta = a.mode == KVC_FIT_DELTA;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int g = lane >> 4, n = lane & 15;
-
-  f32x4 acc[TPWV];
+// Row offsets of the 8 consecutive tokens t .. t + 7 of a block sequence (entries past t_end are -1); with a
+// power-of-two block size of at least 8 the 8 tokens touch at most two blocks, so two table reads suffice.
+__device__ __forceinline__ void row_offsets8(const PoolView& pv, const int32_t* __restrict__ table, int32_t off,
+                                             int t, int t_end, int head, int64_t* o) {
+  if (pv.block_shift >= 3) {
+    const int32_t p = off + t;
+    const int32_t lb0 = p >> pv.block_shift, lb1 = (p + 7) >> pv.block_shift;
+    // a table entry is read only if a token before t_end lies in its block (the host checked those are in range)
+    const int32_t b0 = t < t_end ? (table ? table[lb0] : lb0) : -1;
+    const int first_in_lb1 = (lb1 << pv.block_shift) - off;
+    const int32_t b1 = lb1 == lb0 ? b0 : (first_in_lb1 < t_end ? (table ? table[lb1] : lb1) : -1);
 #pragma unroll
-  for (int q = 0; q < TPWV; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  u32x4 rd[SPT], rs[SPT];
-  auto load_step = [&](int t0) {
-#pragma unroll
-    for (int q = 0; q < SPT; ++q) {
-      const int seg = tid + q * kFitThreads;
-      const int tk = seg / (D / 8), part = seg - tk * (D / 8);
-      const int t = t0 + tk;
-      rd[q] = u32x4{0, 0, 0, 0};
-      rs[q] = u32x4{0, 0, 0, 0};
-      if (t < t_end) {
-        const int64_t od = row_offset(a.pv, dst_tab, itp->dst_offset, t, f.head);
-        if (od >= 0) rd[q] = *reinterpret_cast<const u32x4*>(pool + od + 8 * part);
-        if (delta) {
-          const int64_t os = row_offset(a.pv, src_tab, itp->src_offset, t, f.head);
-          if (os >= 0) rs[q] = *reinterpret_cast<const u32x4*>(pool + os + 8 * part);
-        }
-      }
+    for (int j = 0; j < 8; ++j) {
+      const int32_t pj = p + j;
+      const int32_t lb = pj >> pv.block_shift;
+      const int32_t blk = lb == lb0 ? b0 : b1;
+      const bool ok = (t + j < t_end) && blk >= 0 && blk < pv.num_blocks;
+      o[j] = ok ? (int64_t)blk * pv.block_stride + (int64_t)(pj - (lb << pv.block_shift)) * pv.token_stride +
+                      (int64_t)head * pv.head_stride
+                : -1;
     }
-  };
-  auto stage_step = [&]() {
+  } else {
 #pragma unroll
-    for (int q = 0; q < SPT; ++q) {
-      const int seg = tid + q * kFitThreads;
-      const int tk = seg / (D / 8), part = seg - tk * (D / 8);
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float z0 = bf16_lo_to_f32(rd[q][w]) - bf16_lo_to_f32(rs[q][w]);
-        const float z1 = bf16_hi_to_f32(rd[q][w]) - bf16_hi_to_f32(rs[q][w]);
-        uint32_t h0, l0, h1, l1;
-        split_bf16(z0, h0, l0);
-        split_bf16(z1, h1, l1);
-        const int fe = 8 * part + 2 * w;
-        s_hi[fe * LDT + tk] = (uint16_t)h0;
-        s_lo[fe * LDT + tk] = (uint16_t)l0;
-        s_hi[(fe + 1) * LDT + tk] = (uint16_t)h1;
-        s_lo[(fe + 1) * LDT + tk] = (uint16_t)l1;
-      }
-    }
-  };
-
-  load_step(t_begin);
-  for (int t0 = t_begin; t0 < t_end; t0 += S::STEP) {
-    stage_step();
-    __syncthreads();
-    if (t0 + S::STEP < t_end) load_step(t0 + S::STEP);
-    bf16x8 fh[FT], fl[FT];
-#pragma unroll
-    for (int ft = 0; ft < FT; ++ft) {
-      fh[ft] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[(16 * ft + n) * LDT + 8 * g]));
-      fl[ft] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[(16 * ft + n) * LDT + 8 * g]));
-    }
-    gram_tiles<D, W>(acc, fh, fl, std::make_integer_sequence<int, TPWV>{});
-    __syncthreads();
+    for (int j = 0; j < 8; ++j) o[j] = (t + j < t_end) ? row_offset(pv, table, off, t + j, head) : -1;
   }
-  const int64_t lu = fit_linear_unit(a, f);
-  float* P = a.partials + ((size_t)lu * a.max_parts + blockIdx.x) * D * D;
-  gram_stores<D, W>(P, acc, g, n, std::make_integer_sequence<int, TPWV>{});
 }
 
+// bf16 Gram, one wave per partial: the wave streams its own token range 32 tokens at a time.  Lane (g, m) loads,
+// for tokens t0 + 8 g + j (j = 0..7), the 2 FT bytes of features FT m .. FT m + FT - 1 of the dst (and src) row:
+// sixteen lanes cover one row with one coalesced load.  Z = dst - src is split into bf16 hi/lo in registers and
+// the MFMA fragments of every tile row are gathered from those segments with byte permutes, so the Gram needs no
+// LDS and no barrier; all upper tiles accumulate in the wave's registers.  The next step's rows are loaded while
+// the current step is multiplied.
 template <int D>
 __global__ __launch_bounds__(kFitThreads) void gram_bf16_mfma(FitArgs a) {
-  using S = GramShape<D>;
-  static_assert(S::SEGS % kFitThreads == 0, "segments per thread");
-  __shared__ __attribute__((aligned(16))) uint16_t s_hi[D * S::LDT];
-  __shared__ __attribute__((aligned(16))) uint16_t s_lo[D * S::LDT];
+  constexpr int FT = D / 16;
+  constexpr int NT = FT * (FT + 1) / 2;
+  constexpr int STEP = 32;
+  using Seg = typename GramSeg<FT>::T;
   const FitUnit f = fit_unit(a);
   const kvc_item* itp = a.items + f.item;
   const int r = itp->state.rank;
   const int Ts = itp->state.num_tokens;
-  const int t_begin = blockIdx.x * a.part_tokens;
-  if (r == 0 || t_begin >= Ts) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int part = blockIdx.x * kFitWaves + wave;
+  const int t_begin = part * a.part_tokens;
+  if (r == 0 || t_begin >= Ts) return;  // per wave: the kernel has no barrier
   const int t_end = min(Ts, t_begin + a.part_tokens);
-  switch (threadIdx.x >> 6) {
-    case 0: gram_bf16_body<D, 0>(a, f, itp, t_begin, t_end, s_hi, s_lo); break;
-    case 1: gram_bf16_body<D, 1>(a, f, itp, t_begin, t_end, s_hi, s_lo); break;
-    case 2: gram_bf16_body<D, 2>(a, f, itp, t_begin, t_end, s_hi, s_lo); break;
-    default: gram_bf16_body<D, 3>(a, f, itp, t_begin, t_end, s_hi, s_lo); break;
+  const int g = lane >> 4, n = lane & 15;
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const uint16_t* pool = static_cast<const uint16_t*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
+  const bool delta = a.mode == KVC_FIT_DELTA;
+
+  f32x4 acc[NT];
+#pragma unroll
+  for (int q = 0; q < NT; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto load = [&](int t0, Seg* rd, Seg* rs) {
+    int64_t od[8], os[8];
+    const int t = t0 + 8 * g;
+    row_offsets8(a.pv, dst_tab, itp->dst_offset, t, t_end, f.head, od);
+    if (delta) row_offsets8(a.pv, src_tab, itp->src_offset, t, t_end, f.head, os);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      rd[j] = od[j] >= 0 ? *reinterpret_cast<const Seg*>(pool + od[j] + FT * n) : Seg{};
+      rs[j] = (delta && os[j] >= 0) ? *reinterpret_cast<const Seg*>(pool + os[j] + FT * n) : Seg{};
+    }
+  };
+  // Z of the loaded step into bf16 hi/lo segments
+  auto form_z = [&](const Seg* rd, const Seg* rs, Seg* zh, Seg* zl) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+#pragma unroll
+      for (int w = 0; w < FT / 2; ++w) {
+        const uint32_t dw = seg_dword<FT>(rd[j], w), sw = seg_dword<FT>(rs[j], w);
+        uint32_t h, l;
+        split_bf16x2(bf16_lo_to_f32(dw) - bf16_lo_to_f32(sw), bf16_hi_to_f32(dw) - bf16_hi_to_f32(sw), h, l);
+        if constexpr (FT == 8) {
+          zh[j][w] = h;
+          zl[j][w] = l;
+        } else {
+          if (w == 0) {
+            zh[j].x = h;
+            zl[j].x = l;
+          } else {
+            zh[j].y = h;
+            zl[j].y = l;
+          }
+        }
+      }
+    }
+  };
+
+  // one register stage: the next step's rows are loaded into the same registers once Z of this step is formed,
+  // so they are in flight while this step's 3 x NT MFMAs run
+  Seg rd[8], rs[8];
+  load(t_begin, rd, rs);
+  for (int t0 = t_begin; t0 < t_end; t0 += STEP) {
+    Seg zh[8], zl[8];
+    form_z(rd, rs, zh, zl);
+    if (t0 + STEP < t_end) load(t0 + STEP, rd, rs);
+    gram_all_tiles<D>(acc, zh, zl, std::make_integer_sequence<int, NT>{});
   }
+  const int64_t lu = fit_linear_unit(a, f);
+  float* P = a.partials + ((size_t)lu * a.max_parts + part) * D * D;
+  gram_all_stores<D>(P, acc, g, n, std::make_integer_sequence<int, NT>{});
 }
 
 // ---------------------------------------------------------------------------------------------------------------
@@ -442,12 +487,13 @@ __global__ __launch_bounds__(kFitThreads) void proj_f32_valu(FitArgs a) {
 int proj_chunk_tokens() { return kProjChunk; }
 
 hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream) {
-  dim3 grid(a.max_parts, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
   const int D = a.pv.head_dim;
   if (dtype == KVC_BF16) {
+    dim3 grid((a.max_parts + kFitWaves - 1) / kFitWaves, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
     if (D == 64) hipLaunchKernelGGL(gram_bf16_mfma<64>, grid, dim3(kFitThreads), 0, stream, a);
     else hipLaunchKernelGGL(gram_bf16_mfma<128>, grid, dim3(kFitThreads), 0, stream, a);
   } else {
+    dim3 grid(a.max_parts, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
     if (D == 64) hipLaunchKernelGGL(gram_f32_valu<64>, grid, dim3(kFitThreads), 0, stream, a);
     else hipLaunchKernelGGL(gram_f32_valu<128>, grid, dim3(kFitThreads), 0, stream, a);
   }
