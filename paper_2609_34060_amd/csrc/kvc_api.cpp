@@ -149,7 +149,7 @@ kvc_status check_chain(const kvc_state* a, const kvc_state* b, const kvc_state* 
 // Chain workspace: H partials (chunks sized as in the fit), the fp64 intermediates of G = K H K^T, the eigensolver
 // scratch and Y.
 struct ChainPlan {
-  int32_t mp = 16, part_tokens = 256, max_parts = 1;
+  int32_t mp = 16, part_tokens = 256, max_parts = 1, gram_wave_ft = 0;
   size_t units = 0, off_partials = 0, off_hsum = 0, off_pmat = 0, off_gram = 0, off_reflect = 0, off_beta = 0,
          off_vecs = 0, off_ymat = 0, total = 0;
 };
@@ -159,14 +159,28 @@ ChainPlan plan_chain(const kvc_state* a, const kvc_state* b, const kvc_state* o,
   const size_t d = a->head_dim;
   const size_t m = static_cast<size_t>(a->rank) + b->rank;
   p.mp = static_cast<int32_t>(std::max<size_t>(16, (m + 15) / 16 * 16));
+  // bf16 coefficients whose ranks split into whole FT-wide segments use the LDS-free wave Gram
+  if (a->coef_dtype == KVC_BF16) {
+    for (int32_t ft : {2, 4, 8}) {
+      if (m <= static_cast<size_t>(16 * ft) && a->rank % ft == 0 && b->rank % ft == 0) {
+        p.gram_wave_ft = ft;
+        p.mp = 16 * ft;
+        break;
+      }
+    }
+  }
   p.units = static_cast<size_t>(le - lb) * 2 * a->num_kv_heads;
   const int64_t T = std::max<int32_t>(o->num_tokens, 1);
-  const int64_t want_parts = std::max<int64_t>(1, (4096 + static_cast<int64_t>(p.units) - 1) /
+  // the wave Gram has one partial per wave (about 2048 per call, a multiple of 4 per unit); the LDS Gram one per
+  // workgroup (about 4096 per call)
+  const int64_t target = p.gram_wave_ft ? 2048 : 4096;
+  const int64_t want_parts = std::max<int64_t>(1, (target + static_cast<int64_t>(p.units) - 1) /
                                                       std::max<int64_t>(1, static_cast<int64_t>(p.units)));
   int64_t part = (T + want_parts - 1) / want_parts;
   part = std::max<int64_t>(256, (part + 31) / 32 * 32);
   p.part_tokens = static_cast<int32_t>(part);
   p.max_parts = static_cast<int32_t>((T + part - 1) / part);
+  if (p.gram_wave_ft) p.max_parts = (p.max_parts + 3) / 4 * 4;
   const size_t U = p.units, mp = p.mp;
   size_t off = 0;
   p.off_partials = off;
@@ -380,6 +394,7 @@ kvc_status kvc_chain(const kvc_state* first, const kvc_state* second, kvc_state*
   ca.num_layers = layer_end - layer_begin;
   ca.num_units = static_cast<int32_t>(p.units);
   ca.mp = p.mp;
+  ca.gram_wave_ft = p.gram_wave_ft;
   ca.partials = reinterpret_cast<float*>(ws + p.off_partials);
   ca.max_parts = p.max_parts;
   ca.part_tokens = p.part_tokens;

@@ -144,9 +144,190 @@ __global__ __launch_bounds__(kChainThreads) void chain_gram(ChainArgs a) {
   }
 }
 
+// cgram without LDS for bf16 coefficients with r1, r2 multiples of FT and m <= 16 FT: one wave per token range,
+// the same permuted feature order as the fit's Gram (lane (g, m) holds features FT m .. FT m + FT - 1 of tokens
+// 8 g + j), one exact bf16 product per tile.
+template <int FT, int Q>
+__device__ __forceinline__ void cgram_tile(f32x4* acc, const typename GramSeg<FT>::T* seg) {
+  constexpr int fi = tile_fi(Q, FT), fj = tile_fj(Q, FT);
+  acc[Q] = mfma16x16x32(gram_fragment<FT, fi>(seg), gram_fragment<FT, fj>(seg), acc[Q]);
+}
+template <int FT, int... Qs>
+__device__ __forceinline__ void cgram_tiles(f32x4* acc, const typename GramSeg<FT>::T* seg,
+                                            std::integer_sequence<int, Qs...>) {
+  (cgram_tile<FT, Qs>(acc, seg), ...);
+}
+
+template <int FT>
+__global__ __launch_bounds__(kChainThreads) void chain_gram_wave(ChainArgs a) {
+  constexpr int NT = FT * (FT + 1) / 2;
+  constexpr int MP = 16 * FT;
+  constexpr int STEP = 32;
+  using Seg = typename GramSeg<FT>::T;
+  const int u = blockIdx.y;
+  const ChainUnit cu = chain_unit(a, u);
+  const int T = a.out.num_tokens;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int part = blockIdx.x * kChainWaves + wave;
+  const int t_begin = part * a.part_tokens;
+  if (t_begin >= T) return;  // per wave: no barrier in this kernel
+  const int t_end = min(T, t_begin + a.part_tokens);
+  const int r1 = a.first.rank, r2 = a.second.rank, T1 = a.first.num_tokens, T2 = a.second.num_tokens;
+  const uint16_t* A1 = static_cast<const uint16_t*>(a.first.coef) + cu.idx * (int64_t)T1 * r1;
+  const uint16_t* A2 = static_cast<const uint16_t*>(a.second.coef) + cu.idx * (int64_t)T2 * r2;
+  const int g = lane >> 4, n = lane & 15;
+  const int l0 = FT * n;  // first concatenated rank of this lane's segment
+
+  f32x4 acc[NT];
+#pragma unroll
+  for (int q = 0; q < NT; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  Seg seg[8];
+  auto load = [&](int t0) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int t = t0 + 8 * g + j;
+      Seg v{};
+      if (t < t_end) {
+        if (l0 < r1) {
+          if (t < T1) v = *reinterpret_cast<const Seg*>(A1 + (int64_t)t * r1 + l0);
+        } else if (l0 < r1 + r2) {
+          if (t < T2) v = *reinterpret_cast<const Seg*>(A2 + (int64_t)t * r2 + (l0 - r1));
+        }
+      }
+      seg[j] = v;
+    }
+  };
+  load(t_begin);
+  for (int t0 = t_begin; t0 < t_end; t0 += STEP) {
+    Seg cur[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) cur[j] = seg[j];
+    if (t0 + STEP < t_end) load(t0 + STEP);
+    cgram_tiles<FT>(acc, cur, std::make_integer_sequence<int, NT>{});
+  }
+  float* P = a.partials + ((size_t)u * a.max_parts + part) * MP * MP;
+#pragma unroll
+  for (int q = 0; q < NT; ++q) {
+    const int fi = tile_fi(q, FT), fj = tile_fj(q, FT);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = FT * (4 * g + i) + fi, col = FT * n + fj;
+      P[row * MP + col] = acc[q][i];
+      P[col * MP + row] = acc[q][i];
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------------------------------------------
 // assemble: H = sum of partials (fp64), P = H K^T (m x d), G = K P (d x d)
 // ---------------------------------------------------------------------------------------------------------------
+
+// LDS version for m <= 128: H (fp64 sum of the partials, kept as fp32) and K^T = [B1; B2] staged in LDS; P = H K^T
+// with fp64 accumulation in registers (8 x 4 tiles), written back over H; G = K P in 8 x 8 tiles on or above the
+// diagonal, each stored with its mirror.
+__global__ __launch_bounds__(kChainThreads) void chain_assemble_lds(ChainArgs a) {
+  extern __shared__ __attribute__((aligned(16))) float s_asm[];
+  const int u = blockIdx.x;
+  const ChainUnit cu = chain_unit(a, u);
+  const int m = a.first.rank + a.second.rank, MP = a.mp, d = a.first.head_dim;
+  const int M8 = (m + 7) / 8 * 8;
+  const int T = a.out.num_tokens;
+  const int parts = (T + a.part_tokens - 1) / a.part_tokens;
+  const float* PP = a.partials + (size_t)u * a.max_parts * MP * MP;
+  float* R = s_asm;            // H [M8][M8], later P [M8][d]
+  float* Bs = s_asm + M8 * d;  // K^T [M8][d]
+  const int tid = threadIdx.x;
+  for (int e = tid; e < M8 * M8; e += kChainThreads) {
+    const int i = e / M8, j = e - i * M8;
+    double s = 0.0;
+    if (i < m && j < m)
+      for (int c = 0; c < parts; ++c) s += (double)PP[(size_t)c * MP * MP + i * MP + j];
+    R[e] = (float)s;
+  }
+  for (int e = tid; e < M8 * d; e += kChainThreads) {
+    const int l = e / d, f = e - l * d;
+    Bs[e] = l < m ? cat_basis(a, cu.idx, l, f) : 0.f;
+  }
+  __syncthreads();
+  // P = H K^T: tile (8 rows l, 4 columns f); at most two tiles per thread (M8 <= 128)
+  const int ntp = (M8 / 8) * (d / 4);
+  double pacc[2][8][4];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int tile = tid + s * kChainThreads;
+    if (tile < ntp) {
+      const int l0 = 8 * (tile / (d / 4)), f0 = 4 * (tile % (d / 4));
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) pacc[s][i][c] = 0.0;
+      for (int k = 0; k < m; ++k) {
+        const float4 b = *reinterpret_cast<const float4*>(&Bs[k * d + f0]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const double h = R[(l0 + i) * M8 + k];
+          pacc[s][i][0] += h * b.x;
+          pacc[s][i][1] += h * b.y;
+          pacc[s][i][2] += h * b.z;
+          pacc[s][i][3] += h * b.w;
+        }
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int tile = tid + s * kChainThreads;
+    if (tile < ntp) {
+      const int l0 = 8 * (tile / (d / 4)), f0 = 4 * (tile % (d / 4));
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        *reinterpret_cast<float4*>(&R[(l0 + i) * d + f0]) =
+            make_float4((float)pacc[s][i][0], (float)pacc[s][i][1], (float)pacc[s][i][2], (float)pacc[s][i][3]);
+    }
+  }
+  __syncthreads();
+  // G = K P: tiles (8 rows i, 8 columns j) with i0 <= j0
+  double* G = a.gram + (size_t)u * d * d;
+  const int nb = d / 8;
+  for (int tile = tid; tile < nb * (nb + 1) / 2; tile += kChainThreads) {
+    int bi = 0, rem = tile;
+    while (rem >= nb - bi) {
+      rem -= nb - bi;
+      ++bi;
+    }
+    const int i0 = 8 * bi, j0 = 8 * (bi + rem);
+    double g[8][8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) g[i][j] = 0.0;
+    for (int l = 0; l < m; ++l) {
+      const float4 b0 = *reinterpret_cast<const float4*>(&Bs[l * d + i0]);
+      const float4 b1 = *reinterpret_cast<const float4*>(&Bs[l * d + i0 + 4]);
+      const float4 p0 = *reinterpret_cast<const float4*>(&R[l * d + j0]);
+      const float4 p1 = *reinterpret_cast<const float4*>(&R[l * d + j0 + 4]);
+      const double bi8[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+      const double pj8[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) g[i][j] += bi8[i] * pj8[j];
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        // the diagonal tiles are computed twice (i, j) and (j, i) with different rounding; keep the upper value
+        // and mirror it so that G is exactly symmetric
+        if (i0 == j0 && j < i) continue;
+        G[(i0 + i) * d + j0 + j] = g[i][j];
+        G[(j0 + j) * d + i0 + i] = g[i][j];
+      }
+  }
+}
+
+size_t chain_assemble_lds_bytes(int m, int d) { return (size_t)2 * ((m + 7) / 8 * 8) * d * sizeof(float); }
 
 __global__ __launch_bounds__(kChainThreads) void chain_assemble(ChainArgs a) {
   const int u = blockIdx.x;
@@ -208,7 +389,8 @@ __global__ __launch_bounds__(kChainThreads) void chain_ymat(ChainArgs a) {
 constexpr int kCprojTilesPerWave = 8;
 constexpr int kCprojChunk = kChainWaves * kCprojTilesPerWave * 16;
 
-template <int MTR, bool F32>
+// VEC (bf16, r1 and r2 multiples of 8, r_out a multiple of 4): 16-byte coefficient loads and 8-byte stores.
+template <int MTR, bool F32, bool VEC>
 __global__ __launch_bounds__(kChainThreads) void chain_proj(ChainArgs a) {
   extern __shared__ __attribute__((aligned(16))) uint16_t s_y[];  // hi [MTR*16][KP], lo [MTR*16][KP]
   const int u = blockIdx.y;
@@ -247,6 +429,26 @@ __global__ __launch_bounds__(kChainThreads) void chain_proj(ChainArgs a) {
     for (int mt = 0; mt < MTR; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int ks = 0; ks < KSC; ++ks) {
       uint32_t ch[4], cl[4];
+      if constexpr (VEC) {
+        const int l = 32 * ks + 8 * g;
+        const int r1 = a.first.rank;
+        u32x4 v = {0, 0, 0, 0};
+        if (t < T) {
+          if (l < r1) {
+            if (t < a.first.num_tokens)
+              v = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(A1) + (int64_t)t * r1 + l);
+          } else if (l < m) {
+            if (t < a.second.num_tokens)
+              v = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(A2) +
+                                                  (int64_t)t * a.second.rank + (l - r1));
+          }
+        }
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          ch[w] = v[w];
+          cl[w] = 0;
+        }
+      } else {
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
         const int l = 32 * ks + 8 * g + 2 * w;
@@ -263,6 +465,7 @@ __global__ __launch_bounds__(kChainThreads) void chain_proj(ChainArgs a) {
           cl[w] = 0;
         }
       }
+      }
       const bf16x8 bh = as_bf16x8(u32x4{ch[0], ch[1], ch[2], ch[3]});
       const bf16x8 bl = as_bf16x8(u32x4{cl[0], cl[1], cl[2], cl[3]});
 #pragma unroll
@@ -275,7 +478,18 @@ __global__ __launch_bounds__(kChainThreads) void chain_proj(ChainArgs a) {
         acc[mt] = mfma16x16x32(yh, bh, acc[mt]);
       }
     }
-    if (t < T) {
+    if (t < T && VEC) {
+#pragma unroll
+      for (int mt = 0; mt < MTR; ++mt) {
+        const int k0 = 16 * mt + 4 * g;
+        if (k0 < ro) {
+          uint2 w;
+          w.x = pack_bf16x2(acc[mt][0], acc[mt][1]);
+          w.y = pack_bf16x2(acc[mt][2], acc[mt][3]);
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(Co) + (int64_t)t * ro + k0) = w;
+        }
+      }
+    } else if (t < T) {
 #pragma unroll
       for (int mt = 0; mt < MTR; ++mt) {
 #pragma unroll
@@ -306,46 +520,66 @@ static void launch_cgram_ft(int ft, dim3 grid, hipStream_t stream, const ChainAr
   ((ft == FTs + 1 ? launch_cgram_one<FTs + 1, F32>(grid, stream, a) : void()), ...);
 }
 
-template <bool F32>
+template <bool F32, bool VEC>
 static void launch_cproj_mtr(int mtr, dim3 grid, size_t lds, hipStream_t stream, const ChainArgs& a) {
   switch (mtr) {
-    case 1: hipLaunchKernelGGL((chain_proj<1, F32>), grid, dim3(kChainThreads), lds, stream, a); break;
-    case 2: hipLaunchKernelGGL((chain_proj<2, F32>), grid, dim3(kChainThreads), lds, stream, a); break;
+    case 1: hipLaunchKernelGGL((chain_proj<1, F32, VEC>), grid, dim3(kChainThreads), lds, stream, a); break;
+    case 2: hipLaunchKernelGGL((chain_proj<2, F32, VEC>), grid, dim3(kChainThreads), lds, stream, a); break;
     case 3:
-    case 4: hipLaunchKernelGGL((chain_proj<4, F32>), grid, dim3(kChainThreads), lds, stream, a); break;
-    default: hipLaunchKernelGGL((chain_proj<8, F32>), grid, dim3(kChainThreads), lds, stream, a); break;
+    case 4: hipLaunchKernelGGL((chain_proj<4, F32, VEC>), grid, dim3(kChainThreads), lds, stream, a); break;
+    default: hipLaunchKernelGGL((chain_proj<8, F32, VEC>), grid, dim3(kChainThreads), lds, stream, a); break;
   }
+}
+
+template <int FT>
+static void launch_cgram_wave(dim3 grid, hipStream_t stream, const ChainArgs& a) {
+  hipLaunchKernelGGL((chain_gram_wave<FT>), grid, dim3(kChainThreads), 0, stream, a);
 }
 
 hipError_t launch_chain(const ChainArgs& a, const EigArgs& ea, hipStream_t stream) {
   const bool f32 = a.first.coef_dtype == KVC_F32;
-  const int ft = a.mp / 16;
   const int T = a.out.num_tokens;
-  dim3 ggrid(a.max_parts, a.num_units);
-  if (f32) launch_cgram_ft<true>(ft, ggrid, stream, a, std::make_integer_sequence<int, 16>{});
-  else launch_cgram_ft<false>(ft, ggrid, stream, a, std::make_integer_sequence<int, 16>{});
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(chain_assemble, dim3(a.num_units), dim3(kChainThreads), 0, stream, a);
+  const int m = a.first.rank + a.second.rank;
+  const int d = a.first.head_dim;
+  hipError_t e;
+  if (a.gram_wave_ft > 0) {
+    dim3 ggrid((a.max_parts + kChainWaves - 1) / kChainWaves, a.num_units);
+    switch (a.gram_wave_ft) {
+      case 2: launch_cgram_wave<2>(ggrid, stream, a); break;
+      case 4: launch_cgram_wave<4>(ggrid, stream, a); break;
+      default: launch_cgram_wave<8>(ggrid, stream, a); break;
+    }
+  } else {
+    dim3 ggrid(a.max_parts, a.num_units);
+    const int ft = a.mp / 16;
+    if (f32) launch_cgram_ft<true>(ft, ggrid, stream, a, std::make_integer_sequence<int, 16>{});
+    else launch_cgram_ft<false>(ft, ggrid, stream, a, std::make_integer_sequence<int, 16>{});
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (m <= 128) {
+    const size_t lds = chain_assemble_lds_bytes(m, d);
+    e = hipFuncSetAttribute((const void*)chain_assemble_lds, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(chain_assemble_lds, dim3(a.num_units), dim3(kChainThreads), lds, stream, a);
+  } else {
+    hipLaunchKernelGGL(chain_assemble, dim3(a.num_units), dim3(kChainThreads), 0, stream, a);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = launch_eig(ea, stream)) != hipSuccess) return e;
   hipLaunchKernelGGL(chain_ymat, dim3(a.num_units), dim3(kChainThreads), 0, stream, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int mtr = (a.out.rank + 15) / 16;
   const int mtr_inst = mtr <= 2 ? mtr : (mtr <= 4 ? 4 : 8);
-  const int m = a.first.rank + a.second.rank;
   const size_t lds = (size_t)mtr_inst * 16 * ((m + 31) / 32 * 32) * 2 * sizeof(uint16_t);
   dim3 pgrid((T + kCprojChunk - 1) / kCprojChunk, a.num_units);
-  if (f32) {
-    e = hipFuncSetAttribute((const void*)chain_proj<8, true>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    launch_cproj_mtr<true>(mtr, pgrid, lds, stream, a);
-  } else {
-    e = hipFuncSetAttribute((const void*)chain_proj<8, false>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds);
-    if (e != hipSuccess) return e;
-    launch_cproj_mtr<false>(mtr, pgrid, lds, stream, a);
-  }
+  const bool vec = !f32 && a.first.rank % 8 == 0 && a.second.rank % 8 == 0 && a.out.rank % 4 == 0;
+  const void* big = f32 ? (const void*)chain_proj<8, true, false>
+                        : (vec ? (const void*)chain_proj<8, false, true> : (const void*)chain_proj<8, false, false>);
+  e = hipFuncSetAttribute(big, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  if (f32) launch_cproj_mtr<true, false>(mtr, pgrid, lds, stream, a);
+  else if (vec) launch_cproj_mtr<false, true>(mtr, pgrid, lds, stream, a);
+  else launch_cproj_mtr<false, false>(mtr, pgrid, lds, stream, a);
   return hipGetLastError();
 }
 

@@ -79,4 +79,61 @@ __device__ __forceinline__ int64_t unit_index(int32_t layer, int32_t kv, int32_t
   return ((int64_t)layer * 2 + kv) * num_kv_heads + head;
 }
 
+// ---- Gram fragments (shared by the fit and chain Gram kernels) ----------------------------------------------
+
+// Tile idx of the upper triangle (row-major over fi <= fj) of an FT x FT grid of 16 x 16 tiles.
+constexpr int tile_fi(int idx, int FT) {
+  int fi = 0;
+  while (idx >= FT - fi) {
+    idx -= FT - fi;
+    ++fi;
+  }
+  return fi;
+}
+constexpr int tile_fj(int idx, int FT) {
+  int fi = 0;
+  while (idx >= FT - fi) {
+    idx -= FT - fi;
+    ++fi;
+  }
+  return fi + idx;
+}
+
+// The Gram is computed in a permuted feature order: output tile (fi, fj) holds G[FT m + fi][FT n + fj] for
+// m, n in [0, 16).  Lane (g, m) of a wave then needs, for its 8 tokens 8 g + j, the FT contiguous features
+// FT m .. FT m + FT - 1 of each row (one 2 FT-byte read per token), and the MFMA fragment of tile row fi is
+// element fi of those 8 segments, gathered with byte permutes.
+template <int FT>
+struct GramSeg;
+template <>
+struct GramSeg<8> {
+  using T = u32x4;
+};
+template <>
+struct GramSeg<4> {
+  using T = uint2;
+};
+template <>
+struct GramSeg<2> {
+  using T = uint32_t;
+};
+
+template <int FT>
+__device__ __forceinline__ uint32_t seg_dword(const typename GramSeg<FT>::T& s, int w) {
+  if constexpr (FT == 8) return s[w];
+  else if constexpr (FT == 4) return w == 0 ? s.x : s.y;
+  else return s;
+}
+
+// Fragment of tile row fi: bf16 element fi of each of the 8 token segments (tokens 8 g + 0 .. 7).
+template <int FT, int FI>
+__device__ __forceinline__ bf16x8 gram_fragment(const typename GramSeg<FT>::T* seg) {
+  constexpr uint32_t sel = (FI & 1) ? 0x07060302u : 0x05040100u;
+  u32x4 f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w)
+    f[w] = __builtin_amdgcn_perm(seg_dword<FT>(seg[2 * w + 1], FI >> 1), seg_dword<FT>(seg[2 * w], FI >> 1), sel);
+  return as_bf16x8(f);
+}
+
 }  // namespace kvc

@@ -47,61 +47,11 @@ __device__ __forceinline__ int64_t fit_linear_unit(const FitArgs& a, const FitUn
 // Gram, bf16 caches
 // ---------------------------------------------------------------------------------------------------------------
 
-// Tile idx of the upper triangle (row-major over fi <= fj) of an FT x FT grid of 16 x 16 tiles.
-constexpr int tile_fi(int idx, int FT) {
-  int fi = 0;
-  while (idx >= FT - fi) {
-    idx -= FT - fi;
-    ++fi;
-  }
-  return fi;
-}
-constexpr int tile_fj(int idx, int FT) {
-  int fi = 0;
-  while (idx >= FT - fi) {
-    idx -= FT - fi;
-    ++fi;
-  }
-  return fi + idx;
-}
-
 template <int D>
 struct GramShape {
   static constexpr int FT = D / 16;                 // 16 x 16 output tiles per side
   static constexpr int NTILES = FT * (FT + 1) / 2;  // tiles on or above the diagonal
 };
-
-// The Gram is computed in a permuted feature order: output tile (fi, fj) holds G[FT m + fi][FT n + fj] for
-// m, n in [0, 16).  Lane (g, m) of a wave then needs, for its 8 tokens 8 g + j, the FT contiguous features
-// FT m .. FT m + FT - 1 of each row (one 2 FT-byte read per token), and the MFMA fragment of tile row fi is
-// element fi of those 8 segments, gathered with byte permutes.
-template <int FT>
-struct GramSeg;
-template <>
-struct GramSeg<8> {
-  using T = u32x4;
-};
-template <>
-struct GramSeg<4> {
-  using T = uint2;
-};
-
-template <int FT>
-__device__ __forceinline__ uint32_t seg_dword(const typename GramSeg<FT>::T& s, int w) {
-  if constexpr (FT == 8) return s[w];
-  else return w == 0 ? s.x : s.y;
-}
-
-// Fragment of tile row fi: bf16 element fi of each of the 8 token segments (tokens 8 g + 0 .. 7).
-template <int FT, int FI>
-__device__ __forceinline__ bf16x8 gram_fragment(const typename GramSeg<FT>::T* seg) {
-  constexpr uint32_t sel = (FI & 1) ? 0x07060302u : 0x05040100u;
-  u32x4 f;
-#pragma unroll
-  for (int w = 0; w < 4; ++w)
-    f[w] = __builtin_amdgcn_perm(seg_dword<FT>(seg[2 * w + 1], FI >> 1), seg_dword<FT>(seg[2 * w], FI >> 1), sel);
-  return as_bf16x8(f);
-}
 
 // Tile Q of wave W (tile index W + 4 Q): acc += Z_fi^T Z_fj with the hi/lo products.
 template <int D, int W, int Q>

@@ -71,7 +71,8 @@ struct ChainArgs {
   int32_t layer_begin;
   int32_t num_layers;
   int32_t num_units;
-  int32_t mp;                  // r1 + r2 rounded up to a multiple of 16
+  int32_t mp;                  // row stride of the H partials (r1 + r2 rounded up to a multiple of 16)
+  int32_t gram_wave_ft;        // 2, 4 or 8: the LDS-free wave Gram with mp = 16 * gram_wave_ft; 0: LDS Gram
   float* partials;             // workspace [unit][max_parts][mp][mp]
   int32_t max_parts;
   int32_t part_tokens;
