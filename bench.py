@@ -109,8 +109,9 @@ def main():
     ap.add_argument("--workload", default="llama8b_32k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
-                    help="before the steps, copy BYTES device to device once (a plain copy of known size, so that "
-                         "HBM counters of a profiling run can be scaled)")
+                    help="before the steps, run one elementwise kernel that reads BYTES and writes BYTES (dst = -src "
+                         "in float32), a plain copy of known size, so that HBM counters of a profiling run can be "
+                         "scaled")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU: the correction path has no cross-GPU step to measure (asked for "
@@ -149,9 +150,9 @@ def main():
     kvc.kvc_fit_state(cache, fit_batches[0], workspace=ws_fit)
     torch.cuda.synchronize()
     if args.copy_calibration > 0:
-        a_src = torch.ones(args.copy_calibration, dtype=torch.uint8, device=dev)
+        a_src = torch.ones(args.copy_calibration // 4, dtype=torch.float32, device=dev)
         a_dst = torch.empty_like(a_src)
-        a_dst.copy_(a_src)
+        torch.neg(a_src, out=a_dst)
         torch.cuda.synchronize()
         del a_src, a_dst
 
