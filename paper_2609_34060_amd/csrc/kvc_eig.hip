@@ -1,7 +1,8 @@
 // Top-r eigenpairs of the per-unit d x d Gram matrices in fp64: the right singular vectors R_r and singular values
 // of Eq. 7 (Z^T Z = R Sigma^2 R^T).  One workgroup of 1024 threads per (layer, K/V, head) unit:
-//   1. G = sum of the unit's fp32 partial Grams in a fixed order (or a dense fp64 matrix), into LDS.
-//   2. Householder tridiagonalisation G = Q T Q^T in LDS; the reflectors go to the workspace.
+//   1. G = sum of the unit's fp32 partial Grams in a fixed order in fp64 (or a dense fp64 matrix), into LDS.
+//   2. Householder tridiagonalisation G = Q T Q^T in fp64 arithmetic; the trailing matrix is kept in LDS in fp32
+//      (the Gram itself carries fp32 accuracy), which lets two units share a CU; the reflectors go to the workspace.
 //   3. Multisection bisection with Sturm counts for the r largest eigenvalues of T (groups of lanes per
 //      eigenvalue, one ballot per step).
 //   4. Inverse iteration on T (LDL^T without pivoting, tiny pivots replaced) from pseudo-random starts, one lane
@@ -18,17 +19,46 @@ namespace kvc {
 
 constexpr int kEigThreads = 1024;
 constexpr int kEigWaves = kEigThreads / kWave;
-constexpr int kReflChunk = 16;  // reflectors staged in LDS per back-transformation chunk
+constexpr int kReflChunk = 8;   // reflectors staged in LDS per back-transformation chunk
+constexpr int kInvBatch = 32;   // eigenvectors per inverse-iteration batch (one lane each)
 
-__device__ __forceinline__ double wave_sum(double x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, kWave);
+// fp64 cross-lane moves by DPP (two 32-bit halves); lanes whose row is masked off receive 0.
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ double dpp64(double x) {
+  const unsigned long long b = __builtin_bit_cast(unsigned long long, x);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(unsigned)b, CTRL, ROW_MASK, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(unsigned)(b >> 32), CTRL, ROW_MASK, 0xF, false);
+  return __builtin_bit_cast(double, ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
+}
+constexpr int kDppRor1 = 0x121, kDppRor2 = 0x122, kDppRor4 = 0x124, kDppRor8 = 0x128;
+constexpr int kDppBcast15 = 0x142, kDppBcast31 = 0x143;
+
+// Sum over each group of G consecutive lanes (G = 16, 32 or 64); the group's last lane holds the total (other lanes
+// hold partial sums).  A fixed order, so the result is deterministic.  Called with the whole wave active.
+template <int G>
+__device__ __forceinline__ double group_sum(double x) {
+  x += dpp64<kDppRor8>(x);
+  x += dpp64<kDppRor4>(x);
+  x += dpp64<kDppRor2>(x);
+  x += dpp64<kDppRor1>(x);
+  if (G >= 32) x += dpp64<kDppBcast15, 0xA>(x);
+  if (G >= 64) x += dpp64<kDppBcast31, 0xC>(x);
   return x;
 }
+__device__ __forceinline__ double lane_value(double x, int l) {
+  const unsigned long long b = __builtin_bit_cast(unsigned long long, x);
+  const unsigned lo = __builtin_amdgcn_readlane((int)(unsigned)b, l);
+  const unsigned hi = __builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
+  return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
+}
+// Whole-wave sum and maximum, returned in every lane.
+__device__ __forceinline__ double wave_sum(double x) { return lane_value(group_sum<64>(x), 63); }
 __device__ __forceinline__ double wave_max(double x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x = fmax(x, __shfl_xor(x, o, kWave));
-  return x;
+  x = fmax(x, dpp64<kDppRor8>(x));
+  x = fmax(x, dpp64<kDppRor4>(x));
+  x = fmax(x, dpp64<kDppRor2>(x));
+  x = fmax(x, dpp64<kDppRor1>(x));
+  return fmax(fmax(lane_value(x, 0), lane_value(x, 16)), fmax(lane_value(x, 32), lane_value(x, 48)));
 }
 
 struct UnitTarget {
@@ -66,6 +96,18 @@ __device__ __forceinline__ uint32_t hash3(uint32_t a, uint32_t b, uint32_t c) {
   return h;
 }
 
+// Scalars of one Householder step from x_0 and s = ||x||^2: out = {alpha, v_0, beta} with alpha = -sign(x_0) ||x||,
+// v = x - alpha e_1 and beta = 2 / v^T v (0 when x = 0, which makes the step the identity).
+__device__ __forceinline__ void reflector_scalars(double x0, double s, double* out) {
+  const double nrm = sqrt(s);
+  const double alpha = nrm == 0.0 ? 0.0 : -copysign(nrm, x0);
+  const double v0 = x0 - alpha;
+  const double vtv = (s - x0 * x0) + v0 * v0;
+  out[0] = alpha;
+  out[1] = v0;
+  out[2] = vtv > 0.0 ? 2.0 / vtv : 0.0;
+}
+
 // 1 / q from the hardware reciprocal and one Newton step (relative error about 2^-52).
 __device__ __forceinline__ double recip(double q) {
   const double r0 = __builtin_amdgcn_rcp(q);
@@ -88,21 +130,152 @@ __device__ __forceinline__ int sturm_count(const double* sa, const double* sb2, 
   return c;
 }
 
+// ---- Householder tridiagonalisation steps ----------------------------------------------------------------------
+// Step k reflects x = row k beyond the diagonal (the matrix is symmetric) onto alpha e_1 with H_k = I - beta v v^T,
+// v = x - alpha e_1; with p = beta A22 v, K = beta v^T p / 2 and w = p - K v, A22 <- A22 - v w^T - w v^T.
+// The matrix lives in LDS as fp32 [N][N]; the rank-2 update is two fp32 fmas per entry (v and w rounded to fp32),
+// everything else (p, K, w, the scalars, the reflectors) is fp64.  Per step:
+//   pivot (wave 0): p of step k from the row-group partials, K, w; row k + 1 under step k (the next x); the scalars
+//       of step k + 1; {v_C, w_C, x'_C} of every column to s_vw; the reflector to the workspace.
+//   sweep (all threads): rows C > k + 1 under step k; from the updated entries, the row-group partial sums of the
+//       next step's A22 v' (no scaling by beta yet).  Thread (g, R) owns column R of rows g, g + RG, ...; a row
+//       group is whole waves, so row skips are uniform; partial[g][R] goes to LDS, summed by the next pivot.
+// Step k's scalars {alpha, v_0, beta} are in s_ab + 4 (k & 1).
+
+// Wave 0.  Before the first step (k = -1) only the scalars of step 0 and s_vw are formed.
 template <int N>
-__global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
-  constexpr int LD = N + 1;
-  // the matrix region also holds the inverse-iteration scratch (2 x N x 64) and X (r x N)
-  constexpr int AREG = N * LD > 2 * N * kWave ? N * LD : 2 * N * kWave;
+__device__ __forceinline__ void tri_pivot(float* A, const double* partial, float4* s_vw, double* s_ab, double* s_b,
+                                          double* refl, double* refl_beta, int k, int lane) {
+  constexpr int RG = kEigThreads / N;  // row groups of the sweep
+  constexpr int Q = N / kWave;         // columns per lane
+  const int kn = k + 1;
+  double vq[Q], wq[Q];
+  double v0 = 0.0, wR = 0.0;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) vq[q] = wq[q] = 0.0;
+  if (k >= 0) {
+    const double* ab = s_ab + 4 * (k & 1);
+    const double alpha = ab[0], beta = ab[2];
+    v0 = ab[1];
+    double pq[Q], kk = 0.0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int C = lane + kWave * q;
+      double sum = 0.0;
+#pragma unroll
+      for (int gi = 0; gi < RG; ++gi) sum += partial[gi * N + C];
+      pq[q] = beta * sum;
+      vq[q] = C > kn ? (double)A[k * N + C] : (C == kn ? v0 : 0.0);
+      kk += vq[q] * pq[q];
+    }
+    const double K = 0.5 * beta * wave_sum(kk);
+#pragma unroll
+    for (int q = 0; q < Q; ++q) wq[q] = (lane + kWave * q) >= kn ? pq[q] - K * vq[q] : 0.0;
+    wR = lane_value(wq[kn / kWave], kn % kWave);  // w of row k + 1 (its v is v_0)
+    double* refl_k = refl + __builtin_amdgcn_readfirstlane(k * N);
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int C = lane + kWave * q;
+      if (C >= kn) refl_k[C - kn] = vq[q];
+    }
+    if (lane == 0) {
+      s_b[k] = alpha;
+      refl_beta[k] = beta;
+    }
+  }
+  // row k + 1 under step k (same arithmetic as the sweep), its norm beyond the diagonal, the next scalars
+  const float v0f = (float)v0, wRf = (float)wR;
+  double s = 0.0;
+  float xq[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int C = lane + kWave * q;
+    float x = A[kn * N + C];
+    if (k >= 0 && C >= kn) {
+      x = fmaf(-v0f, (float)wq[q], fmaf(-wRf, (float)vq[q], x));
+      A[kn * N + C] = x;
+    }
+    xq[q] = x;
+    s += C > kn ? (double)x * (double)x : 0.0;
+  }
+  s = wave_sum(s);
+  const double x0 = kn + 1 < N ? lane_value((double)xq[((kn + 1) % N) / kWave], (kn + 1) % kWave) : 0.0;
+  if (lane == 0) reflector_scalars(x0, s, s_ab + 4 * (kn & 1));
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int C = lane + kWave * q;
+    s_vw[C] = make_float4((float)vq[q], (float)wq[q], C > kn + 1 ? xq[q] : 0.0f, 0.0f);
+  }
+}
+
+// All threads: rows C > k + 1 under step k (UPD; without UPD, k = -1 and nothing is updated), then the row-group
+// partial sums of A22 v' for step k + 1 (v'_{k+2} = v_0 of step k + 1, v'_C = x'_C beyond).
+template <int N, bool UPD>
+__device__ __forceinline__ void tri_sweep(float* A, double* partial, const float4* s_vw, const double* s_ab, int k,
+                                          int tid) {
+  constexpr int RG = kEigThreads / N;
+  constexpr int RPT = N / RG;
+  const int R = tid & (N - 1), g = tid / N;
+  const int kn = k + 1;
+  const float4 vwR = s_vw[R];
+  const float v0n = (float)s_ab[4 * (kn & 1) + 1];
+  const bool col_live = R > kn;
+  double acc = 0.0;
+#pragma unroll 4
+  for (int t = 0; t < RPT; ++t) {
+    const int C = g + RG * t;
+    if (C <= kn) continue;  // uniform: a row group is whole waves
+    const float4 vwC = s_vw[C];
+    float a = A[C * N + R];
+    if (UPD) {
+      a = fmaf(-vwC.x, vwR.y, fmaf(-vwC.y, vwR.x, a));
+      if (col_live) A[C * N + R] = a;
+    }
+    const float vpC = C == kn + 1 ? v0n : vwC.z;
+    acc += (double)a * (double)vpC;
+  }
+  partial[g * N + R] = acc;
+}
+
+// LDS layout (bytes): the matrix region MREG holds, in turn, G / the trailing matrix as fp32 [N][N] (phases 1-2),
+// the inverse-iteration scratch fp64 [N][kInvBatch] x 2 (phase 4), X fp32 [r][N] (MGS, back-transformation); then
+// fp64 scalars and vectors; then the staging region: the sweep's row-group partials fp64 [RG][N] during phase 2, a
+// chunk of reflectors during phase 5.  About 79 KB for N = 128, so two units share a CU.
+template <int N>
+struct EigLds {
+  static constexpr size_t kMat = (size_t)N * N * 4;
+  static constexpr size_t kScratch = (size_t)2 * N * kInvBatch * 8;
+  static constexpr size_t kX = (size_t)KVC_MAX_RANK * N * 4;
+  static constexpr size_t kMreg = ((kMat > kScratch ? (kMat > kX ? kMat : kX) : (kScratch > kX ? kScratch : kX)) +
+                                   15) / 16 * 16;
+  // s_a, s_b [N]; s_lam [KVC_MAX_RANK]; s_ab [2][4]; s_misc [8]; s_vw float4 [N] (later b^2 [N])
+  static constexpr size_t kSmall = (size_t)(2 * N + KVC_MAX_RANK + 8 + 8) * 8 + (size_t)N * 16;
+  static constexpr size_t kPartial = (size_t)(kEigThreads / N) * N * 8;
+  static constexpr size_t kReflStage = (size_t)kReflChunk * (N + 1) * 8;
+  static constexpr size_t kStage = kPartial > kReflStage ? kPartial : kReflStage;
+  static constexpr size_t kTotal = kMreg + kSmall + kStage;
+};
+
+// Eight waves per SIMD (at most 64 VGPRs) so that two 1024-thread units share a CU.
+template <int N>
+__global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))) void eig_topr(EigArgs a) {
+  using Lay = EigLds<N>;
+  constexpr int LD = N;
   extern __shared__ __attribute__((aligned(16))) double smem[];
-  double* A = smem;                     // N x LD (phase 1-2); scratch / X afterwards
-  double* s_a = A + AREG;               // diagonal of T
-  double* s_b = s_a + N;                // off-diagonal of T: b[i] couples i and i + 1
-  double* s_b2 = s_b + N;               // b^2
-  double* s_lam = s_b2 + N;             // eigenvalues, descending
-  double* s_v = s_lam + KVC_MAX_RANK;   // current reflector
-  double* s_p = s_v + N;                // p / w
-  double* s_misc = s_p + N;             // scalars
-  double* s_rb = s_misc + 8;            // a chunk of reflectors for the back-transformation [kReflChunk][N]
+  char* base = reinterpret_cast<char*>(smem);
+  float* A = reinterpret_cast<float*>(base);             // G, then the trailing matrix (fp32 storage)
+  double* invd = reinterpret_cast<double*>(base);        // inverse-iteration scratch [N][kInvBatch]
+  double* xv = invd + N * kInvBatch;                     // [N][kInvBatch]
+  float* X = reinterpret_cast<float*>(base);             // eigenvectors, vector j in row j (fp32 storage)
+  double* s_a = reinterpret_cast<double*>(base + Lay::kMreg);  // diagonal of T
+  double* s_b = s_a + N;                    // off-diagonal of T: b[i] couples i and i + 1
+  double* s_lam = s_b + N;                  // eigenvalues, descending
+  double* s_ab = s_lam + KVC_MAX_RANK;      // reflector scalars {alpha, v_0, beta, -}, by step parity [2][4]
+  double* s_misc = s_ab + 8;                // scalars
+  float4* s_vw = reinterpret_cast<float4*>(s_misc + 8);  // {v_C, w_C, x'_C, -} of the current step
+  double* s_b2 = reinterpret_cast<double*>(s_vw);        // b^2 (after the tridiagonalisation)
+  double* partial = reinterpret_cast<double*>(base + Lay::kMreg + Lay::kSmall);  // sweep partials [RG][N]
+  double* s_rb = partial;                   // reflector chunk [kReflChunk][N] (back-transformation)
   double* s_rbeta = s_rb + kReflChunk * N;
 
   const int u = blockIdx.x;
@@ -121,84 +294,27 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
     for (int e = tid; e < N * N; e += kEigThreads) {
       double s = 0.0;
       for (int c = 0; c < parts; ++c) s += (double)P[(size_t)c * N * N + e];
-      A[(e / N) * LD + (e % N)] = s;
+      A[(e / N) * LD + (e % N)] = (float)s;
     }
   } else {
     const double* Dm = a.dense + (size_t)u * N * N;
-    for (int e = tid; e < N * N; e += kEigThreads) A[(e / N) * LD + (e % N)] = Dm[e];
+    for (int e = tid; e < N * N; e += kEigThreads) A[(e / N) * LD + (e % N)] = (float)Dm[e];
   }
   __syncthreads();
 
-  // ---- 2. Householder tridiagonalisation ------------------------------------------------------------------
+  // ---- 2. Householder tridiagonalisation -----------------------------------------------------------------------
+  if (wave == 0) tri_pivot<N>(A, partial, s_vw, s_ab, s_b, refl, refl_beta, -1, lane);
+  __syncthreads();
+  tri_sweep<N, false>(A, partial, s_vw, s_ab, -1, tid);
+  __syncthreads();
   for (int k = 0; k < N - 2; ++k) {
-    const int m = N - k - 1;
-    if (wave == 0) {
-      double s = 0.0;
-      for (int i = lane; i < m; i += kWave) {
-        const double x = A[(k + 1 + i) * LD + k];
-        s += x * x;
-      }
-      s = wave_sum(s);
-      const double x0 = A[(k + 1) * LD + k];
-      const double nrm = sqrt(s);
-      const double alpha = nrm == 0.0 ? 0.0 : -copysign(nrm, x0);
-      const double v0 = x0 - alpha;
-      const double vtv = (s - x0 * x0) + v0 * v0;
-      const double beta = vtv > 0.0 ? 2.0 / vtv : 0.0;
-      for (int i = lane; i < m; i += kWave) {
-        const double vi = i == 0 ? v0 : A[(k + 1 + i) * LD + k];
-        s_v[i] = vi;
-        refl[k * N + i] = vi;
-      }
-      if (lane == 0) {
-        s_b[k] = alpha;
-        s_misc[0] = beta;
-        refl_beta[k] = beta;
-      }
-    }
+    if (wave == 0) tri_pivot<N>(A, partial, s_vw, s_ab, s_b, refl, refl_beta, k, lane);
     __syncthreads();
-    const double beta = s_misc[0];
-    if (beta == 0.0) {  // x = 0: H_k = I
-      __syncthreads();  // everyone has read s_misc[0] before wave 0 rewrites it
-      continue;
-    }
-    {
-      // p = beta * A22 v, eight lanes per row
-      const int i = tid >> 3, sub = tid & 7;
-      double s = 0.0;
-      if (i < m) {
-        const double* row = &A[(k + 1 + i) * LD + k + 1];
-        for (int j = sub; j < m; j += 8) s += row[j] * s_v[j];
-      }
-      s += __shfl_xor(s, 1, kWave);
-      s += __shfl_xor(s, 2, kWave);
-      s += __shfl_xor(s, 4, kWave);
-      if (i < m && sub == 0) s_p[i] = beta * s;
-    }
-    __syncthreads();
-    {
-      // w = p - (beta / 2) (v^T p) v; every wave forms the scalar itself
-      double s = 0.0;
-      for (int i = lane; i < m; i += kWave) s += s_v[i] * s_p[i];
-      s = wave_sum(s);
-      const double K = 0.5 * beta * s;
-      __syncthreads();
-      for (int i = tid; i < m; i += kEigThreads) s_p[i] = s_p[i] - K * s_v[i];
-    }
-    __syncthreads();
-    // A22 -= v w^T + w v^T, with the same rounding for (i, j) and (j, i) to keep A exactly symmetric
-    for (int i = tid >> 5; i < m; i += kEigThreads >> 5) {
-      const double vi = s_v[i], wi = s_p[i];
-      double* row = &A[(k + 1 + i) * LD + k + 1];
-      for (int j = tid & 31; j < m; j += 32) {
-        const double t = __dadd_rn(__dmul_rn(vi, s_p[j]), __dmul_rn(wi, s_v[j]));
-        row[j] = __dsub_rn(row[j], t);
-      }
-    }
+    tri_sweep<N, true>(A, partial, s_vw, s_ab, k, tid);
     __syncthreads();
   }
   for (int i = tid; i < N; i += kEigThreads) s_a[i] = A[i * LD + i];
-  if (tid == 0) s_b[N - 2] = A[(N - 1) * LD + N - 2];
+  if (tid == 0) s_b[N - 2] = A[(N - 2) * LD + N - 1];
   __syncthreads();
   for (int i = tid; i < N - 1; i += kEigThreads) s_b2[i] = s_b[i] * s_b[i];
   if (tid == 0) {
@@ -222,7 +338,7 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
 
   if (tnorm == 0.0) {
     // Z = 0: every eigenvalue is 0; take the unit vectors (the product is zero whatever the basis).
-    for (int e = tid; e < r * N; e += kEigThreads) A[e] = (e / N) == (e % N) ? 1.0 : 0.0;
+    for (int e = tid; e < r * N; e += kEigThreads) X[e] = (e / N) == (e % N) ? 1.0f : 0.0f;
     for (int j = tid; j < r; j += kEigThreads) s_lam[j] = 0.0;
     __syncthreads();
   } else {
@@ -232,9 +348,9 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
       while (rp < r) rp <<= 1;
       // lanes per eigenvalue (a power of two dividing 64); 16 trades latency (iterations) against the fp64 work
       const int P = min(16, kEigThreads / rp);
-      int bits = 0;
-      while ((2 << bits) <= P + 1) ++bits;          // floor(log2(P + 1))
-      const int iters = 66 / bits + 1;
+      // each step shrinks the bracket (P + 1)-fold; stop at 2^-44 of the Gershgorin interval, far below the
+      // perturbation that fp32 storage of the matrix already carries
+      const int iters = P >= 16 ? 11 : P >= 8 ? 14 : P >= 4 ? 19 : P >= 2 ? 28 : 44;
       const int grp = tid / P, s = tid - grp * P;
       const int kasc = N - 1 - grp;                  // ascending index of the target eigenvalue
       const double pivmin = s_misc[4];
@@ -254,80 +370,78 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
     }
     __syncthreads();
 
-    // ---- 4. inverse iteration, 64 vectors per batch, one lane each ------------------------------------
-    double* invd = A;                  // [N][64]
-    double* xv = A + N * kWave;        // [N][64]
+    // ---- 4. inverse iteration, kInvBatch vectors per batch, one lane each ------------------------------
     const double piv = 2.220446049250313e-16 * tnorm;
-    for (int j0 = 0; j0 < r; j0 += kWave) {
+    for (int j0 = 0; j0 < r; j0 += kInvBatch) {
       const int j = j0 + tid;
-      if (tid < kWave && j < r) {
+      if (tid < kInvBatch && j < r) {
         const double lam = s_lam[j];
         double d = s_a[0] - lam;
         if (fabs(d) < piv) d = copysign(piv, d);
         invd[tid] = 1.0 / d;
-        #pragma unroll 2
+#pragma unroll 2
         for (int i = 1; i < N; ++i) {
-          const double l = s_b[i - 1] * invd[(i - 1) * kWave + tid];
+          const double l = s_b[i - 1] * invd[(i - 1) * kInvBatch + tid];
           d = (s_a[i] - lam) - l * s_b[i - 1];
           if (fabs(d) < piv) d = copysign(piv, d);
-          invd[i * kWave + tid] = 1.0 / d;
+          invd[i * kInvBatch + tid] = 1.0 / d;
         }
-        #pragma unroll 2
+#pragma unroll 2
         for (int i = 0; i < N; ++i) {
           const uint32_t h = hash3(a.seed ^ (uint32_t)u, (uint32_t)j, (uint32_t)i);
-          xv[i * kWave + tid] = (double)(h >> 11) * (1.0 / 2097152.0) - 1.0;
+          xv[i * kInvBatch + tid] = (double)(h >> 11) * (1.0 / 2097152.0) - 1.0;
         }
         for (int itr = 0; itr < 3; ++itr) {
           double z = xv[tid];
-          #pragma unroll 2
+#pragma unroll 2
           for (int i = 1; i < N; ++i) {
-            z = xv[i * kWave + tid] - s_b[i - 1] * invd[(i - 1) * kWave + tid] * z;
-            xv[i * kWave + tid] = z;
+            z = xv[i * kInvBatch + tid] - s_b[i - 1] * invd[(i - 1) * kInvBatch + tid] * z;
+            xv[i * kInvBatch + tid] = z;
           }
-          double x = xv[(N - 1) * kWave + tid] * invd[(N - 1) * kWave + tid];
-          xv[(N - 1) * kWave + tid] = x;
+          double x = xv[(N - 1) * kInvBatch + tid] * invd[(N - 1) * kInvBatch + tid];
+          xv[(N - 1) * kInvBatch + tid] = x;
           double mx = fabs(x);
-          #pragma unroll 2
+#pragma unroll 2
           for (int i = N - 2; i >= 0; --i) {
-            x = (xv[i * kWave + tid] - s_b[i] * x) * invd[i * kWave + tid];
-            xv[i * kWave + tid] = x;
+            x = (xv[i * kInvBatch + tid] - s_b[i] * x) * invd[i * kInvBatch + tid];
+            xv[i * kInvBatch + tid] = x;
             mx = fmax(mx, fabs(x));
           }
           const double sc = mx > 0.0 ? 1.0 / mx : 1.0;
           double ss = 0.0;
-          #pragma unroll 2
+#pragma unroll 2
           for (int i = 0; i < N; ++i) {
-            const double y = xv[i * kWave + tid] * sc;
+            const double y = xv[i * kInvBatch + tid] * sc;
             ss += y * y;
           }
           const double f = sc / sqrt(ss);
-          #pragma unroll 2
-          for (int i = 0; i < N; ++i) xv[i * kWave + tid] *= f;
+#pragma unroll 2
+          for (int i = 0; i < N; ++i) xv[i * kInvBatch + tid] *= f;
         }
-        #pragma unroll 2
-        for (int i = 0; i < N; ++i) gvec[(size_t)j * N + i] = xv[i * kWave + tid];
+#pragma unroll 2
+        for (int i = 0; i < N; ++i) gvec[(size_t)j * N + i] = xv[i * kInvBatch + tid];
       }
       __syncthreads();
     }
-    // X[j][i] in LDS
-    for (int e = tid; e < r * N; e += kEigThreads) A[e] = gvec[e];
+    // X[j][i] in LDS (fp32 storage, fp64 arithmetic below)
+    for (int e = tid; e < r * N; e += kEigThreads) X[e] = (float)gvec[e];
     __syncthreads();
 
     // modified Gram-Schmidt
     for (int j = 0; j < r; ++j) {
       if (wave == 0) {
         double s = 0.0;
-        for (int i = lane; i < N; i += kWave) s += A[j * N + i] * A[j * N + i];
+        for (int i = lane; i < N; i += kWave) s += (double)X[j * N + i] * X[j * N + i];
         s = wave_sum(s);
         const double f = 1.0 / sqrt(s);
-        for (int i = lane; i < N; i += kWave) A[j * N + i] *= f;
+        for (int i = lane; i < N; i += kWave) X[j * N + i] = (float)(X[j * N + i] * f);
       }
       __syncthreads();
       for (int k = j + 1 + wave; k < r; k += kEigWaves) {
         double s = 0.0;
-        for (int i = lane; i < N; i += kWave) s += A[j * N + i] * A[k * N + i];
+        for (int i = lane; i < N; i += kWave) s += (double)X[j * N + i] * X[k * N + i];
         s = wave_sum(s);
-        for (int i = lane; i < N; i += kWave) A[k * N + i] -= s * A[j * N + i];
+        for (int i = lane; i < N; i += kWave) X[k * N + i] = (float)(X[k * N + i] - s * X[j * N + i]);
       }
       __syncthreads();
     }
@@ -353,9 +467,9 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
         const double* v = &s_rb[c * N];
         for (int j = wave; j < r; j += kEigWaves) {
           double s = 0.0;
-          for (int i = lane; i < m; i += kWave) s += v[i] * A[j * N + k + 1 + i];
+          for (int i = lane; i < m; i += kWave) s += v[i] * X[j * N + k + 1 + i];
           s = wave_sum(s) * beta;
-          for (int i = lane; i < m; i += kWave) A[j * N + k + 1 + i] -= s * v[i];
+          for (int i = lane; i < m; i += kWave) X[j * N + k + 1 + i] = (float)(X[j * N + k + 1 + i] - s * v[i]);
         }
       }
     }
@@ -365,28 +479,25 @@ __global__ __launch_bounds__(kEigThreads) void eig_topr(EigArgs a) {
   // ---- canonical sign and output ----------------------------------------------------------------------------
   for (int j = wave; j < r; j += kEigWaves) {
     double mx = 0.0;
-    for (int i = lane; i < N; i += kWave) mx = fmax(mx, fabs(A[j * N + i]));
+    for (int i = lane; i < N; i += kWave) mx = fmax(mx, fabs((double)X[j * N + i]));
     mx = wave_max(mx);
     const double thr = mx * (1.0 - 9.5367431640625e-07);  // 2^-20
     int first = N;
     for (int i0 = 0; i0 < N; i0 += kWave) {
       const int i = i0 + lane;
-      const uint64_t m = __ballot(i < N && fabs(A[j * N + i]) >= thr);
+      const uint64_t m = __ballot(i < N && fabs((double)X[j * N + i]) >= thr);
       if (m) {
         first = i0 + __ffsll((long long)m) - 1;
         break;
       }
     }
-    const double sgn = (first < N && A[j * N + first] < 0.0) ? -1.0 : 1.0;
-    for (int i = lane; i < N; i += kWave) tg.basis[(size_t)j * N + i] = (float)(sgn * A[j * N + i]);
+    const float sgn = (first < N && X[j * N + first] < 0.0f) ? -1.0f : 1.0f;
+    for (int i = lane; i < N; i += kWave) tg.basis[(size_t)j * N + i] = sgn * X[j * N + i];
     if (lane == 0 && tg.sigma) tg.sigma[j] = (float)sqrt(fmax(s_lam[j], 0.0));
   }
 }
 
-size_t eig_lds_bytes(int n) {
-  const size_t areg = std::max((size_t)n * (n + 1), (size_t)2 * n * kWave);
-  return (areg + 5 * (size_t)n + KVC_MAX_RANK + 8 + (size_t)kReflChunk * (n + 1)) * sizeof(double);
-}
+size_t eig_lds_bytes(int n) { return n == 64 ? EigLds<64>::kTotal : EigLds<128>::kTotal; }
 
 hipError_t launch_eig(const EigArgs& a, hipStream_t stream) {
   if (a.num_units == 0) return hipSuccess;
