@@ -11,6 +11,7 @@
 //   5. Back-transformation by the reflectors, canonical sign (largest-magnitude entry positive, first index on
 //      near-ties), basis rows and sigma = sqrt(lambda) written to the state.
 #include <algorithm>
+#include <type_traits>
 
 #include "kvc_device.h"
 #include "kvc_launch.h"
@@ -96,22 +97,20 @@ __device__ __forceinline__ uint32_t hash3(uint32_t a, uint32_t b, uint32_t c) {
   return h;
 }
 
-// Scalars of one Householder step from x_0 and s = ||x||^2: out = {alpha, v_0, beta} with alpha = -sign(x_0) ||x||,
-// v = x - alpha e_1 and beta = 2 / v^T v (0 when x = 0, which makes the step the identity).
-__device__ __forceinline__ void reflector_scalars(double x0, double s, double* out) {
-  const double nrm = sqrt(s);
-  const double alpha = nrm == 0.0 ? 0.0 : -copysign(nrm, x0);
-  const double v0 = x0 - alpha;
-  const double vtv = (s - x0 * x0) + v0 * v0;
-  out[0] = alpha;
-  out[1] = v0;
-  out[2] = vtv > 0.0 ? 2.0 / vtv : 0.0;
-}
-
 // 1 / q from the hardware reciprocal and one Newton step (relative error about 2^-52).
 __device__ __forceinline__ double recip(double q) {
   const double r0 = __builtin_amdgcn_rcp(q);
   return fma(r0, fma(-q, r0, 1.0), r0);
+}
+
+// Scalars of one Householder step from x_0 and s = ||x||^2: out = {alpha, v_0, beta} with alpha = -sign(x_0) ||x||,
+// v = x - alpha e_1 and beta = 2 / v^T v = 1 / (||x|| (||x|| + |x_0|)) (0 when x = 0: the step is the identity).
+__device__ __forceinline__ void reflector_scalars(double x0, double s, double* out) {
+  const double nrm = sqrt(s);
+  const double alpha = nrm == 0.0 ? 0.0 : -copysign(nrm, x0);
+  out[0] = alpha;
+  out[1] = x0 - alpha;
+  out[2] = nrm == 0.0 ? 0.0 : recip(nrm * (nrm + fabs(x0)));
 }
 
 // Number of eigenvalues of T below x (ratio form of the Sturm sequence; pivots smaller than pivmin are replaced
@@ -142,36 +141,62 @@ __device__ __forceinline__ int sturm_count(const double* sa, const double* sb2, 
 //       group is whole waves, so row skips are uniform; partial[g][R] goes to LDS, summed by the next pivot.
 // Step k's scalars {alpha, v_0, beta} are in s_ab + 4 (k & 1).
 
-// Wave 0.  Before the first step (k = -1) only the scalars of step 0 and s_vw are formed.
+// Wave 0.  Before the first step (k = -1) only the scalars of step 0 and s_vw are formed.  Every LDS load is issued
+// up front (indices stay in range), so the pivot waits for LDS once.
 template <int N>
-__device__ __forceinline__ void tri_pivot(float* A, const double* partial, float4* s_vw, double* s_ab, double* s_b,
-                                          double* refl, double* refl_beta, int k, int lane) {
+__device__ __forceinline__ void tri_pivot(float* A, const double* partial, const double* s_kp, float4* s_vw,
+                                          double* s_ab, double* s_b, double* refl, double* refl_beta, int k, int lane) {
   constexpr int RG = kEigThreads / N;  // row groups of the sweep
   constexpr int Q = N / kWave;         // columns per lane
   const int kn = k + 1;
+  const int kr = k < 0 ? 0 : k;
+  const double* ab = s_ab + 4 * (kr & 1);
+  const double alpha = ab[0], v0 = k < 0 ? 0.0 : ab[1], beta = k < 0 ? 0.0 : ab[2];
+  double psum[Q];
+  float xk[Q], xn[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int C = lane + kWave * q;
+    xk[q] = A[kr * N + C];
+    xn[q] = A[kn * N + C];
+    double sum = 0.0;
+#pragma unroll
+    for (int gi = 0; gi < RG; ++gi) sum += partial[gi * N + C];
+    psum[q] = k < 0 ? 0.0 : sum;  // (before the first step the partials hold nothing yet)
+  }
+  // K = (beta / 2) v^T p = (beta^2 / 2) sum of the sweep's per-wave shares
+  double kk = 0.0;
+#pragma unroll
+  for (int i = 0; i < kEigWaves; ++i) kk += s_kp[i];
+  const double K = k < 0 ? 0.0 : 0.5 * beta * beta * kk;
   double vq[Q], wq[Q];
-  double v0 = 0.0, wR = 0.0;
 #pragma unroll
-  for (int q = 0; q < Q; ++q) vq[q] = wq[q] = 0.0;
+  for (int q = 0; q < Q; ++q) {
+    const int C = lane + kWave * q;
+    vq[q] = k < 0 ? 0.0 : (C > kn ? (double)xk[q] : (C == kn ? v0 : 0.0));
+    wq[q] = C >= kn ? beta * psum[q] - K * vq[q] : 0.0;
+  }
+  const double wR = k < 0 ? 0.0 : lane_value(wq[kn / kWave], kn % kWave);  // w of row k + 1 (its v is v_0)
+  // row k + 1 under step k (same arithmetic as the sweep; columns below k + 1 do not change), its norm beyond the
+  // diagonal, the next scalars; s_vw[C] = {v_C, w_C, v'_C} with v' the next step's v
+  const float v0f = (float)v0, wRf = (float)wR;
+  double s = 0.0;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int C = lane + kWave * q;
+    xn[q] = fmaf(-v0f, (float)wq[q], fmaf(-wRf, (float)vq[q], xn[q]));
+    A[kn * N + C] = xn[q];
+    s += C > kn ? (double)xn[q] * (double)xn[q] : 0.0;
+    s_vw[C] = make_float4((float)vq[q], (float)wq[q], C > kn + 1 ? xn[q] : 0.0f, 0.0f);
+  }
+  s = wave_sum(s);
+  const double x0 = lane_value((double)xn[((kn + 1) % N) / kWave], (kn + 1) % kWave);
+  if (lane == 0) {
+    double* abn = s_ab + 4 * (kn & 1);
+    reflector_scalars(kn + 1 < N ? x0 : 0.0, s, abn);
+    if (kn + 1 < N) s_vw[kn + 1].z = (float)abn[1];  // v'_{k+2} = v_0 of the next step
+  }
   if (k >= 0) {
-    const double* ab = s_ab + 4 * (k & 1);
-    const double alpha = ab[0], beta = ab[2];
-    v0 = ab[1];
-    double pq[Q], kk = 0.0;
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int C = lane + kWave * q;
-      double sum = 0.0;
-#pragma unroll
-      for (int gi = 0; gi < RG; ++gi) sum += partial[gi * N + C];
-      pq[q] = beta * sum;
-      vq[q] = C > kn ? (double)A[k * N + C] : (C == kn ? v0 : 0.0);
-      kk += vq[q] * pq[q];
-    }
-    const double K = 0.5 * beta * wave_sum(kk);
-#pragma unroll
-    for (int q = 0; q < Q; ++q) wq[q] = (lane + kWave * q) >= kn ? pq[q] - K * vq[q] : 0.0;
-    wR = lane_value(wq[kn / kWave], kn % kWave);  // w of row k + 1 (its v is v_0)
     double* refl_k = refl + __builtin_amdgcn_readfirstlane(k * N);
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
@@ -183,58 +208,50 @@ __device__ __forceinline__ void tri_pivot(float* A, const double* partial, float
       refl_beta[k] = beta;
     }
   }
-  // row k + 1 under step k (same arithmetic as the sweep), its norm beyond the diagonal, the next scalars
-  const float v0f = (float)v0, wRf = (float)wR;
-  double s = 0.0;
-  float xq[Q];
-#pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int C = lane + kWave * q;
-    float x = A[kn * N + C];
-    if (k >= 0 && C >= kn) {
-      x = fmaf(-v0f, (float)wq[q], fmaf(-wRf, (float)vq[q], x));
-      A[kn * N + C] = x;
-    }
-    xq[q] = x;
-    s += C > kn ? (double)x * (double)x : 0.0;
-  }
-  s = wave_sum(s);
-  const double x0 = kn + 1 < N ? lane_value((double)xq[((kn + 1) % N) / kWave], (kn + 1) % kWave) : 0.0;
-  if (lane == 0) reflector_scalars(x0, s, s_ab + 4 * (kn & 1));
-#pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int C = lane + kWave * q;
-    s_vw[C] = make_float4((float)vq[q], (float)wq[q], C > kn + 1 ? xq[q] : 0.0f, 0.0f);
-  }
 }
 
 // All threads: rows C > k + 1 under step k (UPD; without UPD, k = -1 and nothing is updated), then the row-group
-// partial sums of A22 v' for step k + 1 (v'_{k+2} = v_0 of step k + 1, v'_C = x'_C beyond).
+// partial sums of A22 v' for step k + 1 and each wave's share of v'^T (A22 v').
 template <int N, bool UPD>
-__device__ __forceinline__ void tri_sweep(float* A, double* partial, const float4* s_vw, const double* s_ab, int k,
-                                          int tid) {
+__device__ __forceinline__ void tri_sweep(float* A, double* partial, double* s_kp, const float4* s_vw, int k,
+                                          int tid, int lane, int wave) {
   constexpr int RG = kEigThreads / N;
   constexpr int RPT = N / RG;
-  const int R = tid & (N - 1), g = tid / N;
+  const int R = tid & (N - 1);
+  const int g = __builtin_amdgcn_readfirstlane(tid / N);  // uniform: a row group is whole waves
   const int kn = k + 1;
   const float4 vwR = s_vw[R];
-  const float v0n = (float)s_ab[4 * (kn & 1) + 1];
-  const bool col_live = R > kn;
-  double acc = 0.0;
-#pragma unroll 4
-  for (int t = 0; t < RPT; ++t) {
-    const int C = g + RG * t;
-    if (C <= kn) continue;  // uniform: a row group is whole waves
-    const float4 vwC = s_vw[C];
-    float a = A[C * N + R];
-    if (UPD) {
-      a = fmaf(-vwC.x, vwR.y, fmaf(-vwC.y, vwR.x, a));
-      if (col_live) A[C * N + R] = a;
+  // first live row of this thread: g + RG t > k + 1.  Entries of eliminated columns (R <= k + 1) are updated too
+  // (with v_R = w_R = 0 they do not change, and column k + 1 is not read again), so that stores need no mask.
+  const int t0 = kn < g ? 0 : (kn - g) / RG + 1;
+  float acc = 0.0f;
+  // rows in batches of four: every load of a batch is issued before its stores
+  auto rows = [&](int t, auto nb) {
+    constexpr int NB = decltype(nb)::value;
+    float4 vwC[NB];
+    float a[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int C = g + RG * (t + j);
+      vwC[j] = s_vw[C];
+      a[j] = A[C * N + R];
     }
-    const float vpC = C == kn + 1 ? v0n : vwC.z;
-    acc += (double)a * (double)vpC;
-  }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int C = g + RG * (t + j);
+      if (UPD) {
+        a[j] = fmaf(-vwC[j].x, vwR.y, fmaf(-vwC[j].y, vwR.x, a[j]));
+        A[C * N + R] = a[j];
+      }
+      acc = fmaf(a[j], vwC[j].z, acc);
+    }
+  };
+  int t = t0;
+  for (; t + 4 <= RPT; t += 4) rows(t, std::integral_constant<int, 4>());
+  for (; t < RPT; ++t) rows(t, std::integral_constant<int, 1>());
   partial[g * N + R] = acc;
+  const double kp = group_sum<kWave>((double)acc * (double)vwR.z);
+  if (lane == kWave - 1) s_kp[wave] = kp;
 }
 
 // LDS layout (bytes): the matrix region MREG holds, in turn, G / the trailing matrix as fp32 [N][N] (phases 1-2),
@@ -248,8 +265,8 @@ struct EigLds {
   static constexpr size_t kX = (size_t)KVC_MAX_RANK * N * 4;
   static constexpr size_t kMreg = ((kMat > kScratch ? (kMat > kX ? kMat : kX) : (kScratch > kX ? kScratch : kX)) +
                                    15) / 16 * 16;
-  // s_a, s_b [N]; s_lam [KVC_MAX_RANK]; s_ab [2][4]; s_misc [8]; s_vw float4 [N] (later b^2 [N])
-  static constexpr size_t kSmall = (size_t)(2 * N + KVC_MAX_RANK + 8 + 8) * 8 + (size_t)N * 16;
+  // s_a, s_b [N]; s_lam [KVC_MAX_RANK]; s_ab [2][4]; s_kp [kEigWaves]; s_misc [8]; s_vw float4 [N] (later b^2 [N])
+  static constexpr size_t kSmall = (size_t)(2 * N + KVC_MAX_RANK + 8 + kEigWaves + 8) * 8 + (size_t)N * 16;
   static constexpr size_t kPartial = (size_t)(kEigThreads / N) * N * 8;
   static constexpr size_t kReflStage = (size_t)kReflChunk * (N + 1) * 8;
   static constexpr size_t kStage = kPartial > kReflStage ? kPartial : kReflStage;
@@ -271,7 +288,8 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   double* s_b = s_a + N;                    // off-diagonal of T: b[i] couples i and i + 1
   double* s_lam = s_b + N;                  // eigenvalues, descending
   double* s_ab = s_lam + KVC_MAX_RANK;      // reflector scalars {alpha, v_0, beta, -}, by step parity [2][4]
-  double* s_misc = s_ab + 8;                // scalars
+  double* s_kp = s_ab + 8;                  // per-wave shares of v^T A22 v from the sweep [kEigWaves]
+  double* s_misc = s_kp + kEigWaves;        // scalars
   float4* s_vw = reinterpret_cast<float4*>(s_misc + 8);  // {v_C, w_C, x'_C, -} of the current step
   double* s_b2 = reinterpret_cast<double*>(s_vw);        // b^2 (after the tridiagonalisation)
   double* partial = reinterpret_cast<double*>(base + Lay::kMreg + Lay::kSmall);  // sweep partials [RG][N]
@@ -303,14 +321,14 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   __syncthreads();
 
   // ---- 2. Householder tridiagonalisation -----------------------------------------------------------------------
-  if (wave == 0) tri_pivot<N>(A, partial, s_vw, s_ab, s_b, refl, refl_beta, -1, lane);
+  if (wave == 0) tri_pivot<N>(A, partial, s_kp, s_vw, s_ab, s_b, refl, refl_beta, -1, lane);
   __syncthreads();
-  tri_sweep<N, false>(A, partial, s_vw, s_ab, -1, tid);
+  tri_sweep<N, false>(A, partial, s_kp, s_vw, -1, tid, lane, wave);
   __syncthreads();
   for (int k = 0; k < N - 2; ++k) {
-    if (wave == 0) tri_pivot<N>(A, partial, s_vw, s_ab, s_b, refl, refl_beta, k, lane);
+    if (wave == 0) tri_pivot<N>(A, partial, s_kp, s_vw, s_ab, s_b, refl, refl_beta, k, lane);
     __syncthreads();
-    tri_sweep<N, true>(A, partial, s_vw, s_ab, k, tid);
+    tri_sweep<N, true>(A, partial, s_kp, s_vw, k, tid, lane, wave);
     __syncthreads();
   }
   for (int i = tid; i < N; i += kEigThreads) s_a[i] = A[i * LD + i];
