@@ -20,7 +20,7 @@ namespace kvc {
 
 constexpr int kEigThreads = 1024;
 constexpr int kEigWaves = kEigThreads / kWave;
-constexpr int kReflChunk = 8;   // reflectors staged in LDS per back-transformation chunk
+constexpr int kReflChunk = 16;  // reflectors staged in LDS per back-transformation chunk
 constexpr int kInvBatch = 32;   // eigenvectors per inverse-iteration batch (one lane each)
 
 // fp64 cross-lane moves by DPP (two 32-bit halves); lanes whose row is masked off receive 0.
@@ -60,6 +60,33 @@ __device__ __forceinline__ double wave_max(double x) {
   x = fmax(x, dpp64<kDppRor2>(x));
   x = fmax(x, dpp64<kDppRor1>(x));
   return fmax(fmax(lane_value(x, 0), lane_value(x, 16)), fmax(lane_value(x, 32), lane_value(x, 48)));
+}
+
+// Reductions over groups of eight consecutive lanes (every lane of the group gets the result; fp32 addition is
+// commutative, so all eight agree).
+template <int CTRL>
+__device__ __forceinline__ float dpp32(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ int dpp32i(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141;
+__device__ __forceinline__ float sum8(float x) {
+  x += dpp32<kDppXor1>(x);
+  x += dpp32<kDppXor2>(x);
+  return x + dpp32<kDppHalfMirror>(x);
+}
+__device__ __forceinline__ float max8(float x) {
+  x = fmaxf(x, dpp32<kDppXor1>(x));
+  x = fmaxf(x, dpp32<kDppXor2>(x));
+  return fmaxf(x, dpp32<kDppHalfMirror>(x));
+}
+__device__ __forceinline__ int min8(int x) {
+  x = min(x, dpp32i<kDppXor1>(x));
+  x = min(x, dpp32i<kDppXor2>(x));
+  return min(x, dpp32i<kDppHalfMirror>(x));
 }
 
 struct UnitTarget {
@@ -268,7 +295,7 @@ struct EigLds {
   // s_a, s_b [N]; s_lam [KVC_MAX_RANK]; s_ab [2][4]; s_kp [kEigWaves]; s_misc [8]; s_vw float4 [N] (later b^2 [N])
   static constexpr size_t kSmall = (size_t)(2 * N + KVC_MAX_RANK + 8 + kEigWaves + 8) * 8 + (size_t)N * 16;
   static constexpr size_t kPartial = (size_t)(kEigThreads / N) * N * 8;
-  static constexpr size_t kReflStage = (size_t)kReflChunk * (N + 1) * 8;
+  static constexpr size_t kReflStage = (size_t)kReflChunk * (N + 1) * 4;
   static constexpr size_t kStage = kPartial > kReflStage ? kPartial : kReflStage;
   static constexpr size_t kTotal = kMreg + kSmall + kStage;
 };
@@ -293,8 +320,8 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   float4* s_vw = reinterpret_cast<float4*>(s_misc + 8);  // {v_C, w_C, x'_C, -} of the current step
   double* s_b2 = reinterpret_cast<double*>(s_vw);        // b^2 (after the tridiagonalisation)
   double* partial = reinterpret_cast<double*>(base + Lay::kMreg + Lay::kSmall);  // sweep partials [RG][N]
-  double* s_rb = partial;                   // reflector chunk [kReflChunk][N] (back-transformation)
-  double* s_rbeta = s_rb + kReflChunk * N;
+  float* s_rb = reinterpret_cast<float*>(partial);  // reflector chunk fp32 [kReflChunk][N] (back-transformation)
+  float* s_rbeta = s_rb + kReflChunk * N;
 
   const int u = blockIdx.x;
   const UnitTarget tg = eig_target(a, u);
@@ -366,9 +393,9 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
       while (rp < r) rp <<= 1;
       // lanes per eigenvalue (a power of two dividing 64); 16 trades latency (iterations) against the fp64 work
       const int P = min(16, kEigThreads / rp);
-      // each step shrinks the bracket (P + 1)-fold; stop at 2^-44 of the Gershgorin interval, far below the
+      // each step shrinks the bracket (P + 1)-fold; stop below 2^-32 of the Gershgorin interval, under the
       // perturbation that fp32 storage of the matrix already carries
-      const int iters = P >= 16 ? 11 : P >= 8 ? 14 : P >= 4 ? 19 : P >= 2 ? 28 : 44;
+      const int iters = P >= 16 ? 8 : P >= 8 ? 11 : P >= 4 ? 14 : P >= 2 ? 21 : 32;
       const int grp = tid / P, s = tid - grp * P;
       const int kasc = N - 1 - grp;                  // ascending index of the target eigenvalue
       const double pivmin = s_misc[4];
@@ -464,54 +491,87 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
       __syncthreads();
     }
 
-    // ---- 5. back-transformation X <- H_0 H_1 ... H_{N-3} X ---------------------------------------------
-    // Reflectors are staged kReflChunk at a time; each wave owns whole columns of X, so the steps inside a chunk
-    // need no barrier.
+    __syncthreads();
+  }
+
+  // ---- 5. back-transformation X <- H_0 H_1 ... H_{N-3} X, canonical sign, output ---------------------------------
+  // Eight lanes per vector: vector jv = tid / 8 keeps positions sub * PB .. sub * PB + PB - 1 (sub = tid % 8) in fp32
+  // registers.  Reflectors are staged kReflChunk at a time at their absolute positions (zero up to k), so the steps
+  // inside a chunk need no barrier.
+  constexpr int PB = N / 8;
+  const int jv = tid >> 3, sub = tid & 7;
+  const bool wave_act = wave * (kWave / 8) < r;  // uniform
+  float xr[PB];
+  if (jv < r) {
+#pragma unroll
+    for (int i = 0; i < PB; i += 4) {
+      const float4 x4 = *reinterpret_cast<const float4*>(&X[jv * N + sub * PB + i]);
+      xr[i] = x4.x;
+      xr[i + 1] = x4.y;
+      xr[i + 2] = x4.z;
+      xr[i + 3] = x4.w;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < PB; ++i) xr[i] = 0.0f;
+  }
+  if (tnorm != 0.0) {
     for (int kc = N - 3; kc >= 0; kc -= kReflChunk) {
       const int nk = min(kReflChunk, kc + 1);
       __syncthreads();
       for (int e = tid; e < nk * N; e += kEigThreads) {
-        const int c = e / N, i = e - c * N;
+        const int c = e / N, pos = e - c * N;
         const int k = kc - c;
-        s_rb[c * N + i] = i < N - k - 1 ? refl[k * N + i] : 0.0;
+        s_rb[c * N + pos] = pos > k ? (float)refl[k * N + pos - k - 1] : 0.0f;
       }
-      for (int c = tid; c < nk; c += kEigThreads) s_rbeta[c] = refl_beta[kc - c];
+      for (int c = tid; c < nk; c += kEigThreads) s_rbeta[c] = (float)refl_beta[kc - c];
       __syncthreads();
-      for (int c = 0; c < nk; ++c) {
-        const int k = kc - c;
-        const int m = N - k - 1;
-        const double beta = s_rbeta[c];
-        if (beta == 0.0) continue;
-        const double* v = &s_rb[c * N];
-        for (int j = wave; j < r; j += kEigWaves) {
-          double s = 0.0;
-          for (int i = lane; i < m; i += kWave) s += v[i] * X[j * N + k + 1 + i];
-          s = wave_sum(s) * beta;
-          for (int i = lane; i < m; i += kWave) X[j * N + k + 1 + i] = (float)(X[j * N + k + 1 + i] - s * v[i]);
+      if (wave_act) {
+        for (int c = 0; c < nk; ++c) {
+          const float beta = s_rbeta[c];
+          float v[PB];
+#pragma unroll
+          for (int i = 0; i < PB; i += 4) {
+            const float4 v4 = *reinterpret_cast<const float4*>(&s_rb[c * N + sub * PB + i]);
+            v[i] = v4.x;
+            v[i + 1] = v4.y;
+            v[i + 2] = v4.z;
+            v[i + 3] = v4.w;
+          }
+          float d0 = 0.0f, d1 = 0.0f;
+#pragma unroll
+          for (int i = 0; i < PB; i += 2) {
+            d0 = fmaf(xr[i], v[i], d0);
+            d1 = fmaf(xr[i + 1], v[i + 1], d1);
+          }
+          const float sc = beta * sum8(d0 + d1);
+#pragma unroll
+          for (int i = 0; i < PB; ++i) xr[i] = fmaf(-sc, v[i], xr[i]);
         }
       }
     }
-    __syncthreads();
   }
 
-  // ---- canonical sign and output ----------------------------------------------------------------------------
-  for (int j = wave; j < r; j += kEigWaves) {
-    double mx = 0.0;
-    for (int i = lane; i < N; i += kWave) mx = fmax(mx, fabs((double)X[j * N + i]));
-    mx = wave_max(mx);
-    const double thr = mx * (1.0 - 9.5367431640625e-07);  // 2^-20
-    int first = N;
-    for (int i0 = 0; i0 < N; i0 += kWave) {
-      const int i = i0 + lane;
-      const uint64_t m = __ballot(i < N && fabs((double)X[j * N + i]) >= thr);
-      if (m) {
-        first = i0 + __ffsll((long long)m) - 1;
-        break;
-      }
+  // canonical sign: the largest-magnitude entry positive; entries within 2^-20 of it count as ties, the first wins
+  if (wave_act) {
+    float mx = 0.0f;
+#pragma unroll
+    for (int i = 0; i < PB; ++i) mx = fmaxf(mx, fabsf(xr[i]));
+    mx = max8(mx);
+    const float thr = (float)((double)mx * (1.0 - 9.5367431640625e-07));
+    int key = 2 * N;  // 2 * position + sign bit of the first entry at or above the threshold
+#pragma unroll
+    for (int i = PB - 1; i >= 0; --i)
+      if (fabsf(xr[i]) >= thr) key = 2 * (sub * PB + i) + (xr[i] < 0.0f ? 1 : 0);
+    key = min8(key);
+    const float sgn = (key < 2 * N && (key & 1)) ? -1.0f : 1.0f;
+    if (jv < r) {
+#pragma unroll
+      for (int i = 0; i < PB; i += 4)
+        *reinterpret_cast<float4*>(&tg.basis[(size_t)jv * N + sub * PB + i]) =
+            make_float4(sgn * xr[i], sgn * xr[i + 1], sgn * xr[i + 2], sgn * xr[i + 3]);
+      if (sub == 0 && tg.sigma) tg.sigma[jv] = (float)sqrt(fmax(s_lam[jv], 0.0));
     }
-    const float sgn = (first < N && X[j * N + first] < 0.0f) ? -1.0f : 1.0f;
-    for (int i = lane; i < N; i += kWave) tg.basis[(size_t)j * N + i] = sgn * X[j * N + i];
-    if (lane == 0 && tg.sigma) tg.sigma[j] = (float)sqrt(fmax(s_lam[j], 0.0));
   }
 }
 
