@@ -203,6 +203,181 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_mfma(FitArgs a) {
   gram_all_stores<D>(P, acc, g, n, std::make_integer_sequence<int, NT>{});
 }
 
+// bf16 Gram, head_dim 128, rows staged through LDS: the same wave-per-partial Gram, but the rows of the next two
+// 32-token steps are loaded straight into a per-wave LDS ring (global_load_lds, 16 bytes per lane), so that twice
+// the bytes of the register pipeline are in flight while only the step being multiplied occupies registers.
+// Each lane reads back exactly the bytes its own loads wrote, so the ring needs no barrier, only vmcnt waits; the
+// read-back is inline assembly because the compiler would otherwise wait for every outstanding LDS load before
+// each LDS read.  Table entries are read with scalar loads (a 32-token step touches at most three blocks of at
+// least 16 tokens), so that using them does not wait on the row loads either.
+constexpr int kGramRing = 2;                          // steps in flight per wave
+constexpr int kGramSlotBytes = 16 * kWave * 16;       // 8 dst + 8 src loads of 16 bytes per lane
+constexpr int kGramTabMax = 768;                      // table entries per partial (dst and src)
+constexpr size_t kGramLdsBytes = (size_t)kFitWaves * (kGramRing * kGramSlotBytes + 2 * kGramTabMax * 4);
+
+// The 16 row segments of one ring slot (8 dst, then 8 src), each 16 bytes at lane * 16 of a 1 KB block.
+__device__ __forceinline__ void gram_ring_read(uint32_t addr, u32x4* d, u32x4* s) {
+  asm volatile(
+      "ds_read_b128 %0, %16\n\tds_read_b128 %1, %16 offset:1024\n\t"
+      "ds_read_b128 %2, %16 offset:2048\n\tds_read_b128 %3, %16 offset:3072\n\t"
+      "ds_read_b128 %4, %16 offset:4096\n\tds_read_b128 %5, %16 offset:5120\n\t"
+      "ds_read_b128 %6, %16 offset:6144\n\tds_read_b128 %7, %16 offset:7168\n\t"
+      "ds_read_b128 %8, %16 offset:8192\n\tds_read_b128 %9, %16 offset:9216\n\t"
+      "ds_read_b128 %10, %16 offset:10240\n\tds_read_b128 %11, %16 offset:11264\n\t"
+      "ds_read_b128 %12, %16 offset:12288\n\tds_read_b128 %13, %16 offset:13312\n\t"
+      "ds_read_b128 %14, %16 offset:14336\n\tds_read_b128 %15, %16 offset:15360\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(d[0]), "=&v"(d[1]), "=&v"(d[2]), "=&v"(d[3]), "=&v"(d[4]), "=&v"(d[5]), "=&v"(d[6]), "=&v"(d[7]),
+        "=&v"(s[0]), "=&v"(s[1]), "=&v"(s[2]), "=&v"(s[3]), "=&v"(s[4]), "=&v"(s[5]), "=&v"(s[6]), "=&v"(s[7])
+      : "v"(addr)
+      : "memory");
+}
+
+template <bool DELTA>
+__global__ __launch_bounds__(kFitThreads) void gram_bf16_ring(FitArgs a) {
+  constexpr int D = 128, FT = 8, NT = FT * (FT + 1) / 2, STEP = 32;
+  constexpr int LPS = DELTA ? 16 : 8;  // loads per step and lane
+  extern __shared__ __attribute__((aligned(16))) unsigned char gram_lds[];
+  const FitUnit f = fit_unit(a);
+  const kvc_item* itp = a.items + f.item;
+  const int r = itp->state.rank;
+  const int Ts = itp->state.num_tokens;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int part = blockIdx.x * kFitWaves + wave;
+  const int t_begin = part * a.part_tokens;
+  if (r == 0 || t_begin >= Ts) return;  // per wave: the kernel has no barrier
+  const int t_end = min(Ts, t_begin + a.part_tokens);
+  const int g = lane >> 4, n = lane & 15;
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const uint16_t* pool = static_cast<const uint16_t*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
+  const int shift = a.pv.block_shift;
+  const int bmask = (1 << shift) - 1;
+  unsigned char* ring = gram_lds + wave * (kGramRing * kGramSlotBytes);
+
+  f32x4 acc[NT];
+#pragma unroll
+  for (int q = 0; q < NT; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // The block-table entries of the wave's whole token range are copied once, before the first row load, into the
+  // wave's LDS table (lane-parallel); a step reads its (at most three) entries back with scalar-addressed LDS reads,
+  // so the loop issues no global memory operation besides the row loads.
+  struct Tab {
+    int32_t lbs, lbe, off;
+    uint32_t lds;  // LDS byte address of the wave's copy
+  };
+  int32_t* tab_lds = reinterpret_cast<int32_t*>(gram_lds + kFitWaves * kGramRing * kGramSlotBytes) +
+                     wave * 2 * kGramTabMax;
+  auto load_tab = [&](const int32_t* tab, int32_t off, int which) {
+    Tab tb;
+    tb.off = __builtin_amdgcn_readfirstlane(off);
+    tb.lbs = (tb.off + t_begin) >> shift;
+    tb.lbe = (tb.off + t_end - 1) >> shift;
+    int32_t* dstp = tab_lds + which * kGramTabMax;
+    for (int i = lane; i < kGramTabMax; i += kWave) {
+      const int32_t lb = tb.lbs + i;
+      dstp[i] = lb <= tb.lbe ? (tab ? tab[lb] : lb) : -1;
+    }
+    tb.lds = (uint32_t)(uintptr_t)dstp;
+    return tb;
+  };
+  const Tab tdst = load_tab(dst_tab, itp->dst_offset, 0);
+  Tab tsrc;
+  if (DELTA) tsrc = load_tab(src_tab, itp->src_offset, 1);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the tables are in LDS before any read-back
+  // entries lb0, lb0 + 1, lb0 + 2 (lb0 uniform); entries past the range read as -1
+  auto entries = [&](const Tab& tb, int32_t lb0, int32_t& e0, int32_t& e1, int32_t& e2) {
+    const int32_t i0 = min(lb0 - tb.lbs, kGramTabMax - 3);
+    const uint32_t addr = tb.lds + 4u * (uint32_t)i0;
+    asm volatile(
+        "ds_read_b32 %0, %3\n\tds_read_b32 %1, %3 offset:4\n\tds_read_b32 %2, %3 offset:8\n\ts_waitcnt lgkmcnt(0)"
+        : "=&v"(e0), "=&v"(e1), "=&v"(e2)
+        : "v"(addr)
+        : "memory");
+    e0 = lb0 <= tb.lbe ? e0 : -1;
+    e1 = lb0 + 1 <= tb.lbe ? e1 : -1;
+    e2 = lb0 + 2 <= tb.lbe ? e2 : -1;
+  };
+
+  // Loads of one step's rows into an LDS slot; returns the validity mask (bit j: token t0 + 8 g + j).  A lane's
+  // eight tokens touch at most two blocks; the row address of token j is the address of the lane's first token
+  // plus j token strides, or, past the block boundary, the start of the next block plus the remaining strides.
+  const int64_t head_off = (int64_t)f.head * a.pv.head_stride + FT * n;
+  auto issue_rows = [&](const Tab& tb, int t0, unsigned char* dst_lds) -> uint32_t {
+    const int32_t p0 = tb.off + t0;
+    const int32_t lb0 = p0 >> shift;
+    int32_t e0, e1, e2;
+    entries(tb, lb0, e0, e1, e2);
+    const int32_t pl = p0 + 8 * g;                    // position of the lane's first token
+    const int bi = (pl >> shift) - lb0;               // its block among the step's three
+    const int32_t blk_a = bi == 0 ? e0 : (bi == 1 ? e1 : e2);
+    const int32_t blk_b = bi == 0 ? e1 : e2;          // the next block
+    const int32_t slot_a = pl & bmask;
+    const int ja = (int)min(8, (1 << shift) - slot_a);  // tokens of the lane left in block a
+    const bool ok_a = blk_a >= 0 && blk_a < a.pv.num_blocks, ok_b = blk_b >= 0 && blk_b < a.pv.num_blocks;
+    const uint16_t* base_a = pool + (int64_t)(ok_a ? blk_a : 0) * a.pv.block_stride +
+                             (int64_t)slot_a * a.pv.token_stride + head_off;
+    const uint16_t* base_b = pool + (int64_t)(ok_b ? blk_b : 0) * a.pv.block_stride + head_off;
+    const int tl = t_end - (t0 + 8 * g);              // tokens of the lane before t_end
+    uint32_t m = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool in_a = j < ja;
+      const uint16_t* src = in_a ? base_a + (int64_t)j * a.pv.token_stride
+                                 : base_b + (int64_t)(j - ja) * a.pv.token_stride;
+      const bool ok = j < tl && (in_a ? ok_a : ok_b);
+      __builtin_amdgcn_global_load_lds(ok ? src : pool, dst_lds + j * (kWave * 16), 16, 0, 0);
+      m |= ok ? 1u << j : 0u;
+    }
+    return m;
+  };
+  auto issue = [&](int sl, int t0) -> uint32_t {
+    unsigned char* base = ring + sl * kGramSlotBytes;
+    uint32_t m = issue_rows(tdst, t0, base);
+    if (DELTA) m |= issue_rows(tsrc, t0, base + 8 * kWave * 16) << 8;
+    return m;
+  };
+
+  uint32_t mask[kGramRing];
+  mask[0] = issue(0, t_begin);
+  mask[1] = t_begin + STEP < t_end ? issue(1, t_begin + STEP) : 0u;
+  int sl = 0;
+  for (int t0 = t_begin; t0 < t_end; t0 += STEP) {
+    // this step's loads are done once at most the next step's are outstanding
+    if (t0 + STEP < t_end) __builtin_amdgcn_s_waitcnt(LPS == 16 ? 0x4F70 : 0x0F78);  // vmcnt(LPS)
+    else __builtin_amdgcn_s_waitcnt(0x0F70);                                         // vmcnt(0)
+    u32x4 rd[8], rs[8];
+    gram_ring_read((uint32_t)(uintptr_t)(ring + sl * kGramSlotBytes) + lane * 16, rd, rs);
+    const uint32_t m = sl ? mask[1] : mask[0];
+    u32x4 zh[8], zl[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const u32x4 dv = (m >> j) & 1 ? rd[j] : u32x4{0u, 0u, 0u, 0u};
+      const u32x4 sv = (DELTA && ((m >> (8 + j)) & 1)) ? rs[j] : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        uint32_t h, l;
+        split_bf16x2(bf16_lo_to_f32(dv[w]) - bf16_lo_to_f32(sv[w]), bf16_hi_to_f32(dv[w]) - bf16_hi_to_f32(sv[w]),
+                     h, l);
+        zh[j][w] = h;
+        zl[j][w] = l;
+      }
+    }
+    // the slot is free again (its reads completed above): refill it with the step after next
+    if (t0 + 2 * STEP < t_end) {
+      const uint32_t mn = issue(sl, t0 + 2 * STEP);
+      if (sl) mask[1] = mn;
+      else mask[0] = mn;
+    }
+    gram_all_tiles<D>(acc, zh, zl, std::make_integer_sequence<int, NT>{});
+    sl ^= 1;
+  }
+  const int64_t lu = fit_linear_unit(a, f);
+  float* P = a.partials + ((size_t)lu * a.max_parts + part) * D * D;
+  gram_all_stores<D>(P, acc, g, n, std::make_integer_sequence<int, NT>{});
+}
+
 // ---------------------------------------------------------------------------------------------------------------
 // Gram, fp32 caches (VALU, fp32 accumulation)
 // ---------------------------------------------------------------------------------------------------------------
@@ -440,8 +615,19 @@ hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hip
   const int D = a.pv.head_dim;
   if (dtype == KVC_BF16) {
     dim3 grid((a.max_parts + kFitWaves - 1) / kFitWaves, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
-    if (D == 64) hipLaunchKernelGGL(gram_bf16_mfma<64>, grid, dim3(kFitThreads), 0, stream, a);
-    else hipLaunchKernelGGL(gram_bf16_mfma<128>, grid, dim3(kFitThreads), 0, stream, a);
+    if (D == 128 && a.pv.block_shift >= 4 && a.part_tokens / a.pv.block_size + 3 <= kGramTabMax) {
+      // LDS-staged rows (block sizes of at least 16 tokens, a partial's table fits the wave's LDS copy)
+      const bool delta = a.mode == KVC_FIT_DELTA;
+      const void* fn = delta ? (const void*)gram_bf16_ring<true> : (const void*)gram_bf16_ring<false>;
+      hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGramLdsBytes);
+      if (e != hipSuccess) return e;
+      if (delta) hipLaunchKernelGGL(gram_bf16_ring<true>, grid, dim3(kFitThreads), kGramLdsBytes, stream, a);
+      else hipLaunchKernelGGL(gram_bf16_ring<false>, grid, dim3(kFitThreads), kGramLdsBytes, stream, a);
+    } else if (D == 64) {
+      hipLaunchKernelGGL(gram_bf16_mfma<64>, grid, dim3(kFitThreads), 0, stream, a);
+    } else {
+      hipLaunchKernelGGL(gram_bf16_mfma<128>, grid, dim3(kFitThreads), 0, stream, a);
+    }
   } else {
     dim3 grid(a.max_parts, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
     if (D == 64) hipLaunchKernelGGL(gram_f32_valu<64>, grid, dim3(kFitThreads), 0, stream, a);
