@@ -211,6 +211,22 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_mfma(FitArgs a) {
 // each LDS read.  Table entries are read with scalar loads (a 32-token step touches at most three blocks of at
 // least 16 tokens), so that using them does not wait on the row loads either.
 constexpr int kGramRing = 2;                          // steps in flight per wave
+
+// The bf16 pair (-1, 0) or (0, -1) in a scalar register: dot2 with it subtracts the low or the high element.  The
+// move is opaque to the compiler, which would otherwise fold the low-element constant into an inline constant that
+// the hardware reads as the 32-bit float -1.0, i.e. the pair (0, -1).
+// A 32-bit word as a bf16 pair.  (Through memcpy: a bit_cast of a vector element to bf16x2 inside an unrolled loop
+// has been seen to lose the element index in code generation.)
+__device__ __forceinline__ bf16x2 as_bf16x2(uint32_t w) {
+  bf16x2 v;
+  __builtin_memcpy(&v, &w, sizeof(v));
+  return v;
+}
+__device__ __forceinline__ bf16x2 bf16_pair_const(uint32_t bits) {
+  uint32_t v;
+  asm volatile("s_mov_b32 %0, %1" : "=s"(v) : "i"(bits));
+  return __builtin_bit_cast(bf16x2, v);
+}
 constexpr int kGramSlotBytes = 16 * kWave * 16;       // 8 dst + 8 src loads of 16 bytes per lane
 constexpr int kGramTabMax = 768;                      // table entries per partial (dst and src)
 constexpr size_t kGramLdsBytes = (size_t)kFitWaves * (kGramRing * kGramSlotBytes + 2 * kGramTabMax * 4);
@@ -238,13 +254,24 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_ring(FitArgs a) {
   constexpr int D = 128, FT = 8, NT = FT * (FT + 1) / 2, STEP = 32;
   constexpr int LPS = DELTA ? 16 : 8;  // loads per step and lane
   extern __shared__ __attribute__((aligned(16))) unsigned char gram_lds[];
-  const FitUnit f = fit_unit(a);
+  // block (part, kv x head group, item x layer): the four waves take four heads of the same token range, so that a
+  // workgroup reads 4 x 256 contiguous bytes of each token row
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int H = a.pv.num_kv_heads;
+  const int HG = (H + kFitWaves - 1) / kFitWaves;
+  FitUnit f;
+  f.item = blockIdx.z / a.num_layers;
+  f.lrel = blockIdx.z - f.item * a.num_layers;
+  f.layer = a.layer_begin + f.lrel;
+  f.kv = blockIdx.y / HG;
+  f.head = (blockIdx.y - f.kv * HG) * kFitWaves + wave;
+  if (f.head >= H) return;
+  f.unit = unit_index(f.layer, f.kv, f.head, H);
   const kvc_item* itp = a.items + f.item;
   const int r = itp->state.rank;
   const int Ts = itp->state.num_tokens;
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int part = blockIdx.x * kFitWaves + wave;
+  const int part = blockIdx.x;
   const int t_begin = part * a.part_tokens;
   if (r == 0 || t_begin >= Ts) return;  // per wave: the kernel has no barrier
   const int t_end = min(Ts, t_begin + a.part_tokens);
@@ -339,40 +366,83 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_ring(FitArgs a) {
     return m;
   };
 
-  uint32_t mask[kGramRing];
-  mask[0] = issue(0, t_begin);
-  mask[1] = t_begin + STEP < t_end ? issue(1, t_begin + STEP) : 0u;
-  int sl = 0;
-  for (int t0 = t_begin; t0 < t_end; t0 += STEP) {
-    // this step's loads are done once at most the next step's are outstanding
-    if (t0 + STEP < t_end) __builtin_amdgcn_s_waitcnt(LPS == 16 ? 0x4F70 : 0x0F78);  // vmcnt(LPS)
-    else __builtin_amdgcn_s_waitcnt(0x0F70);                                         // vmcnt(0)
-    u32x4 rd[8], rs[8];
-    gram_ring_read((uint32_t)(uintptr_t)(ring + sl * kGramSlotBytes) + lane * 16, rd, rs);
-    const uint32_t m = sl ? mask[1] : mask[0];
-    u32x4 zh[8], zl[8];
+  // Z of a step into bf16 hi/lo segments (rows outside the range read as zero).  With dot2 (two bf16 products and
+  // an fp32 addend, rounded once): z = d - s and the residual z - hi are one instruction per element; both are the
+  // same single roundings as fp32 subtractions (the residual is exact).
+  const bf16x2 kBf16NegLo = bf16_pair_const(0x0000BF80u), kBf16NegHi = bf16_pair_const(0xBF800000u);
+  auto form = [&](const u32x4* rd, const u32x4* rs, uint32_t m, u32x4* zh, u32x4* zl) {
+    const bool full = __builtin_amdgcn_ballot_w64(m != (DELTA ? 0xFFFFu : 0xFFu)) == 0;  // uniform
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const u32x4 dv = (m >> j) & 1 ? rd[j] : u32x4{0u, 0u, 0u, 0u};
-      const u32x4 sv = (DELTA && ((m >> (8 + j)) & 1)) ? rs[j] : u32x4{0u, 0u, 0u, 0u};
+      u32x4 dv = rd[j], sv = rs[j];
+      if (!full) {
+        dv = (m >> j) & 1 ? dv : u32x4{0u, 0u, 0u, 0u};
+        sv = (DELTA && ((m >> (8 + j)) & 1)) ? sv : u32x4{0u, 0u, 0u, 0u};
+      }
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        uint32_t h, l;
-        split_bf16x2(bf16_lo_to_f32(dv[w]) - bf16_lo_to_f32(sv[w]), bf16_hi_to_f32(dv[w]) - bf16_hi_to_f32(sv[w]),
-                     h, l);
+        float z0 = __uint_as_float(dv[w] << 16), z1 = __uint_as_float(dv[w] & 0xffff0000u);
+        if (DELTA) {
+          const bf16x2 s2 = as_bf16x2(sv[w]);
+          z0 = __builtin_amdgcn_fdot2_f32_bf16(s2, kBf16NegLo, z0, false);  // d0 - s0
+          z1 = __builtin_amdgcn_fdot2_f32_bf16(s2, kBf16NegHi, z1, false);  // d1 - s1
+        }
+        const uint32_t h = pack_bf16x2(z0, z1);
+        const bf16x2 h2 = as_bf16x2(h);
+        const float r0 = __builtin_amdgcn_fdot2_f32_bf16(h2, kBf16NegLo, z0, false);  // z0 - hi0 (exact)
+        const float r1 = __builtin_amdgcn_fdot2_f32_bf16(h2, kBf16NegHi, z1, false);  // z1 - hi1 (exact)
         zh[j][w] = h;
-        zl[j][w] = l;
+        zl[j][w] = pack_bf16x2(r0, r1);
       }
     }
-    // the slot is free again (its reads completed above): refill it with the step after next
-    if (t0 + 2 * STEP < t_end) {
-      const uint32_t mn = issue(sl, t0 + 2 * STEP);
-      if (sl) mask[1] = mn;
-      else mask[0] = mn;
+  };
+  auto read_slot = [&](int sl, u32x4* rd, u32x4* rs) {
+    gram_ring_read((uint32_t)(uintptr_t)(ring + sl * kGramSlotBytes) + lane * 16, rd, rs);
+  };
+
+  // Software pipeline: slot sl holds the next step, the other slot the one after; Z of the current step is in
+  // registers.  Each iteration reads the next step, refills its slot three steps ahead, and forms the next Z while
+  // the current one is multiplied (scheduling groups interleave the MFMAs with the VALU work).  Loads past the
+  // range are issued too (all rows invalid; they read the pool's first row) so that the loop body has no branch.
+  constexpr int kWaitLps = LPS == 16 ? 0x4F70 : 0x0F78;  // s_waitcnt vmcnt(LPS)
+  uint32_t mask[kGramRing];
+  mask[0] = issue(0, t_begin);
+  mask[1] = issue(1, t_begin + STEP);
+  u32x4 zc_h[8], zc_l[8];
+  {
+    __builtin_amdgcn_s_waitcnt(kWaitLps);
+    u32x4 rd[8], rs[8];
+    read_slot(0, rd, rs);
+    form(rd, rs, mask[0], zc_h, zc_l);
+  }
+  mask[0] = issue(0, t_begin + 2 * STEP);
+  int sl = 1;
+  for (int t0 = t_begin; t0 + STEP < t_end; t0 += STEP) {
+    __builtin_amdgcn_s_waitcnt(kWaitLps);
+    const uint32_t m = sl ? mask[1] : mask[0];
+    u32x4 rd[8], rs[8];
+    read_slot(sl, rd, rs);
+    const uint32_t mn = issue(sl, t0 + 3 * STEP);
+    if (sl) mask[1] = mn;
+    else mask[0] = mn;
+    u32x4 zn_h[8], zn_l[8];
+    form(rd, rs, m, zn_h, zn_l);
+    gram_all_tiles<D>(acc, zc_h, zc_l, std::make_integer_sequence<int, NT>{});
+    // 3 NT = 108 MFMAs, each followed by a share of the VALU work of the next Z
+#pragma unroll
+    for (int q = 0; q < 3 * NT; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);  // VALU
     }
-    gram_all_tiles<D>(acc, zh, zl, std::make_integer_sequence<int, NT>{});
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      zc_h[j] = zn_h[j];
+      zc_l[j] = zn_l[j];
+    }
     sl ^= 1;
   }
+  gram_all_tiles<D>(acc, zc_h, zc_l, std::make_integer_sequence<int, NT>{});
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): no LDS load outstanding when the wave ends
   const int64_t lu = fit_linear_unit(a, f);
   float* P = a.partials + ((size_t)lu * a.max_parts + part) * D * D;
   gram_all_stores<D>(P, acc, g, n, std::make_integer_sequence<int, NT>{});
@@ -618,6 +688,7 @@ hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hip
     if (D == 128 && a.pv.block_shift >= 4 && a.part_tokens / a.pv.block_size + 3 <= kGramTabMax) {
       // LDS-staged rows (block sizes of at least 16 tokens, a partial's table fits the wave's LDS copy)
       const bool delta = a.mode == KVC_FIT_DELTA;
+      grid = dim3(a.max_parts, 2 * ((a.pv.num_kv_heads + kFitWaves - 1) / kFitWaves), num_items * a.num_layers);
       const void* fn = delta ? (const void*)gram_bf16_ring<true> : (const void*)gram_bf16_ring<false>;
       hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGramLdsBytes);
       if (e != hipSuccess) return e;
