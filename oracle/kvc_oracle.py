@@ -13,6 +13,10 @@ Everything is plain float64 NumPy, written to be checked against the paper by ey
                  Eq. 7: A = U_r Sigma_r, B = R_r^T.  Also Z = C_j for a base cache (Section 3.3, Z in {C, Delta}).
   * chain     -- Eq. 6: Delta_{k<-i} = Delta_{k<-j} + Delta_{j<-i}; the composed state is the rank-r truncated SVD
                  (Eq. 7) of the materialised sum A1 B1 + A2 B2.
+  * anchors   -- Eq. 8 with V anchors and token-wise weights: interpolation weights from the mean absolute distance
+                 of the source cache to each anchor's reconstructed base, softmax with T = 1, weighted sum of the
+                 anchors' corrections (Appendix A.3, "Correction Weighting"); the reliability gate of Eq. 9-11 and
+                 the anchor pool's insertion / least-frequently-used eviction rule (Appendix A.3).
   * metrics   -- normalised Frobenius error (Appendix A.1), effective rank at 90 % of the singular-value energy
                  (Section 3.1, Figure 2 caption), memory accounting O(VNLD) vs O(VNr(L+D)) (Sections 3.1, 3.3).
 
@@ -372,3 +376,121 @@ def full_dimensional_pool_bytes(num_anchors: int, num_consumers: int, num_layers
     agent, all full-dimensional."""
     return num_anchors * (1 + num_consumers) * dense_segment_bytes(num_layers, num_kv_heads, head_dim, num_tokens,
                                                                    elem_bytes)
+
+
+# ------------------------------------------------------------------------------------------------------------------
+# Anchored correction: Eq. 8 with V anchors and token-wise weights (Appendix A.3)
+# ------------------------------------------------------------------------------------------------------------------
+
+def anchor_distances(cache: Cache, item: Item, bases: Sequence[State], num_tokens: int, layer_begin: int = 0,
+                     layer_end: Optional[int] = None) -> np.ndarray:
+    """Mean absolute distance of the source cache to each anchor's reconstructed base (Appendix A.3, correction
+    weighting), per layer, K/V and token: d[l, kv, t, v] = mean over the layer's K (or V) row -- every KV head and
+    feature, the paper's feature dimension D = H d -- of |C_src[t] - (A_v B_v)[t]|.  float64 [nl, 2, T, V]."""
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    H, d = cache.num_kv_heads, cache.head_dim
+    out = np.zeros((layer_end - layer_begin, 2, num_tokens, len(bases)))
+    for li, layer in enumerate(range(layer_begin, layer_end)):
+        for kv in range(2):
+            for v, base in enumerate(bases):
+                total = np.zeros(num_tokens)
+                for h in range(H):
+                    src = to_f64(read_rows(cache, layer, kv, h, item.src_table, item.src_offset, num_tokens),
+                                 cache.dtype)
+                    recon = base.coef_f64(layer, kv, h)[:num_tokens] @ base.basis_f64(layer, kv, h)
+                    total += np.abs(src - recon).sum(axis=1)
+                out[li, kv, :, v] = total / (H * d)
+    return out
+
+
+def softmax_weights(distances: np.ndarray, temperature: float = 1.0) -> np.ndarray:
+    """w_v = exp(-d_v / T) / sum_u exp(-d_u / T) over the last axis (Eq. 10 form, T = 1 in the paper); evaluated as
+    exp(-(d_v - min_u d_u) / T) / sum, the same quantity without overflow."""
+    e = np.exp(-(distances - distances.min(axis=-1, keepdims=True)) / temperature)
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def apply_anchored(cache: Cache, item: Item, deltas: Sequence[State], weights: np.ndarray, num_tokens: int,
+                   layer_begin: int = 0, layer_end: Optional[int] = None) -> Cache:
+    """Eq. 8 with token-wise weights: C_hat[t] = C_src[t] + sum_v w[l, kv, t, v] (A_v B_v)[t] for t < num_tokens,
+    bit copy for num_tokens <= t < item.num_tokens; one rounding to the storage dtype.  Returns a new Cache."""
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    out = Cache(cache.dtype, cache.block_size, [a.copy() for a in cache.k], [a.copy() for a in cache.v])
+    for li, layer in enumerate(range(layer_begin, layer_end)):
+        for kv in range(2):
+            for h in range(cache.num_kv_heads):
+                src = read_rows(cache, layer, kv, h, item.src_table, item.src_offset, item.num_tokens)
+                rows = np.array(src, copy=True)
+                if num_tokens > 0:
+                    corr = np.zeros((num_tokens, cache.head_dim))
+                    for v, delta in enumerate(deltas):
+                        prod = delta.coef_f64(layer, kv, h)[:num_tokens] @ delta.basis_f64(layer, kv, h)
+                        corr += weights[li, kv, :, v][:, None] * prod
+                    rows[:num_tokens] = to_storage(to_f64(src[:num_tokens], cache.dtype) + corr, cache.dtype)
+                write_rows(out, layer, kv, h, item.dst_table, item.dst_offset, rows)
+    return out
+
+
+# ------------------------------------------------------------------------------------------------------------------
+# Reliability gate (Eq. 9-11) and anchor pool updates (Appendix A.3)
+# ------------------------------------------------------------------------------------------------------------------
+
+def gate_distances(cache: Cache, item: Item, bases: Sequence[State], prefix: int, layer_begin: int = 0,
+                   layer_end: Optional[int] = None) -> np.ndarray:
+    """Eq. 9: d_v = (sum over layers of ||V_src[:k] - V_v[:k]||_F^2)^(1/2), value states only, V_v the anchor's
+    reconstructed base values (every KV head of the layer's value row).  float64 [V]."""
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    sq = np.zeros(len(bases))
+    for layer in range(layer_begin, layer_end):
+        for v, base in enumerate(bases):
+            for h in range(cache.num_kv_heads):
+                src = to_f64(read_rows(cache, layer, 1, h, item.src_table, item.src_offset, prefix), cache.dtype)
+                recon = base.coef_f64(layer, 1, h)[:prefix] @ base.basis_f64(layer, 1, h)
+                sq[v] += np.sum((src - recon) ** 2)
+    return np.sqrt(sq)
+
+
+def gate(distances: np.ndarray, tau: float, temperature: float = 1.0):
+    """Eq. 10-11: g = softmax(-d / T); normalised entropy H = -sum g log2 g / log2 |A|; the correction is accepted
+    when |A| >= 2 and H <= tau (fewer than two compatible anchors mean dense prefill).  Returns (g, H, accept);
+    with |A| < 2, H is reported as 1."""
+    n = distances.shape[0]
+    if n < 2:
+        return np.ones(n), 1.0, False
+    g = softmax_weights(distances, temperature)
+    nz = g[g > 0]
+    h = float(-(nz * np.log2(nz)).sum() / np.log2(n))
+    return g, h, bool(h <= tau)
+
+
+class AnchorPool:
+    """Anchor bookkeeping of one shared-context slot (Appendix A.3, pool updates): at most `capacity` anchors, each
+    with a stored length and a use count.  A new anchor (inserted after a dense prefill) takes a free slot; when the
+    pool is full it replaces the least frequently used of the five oldest anchors (the oldest of them on equal
+    counts).  Anchors eligible for a comparison prefix k are those whose stored length is at least k."""
+
+    def __init__(self, capacity: int):
+        self.capacity = capacity
+        self.slots: List[Optional[dict]] = [None] * capacity
+        self.clock = 0
+
+    def insert(self, anchor_id: int, length: int) -> tuple:
+        """Returns (slot, evicted anchor id or None)."""
+        free = [i for i, e in enumerate(self.slots) if e is None]
+        evicted = None
+        if free:
+            slot = free[0]
+        else:
+            oldest = sorted(range(self.capacity), key=lambda i: self.slots[i]["order"])[:5]
+            slot = min(oldest, key=lambda i: (self.slots[i]["uses"], self.slots[i]["order"]))
+            evicted = self.slots[slot]["id"]
+        self.slots[slot] = {"id": anchor_id, "length": length, "uses": 0, "order": self.clock}
+        self.clock += 1
+        return slot, evicted
+
+    def record_use(self, slots: Sequence[int]) -> None:
+        for i in slots:
+            self.slots[i]["uses"] += 1
+
+    def eligible(self, prefix: int) -> List[int]:
+        return [i for i, e in enumerate(self.slots) if e is not None and e["length"] >= prefix]

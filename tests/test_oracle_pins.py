@@ -451,3 +451,124 @@ def test_effective_rank_and_error_metric():
     c = np.array([[3.0, 4.0]])
     assert math.isclose(O.normalized_frobenius_error(c + np.array([[0.0, 1.0]]), c), 0.2)
     assert math.isclose(O.max_relative_error(np.array([1.0, -2.5]), np.array([1.0, -2.0])), 0.25)
+
+
+# ------------------------------------------------------------------------------------------------ anchors (Eq. 8-11)
+
+def _anchor_setup(seed=21, T=12, H=2, d=6, L=2, bs=4):
+    """A contiguous f32 cache with source rows at offset 0, and helpers that build per-unit states from functions
+    of (layer, kv, head) -> (A, B)."""
+    rng = np.random.default_rng(seed)
+    nb = 2 * (-(-T // bs))
+    pools = {kv: [O.to_storage(rng.standard_normal((nb, bs, H, d)).astype(np.float32).astype(np.float64), "f32")
+                  for _ in range(L)] for kv in range(2)}
+    cache = O.Cache("f32", bs, pools[0], pools[1])
+    item = O.Item(T, 0, nb * bs // 2, None, None)
+
+    def state(fn):
+        coefs, bases = [], []
+        for layer in range(L):
+            ck, bk = [], []
+            for kv in range(2):
+                ch, bh = zip(*[fn(layer, kv, h) for h in range(H)])
+                ck.append(np.stack(ch))
+                bk.append(np.stack(bh))
+            coefs.append(np.stack(ck))
+            bases.append(np.stack(bk))
+        coef = np.stack(coefs)
+        return O.State(O.to_storage(coef, "f32"), np.stack(bases).astype(np.float32), None, "f32")
+
+    def src(layer, kv, h):
+        return O.read_rows(cache, layer, kv, h, None, 0, T).astype(np.float64)
+
+    return rng, cache, item, state, src
+
+
+def test_anchor_distances_and_weights_closed_form():
+    """An anchor whose base reconstructs the source exactly has distance 0; one that reconstructs source + c has
+    distance |c| (the mean of |c| over every feature of the row); the weights are then 1 / (1 + e^{-|c|/T}) and
+    e^{-|c|/T} / (1 + e^{-|c|/T})."""
+    _, cache, item, state, src = _anchor_setup()
+    T, d, c = item.num_tokens, cache.head_dim, 0.5
+    exact = state(lambda l, kv, h: (src(l, kv, h), np.eye(d)))
+    shifted = state(lambda l, kv, h: (np.hstack([src(l, kv, h), np.full((T, 1), c)]),
+                                      np.vstack([np.eye(d), np.ones((1, d))])))
+    dist = O.anchor_distances(cache, item, [exact, shifted], T)
+    assert np.allclose(dist[..., 0], 0.0, atol=1e-12)
+    assert np.allclose(dist[..., 1], c, atol=1e-12)
+    for temp in (1.0, 2.0):
+        w = O.softmax_weights(dist, temp)
+        e = math.exp(-c / temp)
+        assert np.allclose(w[..., 0], 1.0 / (1.0 + e)) and np.allclose(w[..., 1], e / (1.0 + e))
+    # one anchor: weight 1; swapping anchors swaps the weights
+    assert np.array_equal(O.softmax_weights(dist[..., :1]), np.ones_like(dist[..., :1]))
+    w_swapped = O.softmax_weights(O.anchor_distances(cache, item, [shifted, exact], T))
+    assert np.allclose(w_swapped[..., ::-1], O.softmax_weights(dist))
+
+
+def test_apply_anchored_reduces_to_single_state_apply():
+    """V = 1 (w = 1), or V anchors carrying the same correction with any weights summing to 1, is the single-state
+    apply; a zero correction weighted 1 - a plus a correction weighted a is the single apply of a times it."""
+    rng, cache, item, state, src = _anchor_setup(seed=22)
+    T, d, r, Ts = item.num_tokens, cache.head_dim, 3, 9
+    delta = state(lambda l, kv, h: (rng.standard_normal((T, r)), np.linalg.qr(rng.standard_normal((d, r)))[0].T))
+    single = O.apply(cache, [O.Item(T, 0, item.dst_offset, None, None,
+                                    O.State(delta.coef[:, :, :, :Ts], delta.basis, None, "f32"))])
+    nl = cache.num_layers
+    got = O.apply_anchored(cache, item, [delta], np.ones((nl, 2, Ts, 1)), Ts)
+    for pool_a, pool_b in zip(got.k + got.v, single.k + single.v):
+        assert np.array_equal(pool_a, pool_b)
+    w = rng.uniform(0.1, 1.0, (nl, 2, Ts, 3))
+    w /= w.sum(axis=-1, keepdims=True)
+    got3 = O.apply_anchored(cache, item, [delta, delta, delta], w, Ts)
+    for pool_a, pool_b in zip(got3.k + got3.v, single.k + single.v):
+        assert np.allclose(O.to_f64(pool_a, "f32"), O.to_f64(pool_b, "f32"), atol=2e-6)
+    a = 0.25
+    zero = O.State(np.zeros_like(delta.coef), delta.basis, None, "f32")
+    scaled = O.State(O.to_storage(a * O.to_f64(delta.coef[:, :, :, :Ts], "f32"), "f32"), delta.basis, None, "f32")
+    wz = np.stack([np.full((nl, 2, Ts), 1 - a), np.full((nl, 2, Ts), a)], axis=-1)
+    got_z = O.apply_anchored(cache, item, [zero, delta], wz, Ts)
+    single_a = O.apply(cache, [O.Item(T, 0, item.dst_offset, None, None, scaled)])
+    for pool_a, pool_b in zip(got_z.k + got_z.v, single_a.k + single_a.v):
+        assert np.array_equal(pool_a, pool_b)
+    # rows past the weighted prefix are bit copies of the source
+    rows = O.read_rows(got3, 1, 1, 1, None, item.dst_offset, T)
+    assert np.array_equal(rows[Ts:], O.read_rows(cache, 1, 1, 1, None, 0, T)[Ts:])
+
+
+def test_gate_distances_entropy_and_acceptance():
+    _, cache, item, state, src = _anchor_setup(seed=23)
+    T, H, d, L, c, k = item.num_tokens, cache.num_kv_heads, cache.head_dim, cache.num_layers, 0.5, 7
+    exact = state(lambda l, kv, h: (src(l, kv, h), np.eye(d)))
+    shifted = state(lambda l, kv, h: (np.hstack([src(l, kv, h), np.full((T, 1), c)]),
+                                      np.vstack([np.eye(d), np.ones((1, d))])))
+    dist = O.gate_distances(cache, item, [exact, shifted], k)
+    # Eq. 9: sqrt of the sum over layers, heads, the k prefix rows and d features of c^2
+    assert np.allclose(dist, [0.0, c * math.sqrt(L * H * k * d)], atol=1e-12)
+    # Eq. 10-11 with two anchors: binary entropy of g_0 = 1 / (1 + e^{-d_1})
+    g, h, _ = O.gate(dist, tau=1.0)
+    p = 1.0 / (1.0 + math.exp(-dist[1]))
+    assert np.allclose(g, [p, 1 - p])
+    assert math.isclose(h, -(p * math.log2(p) + (1 - p) * math.log2(1 - p)))
+    assert O.gate(dist, tau=h)[2] and not O.gate(dist, tau=h * 0.999)[2]
+    # equal distances: uniform weights, entropy 1 (accepted only with tau >= 1); fewer than two anchors: dense
+    g, h, acc = O.gate(np.array([3.0, 3.0, 3.0]), tau=0.99)
+    assert np.allclose(g, 1 / 3) and math.isclose(h, 1.0) and not acc
+    assert O.gate(np.array([0.0]), tau=1.0)[2] is False and O.gate(np.zeros(0), tau=1.0)[2] is False
+
+
+def test_anchor_pool_evicts_least_used_of_five_oldest():
+    """A scripted history worked out by hand from the rule (least frequently used among the five oldest, the older
+    one on equal counts)."""
+    pool = O.AnchorPool(6)
+    for i in range(6):
+        assert pool.insert(i, 10 + i) == (i, None)
+    pool.record_use([0, 0, 1, 2, 3, 3, 3, 4])
+    # five oldest: slots 0-4 with uses 2, 1, 1, 3, 1 -> slot 1 (oldest of the three with one use)
+    assert pool.insert(6, 20) == (1, 1)
+    # five oldest now slots 0, 2, 3, 4, 5 with uses 2, 1, 3, 1, 0 -> slot 5
+    assert pool.insert(7, 30) == (5, 5)
+    # five oldest now slots 0, 2, 3, 4, 1 (id 6, no use) with uses 2, 1, 3, 1, 0 -> slot 1
+    assert pool.insert(8, 5) == (1, 6)
+    # eligibility by stored length: ids 0, 2, 3, 4 have lengths 10, 12, 13, 14; id 7: 30; id 8: 5
+    assert pool.eligible(12) == [2, 3, 4, 5] and pool.eligible(31) == [] and len(pool.eligible(0)) == 6
