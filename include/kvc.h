@@ -13,6 +13,15 @@
  *   kvc_chain      Eq. 6 composed in low rank: from S1 = Delta_{j<-i} and S2 = Delta_{k<-j}, the rank-r_out truncated
  *                  SVD of A1 B1 + A2 B2 (rows past a state's coverage are zero), without forming any T x d matrix.
  *
+ * With an anchor pool (Section 3.3, Appendix A.3) the correction of a transfer is estimated from V anchors:
+ *
+ *   kvc_anchor_weights  token-wise interpolation weights from the mean absolute distance of the source cache to
+ *                       each anchor's reconstructed base, softmax over the anchors (Appendix A.3).
+ *   kvc_apply_anchored  Eq. 8 with those weights: C_dst[t] = C_src[t] + sum_v w_v[t] A_v[t] B_v.
+ *   kvc_gate_distances  Eq. 9: value-state distances of the source prefix to each anchor's base; kvc_gate_decide
+ *                       turns them into the gate weights, normalised entropy and accept/reject of Eq. 10-11, and
+ *                       kvc_pool_* keep the pool's insertion and eviction bookkeeping (host only).
+ *
  * Layout.  One pool per layer for K and one for V.  Token slot s of physical block b of KV head h starts at element
  *   b * block_stride + s * token_stride + h * head_stride
  * of the layer's pool, and its head_dim elements are contiguous.  An item's token t sits at position p = offset + t of
@@ -21,8 +30,9 @@
  *   coef  [L][2][H][T_s][r]  (coef_dtype)      basis [L][2][H][r][d] (float32)      sigma [L][2][H][r] (float32)
  *
  * Ownership.  The caller allocates every buffer (pools, tables, states, workspaces, both copies of the item array);
- * the library allocates nothing, keeps no pointer after a call returns, holds no global state and may be called
- * from several threads.  Source rows are only read.
+ * the library allocates no device memory, keeps no pointer after a call returns, holds no global state and may be
+ * called from several threads.  Source rows are only read.  The one host-side object is the anchor-pool bookkeeping
+ * of kvc_pool_create, owned by the caller until kvc_pool_destroy (not thread-safe per pool).
  *
  * Errors.  Every argument check runs on the host before anything is enqueued; on an error nothing is enqueued and
  * the status says why.  A failed launch returns KVC_ERR_HIP (kvc_last_hip_error() gives the hipError_t of the
@@ -42,7 +52,8 @@ extern "C" {
 #endif
 
 #define KVC_VERSION 1
-#define KVC_MAX_RANK 128 /* largest r of a state */
+#define KVC_MAX_RANK 128   /* largest r of a state */
+#define KVC_MAX_ANCHORS 16 /* largest V of an anchor set in one call */
 
 typedef enum kvc_status {
   KVC_OK = 0,
@@ -153,6 +164,70 @@ size_t kvc_chain_workspace_bytes(const kvc_state* first, const kvc_state* second
  * the composition is lossless. */
 kvc_status kvc_chain(const kvc_state* first, const kvc_state* second, kvc_state* out, int32_t layer_begin,
                      int32_t layer_end, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ---- anchor pool (Section 3.3 low-rank anchors, Appendix A.3) --------------------------------------------------- */
+
+/* The anchors of one shared segment, for one call.  `states` is a HOST array of num_anchors states -- each anchor's
+ * base cache (kvc_anchor_weights, kvc_gate_distances) or its delta correction for the consuming agent
+ * (kvc_apply_anchored) -- sharing the cache's num_layers, num_kv_heads, head_dim and dtype, rank >= 1, each covering
+ * at least num_tokens rows.  `weights` is a DEVICE float32 array [layer_end - layer_begin][2][num_tokens]
+ * [num_anchors] (layer relative to layer_begin, then K = 0 / V = 1, token, anchor): written by kvc_anchor_weights,
+ * read by kvc_apply_anchored. */
+typedef struct kvc_anchors {
+  int32_t num_anchors; /* V, 1 .. KVC_MAX_ANCHORS */
+  int32_t num_tokens;  /* T_s: rows weighted and corrected */
+  const kvc_state* states;
+  float* weights;
+} kvc_anchors;
+
+/* Token-wise interpolation weights (Appendix A.3, correction weighting), for layers [layer_begin, layer_end), K and
+ * V separately, and t < T_s: d_v[t] = mean over the layer's K (or V) row -- every KV head and feature, the paper's
+ * D = H d -- of |C_src[t] - (A_v B_v)[t]|, with A_v B_v anchor v's reconstructed base, and
+ * w_v[t] = exp(-d_v[t] / temperature) / sum_u exp(-d_u[t] / temperature) (temperature 1 in the paper).  `batch`
+ * holds exactly one item whose source rows are compared (its state, dst side and items_dev are not used);
+ * T_s <= item.num_tokens. */
+kvc_status kvc_anchor_weights(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
+                              int32_t layer_begin, int32_t layer_end, float temperature, hipStream_t stream);
+
+/* Eq. 8 with token-wise weights: for layers [layer_begin, layer_end), every K/V unit and t < T_s,
+ * C_dst[t] = C_src[t] + sum_v w_v[t] A_v[t] B_v (A_v B_v anchor v's delta correction, w from `anchors->weights`),
+ * one rounding to the storage dtype; rows T_s <= t < item.num_tokens are bit copies.  One item (its state and
+ * items_dev are not used); destination rows must not overlap source rows (as for kvc_apply). */
+kvc_status kvc_apply_anchored(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
+                              int32_t layer_begin, int32_t layer_end, hipStream_t stream);
+
+/* Workspace kvc_gate_distances needs (bytes, 256-byte aligned start required). */
+size_t kvc_gate_workspace_bytes(const kvc_cache* cache, const kvc_anchors* anchors, int32_t prefix,
+                                int32_t layer_begin, int32_t layer_end);
+/* Eq. 9: d_v = (sum over layers [layer_begin, layer_end) of ||V_src[:k] - V_v[:k]||_F^2)^(1/2) with k = prefix,
+ * V_src the value rows of the item's source cache (every KV head) and V_v anchor v's reconstructed base values.
+ * `distances` is a DEVICE float32 array [num_anchors]; the partial sums are added in a fixed order (the result does
+ * not depend on scheduling).  anchors->weights is not used; 1 <= prefix <= anchors->num_tokens. */
+kvc_status kvc_gate_distances(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
+                              int32_t prefix, int32_t layer_begin, int32_t layer_end, float* distances,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream);
+/* Eq. 10-11 on the host: g_v = softmax(-d_v / temperature) over the n compatible anchors (HOST arrays), normalised
+ * entropy H = -sum g log2 g / log2 n; returns 1 (accept the correction) when n >= 2 and H <= tau, else 0 (dense
+ * prefill).  gate_weights may be NULL; with n < 2 *entropy is set to 1. */
+int32_t kvc_gate_decide(const float* distances, int32_t n, float tau, float temperature, float* gate_weights,
+                        float* entropy);
+
+/* Anchor-pool bookkeeping of one shared-context slot (Appendix A.3, pool updates), host only: up to `capacity`
+ * anchors with a stored length and a use count.  A new anchor takes the first free slot; in a full pool it replaces
+ * the least frequently used of the five oldest anchors (the oldest of them on equal counts).  The caller keeps the
+ * anchors' states; the pool only says which slot to overwrite. */
+typedef struct kvc_pool kvc_pool;
+kvc_pool* kvc_pool_create(int32_t capacity);
+void kvc_pool_destroy(kvc_pool* pool);
+/* Slot for a new anchor (id, stored length); *evicted_id gets the replaced anchor's id, or -1 for a free slot.
+ * Returns the slot, or -1 on a bad argument. */
+int32_t kvc_pool_insert(kvc_pool* pool, int64_t anchor_id, int32_t length, int64_t* evicted_id);
+/* Count one use of each listed slot (the anchors of an accepted correction). */
+kvc_status kvc_pool_record_use(kvc_pool* pool, const int32_t* slots, int32_t n);
+/* Occupied slots whose stored length is at least `prefix`, ascending; returns their number (at most capacity). */
+int32_t kvc_pool_eligible(const kvc_pool* pool, int32_t prefix, int32_t* slots);
+/* Id, length and use count of a slot (returns KVC_ERR_SHAPE for a free or invalid slot). */
+kvc_status kvc_pool_slot(const kvc_pool* pool, int32_t slot, int64_t* anchor_id, int32_t* length, int64_t* uses);
 
 #ifdef __cplusplus
 }

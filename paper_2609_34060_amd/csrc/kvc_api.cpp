@@ -2,7 +2,10 @@
 // enqueued; on an error nothing is enqueued.
 #include <algorithm>
 #include <cstdint>
+#include <cmath>
 #include <cstring>
+#include <new>
+#include <vector>
 
 #include "kvc.h"
 #include "kvc_launch.h"
@@ -216,6 +219,79 @@ void fill_pool_view(const kvc_cache* c, kvc::PoolView& pv) {
     if ((int32_t{1} << sh) == c->block_size) pv.block_shift = sh;
 }
 
+
+// Checks shared by the anchor entry points: one item, the anchor states, the weighted rows.
+kvc_status check_anchor_call(const kvc_cache* c, const kvc_batch* b, const kvc_anchors* an, int32_t lb, int32_t le,
+                             bool needs_dst, bool needs_weights) {
+  kvc_status s = check_cache(c, lb, le);
+  if (s != KVC_OK) return s;
+  if (!b || !an) return KVC_ERR_NULL_ARG;
+  if (b->num_items != 1 || b->max_blocks < 0) return KVC_ERR_SHAPE;
+  if (!b->items) return KVC_ERR_NULL_ARG;
+  if ((b->src_tables || b->dst_tables) && b->max_blocks < 1) return KVC_ERR_SHAPE;
+  const kvc_item& it = b->items[0];
+  if (it.reserved != 0 || it.num_tokens < 0) return KVC_ERR_SHAPE;
+  if (!positions_fit(it.src_offset, it.num_tokens, b->src_tables != nullptr, b, c)) return KVC_ERR_SHAPE;
+  if (needs_dst && !positions_fit(it.dst_offset, it.num_tokens, b->dst_tables != nullptr, b, c)) return KVC_ERR_SHAPE;
+  if (an->num_anchors < 1 || an->num_anchors > KVC_MAX_ANCHORS) return KVC_ERR_SHAPE;
+  if (!an->states) return KVC_ERR_NULL_ARG;
+  if (an->num_tokens < 0 || an->num_tokens > it.num_tokens) return KVC_ERR_SHAPE;
+  if (needs_weights && !an->weights) return KVC_ERR_NULL_ARG;
+  for (int32_t v = 0; v < an->num_anchors; ++v) {
+    const kvc_state& st = an->states[v];
+    s = check_state_shape(st, c->num_layers, c->num_kv_heads, c->head_dim);
+    if (s != KVC_OK) return s;
+    if (st.coef_dtype != c->dtype) return KVC_ERR_DTYPE;
+    if (st.rank < 1 || st.num_tokens < an->num_tokens) return KVC_ERR_SHAPE;
+    if (!st.coef || !st.basis) return KVC_ERR_NULL_ARG;
+  }
+  return KVC_OK;
+}
+
+void fill_anchor_args(const kvc_cache* c, const kvc_batch* b, const kvc_anchors* an, int32_t lb, int32_t le,
+                      kvc::AnchorArgs& a) {
+  std::memset(&a, 0, sizeof(a));
+  fill_pool_view(c, a.pv);
+  const kvc_item& it = b->items[0];
+  a.src_table = b->src_tables;
+  a.dst_table = b->dst_tables;
+  a.src_offset = it.src_offset;
+  a.dst_offset = it.dst_offset;
+  a.num_tokens = it.num_tokens;
+  a.num_weighted = an->num_tokens;
+  a.layer_begin = lb;
+  a.num_layers = le - lb;
+  for (int32_t l = lb; l < le; ++l) {
+    a.layers.k[l - lb] = c->k_layers[l];
+    a.layers.v[l - lb] = c->v_layers[l];
+  }
+  a.num_anchors = an->num_anchors;
+  for (int32_t v = 0; v < an->num_anchors; ++v) {
+    a.rank[v] = an->states[v].rank;
+    a.tokens[v] = an->states[v].num_tokens;
+    a.coef[v] = an->states[v].coef;
+    a.basis[v] = an->states[v].basis;
+    a.max_rank = std::max(a.max_rank, an->states[v].rank);
+  }
+  a.weights = an->weights;
+  a.inv_temperature = 1.0f;
+}
+
+// Anchor-pool bookkeeping (Appendix A.3): slots with id, stored length, use count and insertion order.
+struct PoolSlot {
+  bool used = false;
+  int64_t id = -1, uses = 0, order = 0;
+  int32_t length = 0;
+};
+
+}  // namespace
+
+struct kvc_pool {
+  std::vector<PoolSlot> slots;
+  int64_t clock = 0;
+};
+
+namespace {
 }  // namespace
 
 extern "C" {
@@ -416,6 +492,161 @@ kvc_status kvc_chain(const kvc_state* first, const kvc_state* second, kvc_state*
   ea.vecs = reinterpret_cast<double*>(ws + p.off_vecs);
   ea.seed = 0xC4A1u;
   return hip_status(kvc::launch_chain(ca, ea, stream));
+}
+
+kvc_status kvc_anchor_weights(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
+                              int32_t layer_begin, int32_t layer_end, float temperature, hipStream_t stream) {
+  kvc_status s = check_anchor_call(cache, batch, anchors, layer_begin, layer_end, false, true);
+  if (s != KVC_OK) return s;
+  if (!(temperature > 0.0f) || !std::isfinite(temperature)) return KVC_ERR_SHAPE;
+  if (layer_end - layer_begin > kvc::kMaxLayersPerLaunch) return KVC_ERR_SHAPE;
+  if (anchors->num_tokens == 0 || layer_end == layer_begin) return KVC_OK;
+  kvc::AnchorArgs a;
+  fill_anchor_args(cache, batch, anchors, layer_begin, layer_end, a);
+  a.inv_temperature = 1.0f / temperature;
+  return hip_status(kvc::launch_anchor_weights(a, cache->dtype, stream));
+}
+
+kvc_status kvc_apply_anchored(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
+                              int32_t layer_begin, int32_t layer_end, hipStream_t stream) {
+  kvc_status s = check_anchor_call(cache, batch, anchors, layer_begin, layer_end, true, anchors && anchors->num_tokens > 0);
+  if (s != KVC_OK) return s;
+  if (layer_end - layer_begin > kvc::kMaxLayersPerLaunch) return KVC_ERR_SHAPE;
+  if (batch->src_tables && batch->src_tables == batch->dst_tables) return KVC_ERR_ALIAS;
+  const kvc_item& it = batch->items[0];
+  if (!batch->src_tables && !batch->dst_tables && it.num_tokens > 0) {
+    const int64_t a0 = it.src_offset, a1 = a0 + it.num_tokens, b0 = it.dst_offset, b1 = b0 + it.num_tokens;
+    if (a0 < b1 && b0 < a1) return KVC_ERR_ALIAS;
+  }
+  if (it.num_tokens == 0 || layer_end == layer_begin) return KVC_OK;
+  kvc::AnchorArgs a;
+  fill_anchor_args(cache, batch, anchors, layer_begin, layer_end, a);
+  return hip_status(kvc::launch_apply_anchored(a, cache->dtype, stream));
+}
+
+size_t kvc_gate_workspace_bytes(const kvc_cache* cache, const kvc_anchors* anchors, int32_t prefix,
+                                int32_t layer_begin, int32_t layer_end) {
+  if (check_cache(cache, layer_begin, layer_end) != KVC_OK || !anchors || prefix < 1) return 0;
+  if (anchors->num_anchors < 1 || anchors->num_anchors > KVC_MAX_ANCHORS) return 0;
+  const int chunk = cache->dtype == KVC_BF16 ? kvc::anchor_chunk_tokens() : 64;
+  const size_t chunks = static_cast<size_t>((prefix + chunk - 1) / chunk);
+  return align256(static_cast<size_t>(layer_end - layer_begin) * chunks * anchors->num_anchors * sizeof(float));
+}
+
+kvc_status kvc_gate_distances(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
+                              int32_t prefix, int32_t layer_begin, int32_t layer_end, float* distances,
+                              void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  kvc_status s = check_anchor_call(cache, batch, anchors, layer_begin, layer_end, false, false);
+  if (s != KVC_OK) return s;
+  if (!distances) return KVC_ERR_NULL_ARG;
+  if (prefix < 1 || prefix > anchors->num_tokens) return KVC_ERR_SHAPE;
+  if (layer_end - layer_begin > kvc::kMaxLayersPerLaunch || layer_end == layer_begin) return KVC_ERR_SHAPE;
+  const size_t need = kvc_gate_workspace_bytes(cache, anchors, prefix, layer_begin, layer_end);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < need)
+    return KVC_ERR_WORKSPACE;
+  kvc::AnchorArgs a;
+  fill_anchor_args(cache, batch, anchors, layer_begin, layer_end, a);
+  a.num_weighted = prefix;
+  const int chunk = cache->dtype == KVC_BF16 ? kvc::anchor_chunk_tokens() : 64;
+  a.gate_chunks = (prefix + chunk - 1) / chunk;
+  a.gate_partials = static_cast<float*>(workspace);
+  a.distances = distances;
+  return hip_status(kvc::launch_gate_distances(a, cache->dtype, stream));
+}
+
+int32_t kvc_gate_decide(const float* distances, int32_t n, float tau, float temperature, float* gate_weights,
+                        float* entropy) {
+  if (n < 2 || !distances || !(temperature > 0.0f)) {
+    if (entropy) *entropy = 1.0f;
+    if (gate_weights && distances)
+      for (int32_t v = 0; v < n; ++v) gate_weights[v] = 1.0f;
+    return 0;
+  }
+  double dmin = distances[0];
+  for (int32_t v = 1; v < n; ++v) dmin = std::min<double>(dmin, distances[v]);
+  std::vector<double> g(static_cast<size_t>(n));
+  double sum = 0.0;
+  for (int32_t v = 0; v < n; ++v) sum += (g[v] = std::exp(-(distances[v] - dmin) / temperature));
+  double h = 0.0;
+  for (int32_t v = 0; v < n; ++v) {
+    g[v] /= sum;
+    if (g[v] > 0.0) h -= g[v] * std::log2(g[v]);
+    if (gate_weights) gate_weights[v] = static_cast<float>(g[v]);
+  }
+  h /= std::log2(static_cast<double>(n));
+  if (entropy) *entropy = static_cast<float>(h);
+  return h <= tau ? 1 : 0;
+}
+
+kvc_pool* kvc_pool_create(int32_t capacity) {
+  if (capacity < 1) return nullptr;
+  kvc_pool* p = new (std::nothrow) kvc_pool;
+  if (p) p->slots.resize(static_cast<size_t>(capacity));
+  return p;
+}
+
+void kvc_pool_destroy(kvc_pool* pool) { delete pool; }
+
+int32_t kvc_pool_insert(kvc_pool* pool, int64_t anchor_id, int32_t length, int64_t* evicted_id) {
+  if (!pool || length < 0) return -1;
+  const int32_t cap = static_cast<int32_t>(pool->slots.size());
+  int32_t slot = -1;
+  int64_t evicted = -1;
+  for (int32_t i = 0; i < cap && slot < 0; ++i)
+    if (!pool->slots[i].used) slot = i;
+  if (slot < 0) {
+    // the five oldest slots, then the least used among them (the older one on equal counts)
+    std::vector<int32_t> order(static_cast<size_t>(cap));
+    for (int32_t i = 0; i < cap; ++i) order[i] = i;
+    std::sort(order.begin(), order.end(),
+              [&](int32_t x, int32_t y) { return pool->slots[x].order < pool->slots[y].order; });
+    const int32_t m = std::min<int32_t>(5, cap);
+    slot = order[0];
+    for (int32_t i = 1; i < m; ++i) {
+      const PoolSlot& c = pool->slots[order[i]];
+      const PoolSlot& b = pool->slots[slot];
+      if (c.uses < b.uses || (c.uses == b.uses && c.order < b.order)) slot = order[i];
+    }
+    evicted = pool->slots[slot].id;
+  }
+  PoolSlot& e = pool->slots[slot];
+  e.used = true;
+  e.id = anchor_id;
+  e.length = length;
+  e.uses = 0;
+  e.order = pool->clock++;
+  if (evicted_id) *evicted_id = evicted;
+  return slot;
+}
+
+kvc_status kvc_pool_record_use(kvc_pool* pool, const int32_t* slots, int32_t n) {
+  if (!pool || (n > 0 && !slots)) return KVC_ERR_NULL_ARG;
+  const int32_t cap = static_cast<int32_t>(pool->slots.size());
+  for (int32_t i = 0; i < n; ++i)
+    if (slots[i] < 0 || slots[i] >= cap || !pool->slots[slots[i]].used) return KVC_ERR_SHAPE;
+  for (int32_t i = 0; i < n; ++i) ++pool->slots[slots[i]].uses;
+  return KVC_OK;
+}
+
+int32_t kvc_pool_eligible(const kvc_pool* pool, int32_t prefix, int32_t* slots) {
+  if (!pool) return 0;
+  int32_t n = 0;
+  for (int32_t i = 0; i < static_cast<int32_t>(pool->slots.size()); ++i)
+    if (pool->slots[i].used && pool->slots[i].length >= prefix) {
+      if (slots) slots[n] = i;
+      ++n;
+    }
+  return n;
+}
+
+kvc_status kvc_pool_slot(const kvc_pool* pool, int32_t slot, int64_t* anchor_id, int32_t* length, int64_t* uses) {
+  if (!pool) return KVC_ERR_NULL_ARG;
+  if (slot < 0 || slot >= static_cast<int32_t>(pool->slots.size()) || !pool->slots[slot].used) return KVC_ERR_SHAPE;
+  const PoolSlot& e = pool->slots[slot];
+  if (anchor_id) *anchor_id = e.id;
+  if (length) *length = e.length;
+  if (uses) *uses = e.uses;
+  return KVC_OK;
 }
 
 }  // extern "C"

@@ -23,12 +23,6 @@ constexpr int kApplyChunk = kApplyWaves * kApplyTilesPerWave * 16;  // tokens pe
 
 int apply_chunk_tokens() { return kApplyChunk; }
 
-// Feature held by MFMA row m of M-tile mt: the lanes of token-group g = m / 4 own features 32 q + 8 g + [0, 8) of
-// 16-byte load q = mt / 2, the first four in M-tile 2q and the last four in 2q + 1.
-__device__ __forceinline__ int apply_feature(int mt, int m) {
-  return 32 * (mt >> 1) + 8 * (m >> 2) + 4 * (mt & 1) + (m & 3);
-}
-
 // Tuning knobs of the bf16 kernel (chosen by measurement on MI355X; see the launcher).
 //   TPW   16-token tiles per wave per workgroup (a workgroup covers 4 * 16 * TPW tokens)
 //   REGF  A-fragments held in registers for the whole chunk (true) or re-read from LDS per tile (false)
@@ -91,7 +85,7 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
     if constexpr (kRegFrags) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const int f = apply_feature(mt, n);
+        const int f = mfma_row_feature(mt, n);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const int k0 = ks * 32 + 8 * g;
@@ -165,7 +159,7 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
             acc[mt] = mfma16x16x32(alo[mt][ks], cb, acc[mt]);
             acc[mt] = mfma16x16x32(ahi[mt][ks], cb, acc[mt]);
           } else {
-            const int fo = apply_feature(mt, n) * KP + ks * 32 + 8 * g;
+            const int fo = mfma_row_feature(mt, n) * KP + ks * 32 + 8 * g;
             const bf16x8 fl = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[fo]));
             const bf16x8 fh = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[fo]));
             acc[mt] = mfma16x16x32(fl, cb, acc[mt]);

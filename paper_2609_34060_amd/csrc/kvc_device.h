@@ -74,6 +74,14 @@ __device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& a, const bf16x8& b, 
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) { return __builtin_bit_cast(bf16x8, v); }
 
+// Row-correction layout shared by the apply-type kernels: a 16-token tile is the MFMA product D^T = B^T A^T with M =
+// feature (16 per M-tile), N = token, K = rank.  Feature held by MFMA row m of M-tile mt: the lanes of token-group
+// g = m / 4 own features 32 q + 8 g + [0, 8) of 16-byte row load q = mt / 2, the first four in M-tile 2q and the
+// last four in 2q + 1.
+__device__ __forceinline__ int mfma_row_feature(int mt, int m) {
+  return 32 * (mt >> 1) + 8 * (m >> 2) + 4 * (mt & 1) + (m & 3);
+}
+
 // Offset of unit (layer, kv, head) in a state's per-unit arrays.
 __device__ __forceinline__ int64_t unit_index(int32_t layer, int32_t kv, int32_t head, int32_t num_kv_heads) {
   return ((int64_t)layer * 2 + kv) * num_kv_heads + head;

@@ -83,4 +83,32 @@ struct ChainArgs {
 };
 hipError_t launch_chain(const ChainArgs& a, const EigArgs& ea, hipStream_t stream);
 
+// Anchors (kvc_anchor.hip): distances / weights, anchored apply, gate distances.  One item per call.
+struct AnchorArgs {
+  PoolView pv;
+  LayerPtrs layers;
+  const int32_t* src_table;    // device row of the item's src table, or null
+  const int32_t* dst_table;
+  int32_t src_offset, dst_offset;
+  int32_t num_tokens;          // T: rows of the item (apply copies rows T_s <= t < T)
+  int32_t num_weighted;        // T_s (weights, apply) or the gate prefix k
+  int32_t layer_begin, num_layers;
+  int32_t num_anchors;
+  int32_t max_rank;            // largest anchor rank (LDS staging width)
+  int32_t rank[KVC_MAX_ANCHORS];
+  int32_t tokens[KVC_MAX_ANCHORS];  // coefficient rows per unit of each anchor's state
+  const void* coef[KVC_MAX_ANCHORS];
+  const float* basis[KVC_MAX_ANCHORS];
+  float* weights;              // [num_layers][2][num_weighted][num_anchors]
+  float inv_temperature;
+  float* gate_partials;        // [num_layers][chunks][num_anchors] sums of squares (gate)
+  int32_t gate_chunks;
+  float* distances;            // [num_anchors] (gate)
+};
+int anchor_chunk_tokens();
+size_t anchor_lds_bytes(int head_dim, int max_rank, kvc_dtype dtype, int which);
+hipError_t launch_anchor_weights(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream);
+hipError_t launch_apply_anchored(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream);
+hipError_t launch_gate_distances(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream);
+
 }  // namespace kvc

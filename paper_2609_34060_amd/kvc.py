@@ -1,6 +1,7 @@
 """Python binding of libkvc (ctypes): argument marshalling only.
 
-The names mirror the C ABI in include/kvc.h: kvc_fit_state, kvc_apply, kvc_chain and the size queries.  Every step
+The names mirror the C ABI in include/kvc.h: kvc_fit_state, kvc_apply, kvc_chain, the anchor-pool calls
+(kvc_anchor_weights, kvc_apply_anchored, kvc_gate_distances, kvc_gate_decide, kvc_pool_*) and the size queries.  Every step
 of the correction runs in the library's HIP kernels; torch only provides device memory and the stream.  Loading
 fails loudly when the library has not been built.
 """
@@ -19,9 +20,13 @@ KVC_ERR_ALIAS, KVC_ERR_WORKSPACE, KVC_ERR_UNSUPPORTED, KVC_ERR_HIP = 5, 6, 7, 8
 KVC_F32, KVC_BF16 = 0, 1
 KVC_FIT_DELTA, KVC_FIT_BASE = 0, 1
 KVC_MAX_RANK = 128
+KVC_MAX_ANCHORS = 16
 
 EXPORTED = ["kvc_version", "kvc_status_str", "kvc_last_hip_error", "kvc_state_bytes", "kvc_dense_bytes",
-            "kvc_apply", "kvc_fit_workspace_bytes", "kvc_fit_state", "kvc_chain_workspace_bytes", "kvc_chain"]
+            "kvc_apply", "kvc_fit_workspace_bytes", "kvc_fit_state", "kvc_chain_workspace_bytes", "kvc_chain",
+            "kvc_anchor_weights", "kvc_apply_anchored", "kvc_gate_workspace_bytes", "kvc_gate_distances",
+            "kvc_gate_decide", "kvc_pool_create", "kvc_pool_destroy", "kvc_pool_insert", "kvc_pool_record_use",
+            "kvc_pool_eligible", "kvc_pool_slot"]
 
 
 class KvcError(RuntimeError):
@@ -52,6 +57,11 @@ class kvc_batch(ctypes.Structure):
     _fields_ = [("num_items", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
                 ("items", ctypes.POINTER(kvc_item)), ("items_dev", ctypes.c_void_p),
                 ("src_tables", ctypes.c_void_p), ("dst_tables", ctypes.c_void_p)]
+
+
+class kvc_anchors(ctypes.Structure):
+    _fields_ = [("num_anchors", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
+                ("states", ctypes.POINTER(kvc_state)), ("weights", ctypes.c_void_p)]
 
 
 _lib = None
@@ -85,6 +95,30 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.kvc_chain_workspace_bytes.argtypes = [ctypes.POINTER(kvc_state)] * 3 + [i32, i32]
     lib.kvc_chain.restype = ctypes.c_int
     lib.kvc_chain.argtypes = [ctypes.POINTER(kvc_state)] * 3 + [i32, i32, vp, sz, vp]
+    pc, pb, pa = ctypes.POINTER(kvc_cache), ctypes.POINTER(kvc_batch), ctypes.POINTER(kvc_anchors)
+    f32, i64 = ctypes.c_float, ctypes.c_int64
+    lib.kvc_anchor_weights.restype = ctypes.c_int
+    lib.kvc_anchor_weights.argtypes = [pc, pb, pa, i32, i32, f32, vp]
+    lib.kvc_apply_anchored.restype = ctypes.c_int
+    lib.kvc_apply_anchored.argtypes = [pc, pb, pa, i32, i32, vp]
+    lib.kvc_gate_workspace_bytes.restype = sz
+    lib.kvc_gate_workspace_bytes.argtypes = [pc, pa, i32, i32, i32]
+    lib.kvc_gate_distances.restype = ctypes.c_int
+    lib.kvc_gate_distances.argtypes = [pc, pb, pa, i32, i32, i32, vp, vp, sz, vp]
+    lib.kvc_gate_decide.restype = i32
+    lib.kvc_gate_decide.argtypes = [ctypes.POINTER(f32), i32, f32, f32, ctypes.POINTER(f32), ctypes.POINTER(f32)]
+    lib.kvc_pool_create.restype = vp
+    lib.kvc_pool_create.argtypes = [i32]
+    lib.kvc_pool_destroy.restype = None
+    lib.kvc_pool_destroy.argtypes = [vp]
+    lib.kvc_pool_insert.restype = i32
+    lib.kvc_pool_insert.argtypes = [vp, i64, i32, ctypes.POINTER(i64)]
+    lib.kvc_pool_record_use.restype = ctypes.c_int
+    lib.kvc_pool_record_use.argtypes = [vp, ctypes.POINTER(i32), i32]
+    lib.kvc_pool_eligible.restype = i32
+    lib.kvc_pool_eligible.argtypes = [vp, i32, ctypes.POINTER(i32)]
+    lib.kvc_pool_slot.restype = ctypes.c_int
+    lib.kvc_pool_slot.argtypes = [vp, i32, ctypes.POINTER(i64), ctypes.POINTER(i32), ctypes.POINTER(i64)]
     _lib = lib
     return lib
 
@@ -258,3 +292,115 @@ def kvc_chain(first: State, second: State, out: State, layer_begin: int = 0, lay
                           layer_end, ctypes.c_void_p(workspace.data_ptr()), workspace.numel(),
                           _stream_handle(stream))
     _check(st, "kvc_chain")
+
+
+# ------------------------------------------------------------------------------------------------------------------
+# Anchor pool (Section 3.3, Appendix A.3)
+# ------------------------------------------------------------------------------------------------------------------
+
+class Anchors:
+    """kvc_anchors: the anchors' states (bases or delta corrections) and the weights tensor
+    [layers, 2, num_tokens, V] float32 (allocated here when not given)."""
+
+    def __init__(self, states: Sequence[State], num_tokens: int, num_layers: int,
+                 weights: Optional[torch.Tensor] = None):
+        self.states = list(states)
+        V = len(self.states)
+        self._arr = (kvc_state * max(V, 1))(*[st.s for st in self.states])
+        if weights is None and V:
+            weights = torch.empty(num_layers, 2, num_tokens, V, dtype=torch.float32,
+                                  device=self.states[0].basis.device)
+        self.weights = weights
+        self.a = kvc_anchors(V, num_tokens, ctypes.cast(self._arr, ctypes.POINTER(kvc_state)),
+                             None if weights is None or weights.numel() == 0 else weights.data_ptr())
+
+    def with_states(self, states: Sequence[State]) -> "Anchors":
+        """The same weights with other states (the delta corrections after the weights came from the bases)."""
+        return Anchors(states, self.a.num_tokens, 0 if self.weights is None else self.weights.shape[0], self.weights)
+
+
+def kvc_anchor_weights(cache: Cache, batch: Batch, anchors: Anchors, layer_begin: int = 0,
+                       layer_end: Optional[int] = None, temperature: float = 1.0, stream=None) -> None:
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    st = load().kvc_anchor_weights(ctypes.byref(cache.c), ctypes.byref(batch.b), ctypes.byref(anchors.a), layer_begin,
+                                   layer_end, float(temperature), _stream_handle(stream))
+    _check(st, "kvc_anchor_weights")
+
+
+def kvc_apply_anchored(cache: Cache, batch: Batch, anchors: Anchors, layer_begin: int = 0,
+                       layer_end: Optional[int] = None, stream=None) -> None:
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    st = load().kvc_apply_anchored(ctypes.byref(cache.c), ctypes.byref(batch.b), ctypes.byref(anchors.a),
+                                   layer_begin, layer_end, _stream_handle(stream))
+    _check(st, "kvc_apply_anchored")
+
+
+def kvc_gate_workspace_bytes(cache: Cache, anchors: Anchors, prefix: int, layer_begin: int = 0,
+                             layer_end: Optional[int] = None) -> int:
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    return load().kvc_gate_workspace_bytes(ctypes.byref(cache.c), ctypes.byref(anchors.a), prefix, layer_begin,
+                                           layer_end)
+
+
+def kvc_gate_distances(cache: Cache, batch: Batch, anchors: Anchors, prefix: int, layer_begin: int = 0,
+                       layer_end: Optional[int] = None, distances: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    dev = cache.k_pools[0].device
+    if distances is None:
+        distances = torch.empty(len(anchors.states), dtype=torch.float32, device=dev)
+    need = kvc_gate_workspace_bytes(cache, anchors, prefix, layer_begin, layer_end)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    st = load().kvc_gate_distances(ctypes.byref(cache.c), ctypes.byref(batch.b), ctypes.byref(anchors.a), prefix,
+                                   layer_begin, layer_end, ctypes.c_void_p(distances.data_ptr()),
+                                   ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream_handle(stream))
+    _check(st, "kvc_gate_distances")
+    return distances
+
+
+def kvc_gate_decide(distances: Sequence[float], tau: float, temperature: float = 1.0):
+    """Returns (accept, gate weights, normalised entropy) of Eq. 10-11 for host distances."""
+    n = len(distances)
+    d = (ctypes.c_float * max(n, 1))(*[float(x) for x in distances])
+    g = (ctypes.c_float * max(n, 1))()
+    h = ctypes.c_float()
+    acc = load().kvc_gate_decide(d, n, float(tau), float(temperature), g, ctypes.byref(h))
+    return bool(acc), [g[i] for i in range(n)], h.value
+
+
+class Pool:
+    """kvc_pool_*: the anchor bookkeeping of one shared-context slot (host only)."""
+
+    def __init__(self, capacity: int):
+        self.p = load().kvc_pool_create(capacity)
+        if not self.p:
+            raise KvcError(KVC_ERR_SHAPE, "kvc_pool_create")
+        self.capacity = capacity
+
+    def __del__(self):
+        if getattr(self, "p", None) and _lib is not None:
+            _lib.kvc_pool_destroy(self.p)
+            self.p = None
+
+    def insert(self, anchor_id: int, length: int):
+        ev = ctypes.c_int64()
+        slot = load().kvc_pool_insert(self.p, anchor_id, length, ctypes.byref(ev))
+        if slot < 0:
+            raise KvcError(KVC_ERR_SHAPE, "kvc_pool_insert")
+        return slot, (None if ev.value < 0 else ev.value)
+
+    def record_use(self, slots: Sequence[int]) -> None:
+        arr = (ctypes.c_int32 * max(len(slots), 1))(*slots)
+        _check(load().kvc_pool_record_use(self.p, arr, len(slots)), "kvc_pool_record_use")
+
+    def eligible(self, prefix: int) -> List[int]:
+        arr = (ctypes.c_int32 * self.capacity)()
+        n = load().kvc_pool_eligible(self.p, prefix, arr)
+        return [arr[i] for i in range(n)]
+
+    def slot(self, slot: int):
+        aid, length, uses = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int64()
+        _check(load().kvc_pool_slot(self.p, slot, ctypes.byref(aid), ctypes.byref(length), ctypes.byref(uses)),
+               "kvc_pool_slot")
+        return aid.value, length.value, uses.value
