@@ -178,3 +178,108 @@ def test_apply_empty_batch_is_a_noop():
     assert f.apply() == kvc.KVC_OK
     f = Fixture()
     assert f.apply(1, 1) == kvc.KVC_OK           # an empty layer range is valid (nothing to launch)
+
+
+class AnchorFixture(Fixture):
+    """Fixture plus a valid-looking anchor set of V fake states (no kernel is ever launched by these cases)."""
+
+    def __init__(self, V=3, Ts=80, **kw):
+        super().__init__(**kw)
+        L, H, d = self.cache.num_layers, self.cache.num_kv_heads, self.cache.head_dim
+        self.states = (kvc.kvc_state * V)(*[kvc.kvc_state(L, H, d, 100, 16, kvc.KVC_BF16, FAKE + 0x10000000 * (v + 1),
+                                                          FAKE + 0x10000000 * (v + 1) + 0x8000000, None)
+                                            for v in range(V)])
+        self.anchors = kvc.kvc_anchors(V, Ts, ctypes.cast(self.states, ctypes.POINTER(kvc.kvc_state)), FAKE + 0x300000)
+        self.ws = (ctypes.c_uint8 * 0)()
+
+    def weights(self, temperature=1.0, lb=0, le=None):
+        le = self.cache.num_layers if le is None else le
+        return kvc.load().kvc_anchor_weights(ctypes.byref(self.cache), ctypes.byref(self.batch),
+                                             ctypes.byref(self.anchors), lb, le, temperature, None)
+
+    def anchored(self):
+        return kvc.load().kvc_apply_anchored(ctypes.byref(self.cache), ctypes.byref(self.batch),
+                                             ctypes.byref(self.anchors), 0, self.cache.num_layers, None)
+
+    def gate(self, prefix=50, ws=FAKE, ws_bytes=1 << 20, dist=FAKE + 0x200000):
+        return kvc.load().kvc_gate_distances(ctypes.byref(self.cache), ctypes.byref(self.batch),
+                                             ctypes.byref(self.anchors), prefix, 0, self.cache.num_layers, dist, ws,
+                                             ws_bytes, None)
+
+
+def _anchor_cases():
+    def two_items(f):
+        f.batch.num_items = 2
+        return f.weights(), kvc.KVC_ERR_SHAPE
+
+    def no_anchors(f):
+        f.anchors.num_anchors = 0
+        return f.anchored(), kvc.KVC_ERR_SHAPE
+
+    def too_many_anchors(f):
+        f.anchors.num_anchors = kvc.KVC_MAX_ANCHORS + 1
+        return f.weights(), kvc.KVC_ERR_SHAPE
+
+    def null_states(f):
+        f.anchors.states = None
+        return f.weights(), kvc.KVC_ERR_NULL_ARG
+
+    def null_weights(f):
+        f.anchors.weights = None
+        return f.anchored(), kvc.KVC_ERR_NULL_ARG
+
+    def weighted_beyond_item(f):
+        f.anchors.num_tokens = 101
+        return f.weights(), kvc.KVC_ERR_SHAPE
+
+    def anchor_short(f):
+        f.states[1].num_tokens = 70
+        return f.anchored(), kvc.KVC_ERR_SHAPE
+
+    def anchor_rank0(f):
+        f.states[2].rank = 0
+        return f.weights(), kvc.KVC_ERR_SHAPE
+
+    def anchor_dtype(f):
+        f.states[0].coef_dtype = kvc.KVC_F32
+        return f.anchored(), kvc.KVC_ERR_DTYPE
+
+    def anchor_shape(f):
+        f.states[0].num_kv_heads = 5
+        return f.weights(), kvc.KVC_ERR_SHAPE
+
+    def bad_temperature(f):
+        return f.weights(temperature=0.0), kvc.KVC_ERR_SHAPE
+
+    def overlap(f):
+        f.items[0].dst_offset = 30
+        return f.anchored(), kvc.KVC_ERR_ALIAS
+
+    def gate_prefix(f):
+        return f.gate(prefix=81), kvc.KVC_ERR_SHAPE
+
+    def gate_workspace(f):
+        return f.gate(ws_bytes=16), kvc.KVC_ERR_WORKSPACE
+
+    def gate_workspace_align(f):
+        return f.gate(ws=FAKE + 8), kvc.KVC_ERR_WORKSPACE
+
+    def gate_null_distances(f):
+        return f.gate(dist=None), kvc.KVC_ERR_NULL_ARG
+
+    return [two_items, no_anchors, too_many_anchors, null_states, null_weights, weighted_beyond_item, anchor_short,
+            anchor_rank0, anchor_dtype, anchor_shape, bad_temperature, overlap, gate_prefix, gate_workspace,
+            gate_workspace_align, gate_null_distances]
+
+
+@pytest.mark.parametrize("case", _anchor_cases(), ids=lambda c: c.__name__)
+def test_anchor_calls_reject_bad_arguments_before_launch(case):
+    got, expected = case(AnchorFixture())
+    assert got == expected, (kvc.status_str(got), kvc.status_str(expected))
+
+
+def test_gate_workspace_query():
+    f = AnchorFixture(V=4)
+    need = kvc.load().kvc_gate_workspace_bytes(ctypes.byref(f.cache), ctypes.byref(f.anchors), 1200, 0, 2)
+    # bf16: 512-token chunks, one float per (layer, chunk, anchor), 256-byte granules
+    assert need == -(-(2 * 3 * 4 * 4) // 256) * 256
