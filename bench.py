@@ -57,6 +57,77 @@ def _traffic(kernel_src_hash):
     return rec.get("traffic_bytes_per_launch")
 
 
+def _anchored_bytes(L, H, d, T, V, r, elem=2, coef_elem=2):
+    # src and dst rows, every anchor's coefficient rows, the weights (read once per unit), the bases
+    rows = L * 2 * H * T
+    return rows * (2 * d * elem + V * r * coef_elem) + L * 2 * T * V * 4 * H + V * L * 2 * H * r * d * 4
+
+
+def _weights_bytes(L, H, d, T, V, r, elem=2, coef_elem=2):
+    # src rows, every anchor's base coefficient rows, the weights written, the bases
+    rows = L * 2 * H * T
+    return rows * (d * elem + V * r * coef_elem) + L * 2 * T * V * 4 + V * L * 2 * H * r * d * 4
+
+
+def anchor_pool_measurement(args, kvc, synth, torch):
+    """The anchor-pool path of one transfer at the paper's anchor setting (V anchors of rank r on a shared segment):
+    token-wise weights from the anchors' bases, the anchored apply of Eq. 8, and the gate distances of Eq. 9."""
+    w = synth.WORKLOADS[args.anchor_workload].with_(num_agents=1)
+    L, H, d, T, r, V = w.num_layers, w.num_kv_heads, w.head_dim, w.seq_tokens[0], w.rank, args.anchors
+    r = args.anchor_rank
+    pc = synth.build_paged(w, device="cuda", num_output_agents=1)
+    cache = kvc.Cache(pc.k_pools, pc.v_pools)
+    src, dst = pc.seqs[(0, 0)], pc.seqs[(0, 100)]
+    tab = lambda s: pc.tables[[s.table_row]]
+    sdt = torch.bfloat16
+
+    def states(key, scale_of):
+        out = []
+        for v in range(V):
+            c, b, sg = synth.random_state(L, H, d, T, r, sdt, "cuda", key, v, coef_scale=scale_of(v))
+            out.append(kvc.State(c, b, sg))
+        return out
+
+    bases = states(11, lambda v: (0.1 + 0.9 * v) / (r / d) ** 0.5)
+    deltas = states(12, lambda v: 0.25 * (d / r) ** 0.5)
+    anchors = kvc.Anchors(bases, T, L)
+    anchors_d = anchors.with_states(deltas)
+    empty = kvc.State.empty(L, H, d, 0, 0, sdt, "cuda")
+    bw = kvc.Batch([T], [src.offset], [src.offset], [empty], tab(src), tab(src))
+    ba = kvc.Batch([T], [src.offset], [dst.offset], [empty], tab(src), tab(dst))
+    prefix = T
+    gws = torch.empty(max(1, kvc.kvc_gate_workspace_bytes(cache, anchors, prefix)), dtype=torch.uint8, device="cuda")
+    dist = torch.empty(V, dtype=torch.float32, device="cuda")
+    for _ in range(args.warmup):
+        kvc.kvc_gate_distances(cache, bw, anchors, prefix, distances=dist, workspace=gws)
+        kvc.kvc_anchor_weights(cache, bw, anchors)
+        kvc.kvc_apply_anchored(cache, ba, anchors_d)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        ev[k][0].record()
+        kvc.kvc_gate_distances(cache, bw, anchors, prefix, distances=dist, workspace=gws)
+        ev[k][1].record()
+        kvc.kvc_anchor_weights(cache, bw, anchors)
+        ev[k][2].record()
+        kvc.kvc_apply_anchored(cache, ba, anchors_d)
+        ev[k][3].record()
+    torch.cuda.synchronize()
+    gate_ms = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+    weights_ms = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+    apply_ms = sum(e[2].elapsed_time(e[3]) for e in ev) / args.steps
+    ab, wb = _anchored_bytes(L, H, d, T, V, r), _weights_bytes(L, H, d, T, V, r)
+    del pc, cache, bases, deltas, anchors, anchors_d
+    torch.cuda.empty_cache()
+    return {"workload": f"{w.name}: {L} layers x {H} KV heads x head_dim {d}, {T} shared tokens, {V} anchors of "
+                        f"rank {r} (bf16 paged); gate prefix {prefix}",
+            "gate_ms": round(gate_ms, 4), "weights_ms": round(weights_ms, 4), "apply_anchored_ms": round(apply_ms, 4),
+            "apply_anchored_gbps": round(ab / (apply_ms * 1e-3) / 1e9, 2),
+            "apply_anchored_frac": round(ab / (apply_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "apply_anchored_bytes": ab,
+            "weights_gbps": round(wb / (weights_ms * 1e-3) / 1e9, 2), "weights_bytes": wb}
+
+
 def cpu_baseline(pc, w, sample_layers=(0, 1)):
     """The oracle as it stands on a bounded sample of the same workload: `sample_layers` (every K/V head) of the
     first two edges -- fit S_1 and S_2, compose T_2 = chain(S_1, S_2), apply T_2 to the first agent's cache."""
@@ -108,6 +179,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama8b_32k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--anchor-workload", default="llama8b_4k",
+                    help="shapes of the anchor-pool measurement (the paper's 4K-token pool example)")
+    ap.add_argument("--anchors", type=int, default=10, help="anchors per shared slot (the paper's default V)")
+    ap.add_argument("--anchor-rank", type=int, default=32)
+    ap.add_argument("--no-anchor-pool", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the steps, run one elementwise kernel that reads BYTES and writes BYTES (dst = -src "
                          "in float32), a plain copy of known size, so that HBM counters of a profiling run can be "
@@ -224,6 +300,10 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(pc, w)
+    if not args.no_anchor_pool:
+        del cache, S, Tc, fit_batches, apply_batches, ws_fit, ws_chain, pc
+        torch.cuda.empty_cache()
+        out["anchor_pool"] = anchor_pool_measurement(args, kvc, synth, torch)
     print(json.dumps(out), flush=True)
     return 0
 
