@@ -27,18 +27,37 @@ constexpr int kF32Chunk = 64;                                       // tokens pe
 
 int anchor_chunk_tokens() { return kAnchorChunk; }
 
-// Stage B^T of one unit as bf16 hi/lo, zero-padded to KP ranks: s[f * KP + k] = split(B[k][f]).
-template <int D>
-__device__ __forceinline__ void stage_basis_hilo(const float* basis, int r, int KP, uint16_t* s_hi, uint16_t* s_lo) {
-  for (int e = threadIdx.x; e < D * KP; e += kAnchorThreads) {
-    const int k = e / D, f = e - k * D;
-    const float x = k < r ? basis[k * D + f] : 0.0f;
-    uint32_t hb, lb;
-    split_bf16(x, hb, lb);
-    s_hi[f * KP + k] = (uint16_t)hb;
-    s_lo[f * KP + k] = (uint16_t)lb;
+// B^T of one unit staged as bf16 hi/lo, zero-padded to KP = 32 KSM ranks: s[f * KP + k] = split(B[k][f]).  The
+// float4 loads of the next basis are issued into registers before the current one is used (load), and written to
+// the other LDS buffer one step later (store), so a workgroup waits once per basis at its barrier.
+template <int D, int KSM>
+struct BasisStager {
+  static constexpr int KP = 32 * KSM;
+  static constexpr int N4 = D * KP / (kAnchorThreads * 4);  // float4 per thread
+  f32x4 v[N4];
+  __device__ __forceinline__ void load(const float* basis, int r) {
+#pragma unroll
+    for (int i = 0; i < N4; ++i) {
+      const int e = 4 * ((int)threadIdx.x + i * kAnchorThreads);
+      const int k = e / D, f = e - k * D;
+      v[i] = k < r ? *reinterpret_cast<const f32x4*>(basis + k * D + f) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
   }
-}
+  __device__ __forceinline__ void store(uint16_t* s_hi, uint16_t* s_lo) const {
+#pragma unroll
+    for (int i = 0; i < N4; ++i) {
+      const int e = 4 * ((int)threadIdx.x + i * kAnchorThreads);
+      const int k = e / D, f = e - k * D;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        uint32_t hb, lb;
+        split_bf16(v[i][c], hb, lb);
+        s_hi[(f + c) * KP + k] = (uint16_t)hb;
+        s_lo[(f + c) * KP + k] = (uint16_t)lb;
+      }
+    }
+  }
+};
 
 // Eight bf16 coefficients of row t, ranks k0 .. k0 + 7 (zero past r).
 __device__ __forceinline__ u32x4 load_coef8(const uint16_t* coef, int r, int t, int k0) {
@@ -62,14 +81,12 @@ __device__ __forceinline__ void load_row_segments(const uint16_t* pool, int64_t 
 // distances (weights / gate), bf16
 // ---------------------------------------------------------------------------------------------------------------
 
-template <int D, bool GATE>
+template <int D, int KSM, bool GATE>
 __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_bf16(AnchorArgs a) {
-  constexpr int MT = D / 16, NQ = D / 32;
+  constexpr int MT = D / 16, NQ = D / 32, KP = 32 * KSM;
   extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
-  const int KP = 32 * ((a.max_rank + 31) / 32);
-  uint16_t* s_hi = reinterpret_cast<uint16_t*>(anchor_lds);
-  uint16_t* s_lo = s_hi + D * KP;
-  float* s_d = reinterpret_cast<float*>(s_lo + D * KP);  // GATE: [waves][V]; else [chunk][V]
+  uint16_t* s_b = reinterpret_cast<uint16_t*>(anchor_lds);   // [2 buffers][hi, lo][D * KP]
+  float* s_d = reinterpret_cast<float*>(s_b + 4 * D * KP);     // GATE: [waves][V]; else [chunk][V]
 
   const int lrel = blockIdx.z, layer = a.layer_begin + lrel;
   const int kv = GATE ? 1 : blockIdx.y;
@@ -82,59 +99,68 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_bf16(AnchorArgs a)
   const int nd = GATE ? kAnchorWaves * V : kAnchorChunk * V;
   for (int e = threadIdx.x; e < nd; e += kAnchorThreads) s_d[e] = 0.0f;
 
-  for (int h = 0; h < H; ++h) {
+  BasisStager<D, KSM> stager;
+  auto basis_of = [&](int hv) {
+    const int h = hv / V, v = hv - h * V;
+    return a.basis[v] + unit_index(layer, kv, h, H) * (int64_t)a.rank[v] * D;
+  };
+  stager.load(basis_of(0), a.rank[0]);
+  for (int hv = 0; hv < H * V; ++hv) {
+    const int h = hv / V, v = hv - h * V;
+    const int r = a.rank[v], KS = (r + 31) / 32;
+    uint16_t* s_hi = s_b + (hv & 1) * 2 * D * KP;
+    uint16_t* s_lo = s_hi + D * KP;
+    stager.store(s_hi, s_lo);
+    __syncthreads();  // this basis is in LDS; the other buffer is no longer read (and s_d is initialised)
+    if (hv + 1 < H * V) stager.load(basis_of(hv + 1), a.rank[(hv + 1) % V]);
     const int64_t unit = unit_index(layer, kv, h, H);
-    for (int v = 0; v < V; ++v) {
-      const int r = a.rank[v], KS = (r + 31) / 32;
-      __syncthreads();  // the previous basis is consumed (and s_d is initialised)
-      stage_basis_hilo<D>(a.basis[v] + unit * (int64_t)r * D, r, KP, s_hi, s_lo);
-      __syncthreads();
-      const uint16_t* coef = static_cast<const uint16_t*>(a.coef[v]) + unit * (int64_t)a.tokens[v] * r;
-      float part = 0.0f;
-      for (int j = 0; j < kAnchorTiles; ++j) {
-        const int tile = j * kAnchorWaves + wave;
-        const int t0 = t_begin + tile * 16;
-        if (t0 >= Tl) break;
-        const int t = t0 + n;
-        const bool valid = t < Tl;
-        u32x4 raw[NQ];
-        load_row_segments<NQ>(pool, valid ? row_offset(a.pv, a.src_table, a.src_offset, t, h) : -1, g, raw);
-        f32x4 acc[MT];
+    const uint16_t* coef = static_cast<const uint16_t*>(a.coef[v]) + unit * (int64_t)a.tokens[v] * r;
+    float part = 0.0f;
+    for (int j = 0; j < kAnchorTiles; ++j) {
+      const int tile = j * kAnchorWaves + wave;
+      const int t0 = t_begin + tile * 16;
+      if (t0 >= Tl) break;
+      const int t = t0 + n;
+      const bool valid = t < Tl;
+      u32x4 raw[NQ];
+      load_row_segments<NQ>(pool, valid ? row_offset(a.pv, a.src_table, a.src_offset, t, h) : -1, g, raw);
+      f32x4 acc[MT];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 cb = as_bf16x8(valid ? load_coef8(coef, r, t, ks * 32 + 8 * g) : u32x4{0u, 0u, 0u, 0u});
+      for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            const int fo = mfma_row_feature(mt, n) * KP + ks * 32 + 8 * g;
-            acc[mt] = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[fo])), cb, acc[mt]);
-            acc[mt] = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[fo])), cb, acc[mt]);
-          }
-        }
-        float s = 0.0f;
+      for (int ks = 0; ks < KSM; ++ks) {
+        if (ks >= KS) break;
+        const bf16x8 cb = as_bf16x8(valid ? load_coef8(coef, r, t, ks * 32 + 8 * g) : u32x4{0u, 0u, 0u, 0u});
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const uint32_t w = raw[q][e >> 1];
-            const float x = (e & 1) ? bf16_hi_to_f32(w) : bf16_lo_to_f32(w);
-            const float diff = x - acc[2 * q + (e >> 2)][e & 3];
-            s += GATE ? diff * diff : fabsf(diff);
-          }
-        }
-        s += __shfl_xor(s, 16, kWave);
-        s += __shfl_xor(s, 32, kWave);
-        if (GATE) {
-          part += valid ? s : 0.0f;
-        } else if (g == 0 && valid) {
-          s_d[(tile * 16 + n) * V + v] += s;  // this lane owns the token: no race
+        for (int mt = 0; mt < MT; ++mt) {
+          const int fo = mfma_row_feature(mt, n) * KP + ks * 32 + 8 * g;
+          acc[mt] = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[fo])), cb, acc[mt]);
+          acc[mt] = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[fo])), cb, acc[mt]);
         }
       }
+      float s = 0.0f;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t w = raw[q][e >> 1];
+          const float x = (e & 1) ? bf16_hi_to_f32(w) : bf16_lo_to_f32(w);
+          const float diff = x - acc[2 * q + (e >> 2)][e & 3];
+          s += GATE ? diff * diff : fabsf(diff);
+        }
+      }
+      s += __shfl_xor(s, 16, kWave);
+      s += __shfl_xor(s, 32, kWave);
       if (GATE) {
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) part += __shfl_xor(part, o, kWave);
-        if (lane == 0) s_d[wave * V + v] += part;
+        part += valid ? s : 0.0f;
+      } else if (g == 0 && valid) {
+        s_d[(tile * 16 + n) * V + v] += s;  // this lane owns the token: no race
       }
+    }
+    if (GATE) {
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) part += __shfl_xor(part, o, kWave);
+      if (lane == 0) s_d[wave * V + v] += part;
     }
   }
   __syncthreads();
@@ -254,13 +280,11 @@ __global__ __launch_bounds__(kAnchorThreads) void gate_finish(AnchorArgs a) {
 // (one basis staging per anchor and workgroup), then C_src + correction is rounded once and stored
 // ---------------------------------------------------------------------------------------------------------------
 
-template <int D>
+template <int D, int KSM>
 __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_bf16(AnchorArgs a) {
-  constexpr int MT = D / 16, NQ = D / 32, TPW = kAnchoredTiles;
+  constexpr int MT = D / 16, NQ = D / 32, TPW = kAnchoredTiles, KP = 32 * KSM;
   extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
-  const int KP = 32 * ((a.max_rank + 31) / 32);
-  uint16_t* s_hi = reinterpret_cast<uint16_t*>(anchor_lds);
-  uint16_t* s_lo = s_hi + D * KP;
+  uint16_t* s_b = reinterpret_cast<uint16_t*>(anchor_lds);  // [2 buffers][hi, lo][D * KP]
 
   const int lrel = blockIdx.z, layer = a.layer_begin + lrel;
   const int H = a.pv.num_kv_heads;
@@ -281,11 +305,15 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_bf16(AnchorArgs
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   if (t_begin < Ts) {  // whole workgroup
+    BasisStager<D, KSM> stager;
+    stager.load(a.basis[0] + unit * (int64_t)a.rank[0] * D, a.rank[0]);
     for (int v = 0; v < V; ++v) {
       const int r = a.rank[v], KS = (r + 31) / 32;
-      __syncthreads();
-      stage_basis_hilo<D>(a.basis[v] + unit * (int64_t)r * D, r, KP, s_hi, s_lo);
-      __syncthreads();
+      uint16_t* s_hi = s_b + (v & 1) * 2 * D * KP;
+      uint16_t* s_lo = s_hi + D * KP;
+      stager.store(s_hi, s_lo);
+      __syncthreads();  // this basis is in LDS; the other buffer is no longer read
+      if (v + 1 < V) stager.load(a.basis[v + 1] + unit * (int64_t)a.rank[v + 1] * D, a.rank[v + 1]);
       const uint16_t* coef = static_cast<const uint16_t*>(a.coef[v]) + unit * (int64_t)a.tokens[v] * r;
 #pragma unroll
       for (int j = 0; j < TPW; ++j) {
@@ -294,7 +322,9 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_bf16(AnchorArgs
         const int t = t0 + n;
         const bool valid = t < Ts;
         const float w = valid ? wrow[(int64_t)t * V + v] : 0.0f;
-        for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+        for (int ks = 0; ks < KSM; ++ks) {
+          if (ks >= KS) break;
           const u32x4 cw = valid ? load_coef8(coef, r, t, ks * 32 + 8 * g) : u32x4{0u, 0u, 0u, 0u};
           u32x4 ch, cl;
 #pragma unroll
@@ -418,7 +448,7 @@ size_t anchor_lds_bytes(int D, int max_rank, kvc_dtype dtype, int which) {
   const int V = KVC_MAX_ANCHORS;
   if (dtype == KVC_BF16) {
     const size_t kp = 32 * (size_t)((max_rank + 31) / 32);
-    const size_t basis = 2 * (size_t)D * kp * sizeof(uint16_t);
+    const size_t basis = 4 * (size_t)D * kp * sizeof(uint16_t);  // two buffers of hi/lo
     if (which == 1) return basis;
     return basis + (size_t)(which == 2 ? kAnchorWaves : kAnchorChunk) * V * sizeof(float);
   }
@@ -436,14 +466,33 @@ static hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, const AnchorA
   return hipGetLastError();
 }
 
+template <int D, bool GATE>
+static hipError_t launch_dist_bf16(const AnchorArgs& a, dim3 grid, size_t lds, hipStream_t stream) {
+  switch ((a.max_rank + 31) / 32) {
+    case 1: return launch_with_lds(anchor_dist_bf16<D, 1, GATE>, grid, lds, a, stream);
+    case 2: return launch_with_lds(anchor_dist_bf16<D, 2, GATE>, grid, lds, a, stream);
+    case 3: return launch_with_lds(anchor_dist_bf16<D, 3, GATE>, grid, lds, a, stream);
+    default: return launch_with_lds(anchor_dist_bf16<D, 4, GATE>, grid, lds, a, stream);
+  }
+}
+
+template <int D>
+static hipError_t launch_anchored_bf16(const AnchorArgs& a, dim3 grid, size_t lds, hipStream_t stream) {
+  switch ((a.max_rank + 31) / 32) {
+    case 1: return launch_with_lds(apply_anchored_bf16<D, 1>, grid, lds, a, stream);
+    case 2: return launch_with_lds(apply_anchored_bf16<D, 2>, grid, lds, a, stream);
+    case 3: return launch_with_lds(apply_anchored_bf16<D, 3>, grid, lds, a, stream);
+    default: return launch_with_lds(apply_anchored_bf16<D, 4>, grid, lds, a, stream);
+  }
+}
+
 hipError_t launch_anchor_weights(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream) {
   if (a.num_weighted == 0 || a.num_layers == 0) return hipSuccess;
   const int D = a.pv.head_dim;
   const size_t lds = anchor_lds_bytes(D, a.max_rank, dtype, 0);
   if (dtype == KVC_BF16) {
     dim3 grid((a.num_weighted + kAnchorChunk - 1) / kAnchorChunk, 2, a.num_layers);
-    return D == 64 ? launch_with_lds(anchor_dist_bf16<64, false>, grid, lds, a, stream)
-                   : launch_with_lds(anchor_dist_bf16<128, false>, grid, lds, a, stream);
+    return D == 64 ? launch_dist_bf16<64, false>(a, grid, lds, stream) : launch_dist_bf16<128, false>(a, grid, lds, stream);
   }
   dim3 grid((a.num_weighted + kF32Chunk - 1) / kF32Chunk, 2, a.num_layers);
   return D == 64 ? launch_with_lds(anchor_dist_f32<64, false>, grid, lds, a, stream)
@@ -454,12 +503,10 @@ hipError_t launch_gate_distances(const AnchorArgs& a, kvc_dtype dtype, hipStream
   const int D = a.pv.head_dim;
   const size_t lds = anchor_lds_bytes(D, a.max_rank, dtype, 2);
   hipError_t e;
+  dim3 grid(a.gate_chunks, 1, a.num_layers);
   if (dtype == KVC_BF16) {
-    dim3 grid(a.gate_chunks, 1, a.num_layers);
-    e = D == 64 ? launch_with_lds(anchor_dist_bf16<64, true>, grid, lds, a, stream)
-                : launch_with_lds(anchor_dist_bf16<128, true>, grid, lds, a, stream);
+    e = D == 64 ? launch_dist_bf16<64, true>(a, grid, lds, stream) : launch_dist_bf16<128, true>(a, grid, lds, stream);
   } else {
-    dim3 grid(a.gate_chunks, 1, a.num_layers);
     e = D == 64 ? launch_with_lds(anchor_dist_f32<64, true>, grid, lds, a, stream)
                 : launch_with_lds(anchor_dist_f32<128, true>, grid, lds, a, stream);
   }
@@ -474,8 +521,7 @@ hipError_t launch_apply_anchored(const AnchorArgs& a, kvc_dtype dtype, hipStream
   const size_t lds = anchor_lds_bytes(D, a.max_rank, dtype, 1);
   if (dtype == KVC_BF16) {
     dim3 grid((a.num_tokens + kAnchoredChunk - 1) / kAnchoredChunk, 2 * a.pv.num_kv_heads, a.num_layers);
-    return D == 64 ? launch_with_lds(apply_anchored_bf16<64>, grid, lds, a, stream)
-                   : launch_with_lds(apply_anchored_bf16<128>, grid, lds, a, stream);
+    return D == 64 ? launch_anchored_bf16<64>(a, grid, lds, stream) : launch_anchored_bf16<128>(a, grid, lds, stream);
   }
   dim3 grid((a.num_tokens + kF32Chunk - 1) / kF32Chunk, 2 * a.pv.num_kv_heads, a.num_layers);
   return D == 64 ? launch_with_lds(apply_anchored_f32<64>, grid, lds, a, stream)
