@@ -12,6 +12,8 @@
 // apply the weight multiplies the bf16 coefficients in fp32, so the scaled coefficients are split into hi/lo as
 // well (hi*hi + hi*lo + lo*hi on the MFMA), and the correction of all anchors accumulates in fp32 before one
 // rounding of C_src + correction.  float32 caches use VALU kernels in fp32.
+#include <algorithm>
+
 #include "kvc_device.h"
 #include "kvc_launch.h"
 
@@ -27,34 +29,40 @@ constexpr int kF32Chunk = 64;                                       // tokens pe
 
 int anchor_chunk_tokens() { return kAnchorChunk; }
 
-// B^T of one unit staged as bf16 hi/lo, zero-padded to KP = 32 KSM ranks: s[f * KP + k] = split(B[k][f]).  The
-// float4 loads of the next basis are issued into registers before the current one is used (load), and written to
-// the other LDS buffer one step later (store), so a workgroup waits once per basis at its barrier.
+// B^T of one unit staged as bf16 hi/lo, zero-padded to KP = 32 KSM ranks: s[f * KP + k] = split(B[k][f]).  A thread
+// owns (feature f, eight ranks 8c .. 8c + 7) items, consecutive threads the consecutive 16-byte LDS granules, so the
+// stores are conflict-free (the loads read 64-byte row segments).  The loads of the next basis are issued into
+// registers before the current one is used (load) and written to the other LDS buffer one step later (store), so a
+// workgroup waits once per basis at its barrier.
 template <int D, int KSM>
 struct BasisStager {
-  static constexpr int KP = 32 * KSM;
-  static constexpr int N4 = D * KP / (kAnchorThreads * 4);  // float4 per thread
-  f32x4 v[N4];
+  static constexpr int KP = 32 * KSM, KG = KP / 8;
+  static constexpr int NI = D * KG / kAnchorThreads;  // items per thread
+  static_assert(NI * kAnchorThreads == D * KG, "whole items per thread");
+  float v[NI][8];
   __device__ __forceinline__ void load(const float* basis, int r) {
 #pragma unroll
-    for (int i = 0; i < N4; ++i) {
-      const int e = 4 * ((int)threadIdx.x + i * kAnchorThreads);
-      const int k = e / D, f = e - k * D;
-      v[i] = k < r ? *reinterpret_cast<const f32x4*>(basis + k * D + f) : f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < NI; ++i) {
+      const int idx = (int)threadIdx.x + i * kAnchorThreads;
+      const int c = idx % KG, f = idx / KG;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[i][e] = 8 * c + e < r ? basis[(8 * c + e) * D + f] : 0.0f;
     }
   }
   __device__ __forceinline__ void store(uint16_t* s_hi, uint16_t* s_lo) const {
 #pragma unroll
-    for (int i = 0; i < N4; ++i) {
-      const int e = 4 * ((int)threadIdx.x + i * kAnchorThreads);
-      const int k = e / D, f = e - k * D;
+    for (int i = 0; i < NI; ++i) {
+      const int idx = (int)threadIdx.x + i * kAnchorThreads;
+      u32x4 hi, lo;
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        uint32_t hb, lb;
-        split_bf16(v[i][c], hb, lb);
-        s_hi[(f + c) * KP + k] = (uint16_t)hb;
-        s_lo[(f + c) * KP + k] = (uint16_t)lb;
+      for (int p = 0; p < 4; ++p) {
+        uint32_t hh, ll;
+        split_bf16x2(v[i][2 * p], v[i][2 * p + 1], hh, ll);
+        hi[p] = hh;
+        lo[p] = ll;
       }
+      *reinterpret_cast<u32x4*>(s_hi + 8 * idx) = hi;  // = s_hi + f * KP + 8 c
+      *reinterpret_cast<u32x4*>(s_lo + 8 * idx) = lo;
     }
   }
 };
@@ -440,6 +448,321 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_f32(AnchorArgs 
 }
 
 // ---------------------------------------------------------------------------------------------------------------
+// Resident-basis kernels, bf16: the bases of every anchor of one unit sit in LDS at once (the anchors' ranks cut
+// into 32-rank chunks, at most kResMaxChunks of them and 160 KB as hi/lo), so a wave streams its tokens through
+// all anchors in one pass, the way kvc_apply streams them through one state.  Used whenever the chunks fit; the
+// kernels above (one anchor's basis at a time) take the rest.
+// ---------------------------------------------------------------------------------------------------------------
+
+constexpr int kResWaves = 8;
+constexpr int kResThreads = kResWaves * kWave;
+constexpr int kResTiles = 8;                            // 16-token tiles per wave
+constexpr int kResChunk = kResWaves * kResTiles * 16;  // 1024 tokens per workgroup
+constexpr size_t kResMaxLds = 160 * 1024;
+
+// LDS holds hi [D][32 NC] then lo; the 16-byte granule (8 ranks) q of feature row f sits at q ^ res_swz(f), a
+// swizzle inside each 32-rank chunk that spreads the staging stores (consecutive f) and the fragment reads (the
+// features of one MFMA tile) over the banks.
+__device__ __forceinline__ int res_swz(int f) { return ((f >> 1) & 1) | (((f >> 3) & 1) << 1); }
+
+__device__ __forceinline__ bf16x8 res_frag(const uint16_t* s, int kpt, int f, int c, int g) {
+  return as_bf16x8(*reinterpret_cast<const u32x4*>(s + f * kpt + 8 * (4 * c + (g ^ res_swz(f)))));
+}
+
+// Every chunk of unit `unit` into LDS: a thread takes (feature f, eight ranks of one chunk); the lanes of a wave
+// take 64 consecutive features, so each of the eight 4-byte loads is one coalesced 256-byte row segment.
+template <int D>
+__device__ __forceinline__ void stage_stacked(const AnchorArgs& a, int64_t unit, uint16_t* s_hi, uint16_t* s_lo) {
+  const int NC = a.num_chunks, kpt = 32 * NC, items = D * 4 * NC;
+  for (int base = 0; base < items; base += kResThreads) {
+    const int idx = base + (int)threadIdx.x;
+    if (idx >= items) break;  // whole waves: items is a multiple of 64
+    const int q = __builtin_amdgcn_readfirstlane(idx / D);  // the same for the 64 lanes of a wave
+    const int f = idx - q * D;
+    const int c = q >> 2, v = a.chunk_anchor[c], k0 = a.chunk_k0[c] + 8 * (q & 3), r = a.rank[v];
+    const float* b = a.basis[v] + unit * (int64_t)r * D + f;
+    float x[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = k0 + e < r ? b[(int64_t)(k0 + e) * D] : 0.0f;
+    u32x4 hi, lo;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      uint32_t hh, ll;
+      split_bf16x2(x[2 * p], x[2 * p + 1], hh, ll);
+      hi[p] = hh;
+      lo[p] = ll;
+    }
+    const int off = f * kpt + 8 * ((q & ~3) | ((q & 3) ^ res_swz(f)));
+    *reinterpret_cast<u32x4*>(s_hi + off) = hi;
+    *reinterpret_cast<u32x4*>(s_lo + off) = lo;
+  }
+}
+
+// Eq. 8 with every anchor resident: per 16-token tile the accumulator starts from the source rows in fp32 and
+// takes sum_c (w_v A_v)[t, chunk c] B_v[chunk c] over all chunks (weight-scaled coefficients split hi/lo, three
+// MFMAs per fragment), then one rounding.
+template <int D>
+__global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArgs a) {
+  constexpr int MT = D / 16, NQ = D / 32, NCM = kResMaxChunks;
+  extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
+  const int NC = a.num_chunks, kpt = 32 * NC;
+  uint16_t* s_hi = reinterpret_cast<uint16_t*>(anchor_lds);
+  uint16_t* s_lo = s_hi + D * kpt;
+
+  const int lrel = blockIdx.z, layer = a.layer_begin + lrel;
+  const int H = a.pv.num_kv_heads;
+  const int kv = blockIdx.y / H, head = blockIdx.y - kv * H;
+  const int T = a.num_tokens, Ts = a.num_weighted, V = a.num_anchors;
+  const int t_begin = blockIdx.x * kResChunk;
+  if (t_begin >= T) return;  // whole workgroup
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave, g = lane >> 4, n = lane & 15;
+  const int64_t unit = unit_index(layer, kv, head, H);
+  const uint16_t* src_pool = static_cast<const uint16_t*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
+  uint16_t* dst_pool = static_cast<uint16_t*>(const_cast<void*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]));
+  const float* wrow = a.weights + (int64_t)(lrel * 2 + kv) * Ts * V;
+  if (t_begin < Ts) {  // whole workgroup
+    stage_stacked<D>(a, unit, s_hi, s_lo);
+    __syncthreads();
+  }
+
+  struct Tile {
+    u32x4 raw[NQ];
+    u32x4 cw[NCM];
+    float w[NCM];
+    int64_t dof;
+  };
+  auto load_tile = [&](int j, Tile& tl) __attribute__((always_inline)) {
+    const int t = t_begin + (j * kResWaves + wave) * 16 + n;
+    const bool valid = t < T, crow = t < Ts;
+    tl.dof = valid ? row_offset(a.pv, a.dst_table, a.dst_offset, t, head) : -1;
+    load_row_segments<NQ>(src_pool, valid ? row_offset(a.pv, a.src_table, a.src_offset, t, head) : -1, g, tl.raw);
+#pragma unroll
+    for (int c = 0; c < NCM; ++c) {
+      tl.cw[c] = u32x4{0u, 0u, 0u, 0u};
+      tl.w[c] = 0.0f;
+      if (c < NC && crow) {
+        const int v = a.chunk_anchor[c], r = a.rank[v];
+        const uint16_t* coef = static_cast<const uint16_t*>(a.coef[v]) + unit * (int64_t)a.tokens[v] * r;
+        tl.cw[c] = load_coef8(coef, r, t, a.chunk_k0[c] + 8 * g);
+        tl.w[c] = wrow[(int64_t)t * V + v];
+      }
+    }
+  };
+  auto finish_tile = [&](int j, const Tile& tl) __attribute__((always_inline)) {
+    const int t0 = t_begin + (j * kResWaves + wave) * 16, t = t0 + n;
+    u32x4 outw[NQ];
+    if (t0 < Ts) {  // uniform over the wave
+      f32x4 acc[MT];
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        acc[2 * q] = f32x4{bf16_lo_to_f32(tl.raw[q][0]), bf16_hi_to_f32(tl.raw[q][0]),
+                           bf16_lo_to_f32(tl.raw[q][1]), bf16_hi_to_f32(tl.raw[q][1])};
+        acc[2 * q + 1] = f32x4{bf16_lo_to_f32(tl.raw[q][2]), bf16_hi_to_f32(tl.raw[q][2]),
+                               bf16_lo_to_f32(tl.raw[q][3]), bf16_hi_to_f32(tl.raw[q][3])};
+      }
+#pragma unroll
+      for (int c = 0; c < NCM; ++c) {
+        if (c >= NC) break;
+        int kc = kpt;
+        asm volatile("" : "+s"(kc));  // keeps the fragment reads in this chunk's step (not hoisted out of the tiles)
+        u32x4 ch, cl;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          uint32_t hh, ll;
+          split_bf16x2(tl.w[c] * bf16_lo_to_f32(tl.cw[c][i]), tl.w[c] * bf16_hi_to_f32(tl.cw[c][i]), hh, ll);
+          ch[i] = hh;
+          cl[i] = ll;
+        }
+        const bf16x8 bh = as_bf16x8(ch), bl = as_bf16x8(cl);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const int f = mfma_row_feature(mt, n);
+          const bf16x8 fl = res_frag(s_lo, kc, f, c, g), fh = res_frag(s_hi, kc, f, c, g);
+          acc[mt] = mfma16x16x32(fl, bh, acc[mt]);
+          acc[mt] = mfma16x16x32(fh, bl, acc[mt]);
+          acc[mt] = mfma16x16x32(fh, bh, acc[mt]);
+        }
+      }
+      const bool crow = t < Ts;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const f32x4 x = acc[2 * q], y = acc[2 * q + 1];
+        const u32x4 c = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(y[0], y[1]),
+                         pack_bf16x2(y[2], y[3])};
+        outw[q] = crow ? c : tl.raw[q];
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) outw[q] = tl.raw[q];
+    }
+    if (tl.dof >= 0) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) *reinterpret_cast<u32x4*>(dst_pool + tl.dof + 32 * q + 8 * g) = outw[q];
+    }
+  };
+
+  // no software prefetch: eight waves per CU keep enough tiles in flight (as in kvc_apply)
+  for (int j = 0; j < kResTiles; ++j) {
+    if (t_begin + (j * kResWaves + wave) * 16 >= T) break;  // uniform over the wave
+    Tile cur;
+    load_tile(j, cur);
+    finish_tile(j, cur);
+  }
+}
+
+// Distances with every anchor of one head resident: a workgroup covers 1024 tokens of one (layer, K/V) and walks
+// the heads, staging each head's anchors once.  Per tile and anchor the reconstruction A_v B_v accumulates over the
+// anchor's chunks (bf16 coefficients are exact MFMA operands, B as hi/lo), then |x - recon| (weights) or
+// (x - recon)^2 (gate) is summed over the row.  Lane (g, n) keeps the sums of anchors v = 4u + g of its tiles'
+// token n in registers across heads.
+template <int D, bool GATE>
+__global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a) {
+  constexpr int MT = D / 16, NQ = D / 32, NCM = kResMaxChunks, TPW = kResTiles;
+  static_assert(KVC_MAX_ANCHORS <= 16, "four anchors per lane group");
+  extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
+  const int NC = a.num_chunks, kpt = 32 * NC;
+  uint16_t* s_hi = reinterpret_cast<uint16_t*>(anchor_lds);
+  uint16_t* s_lo = s_hi + D * kpt;
+
+  const int lrel = blockIdx.z, layer = a.layer_begin + lrel;
+  const int kv = GATE ? 1 : blockIdx.y;
+  const int H = a.pv.num_kv_heads, V = a.num_anchors;
+  const int Tl = a.num_weighted;
+  const int t_begin = blockIdx.x * kResChunk;
+  if (t_begin >= Tl) return;  // whole workgroup
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave, g = lane >> 4, n = lane & 15;
+  const uint16_t* pool = static_cast<const uint16_t*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
+
+  float dist[TPW][4];
+#pragma unroll
+  for (int j = 0; j < TPW; ++j)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) dist[j][u] = 0.0f;
+
+  struct Tile {
+    u32x4 raw[NQ];
+    u32x4 cw[NCM];
+  };
+  for (int h = 0; h < H; ++h) {
+    const int64_t unit = unit_index(layer, kv, h, H);
+    if (h > 0) __syncthreads();  // every wave is done with the previous head's bases
+    stage_stacked<D>(a, unit, s_hi, s_lo);
+    __syncthreads();
+    auto load_tile = [&](int j, Tile& tl) __attribute__((always_inline)) {
+      const int t = t_begin + (j * kResWaves + wave) * 16 + n;
+      const bool valid = t < Tl;
+      load_row_segments<NQ>(pool, valid ? row_offset(a.pv, a.src_table, a.src_offset, t, h) : -1, g, tl.raw);
+#pragma unroll
+      for (int c = 0; c < NCM; ++c) {
+        tl.cw[c] = u32x4{0u, 0u, 0u, 0u};
+        if (c < NC && valid) {
+          const int v = a.chunk_anchor[c], r = a.rank[v];
+          const uint16_t* coef = static_cast<const uint16_t*>(a.coef[v]) + unit * (int64_t)a.tokens[v] * r;
+          tl.cw[c] = load_coef8(coef, r, t, a.chunk_k0[c] + 8 * g);
+        }
+      }
+    };
+    // dist[0] always belongs to the current tile: the array is rotated by one after every tile (static register
+    // indices with a rolled tile loop), so after TPW tiles dist[j] is tile j's again
+#pragma unroll 1
+    for (int j = 0; j < TPW; ++j) {
+      const int t0 = t_begin + (j * kResWaves + wave) * 16;
+      if (t0 < Tl) {  // uniform over the wave
+        Tile cur;
+        load_tile(j, cur);
+        const bool valid = t0 + n < Tl;
+        f32x4 acc[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NCM; ++c) {
+          if (c < NC) {  // a guard, not a break: the loop must unroll fully (cw stays in registers)
+          int kc = kpt;
+          asm volatile("" : "+s"(kc));  // keeps the fragment reads in this chunk's step
+          const bf16x8 cb = as_bf16x8(cur.cw[c]);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            const int f = mfma_row_feature(mt, n);
+            acc[mt] = mfma16x16x32(res_frag(s_lo, kc, f, c, g), cb, acc[mt]);
+            acc[mt] = mfma16x16x32(res_frag(s_hi, kc, f, c, g), cb, acc[mt]);
+          }
+          if (a.chunk_last[c]) {  // uniform: anchor v's reconstruction is complete
+            float s = 0.0f;
+#pragma unroll
+            for (int q = 0; q < NQ; ++q) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const uint32_t w = cur.raw[q][e >> 1];
+                const float x = (e & 1) ? bf16_hi_to_f32(w) : bf16_lo_to_f32(w);
+                const float diff = x - acc[2 * q + (e >> 2)][e & 3];
+                s += GATE ? diff * diff : fabsf(diff);
+              }
+            }
+            s += __shfl_xor(s, 16, kWave);
+            s += __shfl_xor(s, 32, kWave);
+            s = valid ? s : 0.0f;
+            const int v = a.chunk_anchor[c];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) dist[0][u] += (v == 4 * u + g) ? s : 0.0f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+          }
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float d0 = dist[0][u];
+#pragma unroll
+        for (int jj = 0; jj + 1 < TPW; ++jj) dist[jj][u] = dist[jj + 1][u];
+        dist[TPW - 1][u] = d0;
+      }
+    }
+  }
+  __syncthreads();  // the bases are no longer read: LDS now holds the per-token (or per-wave) sums
+  float* s_d = reinterpret_cast<float*>(anchor_lds);
+  if (GATE) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      float p = 0.0f;
+#pragma unroll
+      for (int j = 0; j < TPW; ++j) p += dist[j][u];
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) p += __shfl_xor(p, o, kWave);
+      if (n == 0 && 4 * u + g < V) s_d[wave * V + 4 * u + g] = p;
+    }
+    __syncthreads();
+    if (threadIdx.x < V) {
+      const int v = threadIdx.x;
+      float s = 0.0f;
+      for (int w = 0; w < kResWaves; ++w) s += s_d[w * V + v];
+      a.gate_partials[((int64_t)lrel * a.gate_chunks + blockIdx.x) * V + v] = s;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < TPW; ++j) {
+      const int tok = (j * kResWaves + wave) * 16 + n;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (4 * u + g < V) s_d[tok * V + 4 * u + g] = dist[j][u];
+    }
+    __syncthreads();
+    const float inv_feat = 1.0f / (float)(H * D);
+    for (int tok = threadIdx.x; tok < kResChunk; tok += kResThreads) {
+      const int t = t_begin + tok;
+      if (t >= Tl) break;
+      float dmin = INFINITY;
+      for (int v = 0; v < V; ++v) dmin = fminf(dmin, s_d[tok * V + v] * inv_feat);
+      float sum = 0.0f;
+      for (int v = 0; v < V; ++v) sum += __expf(-(s_d[tok * V + v] * inv_feat - dmin) * a.inv_temperature);
+      const float inv = 1.0f / sum;
+      float* wout = a.weights + ((int64_t)(lrel * 2 + kv) * Tl + t) * V;
+      for (int v = 0; v < V; ++v) wout[v] = __expf(-(s_d[tok * V + v] * inv_feat - dmin) * a.inv_temperature) * inv;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------------------------------------------
 
@@ -458,12 +781,39 @@ size_t anchor_lds_bytes(int D, int max_rank, kvc_dtype dtype, int which) {
 }
 
 template <typename K>
-static hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, const AnchorArgs& a, hipStream_t stream) {
+static hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, const AnchorArgs& a, hipStream_t stream,
+                                  int threads = kAnchorThreads) {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
                                      (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(kernel, grid, dim3(kAnchorThreads), lds, stream, a);
+  hipLaunchKernelGGL(kernel, grid, dim3(threads), lds, stream, a);
   return hipGetLastError();
+}
+
+// The chunk map of the resident-basis kernels (bf16); false when the anchors' chunks do not fit in LDS at once.
+static bool plan_resident(AnchorArgs& a) {
+  int nc = 0;
+  for (int v = 0; v < a.num_anchors; ++v) {
+    const int ks = std::max(1, (a.rank[v] + 31) / 32);
+    for (int k = 0; k < ks; ++k) {
+      if (nc == kResMaxChunks) return false;
+      a.chunk_anchor[nc] = v;
+      a.chunk_k0[nc] = 32 * k;
+      a.chunk_last[nc] = k == ks - 1;
+      ++nc;
+    }
+  }
+  a.num_chunks = nc;
+  return (size_t)a.pv.head_dim * 32 * nc * 2 * sizeof(uint16_t) <= kResMaxLds;
+}
+
+// which: 0 weights, 1 apply, 2 gate
+static size_t res_lds_bytes(const AnchorArgs& a, int which) {
+  const size_t basis = (size_t)a.pv.head_dim * 32 * a.num_chunks * 2 * sizeof(uint16_t);
+  const size_t sums = which == 0   ? (size_t)kResChunk * a.num_anchors * sizeof(float)
+                      : which == 2 ? (size_t)kResWaves * a.num_anchors * sizeof(float)
+                                   : 0;
+  return std::max(basis, sums);
 }
 
 template <int D, bool GATE>
@@ -491,6 +841,13 @@ hipError_t launch_anchor_weights(const AnchorArgs& a, kvc_dtype dtype, hipStream
   const int D = a.pv.head_dim;
   const size_t lds = anchor_lds_bytes(D, a.max_rank, dtype, 0);
   if (dtype == KVC_BF16) {
+    AnchorArgs r = a;
+    if (plan_resident(r)) {
+      dim3 grid((a.num_weighted + kResChunk - 1) / kResChunk, 2, a.num_layers);
+      const size_t rl = res_lds_bytes(r, 0);
+      return D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, false>, grid, rl, r, stream, kResThreads)
+                     : launch_with_lds(anchor_dist_res_bf16<128, false>, grid, rl, r, stream, kResThreads);
+    }
     dim3 grid((a.num_weighted + kAnchorChunk - 1) / kAnchorChunk, 2, a.num_layers);
     return D == 64 ? launch_dist_bf16<64, false>(a, grid, lds, stream) : launch_dist_bf16<128, false>(a, grid, lds, stream);
   }
@@ -499,12 +856,20 @@ hipError_t launch_anchor_weights(const AnchorArgs& a, kvc_dtype dtype, hipStream
                  : launch_with_lds(anchor_dist_f32<128, false>, grid, lds, a, stream);
 }
 
-hipError_t launch_gate_distances(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream) {
+hipError_t launch_gate_distances(const AnchorArgs& args, kvc_dtype dtype, hipStream_t stream) {
+  AnchorArgs a = args;
   const int D = a.pv.head_dim;
   const size_t lds = anchor_lds_bytes(D, a.max_rank, dtype, 2);
   hipError_t e;
   dim3 grid(a.gate_chunks, 1, a.num_layers);
-  if (dtype == KVC_BF16) {
+  if (dtype == KVC_BF16 && plan_resident(a)) {
+    // fewer, larger chunks than the workspace was sized for
+    a.gate_chunks = (a.num_weighted + kResChunk - 1) / kResChunk;
+    grid.x = a.gate_chunks;
+    const size_t rl = res_lds_bytes(a, 2);
+    e = D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, true>, grid, rl, a, stream, kResThreads)
+                : launch_with_lds(anchor_dist_res_bf16<128, true>, grid, rl, a, stream, kResThreads);
+  } else if (dtype == KVC_BF16) {
     e = D == 64 ? launch_dist_bf16<64, true>(a, grid, lds, stream) : launch_dist_bf16<128, true>(a, grid, lds, stream);
   } else {
     e = D == 64 ? launch_with_lds(anchor_dist_f32<64, true>, grid, lds, a, stream)
@@ -520,6 +885,13 @@ hipError_t launch_apply_anchored(const AnchorArgs& a, kvc_dtype dtype, hipStream
   const int D = a.pv.head_dim;
   const size_t lds = anchor_lds_bytes(D, a.max_rank, dtype, 1);
   if (dtype == KVC_BF16) {
+    AnchorArgs r = a;
+    if (plan_resident(r)) {
+      dim3 grid((a.num_tokens + kResChunk - 1) / kResChunk, 2 * a.pv.num_kv_heads, a.num_layers);
+      const size_t rl = res_lds_bytes(r, 1);
+      return D == 64 ? launch_with_lds(apply_anchored_res_bf16<64>, grid, rl, r, stream, kResThreads)
+                     : launch_with_lds(apply_anchored_res_bf16<128>, grid, rl, r, stream, kResThreads);
+    }
     dim3 grid((a.num_tokens + kAnchoredChunk - 1) / kAnchoredChunk, 2 * a.pv.num_kv_heads, a.num_layers);
     return D == 64 ? launch_anchored_bf16<64>(a, grid, lds, stream) : launch_anchored_bf16<128>(a, grid, lds, stream);
   }

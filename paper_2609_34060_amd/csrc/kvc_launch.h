@@ -84,6 +84,8 @@ struct ChainArgs {
 hipError_t launch_chain(const ChainArgs& a, const EigArgs& ea, hipStream_t stream);
 
 // Anchors (kvc_anchor.hip): distances / weights, anchored apply, gate distances.  One item per call.
+constexpr int kResMaxChunks = 10;  // 32-rank chunks of all anchors of one unit held in LDS at once
+
 struct AnchorArgs {
   PoolView pv;
   LayerPtrs layers;
@@ -104,6 +106,11 @@ struct AnchorArgs {
   float* gate_partials;        // [num_layers][chunks][num_anchors] sums of squares (gate)
   int32_t gate_chunks;
   float* distances;            // [num_anchors] (gate)
+  // resident-basis kernels: the anchors' ranks cut into 32-rank chunks (an anchor of rank 0 keeps one zero chunk)
+  int32_t num_chunks;
+  int32_t chunk_anchor[kResMaxChunks];
+  int32_t chunk_k0[kResMaxChunks];
+  int32_t chunk_last[kResMaxChunks];  // 1 on an anchor's last chunk
 };
 int anchor_chunk_tokens();
 size_t anchor_lds_bytes(int head_dim, int max_rank, kvc_dtype dtype, int which);

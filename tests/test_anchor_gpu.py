@@ -45,10 +45,13 @@ def _setup(name, layers, num_tokens=None):
     return w, pc, cache, T, src, dst, tab
 
 
+# The first three cases fit every anchor's basis in LDS at once (at most ten 32-rank chunks); the last one does not
+# and takes the one-anchor-at-a-time kernels.
 @pytest.mark.parametrize("name,layers,ranks,Ts", [
     ("tiny", 2, [8, 4, 8], 200),
     ("llama8b_4k", 2, [32] * 10, 4096),
     ("llama8b_4k", 1, [16, 32, 48, 8, 40], 1531),
+    ("llama8b_4k", 1, [64, 48, 64, 40, 64, 56], 2050),
 ])
 def test_anchor_weights_and_anchored_apply(name, layers, ranks, Ts):
     w, pc, cache, T, src, dst, tab = _setup(name, layers, num_tokens=None)
@@ -117,10 +120,12 @@ def test_anchored_apply_with_one_anchor_matches_kvc_apply():
         assert bool(ok.all()), float((a32 - b32).abs().nan_to_num().max())
 
 
-@pytest.mark.parametrize("name,layers,prefix", [("tiny", 2, 100), ("llama8b_4k", 3, 1000), ("llama8b_4k", 2, 4096)])
-def test_gate_distances_and_decision(name, layers, prefix):
+@pytest.mark.parametrize("name,layers,prefix,ranks", [("tiny", 2, 100, [8, 8, 8]),
+                                                      ("llama8b_4k", 3, 1000, [32] * 4),
+                                                      ("llama8b_4k", 2, 4096, [32] * 4),
+                                                      ("llama8b_4k", 1, 1500, [96, 96, 64, 96])])
+def test_gate_distances_and_decision(name, layers, prefix, ranks):
     w, pc, cache, T, src, dst, tab = _setup(name, layers, num_tokens=None)
-    ranks = [8, 8, 8] if name == "tiny" else [32, 32, 32, 32]
     bases = _anchor_states(w, layers, T, ranks, [(0.1 + 0.9 * v) / np.sqrt(r / w.head_dim)
                                                  for v, r in enumerate(ranks)], 6)
     anchors = kvc.Anchors(bases, T, layers, weights=torch.empty(0, device="cuda"))
