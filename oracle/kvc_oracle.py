@@ -9,19 +9,23 @@ Everything is plain float64 NumPy, written to be checked against the paper by ey
   * apply     -- Eq. 4 with the source agent's materialised cache as the reference (Section 3.2, Eq. 6) and a
                  single state (Eq. 8 with V = 1, w = 1): C_hat_j = C_i + A B, rows past the state's coverage copied
                  (Appendix A.3, "Variable Segment Lengths").  One round-to-nearest-even to the storage dtype.
-  * fit       -- Eq. 12 observed transition Z = C_j - Align(C_i) (Align = identity) and the rank-r truncated SVD of
-                 Eq. 7: A = U_r Sigma_r, B = R_r^T.  Also Z = C_j for a base cache (Section 3.3, Z in {C, Delta}).
+  * fit       -- Eq. 12 observed transition Z = C_j - Align(C_i) (in canonical coordinates for rotary keys) and the
+                 rank-r truncated SVD of Eq. 7: A = U_r Sigma_r, B = R_r^T.  Also Z = C_j for a base cache
+                 (Section 3.3, Z in {C, Delta}).
   * chain     -- Eq. 6: Delta_{k<-i} = Delta_{k<-j} + Delta_{j<-i}; the composed state is the rank-r truncated SVD
                  (Eq. 7) of the materialised sum A1 B1 + A2 B2.
   * anchors   -- Eq. 8 with V anchors and token-wise weights: interpolation weights from the mean absolute distance
                  of the source cache to each anchor's reconstructed base, softmax with T = 1, weighted sum of the
                  anchors' corrections (Appendix A.3, "Correction Weighting"); the reliability gate of Eq. 9-11 and
                  the anchor pool's insertion / least-frequently-used eviction rule (Appendix A.3).
+  * rope      -- positional alignment of the key rows (Section 2.2, Appendix A.3 "Positional Alignment"): keys are
+                 compared, fitted and corrected in canonical coordinates (segment token t at position t) and the
+                 corrected keys are rotated to their target positions; values are never rotated.
   * metrics   -- normalised Frobenius error (Appendix A.1), effective rank at 90 % of the singular-value energy
                  (Section 3.1, Figure 2 caption), memory accounting O(VNLD) vs O(VNr(L+D)) (Sections 3.1, 3.3).
 
 Readings of the paper taken here (all listed in the design notes): factorisation per (layer, K/V, KV head);
-Align = identity; canonical sign = largest-magnitude basis entry positive (lowest index on ties); the state's
+Align = the rotary re-alignment of the keys (identity for a cache without rotary encoding, or at equal positions); canonical sign = largest-magnitude basis entry positive (lowest index on ties); the state's
 coefficients are stored in the cache dtype, bases and singular values in float32.
 """
 from __future__ import annotations
@@ -91,13 +95,46 @@ def to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
 # ------------------------------------------------------------------------------------------------------------------
 
 @dataclasses.dataclass
+class Rope:
+    """Rotary position encoding of the key rows: feature pair i of a key at position p is rotated by the angle
+    p * inv_freq[i].  style "half" pairs feature i with i + d/2 (the rotate-half layout of Llama and Qwen models),
+    "pairs" pairs 2i with 2i + 1.  inv_freq: float64 [d/2]."""
+    inv_freq: np.ndarray
+    style: str = "half"
+
+    def pair_index(self, d: int):
+        """Feature indices (a, b) of the d/2 rotation pairs."""
+        i = np.arange(d // 2)
+        return (i, i + d // 2) if self.style == "half" else (2 * i, 2 * i + 1)
+
+
+def rope_rotate(rows: np.ndarray, position, rope: Rope) -> np.ndarray:
+    """Rotate key rows [..., d] to `position` (a scalar, or one position per row): every pair (a, b) becomes
+    (a cos th - b sin th, a sin th + b cos th) with th = position * inv_freq[i].  float64 in and out."""
+    rows = np.asarray(rows, dtype=np.float64)
+    ia, ib = rope.pair_index(rows.shape[-1])
+    pos = np.asarray(position, dtype=np.float64)
+    theta = (pos[..., None] if pos.ndim else pos) * np.asarray(rope.inv_freq, dtype=np.float64)
+    c, s = np.cos(theta), np.sin(theta)
+    out = rows.copy()
+    a, b = rows[..., ia], rows[..., ib]
+    out[..., ia] = a * c - b * s
+    out[..., ib] = a * s + b * c
+    return out
+
+
+@dataclasses.dataclass
 class Cache:
     """Paged K/V pools: k[layer] and v[layer] are arrays [num_blocks, block_size, num_kv_heads, head_dim] holding
-    float32 values or bfloat16 bit patterns (uint16)."""
+    float32 values or bfloat16 bit patterns (uint16).  `rope` set: the key rows carry rotary position encoding."""
     dtype: str
     block_size: int
     k: List[np.ndarray]
     v: List[np.ndarray]
+    rope: Optional[Rope] = None
+
+    def copy(self) -> "Cache":
+        return Cache(self.dtype, self.block_size, [a.copy() for a in self.k], [a.copy() for a in self.v], self.rope)
 
     @property
     def num_layers(self) -> int:
@@ -144,13 +181,32 @@ class State:
 @dataclasses.dataclass
 class Item:
     """One shared segment: rows t < num_tokens read from the src block sequence and written to / compared with the
-    dst block sequence.  A table of None maps block index b to physical block b (contiguous rows)."""
+    dst block sequence.  A table of None maps block index b to physical block b (contiguous rows).  With a rotary
+    cache, segment token t sits at position src_position + t in the source agent's context and dst_position + t in
+    the target's (canonical coordinates put it at t)."""
     num_tokens: int
     src_offset: int
     dst_offset: int
     src_table: Optional[np.ndarray]
     dst_table: Optional[np.ndarray]
     state: Optional[State] = None
+    src_position: int = 0
+    dst_position: int = 0
+
+
+def to_canonical(rows_f64: np.ndarray, cache: "Cache", kv: int, position: int) -> np.ndarray:
+    """Key rows of a segment starting at `position` in canonical coordinates (rotated back by `position`); values,
+    and keys of a cache without rotary encoding, are returned as they are."""
+    if kv == 1 or cache.rope is None:
+        return rows_f64
+    return rope_rotate(rows_f64, -position, cache.rope)
+
+
+def to_target(rows_f64: np.ndarray, cache: "Cache", kv: int, position: int) -> np.ndarray:
+    """Canonical key rows rotated to a segment starting at `position` (values unchanged)."""
+    if kv == 1 or cache.rope is None:
+        return rows_f64
+    return rope_rotate(rows_f64, position, cache.rope)
 
 
 # ------------------------------------------------------------------------------------------------------------------
@@ -230,17 +286,40 @@ def correct_rows(src: np.ndarray, coef: np.ndarray, basis: np.ndarray, dtype: st
     return out
 
 
+def materialise_aligned(src: np.ndarray, corr: np.ndarray, dtype: str, rope: Rope, src_position: int,
+                        dst_position: int) -> np.ndarray:
+    """Key rows of a rotary cache (Appendix A.3, positional alignment): the source keys are taken to canonical
+    coordinates, the canonical correction (float64, covering the first corr.shape[0] rows) is added there, and the
+    result is rotated to the target positions, C_hat = R(p_dst) (R(-p_src) C_src + corr), one rounding.  Rows past
+    the correction keep the re-aligned source R(p_dst) R(-p_src) C_src; at equal positions they are bit copies."""
+    out = np.array(src, copy=True)
+    canon = rope_rotate(to_f64(src, dtype), -src_position, rope)
+    ts = corr.shape[0]
+    canon[:ts] += corr
+    n = out.shape[0] if src_position != dst_position else ts
+    if n > 0:
+        out[:n] = to_storage(rope_rotate(canon[:n], dst_position, rope), dtype)
+    return out
+
+
 def apply(cache: Cache, items: Sequence[Item], layer_begin: int = 0, layer_end: Optional[int] = None) -> Cache:
-    """Materialise each item's target cache from its source rows and state; returns a new Cache (src untouched)."""
+    """Materialise each item's target cache from its source rows and state; returns a new Cache (src untouched).
+    Keys of a rotary cache are corrected in canonical coordinates and rotated to the item's target positions."""
     layer_end = cache.num_layers if layer_end is None else layer_end
-    out = Cache(cache.dtype, cache.block_size, [a.copy() for a in cache.k], [a.copy() for a in cache.v])
+    out = cache.copy()
     for it in items:
         st = it.state
         for layer in range(layer_begin, layer_end):
             for kv in range(2):
                 for h in range(cache.num_kv_heads):
                     src = read_rows(cache, layer, kv, h, it.src_table, it.src_offset, it.num_tokens)
-                    if st is None or st.rank == 0:
+                    empty = st is None or st.rank == 0
+                    if kv == 0 and cache.rope is not None:
+                        corr = np.zeros((0, cache.head_dim)) if empty else \
+                            st.coef_f64(layer, kv, h) @ st.basis_f64(layer, kv, h)
+                        rows = materialise_aligned(src, corr, cache.dtype, cache.rope, it.src_position,
+                                                   it.dst_position)
+                    elif empty:
                         rows = src.copy()
                     else:
                         rows = correct_rows(src, st.coef_f64(layer, kv, h), st.basis_f64(layer, kv, h), cache.dtype)
@@ -282,11 +361,13 @@ def fit(cache: Cache, items: Sequence[Item], rank: int, coef_dtype: Optional[str
         for layer in range(layer_begin, layer_end):
             for kv in range(2):
                 for h in range(H):
-                    dst = read_rows(cache, layer, kv, h, it.dst_table, it.dst_offset, Ts)
-                    src = None
+                    # Eq. 12 in canonical coordinates: Z = R(-p_dst) C_dst - R(-p_src) C_src for rotary keys
+                    z = to_canonical(to_f64(read_rows(cache, layer, kv, h, it.dst_table, it.dst_offset, Ts),
+                                            cache.dtype), cache, kv, it.dst_position)
                     if mode == MODE_DELTA:
-                        src = read_rows(cache, layer, kv, h, it.src_table, it.src_offset, Ts)
-                    a, b, s = fit_unit(src, dst, cache.dtype, rank)
+                        z = z - to_canonical(to_f64(read_rows(cache, layer, kv, h, it.src_table, it.src_offset, Ts),
+                                                    cache.dtype), cache, kv, it.src_position)
+                    a, b, s = truncated_svd(z, rank)
                     coef[layer, kv, h] = a
                     basis[layer, kv, h] = b
                     sigma[layer, kv, h] = s
@@ -395,8 +476,8 @@ def anchor_distances(cache: Cache, item: Item, bases: Sequence[State], num_token
             for v, base in enumerate(bases):
                 total = np.zeros(num_tokens)
                 for h in range(H):
-                    src = to_f64(read_rows(cache, layer, kv, h, item.src_table, item.src_offset, num_tokens),
-                                 cache.dtype)
+                    src = to_canonical(to_f64(read_rows(cache, layer, kv, h, item.src_table, item.src_offset,
+                                                        num_tokens), cache.dtype), cache, kv, item.src_position)
                     recon = base.coef_f64(layer, kv, h)[:num_tokens] @ base.basis_f64(layer, kv, h)
                     total += np.abs(src - recon).sum(axis=1)
                 out[li, kv, :, v] = total / (H * d)
@@ -415,18 +496,22 @@ def apply_anchored(cache: Cache, item: Item, deltas: Sequence[State], weights: n
     """Eq. 8 with token-wise weights: C_hat[t] = C_src[t] + sum_v w[l, kv, t, v] (A_v B_v)[t] for t < num_tokens,
     bit copy for num_tokens <= t < item.num_tokens; one rounding to the storage dtype.  Returns a new Cache."""
     layer_end = cache.num_layers if layer_end is None else layer_end
-    out = Cache(cache.dtype, cache.block_size, [a.copy() for a in cache.k], [a.copy() for a in cache.v])
+    out = cache.copy()
     for li, layer in enumerate(range(layer_begin, layer_end)):
         for kv in range(2):
             for h in range(cache.num_kv_heads):
                 src = read_rows(cache, layer, kv, h, item.src_table, item.src_offset, item.num_tokens)
-                rows = np.array(src, copy=True)
-                if num_tokens > 0:
-                    corr = np.zeros((num_tokens, cache.head_dim))
-                    for v, delta in enumerate(deltas):
-                        prod = delta.coef_f64(layer, kv, h)[:num_tokens] @ delta.basis_f64(layer, kv, h)
-                        corr += weights[li, kv, :, v][:, None] * prod
-                    rows[:num_tokens] = to_storage(to_f64(src[:num_tokens], cache.dtype) + corr, cache.dtype)
+                corr = np.zeros((num_tokens, cache.head_dim))
+                for v, delta in enumerate(deltas):
+                    prod = delta.coef_f64(layer, kv, h)[:num_tokens] @ delta.basis_f64(layer, kv, h)
+                    corr += weights[li, kv, :, v][:, None] * prod
+                if kv == 0 and cache.rope is not None:
+                    rows = materialise_aligned(src, corr, cache.dtype, cache.rope, item.src_position,
+                                               item.dst_position)
+                else:
+                    rows = np.array(src, copy=True)
+                    if num_tokens > 0:
+                        rows[:num_tokens] = to_storage(to_f64(src[:num_tokens], cache.dtype) + corr, cache.dtype)
                 write_rows(out, layer, kv, h, item.dst_table, item.dst_offset, rows)
     return out
 

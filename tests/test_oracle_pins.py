@@ -572,3 +572,136 @@ def test_anchor_pool_evicts_least_used_of_five_oldest():
     assert pool.insert(8, 5) == (1, 6)
     # eligibility by stored length: ids 0, 2, 3, 4 have lengths 10, 12, 13, 14; id 7: 30; id 8: 5
     assert pool.eligible(12) == [2, 3, 4, 5] and pool.eligible(31) == [] and len(pool.eligible(0)) == 6
+
+
+# ----------------------------------------------------------------------- rotary positional alignment (Appendix A.3)
+
+def _llama_inv_freq(d, theta=500000.0):
+    return theta ** (-np.arange(0, d, 2, dtype=np.float64) / d)
+
+
+@pytest.mark.parametrize("style", ["half", "pairs"])
+def test_rope_rotation_matches_complex_multiplication(style):
+    """The rotation of each feature pair is multiplication of the complex number a + ib by e^{i theta}."""
+    rng = np.random.default_rng(31)
+    d, T = 16, 5
+    rope = O.Rope(_llama_inv_freq(d, 10000.0), style)
+    x = rng.standard_normal((T, d))
+    pos = np.array([0, 3, 17, 4096, 32767])
+    got = O.rope_rotate(x, pos, rope)
+    if style == "half":
+        z = x[:, : d // 2] + 1j * x[:, d // 2:]
+    else:
+        z = x[:, 0::2] + 1j * x[:, 1::2]
+    w = z * np.exp(1j * np.outer(pos, rope.inv_freq))
+    ref = np.hstack([w.real, w.imag]) if style == "half" else np.stack([w.real, w.imag], axis=-1).reshape(T, d)
+    assert np.allclose(got, ref, rtol=0, atol=1e-12)
+
+
+def test_rope_worked_example():
+    """Hand-worked: d = 4, inv_freq (pi/2, pi), row (1, 2, 3, 4) at position 1.  Rotate-half pairs (1, 3) by pi/2 ->
+    (-3, 1) and (2, 4) by pi -> (-2, -4); adjacent pairs (1, 2) by pi/2 -> (-2, 1) and (3, 4) by pi -> (-3, -4)."""
+    x = np.array([[1.0, 2.0, 3.0, 4.0]])
+    inv = np.array([math.pi / 2, math.pi])
+    assert np.allclose(O.rope_rotate(x, 1, O.Rope(inv, "half")), [[-3.0, -2.0, 1.0, -4.0]], atol=1e-15)
+    assert np.allclose(O.rope_rotate(x, 1, O.Rope(inv, "pairs")), [[-2.0, 1.0, -3.0, -4.0]], atol=1e-15)
+
+
+def test_rope_group_and_relative_position_properties():
+    rng = np.random.default_rng(32)
+    d = 32
+    rope = O.Rope(_llama_inv_freq(d), "half")
+    q, k = rng.standard_normal((2, d))
+    # R(a) R(b) = R(a + b), R(0) = I, norms preserved
+    assert np.allclose(O.rope_rotate(O.rope_rotate(k, 700, rope), 1234, rope), O.rope_rotate(k, 1934, rope))
+    assert np.array_equal(O.rope_rotate(k, 0, rope), k)
+    assert math.isclose(np.linalg.norm(O.rope_rotate(k, 31000, rope)), np.linalg.norm(k))
+    # attention logits depend only on the relative position: <R(p) q, R(p') k> = <R(p - p') q, k>
+    lhs = O.rope_rotate(q, 9000, rope) @ O.rope_rotate(k, 8000, rope)
+    assert math.isclose(lhs, O.rope_rotate(q, 1000, rope) @ k, rel_tol=1e-9)
+
+
+def _rope_cache(rng, T, H, d, L, bs, dtype, rope):
+    nb = 2 * (-(-T // bs))
+    mk = lambda: [O.to_storage(rng.standard_normal((nb, bs, H, d)), dtype) for _ in range(L)]
+    return O.Cache(dtype, bs, mk(), mk(), rope)
+
+
+def test_apply_with_rope_reduces_to_plain_apply_and_rotates_keys_only():
+    """At source and target position 0 the rotary apply is the plain apply (R(0) = I); values never rotate; keys
+    with a rank-0 state are the source rotated by p_dst - p_src."""
+    rng = np.random.default_rng(33)
+    T, H, d, L, bs, r, Ts = 10, 2, 8, 2, 4, 3, 7
+    rope = O.Rope(_llama_inv_freq(d, 10000.0), "half")
+    cache = _rope_cache(rng, T, H, d, L, bs, "f32", rope)
+    plain = O.Cache("f32", bs, cache.k, cache.v)
+    coef = O.to_storage(rng.standard_normal((L, 2, H, Ts, r)), "f32")
+    basis = np.linalg.qr(rng.standard_normal((L * 2 * H, d, r)))[0].transpose(0, 2, 1).reshape(L, 2, H, r, d)
+    st = O.State(coef, basis.astype(np.float32), None, "f32")
+    dst_off = cache.k[0].shape[0] * bs // 2
+    a = O.apply(cache, [O.Item(T, 0, dst_off, None, None, st, 0, 0)])
+    b = O.apply(plain, [O.Item(T, 0, dst_off, None, None, st)])
+    for x, y in zip(a.k + a.v, b.k + b.v):
+        assert np.array_equal(O.to_f64(x, "f32"), O.to_f64(y, "f32"))
+    moved = O.apply(cache, [O.Item(T, 0, dst_off, None, None, st, 5, 4000)])
+    for x, y in zip(moved.v, b.v):
+        assert np.array_equal(x, y)
+    zero = O.State(np.zeros((L, 2, H, 0, 0), np.float32), np.zeros((L, 2, H, 0, d), np.float32), None, "f32")
+    shifted = O.apply(cache, [O.Item(T, 0, dst_off, None, None, zero, 5, 4000)])
+    for layer in range(L):
+        for h in range(H):
+            src = O.to_f64(O.read_rows(cache, layer, 0, h, None, 0, T), "f32")
+            got = O.to_f64(O.read_rows(shifted, layer, 0, h, None, dst_off, T), "f32")
+            assert np.allclose(got, O.rope_rotate(src, 3995, rope), rtol=2e-7, atol=1e-7)
+
+
+@pytest.mark.parametrize("style", ["half", "pairs"])
+def test_fit_and_apply_with_rope_recover_canonical_deviation(style):
+    """Canonical keys Kc_j = Kc_i + D (D of rank r) stored at different positions, K = R(p) Kc: the rotary fit
+    returns D itself (Eq. 12 in canonical coordinates), a fit that ignores the positions does not, and applying the
+    fitted state to K_i at p_i with target p_j reproduces K_j."""
+    rng = np.random.default_rng(34)
+    T, H, d, L, bs, r = 24, 2, 8, 1, 4, 2
+    pi, pj = 37, 5000
+    rope = O.Rope(_llama_inv_freq(d, 10000.0), style)
+    nb = 2 * (-(-T // bs))
+    kc = rng.standard_normal((nb * bs // 2, H, d))
+    dev = np.stack([rng.standard_normal((T, r)) @ rng.standard_normal((r, d)) for _ in range(H)], axis=1)
+    ki = O.rope_rotate(kc[:T], pi, rope)
+    kj = O.rope_rotate(kc[:T] + dev, pj, rope)
+    pool = np.zeros((nb * bs, H, d))
+    pool[:T], pool[nb * bs // 2: nb * bs // 2 + T] = ki, kj
+    k = [O.to_storage(pool.reshape(nb, bs, H, d), "f32")]
+    v = [O.to_storage(rng.standard_normal((nb, bs, H, d)), "f32")]
+    cache = O.Cache("f32", bs, k, v, rope)
+    item = O.Item(T, 0, nb * bs // 2, None, None, None, pi, pj)
+    states, raw = O.fit(cache, [item], r)
+    for h in range(H):
+        prod = raw[0][0][0, 0, h] @ raw[0][1][0, 0, h]
+        assert np.allclose(prod, dev[:, h], atol=2e-5)
+    _, wrong = O.fit(O.Cache("f32", bs, k, v, None), [item], r)
+    assert max(np.max(np.abs(wrong[0][0][0, 0, h] @ wrong[0][1][0, 0, h] - dev[:, h])) for h in range(H)) > 0.1
+    out = O.apply(cache, [O.Item(T, 0, nb * bs // 2, None, None, states[0], pi, pj)])
+    got = O.to_f64(out.k[0], "f32").reshape(nb * bs, H, d)[nb * bs // 2: nb * bs // 2 + T]
+    assert np.allclose(got, kj, atol=5e-5)
+
+
+def test_anchor_distance_with_rope_uses_canonical_source_keys():
+    """An anchor whose base reconstructs the canonical source keys exactly is at distance 0 for keys whatever the
+    source position; the same anchor compared without re-alignment is not."""
+    rng = np.random.default_rng(35)
+    T, H, d, L, bs, ps = 8, 2, 6, 1, 4, 321
+    rope = O.Rope(_llama_inv_freq(d, 10000.0), "half")
+    cache = _rope_cache(rng, T, H, d, L, bs, "f32", rope)
+    item = O.Item(T, 0, 0, None, None, None, ps, 0)
+    coef = np.zeros((L, 2, H, T, d))
+    for kv in range(2):
+        for h in range(H):
+            rows = O.to_f64(O.read_rows(cache, 0, kv, h, None, 0, T), "f32")
+            coef[0, kv, h] = O.rope_rotate(rows, -ps, rope) if kv == 0 else rows
+    exact = O.State(O.to_storage(coef, "f32"), np.broadcast_to(np.eye(d), (L, 2, H, d, d)).astype(np.float32),
+                    None, "f32")
+    dist = O.anchor_distances(cache, item, [exact], T)
+    assert np.allclose(dist, 0.0, atol=1e-6)
+    plain = O.anchor_distances(O.Cache("f32", bs, cache.k, cache.v), item, [exact], T)
+    assert np.all(plain[:, 0] > 0.05) and np.allclose(plain[:, 1], 0.0, atol=1e-6)
