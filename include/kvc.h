@@ -3,13 +3,16 @@
  *
  * Three operations on a paged K/V cache, all asynchronous on the caller's HIP stream:
  *
- *   kvc_fit_state  Eq. 12 then Eq. 7.  For each (layer, K/V, KV head) unit of an item, Z = C_dst - C_src over the
- *                  first T_s rows (the observed transition after a dense prefill, with identity alignment), or
- *                  Z = C_dst (a base cache, Section 3.3), and its rank-r truncated SVD Z ~ A B with A = U_r Sigma_r
- *                  (T_s x r, "coef") and B = R_r^T (r x d, "basis", orthonormal rows), plus sigma.
+ *   kvc_fit_state  Eq. 12 then Eq. 7.  For each (layer, K/V, KV head) unit of an item, Z = C_dst - Align(C_src)
+ *                  over the first T_s rows (the observed transition after a dense prefill), or Z = C_dst (a base
+ *                  cache, Section 3.3), and its rank-r truncated SVD Z ~ A B with A = U_r Sigma_r (T_s x r, "coef")
+ *                  and B = R_r^T (r x d, "basis", orthonormal rows), plus sigma.  Align is the identity, except for
+ *                  the keys of a rotary cache, which are fitted in canonical coordinates (see kvc_rope_style).
  *   kvc_apply      Eq. 4 with the source agent's materialised cache as the reference (Section 3.2, Eq. 6) and one
  *                  state (Eq. 8 with a single anchor, w = 1): C_dst[t] = C_src[t] + A[t] B for t < T_s and
- *                  C_dst[t] = C_src[t] (bit copy) for T_s <= t < T (Appendix A.3, "Variable Segment Lengths").
+ *                  C_dst[t] = C_src[t] (bit copy) for T_s <= t < T (Appendix A.3, "Variable Segment Lengths");
+ *                  the keys of a rotary cache are corrected in canonical coordinates and rotated to the target
+ *                  positions in the same pass (Appendix A.3, "Positional Alignment").
  *   kvc_chain      Eq. 6 composed in low rank: from S1 = Delta_{j<-i} and S2 = Delta_{k<-j}, the rank-r_out truncated
  *                  SVD of A1 B1 + A2 B2 (rows past a state's coverage are zero), without forming any T x d matrix.
  *
@@ -69,6 +72,17 @@ typedef enum kvc_status {
 
 typedef enum kvc_dtype { KVC_F32 = 0, KVC_BF16 = 1 } kvc_dtype;
 
+/* Rotary position encoding of the key rows (the models the method serves use RoPE).  The key of a token at context
+ * position p carries every feature pair i rotated by the angle p * inv_freq[i].  Sharing a segment across agents
+ * moves its tokens to other positions, so keys are compared, fitted and corrected in canonical coordinates
+ * (segment token t at position t) and the corrected keys are rotated to their target positions (Section 2.2,
+ * Appendix A.3 "Positional Alignment"); values are never rotated. */
+typedef enum kvc_rope_style {
+  KVC_ROPE_NONE = 0,  /* the keys carry no rotary encoding (no re-alignment anywhere) */
+  KVC_ROPE_HALF = 1,  /* pair i = features (i, i + head_dim / 2): the rotate-half layout of Llama and Qwen models */
+  KVC_ROPE_PAIRS = 2  /* pair i = features (2 i, 2 i + 1) */
+} kvc_rope_style;
+
 typedef enum kvc_fit_mode {
   KVC_FIT_DELTA = 0, /* Z = C_dst - C_src: the observed transition of Eq. 12 */
   KVC_FIT_BASE = 1   /* Z = C_dst: a base cache (Z in {C, Delta}, Section 3.3); the src side is not read */
@@ -76,7 +90,9 @@ typedef enum kvc_fit_mode {
 
 /* A paged K/V pool set.  k_layers / v_layers are HOST arrays of num_layers DEVICE pointers.  Strides are in
  * elements; block_stride, token_stride and head_stride times the element size must be multiples of 16 bytes and
- * every layer pointer 16-byte aligned.  head_dim is 64 or 128. */
+ * every layer pointer 16-byte aligned.  head_dim is 64 or 128.  rope_style says how the key rows are rotary-encoded
+ * (KVC_ROPE_NONE when they are not; a zero-initialised struct is that); with another style rope_inv_freq is a HOST
+ * array of head_dim / 2 finite angles per position step, read during the call only. */
 typedef struct kvc_cache {
   kvc_dtype dtype;
   int32_t num_layers;
@@ -89,6 +105,9 @@ typedef struct kvc_cache {
   int64_t head_stride;
   void* const* k_layers;
   void* const* v_layers;
+  int32_t rope_style;          /* kvc_rope_style */
+  int32_t rope_reserved;       /* must be 0 */
+  const double* rope_inv_freq; /* HOST [head_dim / 2], or NULL with KVC_ROPE_NONE */
 } kvc_cache;
 
 /* Low-rank state of one sequence (Eq. 7): coef = A, basis = B per unit.  DEVICE pointers.  coef_dtype is the cache
@@ -107,12 +126,16 @@ typedef struct kvc_state {
 } kvc_state;
 
 /* One shared segment of an agent edge.  apply reads `state`; fit writes it (its rank, num_tokens and pointers say
- * what to produce: rows t < state.num_tokens are fitted).  state.num_tokens <= num_tokens. */
+ * what to produce: rows t < state.num_tokens are fitted).  state.num_tokens <= num_tokens.  src_position and
+ * dst_position place the segment in the source and target agents' contexts (token t at position + t); they matter
+ * only for the keys of a rotary cache, whose states are kept in canonical coordinates. */
 typedef struct kvc_item {
-  int32_t num_tokens; /* T: rows of the segment */
-  int32_t src_offset; /* position of row 0 within the src block sequence */
-  int32_t dst_offset; /* position of row 0 within the dst block sequence */
-  int32_t reserved;   /* must be 0 */
+  int32_t num_tokens;   /* T: rows of the segment */
+  int32_t src_offset;   /* position of row 0 within the src block sequence */
+  int32_t dst_offset;   /* position of row 0 within the dst block sequence */
+  int32_t src_position; /* context position of row 0 in the source agent, >= 0 */
+  int32_t dst_position; /* context position of row 0 in the target agent, >= 0 */
+  int32_t reserved;     /* must be 0 */
   kvc_state state;
 } kvc_item;
 
@@ -143,7 +166,10 @@ size_t kvc_dense_bytes(int32_t num_layers, int32_t num_kv_heads, int32_t head_di
 /* Materialise each item's destination rows from its source rows and state, for layers [layer_begin, layer_end).
  * One launch covers every item, layer, K/V and head of the call (a serving batch corrects a whole layer at once).
  * Destination rows must not overlap any source row of the call; with NULL tables and equal pools the host checks the
- * row ranges, with tables it rejects src_tables == dst_tables. */
+ * row ranges, with tables it rejects src_tables == dst_tables.
+ * Keys of a rotary cache (rope_style != KVC_ROPE_NONE), with R(p) the rotation to position p, ps = src_position and
+ * pd = dst_position: C_dst[t] = R(pd) (R(-ps) C_src[t] + A[t] B) for t < T_s (the state is canonical) and
+ * C_dst[t] = R(pd - ps) C_src[t] for T_s <= t < T (the re-aligned source; a bit copy when pd = ps), one rounding. */
 kvc_status kvc_apply(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
                      hipStream_t stream);
 
@@ -151,7 +177,9 @@ kvc_status kvc_apply(const kvc_cache* cache, const kvc_batch* batch, int32_t lay
 size_t kvc_fit_workspace_bytes(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin,
                                int32_t layer_end);
 /* Fit each item's state for layers [layer_begin, layer_end); other layers of the state are left as they are.
- * Sigma descending; each basis row has its largest-magnitude entry positive. */
+ * Sigma descending; each basis row has its largest-magnitude entry positive.  Keys of a rotary cache:
+ * Z = R(-dst_position) C_dst - R(-src_position) C_src (KVC_FIT_BASE: Z = R(-dst_position) C_dst), so the state is in
+ * canonical coordinates. */
 kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
                          kvc_fit_mode mode, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
@@ -185,14 +213,16 @@ typedef struct kvc_anchors {
  * D = H d -- of |C_src[t] - (A_v B_v)[t]|, with A_v B_v anchor v's reconstructed base, and
  * w_v[t] = exp(-d_v[t] / temperature) / sum_u exp(-d_u[t] / temperature) (temperature 1 in the paper).  `batch`
  * holds exactly one item whose source rows are compared (its state, dst side and items_dev are not used);
- * T_s <= item.num_tokens. */
+ * T_s <= item.num_tokens.  Keys of a rotary cache are compared in canonical coordinates, R(-src_position) C_src[t]
+ * (the anchors' bases are canonical). */
 kvc_status kvc_anchor_weights(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
                               int32_t layer_begin, int32_t layer_end, float temperature, hipStream_t stream);
 
 /* Eq. 8 with token-wise weights: for layers [layer_begin, layer_end), every K/V unit and t < T_s,
  * C_dst[t] = C_src[t] + sum_v w_v[t] A_v[t] B_v (A_v B_v anchor v's delta correction, w from `anchors->weights`),
  * one rounding to the storage dtype; rows T_s <= t < item.num_tokens are bit copies.  One item (its state and
- * items_dev are not used); destination rows must not overlap source rows (as for kvc_apply). */
+ * items_dev are not used); destination rows must not overlap source rows (as for kvc_apply).  Keys of a rotary
+ * cache as in kvc_apply: R(pd) (R(-ps) C_src[t] + sum_v w_v[t] A_v[t] B_v), re-aligned source past T_s. */
 kvc_status kvc_apply_anchored(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
                               int32_t layer_begin, int32_t layer_end, hipStream_t stream);
 
@@ -202,7 +232,8 @@ size_t kvc_gate_workspace_bytes(const kvc_cache* cache, const kvc_anchors* ancho
 /* Eq. 9: d_v = (sum over layers [layer_begin, layer_end) of ||V_src[:k] - V_v[:k]||_F^2)^(1/2) with k = prefix,
  * V_src the value rows of the item's source cache (every KV head) and V_v anchor v's reconstructed base values.
  * `distances` is a DEVICE float32 array [num_anchors]; the partial sums are added in a fixed order (the result does
- * not depend on scheduling).  anchors->weights is not used; 1 <= prefix <= anchors->num_tokens. */
+ * not depend on scheduling).  anchors->weights is not used; 1 <= prefix <= anchors->num_tokens.  Values carry no
+ * rotary encoding, so positions play no part here. */
 kvc_status kvc_gate_distances(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
                               int32_t prefix, int32_t layer_begin, int32_t layer_end, float* distances,
                               void* workspace, size_t workspace_bytes, hipStream_t stream);

@@ -37,6 +37,14 @@ kvc_status check_cache(const kvc_cache* c, int32_t lb, int32_t le) {
   if ((c->block_stride * es) % 16 || (c->token_stride * es) % 16 || (c->head_stride * es) % 16) return KVC_ERR_ALIGN;
   // a row must fit between two token slots and two heads (head_dim contiguous elements)
   if (c->head_stride < c->head_dim && c->num_kv_heads > 1) return KVC_ERR_SHAPE;
+  if (c->rope_reserved != 0) return KVC_ERR_SHAPE;
+  if (c->rope_style != KVC_ROPE_NONE && c->rope_style != KVC_ROPE_HALF && c->rope_style != KVC_ROPE_PAIRS)
+    return KVC_ERR_SHAPE;
+  if (c->rope_style != KVC_ROPE_NONE) {
+    if (!c->rope_inv_freq) return KVC_ERR_NULL_ARG;
+    for (int32_t i = 0; i < c->head_dim / 2; ++i)
+      if (!std::isfinite(c->rope_inv_freq[i])) return KVC_ERR_SHAPE;
+  }
   if (le > lb && (!c->k_layers || !c->v_layers)) return KVC_ERR_NULL_ARG;
   for (int32_t l = lb; l < le; ++l) {
     if (!c->k_layers[l] || !c->v_layers[l]) return KVC_ERR_NULL_ARG;
@@ -74,7 +82,7 @@ kvc_status check_batch(const kvc_cache* c, const kvc_batch* b, bool needs_src) {
   if ((b->src_tables || b->dst_tables) && b->max_blocks < 1) return KVC_ERR_SHAPE;
   for (int32_t i = 0; i < b->num_items; ++i) {
     const kvc_item& it = b->items[i];
-    if (it.reserved != 0 || it.num_tokens < 0) return KVC_ERR_SHAPE;
+    if (it.reserved != 0 || it.num_tokens < 0 || it.src_position < 0 || it.dst_position < 0) return KVC_ERR_SHAPE;
     if (!positions_fit(it.dst_offset, it.num_tokens, b->dst_tables != nullptr, b, c)) return KVC_ERR_SHAPE;
     if (needs_src && !positions_fit(it.src_offset, it.num_tokens, b->src_tables != nullptr, b, c))
       return KVC_ERR_SHAPE;
@@ -217,6 +225,10 @@ void fill_pool_view(const kvc_cache* c, kvc::PoolView& pv) {
   pv.block_shift = -1;
   for (int32_t sh = 0; sh < 31; ++sh)
     if ((int32_t{1} << sh) == c->block_size) pv.block_shift = sh;
+  std::memset(&pv.rope, 0, sizeof(pv.rope));
+  pv.rope.style = c->rope_style;
+  if (c->rope_style != KVC_ROPE_NONE)
+    for (int32_t i = 0; i < c->head_dim / 2; ++i) pv.rope.inv_freq[i] = c->rope_inv_freq[i];
 }
 
 
@@ -230,7 +242,7 @@ kvc_status check_anchor_call(const kvc_cache* c, const kvc_batch* b, const kvc_a
   if (!b->items) return KVC_ERR_NULL_ARG;
   if ((b->src_tables || b->dst_tables) && b->max_blocks < 1) return KVC_ERR_SHAPE;
   const kvc_item& it = b->items[0];
-  if (it.reserved != 0 || it.num_tokens < 0) return KVC_ERR_SHAPE;
+  if (it.reserved != 0 || it.num_tokens < 0 || it.src_position < 0 || it.dst_position < 0) return KVC_ERR_SHAPE;
   if (!positions_fit(it.src_offset, it.num_tokens, b->src_tables != nullptr, b, c)) return KVC_ERR_SHAPE;
   if (needs_dst && !positions_fit(it.dst_offset, it.num_tokens, b->dst_tables != nullptr, b, c)) return KVC_ERR_SHAPE;
   if (an->num_anchors < 1 || an->num_anchors > KVC_MAX_ANCHORS) return KVC_ERR_SHAPE;
@@ -257,6 +269,8 @@ void fill_anchor_args(const kvc_cache* c, const kvc_batch* b, const kvc_anchors*
   a.dst_table = b->dst_tables;
   a.src_offset = it.src_offset;
   a.dst_offset = it.dst_offset;
+  a.src_position = it.src_position;
+  a.dst_position = it.dst_position;
   a.num_tokens = it.num_tokens;
   a.num_weighted = an->num_tokens;
   a.layer_begin = lb;

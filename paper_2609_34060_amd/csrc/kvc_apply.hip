@@ -29,7 +29,10 @@ int apply_chunk_tokens() { return kApplyChunk; }
 //   PF    software prefetch: the next tile's rows and coefficients are loaded before this tile's MFMAs
 //   NTL   non-temporal loads of the streamed source rows (read exactly once)
 //   NTS   non-temporal stores of the destination rows (written exactly once)
-template <int D, int KS, int TPW, bool REGF, bool PF, bool NTL, bool NTS>
+//   ROPE  the keys are rotary-encoded: corrected in canonical coordinates and rotated to the target positions,
+//         C_dst = R(pd - ps) C_src + (A B R(pd)^T): the accumulator starts from the source rotated by pd - ps and B is
+//         staged rotated by pd, so the rotation costs no extra pass (rows past T_s get the rotated source)
+template <int D, int KS, int TPW, bool REGF, bool PF, bool NTL, bool NTS, bool ROPE>
 __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
   constexpr int MT = D / 16;  // M-tiles per row
   constexpr int NQ = D / 32;  // 16-byte loads per lane per row
@@ -68,6 +71,19 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
   const int n = lane & 15;
   const bool correct = t_begin < Ts;  // uniform over the workgroup
 
+  // keys of a rotary cache: angle tables of the shift pd - ps (source rows) and of pd (the basis)
+  __shared__ float s_rope[4][ROPE ? D / 2 : 1];
+  const bool rope = ROPE && kv == 0;  // uniform over the workgroup
+  const int style = a.pv.rope.style;
+  bool shift = false;
+  if (rope) {
+    const int ps = itp->src_position, pd = itp->dst_position;
+    shift = pd != ps;
+    rope_table(a.pv.rope, D, (double)pd - (double)ps, s_rope[0], s_rope[1]);
+    rope_table(a.pv.rope, D, (double)pd, s_rope[2], s_rope[3]);
+    __syncthreads();
+  }
+
   constexpr bool kRegFrags = REGF && KS <= 2;
   constexpr int FM = kRegFrags ? MT : 1, FK = kRegFrags ? KS : 1;
   bf16x8 ahi[FM][FK], alo[FM][FK];
@@ -75,7 +91,12 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
     // Stage B^T as bf16 hi/lo, zero-padded to KP ranks: s[f * KP + k] = split(B[k][f]).
     for (int e = threadIdx.x; e < D * KP; e += kApplyThreads) {
       const int k = e / D, f = e - k * D;
-      const float x = k < r ? basis[k * D + f] : 0.0f;
+      float x = k < r ? basis[k * D + f] : 0.0f;
+      if (rope && k < r) {  // B R(pd)^T: each basis row rotated like a key row at position pd
+        const int i = rope_pair(style, D, f);
+        x = rope_rotated(rope_first(style, D, f), x, basis[k * D + rope_partner(style, D, f)], s_rope[2][i],
+                         s_rope[3][i]);
+      }
       uint32_t hb, lb;
       split_bf16(x, hb, lb);
       s_hi[f * KP + k] = (uint16_t)hb;
@@ -150,6 +171,7 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
         acc[2 * q + 1] = f32x4{bf16_lo_to_f32(tl.raw[q][2]), bf16_hi_to_f32(tl.raw[q][2]),
                                bf16_lo_to_f32(tl.raw[q][3]), bf16_hi_to_f32(tl.raw[q][3])};
       }
+      if (ROPE && shift) rope_rotate_rows<D>(acc, style, g, s_rope[0], s_rope[1]);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
@@ -167,7 +189,8 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
           }
         }
       }
-      const bool crow = t < Ts;
+      // rows past T_s had zero coefficients: with a shift they hold the rotated source, else they are bit copies
+      const bool crow = t < Ts || (ROPE && shift);
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         const f32x4 x = acc[2 * q], y = acc[2 * q + 1];
@@ -175,6 +198,20 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
                          pack_bf16x2(y[2], y[3])};
         outw[q] = crow ? c : tl.raw[q];
       }
+    } else if (ROPE && shift) {  // uncovered tile: the re-aligned source
+      f32x4 v[MT];
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        v[2 * q] = f32x4{bf16_lo_to_f32(tl.raw[q][0]), bf16_hi_to_f32(tl.raw[q][0]), bf16_lo_to_f32(tl.raw[q][1]),
+                         bf16_hi_to_f32(tl.raw[q][1])};
+        v[2 * q + 1] = f32x4{bf16_lo_to_f32(tl.raw[q][2]), bf16_hi_to_f32(tl.raw[q][2]),
+                             bf16_lo_to_f32(tl.raw[q][3]), bf16_hi_to_f32(tl.raw[q][3])};
+      }
+      rope_rotate_rows<D>(v, style, g, s_rope[0], s_rope[1]);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+        outw[q] = u32x4{pack_bf16x2(v[2 * q][0], v[2 * q][1]), pack_bf16x2(v[2 * q][2], v[2 * q][3]),
+                        pack_bf16x2(v[2 * q + 1][0], v[2 * q + 1][1]), pack_bf16x2(v[2 * q + 1][2], v[2 * q + 1][3])};
     } else {
 #pragma unroll
       for (int q = 0; q < NQ; ++q) outw[q] = tl.raw[q];
@@ -241,9 +278,29 @@ __global__ __launch_bounds__(kApplyThreads) void apply_f32_valu(ApplyArgs a) {
   const float* src_pool = static_cast<const float*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
   float* dst_pool = static_cast<float*>(const_cast<void*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]));
 
+  // keys of a rotary cache: C_dst = R(pd - ps) C_src + A (B R(pd)^T), with the angle tables in LDS
+  __shared__ float s_rope[4][D / 2];
+  const bool rope = a.pv.rope.style != KVC_ROPE_NONE && kv == 0;  // uniform over the workgroup
+  const int style = a.pv.rope.style;
+  bool shift = false;
+  if (rope) {
+    const int ps = itp->src_position, pd = itp->dst_position;
+    shift = pd != ps;
+    rope_table(a.pv.rope, D, (double)pd - (double)ps, s_rope[0], s_rope[1]);
+    rope_table(a.pv.rope, D, (double)pd, s_rope[2], s_rope[3]);
+    __syncthreads();
+  }
   const bool correct = t_begin < Ts;
   if (correct) {
-    for (int e = threadIdx.x; e < r * D; e += kApplyThreads) s_b[e] = basis[e];
+    for (int e = threadIdx.x; e < r * D; e += kApplyThreads) {
+      float x = basis[e];
+      if (rope) {
+        const int k = e / D, f = e - k * D, i = rope_pair(style, D, f);
+        x = rope_rotated(rope_first(style, D, f), x, basis[k * D + rope_partner(style, D, f)], s_rope[2][i],
+                         s_rope[3][i]);
+      }
+      s_b[e] = x;
+    }
     __syncthreads();
   }
   const int sub = threadIdx.x / LPT;
@@ -255,6 +312,16 @@ __global__ __launch_bounds__(kApplyThreads) void apply_f32_valu(ApplyArgs a) {
     if (so < 0 || dof < 0) continue;
     const f32x4 s = *reinterpret_cast<const f32x4*>(src_pool + so + f0);
     f32x4 o = s;
+    if (shift) {  // the source rotated by pd - ps (the four features' partners: another quad, or inside this one)
+      const int pf = rope_partner(style, D, f0) & ~3;
+      const f32x4 y = *reinterpret_cast<const f32x4*>(src_pool + so + pf);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int f = f0 + j, i = rope_pair(style, D, f);
+        const float partner = style == KVC_ROPE_HALF ? y[j] : s[j ^ 1];
+        o[j] = rope_rotated(rope_first(style, D, f), s[j], partner, s_rope[0][i], s_rope[1][i]);
+      }
+    }
     if (t < Ts) {
       const float* crow = coef + (int64_t)t * r;
       for (int k = 0; k < r; ++k) {
@@ -276,7 +343,12 @@ constexpr bool kREGF = false, kPF = false, kNTL = false, kNTS = false;
 
 template <int D, int KS>
 static hipError_t launch_bf16(const ApplyArgs& a, dim3 grid, hipStream_t stream) {
-  hipLaunchKernelGGL((apply_bf16_mfma<D, KS, kTPW, kREGF, kPF, kNTL, kNTS>), grid, dim3(kApplyThreads), 0, stream, a);
+  if (a.pv.rope.style != KVC_ROPE_NONE)
+    hipLaunchKernelGGL((apply_bf16_mfma<D, KS, kTPW, kREGF, kPF, kNTL, kNTS, true>), grid, dim3(kApplyThreads), 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL((apply_bf16_mfma<D, KS, kTPW, kREGF, kPF, kNTL, kNTS, false>), grid, dim3(kApplyThreads), 0,
+                       stream, a);
   return hipGetLastError();
 }
 

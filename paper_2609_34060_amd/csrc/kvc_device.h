@@ -14,11 +14,20 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 
+// Rotary encoding of the key rows (device-side view of kvc_cache's rope fields): pair i of a key at position p is
+// rotated by the angle p * inv_freq[i].
+struct RopeView {
+  int32_t style;        // kvc_rope_style
+  int32_t pad;
+  double inv_freq[64];  // [head_dim / 2]
+};
+
 // Per-launch description of the pools of one cache (device-side view of kvc_cache).
 struct PoolView {
   int64_t block_stride, token_stride, head_stride;  // elements
   int32_t block_size, num_blocks, num_kv_heads, head_dim;
   int32_t block_shift;                               // log2(block_size) when it is a power of two, else -1
+  RopeView rope;
 };
 
 // Layer pointer tables travel in the kernel arguments (up to this many layers per launch).
@@ -80,6 +89,61 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) { return __builtin_b
 // last four in 2q + 1.
 __device__ __forceinline__ int mfma_row_feature(int mt, int m) {
   return 32 * (mt >> 1) + 8 * (m >> 2) + 4 * (mt & 1) + (m & 3);
+}
+
+// ---- rotary re-alignment of key rows (Appendix A.3, positional alignment) ----------------------------------------
+// Pair i of a row is features (i, i + D/2) (KVC_ROPE_HALF) or (2i, 2i + 1) (KVC_ROPE_PAIRS); rotating it by the angle
+// th maps (a, b) to (a cos th - b sin th, a sin th + b cos th).
+
+// cos / sin of the angles p * inv_freq[i] of the D/2 pairs, evaluated in fp64 and rounded to fp32, by the threads
+// of the calling workgroup (the caller synchronises before reading c and s).
+__device__ __forceinline__ void rope_table(const RopeView& rp, int D, double p, float* c, float* s) {
+  for (int i = threadIdx.x; i < D / 2; i += blockDim.x) {
+    double sn, cs;
+    sincos(p * rp.inv_freq[i], &sn, &cs);
+    c[i] = (float)cs;
+    s[i] = (float)sn;
+  }
+}
+__device__ __forceinline__ int rope_partner(int style, int D, int f) {
+  return style == KVC_ROPE_HALF ? (f < D / 2 ? f + D / 2 : f - D / 2) : (f ^ 1);
+}
+__device__ __forceinline__ int rope_pair(int style, int D, int f) {
+  return style == KVC_ROPE_HALF ? (f < D / 2 ? f : f - D / 2) : (f >> 1);
+}
+__device__ __forceinline__ bool rope_first(int style, int D, int f) {
+  return style == KVC_ROPE_HALF ? f < D / 2 : (f & 1) == 0;
+}
+// Feature value after the rotation, from its own value x and its partner's y (angle given by c, s).
+__device__ __forceinline__ float rope_rotated(bool first, float x, float y, float c, float s) {
+  return first ? x * c - y * s : y * s + x * c;
+}
+// Rotate a row held in the row layout of the MFMA kernels (the lane of token-group g holds features 32 q + 8 g + e,
+// e < 8, in v[2 q + (e >> 2)][e & 3]) by the angles of a table; the pairs of both styles stay inside the lane.
+template <int D>
+__device__ __forceinline__ void rope_rotate_rows(f32x4* v, int style, int g, const float* c, const float* s) {
+  constexpr int NQ = D / 32;
+  if (style == KVC_ROPE_HALF) {
+#pragma unroll
+    for (int q = 0; q < NQ / 2; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int i = 32 * q + 8 * g + e, ja = 2 * q + (e >> 2), jb = 2 * (q + NQ / 2) + (e >> 2);
+        const float a = v[ja][e & 3], b = v[jb][e & 3], cc = c[i], ss = s[i];
+        v[ja][e & 3] = a * cc - b * ss;
+        v[jb][e & 3] = a * ss + b * cc;
+      }
+  } else {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const int i = 16 * q + 4 * g + (e >> 1), j = 2 * q + (e >> 2);
+        const float a = v[j][e & 3], b = v[j][(e & 3) + 1], cc = c[i], ss = s[i];
+        v[j][e & 3] = a * cc - b * ss;
+        v[j][(e & 3) + 1] = a * ss + b * cc;
+      }
+  }
 }
 
 // Offset of unit (layer, kv, head) in a state's per-unit arrays.

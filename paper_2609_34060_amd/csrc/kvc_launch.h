@@ -92,6 +92,7 @@ struct AnchorArgs {
   const int32_t* src_table;    // device row of the item's src table, or null
   const int32_t* dst_table;
   int32_t src_offset, dst_offset;
+  int32_t src_position, dst_position;  // context positions of row 0 (keys of a rotary cache)
   int32_t num_tokens;          // T: rows of the item (apply copies rows T_s <= t < T)
   int32_t num_weighted;        // T_s (weights, apply) or the gate prefix k
   int32_t layer_begin, num_layers;

@@ -19,6 +19,7 @@ KVC_OK, KVC_ERR_NULL_ARG, KVC_ERR_SHAPE, KVC_ERR_DTYPE, KVC_ERR_ALIGN = 0, 1, 2,
 KVC_ERR_ALIAS, KVC_ERR_WORKSPACE, KVC_ERR_UNSUPPORTED, KVC_ERR_HIP = 5, 6, 7, 8
 KVC_F32, KVC_BF16 = 0, 1
 KVC_FIT_DELTA, KVC_FIT_BASE = 0, 1
+KVC_ROPE_NONE, KVC_ROPE_HALF, KVC_ROPE_PAIRS = 0, 1, 2
 KVC_MAX_RANK = 128
 KVC_MAX_ANCHORS = 16
 
@@ -39,7 +40,9 @@ class kvc_cache(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int), ("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32), ("num_blocks", ctypes.c_int32),
                 ("block_stride", ctypes.c_int64), ("token_stride", ctypes.c_int64), ("head_stride", ctypes.c_int64),
-                ("k_layers", ctypes.POINTER(ctypes.c_void_p)), ("v_layers", ctypes.POINTER(ctypes.c_void_p))]
+                ("k_layers", ctypes.POINTER(ctypes.c_void_p)), ("v_layers", ctypes.POINTER(ctypes.c_void_p)),
+                ("rope_style", ctypes.c_int32), ("rope_reserved", ctypes.c_int32),
+                ("rope_inv_freq", ctypes.POINTER(ctypes.c_double))]
 
 
 class kvc_state(ctypes.Structure):
@@ -50,7 +53,8 @@ class kvc_state(ctypes.Structure):
 
 class kvc_item(ctypes.Structure):
     _fields_ = [("num_tokens", ctypes.c_int32), ("src_offset", ctypes.c_int32), ("dst_offset", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("state", kvc_state)]
+                ("src_position", ctypes.c_int32), ("dst_position", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("state", kvc_state)]
 
 
 class kvc_batch(ctypes.Structure):
@@ -152,10 +156,12 @@ def _stream_handle(stream) -> ctypes.c_void_p:
 
 class Cache:
     """kvc_cache over per-layer pools [num_blocks, block_size, num_kv_heads, head_dim] (or any strided view whose
-    head_dim is contiguous)."""
+    head_dim is contiguous).  rope_style / rope_inv_freq describe a rotary encoding of the key rows
+    (KVC_ROPE_NONE: none)."""
 
     def __init__(self, k_pools: Sequence[torch.Tensor], v_pools: Sequence[torch.Tensor],
-                 strides: Optional[Sequence[int]] = None):
+                 strides: Optional[Sequence[int]] = None, rope_style: int = 0,
+                 rope_inv_freq: Optional[Sequence[float]] = None):
         assert len(k_pools) == len(v_pools) and len(k_pools) > 0
         p0 = k_pools[0]
         self.k_pools, self.v_pools = list(k_pools), list(v_pools)
@@ -165,9 +171,14 @@ class Cache:
         n = len(k_pools)
         self._k = (ctypes.c_void_p * n)(*[p.data_ptr() for p in k_pools])
         self._v = (ctypes.c_void_p * n)(*[p.data_ptr() for p in v_pools])
+        self._inv_freq = None
+        if rope_inv_freq is not None:
+            self._inv_freq = (ctypes.c_double * len(rope_inv_freq))(*[float(x) for x in rope_inv_freq])
         self.c = kvc_cache(_dtype_code(p0.dtype), n, H, d, bs, nb, strides[0], strides[1], strides[2],
                            ctypes.cast(self._k, ctypes.POINTER(ctypes.c_void_p)),
-                           ctypes.cast(self._v, ctypes.POINTER(ctypes.c_void_p)))
+                           ctypes.cast(self._v, ctypes.POINTER(ctypes.c_void_p)), int(rope_style), 0,
+                           None if self._inv_freq is None
+                           else ctypes.cast(self._inv_freq, ctypes.POINTER(ctypes.c_double)))
 
     @property
     def num_layers(self):
@@ -206,7 +217,8 @@ class Batch:
 
     def __init__(self, num_tokens: Sequence[int], src_offsets: Sequence[int], dst_offsets: Sequence[int],
                  states: Sequence[State], src_tables: Optional[torch.Tensor] = None,
-                 dst_tables: Optional[torch.Tensor] = None, device=None):
+                 dst_tables: Optional[torch.Tensor] = None, device=None,
+                 src_positions: Optional[Sequence[int]] = None, dst_positions: Optional[Sequence[int]] = None):
         n = len(num_tokens)
         self.states = list(states)
         arr = (kvc_item * max(n, 1))()
@@ -214,6 +226,8 @@ class Batch:
             arr[i].num_tokens = int(num_tokens[i])
             arr[i].src_offset = int(src_offsets[i])
             arr[i].dst_offset = int(dst_offsets[i])
+            arr[i].src_position = 0 if src_positions is None else int(src_positions[i])
+            arr[i].dst_position = 0 if dst_positions is None else int(dst_positions[i])
             arr[i].reserved = 0
             arr[i].state = states[i].s
         self._items = arr

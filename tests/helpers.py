@@ -19,9 +19,17 @@ def storage_name(t: torch.dtype) -> str:
     return "bf16" if t == torch.bfloat16 else "f32"
 
 
-def oracle_cache(k_pools, v_pools, block_size: int) -> O.Cache:
+def oracle_cache(k_pools, v_pools, block_size: int, rope: "O.Rope | None" = None) -> O.Cache:
     dt = storage_name(k_pools[0].dtype)
-    return O.Cache(dt, block_size, [to_np_storage(p) for p in k_pools], [to_np_storage(p) for p in v_pools])
+    return O.Cache(dt, block_size, [to_np_storage(p) for p in k_pools], [to_np_storage(p) for p in v_pools], rope)
+
+
+ROPE_STYLE_NAME = {1: "half", 2: "pairs"}
+
+
+def rope_inv_freq(d: int, theta: float) -> np.ndarray:
+    """Inverse frequencies theta^(-2i/d) of the standard rotary encoding (float64)."""
+    return theta ** (-np.arange(0, d, 2, dtype=np.float64) / d)
 
 
 def oracle_state(coef: torch.Tensor, basis: torch.Tensor, sigma=None) -> O.State:
