@@ -127,7 +127,10 @@ __device__ __forceinline__ void row_offsets8(const PoolView& pv, const int32_t* 
 // the MFMA fragments of every tile row are gathered from those segments with byte permutes, so the Gram needs no
 // LDS and no barrier; all upper tiles accumulate in the wave's registers.  The next step's rows are loaded while
 // the current step is multiplied.
-template <int D>
+// ROPE: keys of a rotary cache are fitted in canonical coordinates, Z = R(-pd) C_dst - R(-ps) C_src.  The partner of
+// a rotate-half pair sits in lane n ^ 8 of the same row (features FT n + e and FT (n + 8) + e) and is fetched with a
+// row rotation by 8; an adjacent pair sits in the same dword.
+template <int D, bool ROPE>
 __global__ __launch_bounds__(kFitThreads) void gram_bf16_mfma(FitArgs a) {
   constexpr int FT = D / 16;
   constexpr int NT = FT * (FT + 1) / 2;
@@ -138,6 +141,15 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_mfma(FitArgs a) {
   const int r = itp->state.rank;
   const int Ts = itp->state.num_tokens;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // angle tables of -pd (dst rows) and -ps (src rows), before any wave leaves (the barrier needs every wave)
+  __shared__ float s_rope[4][ROPE ? D / 2 : 1];
+  const bool rope = ROPE && f.kv == 0;  // uniform over the workgroup
+  const int style = a.pv.rope.style;
+  if (rope) {
+    rope_table(a.pv.rope, D, -(double)itp->dst_position, s_rope[0], s_rope[1]);
+    rope_table(a.pv.rope, D, -(double)itp->src_position, s_rope[2], s_rope[3]);
+    __syncthreads();
+  }
   const int part = blockIdx.x * kFitWaves + wave;
   const int t_begin = part * a.part_tokens;
   if (r == 0 || t_begin >= Ts) return;  // per wave: the kernel has no barrier
@@ -188,13 +200,68 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_mfma(FitArgs a) {
     }
   };
 
+  // canonical Z of the loaded step (rotary keys): per element its own and its partner's value, both sides rotated
+  float rc[2][FT], rsn[2][FT];  // cos / sin of -pd and -ps for the lane's FT features
+  if (ROPE && rope) {
+#pragma unroll
+    for (int e = 0; e < FT; ++e) {
+      const int i = rope_pair(style, D, FT * n + e);
+      rc[0][e] = s_rope[0][i];
+      rsn[0][e] = s_rope[1][i];
+      rc[1][e] = s_rope[2][i];
+      rsn[1][e] = s_rope[3][i];
+    }
+  }
+  auto form_z_rope = [&](const Seg* rd, const Seg* rs, Seg* zh, Seg* zl) {
+    const bool half = style == KVC_ROPE_HALF;
+    const bool first_half = FT * n < D / 2;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+#pragma unroll
+      for (int w = 0; w < FT / 2; ++w) {
+        const uint32_t dw = seg_dword<FT>(rd[j], w), sw = seg_dword<FT>(rs[j], w);
+        // partner dword: the same dword of lane n ^ 8 (rotate-half) or this dword with its halves swapped
+        const uint32_t dpw = half ? (uint32_t)__builtin_amdgcn_mov_dpp((int)dw, 0x128, 0xF, 0xF, false)
+                                  : ((dw >> 16) | (dw << 16));
+        const uint32_t spw = half ? (uint32_t)__builtin_amdgcn_mov_dpp((int)sw, 0x128, 0xF, 0xF, false)
+                                  : ((sw >> 16) | (sw << 16));
+        float z[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int e = 2 * w + h;
+          const bool first = half ? first_half : h == 0;
+          const float xd = h ? bf16_hi_to_f32(dw) : bf16_lo_to_f32(dw);
+          const float yd = h ? bf16_hi_to_f32(dpw) : bf16_lo_to_f32(dpw);
+          const float xs = h ? bf16_hi_to_f32(sw) : bf16_lo_to_f32(sw);
+          const float ys = h ? bf16_hi_to_f32(spw) : bf16_lo_to_f32(spw);
+          z[h] = rope_rotated(first, xd, yd, rc[0][e], rsn[0][e]) - rope_rotated(first, xs, ys, rc[1][e], rsn[1][e]);
+        }
+        uint32_t hh, ll;
+        split_bf16x2(z[0], z[1], hh, ll);
+        if constexpr (FT == 8) {
+          zh[j][w] = hh;
+          zl[j][w] = ll;
+        } else {
+          if (w == 0) {
+            zh[j].x = hh;
+            zl[j].x = ll;
+          } else {
+            zh[j].y = hh;
+            zl[j].y = ll;
+          }
+        }
+      }
+    }
+  };
+
   // one register stage: the next step's rows are loaded into the same registers once Z of this step is formed,
   // so they are in flight while this step's 3 x NT MFMAs run
   Seg rd[8], rs[8];
   load(t_begin, rd, rs);
   for (int t0 = t_begin; t0 < t_end; t0 += STEP) {
     Seg zh[8], zl[8];
-    form_z(rd, rs, zh, zl);
+    if (ROPE && rope) form_z_rope(rd, rs, zh, zl);
+    else form_z(rd, rs, zh, zl);
     if (t0 + STEP < t_end) load(t0 + STEP, rd, rs);
     gram_all_tiles<D>(acc, zh, zl, std::make_integer_sequence<int, NT>{});
   }
@@ -452,7 +519,7 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_ring(FitArgs a) {
 // Gram, fp32 caches (VALU, fp32 accumulation)
 // ---------------------------------------------------------------------------------------------------------------
 
-template <int D>
+template <int D, bool ROPE>
 __global__ __launch_bounds__(kFitThreads) void gram_f32_valu(FitArgs a) {
   constexpr int STEP = 32;
   constexpr int NE = D * (D + 1) / 2;
@@ -472,6 +539,14 @@ __global__ __launch_bounds__(kFitThreads) void gram_f32_valu(FitArgs a) {
   const float* pool = static_cast<const float*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
   const bool delta = a.mode == KVC_FIT_DELTA;
   const int tid = threadIdx.x;
+  __shared__ float s_rope[4][ROPE ? D / 2 : 1];  // cos / sin of -pd and -ps (rotary keys)
+  const bool rope = ROPE && f.kv == 0;
+  const int style = a.pv.rope.style;
+  if (rope) {
+    rope_table(a.pv.rope, D, -(double)itp->dst_position, s_rope[0], s_rope[1]);
+    rope_table(a.pv.rope, D, -(double)itp->src_position, s_rope[2], s_rope[3]);
+    __syncthreads();
+  }
 
   int ei[EPT], ej[EPT];
   float acc[EPT];
@@ -498,9 +573,14 @@ __global__ __launch_bounds__(kFitThreads) void gram_f32_valu(FitArgs a) {
       float z = 0.f;
       if (t < t_end) {
         const int64_t od = row_offset(a.pv, dst_tab, itp->dst_offset, t, f.head);
-        if (od >= 0) z = pool[od + fe];
-        if (delta) {
-          const int64_t os = row_offset(a.pv, src_tab, itp->src_offset, t, f.head);
+        const int64_t os = delta ? row_offset(a.pv, src_tab, itp->src_offset, t, f.head) : -1;
+        if (rope) {  // Z = R(-pd) C_dst - R(-ps) C_src
+          const int pf = rope_partner(style, D, fe), i = rope_pair(style, D, fe);
+          const bool first = rope_first(style, D, fe);
+          if (od >= 0) z = rope_rotated(first, pool[od + fe], pool[od + pf], s_rope[0][i], s_rope[1][i]);
+          if (os >= 0) z -= rope_rotated(first, pool[os + fe], pool[os + pf], s_rope[2][i], s_rope[3][i]);
+        } else {
+          if (od >= 0) z = pool[od + fe];
           if (os >= 0) z -= pool[os + fe];
         }
       }
@@ -532,7 +612,7 @@ __global__ __launch_bounds__(kFitThreads) void gram_f32_valu(FitArgs a) {
 constexpr int kProjTilesPerWave = 16;
 constexpr int kProjChunk = kFitWaves * kProjTilesPerWave * 16;
 
-template <int D, int MTR>
+template <int D, int MTR, bool ROPE>
 __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
   constexpr int KS = D / 32;          // K-steps over features
   constexpr int RP = MTR * 16;        // padded rank
@@ -556,6 +636,14 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, n = lane & 15;
+  // rotary keys: Z = R(-pd) C_dst - R(-ps) C_src (angle tables ready at the staging barrier below)
+  __shared__ float s_rope[4][ROPE ? D / 2 : 1];
+  const bool rope = ROPE && f.kv == 0;  // uniform over the workgroup
+  const int style = a.pv.rope.style;
+  if (rope) {
+    rope_table(a.pv.rope, D, -(double)itp->dst_position, s_rope[0], s_rope[1]);
+    rope_table(a.pv.rope, D, -(double)itp->src_position, s_rope[2], s_rope[3]);
+  }
 
   for (int e = tid; e < RP * D; e += kFitThreads) {
     const int k = e / D;
@@ -586,6 +674,34 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
     const int64_t od = valid ? row_offset(a.pv, dst_tab, itp->dst_offset, t, f.head) : -1;
     const int64_t os = (valid && delta) ? row_offset(a.pv, src_tab, itp->src_offset, t, f.head) : -1;
     bf16x8 zh[KS], zl[KS];
+    if (ROPE && rope) {
+      f32x4 dv[2 * KS], sv[2 * KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 d = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+        const u32x4 s = os >= 0 ? *reinterpret_cast<const u32x4*>(pool + os + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+        dv[2 * ks] = f32x4{bf16_lo_to_f32(d[0]), bf16_hi_to_f32(d[0]), bf16_lo_to_f32(d[1]), bf16_hi_to_f32(d[1])};
+        dv[2 * ks + 1] = f32x4{bf16_lo_to_f32(d[2]), bf16_hi_to_f32(d[2]), bf16_lo_to_f32(d[3]), bf16_hi_to_f32(d[3])};
+        sv[2 * ks] = f32x4{bf16_lo_to_f32(s[0]), bf16_hi_to_f32(s[0]), bf16_lo_to_f32(s[1]), bf16_hi_to_f32(s[1])};
+        sv[2 * ks + 1] = f32x4{bf16_lo_to_f32(s[2]), bf16_hi_to_f32(s[2]), bf16_lo_to_f32(s[3]), bf16_hi_to_f32(s[3])};
+      }
+      rope_rotate_rows<D>(dv, style, g, s_rope[0], s_rope[1]);
+      rope_rotate_rows<D>(sv, style, g, s_rope[2], s_rope[3]);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        u32x4 hw, lw;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const int j = 2 * ks + (w >> 1), e = 2 * (w & 1);
+          uint32_t hh, ll;
+          split_bf16x2(dv[j][e] - sv[j][e], dv[j][e + 1] - sv[j][e + 1], hh, ll);
+          hw[w] = hh;
+          lw[w] = ll;
+        }
+        zh[ks] = as_bf16x8(hw);
+        zl[ks] = as_bf16x8(lw);
+      }
+    } else {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const u32x4 d = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
@@ -603,6 +719,7 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
       }
       zh[ks] = as_bf16x8(hw);
       zl[ks] = as_bf16x8(lw);
+    }
     }
 #pragma unroll
     for (int mt = 0; mt < MTR; ++mt) {
@@ -642,7 +759,7 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
 }
 
 // Projection, fp32 caches: one thread per (token, rank), fp32 FMAs over the features.
-template <int D>
+template <int D, bool ROPE>
 __global__ __launch_bounds__(kFitThreads) void proj_f32_valu(FitArgs a) {
   extern __shared__ __attribute__((aligned(16))) float s_b[];  // [r][D]
   const FitUnit f = fit_unit(a);
@@ -658,6 +775,13 @@ __global__ __launch_bounds__(kFitThreads) void proj_f32_valu(FitArgs a) {
   const bool delta = a.mode == KVC_FIT_DELTA;
   const float* basis = itp->state.basis + f.unit * (int64_t)r * D;
   float* coef = static_cast<float*>(itp->state.coef) + f.unit * (int64_t)Ts * r;
+  __shared__ float s_rope[4][ROPE ? D / 2 : 1];  // cos / sin of -pd and -ps (rotary keys)
+  const bool rope = ROPE && f.kv == 0;
+  const int style = a.pv.rope.style;
+  if (rope) {
+    rope_table(a.pv.rope, D, -(double)itp->dst_position, s_rope[0], s_rope[1]);
+    rope_table(a.pv.rope, D, -(double)itp->src_position, s_rope[2], s_rope[3]);
+  }
   for (int e = threadIdx.x; e < r * D; e += kFitThreads) s_b[e] = basis[e];
   __syncthreads();
   const int64_t total = (int64_t)(t_end - t_begin) * r;
@@ -667,8 +791,16 @@ __global__ __launch_bounds__(kFitThreads) void proj_f32_valu(FitArgs a) {
     const int64_t os = delta ? row_offset(a.pv, src_tab, itp->src_offset, t, f.head) : -1;
     float s = 0.f;
     for (int fe = 0; fe < D; ++fe) {
-      float z = od >= 0 ? pool[od + fe] : 0.f;
-      if (os >= 0) z -= pool[os + fe];
+      float z;
+      if (rope) {  // Z = R(-pd) C_dst - R(-ps) C_src
+        const int pf = rope_partner(style, D, fe), i = rope_pair(style, D, fe);
+        const bool first = rope_first(style, D, fe);
+        z = od >= 0 ? rope_rotated(first, pool[od + fe], pool[od + pf], s_rope[0][i], s_rope[1][i]) : 0.f;
+        if (os >= 0) z -= rope_rotated(first, pool[os + fe], pool[os + pf], s_rope[2][i], s_rope[3][i]);
+      } else {
+        z = od >= 0 ? pool[od + fe] : 0.f;
+        if (os >= 0) z -= pool[os + fe];
+      }
       s = fmaf(z, s_b[k * D + fe], s);
     }
     coef[(int64_t)t * r + k] = s;
@@ -681,11 +813,12 @@ __global__ __launch_bounds__(kFitThreads) void proj_f32_valu(FitArgs a) {
 
 int proj_chunk_tokens() { return kProjChunk; }
 
-hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream) {
+template <bool ROPE>
+static hipError_t launch_gram_variants(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream) {
   const int D = a.pv.head_dim;
   if (dtype == KVC_BF16) {
     dim3 grid((a.max_parts + kFitWaves - 1) / kFitWaves, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
-    if (D == 128 && a.pv.block_shift >= 4 && a.part_tokens / a.pv.block_size + 3 <= kGramTabMax) {
+    if (!ROPE && D == 128 && a.pv.block_shift >= 4 && a.part_tokens / a.pv.block_size + 3 <= kGramTabMax) {
       // LDS-staged rows (block sizes of at least 16 tokens, a partial's table fits the wave's LDS copy)
       const bool delta = a.mode == KVC_FIT_DELTA;
       grid = dim3(a.max_parts, 2 * ((a.pv.num_kv_heads + kFitWaves - 1) / kFitWaves), num_items * a.num_layers);
@@ -695,43 +828,58 @@ hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hip
       if (delta) hipLaunchKernelGGL(gram_bf16_ring<true>, grid, dim3(kFitThreads), kGramLdsBytes, stream, a);
       else hipLaunchKernelGGL(gram_bf16_ring<false>, grid, dim3(kFitThreads), kGramLdsBytes, stream, a);
     } else if (D == 64) {
-      hipLaunchKernelGGL(gram_bf16_mfma<64>, grid, dim3(kFitThreads), 0, stream, a);
+      hipLaunchKernelGGL((gram_bf16_mfma<64, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
     } else {
-      hipLaunchKernelGGL(gram_bf16_mfma<128>, grid, dim3(kFitThreads), 0, stream, a);
+      hipLaunchKernelGGL((gram_bf16_mfma<128, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
     }
   } else {
     dim3 grid(a.max_parts, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
-    if (D == 64) hipLaunchKernelGGL(gram_f32_valu<64>, grid, dim3(kFitThreads), 0, stream, a);
-    else hipLaunchKernelGGL(gram_f32_valu<128>, grid, dim3(kFitThreads), 0, stream, a);
+    if (D == 64) hipLaunchKernelGGL((gram_f32_valu<64, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
+    else hipLaunchKernelGGL((gram_f32_valu<128, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
   }
   return hipGetLastError();
 }
 
-template <int D>
+// A rotary cache takes the register-pipelined Gram (the rotation needs each feature's partner, which that layout
+// reaches with one row rotation).
+hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream) {
+  return a.pv.rope.style != KVC_ROPE_NONE ? launch_gram_variants<true>(a, dtype, num_items, stream)
+                                          : launch_gram_variants<false>(a, dtype, num_items, stream);
+}
+
+template <int D, bool ROPE>
 static hipError_t launch_proj_bf16(const FitArgs& a, int mtr, dim3 grid, hipStream_t stream) {
   switch (mtr) {
-    case 1: hipLaunchKernelGGL((proj_bf16_mfma<D, 1>), grid, dim3(kFitThreads), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((proj_bf16_mfma<D, 2>), grid, dim3(kFitThreads), 0, stream, a); break;
+    case 1: hipLaunchKernelGGL((proj_bf16_mfma<D, 1, ROPE>), grid, dim3(kFitThreads), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((proj_bf16_mfma<D, 2, ROPE>), grid, dim3(kFitThreads), 0, stream, a); break;
     case 3:
-    case 4: hipLaunchKernelGGL((proj_bf16_mfma<D, 4>), grid, dim3(kFitThreads), 0, stream, a); break;
-    default: hipLaunchKernelGGL((proj_bf16_mfma<D, 8>), grid, dim3(kFitThreads), 0, stream, a); break;
+    case 4: hipLaunchKernelGGL((proj_bf16_mfma<D, 4, ROPE>), grid, dim3(kFitThreads), 0, stream, a); break;
+    default: hipLaunchKernelGGL((proj_bf16_mfma<D, 8, ROPE>), grid, dim3(kFitThreads), 0, stream, a); break;
   }
+  return hipGetLastError();
+}
+
+template <bool ROPE>
+static hipError_t launch_proj_variants(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens,
+                                       int max_rank, hipStream_t stream) {
+  dim3 grid((max_tokens + kProjChunk - 1) / kProjChunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+  const int D = a.pv.head_dim;
+  if (dtype == KVC_BF16) {
+    const int mtr = (max_rank + 15) / 16;
+    return D == 64 ? launch_proj_bf16<64, ROPE>(a, mtr, grid, stream) : launch_proj_bf16<128, ROPE>(a, mtr, grid, stream);
+  }
+  const size_t lds = (size_t)max_rank * D * sizeof(float);
+  if (D == 64) hipLaunchKernelGGL((proj_f32_valu<64, ROPE>), grid, dim3(kFitThreads), lds, stream, a);
+  else hipLaunchKernelGGL((proj_f32_valu<128, ROPE>), grid, dim3(kFitThreads), lds, stream, a);
   return hipGetLastError();
 }
 
 hipError_t launch_fit_proj(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens, int max_rank,
                            hipStream_t stream) {
   if (max_rank == 0 || max_tokens == 0) return hipSuccess;
-  dim3 grid((max_tokens + kProjChunk - 1) / kProjChunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
-  const int D = a.pv.head_dim;
-  if (dtype == KVC_BF16) {
-    const int mtr = (max_rank + 15) / 16;
-    return D == 64 ? launch_proj_bf16<64>(a, mtr, grid, stream) : launch_proj_bf16<128>(a, mtr, grid, stream);
-  }
-  const size_t lds = (size_t)max_rank * D * sizeof(float);
-  if (D == 64) hipLaunchKernelGGL(proj_f32_valu<64>, grid, dim3(kFitThreads), lds, stream, a);
-  else hipLaunchKernelGGL(proj_f32_valu<128>, grid, dim3(kFitThreads), lds, stream, a);
-  return hipGetLastError();
+  return a.pv.rope.style != KVC_ROPE_NONE
+             ? launch_proj_variants<true>(a, dtype, num_items, max_tokens, max_rank, stream)
+             : launch_proj_variants<false>(a, dtype, num_items, max_tokens, max_rank, stream);
 }
 
 }  // namespace kvc

@@ -76,3 +76,80 @@ def test_apply_with_rope_matches_oracle(name, layers, style, theta, ps, pd, Ts, 
     assert worst <= TOL[dt], worst
     if ps != pd or rank > 0:
         assert teeth >= 10 * TOL[dt]
+
+
+def _rotate_torch(rows, pos, inv_freq, style):
+    """Rows [..., d] (float64, CPU) rotated to position `pos` -- the input side of the fit tests, written with torch
+    so that the inputs do not come from the oracle."""
+    d = rows.shape[-1]
+    ang = torch.tensor(inv_freq, dtype=torch.float64) * float(pos)
+    c, s = torch.cos(ang), torch.sin(ang)
+    out = rows.clone()
+    if style == HALF:
+        a, b = rows[..., : d // 2], rows[..., d // 2:]
+        out[..., : d // 2], out[..., d // 2:] = a * c - b * s, a * s + b * c
+    else:
+        a, b = rows[..., 0::2], rows[..., 1::2]
+        out[..., 0::2], out[..., 1::2] = a * c - b * s, a * s + b * c
+    return out
+
+
+def _rotate_keys_in_place(pc, seq, pos, inv_freq, style):
+    """Rewrite the key rows of one sequence as rotary keys at `pos` (the generated rows are taken as canonical)."""
+    w = pc.workload
+    T, bs = seq.num_tokens, w.block_size
+    t = torch.arange(T) + seq.offset
+    blk = t // bs if pc.tables is None else pc.tables[seq.table_row].cpu().long()[t // bs]
+    slot = t % bs
+    for pool in pc.k_pools:
+        rows = pool[blk.to(pool.device), slot.to(pool.device)].to("cpu", torch.float64)  # [T, H, d]
+        pool[blk.to(pool.device), slot.to(pool.device)] = _rotate_torch(rows, pos, inv_freq, style).to(pool.dtype).to(
+            pool.device)
+
+
+@pytest.mark.parametrize("name,layers,style,ps,pd,rank", [
+    ("tiny", 2, HALF, 37, 5000, 8),
+    ("tiny", 1, PAIRS, 0, 0, 8),
+    ("llama8b_4k", 2, HALF, 4096, 1000, 16),
+    ("llama8b_4k", 1, PAIRS, 100, 2100, 16),
+])
+def test_fit_with_rope_matches_oracle(name, layers, style, ps, pd, rank):
+    from tests.test_fit_gpu import _compare_states
+    w = synth.WORKLOADS[name].with_(num_layers=layers)
+    pc = synth.build_paged(w, device="cuda", num_output_agents=1)
+    H, d = w.num_kv_heads, w.head_dim
+    inv = Hp.rope_inv_freq(d, 5e5 if name != "tiny" else 1e4)
+    s0, s1, out = pc.seqs[(0, 0)], pc.seqs[(0, 1)], pc.seqs[(0, 100)]
+    _rotate_keys_in_place(pc, s0, ps, inv, style)
+    _rotate_keys_in_place(pc, s1, pd, inv, style)
+    tab = (lambda s: None) if pc.tables is None else (lambda s: pc.tables[[s.table_row]])
+    T = s1.num_tokens
+    sdt = synth.storage_dtype(w)
+    st = kvc.State.empty(layers, H, d, T, rank, sdt, "cuda")
+    cache = kvc.Cache(pc.k_pools, pc.v_pools, rope_style=style, rope_inv_freq=inv)
+    batch = kvc.Batch([T], [s0.offset], [s1.offset], [st], tab(s0), tab(s1), src_positions=[ps], dst_positions=[pd])
+    kvc.kvc_fit_state(cache, batch)
+    torch.cuda.synchronize()
+    rope = O.Rope(inv, Hp.ROPE_STYLE_NAME[style])
+    cnp = Hp.oracle_cache(pc.k_pools, pc.v_pools, w.block_size, rope)
+    item = O.Item(T, s0.offset, s1.offset, Hp.table_np(tab(s0), 0), Hp.table_np(tab(s1), 0), None, ps, pd)
+    ost, raw = O.fit(cnp, [item], rank)
+    worst_p, worst_s = _compare_states([st], [raw[0]], cnp.dtype)
+    print(f"{name} style {style} ({ps}->{pd}): product err {worst_p:.2e}, sigma err {worst_s:.2e}")
+    # the canonical state carries agent 1 from agent 0: applying it from ps to pd rebuilds agent 1's keys
+    batch_a = kvc.Batch([T], [s0.offset], [out.offset], [st], tab(s0), tab(out), src_positions=[ps],
+                        dst_positions=[pd])
+    kvc.kvc_apply(cache, batch_a)
+    torch.cuda.synchronize()
+    got = Hp.oracle_cache(pc.k_pools, pc.v_pools, w.block_size, rope)
+    ref = O.apply(cnp, [O.Item(T, s0.offset, out.offset, item.src_table, Hp.table_np(tab(out), 0), ost[0], ps, pd)])
+    dt = cnp.dtype
+    worst = 0.0
+    for layer in range(layers):
+        for kv_ in range(2):
+            for h in range(H):
+                g = O.read_rows(got, layer, kv_, h, Hp.table_np(tab(out), 0), out.offset, T)
+                e = O.read_rows(ref, layer, kv_, h, Hp.table_np(tab(out), 0), out.offset, T)
+                worst = max(worst, O.max_relative_error(O.to_f64(g, dt), O.to_f64(e, dt)))
+    print(f"  materialised from the fitted state: err {worst:.2e}")
+    assert worst <= TOL[dt], worst
