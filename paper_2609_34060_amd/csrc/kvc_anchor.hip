@@ -34,30 +34,48 @@ int anchor_chunk_tokens() { return kAnchorChunk; }
 // stores are conflict-free (the loads read 64-byte row segments).  The loads of the next basis are issued into
 // registers before the current one is used (load) and written to the other LDS buffer one step later (store), so a
 // workgroup waits once per basis at its barrier.
-template <int D, int KSM>
+// ROPE: with `rot` set (keys of a rotary cache) each basis row is rotated like a key row by the angles of the table
+// (c, s): the partner feature's values are loaded with the item's own and the rotation is applied at the store.
+template <int D, int KSM, bool ROPE = false>
 struct BasisStager {
   static constexpr int KP = 32 * KSM, KG = KP / 8;
   static constexpr int NI = D * KG / kAnchorThreads;  // items per thread
   static_assert(NI * kAnchorThreads == D * KG, "whole items per thread");
   float v[NI][8];
-  __device__ __forceinline__ void load(const float* basis, int r) {
+  float pv[ROPE ? NI : 1][8];
+  __device__ __forceinline__ void load(const float* basis, int r, bool rot = false, int style = 0) {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int idx = (int)threadIdx.x + i * kAnchorThreads;
       const int c = idx % KG, f = idx / KG;
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[i][e] = 8 * c + e < r ? basis[(8 * c + e) * D + f] : 0.0f;
+      if (ROPE && rot) {
+        const int pf = rope_partner(style, D, f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pv[i][e] = 8 * c + e < r ? basis[(8 * c + e) * D + pf] : 0.0f;
+      }
     }
   }
-  __device__ __forceinline__ void store(uint16_t* s_hi, uint16_t* s_lo) const {
+  __device__ __forceinline__ void store(uint16_t* s_hi, uint16_t* s_lo, bool rot = false, int style = 0,
+                                        const float* rc = nullptr, const float* rs = nullptr) const {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int idx = (int)threadIdx.x + i * kAnchorThreads;
+      float x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = v[i][e];
+      if (ROPE && rot) {
+        const int f = idx / KG, pi = rope_pair(style, D, f);
+        const bool first = rope_first(style, D, f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = rope_rotated(first, v[i][e], pv[i][e], rc[pi], rs[pi]);
+      }
       u32x4 hi, lo;
 #pragma unroll
       for (int p = 0; p < 4; ++p) {
         uint32_t hh, ll;
-        split_bf16x2(v[i][2 * p], v[i][2 * p + 1], hh, ll);
+        split_bf16x2(x[2 * p], x[2 * p + 1], hh, ll);
         hi[p] = hh;
         lo[p] = ll;
       }
@@ -89,12 +107,14 @@ __device__ __forceinline__ void load_row_segments(const uint16_t* pool, int64_t 
 // distances (weights / gate), bf16
 // ---------------------------------------------------------------------------------------------------------------
 
-template <int D, int KSM, bool GATE>
+// ROPE: keys of a rotary cache are compared in canonical coordinates, R(-ps) C_src (the anchors are canonical).
+template <int D, int KSM, bool GATE, bool ROPE>
 __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_bf16(AnchorArgs a) {
   constexpr int MT = D / 16, NQ = D / 32, KP = 32 * KSM;
   extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
   uint16_t* s_b = reinterpret_cast<uint16_t*>(anchor_lds);   // [2 buffers][hi, lo][D * KP]
   float* s_d = reinterpret_cast<float*>(s_b + 4 * D * KP);     // GATE: [waves][V]; else [chunk][V]
+  float* s_rope = s_d + (GATE ? kAnchorWaves : kAnchorChunk) * KVC_MAX_ANCHORS;  // cos / sin of -ps
 
   const int lrel = blockIdx.z, layer = a.layer_begin + lrel;
   const int kv = GATE ? 1 : blockIdx.y;
@@ -106,6 +126,9 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_bf16(AnchorArgs a)
   const uint16_t* pool = static_cast<const uint16_t*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
   const int nd = GATE ? kAnchorWaves * V : kAnchorChunk * V;
   for (int e = threadIdx.x; e < nd; e += kAnchorThreads) s_d[e] = 0.0f;
+  const bool rot = ROPE && kv == 0;  // uniform; read after the first barrier below
+  const int style = a.pv.rope.style;
+  if (rot) rope_table(a.pv.rope, D, -(double)a.src_position, s_rope, s_rope + D / 2);
 
   BasisStager<D, KSM> stager;
   auto basis_of = [&](int hv) {
@@ -146,14 +169,21 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_bf16(AnchorArgs a)
           acc[mt] = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[fo])), cb, acc[mt]);
         }
       }
-      float s = 0.0f;
+      f32x4 xv[MT];
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
+        xv[2 * q] = f32x4{bf16_lo_to_f32(raw[q][0]), bf16_hi_to_f32(raw[q][0]), bf16_lo_to_f32(raw[q][1]),
+                          bf16_hi_to_f32(raw[q][1])};
+        xv[2 * q + 1] = f32x4{bf16_lo_to_f32(raw[q][2]), bf16_hi_to_f32(raw[q][2]), bf16_lo_to_f32(raw[q][3]),
+                              bf16_hi_to_f32(raw[q][3])};
+      }
+      if (ROPE && rot) rope_rotate_rows<D>(xv, style, g, s_rope, s_rope + D / 2);
+      float s = 0.0f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t w = raw[q][e >> 1];
-          const float x = (e & 1) ? bf16_hi_to_f32(w) : bf16_lo_to_f32(w);
-          const float diff = x - acc[2 * q + (e >> 2)][e & 3];
+      for (int m = 0; m < MT; ++m) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float diff = xv[m][e] - acc[m][e];
           s += GATE ? diff * diff : fabsf(diff);
         }
       }
@@ -199,12 +229,13 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_bf16(AnchorArgs a)
 // distances, float32 (VALU): D / 4 lanes per token, four features per lane
 // ---------------------------------------------------------------------------------------------------------------
 
-template <int D, bool GATE>
+template <int D, bool GATE, bool ROPE>
 __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_f32(AnchorArgs a) {
   constexpr int LPT = D / 4, TPP = kAnchorThreads / LPT;
   extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
   float* s_b = reinterpret_cast<float*>(anchor_lds);           // [max_rank][D]
   float* s_d = s_b + a.max_rank * D;                            // GATE: [TPP][V]; else [chunk][V]
+  float* s_rope = s_d + (GATE ? TPP : kF32Chunk) * KVC_MAX_ANCHORS;  // cos / sin of -ps (rotary keys)
   const int lrel = blockIdx.z, layer = a.layer_begin + lrel;
   const int kv = GATE ? 1 : blockIdx.y;
   const int H = a.pv.num_kv_heads, V = a.num_anchors;
@@ -215,6 +246,9 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_f32(AnchorArgs a) 
   const float* pool = static_cast<const float*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
   const int nd = GATE ? TPP * V : kF32Chunk * V;
   for (int e = threadIdx.x; e < nd; e += kAnchorThreads) s_d[e] = 0.0f;
+  const bool rot = ROPE && kv == 0;  // canonical source keys R(-ps) C_src; the table is read after a barrier
+  const int style = a.pv.rope.style;
+  if (rot) rope_table(a.pv.rope, D, -(double)a.src_position, s_rope, s_rope + D / 2);
   for (int h = 0; h < H; ++h) {
     const int64_t unit = unit_index(layer, kv, h, H);
     for (int v = 0; v < V; ++v) {
@@ -230,6 +264,17 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_f32(AnchorArgs a) 
         if (t < Tl) {
           const int64_t so = row_offset(a.pv, a.src_table, a.src_offset, t, h);
           f32x4 x = so >= 0 ? *reinterpret_cast<const f32x4*>(pool + so + f0) : f32x4{0.f, 0.f, 0.f, 0.f};
+          if (ROPE && rot && so >= 0) {
+            const f32x4 y = *reinterpret_cast<const f32x4*>(pool + so + (rope_partner(style, D, f0) & ~3));
+            f32x4 xc;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int f = f0 + j, i = rope_pair(style, D, f);
+              const float partner = style == KVC_ROPE_HALF ? y[j] : x[j ^ 1];
+              xc[j] = rope_rotated(rope_first(style, D, f), x[j], partner, s_rope[i], s_rope[D / 2 + i]);
+            }
+            x = xc;
+          }
           const float* crow = coef + (int64_t)t * r;
           for (int k = 0; k < r; ++k) {
             const float c = crow[k];
@@ -288,11 +333,13 @@ __global__ __launch_bounds__(kAnchorThreads) void gate_finish(AnchorArgs a) {
 // (one basis staging per anchor and workgroup), then C_src + correction is rounded once and stored
 // ---------------------------------------------------------------------------------------------------------------
 
-template <int D, int KSM>
+// ROPE: keys of a rotary cache, C_dst = R(pd - ps) C_src + sum_v w_v A_v (B_v R(pd)^T) (bases staged rotated).
+template <int D, int KSM, bool ROPE>
 __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_bf16(AnchorArgs a) {
   constexpr int MT = D / 16, NQ = D / 32, TPW = kAnchoredTiles, KP = 32 * KSM;
   extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
   uint16_t* s_b = reinterpret_cast<uint16_t*>(anchor_lds);  // [2 buffers][hi, lo][D * KP]
+  float* s_rope = reinterpret_cast<float*>(s_b + 4 * D * KP);  // cos / sin of pd - ps, then of pd
 
   const int lrel = blockIdx.z, layer = a.layer_begin + lrel;
   const int H = a.pv.num_kv_heads;
@@ -305,6 +352,14 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_bf16(AnchorArgs
   const uint16_t* src_pool = static_cast<const uint16_t*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
   uint16_t* dst_pool = static_cast<uint16_t*>(const_cast<void*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]));
   const float* wrow = a.weights + (int64_t)(lrel * 2 + kv) * Ts * V;
+  const bool rot = ROPE && kv == 0;  // uniform over the workgroup
+  const bool shift = rot && a.dst_position != a.src_position;
+  const int style = a.pv.rope.style;
+  if (rot) {
+    rope_table(a.pv.rope, D, (double)a.dst_position - (double)a.src_position, s_rope, s_rope + D / 2);
+    rope_table(a.pv.rope, D, (double)a.dst_position, s_rope + D, s_rope + 3 * D / 2);
+    __syncthreads();
+  }
 
   f32x4 acc[TPW][MT];
 #pragma unroll
@@ -313,15 +368,15 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_bf16(AnchorArgs
     for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   if (t_begin < Ts) {  // whole workgroup
-    BasisStager<D, KSM> stager;
-    stager.load(a.basis[0] + unit * (int64_t)a.rank[0] * D, a.rank[0]);
+    BasisStager<D, KSM, ROPE> stager;
+    stager.load(a.basis[0] + unit * (int64_t)a.rank[0] * D, a.rank[0], rot, style);
     for (int v = 0; v < V; ++v) {
       const int r = a.rank[v], KS = (r + 31) / 32;
       uint16_t* s_hi = s_b + (v & 1) * 2 * D * KP;
       uint16_t* s_lo = s_hi + D * KP;
-      stager.store(s_hi, s_lo);
+      stager.store(s_hi, s_lo, rot, style, s_rope + D, s_rope + 3 * D / 2);
       __syncthreads();  // this basis is in LDS; the other buffer is no longer read
-      if (v + 1 < V) stager.load(a.basis[v + 1] + unit * (int64_t)a.rank[v + 1] * D, a.rank[v + 1]);
+      if (v + 1 < V) stager.load(a.basis[v + 1] + unit * (int64_t)a.rank[v + 1] * D, a.rank[v + 1], rot, style);
       const uint16_t* coef = static_cast<const uint16_t*>(a.coef[v]) + unit * (int64_t)a.tokens[v] * r;
 #pragma unroll
       for (int j = 0; j < TPW; ++j) {
@@ -366,14 +421,22 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_bf16(AnchorArgs
     load_row_segments<NQ>(src_pool, valid ? row_offset(a.pv, a.src_table, a.src_offset, t, head) : -1, g, raw);
     const int64_t dof = valid ? row_offset(a.pv, a.dst_table, a.dst_offset, t, head) : -1;
     u32x4 outw[NQ];
-    const bool crow = t < Ts;
+    // rows past T_s have a zero correction: the re-aligned source with a shift, else bit copies
+    const bool crow = t < Ts || shift;
+    f32x4 xv[MT];
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      const f32x4 x = acc[j][2 * q], y = acc[j][2 * q + 1];
-      const u32x4 c = {pack_bf16x2(bf16_lo_to_f32(raw[q][0]) + x[0], bf16_hi_to_f32(raw[q][0]) + x[1]),
-                       pack_bf16x2(bf16_lo_to_f32(raw[q][1]) + x[2], bf16_hi_to_f32(raw[q][1]) + x[3]),
-                       pack_bf16x2(bf16_lo_to_f32(raw[q][2]) + y[0], bf16_hi_to_f32(raw[q][2]) + y[1]),
-                       pack_bf16x2(bf16_lo_to_f32(raw[q][3]) + y[2], bf16_hi_to_f32(raw[q][3]) + y[3])};
+      xv[2 * q] = f32x4{bf16_lo_to_f32(raw[q][0]), bf16_hi_to_f32(raw[q][0]), bf16_lo_to_f32(raw[q][1]),
+                        bf16_hi_to_f32(raw[q][1])};
+      xv[2 * q + 1] = f32x4{bf16_lo_to_f32(raw[q][2]), bf16_hi_to_f32(raw[q][2]), bf16_lo_to_f32(raw[q][3]),
+                            bf16_hi_to_f32(raw[q][3])};
+    }
+    if (ROPE && shift) rope_rotate_rows<D>(xv, style, g, s_rope, s_rope + D / 2);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const f32x4 x = xv[2 * q] + acc[j][2 * q], y = xv[2 * q + 1] + acc[j][2 * q + 1];
+      const u32x4 c = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(y[0], y[1]),
+                       pack_bf16x2(y[2], y[3])};
       outw[q] = crow ? c : raw[q];
     }
     if (dof >= 0) {
@@ -384,11 +447,12 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_bf16(AnchorArgs
 }
 
 // anchored apply, float32 (VALU): D / 4 lanes per token; the tokens of a workgroup accumulate over the anchors
-template <int D>
+template <int D, bool ROPE>
 __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_f32(AnchorArgs a) {
   constexpr int LPT = D / 4, TPP = kAnchorThreads / LPT, NP = kF32Chunk / TPP;
   extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
   float* s_b = reinterpret_cast<float*>(anchor_lds);  // [max_rank][D]
+  float* s_rope = s_b + a.max_rank * D;               // cos / sin of pd - ps, then of pd (rotary keys)
   const int lrel = blockIdx.z, layer = a.layer_begin + lrel;
   const int H = a.pv.num_kv_heads;
   const int kv = blockIdx.y / H, head = blockIdx.y - kv * H;
@@ -400,6 +464,14 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_f32(AnchorArgs 
   const float* src_pool = static_cast<const float*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
   float* dst_pool = static_cast<float*>(const_cast<void*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]));
   const float* wrow = a.weights + (int64_t)(lrel * 2 + kv) * Ts * V;
+  const bool rot = ROPE && kv == 0;  // uniform over the workgroup
+  const bool shift = rot && a.dst_position != a.src_position;
+  const int style = a.pv.rope.style;
+  if (rot) {
+    rope_table(a.pv.rope, D, (double)a.dst_position - (double)a.src_position, s_rope, s_rope + D / 2);
+    rope_table(a.pv.rope, D, (double)a.dst_position, s_rope + D, s_rope + 3 * D / 2);
+    __syncthreads();
+  }
   f32x4 acc[NP];
 #pragma unroll
   for (int p = 0; p < NP; ++p) acc[p] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -407,7 +479,16 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_f32(AnchorArgs 
     for (int v = 0; v < V; ++v) {
       const int r = a.rank[v];
       __syncthreads();
-      for (int e = threadIdx.x; e < r * D; e += kAnchorThreads) s_b[e] = a.basis[v][unit * (int64_t)r * D + e];
+      const float* bv = a.basis[v] + unit * (int64_t)r * D;
+      for (int e = threadIdx.x; e < r * D; e += kAnchorThreads) {
+        float x = bv[e];
+        if (rot) {  // B_v R(pd)^T
+          const int k = e / D, f = e - k * D, i = rope_pair(style, D, f);
+          x = rope_rotated(rope_first(style, D, f), x, bv[k * D + rope_partner(style, D, f)], s_rope[D + i],
+                           s_rope[3 * D / 2 + i]);
+        }
+        s_b[e] = x;
+      }
       __syncthreads();
       const float* coef = static_cast<const float*>(a.coef[v]) + unit * (int64_t)a.tokens[v] * r;
 #pragma unroll
@@ -437,7 +518,18 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_f32(AnchorArgs 
     const int64_t so = row_offset(a.pv, a.src_table, a.src_offset, t, head);
     const int64_t dof = row_offset(a.pv, a.dst_table, a.dst_offset, t, head);
     if (so < 0 || dof < 0) continue;
-    const f32x4 x = *reinterpret_cast<const f32x4*>(src_pool + so + f0);
+    f32x4 x = *reinterpret_cast<const f32x4*>(src_pool + so + f0);
+    if (ROPE && shift) {  // the source rotated by pd - ps
+      const f32x4 y = *reinterpret_cast<const f32x4*>(src_pool + so + (rope_partner(style, D, f0) & ~3));
+      f32x4 xr;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int f = f0 + j, i = rope_pair(style, D, f);
+        const float partner = style == KVC_ROPE_HALF ? y[j] : x[j ^ 1];
+        xr[j] = rope_rotated(rope_first(style, D, f), x[j], partner, s_rope[i], s_rope[D / 2 + i]);
+      }
+      x = xr;
+    }
     f32x4 o = x;
     if (t < Ts) {
 #pragma unroll
@@ -766,18 +858,19 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
 // launchers
 // ---------------------------------------------------------------------------------------------------------------
 
-// which: 0 weights, 1 apply, 2 gate
+// which: 0 weights, 1 apply, 2 gate.  Every layout ends with room for the rotary angle tables (4 x 64 floats).
 size_t anchor_lds_bytes(int D, int max_rank, kvc_dtype dtype, int which) {
   const int V = KVC_MAX_ANCHORS;
+  const size_t rope = 4 * 64 * sizeof(float);
   if (dtype == KVC_BF16) {
     const size_t kp = 32 * (size_t)((max_rank + 31) / 32);
     const size_t basis = 4 * (size_t)D * kp * sizeof(uint16_t);  // two buffers of hi/lo
-    if (which == 1) return basis;
-    return basis + (size_t)(which == 2 ? kAnchorWaves : kAnchorChunk) * V * sizeof(float);
+    if (which == 1) return basis + rope;
+    return basis + (size_t)(which == 2 ? kAnchorWaves : kAnchorChunk) * V * sizeof(float) + rope;
   }
   const size_t basis = (size_t)max_rank * D * sizeof(float);
-  if (which == 1) return basis;
-  return basis + (size_t)(which == 2 ? kAnchorThreads / (D / 4) : kF32Chunk) * V * sizeof(float);
+  if (which == 1) return basis + rope;
+  return basis + (size_t)(which == 2 ? kAnchorThreads / (D / 4) : kF32Chunk) * V * sizeof(float) + rope;
 }
 
 template <typename K>
@@ -790,8 +883,9 @@ static hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, const AnchorA
   return hipGetLastError();
 }
 
-// The chunk map of the resident-basis kernels (bf16); false when the anchors' chunks do not fit in LDS at once.
+// The chunk map of the resident-basis kernels (bf16, no rotary keys); false when they do not apply.
 static bool plan_resident(AnchorArgs& a) {
+  if (a.pv.rope.style != KVC_ROPE_NONE) return false;
   int nc = 0;
   for (int v = 0; v < a.num_anchors; ++v) {
     const int ks = std::max(1, (a.rank[v] + 31) / 32);
@@ -816,28 +910,28 @@ static size_t res_lds_bytes(const AnchorArgs& a, int which) {
   return std::max(basis, sums);
 }
 
-template <int D, bool GATE>
+template <int D, bool GATE, bool ROPE>
 static hipError_t launch_dist_bf16(const AnchorArgs& a, dim3 grid, size_t lds, hipStream_t stream) {
   switch ((a.max_rank + 31) / 32) {
-    case 1: return launch_with_lds(anchor_dist_bf16<D, 1, GATE>, grid, lds, a, stream);
-    case 2: return launch_with_lds(anchor_dist_bf16<D, 2, GATE>, grid, lds, a, stream);
-    case 3: return launch_with_lds(anchor_dist_bf16<D, 3, GATE>, grid, lds, a, stream);
-    default: return launch_with_lds(anchor_dist_bf16<D, 4, GATE>, grid, lds, a, stream);
+    case 1: return launch_with_lds(anchor_dist_bf16<D, 1, GATE, ROPE>, grid, lds, a, stream);
+    case 2: return launch_with_lds(anchor_dist_bf16<D, 2, GATE, ROPE>, grid, lds, a, stream);
+    case 3: return launch_with_lds(anchor_dist_bf16<D, 3, GATE, ROPE>, grid, lds, a, stream);
+    default: return launch_with_lds(anchor_dist_bf16<D, 4, GATE, ROPE>, grid, lds, a, stream);
   }
 }
 
-template <int D>
+template <int D, bool ROPE>
 static hipError_t launch_anchored_bf16(const AnchorArgs& a, dim3 grid, size_t lds, hipStream_t stream) {
   switch ((a.max_rank + 31) / 32) {
-    case 1: return launch_with_lds(apply_anchored_bf16<D, 1>, grid, lds, a, stream);
-    case 2: return launch_with_lds(apply_anchored_bf16<D, 2>, grid, lds, a, stream);
-    case 3: return launch_with_lds(apply_anchored_bf16<D, 3>, grid, lds, a, stream);
-    default: return launch_with_lds(apply_anchored_bf16<D, 4>, grid, lds, a, stream);
+    case 1: return launch_with_lds(apply_anchored_bf16<D, 1, ROPE>, grid, lds, a, stream);
+    case 2: return launch_with_lds(apply_anchored_bf16<D, 2, ROPE>, grid, lds, a, stream);
+    case 3: return launch_with_lds(apply_anchored_bf16<D, 3, ROPE>, grid, lds, a, stream);
+    default: return launch_with_lds(apply_anchored_bf16<D, 4, ROPE>, grid, lds, a, stream);
   }
 }
 
-hipError_t launch_anchor_weights(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream) {
-  if (a.num_weighted == 0 || a.num_layers == 0) return hipSuccess;
+template <bool ROPE>
+static hipError_t launch_weights_variant(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream) {
   const int D = a.pv.head_dim;
   const size_t lds = anchor_lds_bytes(D, a.max_rank, dtype, 0);
   if (dtype == KVC_BF16) {
@@ -849,15 +943,24 @@ hipError_t launch_anchor_weights(const AnchorArgs& a, kvc_dtype dtype, hipStream
                      : launch_with_lds(anchor_dist_res_bf16<128, false>, grid, rl, r, stream, kResThreads);
     }
     dim3 grid((a.num_weighted + kAnchorChunk - 1) / kAnchorChunk, 2, a.num_layers);
-    return D == 64 ? launch_dist_bf16<64, false>(a, grid, lds, stream) : launch_dist_bf16<128, false>(a, grid, lds, stream);
+    return D == 64 ? launch_dist_bf16<64, false, ROPE>(a, grid, lds, stream)
+                   : launch_dist_bf16<128, false, ROPE>(a, grid, lds, stream);
   }
   dim3 grid((a.num_weighted + kF32Chunk - 1) / kF32Chunk, 2, a.num_layers);
-  return D == 64 ? launch_with_lds(anchor_dist_f32<64, false>, grid, lds, a, stream)
-                 : launch_with_lds(anchor_dist_f32<128, false>, grid, lds, a, stream);
+  return D == 64 ? launch_with_lds(anchor_dist_f32<64, false, ROPE>, grid, lds, a, stream)
+                 : launch_with_lds(anchor_dist_f32<128, false, ROPE>, grid, lds, a, stream);
 }
 
+hipError_t launch_anchor_weights(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream) {
+  if (a.num_weighted == 0 || a.num_layers == 0) return hipSuccess;
+  return a.pv.rope.style != KVC_ROPE_NONE ? launch_weights_variant<true>(a, dtype, stream)
+                                          : launch_weights_variant<false>(a, dtype, stream);
+}
+
+// The gate reads value rows only, which carry no rotary encoding.
 hipError_t launch_gate_distances(const AnchorArgs& args, kvc_dtype dtype, hipStream_t stream) {
   AnchorArgs a = args;
+  a.pv.rope.style = KVC_ROPE_NONE;
   const int D = a.pv.head_dim;
   const size_t lds = anchor_lds_bytes(D, a.max_rank, dtype, 2);
   hipError_t e;
@@ -870,18 +973,19 @@ hipError_t launch_gate_distances(const AnchorArgs& args, kvc_dtype dtype, hipStr
     e = D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, true>, grid, rl, a, stream, kResThreads)
                 : launch_with_lds(anchor_dist_res_bf16<128, true>, grid, rl, a, stream, kResThreads);
   } else if (dtype == KVC_BF16) {
-    e = D == 64 ? launch_dist_bf16<64, true>(a, grid, lds, stream) : launch_dist_bf16<128, true>(a, grid, lds, stream);
+    e = D == 64 ? launch_dist_bf16<64, true, false>(a, grid, lds, stream)
+                : launch_dist_bf16<128, true, false>(a, grid, lds, stream);
   } else {
-    e = D == 64 ? launch_with_lds(anchor_dist_f32<64, true>, grid, lds, a, stream)
-                : launch_with_lds(anchor_dist_f32<128, true>, grid, lds, a, stream);
+    e = D == 64 ? launch_with_lds(anchor_dist_f32<64, true, false>, grid, lds, a, stream)
+                : launch_with_lds(anchor_dist_f32<128, true, false>, grid, lds, a, stream);
   }
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(gate_finish, dim3(1), dim3(kAnchorThreads), 0, stream, a);
   return hipGetLastError();
 }
 
-hipError_t launch_apply_anchored(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream) {
-  if (a.num_tokens == 0 || a.num_layers == 0) return hipSuccess;
+template <bool ROPE>
+static hipError_t launch_anchored_variant(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream) {
   const int D = a.pv.head_dim;
   const size_t lds = anchor_lds_bytes(D, a.max_rank, dtype, 1);
   if (dtype == KVC_BF16) {
@@ -893,11 +997,18 @@ hipError_t launch_apply_anchored(const AnchorArgs& a, kvc_dtype dtype, hipStream
                      : launch_with_lds(apply_anchored_res_bf16<128>, grid, rl, r, stream, kResThreads);
     }
     dim3 grid((a.num_tokens + kAnchoredChunk - 1) / kAnchoredChunk, 2 * a.pv.num_kv_heads, a.num_layers);
-    return D == 64 ? launch_anchored_bf16<64>(a, grid, lds, stream) : launch_anchored_bf16<128>(a, grid, lds, stream);
+    return D == 64 ? launch_anchored_bf16<64, ROPE>(a, grid, lds, stream)
+                   : launch_anchored_bf16<128, ROPE>(a, grid, lds, stream);
   }
   dim3 grid((a.num_tokens + kF32Chunk - 1) / kF32Chunk, 2 * a.pv.num_kv_heads, a.num_layers);
-  return D == 64 ? launch_with_lds(apply_anchored_f32<64>, grid, lds, a, stream)
-                 : launch_with_lds(apply_anchored_f32<128>, grid, lds, a, stream);
+  return D == 64 ? launch_with_lds(apply_anchored_f32<64, ROPE>, grid, lds, a, stream)
+                 : launch_with_lds(apply_anchored_f32<128, ROPE>, grid, lds, a, stream);
+}
+
+hipError_t launch_apply_anchored(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream) {
+  if (a.num_tokens == 0 || a.num_layers == 0) return hipSuccess;
+  return a.pv.rope.style != KVC_ROPE_NONE ? launch_anchored_variant<true>(a, dtype, stream)
+                                          : launch_anchored_variant<false>(a, dtype, stream);
 }
 
 }  // namespace kvc

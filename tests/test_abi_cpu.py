@@ -161,9 +161,33 @@ def _cases():
         f.items[0].src_offset = -1
         return f.apply(), kvc.KVC_ERR_SHAPE
 
+    def negative_position(f):
+        f.items[0].dst_position = -5
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def rope_style(f):
+        f.cache.rope_style = 3
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def rope_reserved(f):
+        f.cache.rope_reserved = 1
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def rope_null_freq(f):
+        f.cache.rope_style = kvc.KVC_ROPE_HALF
+        f.cache.rope_inv_freq = None
+        return f.apply(), kvc.KVC_ERR_NULL_ARG
+
+    def rope_nonfinite_freq(f):
+        f.inv = (ctypes.c_double * 64)(*([1.0] * 63 + [float("inf")]))
+        f.cache.rope_style = kvc.KVC_ROPE_PAIRS
+        f.cache.rope_inv_freq = ctypes.cast(f.inv, ctypes.POINTER(ctypes.c_double))
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
     return [null_cache, null_batch, head_dim, dtype, layer_range, stride_align, layer_ptr_align, null_layer,
             rank_gt_d, rank_gt_max, state_tokens, state_shape, coef_dtype, coef_align, null_coef, beyond_pool,
-            beyond_table, same_tables, overlap_rows, null_items_dev, reserved, negative_offset]
+            beyond_table, same_tables, overlap_rows, null_items_dev, reserved, negative_offset, negative_position,
+            rope_style, rope_reserved, rope_null_freq, rope_nonfinite_freq]
 
 
 @pytest.mark.parametrize("case", _cases(), ids=lambda c: c.__name__)

@@ -153,3 +153,55 @@ def test_fit_with_rope_matches_oracle(name, layers, style, ps, pd, rank):
                 worst = max(worst, O.max_relative_error(O.to_f64(g, dt), O.to_f64(e, dt)))
     print(f"  materialised from the fitted state: err {worst:.2e}")
     assert worst <= TOL[dt], worst
+
+
+@pytest.mark.parametrize("name,layers,style,ps,pd,ranks,Ts", [
+    ("tiny", 2, HALF, 300, 4000, [8, 4, 8], 200),
+    ("llama8b_4k", 1, PAIRS, 0, 0, [32, 16, 32], 2000),
+    ("llama8b_4k", 1, HALF, 2048, 100, [32, 64, 96], 4096),
+])
+def test_anchor_weights_and_anchored_apply_with_rope(name, layers, style, ps, pd, ranks, Ts):
+    """Key distances in canonical coordinates (R(-ps) C_src against the canonical anchor bases) and the anchored
+    correction rotated to the target positions."""
+    w, pc, src, dst, tab = _case(name, layers)
+    T, H, d = w.seq_tokens[0], w.num_kv_heads, w.head_dim
+    Ts = min(Ts, T)
+    inv = Hp.rope_inv_freq(d, 1e4 if name == "tiny" else 5e5)
+    sdt = synth.storage_dtype(w)
+    rope = O.Rope(inv, Hp.ROPE_STYLE_NAME[style])
+
+    def states(key, scales):
+        out = []
+        for v, (r, sc) in enumerate(zip(ranks, scales)):
+            c, b, _ = synth.random_state(layers, H, d, T, r, sdt, "cuda", key, v, coef_scale=sc)
+            out.append(kvc.State(c.contiguous(), b.contiguous()))
+        return out
+
+    bases = states(51, [(0.1 + 0.9 * v) / np.sqrt(r / d) for v, r in enumerate(ranks)])
+    deltas = states(52, [0.25 * np.sqrt(d / r) for r in ranks])
+    before = Hp.oracle_cache(pc.k_pools, pc.v_pools, w.block_size, rope)
+    cache = kvc.Cache(pc.k_pools, pc.v_pools, rope_style=style, rope_inv_freq=inv)
+    empty = kvc.State.empty(layers, H, d, 0, 0, sdt, "cuda")
+    anchors = kvc.Anchors(bases, Ts, layers)
+    kvc.kvc_anchor_weights(cache, kvc.Batch([T], [src.offset], [src.offset], [empty], tab(src), tab(src),
+                                            src_positions=[ps], dst_positions=[ps]), anchors)
+    kvc.kvc_apply_anchored(cache, kvc.Batch([T], [src.offset], [dst.offset], [empty], tab(src), tab(dst),
+                                            src_positions=[ps], dst_positions=[pd]), anchors.with_states(deltas))
+    torch.cuda.synchronize()
+    got_w = anchors.weights.cpu().numpy().astype(np.float64)
+    item = O.Item(T, src.offset, dst.offset, Hp.table_np(tab(src), 0), Hp.table_np(tab(dst), 0), None, ps, pd)
+    ref_w = O.softmax_weights(O.anchor_distances(before, item, [Hp.oracle_state(b.coef, b.basis) for b in bases], Ts))
+    werr = np.max(np.abs(got_w - ref_w))
+    ref = O.apply_anchored(before, item, [Hp.oracle_state(x.coef, x.basis) for x in deltas], ref_w, Ts)
+    got = Hp.oracle_cache(pc.k_pools, pc.v_pools, w.block_size, rope)
+    dt = before.dtype
+    worst = 0.0
+    for layer in range(layers):
+        for kv_ in range(2):
+            for h in range(H):
+                g = O.read_rows(got, layer, kv_, h, item.dst_table, item.dst_offset, T)
+                e = O.read_rows(ref, layer, kv_, h, item.dst_table, item.dst_offset, T)
+                worst = max(worst, O.max_relative_error(O.to_f64(g, dt), O.to_f64(e, dt)))
+    print(f"{name} style {style} ({ps}->{pd}): weight err {werr:.2e}, anchored apply err {worst:.2e}")
+    assert werr <= 2e-4, werr
+    assert worst <= TOL[dt], worst
