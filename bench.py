@@ -128,6 +128,45 @@ def anchor_pool_measurement(args, kvc, synth, torch):
             "weights_gbps": round(wb / (weights_ms * 1e-3) / 1e9, 2), "weights_bytes": wb}
 
 
+def rope_measurement(args, kvc, torch, pc, w, state, batch):
+    """The same apply and fit with rotary keys (rotate-half pairs, theta 5 x 10^5 as in Llama-3.1): the segment moves
+    from position 0 in the source agent to position 4096 in the target, so every key row is rotated in the pass."""
+    import numpy as np
+    L, H, d, T, r = w.num_layers, w.num_kv_heads, w.head_dim, w.seq_tokens[0], w.rank
+    inv = 500000.0 ** (-np.arange(0, d, 2, dtype=np.float64) / d)
+    cache = kvc.Cache(pc.k_pools, pc.v_pools, rope_style=kvc.KVC_ROPE_HALF, rope_inv_freq=inv)
+    src, dst, prev = pc.seqs[(0, 0)], pc.seqs[(0, 100)], pc.seqs[(0, 1)]
+
+    def positioned(a, b, st, pa, pb):
+        return kvc.Batch([T], [a.offset], [b.offset], [st], pc.tables[[a.table_row]], pc.tables[[b.table_row]],
+                         src_positions=[pa], dst_positions=[pb])
+
+    ab = positioned(src, dst, state, 0, 4096)
+    fs = kvc.State.empty(L, H, d, T, r, torch.bfloat16, "cuda")
+    fb = positioned(src, prev, fs, 0, 4096)
+    ws = torch.empty(kvc.kvc_fit_workspace_bytes(cache, fb), dtype=torch.uint8, device="cuda")
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * args.steps)]
+        for k in range(args.steps):
+            ev[2 * k].record()
+            fn()
+            ev[2 * k + 1].record()
+        torch.cuda.synchronize()
+        return sum(ev[2 * k].elapsed_time(ev[2 * k + 1]) for k in range(args.steps)) / args.steps
+
+    apply_ms = timed(lambda: kvc.kvc_apply(cache, ab))
+    fit_ms = timed(lambda: kvc.kvc_fit_state(cache, fb, workspace=ws))
+    gbps = _apply_bytes(L, H, d, T, r) / (apply_ms * 1e-3) / 1e9
+    del ws, fs
+    return {"workload": f"{w.name} with rotary keys (rotate-half, theta 5e5), segment moved from position 0 to 4096",
+            "apply_ms": round(apply_ms, 4), "apply_gbps": round(gbps, 2),
+            "apply_frac": round(gbps / HBM_PEAK_GBPS, 4), "fit_ms": round(fit_ms, 4),
+            "fit_token_layers_per_s": round(T * L / (fit_ms * 1e-3), 1)}
+
+
 def cpu_baseline(pc, w, sample_layers=(0, 1)):
     """The oracle as it stands on a bounded sample of the same workload: `sample_layers` (every K/V head) of the
     first two edges -- fit S_1 and S_2, compose T_2 = chain(S_1, S_2), apply T_2 to the first agent's cache."""
@@ -184,6 +223,7 @@ def main():
     ap.add_argument("--anchors", type=int, default=10, help="anchors per shared slot (the paper's default V)")
     ap.add_argument("--anchor-rank", type=int, default=32)
     ap.add_argument("--no-anchor-pool", action="store_true")
+    ap.add_argument("--no-rope", action="store_true", help="skip the rotary re-alignment measurement")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the steps, run one elementwise kernel that reads BYTES and writes BYTES (dst = -src "
                          "in float32), a plain copy of known size, so that HBM counters of a profiling run can be "
@@ -298,6 +338,8 @@ def main():
         "generation_s": round(t_gen, 2),
         "source_hash": src_hash,
     }
+    if not args.no_rope:
+        out["rope"] = rope_measurement(args, kvc, torch, pc, w, Tc[0], batch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(pc, w)
     if not args.no_anchor_pool:
