@@ -12,6 +12,8 @@ Everything is plain float64 NumPy, written to be checked against the paper by ey
   * fit       -- Eq. 12 observed transition Z = C_j - Align(C_i) (in canonical coordinates for rotary keys) and the
                  rank-r truncated SVD of Eq. 7: A = U_r Sigma_r, B = R_r^T.  Also Z = C_j for a base cache
                  (Section 3.3, Z in {C, Delta}).
+  * grouping  -- the factorisation unit: one (layer, K/V, KV head) with D = d, or one (layer, K/V) with all KV heads
+                 side by side, D = H d (the paper's per-layer feature dimension, Section 3.3).
   * chain     -- Eq. 6: Delta_{k<-i} = Delta_{k<-j} + Delta_{j<-i}; the composed state is the rank-r truncated SVD
                  (Eq. 7) of the materialised sum A1 B1 + A2 B2.
   * anchors   -- Eq. 8 with V anchors and token-wise weights: interpolation weights from the mean absolute distance
@@ -24,7 +26,8 @@ Everything is plain float64 NumPy, written to be checked against the paper by ey
   * metrics   -- normalised Frobenius error (Appendix A.1), effective rank at 90 % of the singular-value energy
                  (Section 3.1, Figure 2 caption), memory accounting O(VNLD) vs O(VNr(L+D)) (Sections 3.1, 3.3).
 
-Readings of the paper taken here (all listed in the design notes): factorisation per (layer, K/V, KV head);
+Readings of the paper taken here (all listed in the design notes): factorisation per (layer, K/V, KV head), or per
+(layer, K/V) with the heads side by side;
 Align = the rotary re-alignment of the keys (identity for a cache without rotary encoding, or at equal positions); canonical sign = largest-magnitude basis entry positive (lowest index on ties); the state's
 coefficients are stored in the cache dtype, bases and singular values in float32.
 """
@@ -152,29 +155,38 @@ class Cache:
         return (self.k, self.v)[kv][layer]
 
 
+GROUP_HEAD = 0   # one factorisation per (layer, K/V, KV head): Z is T x d
+GROUP_LAYER = 1  # one per (layer, K/V): Z is T x (H d), every KV head's features side by side (Section 3.3, D)
+
+
 @dataclasses.dataclass
 class State:
-    """Low-rank state of one sequence (Eq. 7): per (layer, K/V, head) unit, coef = A (T x r) and basis = B (r x d).
-
-    coef [L, 2, H, T, r] in the coefficient dtype (float32 values or bf16 bits), basis [L, 2, H, r, d] float32,
-    sigma [L, 2, H, r] float32."""
+    """Low-rank state of one sequence (Eq. 7).  Per KV head (GROUP_HEAD): coef = A (T x r) and basis = B (r x d) per
+    (layer, K/V, head), coef [L, 2, H, T, r], basis [L, 2, H, r, d], sigma [L, 2, H, r].  Per layer (GROUP_LAYER): one
+    factorisation of the layer's K (or V) rows with D = H d features, coef [L, 2, T, r], basis [L, 2, r, H, d]
+    (row k of B is basis[l, kv, k].reshape(H d): head h's features are its columns h d .. h d + d - 1),
+    sigma [L, 2, r].  coef in the coefficient dtype (float32 values or bf16 bits), basis and sigma float32."""
     coef: np.ndarray
     basis: np.ndarray
     sigma: Optional[np.ndarray]
     coef_dtype: str
+    grouping: int = GROUP_HEAD
 
     @property
     def num_tokens(self) -> int:
-        return self.coef.shape[3]
+        return self.coef.shape[-2]
 
     @property
     def rank(self) -> int:
-        return self.coef.shape[4]
+        return self.coef.shape[-1]
 
     def coef_f64(self, layer: int, kv: int, head: int) -> np.ndarray:
-        return to_f64(self.coef[layer, kv, head], self.coef_dtype)
+        c = self.coef[layer, kv] if self.grouping == GROUP_LAYER else self.coef[layer, kv, head]
+        return to_f64(c, self.coef_dtype)
 
     def basis_f64(self, layer: int, kv: int, head: int) -> np.ndarray:
+        if self.grouping == GROUP_LAYER:
+            return self.basis[layer, kv, :, head, :].astype(np.float64)
         return self.basis[layer, kv, head].astype(np.float64)
 
 
@@ -344,30 +356,50 @@ def fit_unit(src: Optional[np.ndarray], dst: np.ndarray, dtype: str, rank: int):
 
 
 def fit(cache: Cache, items: Sequence[Item], rank: int, coef_dtype: Optional[str] = None, mode: int = MODE_DELTA,
-        layer_begin: int = 0, layer_end: Optional[int] = None, state_tokens: Optional[Sequence[int]] = None):
+        layer_begin: int = 0, layer_end: Optional[int] = None, state_tokens: Optional[Sequence[int]] = None,
+        grouping: int = GROUP_HEAD):
     """A state per item, fitted over its first state_tokens[i] rows (default: all rows).
 
+    grouping GROUP_HEAD factorises every (layer, K/V, KV head) unit; GROUP_LAYER factorises each layer's K (or V)
+    rows with all KV heads side by side, Z = [Z_0 ... Z_{H-1}] (T x H d), the paper's per-layer feature dimension.
     Layers outside [layer_begin, layer_end) are left zero.  Coefficients are rounded once to coef_dtype (default:
-    the cache dtype), bases and singular values to float32.  Also returns the float64 factors per unit."""
+    the cache dtype), bases and singular values to float32.  Also returns the float64 factors (per unit, or per
+    layer with the basis as [r, H d])."""
     layer_end = cache.num_layers if layer_end is None else layer_end
     coef_dtype = cache.dtype if coef_dtype is None else coef_dtype
     L, H, d = cache.num_layers, cache.num_kv_heads, cache.head_dim
     states, raw = [], []
     for i, it in enumerate(items):
         Ts = it.num_tokens if state_tokens is None else int(state_tokens[i])
+
+        def deviation(layer, kv, h):
+            # Eq. 12 in canonical coordinates: Z = R(-p_dst) C_dst - R(-p_src) C_src for rotary keys
+            z = to_canonical(to_f64(read_rows(cache, layer, kv, h, it.dst_table, it.dst_offset, Ts), cache.dtype),
+                             cache, kv, it.dst_position)
+            if mode == MODE_DELTA:
+                z = z - to_canonical(to_f64(read_rows(cache, layer, kv, h, it.src_table, it.src_offset, Ts),
+                                            cache.dtype), cache, kv, it.src_position)
+            return z
+
+        if grouping == GROUP_LAYER:
+            coef = np.zeros((L, 2, Ts, rank))
+            basis = np.zeros((L, 2, rank, H * d))
+            sigma = np.zeros((L, 2, rank))
+            for layer in range(layer_begin, layer_end):
+                for kv in range(2):
+                    z = np.hstack([deviation(layer, kv, h) for h in range(H)])
+                    coef[layer, kv], basis[layer, kv], sigma[layer, kv] = truncated_svd(z, rank)
+            raw.append((coef, basis, sigma))
+            states.append(State(to_storage(coef, coef_dtype), f64_to_f32(basis).reshape(L, 2, rank, H, d),
+                                f64_to_f32(sigma), coef_dtype, GROUP_LAYER))
+            continue
         coef = np.zeros((L, 2, H, Ts, rank))
         basis = np.zeros((L, 2, H, rank, d))
         sigma = np.zeros((L, 2, H, rank))
         for layer in range(layer_begin, layer_end):
             for kv in range(2):
                 for h in range(H):
-                    # Eq. 12 in canonical coordinates: Z = R(-p_dst) C_dst - R(-p_src) C_src for rotary keys
-                    z = to_canonical(to_f64(read_rows(cache, layer, kv, h, it.dst_table, it.dst_offset, Ts),
-                                            cache.dtype), cache, kv, it.dst_position)
-                    if mode == MODE_DELTA:
-                        z = z - to_canonical(to_f64(read_rows(cache, layer, kv, h, it.src_table, it.src_offset, Ts),
-                                                    cache.dtype), cache, kv, it.src_position)
-                    a, b, s = truncated_svd(z, rank)
+                    a, b, s = truncated_svd(deviation(layer, kv, h), rank)
                     coef[layer, kv, h] = a
                     basis[layer, kv, h] = b
                     sigma[layer, kv, h] = s

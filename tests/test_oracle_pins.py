@@ -705,3 +705,85 @@ def test_anchor_distance_with_rope_uses_canonical_source_keys():
     assert np.allclose(dist, 0.0, atol=1e-6)
     plain = O.anchor_distances(O.Cache("f32", bs, cache.k, cache.v), item, [exact], T)
     assert np.all(plain[:, 0] > 0.05) and np.allclose(plain[:, 1], 0.0, atol=1e-6)
+
+
+# -------------------------------------------------------------- per-layer factorisation (Section 3.3, D = H d)
+
+def _layer_cache(zs, bs=4):
+    """A contiguous f32 cache whose layer-0 K and V rows of head h hold zs[h] (T x d); fitted in base mode."""
+    H = len(zs)
+    T, d = zs[0].shape
+    nb = -(-T // bs)
+    pool = np.zeros((nb * bs, H, d))
+    for h in range(H):
+        pool[:T, h] = zs[h]
+    k = [O.to_storage(pool.reshape(nb, bs, H, d), "f32")]
+    return O.Cache("f32", bs, k, [k[0].copy()]), O.Item(T, 0, 0, None, None)
+
+
+def test_layer_fit_of_independent_heads_has_the_union_of_their_singular_values():
+    """Head deviations with mutually orthogonal left factors: the per-layer SVD of [Z_0 ... Z_{H-1}] has exactly the
+    heads' singular values, and rank sum(r_h) reproduces every head."""
+    rng = np.random.default_rng(41)
+    T, H, d, r = 40, 3, 8, 2
+    u = np.linalg.qr(rng.standard_normal((T, H * r)))[0]
+    s = [np.array([5.0, 1.5]), np.array([3.0, 0.5]), np.array([4.0, 2.5])]
+    zs = [u[:, h * r:(h + 1) * r] * s[h] @ np.linalg.qr(rng.standard_normal((d, r)))[0].T for h in range(H)]
+    cache, item = _layer_cache(zs)
+    _, raw = O.fit(cache, [item], H * r, mode=O.MODE_BASE, grouping=O.GROUP_LAYER)
+    coef, basis, sigma = raw[0]
+    assert np.allclose(sigma[0, 0], np.sort(np.concatenate(s))[::-1], rtol=1e-6)
+    assert np.allclose(coef[0, 0] @ basis[0, 0], np.hstack(zs), atol=1e-5)
+
+
+def test_layer_fit_of_a_shared_left_factor_scales_singular_values_by_sqrt_heads():
+    """Z_h = U diag(s) V_h^T with orthonormal V_h: [Z_0 ... Z_{H-1}] = U diag(s) [V_0^T ... V_{H-1}^T] and the
+    right factor's rows have norm sqrt(H), so the per-layer singular values are sqrt(H) s and rank r is exact."""
+    rng = np.random.default_rng(42)
+    T, H, d, r = 30, 4, 8, 3
+    s = np.array([4.0, 2.0, 1.0])
+    u = np.linalg.qr(rng.standard_normal((T, r)))[0]
+    zs = [u * s @ np.linalg.qr(rng.standard_normal((d, r)))[0].T for _ in range(H)]
+    cache, item = _layer_cache(zs)
+    states, raw = O.fit(cache, [item], r, mode=O.MODE_BASE, grouping=O.GROUP_LAYER)
+    assert np.allclose(raw[0][2][0, 0], np.sqrt(H) * s, rtol=1e-6)
+    st = states[0]
+    for h in range(H):
+        assert np.allclose(st.coef_f64(0, 0, h) @ st.basis_f64(0, 0, h), zs[h], atol=1e-5)
+
+
+def test_layer_fit_eckart_young_against_independent_eigensolver():
+    rng = np.random.default_rng(43)
+    T, H, d, r = 50, 2, 8, 5
+    zs = [rng.standard_normal((T, d)) for _ in range(H)]
+    cache, item = _layer_cache(zs)
+    _, raw = O.fit(cache, [item], r, mode=O.MODE_BASE, grouping=O.GROUP_LAYER)
+    z = np.hstack([O.to_f64(O.read_rows(cache, 0, 0, h, None, 0, T), "f32") for h in range(H)])
+    lam = np.linalg.eigvalsh(z.T @ z)[::-1]  # LAPACK's symmetric eigensolver, not the SVD
+    res = np.linalg.norm(z - raw[0][0][0, 0] @ raw[0][1][0, 0]) ** 2
+    assert math.isclose(res, lam[r:].sum(), rel_tol=1e-9)
+    assert np.allclose(raw[0][2][0, 0] ** 2, lam[:r], rtol=1e-9)
+
+
+def test_apply_with_a_layer_state_uses_each_heads_columns():
+    """Brute force: head h of the corrected cache is C_src[h] + A B[:, h d : (h + 1) d], element by element."""
+    rng = np.random.default_rng(44)
+    T, H, d, r, bs = 6, 2, 4, 2, 4
+    nb = 2 * (-(-T // bs))
+    k = [O.to_storage(rng.standard_normal((nb, bs, H, d)), "f32")]
+    v = [O.to_storage(rng.standard_normal((nb, bs, H, d)), "f32")]
+    cache = O.Cache("f32", bs, k, v)
+    coef = O.to_storage(rng.standard_normal((1, 2, T, r)), "f32")
+    basis = rng.standard_normal((1, 2, r, H, d)).astype(np.float32)
+    st = O.State(coef, basis, None, "f32", O.GROUP_LAYER)
+    dst_off = nb * bs // 2
+    out = O.apply(cache, [O.Item(T, 0, dst_off, None, None, st)])
+    for kv, pools in ((0, out.k), (1, out.v)):
+        for h in range(H):
+            for t in range(T):
+                for f in range(d):
+                    acc = float(O.to_f64((k, v)[kv][0], "f32").reshape(nb * bs, H, d)[t, h, f])
+                    for j in range(r):
+                        acc += float(O.to_f64(coef[0, kv, t, j], "f32")) * float(basis[0, kv, j, h, f])
+                    got = float(O.to_f64(pools[0], "f32").reshape(nb * bs, H, d)[dst_off + t, h, f])
+                    assert math.isclose(got, acc, rel_tol=1e-6, abs_tol=1e-6)
