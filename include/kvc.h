@@ -110,9 +110,19 @@ typedef struct kvc_cache {
   const double* rope_inv_freq; /* HOST [head_dim / 2], or NULL with KVC_ROPE_NONE */
 } kvc_cache;
 
+/* Factorisation unit of a state.  The paper factorises each layer's keys (values) with the KV feature dimension D
+ * of the layer (Section 3.3); per KV head D = head_dim, per layer D = num_kv_heads * head_dim. */
+typedef enum kvc_grouping {
+  KVC_GROUP_HEAD = 0, /* unit (layer, K/V, head): coef [L][2][H][T_s][r], basis [L][2][H][r][d], sigma [L][2][H][r] */
+  KVC_GROUP_LAYER = 1 /* unit (layer, K/V): coef [L][2][T_s][r], basis [L][2][r][H d] (head h's features are the
+                         columns h d .. h d + d - 1 of a row), sigma [L][2][r] */
+} kvc_grouping;
+
 /* Low-rank state of one sequence (Eq. 7): coef = A, basis = B per unit.  DEVICE pointers.  coef_dtype is the cache
- * dtype for fit/apply (bf16 coefficients for bf16 caches, float32 for float32 caches).  0 <= rank <= min(head_dim,
- * KVC_MAX_RANK); rank 0 makes apply a copy.  coef must be 16-byte aligned.  sigma may be NULL. */
+ * dtype for fit/apply (bf16 coefficients for bf16 caches, float32 for float32 caches).  0 <= rank <= min(D,
+ * KVC_MAX_RANK) with D the unit's feature dimension; rank 0 makes apply a copy.  coef must be 16-byte aligned.
+ * sigma may be NULL.  Per-layer states (KVC_GROUP_LAYER) are fitted by kvc_fit_state and read by kvc_apply; the
+ * chain and anchor calls take per-head states. */
 typedef struct kvc_state {
   int32_t num_layers;
   int32_t num_kv_heads;
@@ -120,6 +130,8 @@ typedef struct kvc_state {
   int32_t num_tokens; /* T_s: coefficient rows per unit */
   int32_t rank;
   kvc_dtype coef_dtype;
+  int32_t grouping;   /* kvc_grouping */
+  int32_t reserved;   /* must be 0 */
   void* coef;
   float* basis;
   float* sigma;
@@ -159,6 +171,9 @@ int32_t kvc_last_hip_error(void);
 /* Bytes of one low-rank state (coef + basis + sigma), the O(N r (L + D)) term of Section 3.3. */
 size_t kvc_state_bytes(int32_t num_layers, int32_t num_kv_heads, int32_t head_dim, int32_t num_tokens, int32_t rank,
                        kvc_dtype coef_dtype);
+/* Bytes of a per-layer state (KVC_GROUP_LAYER): L x {K,V} x (T r coefficients + r H d basis + r sigma). */
+size_t kvc_layer_state_bytes(int32_t num_layers, int32_t num_kv_heads, int32_t head_dim, int32_t num_tokens,
+                             int32_t rank, kvc_dtype coef_dtype);
 /* Bytes of the same segment kept full-dimensional (L x {K,V} x T x H d), the O(N L D) term of Section 3.1. */
 size_t kvc_dense_bytes(int32_t num_layers, int32_t num_kv_heads, int32_t head_dim, int32_t num_tokens,
                        kvc_dtype dtype);

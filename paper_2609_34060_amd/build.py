@@ -14,7 +14,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_PATH = os.path.join(PKG, "libkvc.so")
 
-SOURCES = ["kvc_api.cpp", "kvc_apply.hip", "kvc_fit.hip", "kvc_eig.hip", "kvc_chain.hip", "kvc_anchor.hip"]
+SOURCES = ["kvc_api.cpp", "kvc_apply.hip", "kvc_fit.hip", "kvc_eig.hip", "kvc_chain.hip", "kvc_anchor.hip",
+           "kvc_layer.hip"]
 
 # Packed fp32 instructions are switched off for all device code.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",

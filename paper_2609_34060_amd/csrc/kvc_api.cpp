@@ -56,7 +56,9 @@ kvc_status check_cache(const kvc_cache* c, int32_t lb, int32_t le) {
 kvc_status check_state_shape(const kvc_state& s, int32_t L, int32_t H, int32_t d) {
   if (s.num_layers != L || s.num_kv_heads != H || s.head_dim != d) return KVC_ERR_SHAPE;
   if (!valid_dtype(s.coef_dtype)) return KVC_ERR_DTYPE;
-  if (s.rank < 0 || s.rank > std::min<int32_t>(d, KVC_MAX_RANK) || s.num_tokens < 0) return KVC_ERR_SHAPE;
+  if (s.reserved != 0 || (s.grouping != KVC_GROUP_HEAD && s.grouping != KVC_GROUP_LAYER)) return KVC_ERR_SHAPE;
+  const int32_t D = s.grouping == KVC_GROUP_LAYER ? H * d : d;
+  if (s.rank < 0 || s.rank > std::min<int32_t>(D, KVC_MAX_RANK) || s.num_tokens < 0) return KVC_ERR_SHAPE;
   if (s.rank > 0 && s.num_tokens > 0) {
     if (!s.coef || !s.basis) return KVC_ERR_NULL_ARG;
     if (!aligned16(s.coef) || !aligned16(s.basis)) return KVC_ERR_ALIGN;
@@ -135,6 +137,78 @@ FitPlan plan_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int32_t le)
   return p;
 }
 
+// Per-layer fit (KVC_GROUP_LAYER): items one at a time, all layers of the call (up to the launch limit) together;
+// at most 8 token partials per layer unit (a partial of D = H d is up to 4 MB).
+struct LayerPlan {
+  int32_t layers_per_group = 1, part_tokens = 256, max_parts = 1, k = 64;
+  size_t units = 0, off_partials = 0, off_gram = 0, off_x = 0, off_y = 0, off_h = 0, off_vrows = 0, off_vsigma = 0,
+         off_reflect = 0, off_beta = 0, off_vecs = 0, total = 0;
+};
+
+// Which calls the per-layer path takes (every item per layer, no rotary keys, D = H d <= 1024, rank + 16 <= k).
+kvc_status check_layer_fit(const kvc_cache* c, const kvc_batch* b) {
+  const int32_t DL = c->num_kv_heads * c->head_dim;
+  if (c->rope_style != KVC_ROPE_NONE || DL > 1024) return KVC_ERR_UNSUPPORTED;
+  for (int32_t i = 0; i < b->num_items; ++i) {
+    const kvc_state& st = b->items[i].state;
+    if (st.grouping != KVC_GROUP_LAYER) return KVC_ERR_UNSUPPORTED;
+    const int32_t k = st.rank + 16 <= 64 ? 64 : 128;
+    if (st.rank + 16 > 128 || k > DL) return KVC_ERR_UNSUPPORTED;
+    if (c->dtype == KVC_F32 && static_cast<size_t>(st.rank) * DL * 4 > 160 * 1024) return KVC_ERR_UNSUPPORTED;
+  }
+  return KVC_OK;
+}
+
+LayerPlan plan_layer_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int32_t le) {
+  LayerPlan p;
+  const int32_t nl = le - lb;
+  if (nl <= 0 || b->num_items <= 0) return p;
+  p.layers_per_group = std::min<int32_t>(nl, kvc::kMaxLayersPerLaunch);
+  int32_t tmax = 0, rmax = 0;
+  for (int32_t i = 0; i < b->num_items; ++i) {
+    tmax = std::max(tmax, b->items[i].state.num_tokens);
+    rmax = std::max(rmax, b->items[i].state.rank);
+  }
+  p.k = rmax + 16 <= 64 ? 64 : 128;
+  const size_t DL = static_cast<size_t>(c->num_kv_heads) * c->head_dim, k = p.k;
+  p.units = static_cast<size_t>(p.layers_per_group) * 2;
+  int64_t part = (std::max<int32_t>(tmax, 1) + 7) / 8;
+  part = std::max<int64_t>(256, (part + 31) / 32 * 32);
+  p.part_tokens = static_cast<int32_t>(part);
+  p.max_parts = static_cast<int32_t>(std::max<int64_t>(1, (tmax + part - 1) / part));
+  p.max_parts = (p.max_parts + 1) / 2 * 2;  // two token ranges per Gram workgroup
+  const size_t U = p.units;
+  size_t off = 0;
+  p.off_partials = off;
+  off = align256(off + U * p.max_parts * DL * DL * sizeof(float));
+  p.off_gram = off;
+  off = align256(off + U * DL * DL * sizeof(double));
+  p.off_x = off;
+  off = align256(off + U * k * DL * sizeof(double));
+  p.off_y = off;
+  off = align256(off + U * k * DL * sizeof(double));
+  p.off_h = off;
+  off = align256(off + U * k * k * sizeof(double));
+  p.off_vrows = off;
+  off = align256(off + U * KVC_MAX_RANK * k * sizeof(float));
+  p.off_vsigma = off;
+  off = align256(off + U * KVC_MAX_RANK * sizeof(float));
+  p.off_reflect = off;
+  off = align256(off + U * k * k * sizeof(double));
+  p.off_beta = off;
+  off = align256(off + U * k * sizeof(double));
+  p.off_vecs = off;
+  off = align256(off + U * KVC_MAX_RANK * k * sizeof(double));
+  p.total = off;
+  return p;
+}
+
+bool batch_is_per_layer(const kvc_batch* b) {
+  for (int32_t i = 0; i < b->num_items; ++i)
+    if (b->items[i].state.grouping == KVC_GROUP_LAYER) return true;
+  return false;
+}
+
 kvc_status check_chain(const kvc_state* a, const kvc_state* b, const kvc_state* o, int32_t lb, int32_t le) {
   if (!a || !b || !o) return KVC_ERR_NULL_ARG;
   const int32_t L = a->num_layers, H = a->num_kv_heads, d = a->head_dim;
@@ -143,6 +217,7 @@ kvc_status check_chain(const kvc_state* a, const kvc_state* b, const kvc_state* 
   for (const kvc_state* s : {a, b, o}) {
     kvc_status st = check_state_shape(*s, L, H, d);
     if (st != KVC_OK) return st;
+    if (s->grouping != KVC_GROUP_HEAD) return KVC_ERR_UNSUPPORTED;
   }
   if (b->coef_dtype != a->coef_dtype || o->coef_dtype != a->coef_dtype) return KVC_ERR_DTYPE;
   if (lb < 0 || le < lb || le > L) return KVC_ERR_SHAPE;
@@ -253,6 +328,7 @@ kvc_status check_anchor_call(const kvc_cache* c, const kvc_batch* b, const kvc_a
     const kvc_state& st = an->states[v];
     s = check_state_shape(st, c->num_layers, c->num_kv_heads, c->head_dim);
     if (s != KVC_OK) return s;
+    if (st.grouping != KVC_GROUP_HEAD) return KVC_ERR_UNSUPPORTED;
     if (st.coef_dtype != c->dtype) return KVC_ERR_DTYPE;
     if (st.rank < 1 || st.num_tokens < an->num_tokens) return KVC_ERR_SHAPE;
     if (!st.coef || !st.basis) return KVC_ERR_NULL_ARG;
@@ -336,6 +412,13 @@ size_t kvc_state_bytes(int32_t L, int32_t H, int32_t d, int32_t T, int32_t r, kv
                   static_cast<size_t>(r) * 4);
 }
 
+size_t kvc_layer_state_bytes(int32_t L, int32_t H, int32_t d, int32_t T, int32_t r, kvc_dtype coef_dtype) {
+  if (L < 0 || H < 0 || d < 0 || T < 0 || r < 0 || !valid_dtype(coef_dtype)) return 0;
+  const size_t units = static_cast<size_t>(L) * 2;
+  return units * (static_cast<size_t>(T) * r * dtype_size(coef_dtype) + static_cast<size_t>(r) * H * d * 4 +
+                  static_cast<size_t>(r) * 4);
+}
+
 size_t kvc_dense_bytes(int32_t L, int32_t H, int32_t d, int32_t T, kvc_dtype dtype) {
   if (L < 0 || H < 0 || d < 0 || T < 0 || !valid_dtype(dtype)) return 0;
   return static_cast<size_t>(L) * 2 * H * static_cast<size_t>(T) * d * dtype_size(dtype);
@@ -393,7 +476,84 @@ size_t kvc_fit_workspace_bytes(const kvc_cache* cache, const kvc_batch* batch, i
                                int32_t layer_end) {
   if (check_cache(cache, layer_begin, layer_end) != KVC_OK || !batch || batch->num_items < 0) return 0;
   if (batch->num_items > 0 && !batch->items) return 0;
+  if (batch_is_per_layer(batch)) {
+    if (check_layer_fit(cache, batch) != KVC_OK) return 0;
+    return plan_layer_fit(cache, batch, layer_begin, layer_end).total;
+  }
   return plan_fit(cache, batch, layer_begin, layer_end).total;
+}
+
+// Per-layer fit: for each item and group of layers, the head-pair Gram, the subspace iteration with its
+// Rayleigh-Ritz eigenproblem, the basis rows and the multi-head projection.
+kvc_status fit_per_layer(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
+                         kvc_fit_mode mode, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  const LayerPlan p = plan_layer_fit(cache, batch, layer_begin, layer_end);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < p.total)
+    return KVC_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  kvc::LayerFitArgs la;
+  std::memset(&la, 0, sizeof(la));
+  fill_pool_view(cache, la.pv);
+  la.max_blocks = batch->max_blocks;
+  la.mode = mode;
+  la.k = p.k;
+  la.max_parts = p.max_parts;
+  la.part_tokens = p.part_tokens;
+  la.partials = reinterpret_cast<float*>(ws + p.off_partials);
+  la.gram = reinterpret_cast<double*>(ws + p.off_gram);
+  la.x = reinterpret_cast<double*>(ws + p.off_x);
+  la.y = reinterpret_cast<double*>(ws + p.off_y);
+  la.hmat = reinterpret_cast<double*>(ws + p.off_h);
+  la.vrows = reinterpret_cast<float*>(ws + p.off_vrows);
+  la.vsigma = reinterpret_cast<float*>(ws + p.off_vsigma);
+  kvc_status s = KVC_OK;
+  for (int32_t i = 0; i < batch->num_items; ++i) {
+    const kvc_state& st = batch->items[i].state;
+    if (st.rank == 0 || st.num_tokens == 0) continue;
+    la.rank = st.rank;
+    la.items = batch->items_dev + i;
+    la.src_tables = batch->src_tables ? batch->src_tables + static_cast<int64_t>(i) * batch->max_blocks : nullptr;
+    la.dst_tables = batch->dst_tables ? batch->dst_tables + static_cast<int64_t>(i) * batch->max_blocks : nullptr;
+    for (int32_t l0 = layer_begin; l0 < layer_end; l0 += p.layers_per_group) {
+      const int32_t l1 = std::min(layer_end, l0 + p.layers_per_group);
+      la.layer_begin = l0;
+      la.num_layers = l1 - l0;
+      la.num_units = 2 * la.num_layers;
+      for (int32_t l = l0; l < l1; ++l) {
+        la.layers.k[l - l0] = cache->k_layers[l];
+        la.layers.v[l - l0] = cache->v_layers[l];
+      }
+      // the Rayleigh-Ritz eigenproblem of each layer unit, through the dense-input eigensolver into scratch rows
+      kvc::EigArgs ea;
+      std::memset(&ea, 0, sizeof(ea));
+      ea.n = p.k;
+      ea.num_units = la.num_units;
+      ea.dense = la.hmat;
+      ea.items = nullptr;
+      ea.state.num_layers = la.num_layers;
+      ea.state.num_kv_heads = 1;
+      ea.state.head_dim = p.k;
+      ea.state.num_tokens = st.num_tokens;
+      ea.state.rank = st.rank;
+      ea.state.coef_dtype = cache->dtype;
+      ea.state.basis = la.vrows;
+      ea.state.sigma = la.vsigma;
+      ea.layer_begin = 0;
+      ea.num_layers = la.num_layers;
+      ea.num_kv_heads = 1;
+      ea.reflect = reinterpret_cast<double*>(ws + p.off_reflect);
+      ea.reflect_beta = reinterpret_cast<double*>(ws + p.off_beta);
+      ea.vecs = reinterpret_cast<double*>(ws + p.off_vecs);
+      ea.seed = 0x1A7Eu;
+      s = hip_status(kvc::launch_layer_gram(la, cache->dtype, stream));
+      if (s != KVC_OK) return s;
+      s = hip_status(kvc::launch_layer_subspace(la, ea, stream));
+      if (s != KVC_OK) return s;
+      s = hip_status(kvc::launch_layer_proj(la, cache->dtype, st.num_tokens, stream));
+      if (s != KVC_OK) return s;
+    }
+  }
+  return KVC_OK;
 }
 
 kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
@@ -411,7 +571,13 @@ kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t
     max_rank = std::max(max_rank, st.rank);
     if (st.rank > 0) max_tokens = std::max(max_tokens, st.num_tokens);
   }
+  if (batch_is_per_layer(batch)) {
+    s = check_layer_fit(cache, batch);
+    if (s != KVC_OK) return s;
+  }
   if (batch->num_items == 0 || layer_end == layer_begin || max_rank == 0) return KVC_OK;
+  if (batch_is_per_layer(batch))
+    return fit_per_layer(cache, batch, layer_begin, layer_end, mode, workspace, workspace_bytes, stream);
   const FitPlan p = plan_fit(cache, batch, layer_begin, layer_end);
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < p.total)
     return KVC_ERR_WORKSPACE;

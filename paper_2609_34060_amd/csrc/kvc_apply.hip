@@ -59,9 +59,13 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
   const int src_off = itp->src_offset, dst_off = itp->dst_offset;
   const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)item_id * a.max_blocks : nullptr;
   const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)item_id * a.max_blocks : nullptr;
-  const int64_t unit = unit_index(layer, kv, head, H);
+  // a per-layer state shares the coefficient rows of a (layer, K/V) across heads; head h reads its d columns of the
+  // basis rows of H d features
+  const bool per_layer = itp->state.grouping == KVC_GROUP_LAYER;
+  const int64_t unit = per_layer ? (int64_t)layer * 2 + kv : unit_index(layer, kv, head, H);
+  const int bstride = per_layer ? H * D : D;
   const uint16_t* coef = static_cast<const uint16_t*>(itp->state.coef) + unit * (int64_t)Tdecl * r;
-  const float* basis = itp->state.basis + unit * (int64_t)r * D;
+  const float* basis = itp->state.basis + unit * (int64_t)r * bstride + (per_layer ? head * D : 0);
   const uint16_t* src_pool = static_cast<const uint16_t*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
   uint16_t* dst_pool = static_cast<uint16_t*>(const_cast<void*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]));
 
@@ -91,10 +95,10 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
     // Stage B^T as bf16 hi/lo, zero-padded to KP ranks: s[f * KP + k] = split(B[k][f]).
     for (int e = threadIdx.x; e < D * KP; e += kApplyThreads) {
       const int k = e / D, f = e - k * D;
-      float x = k < r ? basis[k * D + f] : 0.0f;
+      float x = k < r ? basis[k * bstride + f] : 0.0f;
       if (rope && k < r) {  // B R(pd)^T: each basis row rotated like a key row at position pd
         const int i = rope_pair(style, D, f);
-        x = rope_rotated(rope_first(style, D, f), x, basis[k * D + rope_partner(style, D, f)], s_rope[2][i],
+        x = rope_rotated(rope_first(style, D, f), x, basis[k * bstride + rope_partner(style, D, f)], s_rope[2][i],
                          s_rope[3][i]);
       }
       uint32_t hb, lb;
@@ -272,9 +276,11 @@ __global__ __launch_bounds__(kApplyThreads) void apply_f32_valu(ApplyArgs a) {
   const int Ts = r > 0 ? min(Tdecl, T) : 0;
   const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)item_id * a.max_blocks : nullptr;
   const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)item_id * a.max_blocks : nullptr;
-  const int64_t unit = unit_index(layer, kv, head, H);
+  const bool per_layer = itp->state.grouping == KVC_GROUP_LAYER;
+  const int64_t unit = per_layer ? (int64_t)layer * 2 + kv : unit_index(layer, kv, head, H);
+  const int bstride = per_layer ? H * D : D;
   const float* coef = static_cast<const float*>(itp->state.coef) + unit * (int64_t)Tdecl * r;
-  const float* basis = itp->state.basis + unit * (int64_t)r * D;
+  const float* basis = itp->state.basis + unit * (int64_t)r * bstride + (per_layer ? head * D : 0);
   const float* src_pool = static_cast<const float*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
   float* dst_pool = static_cast<float*>(const_cast<void*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]));
 
@@ -293,10 +299,11 @@ __global__ __launch_bounds__(kApplyThreads) void apply_f32_valu(ApplyArgs a) {
   const bool correct = t_begin < Ts;
   if (correct) {
     for (int e = threadIdx.x; e < r * D; e += kApplyThreads) {
-      float x = basis[e];
+      const int k = e / D, f = e - k * D;
+      float x = basis[k * bstride + f];
       if (rope) {
-        const int k = e / D, f = e - k * D, i = rope_pair(style, D, f);
-        x = rope_rotated(rope_first(style, D, f), x, basis[k * D + rope_partner(style, D, f)], s_rope[2][i],
+        const int i = rope_pair(style, D, f);
+        x = rope_rotated(rope_first(style, D, f), x, basis[k * bstride + rope_partner(style, D, f)], s_rope[2][i],
                          s_rope[3][i]);
       }
       s_b[e] = x;

@@ -208,4 +208,31 @@ __device__ __forceinline__ bf16x8 gram_fragment(const typename GramSeg<FT>::T* s
   return as_bf16x8(f);
 }
 
+// Row offsets of the 8 consecutive tokens t .. t + 7 of a block sequence (entries past t_end are -1); with a
+// power-of-two block size of at least 8 the 8 tokens touch at most two blocks, so two table reads suffice.
+__device__ __forceinline__ void row_offsets8(const PoolView& pv, const int32_t* __restrict__ table, int32_t off,
+                                             int t, int t_end, int head, int64_t* o) {
+  if (pv.block_shift >= 3) {
+    const int32_t p = off + t;
+    const int32_t lb0 = p >> pv.block_shift, lb1 = (p + 7) >> pv.block_shift;
+    // a table entry is read only if a token before t_end lies in its block (the host checked those are in range)
+    const int32_t b0 = t < t_end ? (table ? table[lb0] : lb0) : -1;
+    const int first_in_lb1 = (lb1 << pv.block_shift) - off;
+    const int32_t b1 = lb1 == lb0 ? b0 : (first_in_lb1 < t_end ? (table ? table[lb1] : lb1) : -1);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int32_t pj = p + j;
+      const int32_t lb = pj >> pv.block_shift;
+      const int32_t blk = lb == lb0 ? b0 : b1;
+      const bool ok = (t + j < t_end) && blk >= 0 && blk < pv.num_blocks;
+      o[j] = ok ? (int64_t)blk * pv.block_stride + (int64_t)(pj - (lb << pv.block_shift)) * pv.token_stride +
+                      (int64_t)head * pv.head_stride
+                : -1;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[j] = (t + j < t_end) ? row_offset(pv, table, off, t + j, head) : -1;
+  }
+}
+
 }  // namespace kvc

@@ -94,33 +94,6 @@ __device__ __forceinline__ void gram_all_stores(float* P, const f32x4* acc, int 
   (gram_store<D, Is, 0>(P, acc + Is, g, n), ...);
 }
 
-// Row offsets of the 8 consecutive tokens t .. t + 7 of a block sequence (entries past t_end are -1); with a
-// power-of-two block size of at least 8 the 8 tokens touch at most two blocks, so two table reads suffice.
-__device__ __forceinline__ void row_offsets8(const PoolView& pv, const int32_t* __restrict__ table, int32_t off,
-                                             int t, int t_end, int head, int64_t* o) {
-  if (pv.block_shift >= 3) {
-    const int32_t p = off + t;
-    const int32_t lb0 = p >> pv.block_shift, lb1 = (p + 7) >> pv.block_shift;
-    // a table entry is read only if a token before t_end lies in its block (the host checked those are in range)
-    const int32_t b0 = t < t_end ? (table ? table[lb0] : lb0) : -1;
-    const int first_in_lb1 = (lb1 << pv.block_shift) - off;
-    const int32_t b1 = lb1 == lb0 ? b0 : (first_in_lb1 < t_end ? (table ? table[lb1] : lb1) : -1);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int32_t pj = p + j;
-      const int32_t lb = pj >> pv.block_shift;
-      const int32_t blk = lb == lb0 ? b0 : b1;
-      const bool ok = (t + j < t_end) && blk >= 0 && blk < pv.num_blocks;
-      o[j] = ok ? (int64_t)blk * pv.block_stride + (int64_t)(pj - (lb << pv.block_shift)) * pv.token_stride +
-                      (int64_t)head * pv.head_stride
-                : -1;
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) o[j] = (t + j < t_end) ? row_offset(pv, table, off, t + j, head) : -1;
-  }
-}
-
 // bf16 Gram, one wave per partial: the wave streams its own token range 32 tokens at a time.  Lane (g, m) loads,
 // for tokens t0 + 8 g + j (j = 0..7), the 2 FT bytes of features FT m .. FT m + FT - 1 of the dst (and src) row:
 // sixteen lanes cover one row with one coalesced load.  Z = dst - src is split into bf16 hi/lo in registers and

@@ -43,6 +43,35 @@ hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hip
 hipError_t launch_fit_proj(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens, int max_rank,
                            hipStream_t stream);
 
+// Per-layer factorisation (kvc_layer.hip).  A layer unit u = (item * num_layers + layer - layer_begin) * 2 + kv
+// covers every KV head of one layer's K (or V) rows: Z is T x D with D = H d.
+struct LayerFitArgs {
+  PoolView pv;
+  LayerPtrs layers;
+  const kvc_item* items;       // device; each item's (per-layer) state receives the fit
+  const int32_t* src_tables;
+  const int32_t* dst_tables;
+  int32_t max_blocks;
+  int32_t layer_begin, num_layers;
+  int32_t mode;                // kvc_fit_mode
+  int32_t num_units;
+  int32_t k;                   // subspace columns (64 or 128)
+  int32_t rank;                // the items' rank (one rank per call group)
+  int32_t max_parts, part_tokens;
+  float* partials;             // [unit][max_parts][D][D]
+  double* gram;                // [unit][D][D]
+  double* x;                   // [unit][k][D] orthonormal columns (stored as rows)
+  double* y;                   // [unit][k][D]
+  double* hmat;                // [unit][k][k]
+  float* vrows;                // [unit][rank][k] eigenvectors of hmat (rows)
+  float* vsigma;               // [unit][rank]
+};
+constexpr int kLayerIters = 8;  // subspace iterations before the Rayleigh-Ritz step
+struct EigArgs;
+hipError_t launch_layer_gram(const LayerFitArgs& a, kvc_dtype dtype, hipStream_t stream);
+hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipStream_t stream);
+hipError_t launch_layer_proj(const LayerFitArgs& a, kvc_dtype dtype, int max_tokens, hipStream_t stream);
+
 // Top-r eigenpairs of per-unit Gram matrices (kvc_eig.hip).  Unit u enumerates (item, layer, K/V, head) with the
 // head fastest: u = ((item * num_layers + layer - layer_begin) * 2 + kv) * num_kv_heads + head.
 struct EigArgs {

@@ -1,0 +1,686 @@
+// Per-layer factorisation (Section 3.3 with the layer's whole KV feature dimension D = H d).  The K (or V) rows of one
+// layer, every KV head side by side, form one T x D matrix Z per (item, layer, K/V) "layer unit"; its rank-r
+// truncated SVD (Eq. 7) is reached through the Gram G = Z^T Z (D x D, D up to 1024):
+//   gram_pair    the d x d block Z_h1^T Z_h2 of a head pair (h1 <= h2) over one token range (bf16 hi/lo MFMA in the
+//                register layout of the per-head Gram; two waves split the block's tiles), written with its mirror
+//                into the unit's partial.  float32 caches: 64 x 64 blocks on VALU.
+//   gram_reduce  the partials of a unit summed in a fixed order in fp64.
+//   subspace     k = 64 or 128 columns: X <- orth(G X) (fp64 GEMM, two passes of modified Gram-Schmidt), then the
+//                Rayleigh-Ritz matrix X^T G X goes to the per-head eigensolver as a dense k x k input; its top r
+//                eigenvectors V give the basis rows (X V^T)^T and sigma = sqrt(Ritz value).  The top-r subspace
+//                converges like (lambda_{k+1} / lambda_r)^iterations.
+//   proj_layer   coef = Z B^T summed over the heads (bf16 MFMA; each head's d columns of B staged hi/lo in LDS).
+#include <algorithm>
+
+#include "kvc_device.h"
+#include "kvc_launch.h"
+
+namespace kvc {
+
+constexpr int kLayerThreads = 256;
+constexpr int kLayerWaves = kLayerThreads / kWave;
+
+struct LayerUnit {
+  int item, lrel, layer, kv;
+};
+__device__ __forceinline__ LayerUnit layer_unit(const LayerFitArgs& a, int u) {
+  LayerUnit lu;
+  lu.item = u / (a.num_layers * 2);
+  const int rem = u - lu.item * a.num_layers * 2;
+  lu.lrel = rem >> 1;
+  lu.kv = rem & 1;
+  lu.layer = a.layer_begin + lu.lrel;
+  return lu;
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Gram of head pairs, bf16
+// ---------------------------------------------------------------------------------------------------------------
+
+// Z = dst - src of 8 tokens' segments as bf16 hi/lo (the difference of two bf16 values is exact in fp32).
+template <int FT>
+__device__ __forceinline__ void pair_form_z(const typename GramSeg<FT>::T* rd, const typename GramSeg<FT>::T* rs,
+                                            typename GramSeg<FT>::T* zh, typename GramSeg<FT>::T* zl) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+#pragma unroll
+    for (int w = 0; w < FT / 2; ++w) {
+      const uint32_t dw = seg_dword<FT>(rd[j], w), sw = seg_dword<FT>(rs[j], w);
+      uint32_t h, l;
+      split_bf16x2(bf16_lo_to_f32(dw) - bf16_lo_to_f32(sw), bf16_hi_to_f32(dw) - bf16_hi_to_f32(sw), h, l);
+      if constexpr (FT == 8) {
+        zh[j][w] = h;
+        zl[j][w] = l;
+      } else {
+        if (w == 0) {
+          zh[j].x = h;
+          zl[j].x = l;
+        } else {
+          zh[j].y = h;
+          zl[j].y = l;
+        }
+      }
+    }
+  }
+}
+
+// Tile IDX of half HALF: rows fi = HALF FT/2 + IDX / FT of head 1, columns fj = IDX % FT of head 2.
+template <int D, int HALF, int IDX>
+__device__ __forceinline__ void pair_tile(f32x4* acc, const typename GramSeg<D / 16>::T* ah_,
+                                          const typename GramSeg<D / 16>::T* al_,
+                                          const typename GramSeg<D / 16>::T* bh_,
+                                          const typename GramSeg<D / 16>::T* bl_) {
+  constexpr int FT = D / 16, fi = HALF * (FT / 2) + IDX / FT, fj = IDX % FT;
+  const bf16x8 ah = gram_fragment<FT, fi>(ah_), al = gram_fragment<FT, fi>(al_);
+  const bf16x8 bh = gram_fragment<FT, fj>(bh_), bl = gram_fragment<FT, fj>(bl_);
+  acc[IDX] = mfma16x16x32(al, bh, acc[IDX]);
+  acc[IDX] = mfma16x16x32(ah, bl, acc[IDX]);
+  acc[IDX] = mfma16x16x32(ah, bh, acc[IDX]);
+}
+template <int D, int HALF, int... Is>
+__device__ __forceinline__ void pair_tiles(f32x4* acc, const typename GramSeg<D / 16>::T* ah,
+                                           const typename GramSeg<D / 16>::T* al,
+                                           const typename GramSeg<D / 16>::T* bh,
+                                           const typename GramSeg<D / 16>::T* bl, std::integer_sequence<int, Is...>) {
+  (pair_tile<D, HALF, Is>(acc, ah, al, bh, bl), ...);
+}
+
+// One wave per (token range, half of the block's tiles); the two waves of a range read the same rows.
+template <int D>
+__global__ __launch_bounds__(kLayerThreads) void gram_pair_bf16(LayerFitArgs a) {
+  constexpr int FT = D / 16, NTW = FT * FT / 2, STEP = 32;
+  using Seg = typename GramSeg<FT>::T;
+  const int H = a.pv.num_kv_heads, DL = H * D;
+  const int u = blockIdx.z;
+  const LayerUnit lu = layer_unit(a, u);
+  const kvc_item* itp = a.items + lu.item;
+  const int r = itp->state.rank, Ts = itp->state.num_tokens;
+  int p = blockIdx.y, h1 = 0;
+  while (p >= H - h1) {
+    p -= H - h1;
+    ++h1;
+  }
+  const int h2 = h1 + p;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, g = lane >> 4, n = lane & 15;
+  const int part = blockIdx.x * (kLayerWaves / 2) + (wave >> 1), half = wave & 1;
+  const int t_begin = part * a.part_tokens;
+  if (r == 0 || t_begin >= Ts) return;  // per wave: no barrier in this kernel
+  const int t_end = min(Ts, t_begin + a.part_tokens);
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const uint16_t* pool = static_cast<const uint16_t*>(lu.kv ? a.layers.v[lu.lrel] : a.layers.k[lu.lrel]);
+  const bool delta = a.mode == KVC_FIT_DELTA;
+
+  f32x4 acc[NTW];
+#pragma unroll
+  for (int q = 0; q < NTW; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int t0 = t_begin; t0 < t_end; t0 += STEP) {
+    const int t = t0 + 8 * g;
+    Seg z1h[8], z1l[8], z2h[8], z2l[8];
+    {
+      int64_t od[8], os[8];
+      Seg rd[8], rs[8];
+      row_offsets8(a.pv, dst_tab, itp->dst_offset, t, t_end, h1, od);
+      if (delta) row_offsets8(a.pv, src_tab, itp->src_offset, t, t_end, h1, os);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        rd[j] = od[j] >= 0 ? *reinterpret_cast<const Seg*>(pool + od[j] + FT * n) : Seg{};
+        rs[j] = (delta && os[j] >= 0) ? *reinterpret_cast<const Seg*>(pool + os[j] + FT * n) : Seg{};
+      }
+      pair_form_z<FT>(rd, rs, z1h, z1l);
+      row_offsets8(a.pv, dst_tab, itp->dst_offset, t, t_end, h2, od);
+      if (delta) row_offsets8(a.pv, src_tab, itp->src_offset, t, t_end, h2, os);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        rd[j] = od[j] >= 0 ? *reinterpret_cast<const Seg*>(pool + od[j] + FT * n) : Seg{};
+        rs[j] = (delta && os[j] >= 0) ? *reinterpret_cast<const Seg*>(pool + os[j] + FT * n) : Seg{};
+      }
+      pair_form_z<FT>(rd, rs, z2h, z2l);
+    }
+    if (half == 0) pair_tiles<D, 0>(acc, z1h, z1l, z2h, z2l, std::make_integer_sequence<int, NTW>{});
+    else pair_tiles<D, 1>(acc, z1h, z1l, z2h, z2l, std::make_integer_sequence<int, NTW>{});
+  }
+  float* P = a.partials + ((size_t)u * a.max_parts + part) * DL * DL;
+#pragma unroll
+  for (int q = 0; q < NTW; ++q) {
+    const int fi = half * (FT / 2) + q / FT, fj = q % FT;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = h1 * D + FT * (4 * g + i) + fi, col = h2 * D + FT * n + fj;
+      P[(size_t)row * DL + col] = acc[q][i];
+      if (h1 != h2) P[(size_t)col * DL + row] = acc[q][i];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Gram, float32 caches: one 64 x 64 block of G over one token range per workgroup (VALU, 4 x 4 outputs per thread)
+// ---------------------------------------------------------------------------------------------------------------
+
+constexpr int kF32Block = 64, kF32Step = 16;
+
+template <int D>
+__global__ __launch_bounds__(kLayerThreads) void gram_block_f32(LayerFitArgs a) {
+  __shared__ float s_a[kF32Step][kF32Block + 1], s_b[kF32Step][kF32Block + 1];
+  const int H = a.pv.num_kv_heads, DL = H * D, nb = DL / kF32Block;
+  const int bi = blockIdx.x / nb, bj = blockIdx.x - bi * nb;
+  const int part = blockIdx.y, u = blockIdx.z;
+  const LayerUnit lu = layer_unit(a, u);
+  const kvc_item* itp = a.items + lu.item;
+  const int r = itp->state.rank, Ts = itp->state.num_tokens;
+  const int t_begin = part * a.part_tokens;
+  if (r == 0 || t_begin >= Ts) return;  // whole workgroup
+  const int t_end = min(Ts, t_begin + a.part_tokens);
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const float* pool = static_cast<const float*>(lu.kv ? a.layers.v[lu.lrel] : a.layers.k[lu.lrel]);
+  const bool delta = a.mode == KVC_FIT_DELTA;
+  const int tid = threadIdx.x, ti = tid / 16, tj = tid % 16;
+  float acc[4][4] = {};
+  // every 64-feature block lies inside one head (64 divides d)
+  auto z_of = [&](int t, int F) {
+    const int h = F / D, f = F - h * D;
+    const int64_t od = row_offset(a.pv, dst_tab, itp->dst_offset, t, h);
+    float z = od >= 0 ? pool[od + f] : 0.0f;
+    if (delta) {
+      const int64_t os = row_offset(a.pv, src_tab, itp->src_offset, t, h);
+      if (os >= 0) z -= pool[os + f];
+    }
+    return z;
+  };
+  for (int t0 = t_begin; t0 < t_end; t0 += kF32Step) {
+    for (int e = tid; e < kF32Step * kF32Block; e += kLayerThreads) {
+      const int tk = e / kF32Block, c = e - tk * kF32Block, t = t0 + tk;
+      s_a[tk][c] = t < t_end ? z_of(t, bi * kF32Block + c) : 0.0f;
+      s_b[tk][c] = t < t_end ? z_of(t, bj * kF32Block + c) : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int tk = 0; tk < kF32Step; ++tk) {
+      float x[4], y[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        x[i] = s_a[tk][4 * ti + i];
+        y[i] = s_b[tk][4 * tj + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(x[i], y[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  float* P = a.partials + ((size_t)u * a.max_parts + part) * DL * DL;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      P[(size_t)(bi * kF32Block + 4 * ti + i) * DL + bj * kF32Block + 4 * tj + j] = acc[i][j];
+}
+
+// G = sum of the unit's partials in order, fp64.
+__global__ __launch_bounds__(kLayerThreads) void gram_reduce(LayerFitArgs a) {
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
+  const int u = blockIdx.y;
+  const size_t e = (size_t)blockIdx.x * kLayerThreads + threadIdx.x;
+  if (e >= (size_t)DL * DL) return;
+  const LayerUnit lu = layer_unit(a, u);
+  const int Ts = a.items[lu.item].state.num_tokens;
+  const int parts = min(a.max_parts, (Ts + a.part_tokens - 1) / a.part_tokens);
+  const float* P = a.partials + (size_t)u * a.max_parts * DL * DL + e;
+  double s = 0.0;
+  for (int p = 0; p < parts; ++p) s += (double)P[(size_t)p * DL * DL];
+  a.gram[(size_t)u * DL * DL + e] = s;
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Subspace iteration on G (fp64)
+// ---------------------------------------------------------------------------------------------------------------
+
+__device__ __forceinline__ double hash_uniform(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t h = a * 0x9E3779B1u ^ (b + 0x7F4A7C15u) * 0x85EBCA77u ^ (c + 0x165667B1u) * 0xC2B2AE3Du;
+  h ^= h >> 15;
+  h *= 0x2C1B3C6Du;
+  h ^= h >> 12;
+  h *= 0x297A2D39u;
+  h ^= h >> 15;
+  return (double)h * (2.0 / 4294967296.0) - 1.0;
+}
+
+// Starting columns: deterministic pseudo-random entries in [-1, 1).
+__global__ __launch_bounds__(kLayerThreads) void sub_init(LayerFitArgs a) {
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
+  const int u = blockIdx.y;
+  const int e = blockIdx.x * kLayerThreads + threadIdx.x;
+  if (e >= a.k * DL) return;
+  a.y[(size_t)u * a.k * DL + e] = hash_uniform((uint32_t)u, (uint32_t)(e / DL), (uint32_t)(e % DL));
+}
+
+// Y = G X for every unit: a 64 x 64 tile (features x columns) per workgroup, 4 x 4 outputs per thread.
+__global__ __launch_bounds__(kLayerThreads) void sub_gemm(LayerFitArgs a) {
+  constexpr int TB = 64, KB = 16;
+  __shared__ double s_g[TB][KB + 1], s_x[KB][TB + 1];
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
+  const int f0 = blockIdx.x * TB, c0 = blockIdx.y * TB, u = blockIdx.z;
+  const double* G = a.gram + (size_t)u * DL * DL;
+  const double* X = a.x + (size_t)u * a.k * DL;
+  double* Y = a.y + (size_t)u * a.k * DL;
+  const int tid = threadIdx.x, ti = tid / 16, tj = tid % 16;
+  double acc[4][4] = {};
+  for (int k0 = 0; k0 < DL; k0 += KB) {
+    for (int e = tid; e < TB * KB; e += kLayerThreads) {
+      const int i = e / KB, kk = e - i * KB;
+      s_g[i][kk] = G[(size_t)(f0 + i) * DL + k0 + kk];
+      const int c = e / KB, k2 = e - c * KB;
+      s_x[k2][c] = X[(size_t)(c0 + c) * DL + k0 + k2];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < KB; ++kk) {
+      double g4[4], x4[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        g4[i] = s_g[4 * ti + i][kk];
+        x4[i] = s_x[kk][4 * tj + i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fma(g4[i], x4[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) Y[(size_t)(c0 + 4 * tj + j) * DL + f0 + 4 * ti + i] = acc[i][j];
+}
+
+// Whole-workgroup sum (fixed order: waves in order), result in every thread.
+template <int NW>
+__device__ __forceinline__ double block_sum(double v, double* s_red) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);
+  const int wave = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) s_red[wave] = v;
+  __syncthreads();
+  double s = 0.0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) s += s_red[w];
+  return s;
+}
+
+// X = orthonormal columns spanning Y (two passes of modified Gram-Schmidt), one 1024-thread workgroup per unit.  A
+// column that vanishes against the earlier ones (rank of G below k) is replaced by a pseudo-random one in the first
+// pass; the second pass orthogonalises it.
+constexpr int kMgsThreads = 1024;
+__global__ __launch_bounds__(kMgsThreads) void sub_orth(LayerFitArgs a, uint32_t round) {
+  __shared__ double s_red[kMgsThreads / kWave];
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, k = a.k;
+  const int u = blockIdx.x;
+  const double* Y = a.y + (size_t)u * k * DL;
+  double* X = a.x + (size_t)u * k * DL;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int e = tid; e < k * DL; e += kMgsThreads) X[e] = Y[e];
+  __syncthreads();
+  double scale_ref = 0.0;
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int i = 0; i < k; ++i) {
+      double* xi = X + (size_t)i * DL;
+      double s = 0.0;
+      for (int f = tid; f < DL; f += kMgsThreads) s += xi[f] * xi[f];
+      const double nrm = sqrt(block_sum<kMgsThreads / kWave>(s, s_red));
+      if (pass == 0 && i == 0) scale_ref = nrm;
+      if (pass == 0 && !(nrm > 1e-13 * scale_ref)) {
+        // numerically inside the span of the earlier columns: a fresh direction
+        for (int f = tid; f < DL; f += kMgsThreads) xi[f] = hash_uniform(0xA5A5u + round, (uint32_t)(u * k + i), f);
+        __syncthreads();
+        double s2 = 0.0;
+        for (int f = tid; f < DL; f += kMgsThreads) s2 += xi[f] * xi[f];
+        const double n2 = sqrt(block_sum<kMgsThreads / kWave>(s2, s_red));
+        for (int f = tid; f < DL; f += kMgsThreads) xi[f] /= n2;
+      } else {
+        const double inv = nrm > 0.0 ? 1.0 / nrm : 0.0;
+        for (int f = tid; f < DL; f += kMgsThreads) xi[f] *= inv;
+      }
+      __syncthreads();
+      // remove column i from the later columns, one wave per column
+      for (int j = i + 1 + wave; j < k; j += kMgsThreads / kWave) {
+        double* xj = X + (size_t)j * DL;
+        double dp = 0.0;
+        for (int f = lane; f < DL; f += kWave) dp += xi[f] * xj[f];
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) dp += __shfl_xor(dp, o, kWave);
+        for (int f = lane; f < DL; f += kWave) xj[f] -= dp * xi[f];
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Rayleigh-Ritz matrix H = X^T Y (Y = G X), symmetrised, one workgroup per unit.
+__global__ __launch_bounds__(kLayerThreads) void sub_rayleigh(LayerFitArgs a) {
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, k = a.k;
+  const int u = blockIdx.x;
+  const double* X = a.x + (size_t)u * k * DL;
+  const double* Y = a.y + (size_t)u * k * DL;
+  double* Hm = a.hmat + (size_t)u * k * k;
+  for (int e = threadIdx.x; e < k * k; e += kLayerThreads) {
+    const int i = e / k, j = e - i * k;
+    if (j < i) continue;
+    double s1 = 0.0, s2 = 0.0;
+    for (int f = 0; f < DL; ++f) {
+      s1 = fma(X[(size_t)i * DL + f], Y[(size_t)j * DL + f], s1);
+      s2 = fma(X[(size_t)j * DL + f], Y[(size_t)i * DL + f], s2);
+    }
+    const double h = 0.5 * (s1 + s2);
+    Hm[i * k + j] = h;
+    Hm[j * k + i] = h;
+  }
+}
+
+// Basis row j of unit u = (X^T v_j)^T with v_j the j-th Ritz vector, canonical sign (largest-magnitude entry
+// positive, the first of the entries within 2^-20 of it), written with sigma to the item's per-layer state.
+__global__ __launch_bounds__(kLayerThreads) void sub_basis(LayerFitArgs a) {
+  __shared__ double s_red[kLayerWaves];
+  __shared__ float s_v[128];
+  const int D = a.pv.head_dim, DL = a.pv.num_kv_heads * D, k = a.k;
+  const int j = blockIdx.x, u = blockIdx.y;
+  const LayerUnit lu = layer_unit(a, u);
+  const kvc_state& st = a.items[lu.item].state;
+  const int r = st.rank;
+  if (j >= r) return;  // whole workgroup
+  const float* v = a.vrows + ((size_t)u * a.rank + j) * k;
+  const double* X = a.x + (size_t)u * k * DL;
+  for (int c = threadIdx.x; c < k; c += kLayerThreads) s_v[c] = v[c];
+  __syncthreads();
+  constexpr int MAXF = 1024 / kLayerThreads;
+  double b[MAXF];
+  double mx = 0.0;
+#pragma unroll
+  for (int q = 0; q < MAXF; ++q) {
+    const int f = threadIdx.x + q * kLayerThreads;
+    b[q] = 0.0;
+    if (f < DL) {
+      double s = 0.0;
+      for (int c = 0; c < k; ++c) s = fma((double)s_v[c], X[(size_t)c * DL + f], s);
+      b[q] = s;
+      mx = fmax(mx, fabs(s));
+    }
+  }
+  // largest magnitude over the row, then the first index within 2^-20 of it
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, kWave));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  for (int w = 0; w < kLayerWaves; ++w) mx = fmax(mx, s_red[w]);
+  const double thr = mx * (1.0 - 0.00000095367431640625);  // 2^-20
+  int first = DL;
+#pragma unroll
+  for (int q = 0; q < MAXF; ++q) {
+    const int f = threadIdx.x + q * kLayerThreads;
+    if (f < DL && fabs(b[q]) >= thr) first = min(first, f);
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) first = min(first, __shfl_xor(first, o, kWave));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = (double)first;
+  __syncthreads();
+  for (int w = 0; w < kLayerWaves; ++w) first = min(first, (int)s_red[w]);
+  // the sign of entry `first`, read from the thread that holds it
+  __shared__ double s_sign;
+#pragma unroll
+  for (int q = 0; q < MAXF; ++q)
+    if (threadIdx.x + q * kLayerThreads == first) s_sign = b[q] < 0.0 ? -1.0 : 1.0;
+  __syncthreads();
+  const double sg = s_sign;
+  const int64_t lunit = (int64_t)lu.layer * 2 + lu.kv;
+  float* brow = st.basis + (lunit * r + j) * DL;
+#pragma unroll
+  for (int q = 0; q < MAXF; ++q) {
+    const int f = threadIdx.x + q * kLayerThreads;
+    if (f < DL) brow[f] = (float)(sg * b[q]);
+  }
+  if (threadIdx.x == 0 && st.sigma) st.sigma[lunit * r + j] = a.vsigma[(size_t)u * a.rank + j];
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Projection coef = Z B^T over the heads
+// ---------------------------------------------------------------------------------------------------------------
+
+constexpr int kPLTiles = 4;                               // 16-token tiles per wave
+constexpr int kPLChunk = kLayerWaves * kPLTiles * 16;     // 256 tokens per workgroup
+
+// bf16: per head h the d columns of B (rank rows padded to RP = 16 MTR) are staged hi/lo in LDS (two buffers), the
+// rows of h are read in MFMA B-operand layout and Z split hi/lo; the coefficient tiles accumulate over the heads.
+template <int D, int MTR>
+__global__ __launch_bounds__(kLayerThreads) void proj_layer_bf16(LayerFitArgs a) {
+  constexpr int KS = D / 32, RP = MTR * 16;
+  extern __shared__ __attribute__((aligned(16))) unsigned char layer_lds[];
+  uint16_t* s_b = reinterpret_cast<uint16_t*>(layer_lds);  // [2][hi, lo][RP][D]
+  const int H = a.pv.num_kv_heads, DL = H * D;
+  const int u = blockIdx.y;
+  const LayerUnit lu = layer_unit(a, u);
+  const kvc_item* itp = a.items + lu.item;
+  const kvc_state& st = itp->state;
+  const int r = st.rank, Ts = st.num_tokens;
+  const int t_begin = blockIdx.x * kPLChunk;
+  if (r == 0 || t_begin >= Ts) return;  // whole workgroup
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const uint16_t* pool = static_cast<const uint16_t*>(lu.kv ? a.layers.v[lu.lrel] : a.layers.k[lu.lrel]);
+  const bool delta = a.mode == KVC_FIT_DELTA;
+  const int64_t lunit = (int64_t)lu.layer * 2 + lu.kv;
+  const float* basis = st.basis + lunit * r * DL;
+  uint16_t* coef = static_cast<uint16_t*>(st.coef) + lunit * (int64_t)Ts * r;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, n = lane & 15;
+
+  f32x4 acc[kPLTiles][MTR];
+#pragma unroll
+  for (int j = 0; j < kPLTiles; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MTR; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int h = 0; h < H; ++h) {
+    uint16_t* s_hi = s_b + (h & 1) * 2 * RP * D;
+    uint16_t* s_lo = s_hi + RP * D;
+    for (int e = tid; e < RP * D; e += kLayerThreads) {
+      const int kk = e / D, f = e - kk * D;
+      const float x = kk < r ? basis[(int64_t)kk * DL + h * D + f] : 0.f;
+      uint32_t hb, lb;
+      split_bf16(x, hb, lb);
+      s_hi[e] = (uint16_t)hb;
+      s_lo[e] = (uint16_t)lb;
+    }
+    __syncthreads();  // head h's columns are staged; the other buffer (head h - 1) is still read until here
+#pragma unroll
+    for (int j = 0; j < kPLTiles; ++j) {
+      const int t0 = t_begin + (j * kLayerWaves + wave) * 16;
+      if (t0 >= Ts) continue;  // uniform over the wave
+      const int t = t0 + n;
+      const bool valid = t < Ts;
+      const int64_t od = valid ? row_offset(a.pv, dst_tab, itp->dst_offset, t, h) : -1;
+      const int64_t os = (valid && delta) ? row_offset(a.pv, src_tab, itp->src_offset, t, h) : -1;
+      bf16x8 zh[KS], zl[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 d = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+        const u32x4 s = os >= 0 ? *reinterpret_cast<const u32x4*>(pool + os + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+        u32x4 hw, lw;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          uint32_t hh, ll;
+          split_bf16x2(bf16_lo_to_f32(d[w]) - bf16_lo_to_f32(s[w]), bf16_hi_to_f32(d[w]) - bf16_hi_to_f32(s[w]), hh,
+                       ll);
+          hw[w] = hh;
+          lw[w] = ll;
+        }
+        zh[ks] = as_bf16x8(hw);
+        zl[ks] = as_bf16x8(lw);
+      }
+#pragma unroll
+      for (int mt = 0; mt < MTR; ++mt) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const int o = (16 * mt + n) * D + 32 * ks + 8 * g;
+          const bf16x8 fh = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[o]));
+          const bf16x8 fl = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[o]));
+          acc[j][mt] = mfma16x16x32(fl, zh[ks], acc[j][mt]);
+          acc[j][mt] = mfma16x16x32(fh, zl[ks], acc[j][mt]);
+          acc[j][mt] = mfma16x16x32(fh, zh[ks], acc[j][mt]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kPLTiles; ++j) {
+    const int t = t_begin + (j * kLayerWaves + wave) * 16 + n;
+    if (t >= Ts) continue;
+#pragma unroll
+    for (int mt = 0; mt < MTR; ++mt) {
+      // lane holds coef[t][16 mt + 4 g + i], i = 0..3
+      const int k0 = 16 * mt + 4 * g;
+      uint16_t* cp = coef + (int64_t)t * r + k0;
+      if ((r & 3) == 0 && k0 + 4 <= r) {
+        uint2 w;
+        w.x = pack_bf16x2(acc[j][mt][0], acc[j][mt][1]);
+        w.y = pack_bf16x2(acc[j][mt][2], acc[j][mt][3]);
+        *reinterpret_cast<uint2*>(cp) = w;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (k0 + i < r) cp[i] = (uint16_t)f32_to_bf16_bits(acc[j][mt][i]);
+      }
+    }
+  }
+}
+
+// float32: one thread per (token, rank), fp32 FMAs over the D = H d features; the basis [r][D] is in LDS.
+template <int D>
+__global__ __launch_bounds__(kLayerThreads) void proj_layer_f32(LayerFitArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char layer_lds[];
+  float* s_b = reinterpret_cast<float*>(layer_lds);
+  const int H = a.pv.num_kv_heads, DL = H * D;
+  const int u = blockIdx.y;
+  const LayerUnit lu = layer_unit(a, u);
+  const kvc_item* itp = a.items + lu.item;
+  const kvc_state& st = itp->state;
+  const int r = st.rank, Ts = st.num_tokens;
+  const int t_begin = blockIdx.x * kPLChunk;
+  if (r == 0 || t_begin >= Ts) return;
+  const int t_end = min(Ts, t_begin + kPLChunk);
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const float* pool = static_cast<const float*>(lu.kv ? a.layers.v[lu.lrel] : a.layers.k[lu.lrel]);
+  const bool delta = a.mode == KVC_FIT_DELTA;
+  const int64_t lunit = (int64_t)lu.layer * 2 + lu.kv;
+  const float* basis = st.basis + lunit * r * DL;
+  float* coef = static_cast<float*>(st.coef) + lunit * (int64_t)Ts * r;
+  for (int e = threadIdx.x; e < r * DL; e += kLayerThreads) s_b[e] = basis[e];
+  __syncthreads();
+  const int64_t total = (int64_t)(t_end - t_begin) * r;
+  for (int64_t e = threadIdx.x; e < total; e += kLayerThreads) {
+    const int t = t_begin + (int)(e / r), kk = (int)(e % r);
+    float s = 0.f;
+    for (int h = 0; h < H; ++h) {
+      const int64_t od = row_offset(a.pv, dst_tab, itp->dst_offset, t, h);
+      const int64_t os = delta ? row_offset(a.pv, src_tab, itp->src_offset, t, h) : -1;
+      for (int f = 0; f < D; ++f) {
+        float z = od >= 0 ? pool[od + f] : 0.f;
+        if (os >= 0) z -= pool[os + f];
+        s = fmaf(z, s_b[kk * DL + h * D + f], s);
+      }
+    }
+    coef[(int64_t)t * r + kk] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
+// Launchers
+// ---------------------------------------------------------------------------------------------------------------
+
+hipError_t launch_layer_gram(const LayerFitArgs& a, kvc_dtype dtype, hipStream_t stream) {
+  const int D = a.pv.head_dim, H = a.pv.num_kv_heads, DL = H * D;
+  if (dtype == KVC_BF16) {
+    dim3 grid((a.max_parts + kLayerWaves / 2 - 1) / (kLayerWaves / 2), H * (H + 1) / 2, a.num_units);
+    if (D == 64) hipLaunchKernelGGL(gram_pair_bf16<64>, grid, dim3(kLayerThreads), 0, stream, a);
+    else hipLaunchKernelGGL(gram_pair_bf16<128>, grid, dim3(kLayerThreads), 0, stream, a);
+  } else {
+    const int nb = DL / kF32Block;
+    dim3 grid(nb * nb, a.max_parts, a.num_units);
+    if (D == 64) hipLaunchKernelGGL(gram_block_f32<64>, grid, dim3(kLayerThreads), 0, stream, a);
+    else hipLaunchKernelGGL(gram_block_f32<128>, grid, dim3(kLayerThreads), 0, stream, a);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 rgrid((unsigned)(((size_t)DL * DL + kLayerThreads - 1) / kLayerThreads), a.num_units);
+  hipLaunchKernelGGL(gram_reduce, rgrid, dim3(kLayerThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipStream_t stream) {
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
+  hipLaunchKernelGGL(sub_init, dim3((a.k * DL + kLayerThreads - 1) / kLayerThreads, a.num_units),
+                     dim3(kLayerThreads), 0, stream, a);
+  hipLaunchKernelGGL(sub_orth, dim3(a.num_units), dim3(kMgsThreads), 0, stream, a, 0u);
+  const dim3 ggrid(DL / 64, a.k / 64, a.num_units);
+  for (int it = 0; it < kLayerIters; ++it) {
+    hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
+    hipLaunchKernelGGL(sub_orth, dim3(a.num_units), dim3(kMgsThreads), 0, stream, a, (uint32_t)(it + 1));
+  }
+  hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
+  hipLaunchKernelGGL(sub_rayleigh, dim3(a.num_units), dim3(kLayerThreads), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if ((e = launch_eig(ea, stream)) != hipSuccess) return e;
+  hipLaunchKernelGGL(sub_basis, dim3(a.rank, a.num_units), dim3(kLayerThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+size_t layer_proj_lds_bytes(int D, int H, int rank, kvc_dtype dtype) {
+  if (dtype == KVC_BF16) return (size_t)2 * 2 * ((rank + 15) / 16 * 16) * D * sizeof(uint16_t);
+  return (size_t)rank * H * D * sizeof(float);
+}
+
+template <int D>
+static hipError_t launch_proj_layer_bf16(const LayerFitArgs& a, dim3 grid, size_t lds, hipStream_t stream) {
+  const int mtr = (a.rank + 15) / 16;
+  const void* fn;
+  switch (mtr <= 1 ? 1 : mtr <= 2 ? 2 : mtr <= 4 ? 4 : 8) {
+    case 1: fn = (const void*)proj_layer_bf16<D, 1>; break;
+    case 2: fn = (const void*)proj_layer_bf16<D, 2>; break;
+    case 4: fn = (const void*)proj_layer_bf16<D, 4>; break;
+    default: fn = (const void*)proj_layer_bf16<D, 8>; break;
+  }
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  switch (mtr <= 1 ? 1 : mtr <= 2 ? 2 : mtr <= 4 ? 4 : 8) {
+    case 1: hipLaunchKernelGGL((proj_layer_bf16<D, 1>), grid, dim3(kLayerThreads), lds, stream, a); break;
+    case 2: hipLaunchKernelGGL((proj_layer_bf16<D, 2>), grid, dim3(kLayerThreads), lds, stream, a); break;
+    case 4: hipLaunchKernelGGL((proj_layer_bf16<D, 4>), grid, dim3(kLayerThreads), lds, stream, a); break;
+    default: hipLaunchKernelGGL((proj_layer_bf16<D, 8>), grid, dim3(kLayerThreads), lds, stream, a); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_proj(const LayerFitArgs& a, kvc_dtype dtype, int max_tokens, hipStream_t stream) {
+  const int D = a.pv.head_dim, H = a.pv.num_kv_heads;
+  dim3 grid((max_tokens + kPLChunk - 1) / kPLChunk, a.num_units);
+  // the bf16 kernel stages RP = 16 MTR rank rows (MTR in 1, 2, 4, 8) of one head, hi and lo, in two buffers
+  const int mtr = (a.rank + 15) / 16, mtr_inst = mtr <= 1 ? 1 : mtr <= 2 ? 2 : mtr <= 4 ? 4 : 8;
+  const size_t lds = (size_t)2 * 2 * 16 * mtr_inst * D * sizeof(uint16_t);
+  if (dtype == KVC_BF16)
+    return D == 64 ? launch_proj_layer_bf16<64>(a, grid, lds, stream) : launch_proj_layer_bf16<128>(a, grid, lds, stream);
+  const size_t flds = layer_proj_lds_bytes(D, H, a.rank, dtype);
+  const void* fn = D == 64 ? (const void*)proj_layer_f32<64> : (const void*)proj_layer_f32<128>;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)flds);
+  if (e != hipSuccess) return e;
+  if (D == 64) hipLaunchKernelGGL(proj_layer_f32<64>, grid, dim3(kLayerThreads), flds, stream, a);
+  else hipLaunchKernelGGL(proj_layer_f32<128>, grid, dim3(kLayerThreads), flds, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace kvc

@@ -20,10 +20,12 @@ KVC_ERR_ALIAS, KVC_ERR_WORKSPACE, KVC_ERR_UNSUPPORTED, KVC_ERR_HIP = 5, 6, 7, 8
 KVC_F32, KVC_BF16 = 0, 1
 KVC_FIT_DELTA, KVC_FIT_BASE = 0, 1
 KVC_ROPE_NONE, KVC_ROPE_HALF, KVC_ROPE_PAIRS = 0, 1, 2
+KVC_GROUP_HEAD, KVC_GROUP_LAYER = 0, 1
 KVC_MAX_RANK = 128
 KVC_MAX_ANCHORS = 16
 
-EXPORTED = ["kvc_version", "kvc_status_str", "kvc_last_hip_error", "kvc_state_bytes", "kvc_dense_bytes",
+EXPORTED = ["kvc_version", "kvc_status_str", "kvc_last_hip_error", "kvc_state_bytes", "kvc_layer_state_bytes",
+            "kvc_dense_bytes",
             "kvc_apply", "kvc_fit_workspace_bytes", "kvc_fit_state", "kvc_chain_workspace_bytes", "kvc_chain",
             "kvc_anchor_weights", "kvc_apply_anchored", "kvc_gate_workspace_bytes", "kvc_gate_distances",
             "kvc_gate_decide", "kvc_pool_create", "kvc_pool_destroy", "kvc_pool_insert", "kvc_pool_record_use",
@@ -48,6 +50,7 @@ class kvc_cache(ctypes.Structure):
 class kvc_state(ctypes.Structure):
     _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("num_tokens", ctypes.c_int32), ("rank", ctypes.c_int32), ("coef_dtype", ctypes.c_int),
+                ("grouping", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("coef", ctypes.c_void_p), ("basis", ctypes.c_void_p), ("sigma", ctypes.c_void_p)]
 
 
@@ -86,6 +89,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.kvc_last_hip_error.restype = i32
     lib.kvc_state_bytes.restype = sz
     lib.kvc_state_bytes.argtypes = [i32, i32, i32, i32, i32, ctypes.c_int]
+    lib.kvc_layer_state_bytes.restype = sz
+    lib.kvc_layer_state_bytes.argtypes = [i32, i32, i32, i32, i32, ctypes.c_int]
     lib.kvc_dense_bytes.restype = sz
     lib.kvc_dense_bytes.argtypes = [i32, i32, i32, i32, ctypes.c_int]
     lib.kvc_apply.restype = ctypes.c_int
@@ -186,13 +191,22 @@ class Cache:
 
 
 class State:
-    """Low-rank state tensors: coef [L, 2, H, T, r], basis [L, 2, H, r, d] float32, sigma [L, 2, H, r] float32."""
+    """Low-rank state tensors.  Per KV head: coef [L, 2, H, T, r], basis [L, 2, H, r, d] float32, sigma [L, 2, H, r].
+    Per layer (KVC_GROUP_LAYER, recognised by a 4-d coef): coef [L, 2, T, r], basis [L, 2, r, H, d] float32 (a row
+    of H d features), sigma [L, 2, r]."""
 
     def __init__(self, coef: torch.Tensor, basis: torch.Tensor, sigma: Optional[torch.Tensor] = None):
         self.coef, self.basis, self.sigma = coef, basis, sigma
-        L, two, H, T, r = coef.shape
-        assert two == 2 and basis.shape[:4] == (L, 2, H, r)
-        self.s = kvc_state(L, H, basis.shape[-1], T, r, _dtype_code(coef.dtype),
+        if coef.dim() == 4:
+            L, two, T, r = coef.shape
+            assert two == 2 and basis.dim() == 5 and basis.shape[:3] == (L, 2, r)
+            H, d, grouping = basis.shape[3], basis.shape[4], KVC_GROUP_LAYER
+        else:
+            L, two, H, T, r = coef.shape
+            assert two == 2 and basis.shape[:4] == (L, 2, H, r)
+            d, grouping = basis.shape[-1], KVC_GROUP_HEAD
+        self.grouping = grouping
+        self.s = kvc_state(L, H, d, T, r, _dtype_code(coef.dtype), grouping, 0,
                            coef.data_ptr() if coef.numel() else None,
                            basis.data_ptr() if basis.numel() else None,
                            sigma.data_ptr() if (sigma is not None and sigma.numel()) else None)
@@ -202,6 +216,13 @@ class State:
         return State(torch.zeros(L, 2, H, T, rank, dtype=coef_dtype, device=device),
                      torch.zeros(L, 2, H, rank, d, dtype=torch.float32, device=device),
                      torch.zeros(L, 2, H, rank, dtype=torch.float32, device=device))
+
+    @staticmethod
+    def empty_layer(L: int, H: int, d: int, T: int, rank: int, coef_dtype: torch.dtype, device) -> "State":
+        """A per-layer state (one factorisation of each layer's K or V rows, D = H d)."""
+        return State(torch.zeros(L, 2, T, rank, dtype=coef_dtype, device=device),
+                     torch.zeros(L, 2, rank, H, d, dtype=torch.float32, device=device),
+                     torch.zeros(L, 2, rank, dtype=torch.float32, device=device))
 
     @property
     def num_tokens(self) -> int:
@@ -259,6 +280,10 @@ def kvc_version() -> int:
 
 def kvc_state_bytes(L: int, H: int, d: int, T: int, rank: int, coef_dtype: int) -> int:
     return load().kvc_state_bytes(L, H, d, T, rank, coef_dtype)
+
+
+def kvc_layer_state_bytes(L: int, H: int, d: int, T: int, rank: int, coef_dtype: int) -> int:
+    return load().kvc_layer_state_bytes(L, H, d, T, rank, coef_dtype)
 
 
 def kvc_dense_bytes(L: int, H: int, d: int, T: int, dtype: int) -> int:

@@ -57,8 +57,8 @@ class Fixture:
             self.items[i].num_tokens = T
             self.items[i].src_offset = 0
             self.items[i].dst_offset = 512
-            self.items[i].state = kvc.kvc_state(L, H, d, T, rank, kvc.KVC_BF16, FAKE + 0x4000000, FAKE + 0x8000000,
-                                                None)
+            self.items[i].state = kvc.kvc_state(L, H, d, T, rank, kvc.KVC_BF16, kvc.KVC_GROUP_HEAD, 0,
+                                                FAKE + 0x4000000, FAKE + 0x8000000, None)
         self.batch = kvc.kvc_batch(n, 0, ctypes.cast(self.items, ctypes.POINTER(kvc.kvc_item)), FAKE + 0xC000000,
                                    None, None)
 
@@ -210,7 +210,8 @@ class AnchorFixture(Fixture):
     def __init__(self, V=3, Ts=80, **kw):
         super().__init__(**kw)
         L, H, d = self.cache.num_layers, self.cache.num_kv_heads, self.cache.head_dim
-        self.states = (kvc.kvc_state * V)(*[kvc.kvc_state(L, H, d, 100, 16, kvc.KVC_BF16, FAKE + 0x10000000 * (v + 1),
+        self.states = (kvc.kvc_state * V)(*[kvc.kvc_state(L, H, d, 100, 16, kvc.KVC_BF16, kvc.KVC_GROUP_HEAD, 0,
+                                                          FAKE + 0x10000000 * (v + 1),
                                                           FAKE + 0x10000000 * (v + 1) + 0x8000000, None)
                                             for v in range(V)])
         self.anchors = kvc.kvc_anchors(V, Ts, ctypes.cast(self.states, ctypes.POINTER(kvc.kvc_state)), FAKE + 0x300000)
