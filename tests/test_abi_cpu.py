@@ -39,6 +39,8 @@ def test_memory_accounting_matches_oracle_and_paper_example():
                                     (28, 4, 128, 3328, 0, kvc.KVC_BF16, 2)]:
         assert kvc.kvc_state_bytes(L, H, d, T, r, dt) == O.lowrank_state_bytes(L, H, d, T, r, eb)
         assert kvc.kvc_dense_bytes(L, H, d, T, dt) == O.dense_segment_bytes(L, H, d, T, eb)
+    # per-layer state: per (layer, K/V) T r coefficients, r H d basis floats and r sigmas
+    assert kvc.kvc_layer_state_bytes(32, 8, 128, 4096, 32, kvc.KVC_BF16) == 64 * (4096 * 32 * 2 + 32 * 1024 * 4 + 32 * 4)
     # Section 3.1: 20 anchors x (1 base + 4 corrections) of a 4K-token Llama-3.1-8B segment in BF16 = 50 GiB
     assert 20 * (1 + 4) * kvc.kvc_dense_bytes(32, 8, 128, 4096, kvc.KVC_BF16) == 50 * 2 ** 30
 
@@ -178,6 +180,19 @@ def _cases():
         f.cache.rope_inv_freq = None
         return f.apply(), kvc.KVC_ERR_NULL_ARG
 
+    def grouping_value(f):
+        f.items[0].state.grouping = 2
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def state_reserved(f):
+        f.items[0].state.reserved = 1
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
+    def layer_rank_gt_max(f):
+        f.items[0].state.grouping = kvc.KVC_GROUP_LAYER   # D = H d = 1024: the cap is KVC_MAX_RANK
+        f.items[0].state.rank = 129
+        return f.apply(), kvc.KVC_ERR_SHAPE
+
     def rope_nonfinite_freq(f):
         f.inv = (ctypes.c_double * 64)(*([1.0] * 63 + [float("inf")]))
         f.cache.rope_style = kvc.KVC_ROPE_PAIRS
@@ -187,7 +202,8 @@ def _cases():
     return [null_cache, null_batch, head_dim, dtype, layer_range, stride_align, layer_ptr_align, null_layer,
             rank_gt_d, rank_gt_max, state_tokens, state_shape, coef_dtype, coef_align, null_coef, beyond_pool,
             beyond_table, same_tables, overlap_rows, null_items_dev, reserved, negative_offset, negative_position,
-            rope_style, rope_reserved, rope_null_freq, rope_nonfinite_freq]
+            rope_style, rope_reserved, rope_null_freq, rope_nonfinite_freq, grouping_value, state_reserved,
+            layer_rank_gt_max]
 
 
 @pytest.mark.parametrize("case", _cases(), ids=lambda c: c.__name__)
@@ -292,9 +308,13 @@ def _anchor_cases():
     def gate_null_distances(f):
         return f.gate(dist=None), kvc.KVC_ERR_NULL_ARG
 
+    def anchor_per_layer(f):
+        f.states[1].grouping = kvc.KVC_GROUP_LAYER
+        return f.weights(), kvc.KVC_ERR_UNSUPPORTED
+
     return [two_items, no_anchors, too_many_anchors, null_states, null_weights, weighted_beyond_item, anchor_short,
             anchor_rank0, anchor_dtype, anchor_shape, bad_temperature, overlap, gate_prefix, gate_workspace,
-            gate_workspace_align, gate_null_distances]
+            gate_workspace_align, gate_null_distances, anchor_per_layer]
 
 
 @pytest.mark.parametrize("case", _anchor_cases(), ids=lambda c: c.__name__)
@@ -308,3 +328,35 @@ def test_gate_workspace_query():
     need = kvc.load().kvc_gate_workspace_bytes(ctypes.byref(f.cache), ctypes.byref(f.anchors), 1200, 0, 2)
     # bf16: 512-token chunks, one float per (layer, chunk, anchor), 256-byte granules
     assert need == -(-(2 * 3 * 4 * 4) // 256) * 256
+
+
+def test_per_layer_states_are_refused_where_unsupported():
+    """Chain and anchors take per-head states; the per-layer fit takes no rotary keys and D = H d <= 1024 with
+    rank + 16 <= 128 (the Rayleigh-Ritz subspace)."""
+    lib = kvc.load()
+    f = Fixture(T=300)
+    L, H, d = f.cache.num_layers, f.cache.num_kv_heads, f.cache.head_dim
+
+    def st(T, r, grouping):
+        return kvc.kvc_state(L, H, d, T, r, kvc.KVC_BF16, grouping, 0, FAKE + 0x4000000, FAKE + 0x8000000, None)
+
+    a, b, o = st(100, 8, kvc.KVC_GROUP_LAYER), st(100, 8, kvc.KVC_GROUP_HEAD), st(100, 8, kvc.KVC_GROUP_HEAD)
+    assert lib.kvc_chain(ctypes.byref(a), ctypes.byref(b), ctypes.byref(o), 0, L, FAKE, 1 << 30,
+                         None) == kvc.KVC_ERR_UNSUPPORTED
+
+    def fit():
+        return lib.kvc_fit_state(ctypes.byref(f.cache), ctypes.byref(f.batch), 0, L, kvc.KVC_FIT_DELTA, FAKE,
+                                 1 << 40, None)
+
+    def ws():
+        return lib.kvc_fit_workspace_bytes(ctypes.byref(f.cache), ctypes.byref(f.batch), 0, L)
+
+    f.items[0].state = st(300, 32, kvc.KVC_GROUP_LAYER)
+    assert ws() > 0
+    f.items[0].state = st(300, 120, kvc.KVC_GROUP_LAYER)   # rank + 16 > 128
+    assert ws() == 0 and fit() == kvc.KVC_ERR_UNSUPPORTED
+    f.items[0].state = st(300, 32, kvc.KVC_GROUP_LAYER)
+    inv = (ctypes.c_double * 64)(*([1e-3] * 64))
+    f.cache.rope_style = kvc.KVC_ROPE_HALF
+    f.cache.rope_inv_freq = ctypes.cast(inv, ctypes.POINTER(ctypes.c_double))
+    assert fit() == kvc.KVC_ERR_UNSUPPORTED
