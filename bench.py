@@ -167,6 +167,91 @@ def rope_measurement(args, kvc, torch, pc, w, state, batch):
             "fit_token_layers_per_s": round(T * L / (fit_ms * 1e-3), 1)}
 
 
+def layer_fit_measurement(args, kvc, torch, pc, w):
+    """The paper's per-layer factorisation (every KV head of a layer side by side, D = H d = 1024) of one 8B/32K edge
+    at rank 32, and the apply of that state."""
+    L, H, d, T = w.num_layers, w.num_kv_heads, w.head_dim, w.seq_tokens[0]
+    r = 32
+    cache = kvc.Cache(pc.k_pools, pc.v_pools)
+    src, dst, out = pc.seqs[(0, 0)], pc.seqs[(0, 1)], pc.seqs[(0, 100)]
+    st = kvc.State.empty_layer(L, H, d, T, r, torch.bfloat16, "cuda")
+    fb = kvc.Batch([T], [src.offset], [dst.offset], [st], pc.tables[[src.table_row]], pc.tables[[dst.table_row]])
+    ab = kvc.Batch([T], [src.offset], [out.offset], [st], pc.tables[[src.table_row]], pc.tables[[out.table_row]])
+    ws = torch.empty(kvc.kvc_fit_workspace_bytes(cache, fb), dtype=torch.uint8, device="cuda")
+
+    def timed(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * n)]
+        for k in range(n):
+            ev[2 * k].record()
+            fn()
+            ev[2 * k + 1].record()
+        torch.cuda.synchronize()
+        return sum(ev[2 * k].elapsed_time(ev[2 * k + 1]) for k in range(n)) / n
+
+    fit_ms = timed(lambda: kvc.kvc_fit_state(cache, fb, workspace=ws), max(1, args.steps // 2))
+    apply_ms = timed(lambda: kvc.kvc_apply(cache, ab), args.steps)
+    # algorithmic bytes: rows read and written, per-layer coefficients (shared by the heads) and the bases
+    apply_b = L * 2 * T * (H * d * 2 * 2 + r * 2) + L * 2 * r * H * d * 4
+    ws_bytes = ws.numel()
+    del ws, st
+    return {"workload": f"{w.name}: per-layer factorisation (D = {H * d}) of one edge at rank {r}",
+            "fit_ms": round(fit_ms, 3), "fit_token_layers_per_s": round(T * L / (fit_ms * 1e-3), 1),
+            "apply_ms": round(apply_ms, 4), "apply_gbps": round(apply_b / (apply_ms * 1e-3) / 1e9, 2),
+            "workspace_bytes": ws_bytes}
+
+
+def chain_study(args, kvc, synth, torch):
+    """Reuse error of chained and non-chained correction along a four-agent workflow (the paper's reuse-error
+    figure): the generator's agent 0 stands for the context-free reference and agents 1-4 for A0 -> A3, one rank-16
+    deviation per edge on the 8B/4K shapes; normalised Frobenius error per agent and per layer (all heads, K and V),
+    per KV head and per layer factorisation."""
+    import numpy as np
+    from paper_2609_34060_amd import pipelines
+    w = synth.WORKLOADS["llama8b_4k"].with_(num_agents=5)
+    L, H, d, T, r = w.num_layers, w.num_kv_heads, w.head_dim, w.seq_tokens[0], w.rank
+    res = {"workload": f"{w.name} with 5 agents (reference + A0..A3), rank {r} per edge, bf16 paged", "rank": r}
+    for gname, grouping in (("head", kvc.KVC_GROUP_HEAD), ("layer", kvc.KVC_GROUP_LAYER)):
+        for mode in ("chained", "non_chained"):
+            pc = synth.build_paged(w, device="cuda", num_output_agents=4)
+            cache = kvc.Cache(pc.k_pools, pc.v_pools)
+
+            def seq(nm):
+                s = pc.seqs[nm]
+                return (s.offset, pc.tables[[s.table_row]])
+
+            agents = [seq((0, a)) for a in range(5)]
+            outs = [seq((0, 100 + j)) for j in range(4)]
+            if mode == "chained":
+                pipelines.chained(cache, agents[1:], outs, T, r, grouping)
+            else:
+                pipelines.non_chained(cache, agents[0], agents[1:], outs, T, r, grouping)
+            torch.cuda.synchronize()
+            per_agent, per_layer = [], np.zeros((4, L))
+            for j in range(4):
+                num = den = 0.0
+                for layer, (kp, vp) in enumerate(zip(pc.k_pools, pc.v_pools)):
+                    ln = ld = 0.0
+                    for pool in (kp, vp):
+                        def rows(nm):
+                            s = pc.seqs[nm]
+                            t = torch.arange(T, device="cuda") + s.offset
+                            blk = pc.tables[s.table_row].long()[t // w.block_size]
+                            return pool[blk, t % w.block_size].double()
+                        g, e = rows((0, 100 + j)), rows((0, j + 1))
+                        ln += float((g - e).square().sum())
+                        ld += float(e.square().sum())
+                    per_layer[j, layer] = (ln / ld) ** 0.5
+                    num, den = num + ln, den + ld
+                per_agent.append(round((num / den) ** 0.5, 5))
+            res[f"{mode}_{gname}"] = {"per_agent": per_agent,
+                                      "per_layer_mean_over_agents": [round(x, 5) for x in per_layer.mean(0)]}
+            del pc, cache
+            torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(pc, w, sample_layers=(0, 1)):
     """The oracle as it stands on a bounded sample of the same workload: `sample_layers` (every K/V head) of the
     first two edges -- fit S_1 and S_2, compose T_2 = chain(S_1, S_2), apply T_2 to the first agent's cache."""
@@ -224,6 +309,8 @@ def main():
     ap.add_argument("--anchor-rank", type=int, default=32)
     ap.add_argument("--no-anchor-pool", action="store_true")
     ap.add_argument("--no-rope", action="store_true", help="skip the rotary re-alignment measurement")
+    ap.add_argument("--no-layer-fit", action="store_true", help="skip the per-layer factorisation measurement")
+    ap.add_argument("--no-chain-study", action="store_true", help="skip the chained / non-chained error study")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the steps, run one elementwise kernel that reads BYTES and writes BYTES (dst = -src "
                          "in float32), a plain copy of known size, so that HBM counters of a profiling run can be "
@@ -340,12 +427,16 @@ def main():
     }
     if not args.no_rope:
         out["rope"] = rope_measurement(args, kvc, torch, pc, w, Tc[0], batch)
+    if not args.no_layer_fit:
+        out["layer_fit"] = layer_fit_measurement(args, kvc, torch, pc, w)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(pc, w)
     if not args.no_anchor_pool:
         del cache, S, Tc, fit_batches, apply_batches, ws_fit, ws_chain, pc
         torch.cuda.empty_cache()
         out["anchor_pool"] = anchor_pool_measurement(args, kvc, synth, torch)
+    if not args.no_chain_study:
+        out["chain_study"] = chain_study(args, kvc, synth, torch)
     print(json.dumps(out), flush=True)
     return 0
 
