@@ -194,7 +194,10 @@ size_t kvc_fit_workspace_bytes(const kvc_cache* cache, const kvc_batch* batch, i
 /* Fit each item's state for layers [layer_begin, layer_end); other layers of the state are left as they are.
  * Sigma descending; each basis row has its largest-magnitude entry positive.  Keys of a rotary cache:
  * Z = R(-dst_position) C_dst - R(-src_position) C_src (KVC_FIT_BASE: Z = R(-dst_position) C_dst), so the state is in
- * canonical coordinates. */
+ * canonical coordinates.  Per-layer states (KVC_GROUP_LAYER, every item of the call): Z = [Z_0 ... Z_{H-1}] with the
+ * heads side by side, D = H d <= 1024, rank <= 112, no rotary keys (KVC_ERR_UNSUPPORTED otherwise; float32 caches
+ * also need rank * D * 4 <= 160 KiB); the SVD is reached by a fixed number of subspace iterations on Z^T Z followed
+ * by a Rayleigh-Ritz step, exact up to (sigma_{k+1} / sigma_r)^16 with k = 64 (rank <= 48) or 128. */
 kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
                          kvc_fit_mode mode, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
