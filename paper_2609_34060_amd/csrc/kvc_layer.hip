@@ -5,7 +5,7 @@
 //                register layout of the per-head Gram; two waves split the block's tiles), written with its mirror
 //                into the unit's partial.  float32 caches: 64 x 64 blocks on VALU.
 //   gram_reduce  the partials of a unit summed in a fixed order in fp64.
-//   subspace     k = 64 or 128 columns: X <- orth(G X) (fp64 GEMM, two passes of modified Gram-Schmidt), then the
+//   subspace     k = 64 or 128 columns: X <- orth(G X) (fp64 GEMM, Cholesky QR twice), then the
 //                Rayleigh-Ritz matrix X^T G X goes to the per-head eigensolver as a dense k x k input; its top r
 //                eigenvectors V give the basis rows (X V^T)^T and sigma = sqrt(Ritz value).  The top-r subspace
 //                converges like (lambda_{k+1} / lambda_r)^iterations.
@@ -312,72 +312,181 @@ __device__ __forceinline__ double block_sum(double v, double* s_red) {
   return s;
 }
 
-// X = orthonormal columns spanning Y (two passes of modified Gram-Schmidt), one 1024-thread workgroup per unit.  A
-// column that vanishes against the earlier ones (rank of G below k) is replaced by a pseudo-random one in the first
-// pass; the second pass orthogonalises it.
-constexpr int kMgsThreads = 1024;
-__global__ __launch_bounds__(kMgsThreads) void sub_orth(LayerFitArgs a, uint32_t round) {
-  __shared__ double s_red[kMgsThreads / kWave];
-  const int DL = a.pv.num_kv_heads * a.pv.head_dim, k = a.k;
-  const int u = blockIdx.x;
-  const double* Y = a.y + (size_t)u * k * DL;
-  double* X = a.x + (size_t)u * k * DL;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int e = tid; e < k * DL; e += kMgsThreads) X[e] = Y[e];
+// X = orthonormal columns spanning Y by Cholesky QR applied twice: S = Y^T Y (+ shift), S = R^T R, X = Y R^{-1}.
+// The first pass carries a shift of the size of the rounding error of S (11 (D k + k (k + 1)) u ||Y||_F^2), which keeps
+// the factorisation defined for ill-conditioned Y and leaves Y R^{-1} well enough conditioned for the exact second
+// pass.  A perturbation of 1e-12 of Y's RMS (pseudo-random) keeps Y of full rank k when G has lower rank.  One
+// 256-thread workgroup per unit: S by 4 x 4 (k = 64) or 8 x 8 (k = 128) register blocks over LDS tiles of rows,
+// Cholesky and the triangular inverse in LDS, X R^{-1} with each row's outputs in registers.
+constexpr int kCqrThreads = 256, kCqrTile = 16;
+size_t cqr_lds_bytes(int k) { return ((size_t)k * (k + 1) + (size_t)k * kCqrTile + 64) * sizeof(double); }
+
+template <int K>
+__global__ __launch_bounds__(kCqrThreads) void sub_cqr(LayerFitArgs a, uint32_t round) {
+  constexpr int B = K / 16;  // register block of S per thread: B x B entries, 16 x 16 threads
+  extern __shared__ __attribute__((aligned(16))) double cqr_lds[];
+  double* S = cqr_lds;                              // [K][K + 1]
+  double* tile = S + K * (K + 1);                   // [K][kCqrTile]
+  double* red = tile + K * kCqrTile;                // reductions
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const double* Y = a.y + (size_t)u * K * DL;
+  double* X = a.x + (size_t)u * K * DL;
+
+  // perturbed copy X = Y + e * noise (noise in [-1, 1)), e = 1e-12 RMS(Y); a zero Y gets the noise alone
+  double ss = 0.0;
+  for (int e = tid; e < K * DL; e += kCqrThreads) ss += Y[e] * Y[e];
+  ss = block_sum<kCqrThreads / kWave>(ss, red);
+  const double rms = sqrt(ss / ((double)K * DL));
+  const double eps = rms > 0.0 ? 1e-12 * rms : 1.0;
+  for (int e = tid; e < K * DL; e += kCqrThreads)
+    X[e] = Y[e] + eps * hash_uniform(0x51u + round, (uint32_t)u, (uint32_t)e);
   __syncthreads();
-  double scale_ref = 0.0;
+
+  const int bi = tid / 16, bj = tid % 16;
   for (int pass = 0; pass < 2; ++pass) {
-    for (int i = 0; i < k; ++i) {
-      double* xi = X + (size_t)i * DL;
-      double s = 0.0;
-      for (int f = tid; f < DL; f += kMgsThreads) s += xi[f] * xi[f];
-      const double nrm = sqrt(block_sum<kMgsThreads / kWave>(s, s_red));
-      if (pass == 0 && i == 0) scale_ref = nrm;
-      if (pass == 0 && !(nrm > 1e-13 * scale_ref)) {
-        // numerically inside the span of the earlier columns: a fresh direction
-        for (int f = tid; f < DL; f += kMgsThreads) xi[f] = hash_uniform(0xA5A5u + round, (uint32_t)(u * k + i), f);
-        __syncthreads();
-        double s2 = 0.0;
-        for (int f = tid; f < DL; f += kMgsThreads) s2 += xi[f] * xi[f];
-        const double n2 = sqrt(block_sum<kMgsThreads / kWave>(s2, s_red));
-        for (int f = tid; f < DL; f += kMgsThreads) xi[f] /= n2;
-      } else {
-        const double inv = nrm > 0.0 ? 1.0 / nrm : 0.0;
-        for (int f = tid; f < DL; f += kMgsThreads) xi[f] *= inv;
+    // S = X^T X
+    double acc[B][B];
+#pragma unroll
+    for (int i = 0; i < B; ++i)
+#pragma unroll
+      for (int j = 0; j < B; ++j) acc[i][j] = 0.0;
+    for (int f0 = 0; f0 < DL; f0 += kCqrTile) {
+      for (int e = tid; e < K * kCqrTile; e += kCqrThreads) {
+        const int c = e / kCqrTile, ff = e - c * kCqrTile;
+        tile[c * kCqrTile + ff] = X[(size_t)c * DL + f0 + ff];
       }
       __syncthreads();
-      // remove column i from the later columns, one wave per column
-      for (int j = i + 1 + wave; j < k; j += kMgsThreads / kWave) {
-        double* xj = X + (size_t)j * DL;
-        double dp = 0.0;
-        for (int f = lane; f < DL; f += kWave) dp += xi[f] * xj[f];
+#pragma unroll 4
+      for (int ff = 0; ff < kCqrTile; ++ff) {
+        double xi[B], xj[B];
 #pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) dp += __shfl_xor(dp, o, kWave);
-        for (int f = lane; f < DL; f += kWave) xj[f] -= dp * xi[f];
+        for (int i = 0; i < B; ++i) {
+          xi[i] = tile[(bi * B + i) * kCqrTile + ff];
+          xj[i] = tile[(bj * B + i) * kCqrTile + ff];
+        }
+#pragma unroll
+        for (int i = 0; i < B; ++i)
+#pragma unroll
+          for (int j = 0; j < B; ++j) acc[i][j] = fma(xi[i], xj[j], acc[i][j]);
       }
       __syncthreads();
     }
+#pragma unroll
+    for (int i = 0; i < B; ++i)
+#pragma unroll
+      for (int j = 0; j < B; ++j) S[(bi * B + i) * (K + 1) + bj * B + j] = acc[i][j];
+    __syncthreads();
+    if (pass == 0) {
+      double tr = 0.0;
+      for (int c = 0; c < K; ++c) tr += S[c * (K + 1) + c];
+      const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
+      __syncthreads();
+      if (tid < K) S[tid * (K + 1) + tid] += shift;
+      __syncthreads();
+    }
+    // S = R^T R, R upper triangular in S's upper triangle (a pivot that is not positive is replaced by a tiny one)
+    for (int j = 0; j < K; ++j) {
+      if (tid == 0) {
+        const double dj = S[j * (K + 1) + j];
+        S[j * (K + 1) + j] = sqrt(dj > 1e-300 ? dj : 1e-300);
+      }
+      __syncthreads();
+      const double rjj = S[j * (K + 1) + j];
+      for (int i = j + 1 + tid; i < K; i += kCqrThreads) S[j * (K + 1) + i] /= rjj;
+      __syncthreads();
+      const int m = K - 1 - j;  // trailing size
+      for (int e = tid; e < m * m; e += kCqrThreads) {
+        const int i = j + 1 + e / m, l = j + 1 + e % m;
+        if (l >= i) S[i * (K + 1) + l] -= S[j * (K + 1) + i] * S[j * (K + 1) + l];
+      }
+      __syncthreads();
+    }
+    // R^{-1} in place (upper triangular): column j from the inverted leading block and column j of R
+    for (int j = 0; j < K; ++j) {
+      const double inv_jj = 1.0 / S[j * (K + 1) + j];
+      double t = 0.0;
+      if (tid < j)
+        for (int l = tid; l < j; ++l) t += S[tid * (K + 1) + l] * S[l * (K + 1) + j];
+      __syncthreads();
+      if (tid < j) S[tid * (K + 1) + j] = -t * inv_jj;
+      if (tid == j) S[j * (K + 1) + j] = inv_jj;
+      __syncthreads();
+    }
+    // X = X R^{-1}: each thread one row at a time, the K outputs of the row in registers; the row's inputs are
+    // loaded in groups of 16 ahead of their use
+    for (int f = tid; f < DL; f += kCqrThreads) {
+      double x[K];
+#pragma unroll
+      for (int c = 0; c < K; ++c) x[c] = 0.0;
+#pragma unroll 1
+      for (int i0 = 0; i0 < K; i0 += 16) {
+        double y[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) y[q] = X[(size_t)(i0 + q) * DL + f];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          const double* ri = S + (i0 + q) * (K + 1);
+#pragma unroll
+          for (int c = 0; c < K; ++c)
+            if (c >= i0 + q) x[c] = fma(y[q], ri[c], x[c]);
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < K; ++c) X[(size_t)c * DL + f] = x[c];
+    }
+    __syncthreads();
   }
 }
 
-// Rayleigh-Ritz matrix H = X^T Y (Y = G X), symmetrised, one workgroup per unit.
-__global__ __launch_bounds__(kLayerThreads) void sub_rayleigh(LayerFitArgs a) {
-  const int DL = a.pv.num_kv_heads * a.pv.head_dim, k = a.k;
-  const int u = blockIdx.x;
-  const double* X = a.x + (size_t)u * k * DL;
-  const double* Y = a.y + (size_t)u * k * DL;
-  double* Hm = a.hmat + (size_t)u * k * k;
-  for (int e = threadIdx.x; e < k * k; e += kLayerThreads) {
-    const int i = e / k, j = e - i * k;
-    if (j < i) continue;
-    double s1 = 0.0, s2 = 0.0;
-    for (int f = 0; f < DL; ++f) {
-      s1 = fma(X[(size_t)i * DL + f], Y[(size_t)j * DL + f], s1);
-      s2 = fma(X[(size_t)j * DL + f], Y[(size_t)i * DL + f], s2);
+// Rayleigh-Ritz matrix H = (X^T Y + Y^T X) / 2 with Y = G X: one 256-thread workgroup per unit, B x B register
+// blocks of X^T Y over LDS tiles of the rows of X and Y.
+template <int K>
+__global__ __launch_bounds__(kCqrThreads) void sub_rayleigh(LayerFitArgs a) {
+  constexpr int B = K / 16;
+  __shared__ double tx[K][kCqrTile + 1], ty[K][kCqrTile + 1];
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
+  const int u = blockIdx.x, tid = threadIdx.x, bi = tid / 16, bj = tid % 16;
+  const double* X = a.x + (size_t)u * K * DL;
+  const double* Y = a.y + (size_t)u * K * DL;
+  double* Hm = a.hmat + (size_t)u * K * K;
+  double acc[B][B];
+#pragma unroll
+  for (int i = 0; i < B; ++i)
+#pragma unroll
+    for (int j = 0; j < B; ++j) acc[i][j] = 0.0;
+  for (int f0 = 0; f0 < DL; f0 += kCqrTile) {
+    for (int e = tid; e < K * kCqrTile; e += kCqrThreads) {
+      const int c = e / kCqrTile, ff = e - c * kCqrTile;
+      tx[c][ff] = X[(size_t)c * DL + f0 + ff];
+      ty[c][ff] = Y[(size_t)c * DL + f0 + ff];
     }
-    const double h = 0.5 * (s1 + s2);
-    Hm[i * k + j] = h;
-    Hm[j * k + i] = h;
+    __syncthreads();
+#pragma unroll 4
+    for (int ff = 0; ff < kCqrTile; ++ff) {
+      double xi[B], yj[B];
+#pragma unroll
+      for (int i = 0; i < B; ++i) {
+        xi[i] = tx[bi * B + i][ff];
+        yj[i] = ty[bj * B + i][ff];
+      }
+#pragma unroll
+      for (int i = 0; i < B; ++i)
+#pragma unroll
+        for (int j = 0; j < B; ++j) acc[i][j] = fma(xi[i], yj[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  // X^T Y into the unit's Y area (no longer read), then the symmetric part
+  double* raw = a.y + (size_t)u * K * DL;
+#pragma unroll
+  for (int i = 0; i < B; ++i)
+#pragma unroll
+    for (int j = 0; j < B; ++j) raw[(bi * B + i) * K + bj * B + j] = acc[i][j];
+  __syncthreads();
+  for (int e = tid; e < K * K; e += kCqrThreads) {
+    const int i = e / K, j = e - i * K;
+    Hm[e] = 0.5 * (raw[i * K + j] + raw[j * K + i]);
   }
 }
 
@@ -625,14 +734,23 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
   hipLaunchKernelGGL(sub_init, dim3((a.k * DL + kLayerThreads - 1) / kLayerThreads, a.num_units),
                      dim3(kLayerThreads), 0, stream, a);
-  hipLaunchKernelGGL(sub_orth, dim3(a.num_units), dim3(kMgsThreads), 0, stream, a, 0u);
+  const size_t clds = cqr_lds_bytes(a.k);
+  const void* cqr = a.k == 64 ? (const void*)sub_cqr<64> : (const void*)sub_cqr<128>;
+  hipError_t e0 = hipFuncSetAttribute(cqr, hipFuncAttributeMaxDynamicSharedMemorySize, (int)clds);
+  if (e0 != hipSuccess) return e0;
+  auto orth = [&](uint32_t round) {
+    if (a.k == 64) hipLaunchKernelGGL(sub_cqr<64>, dim3(a.num_units), dim3(kCqrThreads), clds, stream, a, round);
+    else hipLaunchKernelGGL(sub_cqr<128>, dim3(a.num_units), dim3(kCqrThreads), clds, stream, a, round);
+  };
+  orth(0u);
   const dim3 ggrid(DL / 64, a.k / 64, a.num_units);
   for (int it = 0; it < kLayerIters; ++it) {
     hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
-    hipLaunchKernelGGL(sub_orth, dim3(a.num_units), dim3(kMgsThreads), 0, stream, a, (uint32_t)(it + 1));
+    orth((uint32_t)(it + 1));
   }
   hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
-  hipLaunchKernelGGL(sub_rayleigh, dim3(a.num_units), dim3(kLayerThreads), 0, stream, a);
+  if (a.k == 64) hipLaunchKernelGGL(sub_rayleigh<64>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
+  else hipLaunchKernelGGL(sub_rayleigh<128>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if ((e = launch_eig(ea, stream)) != hipSuccess) return e;
