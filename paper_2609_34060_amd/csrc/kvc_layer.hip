@@ -1,9 +1,10 @@
 // Per-layer factorisation (Section 3.3 with the layer's whole KV feature dimension D = H d).  The K (or V) rows of one
 // layer, every KV head side by side, form one T x D matrix Z per (item, layer, K/V) "layer unit"; its rank-r
 // truncated SVD (Eq. 7) is reached through the Gram G = Z^T Z (D x D, D up to 1024):
-//   gram_pair    the d x d block Z_h1^T Z_h2 of a head pair (h1 <= h2) over one token range (bf16 hi/lo MFMA in the
-//                register layout of the per-head Gram; two waves split the block's tiles), written with its mirror
-//                into the unit's partial.  float32 caches: 64 x 64 blocks on VALU.
+//   gram_layer   the 128 x 128 blocks on and above the diagonal of G over one token range, a 256 x 256 pair of
+//                feature groups per workgroup (Z hi/lo staged once per step in LDS as MFMA fragments, bf16 hi/lo MFMA).
+//                Block sizes below 8 or not a power of two: gram_pair, the d x d block Z_h1^T Z_h2 of a head pair with
+//                its mirror, rows read straight into registers.  float32 caches: 64 x 64 blocks on VALU.
 //   gram_reduce  the partials of a unit summed in a fixed order in fp64.
 //   subspace     k = 64 or 128 columns: X <- orth(G X) (fp64 GEMM, Cholesky QR twice), then the
 //                Rayleigh-Ritz matrix X^T G X goes to the per-head eigensolver as a dense k x k input; its top r
@@ -155,6 +156,218 @@ __global__ __launch_bounds__(kLayerThreads) void gram_pair_bf16(LayerFitArgs a) 
 }
 
 // ---------------------------------------------------------------------------------------------------------------
+// Gram of the layer, bf16, through LDS (power-of-two block size of at least 8)
+// ---------------------------------------------------------------------------------------------------------------
+// The layer's features fall into 128-feature blocks b and 256-feature groups g = {blocks 2g, 2g + 1}.  One 512-thread
+// workgroup per (unit, token range, group pair g1 <= g2).  Each 32-token step every thread forms Z = dst - src for 4
+// features x 8 tokens of the pair's features, splits it into bf16 hi/lo and writes it transposed into LDS, 16 bytes
+// per (feature, 8 tokens): exactly one MFMA operand lane.  Each wave then accumulates half of one 128 x 128 block
+// b1 <= b2 (4 x 8 tiles, 3 products each) from those fragments.  The next step's rows are in flight during the
+// products and the table entries one step further ahead; the LDS holds two steps (128 KB) and a step costs one
+// barrier.  Only blocks b1 <= b2 are written; the reduction reads the blocks below the diagonal transposed.
+constexpr int kGLThreads = 512, kGLStep = 32, kGLSlots = 512;
+constexpr size_t kGLBufChunks = (size_t)2 * 4 * kGLSlots;                     // hi/lo x 4 token groups x slots
+constexpr size_t kGLLdsBytes = 2 * kGLBufChunks * sizeof(u32x4);              // two steps: 128 KB
+
+// Slot of a feature chunk within its (hi/lo, token group) row: a XOR swizzle inside aligned groups of 8 slots keeps
+// both the producers' stores (slots 4q + j) and the fragment reads (16 consecutive slots) free of bank conflicts.
+__device__ __forceinline__ int gl_swz(int c) { return c ^ ((c >> 3) & 7); }
+
+// Paging of one pool as the Gram reads it (power-of-two block size of at least 8).
+struct GLPaging {
+  int64_t block_stride, token_stride;
+  int32_t shift, num_blocks;
+};
+
+// Table entries of the (at most two) blocks that hold tokens t .. t + 7.  An entry no token before t_end needs is
+// read at index 0 instead (every read stays inside the table row) and is never used: gl_row drops tokens past t_end.
+// The loaded values are not touched here, so the loads stay in flight until the rows are addressed.
+__device__ __forceinline__ int2 gl_blocks(const GLPaging& pg, const int32_t* __restrict__ table, int32_t off, int t,
+                                          int t_end) {
+  const int32_t p = off + t;
+  const int32_t lb0 = p >> pg.shift, lb1 = (p + 7) >> pg.shift;
+  const bool ok0 = t < t_end, ok1 = (lb1 != lb0) & ((lb1 << pg.shift) - off < t_end);
+  if (!table) return make_int2(lb0, lb1);
+  return make_int2(table[ok0 ? lb0 : 0], table[ok1 ? lb1 : 0]);
+}
+
+// Element offset of token t + j of the sequence (head 0), -1 past t_end or outside the pool.
+__device__ __forceinline__ int64_t gl_row(const GLPaging& pg, int2 b, int32_t off, int t, int j, int t_end) {
+  const int32_t p = off + t, lb0 = p >> pg.shift, pj = p + j, lb = pj >> pg.shift;
+  const int32_t blk = lb == lb0 ? b.x : b.y;
+  const bool ok = (t + j < t_end) & (blk >= 0) & (blk < pg.num_blocks);
+  const int64_t o = (int64_t)(ok ? blk : 0) * pg.block_stride + (int64_t)(pj - (lb << pg.shift)) * pg.token_stride;
+  return ok ? o : -1;
+}
+
+template <int D, bool DELTA>
+__global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, int num_pairs, int num_groups) {
+  extern __shared__ __attribute__((aligned(16))) u32x4 gl_lds[];
+  const int H = a.pv.num_kv_heads, DL = H * D, NB = (DL + 127) / 128;
+  // XCD-aware order: the workgroups one XCD receives (every 8th) take consecutive work items, so the group pairs of
+  // one (unit, token range) share that XCD's L2
+  const int nwork = gridDim.x, L = blockIdx.x, xcd = L & 7, pos = L >> 3, per = nwork >> 3, rem = nwork & 7;
+  const int w = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + pos;
+  int pr = w % num_pairs, g1 = 0;
+  const int up = w / num_pairs, part = up % a.max_parts, u = up / a.max_parts;
+  while (pr >= num_groups - g1) {
+    pr -= num_groups - g1;
+    ++g1;
+  }
+  const int g2 = g1 + pr;
+  const bool diag = g1 == g2;
+  const LayerUnit lu = layer_unit(a, u);
+  const kvc_item* itp = a.items + lu.item;
+  const int r = itp->state.rank, Ts = itp->state.num_tokens;
+  const int t_begin = part * a.part_tokens;
+  if (r == 0 || t_begin >= Ts) return;  // whole workgroup
+  const int t_end = min(Ts, t_begin + a.part_tokens);
+  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)lu.item * a.max_blocks : nullptr;
+  const uint16_t* pool = static_cast<const uint16_t*>(lu.kv ? a.layers.v[lu.lrel] : a.layers.k[lu.lrel]);
+  const int32_t doff = itp->dst_offset, soff = itp->src_offset;
+  GLPaging pg;
+  pg.block_stride = a.pv.block_stride;
+  pg.token_stride = a.pv.token_stride;
+  pg.shift = a.pv.block_shift;
+  pg.num_blocks = a.pv.num_blocks;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  // producer: slots 4q .. 4q + 3 (group g1 below slot 256, g2 above; a diagonal pair uses g1's only), tokens
+  // 8 tg .. 8 tg + 7 of the step
+  const int q = tid & 127, tg = tid >> 7, slot = 4 * q;
+  const int fglob = slot < 256 ? g1 * 256 + slot : g2 * 256 + slot - 256;
+  const bool pact = !diag || q < 64;
+  const bool inrange = pact && fglob < DL;
+  const int64_t fofs = inrange ? (int64_t)(fglob / D) * a.pv.head_stride + fglob % D : 0;
+
+  // consumer: wave = 2 x block pair (i1, i2) + row half
+  const int bp = wave >> 1, half = wave & 1, i1 = bp >> 1, i2 = bp & 1;
+  const int b1 = 2 * g1 + i1, b2 = 2 * g2 + i2;
+  const bool job = b1 < NB && b2 < NB && !(diag && i1 > i2);
+  const int sA = i1 * 128 + half * 64, sB = (diag ? 0 : 256) + i2 * 128;
+  const int lrow = lane & 15, ltg = lane >> 4;
+
+  f32x4 acc[4][8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  uint2 rd[8], rs[8];
+  uint32_t present = 0;  // bit j: dst row j of the step exists, bit 8 + j: src row j
+  // row loads of one step; a missing row loads the pool's first element and is zeroed when used, so no register
+  // with a load in flight is written
+  auto issue = [&](int t0, int2 bd, int2 bs) {
+    const int t = t0 + 8 * tg;
+    uint32_t m = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int64_t od = gl_row(pg, bd, doff, t, j, t_end);
+      const bool okd = inrange & (od >= 0);
+      rd[j] = *reinterpret_cast<const uint2*>(pool + (okd ? od + fofs : 0));
+      m |= okd ? 1u << j : 0u;
+      if constexpr (DELTA) {
+        const int64_t os = gl_row(pg, bs, soff, t, j, t_end);
+        const bool oks = inrange & (os >= 0);
+        rs[j] = *reinterpret_cast<const uint2*>(pool + (oks ? os + fofs : 0));
+        m |= oks ? 1u << (8 + j) : 0u;
+      }
+    }
+    present = m;
+  };
+  // Z hi/lo of the loaded rows, transposed into one step's LDS buffer
+  auto produce = [&](u32x4* buf) {
+    uint32_t hi[8][2], lo[8][2];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const bool pd = (present >> j) & 1u, ps = DELTA && ((present >> (8 + j)) & 1u);
+      const uint32_t dx = pd ? rd[j].x : 0u, dy = pd ? rd[j].y : 0u;
+      const uint32_t sx = ps ? rs[j].x : 0u, sy = ps ? rs[j].y : 0u;
+      split_bf16x2(bf16_lo_to_f32(dx) - bf16_lo_to_f32(sx), bf16_hi_to_f32(dx) - bf16_hi_to_f32(sx), hi[j][0],
+                   lo[j][0]);
+      split_bf16x2(bf16_lo_to_f32(dy) - bf16_lo_to_f32(sy), bf16_hi_to_f32(dy) - bf16_hi_to_f32(sy), hi[j][1],
+                   lo[j][1]);
+    }
+#pragma unroll
+    for (int f = 0; f < 4; ++f) {
+      const uint32_t sel = (f & 1) ? 0x07060302u : 0x05040100u;
+      u32x4 ch, cl;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        ch[k] = __builtin_amdgcn_perm(hi[2 * k + 1][f >> 1], hi[2 * k][f >> 1], sel);
+        cl[k] = __builtin_amdgcn_perm(lo[2 * k + 1][f >> 1], lo[2 * k][f >> 1], sel);
+      }
+      buf[tg * kGLSlots + gl_swz(slot + f)] = ch;
+      buf[(4 + tg) * kGLSlots + gl_swz(slot + f)] = cl;
+    }
+  };
+  // the wave's 32 tiles of one step
+  auto products = [&](const u32x4* buf) {
+    bf16x8 ah[4], al[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = gl_swz(sA + 16 * i + lrow);
+      ah[i] = as_bf16x8(buf[ltg * kGLSlots + c]);
+      al[i] = as_bf16x8(buf[(4 + ltg) * kGLSlots + c]);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int c = gl_swz(sB + 16 * j + lrow);
+      const bf16x8 bh = as_bf16x8(buf[ltg * kGLSlots + c]), bl = as_bf16x8(buf[(4 + ltg) * kGLSlots + c]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[i][j] = mfma16x16x32(al[i], bh, acc[i][j]);
+        acc[i][j] = mfma16x16x32(ah[i], bl, acc[i][j]);
+        acc[i][j] = mfma16x16x32(ah[i], bh, acc[i][j]);
+      }
+    }
+  };
+
+  const int nsteps = (t_end - t_begin + kGLStep - 1) / kGLStep;
+  int2 td = make_int2(-1, -1), ts = make_int2(-1, -1);
+  if (pact) {
+    td = gl_blocks(pg, dst_tab, doff, t_begin + 8 * tg, t_end);
+    if constexpr (DELTA) ts = gl_blocks(pg, src_tab, soff, t_begin + 8 * tg, t_end);
+    issue(t_begin, td, ts);
+    if (nsteps > 1) {
+      td = gl_blocks(pg, dst_tab, doff, t_begin + kGLStep + 8 * tg, t_end);
+      if constexpr (DELTA) ts = gl_blocks(pg, src_tab, soff, t_begin + kGLStep + 8 * tg, t_end);
+    }
+    produce(gl_lds);
+  }
+  __syncthreads();
+  for (int s = 0; s < nsteps; ++s) {
+    const bool more = s + 1 < nsteps;
+    if (pact && more) {
+      const int t1 = t_begin + (s + 1) * kGLStep;
+      issue(t1, td, ts);
+      if (s + 2 < nsteps) {
+        td = gl_blocks(pg, dst_tab, doff, t1 + kGLStep + 8 * tg, t_end);
+        if constexpr (DELTA) ts = gl_blocks(pg, src_tab, soff, t1 + kGLStep + 8 * tg, t_end);
+      }
+    }
+    if (job) products(gl_lds + (s & 1) * kGLBufChunks);
+    if (pact && more) produce(gl_lds + ((s + 1) & 1) * kGLBufChunks);
+    __syncthreads();
+  }
+
+  if (!job) return;
+  float* P = a.partials + ((size_t)u * a.max_parts + part) * DL * DL;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int col = b2 * 128 + 16 * j + lrow;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = b1 * 128 + half * 64 + 16 * i + 4 * ltg + e;
+        if (row < DL && col < DL) P[(size_t)row * DL + col] = acc[i][j][e];
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------------------------------------------
 // Gram, float32 caches: one 64 x 64 block of G over one token range per workgroup (VALU, 4 x 4 outputs per thread)
 // ---------------------------------------------------------------------------------------------------------------
 
@@ -219,19 +432,36 @@ __global__ __launch_bounds__(kLayerThreads) void gram_block_f32(LayerFitArgs a) 
       P[(size_t)(bi * kF32Block + 4 * ti + i) * DL + bj * kF32Block + 4 * tj + j] = acc[i][j];
 }
 
-// G = sum of the unit's partials in order, fp64.
-__global__ __launch_bounds__(kLayerThreads) void gram_reduce(LayerFitArgs a) {
-  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
-  const int u = blockIdx.y;
-  const size_t e = (size_t)blockIdx.x * kLayerThreads + threadIdx.x;
-  if (e >= (size_t)DL * DL) return;
+// G = sum of the unit's partials in order, fp64, one 32 x 32 tile per workgroup.  With upper_only the partials hold
+// the 128 x 128 blocks on and above the diagonal, and a tile below it is summed from its mirror and transposed in LDS.
+__global__ __launch_bounds__(kLayerThreads) void gram_reduce(LayerFitArgs a, int upper_only) {
+  __shared__ double tr[32][33];
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, nt = DL / 32;
+  const int u = blockIdx.y, I = blockIdx.x / nt, J = blockIdx.x - I * nt;
   const LayerUnit lu = layer_unit(a, u);
   const int Ts = a.items[lu.item].state.num_tokens;
   const int parts = min(a.max_parts, (Ts + a.part_tokens - 1) / a.part_tokens);
-  const float* P = a.partials + (size_t)u * a.max_parts * DL * DL + e;
-  double s = 0.0;
-  for (int p = 0; p < parts; ++p) s += (double)P[(size_t)p * DL * DL];
-  a.gram[(size_t)u * DL * DL + e] = s;
+  const bool mirror = upper_only && (I >> 2) > (J >> 2);
+  const int sI = mirror ? J : I, sJ = mirror ? I : J;
+  const int rr = threadIdx.x >> 5, c = threadIdx.x & 31;
+  const float* P = a.partials + (size_t)u * a.max_parts * DL * DL;
+  double* G = a.gram + (size_t)u * DL * DL;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int row = rr + 8 * k;
+    const size_t e = (size_t)(sI * 32 + row) * DL + sJ * 32 + c;
+    double s = 0.0;
+    for (int p = 0; p < parts; ++p) s += (double)P[(size_t)p * DL * DL + e];
+    if (mirror) tr[row][c] = s;
+    else G[(size_t)(I * 32 + row) * DL + J * 32 + c] = s;
+  }
+  if (!mirror) return;  // whole workgroup
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int row = rr + 8 * k;
+    G[(size_t)(I * 32 + row) * DL + J * 32 + c] = tr[c][row];
+  }
 }
 
 // ---------------------------------------------------------------------------------------------------------------
@@ -713,7 +943,22 @@ __global__ __launch_bounds__(kLayerThreads) void proj_layer_f32(LayerFitArgs a) 
 
 hipError_t launch_layer_gram(const LayerFitArgs& a, kvc_dtype dtype, hipStream_t stream) {
   const int D = a.pv.head_dim, H = a.pv.num_kv_heads, DL = H * D;
-  if (dtype == KVC_BF16) {
+  int upper_only = 0;
+  if (dtype == KVC_BF16 && a.pv.block_shift >= 3) {
+    const int NB = (DL + 127) / 128, NG = (NB + 1) / 2, pairs = NG * (NG + 1) / 2;
+    const unsigned nwork = (unsigned)a.num_units * a.max_parts * pairs;
+    const bool delta = a.mode == KVC_FIT_DELTA;
+    const void* fn = D == 64 ? (delta ? (const void*)gram_layer_bf16<64, true> : (const void*)gram_layer_bf16<64, false>)
+                             : (delta ? (const void*)gram_layer_bf16<128, true> : (const void*)gram_layer_bf16<128, false>);
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGLLdsBytes);
+    if (e != hipSuccess) return e;
+    const dim3 grid(nwork), block(kGLThreads);
+    if (D == 64 && delta) hipLaunchKernelGGL((gram_layer_bf16<64, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG);
+    else if (D == 64) hipLaunchKernelGGL((gram_layer_bf16<64, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG);
+    else if (delta) hipLaunchKernelGGL((gram_layer_bf16<128, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG);
+    else hipLaunchKernelGGL((gram_layer_bf16<128, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG);
+    upper_only = 1;
+  } else if (dtype == KVC_BF16) {
     dim3 grid((a.max_parts + kLayerWaves / 2 - 1) / (kLayerWaves / 2), H * (H + 1) / 2, a.num_units);
     if (D == 64) hipLaunchKernelGGL(gram_pair_bf16<64>, grid, dim3(kLayerThreads), 0, stream, a);
     else hipLaunchKernelGGL(gram_pair_bf16<128>, grid, dim3(kLayerThreads), 0, stream, a);
@@ -725,8 +970,8 @@ hipError_t launch_layer_gram(const LayerFitArgs& a, kvc_dtype dtype, hipStream_t
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 rgrid((unsigned)(((size_t)DL * DL + kLayerThreads - 1) / kLayerThreads), a.num_units);
-  hipLaunchKernelGGL(gram_reduce, rgrid, dim3(kLayerThreads), 0, stream, a);
+  const int nt = DL / 32;
+  hipLaunchKernelGGL(gram_reduce, dim3(nt * nt, a.num_units), dim3(kLayerThreads), 0, stream, a, upper_only);
   return hipGetLastError();
 }
 

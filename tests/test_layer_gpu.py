@@ -48,24 +48,45 @@ def _plant_layer_deviation(pc, src, dst, rank, seed):
             pool[bd, sd] = (x + dev).reshape(T, H, d).to(pool.dtype).to(pool.device)
 
 
-@pytest.mark.parametrize("name,layers,rank", [("tiny", 2, 8), ("llama8b_4k", 2, 32), ("llama8b_4k", 1, 48)])
-def test_layer_fit_matches_oracle(name, layers, rank):
-    w = synth.WORKLOADS[name].with_(num_layers=layers)
+def _plant_layer_base(pc, dst, rank, seed):
+    """dst = U diag(s) V^T + noise per (layer, K/V): a base cache of exact rank `rank` plus N(0, 1e-3^2)."""
+    w = pc.workload
+    H, d, T = w.num_kv_heads, w.head_dim, dst.num_tokens
+    g = torch.Generator().manual_seed(seed)
+    for pools in (pc.k_pools, pc.v_pools):
+        for pool in pools:
+            bd, sd = _rows(pc, dst, pool)
+            u = torch.linalg.qr(torch.randn(T, rank, generator=g, dtype=torch.float64))[0]
+            v = torch.linalg.qr(torch.randn(H * d, rank, generator=g, dtype=torch.float64))[0]
+            s = torch.sort(0.5 + 0.5 * torch.rand(rank, generator=g, dtype=torch.float64), descending=True)[0]
+            x = (u * s) @ v.T
+            x *= 0.25 / x.square().mean().sqrt()
+            x += 1e-3 * torch.randn(T, H * d, generator=g, dtype=torch.float64)
+            pool[bd, sd] = x.reshape(T, H, d).to(pool.dtype).to(pool.device)
+
+
+def _fit_and_compare(w, layers, rank, mode=kvc.KVC_FIT_DELTA):
+    """Fit a per-layer state on the GPU and in the oracle and compare sigma, A B per unit, the basis's
+    orthonormality and (delta mode) the cache materialised from it."""
     pc = synth.build_paged(w, device="cuda", num_output_agents=1)
     H, d = w.num_kv_heads, w.head_dim
     src, dst, out = pc.seqs[(0, 0)], pc.seqs[(0, 1)], pc.seqs[(0, 100)]
-    _plant_layer_deviation(pc, src, dst, rank, 61 + rank)
+    if mode == kvc.KVC_FIT_DELTA:
+        _plant_layer_deviation(pc, src, dst, rank, 61 + rank)
+    else:
+        _plant_layer_base(pc, dst, rank, 67 + rank)
     tab = (lambda s: None) if pc.tables is None else (lambda s: pc.tables[[s.table_row]])
     T = dst.num_tokens
     sdt = synth.storage_dtype(w)
     st = kvc.State.empty_layer(layers, H, d, T, rank, sdt, "cuda")
     cache = kvc.Cache(pc.k_pools, pc.v_pools)
     batch = kvc.Batch([T], [src.offset], [dst.offset], [st], tab(src), tab(dst))
-    kvc.kvc_fit_state(cache, batch)
+    kvc.kvc_fit_state(cache, batch, mode=mode)
     torch.cuda.synchronize()
     cnp = Hp.oracle_cache(pc.k_pools, pc.v_pools, w.block_size)
     item = O.Item(T, src.offset, dst.offset, Hp.table_np(tab(src), 0), Hp.table_np(tab(dst), 0))
-    ost, raw = O.fit(cnp, [item], rank, grouping=O.GROUP_LAYER)
+    omode = O.MODE_DELTA if mode == kvc.KVC_FIT_DELTA else O.MODE_BASE
+    ost, raw = O.fit(cnp, [item], rank, grouping=O.GROUP_LAYER, mode=omode)
     coef, basis, sigma = raw[0]
     dt = cnp.dtype
     gc = O.to_f64(Hp.to_np_storage(st.coef), dt)
@@ -78,8 +99,11 @@ def test_layer_fit_matches_oracle(name, layers, rank):
         e = O.max_relative_error(gc[idx] @ b, coef[idx] @ basis[idx])
         es = np.max(np.abs(gs[idx] - sigma[idx])) / sigma[idx][0]
         worst_p, worst_s = max(worst_p, e), max(worst_s, es)
-    print(f"{name} rank {rank}: product err {worst_p:.2e}, sigma err {worst_s:.2e}")
+    print(f"{w.name} H {H} d {d} block {w.block_size} T {T} rank {rank} mode {mode}: product err {worst_p:.2e}, "
+          f"sigma err {worst_s:.2e}")
     assert worst_p <= TOL_PROD[dt] and worst_s <= 1e-4
+    if mode != kvc.KVC_FIT_DELTA:
+        return
     # the per-layer state materialises agent 1's cache from agent 0's
     kvc.kvc_apply(cache, kvc.Batch([T], [src.offset], [out.offset], [st], tab(src), tab(out)))
     torch.cuda.synchronize()
@@ -94,6 +118,26 @@ def test_layer_fit_matches_oracle(name, layers, rank):
                 worst = max(worst, O.max_relative_error(O.to_f64(g, dt), O.to_f64(e, dt)))
     print(f"  materialised: err {worst:.2e}")
     assert worst <= TOL_CACHE[dt]
+
+
+@pytest.mark.parametrize("name,layers,rank", [("tiny", 2, 8), ("llama8b_4k", 2, 32), ("llama8b_4k", 1, 48)])
+def test_layer_fit_matches_oracle(name, layers, rank):
+    _fit_and_compare(synth.WORKLOADS[name].with_(num_layers=layers), layers, rank)
+
+
+# bf16 shapes around the Gram's 128-feature blocks and 256-feature groups: 64-dim heads with a half-filled last block
+# (D = 320: blocks 0-2, groups {0, 1} and {2}), block sizes below 8 and not a power of two (the register Gram),
+# a ragged token count over several token ranges, and base-cache fits (the src side unread).
+@pytest.mark.parametrize("H,d,bs,T,rank,mode", [
+    (5, 64, 16, 700, 24, kvc.KVC_FIT_DELTA),
+    (3, 64, 4, 530, 16, kvc.KVC_FIT_DELTA),
+    (2, 128, 12, 610, 16, kvc.KVC_FIT_BASE),
+    (8, 128, 16, 1000, 32, kvc.KVC_FIT_BASE),
+])
+def test_layer_fit_shapes(H, d, bs, T, rank, mode):
+    w = synth.WORKLOADS["llama8b_4k"].with_(num_layers=1, num_kv_heads=H, head_dim=d, block_size=bs, seq_tokens=(T,),
+                                            num_agents=2)
+    _fit_and_compare(w, 1, rank, mode)
 
 
 @pytest.mark.parametrize("name,layers,rank,Ts", [("tiny", 2, 8, 200), ("llama8b_4k", 2, 32, 3001)])
