@@ -141,8 +141,8 @@ FitPlan plan_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int32_t le)
 // at most 8 token partials per layer unit (a partial of D = H d is up to 4 MB).
 struct LayerPlan {
   int32_t layers_per_group = 1, part_tokens = 256, max_parts = 1, k = 64;
-  size_t units = 0, off_partials = 0, off_gram = 0, off_x = 0, off_y = 0, off_h = 0, off_vrows = 0, off_vsigma = 0,
-         off_reflect = 0, off_beta = 0, off_vecs = 0, total = 0;
+  size_t units = 0, off_partials = 0, off_gram = 0, off_x = 0, off_y = 0, off_h = 0, off_spart = 0, off_eps = 0,
+         off_vrows = 0, off_vsigma = 0, off_reflect = 0, off_beta = 0, off_vecs = 0, total = 0;
 };
 
 // Which calls the per-layer path takes (every item per layer, no rotary keys, D = H d <= 1024, rank + 16 <= k).
@@ -189,6 +189,10 @@ LayerPlan plan_layer_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int
   off = align256(off + U * k * DL * sizeof(double));
   p.off_h = off;
   off = align256(off + U * k * k * sizeof(double));
+  p.off_spart = off;
+  off = align256(off + U * ((DL + 255) / 256) * k * k * sizeof(double));
+  p.off_eps = off;
+  off = align256(off + U * sizeof(double));
   p.off_vrows = off;
   off = align256(off + U * KVC_MAX_RANK * k * sizeof(float));
   p.off_vsigma = off;
@@ -504,6 +508,8 @@ kvc_status fit_per_layer(const kvc_cache* cache, const kvc_batch* batch, int32_t
   la.x = reinterpret_cast<double*>(ws + p.off_x);
   la.y = reinterpret_cast<double*>(ws + p.off_y);
   la.hmat = reinterpret_cast<double*>(ws + p.off_h);
+  la.spart = reinterpret_cast<double*>(ws + p.off_spart);
+  la.eps = reinterpret_cast<double*>(ws + p.off_eps);
   la.vrows = reinterpret_cast<float*>(ws + p.off_vrows);
   la.vsigma = reinterpret_cast<float*>(ws + p.off_vsigma);
   kvc_status s = KVC_OK;

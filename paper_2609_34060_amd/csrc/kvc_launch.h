@@ -62,7 +62,9 @@ struct LayerFitArgs {
   double* gram;                // [unit][D][D]
   double* x;                   // [unit][k][D] orthonormal columns (stored as rows)
   double* y;                   // [unit][k][D]
-  double* hmat;                // [unit][k][k]
+  double* hmat;                // [unit][k][k]; during the iteration R^{-1} of the Cholesky QR
+  double* spart;               // [unit][ceil(D / 256)][k][k] partial Y^T Y of the Cholesky QR
+  double* eps;                 // [unit] perturbation size of the Cholesky QR
   float* vrows;                // [unit][rank][k] eigenvectors of hmat (rows)
   float* vsigma;               // [unit][rank]
 };

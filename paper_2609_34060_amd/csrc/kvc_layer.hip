@@ -487,44 +487,66 @@ __global__ __launch_bounds__(kLayerThreads) void sub_init(LayerFitArgs a) {
   a.y[(size_t)u * a.k * DL + e] = hash_uniform((uint32_t)u, (uint32_t)(e / DL), (uint32_t)(e % DL));
 }
 
-// Y = G X for every unit: a 64 x 64 tile (features x columns) per workgroup, 4 x 4 outputs per thread.
+// Y = G X for every unit: a 128 x 64 tile (features x columns) per workgroup; thread (ti, tj) owns features
+// 8 ti .. 8 ti + 7 and columns tj + 16 j.  The next 32-wide slices of G and X are loaded into registers while the
+// current ones are used.
+constexpr int kGemmRows = 128;
 __global__ __launch_bounds__(kLayerThreads) void sub_gemm(LayerFitArgs a) {
-  constexpr int TB = 64, KB = 16;
-  __shared__ double s_g[TB][KB + 1], s_x[KB][TB + 1];
+  constexpr int TR = kGemmRows, TC = 64, KB = 32, NG = TR * KB / kLayerThreads, NX = TC * KB / kLayerThreads;
+  __shared__ double s_g[TR][KB + 1], s_x[KB][TC + 1];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
-  const int f0 = blockIdx.x * TB, c0 = blockIdx.y * TB, u = blockIdx.z;
+  const int f0 = blockIdx.x * TR, c0 = blockIdx.y * TC, u = blockIdx.z;
   const double* G = a.gram + (size_t)u * DL * DL;
   const double* X = a.x + (size_t)u * a.k * DL;
   double* Y = a.y + (size_t)u * a.k * DL;
   const int tid = threadIdx.x, ti = tid / 16, tj = tid % 16;
-  double acc[4][4] = {};
+  double pg[NG], px[NX];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+      const int e = tid + q * kLayerThreads, i = e / KB, kk = e - i * KB;
+      pg[q] = f0 + i < DL ? G[(size_t)(f0 + i) * DL + k0 + kk] : 0.0;
+    }
+#pragma unroll
+    for (int q = 0; q < NX; ++q) {
+      const int e = tid + q * kLayerThreads, i = e / KB, kk = e - i * KB;
+      px[q] = X[(size_t)(c0 + i) * DL + k0 + kk];
+    }
+  };
+  double acc[8][4] = {};
+  load(0);
   for (int k0 = 0; k0 < DL; k0 += KB) {
-    for (int e = tid; e < TB * KB; e += kLayerThreads) {
-      const int i = e / KB, kk = e - i * KB;
-      s_g[i][kk] = G[(size_t)(f0 + i) * DL + k0 + kk];
-      const int c = e / KB, k2 = e - c * KB;
-      s_x[k2][c] = X[(size_t)(c0 + c) * DL + k0 + k2];
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+      const int e = tid + q * kLayerThreads, i = e / KB, kk = e - i * KB;
+      s_g[i][kk] = pg[q];
+    }
+#pragma unroll
+    for (int q = 0; q < NX; ++q) {
+      const int e = tid + q * kLayerThreads, i = e / KB, kk = e - i * KB;
+      s_x[kk][i] = px[q];
     }
     __syncthreads();
-#pragma unroll
+    if (k0 + KB < DL) load(k0 + KB);
+#pragma unroll 4
     for (int kk = 0; kk < KB; ++kk) {
-      double g4[4], x4[4];
+      double g8[8], x4[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        g4[i] = s_g[4 * ti + i][kk];
-        x4[i] = s_x[kk][4 * tj + i];
-      }
+      for (int i = 0; i < 8; ++i) g8[i] = s_g[8 * ti + i][kk];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int j = 0; j < 4; ++j) x4[j] = s_x[kk][tj + 16 * j];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fma(g4[i], x4[j], acc[i][j]);
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fma(g8[i], x4[j], acc[i][j]);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) Y[(size_t)(c0 + 4 * tj + j) * DL + f0 + 4 * ti + i] = acc[i][j];
+    for (int i = 0; i < 8; ++i)
+      if (f0 + 8 * ti + i < DL) Y[(size_t)(c0 + tj + 16 * j) * DL + f0 + 8 * ti + i] = acc[i][j];
 }
 
 // Whole-workgroup sum (fixed order: waves in order), result in every thread.
@@ -545,128 +567,298 @@ __device__ __forceinline__ double block_sum(double v, double* s_red) {
 // X = orthonormal columns spanning Y by Cholesky QR applied twice: S = Y^T Y (+ shift), S = R^T R, X = Y R^{-1}.
 // The first pass carries a shift of the size of the rounding error of S (11 (D k + k (k + 1)) u ||Y||_F^2), which keeps
 // the factorisation defined for ill-conditioned Y and leaves Y R^{-1} well enough conditioned for the exact second
-// pass.  A perturbation of 1e-12 of Y's RMS (pseudo-random) keeps Y of full rank k when G has lower rank.  One
-// 256-thread workgroup per unit: S by 4 x 4 (k = 64) or 8 x 8 (k = 128) register blocks over LDS tiles of rows,
-// Cholesky and the triangular inverse in LDS, X R^{-1} with each row's outputs in registers.
-constexpr int kCqrThreads = 256, kCqrTile = 16;
-size_t cqr_lds_bytes(int k) { return ((size_t)k * (k + 1) + (size_t)k * kCqrTile + 64) * sizeof(double); }
+// pass.  A perturbation of 1e-12 of Y's RMS (pseudo-random) keeps Y of full rank k when G has lower rank.  Four
+// kernels per pass, each spread over the unit's features except the k x k factorisation:
+//   cqr_scale   the perturbation size of each unit (first pass)
+//   cqr_syrk    partial S over 256 features per workgroup (register blocks over LDS tiles of 32 features)
+//   cqr_factor  one wave per unit: the partials summed in order, the shift, Cholesky and the inverse of R (k = 64
+//               in registers, k = 128 in LDS)
+//   cqr_apply   X = Y R^{-1} for 64 features per workgroup (the tile is read whole before it is written, so the
+//               second pass runs in place)
+constexpr int kCqrThreads = 256, kCqrTile = 16, kCqrChunk = 256, kCqrSub = 32, kCqrRows = 64, kCqrWChunk = 32;
+
+// The perturbed entry e of unit u's Y (every kernel of a pass forms it the same way).
+__device__ __forceinline__ double cqr_perturbed(double y, double eps, uint32_t round, int u, size_t e) {
+  return fma(eps, hash_uniform(0x51u + round, (uint32_t)u, (uint32_t)e), y);
+}
+
+constexpr int kScaleThreads = 1024;
+__global__ __launch_bounds__(kScaleThreads) void cqr_scale(LayerFitArgs a) {
+  constexpr int NB = 8;
+  __shared__ double red[kScaleThreads / kWave];
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, u = blockIdx.x;
+  const size_t n = (size_t)a.k * DL;
+  const double* Y = a.y + (size_t)u * n;
+  double ss[NB];
+#pragma unroll
+  for (int q = 0; q < NB; ++q) ss[q] = 0.0;
+  for (size_t e0 = threadIdx.x; e0 < n; e0 += NB * kScaleThreads)
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      const size_t e = e0 + q * kScaleThreads;
+      const double y = e < n ? Y[e] : 0.0;
+      ss[q] = fma(y, y, ss[q]);
+    }
+  double s = 0.0;
+#pragma unroll
+  for (int q = 0; q < NB; ++q) s += ss[q];
+  s = block_sum<kScaleThreads / kWave>(s, red);
+  const double rms = sqrt(s / (double)n);
+  if (threadIdx.x == 0) a.eps[u] = rms > 0.0 ? 1e-12 * rms : 1.0;
+}
 
 template <int K>
-__global__ __launch_bounds__(kCqrThreads) void sub_cqr(LayerFitArgs a, uint32_t round) {
-  constexpr int B = K / 16;  // register block of S per thread: B x B entries, 16 x 16 threads
-  extern __shared__ __attribute__((aligned(16))) double cqr_lds[];
-  double* S = cqr_lds;                              // [K][K + 1]
-  double* tile = S + K * (K + 1);                   // [K][kCqrTile]
-  double* red = tile + K * kCqrTile;                // reductions
-  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
-  const int u = blockIdx.x, tid = threadIdx.x;
-  const double* Y = a.y + (size_t)u * K * DL;
-  double* X = a.x + (size_t)u * K * DL;
-
-  // perturbed copy X = Y + e * noise (noise in [-1, 1)), e = 1e-12 RMS(Y); a zero Y gets the noise alone
-  double ss = 0.0;
-  for (int e = tid; e < K * DL; e += kCqrThreads) ss += Y[e] * Y[e];
-  ss = block_sum<kCqrThreads / kWave>(ss, red);
-  const double rms = sqrt(ss / ((double)K * DL));
-  const double eps = rms > 0.0 ? 1e-12 * rms : 1.0;
-  for (int e = tid; e < K * DL; e += kCqrThreads)
-    X[e] = Y[e] + eps * hash_uniform(0x51u + round, (uint32_t)u, (uint32_t)e);
-  __syncthreads();
-
-  const int bi = tid / 16, bj = tid % 16;
-  for (int pass = 0; pass < 2; ++pass) {
-    // S = X^T X
-    double acc[B][B];
+__global__ __launch_bounds__(kCqrThreads) void cqr_syrk(LayerFitArgs a, const double* __restrict__ src, int perturb,
+                                                         uint32_t round) {
+  constexpr int B = K / 16;
+  __shared__ double tile[K][kCqrSub + 1];
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
+  const int chunk = blockIdx.x, u = blockIdx.y, tid = threadIdx.x, bi = tid / 16, bj = tid % 16;
+  const int f_begin = chunk * kCqrChunk, f_end = min(DL, f_begin + kCqrChunk);
+  const double* Y = src + (size_t)u * K * DL;
+  const double eps = perturb ? a.eps[u] : 0.0;
+  double acc[B][B];
 #pragma unroll
-    for (int i = 0; i < B; ++i)
+  for (int i = 0; i < B; ++i)
 #pragma unroll
-      for (int j = 0; j < B; ++j) acc[i][j] = 0.0;
-    for (int f0 = 0; f0 < DL; f0 += kCqrTile) {
-      for (int e = tid; e < K * kCqrTile; e += kCqrThreads) {
-        const int c = e / kCqrTile, ff = e - c * kCqrTile;
-        tile[c * kCqrTile + ff] = X[(size_t)c * DL + f0 + ff];
-      }
-      __syncthreads();
-#pragma unroll 4
-      for (int ff = 0; ff < kCqrTile; ++ff) {
-        double xi[B], xj[B];
-#pragma unroll
-        for (int i = 0; i < B; ++i) {
-          xi[i] = tile[(bi * B + i) * kCqrTile + ff];
-          xj[i] = tile[(bj * B + i) * kCqrTile + ff];
-        }
-#pragma unroll
-        for (int i = 0; i < B; ++i)
-#pragma unroll
-          for (int j = 0; j < B; ++j) acc[i][j] = fma(xi[i], xj[j], acc[i][j]);
-      }
-      __syncthreads();
+    for (int j = 0; j < B; ++j) acc[i][j] = 0.0;
+  for (int f0 = f_begin; f0 < f_end; f0 += kCqrSub) {
+    for (int e = tid; e < K * kCqrSub; e += kCqrThreads) {
+      const int c = e / kCqrSub, ff = e - c * kCqrSub;
+      const size_t idx = (size_t)c * DL + f0 + ff;
+      const double y = Y[idx];
+      tile[c][ff] = perturb ? cqr_perturbed(y, eps, round, u, idx) : y;
     }
-#pragma unroll
-    for (int i = 0; i < B; ++i)
-#pragma unroll
-      for (int j = 0; j < B; ++j) S[(bi * B + i) * (K + 1) + bj * B + j] = acc[i][j];
     __syncthreads();
-    if (pass == 0) {
-      double tr = 0.0;
-      for (int c = 0; c < K; ++c) tr += S[c * (K + 1) + c];
-      const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
-      __syncthreads();
-      if (tid < K) S[tid * (K + 1) + tid] += shift;
-      __syncthreads();
-    }
-    // S = R^T R, R upper triangular in S's upper triangle (a pivot that is not positive is replaced by a tiny one)
-    for (int j = 0; j < K; ++j) {
-      if (tid == 0) {
-        const double dj = S[j * (K + 1) + j];
-        S[j * (K + 1) + j] = sqrt(dj > 1e-300 ? dj : 1e-300);
-      }
-      __syncthreads();
-      const double rjj = S[j * (K + 1) + j];
-      for (int i = j + 1 + tid; i < K; i += kCqrThreads) S[j * (K + 1) + i] /= rjj;
-      __syncthreads();
-      const int m = K - 1 - j;  // trailing size
-      for (int e = tid; e < m * m; e += kCqrThreads) {
-        const int i = j + 1 + e / m, l = j + 1 + e % m;
-        if (l >= i) S[i * (K + 1) + l] -= S[j * (K + 1) + i] * S[j * (K + 1) + l];
-      }
-      __syncthreads();
-    }
-    // R^{-1} in place (upper triangular): column j from the inverted leading block and column j of R
-    for (int j = 0; j < K; ++j) {
-      const double inv_jj = 1.0 / S[j * (K + 1) + j];
-      double t = 0.0;
-      if (tid < j)
-        for (int l = tid; l < j; ++l) t += S[tid * (K + 1) + l] * S[l * (K + 1) + j];
-      __syncthreads();
-      if (tid < j) S[tid * (K + 1) + j] = -t * inv_jj;
-      if (tid == j) S[j * (K + 1) + j] = inv_jj;
-      __syncthreads();
-    }
-    // X = X R^{-1}: each thread one row at a time, the K outputs of the row in registers; the row's inputs are
-    // loaded in groups of 16 ahead of their use
-    for (int f = tid; f < DL; f += kCqrThreads) {
-      double x[K];
+#pragma unroll 4
+    for (int ff = 0; ff < kCqrSub; ++ff) {
+      double xi[B], xj[B];
 #pragma unroll
-      for (int c = 0; c < K; ++c) x[c] = 0.0;
-#pragma unroll 1
-      for (int i0 = 0; i0 < K; i0 += 16) {
-        double y[16];
-#pragma unroll
-        for (int q = 0; q < 16; ++q) y[q] = X[(size_t)(i0 + q) * DL + f];
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-          const double* ri = S + (i0 + q) * (K + 1);
-#pragma unroll
-          for (int c = 0; c < K; ++c)
-            if (c >= i0 + q) x[c] = fma(y[q], ri[c], x[c]);
-        }
+      for (int i = 0; i < B; ++i) {
+        xi[i] = tile[bi * B + i][ff];
+        xj[i] = tile[bj * B + i][ff];
       }
 #pragma unroll
-      for (int c = 0; c < K; ++c) X[(size_t)c * DL + f] = x[c];
+      for (int i = 0; i < B; ++i)
+#pragma unroll
+        for (int j = 0; j < B; ++j) acc[i][j] = fma(xi[i], xj[j], acc[i][j]);
     }
     __syncthreads();
   }
+  double* P = a.spart + ((size_t)u * nch + chunk) * K * K;
+#pragma unroll
+  for (int i = 0; i < B; ++i)
+#pragma unroll
+    for (int j = 0; j < B; ++j) P[(bi * B + i) * K + bj * B + j] = acc[i][j];
+}
+
+// One wave per unit; S in LDS with rows padded to K + 1.  Cholesky (upper, S = R^T R; a pivot that is not positive is
+// replaced by a tiny one), then R^{-1} in place column by column: column j of the inverse needs only the inverted
+// leading block and column j of R.  R^{-1} goes to hmat with zeros below the diagonal.
+template <int K>
+__global__ __launch_bounds__(kWave) void cqr_factor(LayerFitArgs a, int shifted) {
+  constexpr int KP = K + 1, NB = 8;  // LDS row pitch; loads issued in batches of NB ahead of their stores
+  extern __shared__ double fs[];     // [K][K + 1]
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const double* P = a.spart + (size_t)u * nch * K * K;
+  for (int e0 = tid; e0 < K * K; e0 += NB * kWave) {
+    double s[NB];
+#pragma unroll
+    for (int q = 0; q < NB; ++q) s[q] = 0.0;
+    for (int p = 0; p < nch; ++p)
+#pragma unroll
+      for (int q = 0; q < NB; ++q) s[q] += P[(size_t)p * K * K + e0 + q * kWave];
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      const int e = e0 + q * kWave;
+      fs[(e / K) * KP + e % K] = s[q];
+    }
+  }
+  __syncthreads();
+  if (shifted) {
+    double tr = 0.0;
+    for (int c = 0; c < K; ++c) tr += fs[c * KP + c];
+    const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
+    __syncthreads();
+    for (int c = tid; c < K; c += kWave) fs[c * KP + c] += shift;
+    __syncthreads();
+  }
+  // Cholesky: row j scaled by the pivot, then the trailing upper triangle updated column by column (one column per
+  // lane), NB rows at a time with every load of the batch before its stores
+  for (int j = 0; j < K; ++j) {
+    const double d = fs[j * KP + j];
+    const double rjj = sqrt(d > 1e-300 ? d : 1e-300);
+    __syncthreads();
+    for (int c = j + 1 + tid; c < K; c += kWave) fs[j * KP + c] /= rjj;
+    if (tid == 0) fs[j * KP + j] = rjj;
+    __syncthreads();
+    for (int c = j + 1 + tid; c < K; c += kWave) {
+      const double rjc = fs[j * KP + c];
+      for (int k0 = j + 1; k0 <= c; k0 += NB) {
+        double rj[NB], v[NB];
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+          const int k = min(k0 + q, c);
+          rj[q] = fs[j * KP + k];
+          v[q] = fs[k * KP + c];
+        }
+#pragma unroll
+        for (int q = 0; q < NB; ++q)
+          if (k0 + q <= c) fs[(k0 + q) * KP + c] = v[q] - rj[q] * rjc;
+      }
+    }
+    __syncthreads();
+  }
+  // R^{-1} in place, column by column: V[r][j] = -(sum_{r <= l < j} V[r][l] R[l][j]) / R[j][j]
+  for (int j = 0; j < K; ++j) {
+    const double inv_jj = 1.0 / fs[j * KP + j];
+    double t[K / kWave];
+#pragma unroll
+    for (int m = 0; m < K / kWave; ++m) {
+      const int r = tid + m * kWave;
+      double acc[NB];
+#pragma unroll
+      for (int q = 0; q < NB; ++q) acc[q] = 0.0;
+      for (int l0 = r; l0 < j; l0 += NB) {
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+          const int l = min(l0 + q, j - 1);
+          const double x = fs[r * KP + l] * fs[l * KP + j];
+          acc[q] += l0 + q < j ? x : 0.0;
+        }
+      }
+      double sum = 0.0;
+#pragma unroll
+      for (int q = 0; q < NB; ++q) sum += acc[q];
+      t[m] = sum;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int m = 0; m < K / kWave; ++m) {
+      const int r = tid + m * kWave;
+      if (r < j) fs[r * KP + j] = -t[m] * inv_jj;
+      if (r == j) fs[j * KP + j] = inv_jj;
+    }
+    __syncthreads();
+  }
+  double* W = a.hmat + (size_t)u * K * K;
+  for (int e = tid; e < K * K; e += kWave) {
+    const int i = e / K, j = e - i * K;
+    W[e] = i <= j ? fs[i * KP + j] : 0.0;
+  }
+}
+
+// k = 64 with every value in registers: lane c holds column c of S (entries k <= c are used), the pivots and the
+// entries of row j of R come from their lanes by readlane, and lane i forms row i of R^{-1} from
+// W[i][j] = -(sum_{i <= l < j} W[i][l] R[l][j]) / R[j][j].  Same arithmetic as cqr_factor, no LDS round trips.
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, lane), hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), lane);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+__global__ __launch_bounds__(kWave) void cqr_factor_reg64(LayerFitArgs a, int shifted) {
+  constexpr int K = 64;
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
+  const int u = blockIdx.x, lane = threadIdx.x;
+  const double* P = a.spart + (size_t)u * nch * K * K;
+  double col[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) col[k] = 0.0;
+  for (int p = 0; p < nch; ++p)
+#pragma unroll
+    for (int k = 0; k < K; ++k) col[k] += P[(size_t)p * K * K + k * K + lane];
+  if (shifted) {
+    double d = 0.0;
+#pragma unroll
+    for (int k = 0; k < K; ++k) d = k == lane ? col[k] : d;
+    double tr = 0.0;
+#pragma unroll
+    for (int c = 0; c < K; ++c) tr += readlane_f64(d, c);
+    const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
+#pragma unroll
+    for (int k = 0; k < K; ++k) col[k] += k == lane ? shift : 0.0;
+  }
+  // entries below the diagonal of a lane's column are updated too but never read
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    const double d = readlane_f64(col[j], j);
+    const double rjj = sqrt(d > 1e-300 ? d : 1e-300);
+    col[j] = lane == j ? rjj : col[j] / rjj;
+#pragma unroll
+    for (int k = j + 1; k < K; ++k) col[k] -= readlane_f64(col[j], k) * col[j];
+  }
+  // terms with l < lane are skipped (selected, so an overflowed entry of R cannot turn 0 * inf into NaN)
+  double w[K];
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    const double rjj = readlane_f64(col[j], j);
+    double s = 0.0;
+#pragma unroll
+    for (int l = 0; l < j; ++l) {
+      const double x = w[l] * readlane_f64(col[l], j);
+      s += lane <= l ? x : 0.0;
+    }
+    w[j] = lane == j ? 1.0 / rjj : (lane < j ? -s / rjj : 0.0);
+  }
+  double* W = a.hmat + (size_t)u * K * K + (size_t)lane * K;
+#pragma unroll
+  for (int j = 0; j < K; ++j) W[j] = w[j];
+}
+
+size_t cqr_factor_lds(int k) { return (size_t)k * (k + 1) * sizeof(double); }
+size_t cqr_apply_lds(int k) {
+  return ((size_t)k * (kCqrRows + 1) + (size_t)kCqrWChunk * k) * sizeof(double);
+}
+
+// dst = (src (+ perturbation)) R^{-1} for 64 features: thread (ti, tj) owns features 4 ti .. 4 ti + 3 and columns
+// tj + 16 n; R^{-1} is streamed through LDS 32 rows at a time.
+template <int K>
+__global__ __launch_bounds__(kCqrThreads) void cqr_apply(LayerFitArgs a, const double* src, double* dst, int perturb,
+                                                          uint32_t round) {
+  constexpr int NJ = K / 16;
+  extern __shared__ double as_[];
+  double* ty = as_;                          // [K][kCqrRows + 1]
+  double* tw = as_ + K * (kCqrRows + 1);     // [kCqrWChunk][K]
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
+  const int f0 = blockIdx.x * kCqrRows, u = blockIdx.y, tid = threadIdx.x, ti = tid / 16, tj = tid % 16;
+  const double* Y = src + (size_t)u * K * DL;
+  const double* W = a.hmat + (size_t)u * K * K;
+  const double eps = perturb ? a.eps[u] : 0.0;
+  for (int e = tid; e < K * kCqrRows; e += kCqrThreads) {
+    const int c = e / kCqrRows, ff = e - c * kCqrRows;
+    const size_t idx = (size_t)c * DL + f0 + ff;
+    const double y = Y[idx];
+    ty[c * (kCqrRows + 1) + ff] = perturb ? cqr_perturbed(y, eps, round, u, idx) : y;
+  }
+  double acc[4][NJ];
+#pragma unroll
+  for (int f = 0; f < 4; ++f)
+#pragma unroll
+    for (int n = 0; n < NJ; ++n) acc[f][n] = 0.0;
+  for (int i0 = 0; i0 < K; i0 += kCqrWChunk) {
+    __syncthreads();
+    for (int e = tid; e < kCqrWChunk * K; e += kCqrThreads) tw[e] = W[(size_t)i0 * K + e];
+    __syncthreads();
+#pragma unroll 4
+    for (int ii = 0; ii < kCqrWChunk; ++ii) {
+      double y4[4], w[NJ];
+#pragma unroll
+      for (int f = 0; f < 4; ++f) y4[f] = ty[(i0 + ii) * (kCqrRows + 1) + 4 * ti + f];
+#pragma unroll
+      for (int n = 0; n < NJ; ++n) w[n] = tw[ii * K + tj + 16 * n];
+#pragma unroll
+      for (int f = 0; f < 4; ++f)
+#pragma unroll
+        for (int n = 0; n < NJ; ++n) acc[f][n] = fma(y4[f], w[n], acc[f][n]);
+    }
+  }
+  double* X = dst + (size_t)u * K * DL;
+#pragma unroll
+  for (int n = 0; n < NJ; ++n)
+#pragma unroll
+    for (int f = 0; f < 4; ++f) X[(size_t)(tj + 16 * n) * DL + f0 + 4 * ti + f] = acc[f][n];
 }
 
 // Rayleigh-Ritz matrix H = (X^T Y + Y^T X) / 2 with Y = G X: one 256-thread workgroup per unit, B x B register
@@ -979,16 +1171,35 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
   hipLaunchKernelGGL(sub_init, dim3((a.k * DL + kLayerThreads - 1) / kLayerThreads, a.num_units),
                      dim3(kLayerThreads), 0, stream, a);
-  const size_t clds = cqr_lds_bytes(a.k);
-  const void* cqr = a.k == 64 ? (const void*)sub_cqr<64> : (const void*)sub_cqr<128>;
-  hipError_t e0 = hipFuncSetAttribute(cqr, hipFuncAttributeMaxDynamicSharedMemorySize, (int)clds);
-  if (e0 != hipSuccess) return e0;
+  const int nch = (DL + kCqrChunk - 1) / kCqrChunk;
+  const size_t flds = cqr_factor_lds(a.k), alds = cqr_apply_lds(a.k);
+  {
+    const void* ap = a.k == 64 ? (const void*)cqr_apply<64> : (const void*)cqr_apply<128>;
+    hipError_t e0 = hipFuncSetAttribute(ap, hipFuncAttributeMaxDynamicSharedMemorySize, (int)alds);
+    if (e0 == hipSuccess && a.k == 128)
+      e0 = hipFuncSetAttribute((const void*)cqr_factor<128>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)flds);
+    if (e0 != hipSuccess) return e0;
+  }
+  const dim3 sgrid(nch, a.num_units), agrid(DL / kCqrRows, a.num_units);
+  auto pass = [&](const double* src, double* dst, int first, uint32_t round) {
+    if (a.k == 64) {
+      hipLaunchKernelGGL(cqr_syrk<64>, sgrid, dim3(kCqrThreads), 0, stream, a, src, first, round);
+      hipLaunchKernelGGL(cqr_factor_reg64, dim3(a.num_units), dim3(kWave), 0, stream, a, first);
+      hipLaunchKernelGGL(cqr_apply<64>, agrid, dim3(kCqrThreads), alds, stream, a, src, dst, first, round);
+    } else {
+      hipLaunchKernelGGL(cqr_syrk<128>, sgrid, dim3(kCqrThreads), 0, stream, a, src, first, round);
+      hipLaunchKernelGGL(cqr_factor<128>, dim3(a.num_units), dim3(kWave), flds, stream, a, first);
+      hipLaunchKernelGGL(cqr_apply<128>, agrid, dim3(kCqrThreads), alds, stream, a, src, dst, first, round);
+    }
+  };
+  // X = orth(Y): the perturbed, shifted pass from Y into X, then the exact pass on X in place
   auto orth = [&](uint32_t round) {
-    if (a.k == 64) hipLaunchKernelGGL(sub_cqr<64>, dim3(a.num_units), dim3(kCqrThreads), clds, stream, a, round);
-    else hipLaunchKernelGGL(sub_cqr<128>, dim3(a.num_units), dim3(kCqrThreads), clds, stream, a, round);
+    hipLaunchKernelGGL(cqr_scale, dim3(a.num_units), dim3(kScaleThreads), 0, stream, a);
+    pass(a.y, a.x, 1, round);
+    pass(a.x, a.x, 0, round);
   };
   orth(0u);
-  const dim3 ggrid(DL / 64, a.k / 64, a.num_units);
+  const dim3 ggrid((DL + kGemmRows - 1) / kGemmRows, a.k / 64, a.num_units);
   for (int it = 0; it < kLayerIters; ++it) {
     hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
     orth((uint32_t)(it + 1));

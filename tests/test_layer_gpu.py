@@ -120,15 +120,17 @@ def _fit_and_compare(w, layers, rank, mode=kvc.KVC_FIT_DELTA):
     assert worst <= TOL_CACHE[dt]
 
 
-@pytest.mark.parametrize("name,layers,rank", [("tiny", 2, 8), ("llama8b_4k", 2, 32), ("llama8b_4k", 1, 48)])
+@pytest.mark.parametrize("name,layers,rank", [("tiny", 2, 8), ("llama8b_4k", 2, 32), ("llama8b_4k", 1, 48),
+                                              ("llama8b_4k", 1, 64)])
 def test_layer_fit_matches_oracle(name, layers, rank):
     _fit_and_compare(synth.WORKLOADS[name].with_(num_layers=layers), layers, rank)
 
 
-# bf16 shapes around the Gram's 128-feature blocks and 256-feature groups: 64-dim heads with a half-filled last block
-# (D = 320: blocks 0-2, groups {0, 1} and {2}), block sizes below 8 and not a power of two (the register Gram),
+# bf16 shapes around the Gram's 128-feature blocks and 256-feature groups: one 64-dim head (D = 64 = k, a single
+# half-filled block), 64-dim heads with a half-filled last block (D = 320: blocks 0-2, groups {0, 1} and {2}), block sizes below 8 and not a power of two (the register Gram),
 # a ragged token count over several token ranges, and base-cache fits (the src side unread).
 @pytest.mark.parametrize("H,d,bs,T,rank,mode", [
+    (1, 64, 16, 300, 8, kvc.KVC_FIT_DELTA),
     (5, 64, 16, 700, 24, kvc.KVC_FIT_DELTA),
     (3, 64, 4, 530, 16, kvc.KVC_FIT_DELTA),
     (2, 128, 12, 610, 16, kvc.KVC_FIT_BASE),
