@@ -12,6 +12,7 @@
 //                converges like (lambda_{k+1} / lambda_r)^iterations.
 //   proj_layer   coef = Z B^T summed over the heads (bf16 MFMA; each head's d columns of B staged hi/lo in LDS).
 #include <algorithm>
+#include <type_traits>
 
 #include "kvc_device.h"
 #include "kvc_launch.h"
@@ -191,16 +192,32 @@ __device__ __forceinline__ int2 gl_blocks(const GLPaging& pg, const int32_t* __r
   return make_int2(table[ok0 ? lb0 : 0], table[ok1 ? lb1 : 0]);
 }
 
-// Element offset of token t + j of the sequence (head 0), -1 past t_end or outside the pool.
-__device__ __forceinline__ int64_t gl_row(const GLPaging& pg, int2 b, int32_t off, int t, int j, int t_end) {
-  const int32_t p = off + t, lb0 = p >> pg.shift, pj = p + j, lb = pj >> pg.shift;
-  const int32_t blk = lb == lb0 ? b.x : b.y;
-  const bool ok = (t + j < t_end) & (blk >= 0) & (blk < pg.num_blocks);
-  const int64_t o = (int64_t)(ok ? blk : 0) * pg.block_stride + (int64_t)(pj - (lb << pg.shift)) * pg.token_stride;
-  return ok ? o : -1;
+// Rows of the 8 tokens t .. t + 7 of a sequence (head 0): the first n0 lie in block entry b.x from slot k0 on, the
+// rest in b.y from slot 0, so row j starts at base0 + j * token_stride (j < n0) or base1 + j * token_stride.  Bit j
+// of valid: token t + j lies before t_end in a block inside the pool.
+struct GLRows {
+  int64_t base0, base1;
+  int32_t n0;
+  uint32_t valid;
+};
+__device__ __forceinline__ GLRows gl_rows(const GLPaging& pg, int2 b, int32_t off, int t, int t_end) {
+  GLRows r;
+  const int32_t p = off + t, k0 = p & ((1 << pg.shift) - 1);
+  r.n0 = min(8, (1 << pg.shift) - k0);
+  const bool ok0 = (b.x >= 0) & (b.x < pg.num_blocks), ok1 = (b.y >= 0) & (b.y < pg.num_blocks);
+  r.base0 = ok0 ? (int64_t)b.x * pg.block_stride + (int64_t)k0 * pg.token_stride : 0;
+  r.base1 = ok1 ? (int64_t)b.y * pg.block_stride - (int64_t)r.n0 * pg.token_stride : 0;
+  const int in_seq = min(8, max(0, t_end - t));
+  const uint32_t seq = (1u << in_seq) - 1u, first = (1u << r.n0) - 1u;
+  r.valid = seq & ((ok0 ? first : 0u) | (ok1 ? ~first & 0xffu : 0u));
+  return r;
 }
 
-template <int D, bool DELTA>
+// Zero page the LDS Gram reads in place of a missing row (never written): covers a row's lane offsets up to this size.
+constexpr int kGLZeroBytes = 65536;
+__device__ __attribute__((aligned(256))) uint32_t gl_zero_page[kGLZeroBytes / 4];
+
+template <int D, bool DELTA, bool FULL>
 __global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, int num_pairs, int num_groups) {
   extern __shared__ __attribute__((aligned(16))) u32x4 gl_lds[];
   const int H = a.pv.num_kv_heads, DL = H * D, NB = (DL + 127) / 128;
@@ -231,15 +248,18 @@ __global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, in
   pg.token_stride = a.pv.token_stride;
   pg.shift = a.pv.block_shift;
   pg.num_blocks = a.pv.num_blocks;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index (and every value derived from it alone) is uniform: row addressing runs on the scalar unit
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   // producer: slots 4q .. 4q + 3 (group g1 below slot 256, g2 above; a diagonal pair uses g1's only), tokens
-  // 8 tg .. 8 tg + 7 of the step
-  const int q = tid & 127, tg = tid >> 7, slot = 4 * q;
+  // 8 tg .. 8 tg + 7 of the step; a wave's lanes share tg and cover 256 consecutive slots
+  const int q = tid & 127, tg = wave >> 1, slot = 4 * q;
   const int fglob = slot < 256 ? g1 * 256 + slot : g2 * 256 + slot - 256;
-  const bool pact = !diag || q < 64;
+  const bool pact = !diag || (wave & 1) == 0;
   const bool inrange = pact && fglob < DL;
-  const int64_t fofs = inrange ? (int64_t)(fglob / D) * a.pv.head_stride + fglob % D : 0;
+  // byte offset of the lane's 4 features within a token's row (the launcher checks it fits 32 bits)
+  const uint32_t fbytes = inrange ? 2u * (uint32_t)((fglob / D) * a.pv.head_stride + fglob % D) : 0u;
 
   // consumer: wave = 2 x block pair (i1, i2) + row half
   const int bp = wave >> 1, half = wave & 1, i1 = bp >> 1, i2 = bp & 1;
@@ -255,35 +275,58 @@ __global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, in
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   uint2 rd[8], rs[8];
-  uint32_t present = 0;  // bit j: dst row j of the step exists, bit 8 + j: src row j
-  // row loads of one step; a missing row loads the pool's first element and is zeroed when used, so no register
-  // with a load in flight is written
+  uint32_t present = 0;  // (uniform) bit j: dst row j of the step exists, bit 8 + j: src row j
+  // row loads of one step: a uniform row pointer plus the lane's byte offset.  A missing row (or a lane past D) loads
+  // from the pool's first row and is zeroed when used, so no register with a load in flight is written.
   auto issue = [&](int t0, int2 bd, int2 bs) {
     const int t = t0 + 8 * tg;
-    uint32_t m = 0;
+    const uint32_t fb = fbytes;
+    // every row address stays inside the pool (a block holds at least 8 token rows); rows that do not exist are
+    // dropped through `present` when used
+    auto rows = [&](const GLRows& x, uint2* dstv) {
+      if (x.n0 == 8) {  // the 8 tokens share one block
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int64_t od = gl_row(pg, bd, doff, t, j, t_end);
-      const bool okd = inrange & (od >= 0);
-      rd[j] = *reinterpret_cast<const uint2*>(pool + (okd ? od + fofs : 0));
-      m |= okd ? 1u << j : 0u;
-      if constexpr (DELTA) {
-        const int64_t os = gl_row(pg, bs, soff, t, j, t_end);
-        const bool oks = inrange & (os >= 0);
-        rs[j] = *reinterpret_cast<const uint2*>(pool + (oks ? os + fofs : 0));
-        m |= oks ? 1u << (8 + j) : 0u;
+        for (int j = 0; j < 8; ++j)
+          dstv[j] = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(pool + x.base0 + j * pg.token_stride) + fb);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int64_t o = (j < x.n0 ? x.base0 : x.base1) + j * pg.token_stride;
+          dstv[j] = *reinterpret_cast<const uint2*>(reinterpret_cast<const char*>(pool + o) + fb);
+        }
       }
+    };
+    const GLRows xd = gl_rows(pg, bd, doff, t, t_end);
+    rows(xd, rd);
+    uint32_t m = xd.valid;
+    if constexpr (DELTA) {
+      const GLRows xs = gl_rows(pg, bs, soff, t, t_end);
+      rows(xs, rs);
+      m |= xs.valid << 8;
     }
     present = m;
   };
-  // Z hi/lo of the loaded rows, transposed into one step's LDS buffer
-  auto produce = [&](u32x4* buf) {
+  // Z hi/lo of the loaded rows, transposed into one step's LDS buffer.  MASKED drops rows that do not exist and lanes
+  // past D; a step whose 8 (16) rows all exist in a wave wholly inside D skips it.
+  const bool wave_inside = pact && ((wave & 1) ? g2 : g1) * 256 + 256 <= DL;
+  const uint32_t all_rows = DELTA ? 0xffffu : 0xffu;
+  auto produce = [&](u32x4* buf, auto masked) {
+    constexpr bool MASKED = decltype(masked)::value;
     uint32_t hi[8][2], lo[8][2];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const bool pd = (present >> j) & 1u, ps = DELTA && ((present >> (8 + j)) & 1u);
-      const uint32_t dx = pd ? rd[j].x : 0u, dy = pd ? rd[j].y : 0u;
-      const uint32_t sx = ps ? rs[j].x : 0u, sy = ps ? rs[j].y : 0u;
+      uint32_t dx = rd[j].x, dy = rd[j].y, sx = 0u, sy = 0u;
+      if constexpr (DELTA) {
+        sx = rs[j].x;
+        sy = rs[j].y;
+      }
+      if constexpr (MASKED) {
+        const bool pd = inrange && ((present >> j) & 1u), ps = DELTA && inrange && ((present >> (8 + j)) & 1u);
+        dx = pd ? dx : 0u;
+        dy = pd ? dy : 0u;
+        sx = ps ? sx : 0u;
+        sy = ps ? sy : 0u;
+      }
       split_bf16x2(bf16_lo_to_f32(dx) - bf16_lo_to_f32(sx), bf16_hi_to_f32(dx) - bf16_hi_to_f32(sx), hi[j][0],
                    lo[j][0]);
       split_bf16x2(bf16_lo_to_f32(dy) - bf16_lo_to_f32(sy), bf16_hi_to_f32(dy) - bf16_hi_to_f32(sy), hi[j][1],
@@ -301,6 +344,10 @@ __global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, in
       buf[tg * kGLSlots + gl_swz(slot + f)] = ch;
       buf[(4 + tg) * kGLSlots + gl_swz(slot + f)] = cl;
     }
+  };
+  auto produce_step = [&](u32x4* buf) {
+    if (wave_inside && present == all_rows) produce(buf, std::false_type{});
+    else produce(buf, std::true_type{});
   };
   // the wave's 32 tiles of one step
   auto products = [&](const u32x4* buf) {
@@ -325,31 +372,67 @@ __global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, in
   };
 
   const int nsteps = (t_end - t_begin + kGLStep - 1) / kGLStep;
-  int2 td = make_int2(-1, -1), ts = make_int2(-1, -1);
-  if (pact) {
-    td = gl_blocks(pg, dst_tab, doff, t_begin + 8 * tg, t_end);
-    if constexpr (DELTA) ts = gl_blocks(pg, src_tab, soff, t_begin + 8 * tg, t_end);
-    issue(t_begin, td, ts);
-    if (nsteps > 1) {
-      td = gl_blocks(pg, dst_tab, doff, t_begin + kGLStep + 8 * tg, t_end);
-      if constexpr (DELTA) ts = gl_blocks(pg, src_tab, soff, t_begin + kGLStep + 8 * tg, t_end);
-    }
-    produce(gl_lds);
-  }
-  __syncthreads();
-  for (int s = 0; s < nsteps; ++s) {
-    const bool more = s + 1 < nsteps;
-    if (pact && more) {
-      const int t1 = t_begin + (s + 1) * kGLStep;
-      issue(t1, td, ts);
-      if (s + 2 < nsteps) {
-        td = gl_blocks(pg, dst_tab, doff, t1 + kGLStep + 8 * tg, t_end);
-        if constexpr (DELTA) ts = gl_blocks(pg, src_tab, soff, t1 + kGLStep + 8 * tg, t_end);
+  int2 td = make_int2(-1, -1), ts = make_int2(-1, -1);  // table entries of the next step to issue
+  auto tables = [&](int k) {
+    td = gl_blocks(pg, dst_tab, doff, t_begin + k * kGLStep + 8 * tg, t_end);
+    if constexpr (DELTA) ts = gl_blocks(pg, src_tab, soff, t_begin + k * kGLStep + 8 * tg, t_end);
+  };
+  auto issue_step = [&](int k) {
+    issue(t_begin + k * kGLStep, td, ts);
+    if (k + 1 < nsteps) tables(k + 1);
+  };
+  // rows of step k (any k: past the sequence every row is missing) with missing rows read from the zero page, then
+  // the table entries of step k + 1
+  auto issue_zero = [&](int k) {
+    const int t = t_begin + k * kGLStep + 8 * tg;
+    const char* zero = reinterpret_cast<const char*>(gl_zero_page);
+    auto rows = [&](const GLRows& x, uint2* dstv) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int64_t o = (j < x.n0 ? x.base0 : x.base1) + j * pg.token_stride;
+        const char* row = (x.valid >> j) & 1u ? reinterpret_cast<const char*>(pool + o) : zero;
+        dstv[j] = *reinterpret_cast<const uint2*>(row + fbytes);
       }
-    }
-    if (job) products(gl_lds + (s & 1) * kGLBufChunks);
-    if (pact && more) produce(gl_lds + ((s + 1) & 1) * kGLBufChunks);
+    };
+    rows(gl_rows(pg, td, doff, t, t_end), rd);
+    if constexpr (DELTA) rows(gl_rows(pg, ts, soff, t, t_end), rs);
+    tables(k + 1);
+  };
+  if constexpr (FULL) {
+    // every lane lies inside D and a missing row reads the zero page: one straight-line body per step, products of
+    // step s, then the rows of step s + 1 (loaded one step earlier), then the loads of step s + 2.  Waves without a
+    // block (diagonal pairs) run the products too and drop them; rows past the sequence load zeros.
+    tables(0);
+    issue_zero(0);
+    produce(gl_lds, std::false_type{});
+    issue_zero(1);
     __syncthreads();
+    for (int s = 0; s < nsteps; ++s) {
+      products(gl_lds + (s & 1) * kGLBufChunks);
+      produce(gl_lds + ((s + 1) & 1) * kGLBufChunks, std::false_type{});
+      // each of the 96 MFMAs followed by a share of the VALU work of the next step's rows
+#pragma unroll
+      for (int q = 0; q < 96; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
+      }
+      issue_zero(s + 2);
+      __syncthreads();
+    }
+  } else {
+    if (pact) {
+      tables(0);
+      issue_step(0);
+      produce_step(gl_lds);
+    }
+    __syncthreads();
+    for (int s = 0; s < nsteps; ++s) {
+      const bool more = s + 1 < nsteps;
+      if (pact && more) issue_step(s + 1);
+      if (job) products(gl_lds + (s & 1) * kGLBufChunks);
+      if (pact && more) produce_step(gl_lds + ((s + 1) & 1) * kGLBufChunks);
+      __syncthreads();
+    }
   }
 
   if (!job) return;
@@ -1136,19 +1219,32 @@ __global__ __launch_bounds__(kLayerThreads) void proj_layer_f32(LayerFitArgs a) 
 hipError_t launch_layer_gram(const LayerFitArgs& a, kvc_dtype dtype, hipStream_t stream) {
   const int D = a.pv.head_dim, H = a.pv.num_kv_heads, DL = H * D;
   int upper_only = 0;
-  if (dtype == KVC_BF16 && a.pv.block_shift >= 3) {
+  // the LDS Gram addresses a lane's features within a row by a 32-bit byte offset
+  const bool small_rows = 2 * ((int64_t)(H - 1) * a.pv.head_stride + D) < ((int64_t)1 << 31);
+  if (dtype == KVC_BF16 && a.pv.block_shift >= 3 && small_rows) {
     const int NB = (DL + 127) / 128, NG = (NB + 1) / 2, pairs = NG * (NG + 1) / 2;
     const unsigned nwork = (unsigned)a.num_units * a.max_parts * pairs;
     const bool delta = a.mode == KVC_FIT_DELTA;
-    const void* fn = D == 64 ? (delta ? (const void*)gram_layer_bf16<64, true> : (const void*)gram_layer_bf16<64, false>)
-                             : (delta ? (const void*)gram_layer_bf16<128, true> : (const void*)gram_layer_bf16<128, false>);
-    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGLLdsBytes);
+    // straight-line variant: every producing lane inside D and a row's lane offsets inside the zero page
+    const bool full = DL % 256 == 0 && 2 * ((int64_t)(H - 1) * a.pv.head_stride + D) <= kGLZeroBytes;
+    const int variant = (D == 64 ? 0 : 4) + (delta ? 2 : 0) + (full ? 1 : 0);
+    const void* fns[8] = {(const void*)gram_layer_bf16<64, false, false>, (const void*)gram_layer_bf16<64, false, true>,
+                          (const void*)gram_layer_bf16<64, true, false>,  (const void*)gram_layer_bf16<64, true, true>,
+                          (const void*)gram_layer_bf16<128, false, false>, (const void*)gram_layer_bf16<128, false, true>,
+                          (const void*)gram_layer_bf16<128, true, false>,  (const void*)gram_layer_bf16<128, true, true>};
+    hipError_t e = hipFuncSetAttribute(fns[variant], hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGLLdsBytes);
     if (e != hipSuccess) return e;
     const dim3 grid(nwork), block(kGLThreads);
-    if (D == 64 && delta) hipLaunchKernelGGL((gram_layer_bf16<64, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG);
-    else if (D == 64) hipLaunchKernelGGL((gram_layer_bf16<64, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG);
-    else if (delta) hipLaunchKernelGGL((gram_layer_bf16<128, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG);
-    else hipLaunchKernelGGL((gram_layer_bf16<128, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG);
+    switch (variant) {
+      case 0: hipLaunchKernelGGL((gram_layer_bf16<64, false, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
+      case 1: hipLaunchKernelGGL((gram_layer_bf16<64, false, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
+      case 2: hipLaunchKernelGGL((gram_layer_bf16<64, true, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
+      case 3: hipLaunchKernelGGL((gram_layer_bf16<64, true, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
+      case 4: hipLaunchKernelGGL((gram_layer_bf16<128, false, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
+      case 5: hipLaunchKernelGGL((gram_layer_bf16<128, false, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
+      case 6: hipLaunchKernelGGL((gram_layer_bf16<128, true, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
+      default: hipLaunchKernelGGL((gram_layer_bf16<128, true, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
+    }
     upper_only = 1;
   } else if (dtype == KVC_BF16) {
     dim3 grid((a.max_parts + kLayerWaves / 2 - 1) / (kLayerWaves / 2), H * (H + 1) / 2, a.num_units);
