@@ -5,7 +5,7 @@
 //             token chunk.  bf16 coefficients are exact MFMA operands; fp32 ones use the bf16 hi/lo split.
 //   assemble  G = K H K^T in fp64 (d x d), the Gram of M.
 //   eig       the shared eigensolver: top r_out eigenvectors R of G, sigma = sqrt(lambda) -> out.basis, out.sigma.
-//   ymat      Y = K^T R (m x r_out), so that the new coefficients are M R = A Y.
+//   ymat      Y = K^T R (m x r_out), so that the new coefficients are M R = A Y (operands staged in LDS).
 //   cproj     A_out = A Y, a second pass over the coefficient rows on MFMA (Y as a bf16 hi/lo pair).
 #include <utility>
 
@@ -381,6 +381,40 @@ __global__ __launch_bounds__(kChainThreads) void chain_ymat(ChainArgs a) {
   }
 }
 
+// The same product with K^T and R^T staged in LDS (rows padded to d + 1 floats): lanes take consecutive output
+// columns k of one row l, so the R^T reads fall in distinct banks and the K^T read is a broadcast; the sums run
+// over f in the same order as chain_ymat (identical results).
+__global__ __launch_bounds__(kChainThreads) void chain_ymat_lds(ChainArgs a) {
+  extern __shared__ float s_ym[];
+  const int u = blockIdx.x;
+  const ChainUnit cu = chain_unit(a, u);
+  const int m = a.first.rank + a.second.rank, ro = a.out.rank, d = a.first.head_dim, dp = d + 1;
+  const float* Bo = a.out.basis + cu.idx * (int64_t)ro * d;
+  float* Ks = s_ym;
+  float* Rs = s_ym + m * dp;
+  for (int e = threadIdx.x; e < m * d; e += kChainThreads) {
+    const int l = e / d, f = e - l * d;
+    Ks[l * dp + f] = cat_basis(a, cu.idx, l, f);
+  }
+  for (int e = threadIdx.x; e < ro * d; e += kChainThreads) {
+    const int k = e / d, f = e - k * d;
+    Rs[k * dp + f] = Bo[e];
+  }
+  __syncthreads();
+  float* Y = a.ymat + (size_t)u * m * ro;
+  for (int e = threadIdx.x; e < m * ro; e += kChainThreads) {
+    const int l = e / ro, k = e - l * ro;
+    const float* kr = Ks + l * dp;
+    const float* rr = Rs + k * dp;
+    double s = 0.0;
+#pragma unroll 8
+    for (int f = 0; f < d; ++f) s += (double)kr[f] * (double)rr[f];
+    Y[e] = (float)s;
+  }
+}
+
+size_t chain_ymat_lds_bytes(int m, int ro, int d) { return (size_t)(m + ro) * (d + 1) * sizeof(float); }
+
 // ---------------------------------------------------------------------------------------------------------------
 // cproj: A_out = [A1 A2] Y on MFMA.  M = output rank (16 per tile), N = token (16), K = concatenated rank (32 per
 // step).  Y^T is staged in LDS as a bf16 hi/lo pair; the coefficient rows are the B operand.
@@ -566,7 +600,14 @@ hipError_t launch_chain(const ChainArgs& a, const EigArgs& ea, hipStream_t strea
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if ((e = launch_eig(ea, stream)) != hipSuccess) return e;
-  hipLaunchKernelGGL(chain_ymat, dim3(a.num_units), dim3(kChainThreads), 0, stream, a);
+  const size_t ylds = chain_ymat_lds_bytes(m, a.out.rank, d);
+  if (ylds <= 160 * 1024) {
+    e = hipFuncSetAttribute((const void*)chain_ymat_lds, hipFuncAttributeMaxDynamicSharedMemorySize, (int)ylds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(chain_ymat_lds, dim3(a.num_units), dim3(kChainThreads), ylds, stream, a);
+  } else {
+    hipLaunchKernelGGL(chain_ymat, dim3(a.num_units), dim3(kChainThreads), 0, stream, a);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int mtr = (a.out.rank + 15) / 16;
   const int mtr_inst = mtr <= 2 ? mtr : (mtr <= 4 ? 4 : 8);
