@@ -65,10 +65,11 @@ def _plant_layer_base(pc, dst, rank, seed):
             pool[bd, sd] = x.reshape(T, H, d).to(pool.dtype).to(pool.device)
 
 
-def _fit_and_compare(w, layers, rank, mode=kvc.KVC_FIT_DELTA):
+def _fit_and_compare(w, layers, rank, mode=kvc.KVC_FIT_DELTA, lead_slots=()):
     """Fit a per-layer state on the GPU and in the oracle and compare sigma, A B per unit, the basis's
-    orthonormality and (delta mode) the cache materialised from it."""
-    pc = synth.build_paged(w, device="cuda", num_output_agents=1)
+    orthonormality and (delta mode) the cache materialised from it.  lead_slots offsets the sequences inside their
+    first block (groups of 8 tokens then straddle two blocks)."""
+    pc = synth.build_paged(w, device="cuda", num_output_agents=1, lead_slots=lead_slots)
     H, d = w.num_kv_heads, w.head_dim
     src, dst, out = pc.seqs[(0, 0)], pc.seqs[(0, 1)], pc.seqs[(0, 100)]
     if mode == kvc.KVC_FIT_DELTA:
@@ -140,6 +141,14 @@ def test_layer_fit_shapes(H, d, bs, T, rank, mode):
     w = synth.WORKLOADS["llama8b_4k"].with_(num_layers=1, num_kv_heads=H, head_dim=d, block_size=bs, seq_tokens=(T,),
                                             num_agents=2)
     _fit_and_compare(w, 1, rank, mode)
+
+
+# sequences that start inside a block at offsets that are not multiples of 8 (src 3, dst 11, output 6): the Gram's
+# groups of 8 tokens straddle two blocks, in the straight-line path (D = 1024) and in the masked one (D = 320)
+@pytest.mark.parametrize("H,d,T,rank", [(8, 128, 900, 32), (5, 64, 700, 24)])
+def test_layer_fit_unaligned_offsets(H, d, T, rank):
+    w = synth.WORKLOADS["llama8b_4k"].with_(num_layers=1, num_kv_heads=H, head_dim=d, seq_tokens=(T,), num_agents=2)
+    _fit_and_compare(w, 1, rank, lead_slots=(3, 11, 6))
 
 
 @pytest.mark.parametrize("name,layers,rank,Ts", [("tiny", 2, 8, 200), ("llama8b_4k", 2, 32, 3001)])
