@@ -299,8 +299,8 @@ def cpu_baseline(pc, w, sample_layers=(0, 1)):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=6)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama8b_32k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--anchor-workload", default="llama8b_4k",
@@ -321,6 +321,7 @@ def main():
               f"{args.gpus}).", file=sys.stderr)
         return 2
 
+    import numpy as np
     import torch
     from paper_2609_34060_amd import kvc, synth
 
@@ -384,9 +385,14 @@ def main():
         step(args.warmup + k, evs[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    fit_ms = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
-    chain_ms = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
-    apply_ms = sum(e[2].elapsed_time(e[3]) for e in evs) / args.steps
+    fit_all = [e[0].elapsed_time(e[1]) for e in evs]
+    chain_all = [e[1].elapsed_time(e[2]) for e in evs]
+    apply_all = [e[2].elapsed_time(e[3]) for e in evs]
+    fit_ms, chain_ms, apply_ms = (sum(x) / args.steps for x in (fit_all, chain_all, apply_all))
+
+    def pct(x):
+        q = np.percentile(np.asarray(x), [10, 50, 90])
+        return [round(float(v), 4) for v in q]
 
     apply_b = _apply_bytes(L, H, d, T, r)
     apply_gbps = apply_b / (apply_ms * 1e-3) / 1e9
@@ -415,6 +421,7 @@ def main():
         "apply_ms": round(apply_ms, 4),
         "fit_ms": round(fit_ms, 4),
         "chain_ms": round(chain_ms, 4),
+        "ms_p10_p50_p90": {"apply": pct(apply_all), "fit": pct(fit_all), "chain": pct(chain_all)},
         "fit_token_layers_per_s": round(fit_tl, 1),
         "fit_gbps_two_pass": round(_fit_bytes(L, H, d, T, r) / (fit_ms * 1e-3) / 1e9, 2),
         "roofline": {"bound": "hbm", "achieved": round(apply_gbps, 2), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
