@@ -584,12 +584,14 @@ __global__ __launch_bounds__(kFitThreads) void gram_f32_valu(FitArgs a) {
 
 constexpr int kProjTilesPerWave = 16;
 constexpr int kProjChunk = kFitWaves * kProjTilesPerWave * 16;
+constexpr bool kProjRegFrags = false;  // basis fragments held in registers (ranks up to 32) or read from LDS per tile
+constexpr bool kProjPrefetch = false;  // the next tile's rows are loaded before this tile's products
 
 template <int D, int MTR, bool ROPE>
 __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
   constexpr int KS = D / 32;          // K-steps over features
   constexpr int RP = MTR * 16;        // padded rank
-  constexpr bool kRegFrags = MTR <= 2;
+  constexpr bool kRegFrags = kProjRegFrags && MTR <= 2;
   constexpr int FM = kRegFrags ? MTR : 1, FK = kRegFrags ? KS : 1;
   __shared__ __attribute__((aligned(16))) uint16_t s_hi[RP * D];
   __shared__ __attribute__((aligned(16))) uint16_t s_lo[RP * D];
@@ -639,20 +641,31 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
       }
   }
 
-  for (int j = 0; j < kProjTilesPerWave; ++j) {
-    const int t0 = t_begin + (j * kFitWaves + wave) * 16;
-    if (t0 >= Ts) break;
-    const int t = t0 + n;
+  // Rows of tile j: the dst (and src) row of token t0 + n, features 32 ks + 8 g .. + 7; lanes past T_s load nothing.
+  struct Rows {
+    u32x4 d[KS], s[KS];
+  };
+  auto load_rows = [&](int j, Rows& R) {
+    const int t = t_begin + (j * kFitWaves + wave) * 16 + n;
     const bool valid = t < Ts;
     const int64_t od = valid ? row_offset(a.pv, dst_tab, itp->dst_offset, t, f.head) : -1;
     const int64_t os = (valid && delta) ? row_offset(a.pv, src_tab, itp->src_offset, t, f.head) : -1;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      R.d[ks] = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+      R.s[ks] = os >= 0 ? *reinterpret_cast<const u32x4*>(pool + os + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+    }
+  };
+  // Z hi/lo of tile j, its products with the basis, the coefficient rows.
+  auto finish = [&](int j, const Rows& R) {
+    const int t = t_begin + (j * kFitWaves + wave) * 16 + n;
+    const bool valid = t < Ts;
     bf16x8 zh[KS], zl[KS];
     if (ROPE && rope) {
       f32x4 dv[2 * KS], sv[2 * KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const u32x4 d = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
-        const u32x4 s = os >= 0 ? *reinterpret_cast<const u32x4*>(pool + os + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+        const u32x4 d = R.d[ks], s = R.s[ks];
         dv[2 * ks] = f32x4{bf16_lo_to_f32(d[0]), bf16_hi_to_f32(d[0]), bf16_lo_to_f32(d[1]), bf16_hi_to_f32(d[1])};
         dv[2 * ks + 1] = f32x4{bf16_lo_to_f32(d[2]), bf16_hi_to_f32(d[2]), bf16_lo_to_f32(d[3]), bf16_hi_to_f32(d[3])};
         sv[2 * ks] = f32x4{bf16_lo_to_f32(s[0]), bf16_hi_to_f32(s[0]), bf16_lo_to_f32(s[1]), bf16_hi_to_f32(s[1])};
@@ -665,9 +678,9 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
         u32x4 hw, lw;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-          const int j = 2 * ks + (w >> 1), e = 2 * (w & 1);
+          const int jj = 2 * ks + (w >> 1), e = 2 * (w & 1);
           uint32_t hh, ll;
-          split_bf16x2(dv[j][e] - sv[j][e], dv[j][e + 1] - sv[j][e + 1], hh, ll);
+          split_bf16x2(dv[jj][e] - sv[jj][e], dv[jj][e + 1] - sv[jj][e + 1], hh, ll);
           hw[w] = hh;
           lw[w] = ll;
         }
@@ -676,23 +689,22 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
       }
     } else {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const u32x4 d = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
-      const u32x4 s = os >= 0 ? *reinterpret_cast<const u32x4*>(pool + os + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
-      u32x4 hw, lw;
+      for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 d = R.d[ks], s = R.s[ks];
+        u32x4 hw, lw;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const float z0 = bf16_lo_to_f32(d[w]) - bf16_lo_to_f32(s[w]);
-        const float z1 = bf16_hi_to_f32(d[w]) - bf16_hi_to_f32(s[w]);
-        uint32_t h0, l0, h1, l1;
-        split_bf16(z0, h0, l0);
-        split_bf16(z1, h1, l1);
-        hw[w] = h0 | (h1 << 16);
-        lw[w] = l0 | (l1 << 16);
+        for (int w = 0; w < 4; ++w) {
+          const float z0 = bf16_lo_to_f32(d[w]) - bf16_lo_to_f32(s[w]);
+          const float z1 = bf16_hi_to_f32(d[w]) - bf16_hi_to_f32(s[w]);
+          uint32_t h0, l0, h1, l1;
+          split_bf16(z0, h0, l0);
+          split_bf16(z1, h1, l1);
+          hw[w] = h0 | (h1 << 16);
+          lw[w] = l0 | (l1 << 16);
+        }
+        zh[ks] = as_bf16x8(hw);
+        zl[ks] = as_bf16x8(lw);
       }
-      zh[ks] = as_bf16x8(hw);
-      zl[ks] = as_bf16x8(lw);
-    }
     }
 #pragma unroll
     for (int mt = 0; mt < MTR; ++mt) {
@@ -727,6 +739,25 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
             if (k0 + i < r) cp[i] = (uint16_t)f32_to_bf16_bits(acc[i]);
         }
       }
+    }
+  };
+
+  auto tile_start = [&](int j) { return t_begin + (j * kFitWaves + wave) * 16; };
+  if constexpr (kProjPrefetch) {
+    Rows cur, nxt;
+    load_rows(0, cur);
+    for (int j = 0; j < kProjTilesPerWave; ++j) {
+      if (tile_start(j) >= Ts) break;
+      if (j + 1 < kProjTilesPerWave && tile_start(j + 1) < Ts) load_rows(j + 1, nxt);
+      finish(j, cur);
+      cur = nxt;
+    }
+  } else {
+    for (int j = 0; j < kProjTilesPerWave; ++j) {
+      if (tile_start(j) >= Ts) break;
+      Rows cur;
+      load_rows(j, cur);
+      finish(j, cur);
     }
   }
 }

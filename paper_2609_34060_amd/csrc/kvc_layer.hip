@@ -1065,13 +1065,15 @@ __global__ __launch_bounds__(kLayerThreads) void sub_basis(LayerFitArgs a) {
 // Projection coef = Z B^T over the heads
 // ---------------------------------------------------------------------------------------------------------------
 
-constexpr int kPLTiles = 4;                               // 16-token tiles per wave
-constexpr int kPLChunk = kLayerWaves * kPLTiles * 16;     // 256 tokens per workgroup
+constexpr int kPLTiles = 2;                               // 16-token tiles per wave
+constexpr int kPLWaves = 8;                               // waves per workgroup
+constexpr int kPLThreads = kPLWaves * kWave;
+constexpr int kPLChunk = kPLWaves * kPLTiles * 16;        // tokens per workgroup
 
 // bf16: per head h the d columns of B (rank rows padded to RP = 16 MTR) are staged hi/lo in LDS (two buffers), the
 // rows of h are read in MFMA B-operand layout and Z split hi/lo; the coefficient tiles accumulate over the heads.
 template <int D, int MTR>
-__global__ __launch_bounds__(kLayerThreads) void proj_layer_bf16(LayerFitArgs a) {
+__global__ __launch_bounds__(kPLThreads) void proj_layer_bf16(LayerFitArgs a) {
   constexpr int KS = D / 32, RP = MTR * 16;
   extern __shared__ __attribute__((aligned(16))) unsigned char layer_lds[];
   uint16_t* s_b = reinterpret_cast<uint16_t*>(layer_lds);  // [2][hi, lo][RP][D]
@@ -1101,7 +1103,7 @@ __global__ __launch_bounds__(kLayerThreads) void proj_layer_bf16(LayerFitArgs a)
   for (int h = 0; h < H; ++h) {
     uint16_t* s_hi = s_b + (h & 1) * 2 * RP * D;
     uint16_t* s_lo = s_hi + RP * D;
-    for (int e = tid; e < RP * D; e += kLayerThreads) {
+    for (int e = tid; e < RP * D; e += kPLThreads) {
       const int kk = e / D, f = e - kk * D;
       const float x = kk < r ? basis[(int64_t)kk * DL + h * D + f] : 0.f;
       uint32_t hb, lb;
@@ -1112,7 +1114,7 @@ __global__ __launch_bounds__(kLayerThreads) void proj_layer_bf16(LayerFitArgs a)
     __syncthreads();  // head h's columns are staged; the other buffer (head h - 1) is still read until here
 #pragma unroll
     for (int j = 0; j < kPLTiles; ++j) {
-      const int t0 = t_begin + (j * kLayerWaves + wave) * 16;
+      const int t0 = t_begin + (j * kPLWaves + wave) * 16;
       if (t0 >= Ts) continue;  // uniform over the wave
       const int t = t0 + n;
       const bool valid = t < Ts;
@@ -1151,7 +1153,7 @@ __global__ __launch_bounds__(kLayerThreads) void proj_layer_bf16(LayerFitArgs a)
   }
 #pragma unroll
   for (int j = 0; j < kPLTiles; ++j) {
-    const int t = t_begin + (j * kLayerWaves + wave) * 16 + n;
+    const int t = t_begin + (j * kPLWaves + wave) * 16 + n;
     if (t >= Ts) continue;
 #pragma unroll
     for (int mt = 0; mt < MTR; ++mt) {
@@ -1328,10 +1330,10 @@ static hipError_t launch_proj_layer_bf16(const LayerFitArgs& a, dim3 grid, size_
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   switch (mtr <= 1 ? 1 : mtr <= 2 ? 2 : mtr <= 4 ? 4 : 8) {
-    case 1: hipLaunchKernelGGL((proj_layer_bf16<D, 1>), grid, dim3(kLayerThreads), lds, stream, a); break;
-    case 2: hipLaunchKernelGGL((proj_layer_bf16<D, 2>), grid, dim3(kLayerThreads), lds, stream, a); break;
-    case 4: hipLaunchKernelGGL((proj_layer_bf16<D, 4>), grid, dim3(kLayerThreads), lds, stream, a); break;
-    default: hipLaunchKernelGGL((proj_layer_bf16<D, 8>), grid, dim3(kLayerThreads), lds, stream, a); break;
+    case 1: hipLaunchKernelGGL((proj_layer_bf16<D, 1>), grid, dim3(kPLThreads), lds, stream, a); break;
+    case 2: hipLaunchKernelGGL((proj_layer_bf16<D, 2>), grid, dim3(kPLThreads), lds, stream, a); break;
+    case 4: hipLaunchKernelGGL((proj_layer_bf16<D, 4>), grid, dim3(kPLThreads), lds, stream, a); break;
+    default: hipLaunchKernelGGL((proj_layer_bf16<D, 8>), grid, dim3(kPLThreads), lds, stream, a); break;
   }
   return hipGetLastError();
 }
