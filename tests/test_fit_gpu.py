@@ -128,6 +128,31 @@ def test_fit_bf16_paged_ragged_prefix(rank):
     assert teeth > 10 * TOL_CACHE["bf16"]
 
 
+# Per-head bf16 fit and apply over the shapes the 8B workloads do not reach: head_dim 64, blocks of 8, 12 and 32
+# tokens, contiguous rows, an odd head count and ranks that are not multiples of 8 or 4 (each selects a different
+# kernel or addressing path).
+@pytest.mark.parametrize("d,bs,paged,H,rank,T,Ts,lead", [
+    (64, 16, True, 2, 16, 700, 650, (0, 5, 9)),       # head_dim 64 kernels
+    (128, 8, True, 2, 32, 530, 530, (0, 3, 6)),       # 8-token blocks: the register-loaded Gram
+    (128, 32, True, 2, 24, 1000, 990, (0, 17, 30)),   # 32-token blocks; rank not a multiple of 8
+    (128, 12, True, 2, 16, 400, 400, (0, 7, 11)),     # block size not a power of two (division addressing)
+    (64, 16, False, 2, 8, 300, 300, (0, 4)),          # contiguous rows, head_dim 64
+    (128, 16, False, 2, 40, 600, 577, (0, 5)),        # contiguous rows, two 32-rank steps in apply
+    (128, 16, True, 3, 20, 333, 333, (0, 2, 14)),     # odd head count: a partly filled Gram workgroup
+    (128, 16, True, 2, 10, 257, 250, (0, 1, 15)),     # rank not a multiple of 4: element-wise coefficient access
+])
+def test_fit_and_apply_shapes(d, bs, paged, H, rank, T, Ts, lead):
+    w = synth.WORKLOADS["llama8b_4k"].with_(num_layers=1, num_kv_heads=H, head_dim=d, block_size=bs, paged=paged,
+                                            seq_tokens=(T,), num_agents=2, rank=rank)
+    pc = synth.build_paged(w, device="cuda", num_output_agents=1, lead_slots=lead)
+    states, ostates, raw, cnp, items, tabs = _fit_both(pc, [((0, 0), (0, 1))], [rank], state_tokens=[Ts])
+    wp, ws = _compare_states(states, raw, "bf16")
+    worst, teeth = _apply_compare(pc, states, ostates, items, tabs, (0, 100))
+    print(f"d {d} block {bs} paged {paged} H {H} rank {rank} T {T} Ts {Ts}: prod {wp:.2e} sigma {ws:.2e} "
+          f"cache {worst:.2e} (uncorrected {teeth:.2e})")
+    assert teeth > 10 * TOL_CACHE["bf16"]
+
+
 def test_fit_recovers_generator_singular_values():
     """Exact low-rank deviation (vlm recipe, no noise): sigma of the fit equals the generator's up to bf16 storage."""
     w = synth.WORKLOADS["vlm"].with_(num_layers=1, num_kv_heads=1, seq_tokens=(3328,), num_agents=2)
