@@ -222,7 +222,8 @@ __global__ __launch_bounds__(kChainThreads) void chain_gram_wave(ChainArgs a) {
 // assemble: H = sum of partials (fp64), P = H K^T (m x d), G = K P (d x d)
 // ---------------------------------------------------------------------------------------------------------------
 
-// LDS version for m <= 128: H (fp64 sum of the partials, kept as fp32) and K^T = [B1; B2] staged in LDS; P = H K^T
+// LDS version for m <= 128: H (fp64 sum of the partials, kept as fp32) and K^T = [B1; B2] staged in LDS (H needs
+// M8 x M8 floats, more than P's M8 x d when the rank sum exceeds the head dimension); P = H K^T
 // with fp64 accumulation in registers (8 x 4 tiles), written back over H; G = K P in 8 x 8 tiles on or above the
 // diagonal, each stored with its mirror.
 __global__ __launch_bounds__(kChainThreads) void chain_assemble_lds(ChainArgs a) {
@@ -234,8 +235,9 @@ __global__ __launch_bounds__(kChainThreads) void chain_assemble_lds(ChainArgs a)
   const int T = a.out.num_tokens;
   const int parts = (T + a.part_tokens - 1) / a.part_tokens;
   const float* PP = a.partials + (size_t)u * a.max_parts * MP * MP;
-  float* R = s_asm;            // H [M8][M8], later P [M8][d]
-  float* Bs = s_asm + M8 * d;  // K^T [M8][d]
+  const int RW = M8 > d ? M8 : d;  // the first region holds H [M8][M8], later P [M8][d]
+  float* R = s_asm;
+  float* Bs = s_asm + M8 * RW;     // K^T [M8][d]
   const int tid = threadIdx.x;
   for (int e = tid; e < M8 * M8; e += kChainThreads) {
     const int i = e / M8, j = e - i * M8;
@@ -327,7 +329,10 @@ __global__ __launch_bounds__(kChainThreads) void chain_assemble_lds(ChainArgs a)
   }
 }
 
-size_t chain_assemble_lds_bytes(int m, int d) { return (size_t)2 * ((m + 7) / 8 * 8) * d * sizeof(float); }
+size_t chain_assemble_lds_bytes(int m, int d) {
+  const size_t m8 = (size_t)(m + 7) / 8 * 8;
+  return (m8 * (m8 > (size_t)d ? m8 : (size_t)d) + m8 * d) * sizeof(float);
+}
 
 __global__ __launch_bounds__(kChainThreads) void chain_assemble(ChainArgs a) {
   const int u = blockIdx.x;

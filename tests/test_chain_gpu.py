@@ -91,6 +91,39 @@ def test_chain_lossless(dtype, r1, r2, ro, T1, T2):
     print(f"lossless {dtype} {r1}+{r2}->{ro}: worst prod {w:.2e}")
 
 
+# Shapes beyond the lossless cases above: head_dim 64 in bfloat16, ranks that are not multiples of 8, a rank sum
+# between 64 and 128, float32 at head_dim 128, and a gap-truncated head_dim 64 chain.  Lossless cases (r_out at least
+# r1 + r2, or the head dimension) also check A_out B_out against A1 B1 + A2 B2 of every unit.
+@pytest.mark.parametrize("dtype,d,r1,r2,ro,T1,T2,scale2", [
+    (torch.bfloat16, 64, 16, 8, 24, 500, 450, 1.0),     # head_dim 64, lossless
+    (torch.bfloat16, 64, 40, 40, 64, 600, 600, 1.0),    # head_dim 64, capped at the head dimension
+    (torch.bfloat16, 128, 10, 7, 17, 333, 333, 1.0),    # ranks off multiples of 8, lossless
+    (torch.bfloat16, 128, 48, 40, 88, 400, 380, 1.0),   # rank sum 88, lossless
+    (torch.float32, 128, 16, 16, 32, 256, 256, 1.0),    # float32 at head_dim 128, lossless
+    (torch.bfloat16, 64, 12, 6, 12, 420, 420, 0.01),    # truncated at a gap (second state far below the first)
+])
+def test_chain_shapes(dtype, d, r1, r2, ro, T1, T2, scale2):
+    rng = np.random.default_rng(d * 100000 + r1 * 1000 + r2)
+    L, H = 2, 2
+    s1 = _state(rng, L, H, d, T1, r1, dtype)
+    s2 = _state(rng, L, H, d, T2, r2, dtype, scale=scale2)
+    out, ost, raw = _chain_both(s1, s2, ro)
+    dt = Hp.storage_name(dtype)
+    w = _compare(out, raw, dt)
+    if ro >= min(r1 + r2, d):
+        o1, o2 = Hp.oracle_state(s1.coef, s1.basis), Hp.oracle_state(s2.coef, s2.basis)
+        gc = Hp.rows_f64(Hp.to_np_storage(out.coef), dt)
+        gb = out.basis.cpu().numpy().astype(np.float64)
+        T = max(T1, T2)
+        for layer in range(L):
+            for kv_ in range(2):
+                for h in range(H):
+                    m = O.materialise(o1, layer, kv_, h, T) + O.materialise(o2, layer, kv_, h, T)
+                    e = O.max_relative_error(gc[layer, kv_, h] @ gb[layer, kv_, h], m)
+                    assert e <= TOL_PROD[dt], (layer, kv_, h, e)
+    print(f"chain {dtype} d {d} {r1}+{r2}->{ro}: worst prod {w:.2e}")
+
+
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
 def test_chain_truncated_with_gap(dtype):
     rng = np.random.default_rng(7)
