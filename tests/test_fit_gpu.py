@@ -140,6 +140,9 @@ def test_fit_bf16_paged_ragged_prefix(rank):
     (128, 16, False, 2, 40, 600, 577, (0, 5)),        # contiguous rows, two 32-rank steps in apply
     (128, 16, True, 3, 20, 333, 333, (0, 2, 14)),     # odd head count: a partly filled Gram workgroup
     (128, 16, True, 2, 10, 257, 250, (0, 1, 15)),     # rank not a multiple of 4: element-wise coefficient access
+    (128, 16, True, 2, 128, 400, 400, (0, 3)),        # rank = head_dim: every eigenpair, four inverse-iteration batches
+    (64, 16, True, 2, 64, 300, 290, (0, 6)),          # rank = head_dim 64
+    (128, 16, True, 2, 100, 350, 340, (0, 9)),        # rank 100: the widest projection tile, partly filled
 ])
 def test_fit_and_apply_shapes(d, bs, paged, H, rank, T, Ts, lead):
     w = synth.WORKLOADS["llama8b_4k"].with_(num_layers=1, num_kv_heads=H, head_dim=d, block_size=bs, paged=paged,
@@ -151,6 +154,37 @@ def test_fit_and_apply_shapes(d, bs, paged, H, rank, T, Ts, lead):
     print(f"d {d} block {bs} paged {paged} H {H} rank {rank} T {T} Ts {Ts}: prod {wp:.2e} sigma {ws:.2e} "
           f"cache {worst:.2e} (uncorrected {teeth:.2e})")
     assert teeth > 10 * TOL_CACHE["bf16"]
+
+
+def test_fit_layer_range_leaves_other_layers():
+    """Fitting layers [1, 3) of 4 writes those layers' units only; they match the oracle's fit of the same range."""
+    w = synth.WORKLOADS["llama8b_4k"].with_(num_layers=4, num_kv_heads=2, seq_tokens=(450,), num_agents=2, rank=16)
+    pc = synth.build_paged(w, device="cuda", lead_slots=(0, 5))
+    L, H, d, T, r = 4, 2, 128, 450, 16
+    st = kvc.State.empty(L, H, d, T, r, torch.bfloat16, "cuda")
+    for t in (st.coef, st.basis, st.sigma):
+        t.fill_(3.0)
+    src, dst = pc.seqs[(0, 0)], pc.seqs[(0, 1)]
+    src_tab, dst_tab = pc.tables[[src.table_row]], pc.tables[[dst.table_row]]
+    batch = kvc.Batch([T], [src.offset], [dst.offset], [st], src_tab, dst_tab)
+    kvc.kvc_fit_state(kvc.Cache(pc.k_pools, pc.v_pools), batch, 1, 3)
+    torch.cuda.synchronize()
+    for layer in (0, 3):
+        for t in (st.coef, st.basis, st.sigma):
+            assert bool((t[layer].float() == 3.0).all()), layer
+    cnp = Hp.oracle_cache(pc.k_pools, pc.v_pools, w.block_size)
+    item = O.Item(T, src.offset, dst.offset, Hp.table_np(src_tab, 0), Hp.table_np(dst_tab, 0))
+    _, raw = O.fit(cnp, [item], r, layer_begin=1, layer_end=3)
+    coef, basis, sigma = raw[0]
+    gc = Hp.rows_f64(Hp.to_np_storage(st.coef), "bf16")
+    gb = st.basis.cpu().numpy().astype(np.float64)
+    gs = st.sigma.cpu().numpy().astype(np.float64)
+    for layer in (1, 2):
+        for kv_ in range(2):
+            for h in range(H):
+                idx = (layer, kv_, h)
+                assert O.max_relative_error(gc[idx] @ gb[idx], coef[idx] @ basis[idx]) <= TOL_PROD["bf16"], idx
+                assert np.max(np.abs(gs[idx] - sigma[idx])) / sigma[idx][0] <= TOL_SIGMA, idx
 
 
 def test_fit_recovers_generator_singular_values():
