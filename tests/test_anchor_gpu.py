@@ -33,8 +33,8 @@ def _ostate(st):
     return Hp.oracle_state(st.coef, st.basis)
 
 
-def _setup(name, layers, num_tokens=None):
-    w = synth.WORKLOADS[name].with_(num_layers=layers)
+def _setup(name, layers, num_tokens=None, **over):
+    w = synth.WORKLOADS[name].with_(num_layers=layers, **over)
     if num_tokens is not None:
         w = w.with_(seq_tokens=(num_tokens,))
     pc = synth.build_paged(w, device="cuda", num_output_agents=1)
@@ -45,16 +45,18 @@ def _setup(name, layers, num_tokens=None):
     return w, pc, cache, T, src, dst, tab
 
 
-# The first three cases fit every anchor's basis in LDS at once (at most ten 32-rank chunks); the last one does not
-# and takes the one-anchor-at-a-time kernels.
-@pytest.mark.parametrize("name,layers,ranks,Ts", [
-    ("tiny", 2, [8, 4, 8], 200),
-    ("llama8b_4k", 2, [32] * 10, 4096),
-    ("llama8b_4k", 1, [16, 32, 48, 8, 40], 1531),
-    ("llama8b_4k", 1, [64, 48, 64, 40, 64, 56], 2050),
+# Cases with at most ten 32-rank chunks fit every anchor's basis in LDS at once; those with more (the 6-anchor cases)
+# take the one-anchor-at-a-time kernels.  The last two run at head_dim 64 (bf16), one of them with three KV heads.
+@pytest.mark.parametrize("name,layers,ranks,Ts,over", [
+    ("tiny", 2, [8, 4, 8], 200, {}),
+    ("llama8b_4k", 2, [32] * 10, 4096, {}),
+    ("llama8b_4k", 1, [16, 32, 48, 8, 40], 1531, {}),
+    ("llama8b_4k", 1, [64, 48, 64, 40, 64, 56], 2050, {}),
+    ("llama8b_4k", 1, [32, 16, 40], 900, {"head_dim": 64, "seq_tokens": (1000,)}),
+    ("llama8b_4k", 1, [64, 48, 64, 40, 64, 56], 700, {"head_dim": 64, "num_kv_heads": 3, "seq_tokens": (800,)}),
 ])
-def test_anchor_weights_and_anchored_apply(name, layers, ranks, Ts):
-    w, pc, cache, T, src, dst, tab = _setup(name, layers, num_tokens=None)
+def test_anchor_weights_and_anchored_apply(name, layers, ranks, Ts, over):
+    w, pc, cache, T, src, dst, tab = _setup(name, layers, num_tokens=None, **over)
     Ts = min(Ts, T)
     # base reconstructions of RMS 0.1 + 0.9 v: mean distances from about 0.8 upwards for unit-variance caches
     scales = [(0.1 + 0.9 * v) / np.sqrt(r / w.head_dim) for v, r in enumerate(ranks)]
@@ -120,12 +122,14 @@ def test_anchored_apply_with_one_anchor_matches_kvc_apply():
         assert bool(ok.all()), float((a32 - b32).abs().nan_to_num().max())
 
 
-@pytest.mark.parametrize("name,layers,prefix,ranks", [("tiny", 2, 100, [8, 8, 8]),
-                                                      ("llama8b_4k", 3, 1000, [32] * 4),
-                                                      ("llama8b_4k", 2, 4096, [32] * 4),
-                                                      ("llama8b_4k", 1, 1500, [96, 96, 64, 96])])
-def test_gate_distances_and_decision(name, layers, prefix, ranks):
-    w, pc, cache, T, src, dst, tab = _setup(name, layers, num_tokens=None)
+@pytest.mark.parametrize("name,layers,prefix,ranks,over", [("tiny", 2, 100, [8, 8, 8], {}),
+                                                           ("llama8b_4k", 3, 1000, [32] * 4, {}),
+                                                           ("llama8b_4k", 2, 4096, [32] * 4, {}),
+                                                           ("llama8b_4k", 1, 1500, [96, 96, 64, 96], {}),
+                                                           ("llama8b_4k", 1, 700, [32, 32, 16],
+                                                            {"head_dim": 64, "seq_tokens": (900,)})])
+def test_gate_distances_and_decision(name, layers, prefix, ranks, over):
+    w, pc, cache, T, src, dst, tab = _setup(name, layers, num_tokens=None, **over)
     bases = _anchor_states(w, layers, T, ranks, [(0.1 + 0.9 * v) / np.sqrt(r / w.head_dim)
                                                  for v, r in enumerate(ranks)], 6)
     anchors = kvc.Anchors(bases, T, layers, weights=torch.empty(0, device="cuda"))
