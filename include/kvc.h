@@ -66,7 +66,8 @@ typedef enum kvc_status {
   KVC_ERR_ALIGN = 4,       /* a row or a coefficient array is not 16-byte aligned */
   KVC_ERR_ALIAS = 5,       /* destination rows may overlap source rows */
   KVC_ERR_WORKSPACE = 6,   /* workspace missing, misaligned or smaller than the query says */
-  KVC_ERR_UNSUPPORTED = 7, /* head_dim other than 64 or 128 */
+  KVC_ERR_UNSUPPORTED = 7, /* head_dim other than 64 or 128, or a state grouping or rotary setting the entry point
+                              does not take (stated at each entry point) */
   KVC_ERR_HIP = 8          /* the HIP runtime refused a launch */
 } kvc_status;
 
