@@ -494,11 +494,7 @@ __global__ __launch_bounds__(kChainThreads) void chain_proj(ChainArgs a) {
         const float x0 = (t < T) ? cat_coef<F32>(a, A1, A2, t, l) : 0.f;
         const float x1 = (t < T) ? cat_coef<F32>(a, A1, A2, t, l + 1) : 0.f;
         if (F32) {
-          uint32_t h0, l0, h1, l1;
-          split_bf16(x0, h0, l0);
-          split_bf16(x1, h1, l1);
-          ch[w] = h0 | (h1 << 16);
-          cl[w] = l0 | (l1 << 16);
+          split_bf16x2(x0, x1, ch[w], cl[w]);
         } else {
           ch[w] = (__float_as_uint(x0) >> 16) | (__float_as_uint(x1) & 0xffff0000u);
           cl[w] = 0;

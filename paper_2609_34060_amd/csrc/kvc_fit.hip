@@ -694,13 +694,12 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
         u32x4 hw, lw;
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-          const float z0 = bf16_lo_to_f32(d[w]) - bf16_lo_to_f32(s[w]);
-          const float z1 = bf16_hi_to_f32(d[w]) - bf16_hi_to_f32(s[w]);
-          uint32_t h0, l0, h1, l1;
-          split_bf16(z0, h0, l0);
-          split_bf16(z1, h1, l1);
-          hw[w] = h0 | (h1 << 16);
-          lw[w] = l0 | (l1 << 16);
+          // both features of the word split at once (two packed conversions)
+          uint32_t hh, ll;
+          split_bf16x2(bf16_lo_to_f32(d[w]) - bf16_lo_to_f32(s[w]), bf16_hi_to_f32(d[w]) - bf16_hi_to_f32(s[w]), hh,
+                       ll);
+          hw[w] = hh;
+          lw[w] = ll;
         }
         zh[ks] = as_bf16x8(hw);
         zl[ks] = as_bf16x8(lw);
