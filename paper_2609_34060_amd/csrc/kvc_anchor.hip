@@ -319,7 +319,7 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_f32(AnchorArgs a) 
   }
 }
 
-// Gate: d_v = sqrt(sum of the partials of every (layer, chunk)) in a fixed order, fp64.
+// Gate: d_v = sqrt(sum of the partials of every (layer, chunk[, head])) in a fixed order, fp64.
 __global__ __launch_bounds__(kAnchorThreads) void gate_finish(AnchorArgs a) {
   const int v = threadIdx.x;
   if (v >= a.num_anchors) return;
@@ -550,6 +550,7 @@ constexpr int kResWaves = 8;
 constexpr int kResThreads = kResWaves * kWave;
 constexpr int kResTiles = 8;                            // 16-token tiles per wave
 constexpr int kResChunk = kResWaves * kResTiles * 16;  // 1024 tokens per workgroup
+int anchor_resident_chunk_tokens() { return kResChunk; }
 constexpr size_t kResMaxLds = 160 * 1024;
 
 // LDS holds hi [D][32 NC] then lo; the 16-byte granule (8 ranks) q of feature row f sits at q ^ res_swz(f), a
@@ -719,6 +720,9 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
   const int lrel = blockIdx.z, layer = a.layer_begin + lrel;
   const int kv = GATE ? 1 : blockIdx.y;
   const int H = a.pv.num_kv_heads, V = a.num_anchors;
+  // the gate reads value rows only, so its launch spreads the heads over the grid (one head per workgroup); the
+  // weights need every head of a token in one workgroup (the mean runs over the whole layer row)
+  const int h_lo = GATE ? (int)blockIdx.y : 0, h_hi = GATE ? h_lo + 1 : H;
   const int Tl = a.num_weighted;
   const int t_begin = blockIdx.x * kResChunk;
   if (t_begin >= Tl) return;  // whole workgroup
@@ -735,9 +739,9 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
     u32x4 raw[NQ];
     u32x4 cw[NCM];
   };
-  for (int h = 0; h < H; ++h) {
+  for (int h = h_lo; h < h_hi; ++h) {
     const int64_t unit = unit_index(layer, kv, h, H);
-    if (h > 0) __syncthreads();  // every wave is done with the previous head's bases
+    if (h > h_lo) __syncthreads();  // every wave is done with the previous head's bases
     stage_stacked<D>(a, unit, s_hi, s_lo);
     __syncthreads();
     auto load_tile = [&](int j, Tile& tl) __attribute__((always_inline)) {
@@ -828,7 +832,7 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
       const int v = threadIdx.x;
       float s = 0.0f;
       for (int w = 0; w < kResWaves; ++w) s += s_d[w * V + v];
-      a.gate_partials[((int64_t)lrel * a.gate_chunks + blockIdx.x) * V + v] = s;
+      a.gate_partials[((int64_t)lrel * a.gate_chunks + blockIdx.x * gridDim.y + blockIdx.y) * V + v] = s;
     }
   } else {
 #pragma unroll
@@ -966,9 +970,10 @@ hipError_t launch_gate_distances(const AnchorArgs& args, kvc_dtype dtype, hipStr
   hipError_t e;
   dim3 grid(a.gate_chunks, 1, a.num_layers);
   if (dtype == KVC_BF16 && plan_resident(a)) {
-    // fewer, larger chunks than the workspace was sized for
-    a.gate_chunks = (a.num_weighted + kResChunk - 1) / kResChunk;
-    grid.x = a.gate_chunks;
+    // one partial per (layer, 1024-token chunk, KV head): the workspace query sizes for this count as well
+    grid.x = (a.num_weighted + kResChunk - 1) / kResChunk;
+    grid.y = a.pv.num_kv_heads;
+    a.gate_chunks = (int)(grid.x * grid.y);
     const size_t rl = res_lds_bytes(a, 2);
     e = D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, true>, grid, rl, a, stream, kResThreads)
                 : launch_with_lds(anchor_dist_res_bf16<128, true>, grid, rl, a, stream, kResThreads);

@@ -715,7 +715,11 @@ size_t kvc_gate_workspace_bytes(const kvc_cache* cache, const kvc_anchors* ancho
   if (check_cache(cache, layer_begin, layer_end) != KVC_OK || !anchors || prefix < 1) return 0;
   if (anchors->num_anchors < 1 || anchors->num_anchors > KVC_MAX_ANCHORS) return 0;
   const int chunk = cache->dtype == KVC_BF16 ? kvc::anchor_chunk_tokens() : 64;
-  const size_t chunks = static_cast<size_t>((prefix + chunk - 1) / chunk);
+  size_t chunks = static_cast<size_t>((prefix + chunk - 1) / chunk);
+  if (cache->dtype == KVC_BF16) {  // the resident-basis kernel: one partial per 1024-token chunk and KV head
+    const int res = kvc::anchor_resident_chunk_tokens();
+    chunks = std::max(chunks, static_cast<size_t>((prefix + res - 1) / res) * static_cast<size_t>(cache->num_kv_heads));
+  }
   return align256(static_cast<size_t>(layer_end - layer_begin) * chunks * anchors->num_anchors * sizeof(float));
 }
 

@@ -145,6 +145,7 @@ struct AnchorArgs {
   int32_t chunk_last[kResMaxChunks];  // 1 on an anchor's last chunk
 };
 int anchor_chunk_tokens();
+int anchor_resident_chunk_tokens();
 size_t anchor_lds_bytes(int head_dim, int max_rank, kvc_dtype dtype, int which);
 hipError_t launch_anchor_weights(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream);
 hipError_t launch_apply_anchored(const AnchorArgs& a, kvc_dtype dtype, hipStream_t stream);

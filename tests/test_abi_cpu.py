@@ -325,9 +325,12 @@ def test_anchor_calls_reject_bad_arguments_before_launch(case):
 
 def test_gate_workspace_query():
     f = AnchorFixture(V=4)
+    H = f.cache.num_kv_heads
     need = kvc.load().kvc_gate_workspace_bytes(ctypes.byref(f.cache), ctypes.byref(f.anchors), 1200, 0, 2)
-    # bf16: 512-token chunks, one float per (layer, chunk, anchor), 256-byte granules
-    assert need == -(-(2 * 3 * 4 * 4) // 256) * 256
+    # bf16: one float per (layer, chunk, anchor) for the larger of 512-token chunks and 1024-token chunks times the
+    # KV heads (the resident-basis kernel keeps one partial per chunk and head), in 256-byte granules
+    chunks = max(-(-1200 // 512), -(-1200 // 1024) * H)
+    assert need == -(-(2 * chunks * 4 * 4) // 256) * 256
 
 
 def test_per_layer_states_are_refused_where_unsupported():
