@@ -319,13 +319,19 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_f32(AnchorArgs a) 
   }
 }
 
-// Gate: d_v = sqrt(sum of the partials of every (layer, chunk[, head])) in a fixed order, fp64.
+// Gate: d_v = sqrt(sum of the partials of every (layer, chunk[, head])) in a fixed order, fp64.  Wave w takes
+// anchors v = w, w + 4, ...; lane l adds the partials l, l + 64, ... in order and a fixed xor butterfly combines the
+// lanes, so the sum does not depend on scheduling.
 __global__ __launch_bounds__(kAnchorThreads) void gate_finish(AnchorArgs a) {
-  const int v = threadIdx.x;
-  if (v >= a.num_anchors) return;
-  double s = 0.0;
-  for (int64_t i = 0; i < (int64_t)a.num_layers * a.gate_chunks; ++i) s += (double)a.gate_partials[i * a.num_anchors + v];
-  a.distances[v] = (float)sqrt(s);
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int64_t n = (int64_t)a.num_layers * a.gate_chunks;
+  for (int v = wave; v < a.num_anchors; v += kAnchorWaves) {  // uniform over the wave
+    double s = 0.0;
+    for (int64_t i = lane; i < n; i += kWave) s += (double)a.gate_partials[i * a.num_anchors + v];
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) s += __shfl_xor(s, o, kWave);
+    if (lane == 0) a.distances[v] = (float)sqrt(s);
+  }
 }
 
 // ---------------------------------------------------------------------------------------------------------------
