@@ -10,7 +10,8 @@ Steps cycle over the edges of the workload; inputs are resident in HBM before th
 Printed: one JSON line.  `value` is the corrected-KV throughput of kvc_apply in GB/s (algorithmic bytes: source and
 destination rows, coefficients at their stored width, bases) measured with HIP events on the launch stream; fit
 throughput is token*layers/s.  `roofline` is kvc_apply against the 8 TB/s HBM peak; `cpu_baseline` is the CPU
-oracle timed on a bounded sample of the same workload on this host.
+oracle timed on a bounded sample of the same workload on this host.  `copy_ceiling` gives, on the same GPU, the
+rate of a pure bit copy through the same block tables (kvc_apply with a rank-0 state) and of a contiguous copy.
 """
 import argparse
 import hashlib
@@ -126,6 +127,41 @@ def anchor_pool_measurement(args, kvc, synth, torch):
             "apply_anchored_frac": round(ab / (apply_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
             "apply_anchored_bytes": ab,
             "weights_gbps": round(wb / (weights_ms * 1e-3) / 1e9, 2), "weights_bytes": wb}
+
+
+def copy_ceiling(args, kvc, torch, cache, w, batch):
+    """Copy ceilings on the same GPU, beside the apply: kvc_apply with a rank-0 state (every row a bit copy through
+    the same block tables and the same kernel, no coefficients or bases: the paged per-head copy the apply is built
+    on) and a contiguous device-to-device copy of the same number of row bytes."""
+    L, H, d, T = w.num_layers, w.num_kv_heads, w.head_dim, w.seq_tokens[0]
+    s0 = kvc.State.empty(L, H, d, T, 0, torch.bfloat16, "cuda")
+    b0 = batch((0, 0), (0, 100), s0)
+    row_bytes = L * 2 * H * T * d * 2  # read once and written once
+    src = torch.empty(row_bytes // 2, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    n = max(5, args.steps // 2)
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        ev[0].record()
+        for i in range(n):
+            fn()
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        return sum(ev[i].elapsed_time(ev[i + 1]) for i in range(n)) / n
+
+    paged_ms = timed(lambda: kvc.kvc_apply(cache, b0))
+    contig_ms = timed(lambda: dst.copy_(src))
+    del src, dst
+    torch.cuda.empty_cache()
+    pg, cg = 2 * row_bytes / (paged_ms * 1e-3) / 1e9, 2 * row_bytes / (contig_ms * 1e-3) / 1e9
+    return {"bytes": 2 * row_bytes,
+            "paged_rank0_apply_ms": round(paged_ms, 4), "paged_rank0_apply_gbps": round(pg, 2),
+            "paged_rank0_apply_frac": round(pg / HBM_PEAK_GBPS, 4),
+            "contiguous_copy_ms": round(contig_ms, 4), "contiguous_copy_gbps": round(cg, 2),
+            "contiguous_copy_frac": round(cg / HBM_PEAK_GBPS, 4)}
 
 
 def rope_measurement(args, kvc, torch, pc, w, state, batch):
@@ -311,6 +347,8 @@ def main():
     ap.add_argument("--no-rope", action="store_true", help="skip the rotary re-alignment measurement")
     ap.add_argument("--no-layer-fit", action="store_true", help="skip the per-layer factorisation measurement")
     ap.add_argument("--no-chain-study", action="store_true", help="skip the chained / non-chained error study")
+    ap.add_argument("--no-copy-ceiling", action="store_true",
+                    help="skip the same-GPU copy ceilings (rank-0 apply through the tables, contiguous copy)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="before the steps, run one elementwise kernel that reads BYTES and writes BYTES (dst = -src "
                          "in float32), a plain copy of known size, so that HBM counters of a profiling run can be "
@@ -432,6 +470,8 @@ def main():
         "generation_s": round(t_gen, 2),
         "source_hash": src_hash,
     }
+    if not args.no_copy_ceiling:
+        out["copy_ceiling"] = copy_ceiling(args, kvc, torch, cache, w, batch)
     if not args.no_rope:
         out["rope"] = rope_measurement(args, kvc, torch, pc, w, Tc[0], batch)
     if not args.no_layer_fit:
