@@ -598,8 +598,9 @@ __device__ __forceinline__ void stage_stacked(const AnchorArgs& a, int64_t unit,
 }
 
 // Eq. 8 with every anchor resident: per 16-token tile the accumulator starts from the source rows in fp32 and
-// takes sum_c (w_v A_v)[t, chunk c] B_v[chunk c] over all chunks (weight-scaled coefficients split hi/lo, three
-// MFMAs per fragment), then one rounding.
+// takes w_v[t] (A_v[t, chunk c] B_v[chunk c]) over all chunks (the bf16 coefficients are exact MFMA operands against
+// the basis hi/lo, two MFMAs per fragment, and the product is scaled by the token's weight in fp32), then one
+// rounding.
 template <int D>
 __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArgs a) {
   constexpr int MT = D / 16, NQ = D / 32, NCM = kResMaxChunks;
@@ -664,22 +665,18 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
         if (c >= NC) break;
         int kc = kpt;
         asm volatile("" : "+s"(kc));  // keeps the fragment reads in this chunk's step (not hoisted out of the tiles)
-        u32x4 ch, cl;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          uint32_t hh, ll;
-          split_bf16x2(tl.w[c] * bf16_lo_to_f32(tl.cw[c][i]), tl.w[c] * bf16_hi_to_f32(tl.cw[c][i]), hh, ll);
-          ch[i] = hh;
-          cl[i] = ll;
-        }
-        const bf16x8 bh = as_bf16x8(ch), bl = as_bf16x8(cl);
+        // the chunk's reconstruction from the exact bf16 coefficients (basis hi/lo), then scaled by the lane's
+        // token weight in fp32: lane (g, n) holds rows 4g .. 4g + 3 of token n's column
+        const bf16x8 cb = as_bf16x8(tl.cw[c]);
+        const float wc = tl.w[c];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
           const int f = mfma_row_feature(mt, n);
           const bf16x8 fl = res_frag(s_lo, kc, f, c, g), fh = res_frag(s_hi, kc, f, c, g);
-          acc[mt] = mfma16x16x32(fl, bh, acc[mt]);
-          acc[mt] = mfma16x16x32(fh, bl, acc[mt]);
-          acc[mt] = mfma16x16x32(fh, bh, acc[mt]);
+          f32x4 p = mfma16x16x32(fl, cb, f32x4{0.f, 0.f, 0.f, 0.f});
+          p = mfma16x16x32(fh, cb, p);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[mt][e] = fmaf(wc, p[e], acc[mt][e]);
         }
       }
       const bool crow = t < Ts;
