@@ -125,6 +125,9 @@ def test_anchored_apply_with_one_anchor_matches_kvc_apply():
 @pytest.mark.parametrize("name,layers,prefix,ranks,over", [("tiny", 2, 100, [8, 8, 8], {}),
                                                            ("llama8b_4k", 3, 1000, [32] * 4, {}),
                                                            ("llama8b_4k", 2, 4096, [32] * 4, {}),
+                                                           # 3 layers x 4 chunks x 8 heads = 96 partials per anchor:
+                                                           # the finishing sum takes two per lane for half the lanes
+                                                           ("llama8b_4k", 3, 4096, [32] * 3, {}),
                                                            ("llama8b_4k", 1, 1500, [96, 96, 64, 96], {}),
                                                            ("llama8b_4k", 1, 700, [32, 32, 16],
                                                             {"head_dim": 64, "seq_tokens": (900,)})])
