@@ -135,15 +135,17 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_bf16(AnchorArgs a)
     const int h = hv / V, v = hv - h * V;
     return a.basis[v] + unit_index(layer, kv, h, H) * (int64_t)a.rank[v] * D;
   };
-  stager.load(basis_of(0), a.rank[0]);
-  for (int hv = 0; hv < H * V; ++hv) {
+  // the gate (value rows only) takes one KV head per workgroup; the weights walk every head of the layer row
+  const int hv0 = GATE ? (int)blockIdx.y * V : 0, hv1 = GATE ? hv0 + V : H * V;
+  stager.load(basis_of(hv0), a.rank[hv0 % V]);
+  for (int hv = hv0; hv < hv1; ++hv) {
     const int h = hv / V, v = hv - h * V;
     const int r = a.rank[v], KS = (r + 31) / 32;
     uint16_t* s_hi = s_b + (hv & 1) * 2 * D * KP;
     uint16_t* s_lo = s_hi + D * KP;
     stager.store(s_hi, s_lo);
     __syncthreads();  // this basis is in LDS; the other buffer is no longer read (and s_d is initialised)
-    if (hv + 1 < H * V) stager.load(basis_of(hv + 1), a.rank[(hv + 1) % V]);
+    if (hv + 1 < hv1) stager.load(basis_of(hv + 1), a.rank[(hv + 1) % V]);
     const int64_t unit = unit_index(layer, kv, h, H);
     const uint16_t* coef = static_cast<const uint16_t*>(a.coef[v]) + unit * (int64_t)a.tokens[v] * r;
     float part = 0.0f;
@@ -207,7 +209,7 @@ __global__ __launch_bounds__(kAnchorThreads) void anchor_dist_bf16(AnchorArgs a)
       const int v = threadIdx.x;
       float s = 0.0f;
       for (int w = 0; w < kAnchorWaves; ++w) s += s_d[w * V + v];
-      a.gate_partials[((int64_t)lrel * a.gate_chunks + blockIdx.x) * V + v] = s;
+      a.gate_partials[((int64_t)lrel * a.gate_chunks + blockIdx.x * gridDim.y + blockIdx.y) * V + v] = s;
     }
   } else {
     const float inv_feat = 1.0f / (float)(H * D);
@@ -981,6 +983,9 @@ hipError_t launch_gate_distances(const AnchorArgs& args, kvc_dtype dtype, hipStr
     e = D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, true>, grid, rl, a, stream, kResThreads)
                 : launch_with_lds(anchor_dist_res_bf16<128, true>, grid, rl, a, stream, kResThreads);
   } else if (dtype == KVC_BF16) {
+    // one partial per (layer, 512-token chunk, KV head), as the workspace query sizes
+    grid.y = a.pv.num_kv_heads;
+    a.gate_chunks = (int)(grid.x * grid.y);
     e = D == 64 ? launch_dist_bf16<64, true, false>(a, grid, lds, stream)
                 : launch_dist_bf16<128, true, false>(a, grid, lds, stream);
   } else {

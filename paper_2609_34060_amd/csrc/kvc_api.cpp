@@ -716,9 +716,9 @@ size_t kvc_gate_workspace_bytes(const kvc_cache* cache, const kvc_anchors* ancho
   if (anchors->num_anchors < 1 || anchors->num_anchors > KVC_MAX_ANCHORS) return 0;
   const int chunk = cache->dtype == KVC_BF16 ? kvc::anchor_chunk_tokens() : 64;
   size_t chunks = static_cast<size_t>((prefix + chunk - 1) / chunk);
-  if (cache->dtype == KVC_BF16) {  // the resident-basis kernel: one partial per 1024-token chunk and KV head
+  if (cache->dtype == KVC_BF16) {  // bf16 kernels keep one partial per chunk and KV head (512 or 1024-token chunks)
     const int res = kvc::anchor_resident_chunk_tokens();
-    chunks = std::max(chunks, static_cast<size_t>((prefix + res - 1) / res) * static_cast<size_t>(cache->num_kv_heads));
+    chunks = std::max(chunks, static_cast<size_t>((prefix + res - 1) / res)) * static_cast<size_t>(cache->num_kv_heads);
   }
   return align256(static_cast<size_t>(layer_end - layer_begin) * chunks * anchors->num_anchors * sizeof(float));
 }

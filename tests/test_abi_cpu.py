@@ -327,9 +327,9 @@ def test_gate_workspace_query():
     f = AnchorFixture(V=4)
     H = f.cache.num_kv_heads
     need = kvc.load().kvc_gate_workspace_bytes(ctypes.byref(f.cache), ctypes.byref(f.anchors), 1200, 0, 2)
-    # bf16: one float per (layer, chunk, anchor) for the larger of 512-token chunks and 1024-token chunks times the
-    # KV heads (the resident-basis kernel keeps one partial per chunk and head), in 256-byte granules
-    chunks = max(-(-1200 // 512), -(-1200 // 1024) * H)
+    # bf16: one float per (layer, chunk, KV head, anchor) with 512-token chunks (the larger count of the two bf16
+    # kernels' 512 and 1024-token chunks), in 256-byte granules
+    chunks = max(-(-1200 // 512), -(-1200 // 1024)) * H
     assert need == -(-(2 * chunks * 4 * 4) // 256) * 256
 
 
