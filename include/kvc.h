@@ -32,15 +32,17 @@
  * contiguous rows), slot = p % block_size.  A state's unit u = (layer, kv, head) with kv = 0 for K and 1 for V keeps
  *   coef  [L][2][H][T_s][r]  (coef_dtype)      basis [L][2][H][r][d] (float32)      sigma [L][2][H][r] (float32)
  *
- * Ownership.  The caller allocates every buffer (pools, tables, states, workspaces, both copies of the item array);
- * the library allocates no device memory, keeps no pointer after a call returns, holds no global state and may be
- * called from several threads.  Source rows are only read.  The one host-side object is the anchor-pool bookkeeping
+ * Ownership.  The caller allocates every buffer (pools, tables, states, workspaces, the item scratch); the library
+ * allocates no device memory, keeps no pointer after a call returns, holds no global state and may be called from
+ * several threads.  Source rows are only read.  The one host-side object is the anchor-pool bookkeeping
  * of kvc_pool_create, owned by the caller until kvc_pool_destroy (not thread-safe per pool).
  *
  * Errors.  Every argument check runs on the host before anything is enqueued; on an error nothing is enqueued and
  * the status says why.  A failed launch returns KVC_ERR_HIP (kvc_last_hip_error() gives the hipError_t of the
- * calling thread).  Faults inside a kernel surface at the caller's next synchronisation.  Rows whose block-table
- * entry lies outside [0, num_blocks) are neither read nor written.  NaN and Inf propagate.
+ * calling thread).  Faults inside a kernel surface at the caller's next synchronisation.  A row whose source or
+ * destination block-table entry lies outside [0, num_blocks) is neither read nor written (its destination keeps its
+ * bytes).  NaN and Inf of the cache rows propagate through the corrections; a non-finite state entry gives NaN in the
+ * rows it touches.
  */
 #ifndef KVC_H
 #define KVC_H
@@ -64,7 +66,7 @@ typedef enum kvc_status {
   KVC_ERR_SHAPE = 2,       /* sizes inconsistent or out of range */
   KVC_ERR_DTYPE = 3,       /* unknown dtype, or dtypes that do not go together */
   KVC_ERR_ALIGN = 4,       /* a row or a coefficient array is not 16-byte aligned */
-  KVC_ERR_ALIAS = 5,       /* destination rows may overlap source rows */
+  KVC_ERR_ALIAS = 5,       /* destination rows may overlap source rows or another item's destination rows */
   KVC_ERR_WORKSPACE = 6,   /* workspace missing, misaligned or smaller than the query says */
   KVC_ERR_UNSUPPORTED = 7, /* head_dim other than 64 or 128, or a state grouping or rotary setting the entry point
                               does not take (stated at each entry point) */
@@ -152,14 +154,19 @@ typedef struct kvc_item {
   kvc_state state;
 } kvc_item;
 
-/* A batch of independent items handled by one launch per kernel.  `items` is a HOST array used for checks and launch
- * sizing; `items_dev` is a DEVICE array holding the same bytes, read by the kernels.  Tables are DEVICE int32 arrays
- * [num_items][max_blocks] of physical block ids; NULL means the identity mapping (contiguous rows). */
+/* A batch of independent items handled by one launch per kernel.  `items` is a HOST array: the library checks it and
+ * then copies it (hipMemcpyAsync on the call's stream, before its first launch) into `item_scratch`, a DEVICE buffer
+ * of at least kvc_item_scratch_bytes(num_items) bytes, 16-byte aligned, from which the kernels read the items; the
+ * kernels therefore see exactly the bytes that were checked.  Like every other buffer of an asynchronous call, the
+ * host items (when they are in pinned memory) and the scratch belong to the call until its work on the stream is done:
+ * calls that overlap in time need scratch buffers of their own.  kvc_apply and kvc_fit_state use the scratch; the
+ * anchor calls take their one item by value and ignore it.  Tables are DEVICE int32 arrays [num_items][max_blocks] of
+ * physical block ids; NULL means the identity mapping (contiguous rows). */
 typedef struct kvc_batch {
   int32_t num_items;
   int32_t max_blocks;
   const kvc_item* items;
-  const kvc_item* items_dev;
+  void* item_scratch;
   const int32_t* src_tables;
   const int32_t* dst_tables;
 } kvc_batch;
@@ -169,6 +176,8 @@ const char* kvc_status_str(kvc_status status);
 /* hipError_t of the last failed HIP call made by this thread inside the library (0 if none). */
 int32_t kvc_last_hip_error(void);
 
+/* Bytes of the device item scratch of a batch of num_items items (0 for a negative count). */
+size_t kvc_item_scratch_bytes(int32_t num_items);
 /* Bytes of one low-rank state (coef + basis + sigma), the O(N r (L + D)) term of Section 3.3. */
 size_t kvc_state_bytes(int32_t num_layers, int32_t num_kv_heads, int32_t head_dim, int32_t num_tokens, int32_t rank,
                        kvc_dtype coef_dtype);
@@ -181,8 +190,9 @@ size_t kvc_dense_bytes(int32_t num_layers, int32_t num_kv_heads, int32_t head_di
 
 /* Materialise each item's destination rows from its source rows and state, for layers [layer_begin, layer_end).
  * One launch covers every item, layer, K/V and head of the call (a serving batch corrects a whole layer at once).
- * Destination rows must not overlap any source row of the call; with NULL tables and equal pools the host checks the
- * row ranges, with tables it rejects src_tables == dst_tables.
+ * Destination rows must not overlap any source row of the call, nor another item's destination rows.  With both
+ * tables NULL the host checks this on the row ranges of all items (KVC_ERR_ALIAS); with tables the block ids live in
+ * device memory, so the host only rejects src_tables == dst_tables and the caller guarantees the rest.
  * Keys of a rotary cache (rope_style != KVC_ROPE_NONE), with R(p) the rotation to position p, ps = src_position and
  * pd = dst_position: C_dst[t] = R(pd) (R(-ps) C_src[t] + A[t] B) for t < T_s (the state is canonical) and
  * C_dst[t] = R(pd - ps) C_src[t] for T_s <= t < T (the re-aligned source; a bit copy when pd = ps), one rounding. */
@@ -231,7 +241,7 @@ typedef struct kvc_anchors {
  * V separately, and t < T_s: d_v[t] = mean over the layer's K (or V) row -- every KV head and feature, the paper's
  * D = H d -- of |C_src[t] - (A_v B_v)[t]|, with A_v B_v anchor v's reconstructed base, and
  * w_v[t] = exp(-d_v[t] / temperature) / sum_u exp(-d_u[t] / temperature) (temperature 1 in the paper).  `batch`
- * holds exactly one item whose source rows are compared (its state, dst side and items_dev are not used);
+ * holds exactly one item whose source rows are compared (its state, dst side and item_scratch are not used);
  * T_s <= item.num_tokens.  Keys of a rotary cache are compared in canonical coordinates, R(-src_position) C_src[t]
  * (the anchors' bases are canonical). */
 kvc_status kvc_anchor_weights(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
@@ -240,7 +250,7 @@ kvc_status kvc_anchor_weights(const kvc_cache* cache, const kvc_batch* batch, co
 /* Eq. 8 with token-wise weights: for layers [layer_begin, layer_end), every K/V unit and t < T_s,
  * C_dst[t] = C_src[t] + sum_v w_v[t] A_v[t] B_v (A_v B_v anchor v's delta correction, w from `anchors->weights`),
  * one rounding to the storage dtype; rows T_s <= t < item.num_tokens are bit copies.  One item (its state and
- * items_dev are not used); destination rows must not overlap source rows (as for kvc_apply).  Keys of a rotary
+ * item_scratch are not used); destination rows must not overlap source rows (as for kvc_apply).  Keys of a rotary
  * cache as in kvc_apply: R(pd) (R(-ps) C_src[t] + sum_v w_v[t] A_v[t] B_v), re-aligned source past T_s. */
 kvc_status kvc_apply_anchored(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
                               int32_t layer_begin, int32_t layer_end, hipStream_t stream);

@@ -214,13 +214,6 @@ def to_canonical(rows_f64: np.ndarray, cache: "Cache", kv: int, position: int) -
     return rope_rotate(rows_f64, -position, cache.rope)
 
 
-def to_target(rows_f64: np.ndarray, cache: "Cache", kv: int, position: int) -> np.ndarray:
-    """Canonical key rows rotated to a segment starting at `position` (values unchanged)."""
-    if kv == 1 or cache.rope is None:
-        return rows_f64
-    return rope_rotate(rows_f64, position, cache.rope)
-
-
 # ------------------------------------------------------------------------------------------------------------------
 # Row addressing (the paged layout a serving engine keeps; Section 4.1 serves through vLLM)
 # ------------------------------------------------------------------------------------------------------------------

@@ -426,8 +426,10 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_bf16(AnchorArgs
     const int t = t0 + n;
     const bool valid = t < T;
     u32x4 raw[NQ];
-    load_row_segments<NQ>(src_pool, valid ? row_offset(a.pv, a.src_table, a.src_offset, t, head) : -1, g, raw);
-    const int64_t dof = valid ? row_offset(a.pv, a.dst_table, a.dst_offset, t, head) : -1;
+    const int64_t so = valid ? row_offset(a.pv, a.src_table, a.src_offset, t, head) : -1;
+    load_row_segments<NQ>(src_pool, so, g, raw);
+    // a row whose source block id is out of range is neither read nor written
+    const int64_t dof = so >= 0 ? row_offset(a.pv, a.dst_table, a.dst_offset, t, head) : -1;
     u32x4 outw[NQ];
     // rows past T_s have a zero correction: the re-aligned source with a shift, else bit copies
     const bool crow = t < Ts || shift;
@@ -636,8 +638,10 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
   auto load_tile = [&](int j, Tile& tl) __attribute__((always_inline)) {
     const int t = t_begin + (j * kResWaves + wave) * 16 + n;
     const bool valid = t < T, crow = t < Ts;
-    tl.dof = valid ? row_offset(a.pv, a.dst_table, a.dst_offset, t, head) : -1;
-    load_row_segments<NQ>(src_pool, valid ? row_offset(a.pv, a.src_table, a.src_offset, t, head) : -1, g, tl.raw);
+    const int64_t so = valid ? row_offset(a.pv, a.src_table, a.src_offset, t, head) : -1;
+    // a row whose source block id is out of range is neither read nor written
+    tl.dof = so >= 0 ? row_offset(a.pv, a.dst_table, a.dst_offset, t, head) : -1;
+    load_row_segments<NQ>(src_pool, so, g, tl.raw);
 #pragma unroll
     for (int c = 0; c < NCM; ++c) {
       tl.cw[c] = u32x4{0u, 0u, 0u, 0u};

@@ -80,7 +80,8 @@ kvc_status check_batch(const kvc_cache* c, const kvc_batch* b, bool needs_src) {
   if (!b) return KVC_ERR_NULL_ARG;
   if (b->num_items < 0 || b->max_blocks < 0) return KVC_ERR_SHAPE;
   if (b->num_items == 0) return KVC_OK;
-  if (!b->items || !b->items_dev) return KVC_ERR_NULL_ARG;
+  if (!b->items || !b->item_scratch) return KVC_ERR_NULL_ARG;
+  if (!aligned16(b->item_scratch)) return KVC_ERR_ALIGN;
   if ((b->src_tables || b->dst_tables) && b->max_blocks < 1) return KVC_ERR_SHAPE;
   for (int32_t i = 0; i < b->num_items; ++i) {
     const kvc_item& it = b->items[i];
@@ -94,6 +95,41 @@ kvc_status check_batch(const kvc_cache* c, const kvc_batch* b, bool needs_src) {
     if (it.state.num_tokens > it.num_tokens) return KVC_ERR_SHAPE;
   }
   return KVC_OK;
+}
+
+// The kernels read the items from the caller's device scratch; the library writes the checked host items there on
+// the call's stream before its first launch, so no unchecked item reaches a kernel.
+kvc_status upload_items(const kvc_batch* b, hipStream_t stream) {
+  const size_t bytes = static_cast<size_t>(b->num_items) * sizeof(kvc_item);
+  return hip_status(hipMemcpyAsync(b->item_scratch, b->items, bytes, hipMemcpyHostToDevice, stream));
+}
+
+const kvc_item* device_items(const kvc_batch* b) { return static_cast<const kvc_item*>(b->item_scratch); }
+
+// With both tables NULL all items address the same identity-mapped rows: no destination range of the call may overlap
+// a source range or another destination range.  Sorted sweep over the row ranges of every item.
+bool contiguous_ranges_overlap(const kvc_batch* b) {
+  struct Range {
+    int64_t begin, end;
+    bool dst;
+  };
+  std::vector<Range> rs;
+  rs.reserve(2 * static_cast<size_t>(b->num_items));
+  for (int32_t i = 0; i < b->num_items; ++i) {
+    const kvc_item& it = b->items[i];
+    if (it.num_tokens <= 0) continue;
+    rs.push_back({it.src_offset, static_cast<int64_t>(it.src_offset) + it.num_tokens, false});
+    rs.push_back({it.dst_offset, static_cast<int64_t>(it.dst_offset) + it.num_tokens, true});
+  }
+  std::sort(rs.begin(), rs.end(), [](const Range& x, const Range& y) { return x.begin < y.begin; });
+  // every range is compared with the open ranges before it: the furthest-reaching source and destination so far
+  int64_t src_end = INT64_MIN, dst_end = INT64_MIN;
+  for (const Range& r : rs) {
+    if (r.dst && (src_end > r.begin || dst_end > r.begin)) return true;
+    if (!r.dst && dst_end > r.begin) return true;
+    (r.dst ? dst_end : src_end) = std::max(r.dst ? dst_end : src_end, r.end);
+  }
+  return false;
 }
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -401,13 +437,17 @@ const char* kvc_status_str(kvc_status s) {
     case KVC_ERR_ALIGN: return "pointer or stride not 16-byte aligned";
     case KVC_ERR_ALIAS: return "destination rows may overlap source rows";
     case KVC_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
-    case KVC_ERR_UNSUPPORTED: return "unsupported head_dim (64 or 128)";
+    case KVC_ERR_UNSUPPORTED: return "head_dim other than 64 or 128, or a grouping or rotary setting the call does not take";
     case KVC_ERR_HIP: return "HIP runtime error";
   }
   return "unknown status";
 }
 
 int32_t kvc_last_hip_error(void) { return g_last_hip_error; }
+
+size_t kvc_item_scratch_bytes(int32_t num_items) {
+  return num_items > 0 ? static_cast<size_t>(num_items) * sizeof(kvc_item) : 0;
+}
 
 size_t kvc_state_bytes(int32_t L, int32_t H, int32_t d, int32_t T, int32_t r, kvc_dtype coef_dtype) {
   if (L < 0 || H < 0 || d < 0 || T < 0 || r < 0 || !valid_dtype(coef_dtype)) return 0;
@@ -440,16 +480,15 @@ kvc_status kvc_apply(const kvc_cache* cache, const kvc_batch* batch, int32_t lay
     const kvc_item& it = batch->items[i];
     max_tokens = std::max(max_tokens, it.num_tokens);
     max_rank = std::max(max_rank, it.state.rank);
-    if (!batch->src_tables && !batch->dst_tables && it.num_tokens > 0) {
-      const int64_t a0 = it.src_offset, a1 = a0 + it.num_tokens, b0 = it.dst_offset, b1 = b0 + it.num_tokens;
-      if (a0 < b1 && b0 < a1) return KVC_ERR_ALIAS;
-    }
   }
+  if (!batch->src_tables && !batch->dst_tables && contiguous_ranges_overlap(batch)) return KVC_ERR_ALIAS;
   if (batch->num_items == 0 || layer_end == layer_begin || max_tokens == 0) return KVC_OK;
+  s = upload_items(batch, stream);
+  if (s != KVC_OK) return s;
   kvc::ApplyArgs a;
   std::memset(&a, 0, sizeof(a));
   fill_pool_view(cache, a.pv);
-  a.items = batch->items_dev;
+  a.items = device_items(batch);
   a.src_tables = batch->src_tables;
   a.dst_tables = batch->dst_tables;
   a.max_blocks = batch->max_blocks;
@@ -466,7 +505,7 @@ kvc_status kvc_apply(const kvc_cache* cache, const kvc_batch* batch, int32_t lay
     for (int32_t i0 = 0; i0 < batch->num_items; i0 += per_launch_items) {
       const int32_t n = std::min(per_launch_items, batch->num_items - i0);
       kvc::ApplyArgs ai = a;
-      ai.items = batch->items_dev + i0;
+      ai.items = device_items(batch) + i0;
       ai.src_tables = batch->src_tables ? batch->src_tables + static_cast<int64_t>(i0) * batch->max_blocks : nullptr;
       ai.dst_tables = batch->dst_tables ? batch->dst_tables + static_cast<int64_t>(i0) * batch->max_blocks : nullptr;
       s = hip_status(kvc::launch_apply(ai, cache->dtype, max_rank, max_tokens, n, stream));
@@ -494,6 +533,8 @@ kvc_status fit_per_layer(const kvc_cache* cache, const kvc_batch* batch, int32_t
   const LayerPlan p = plan_layer_fit(cache, batch, layer_begin, layer_end);
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < p.total)
     return KVC_ERR_WORKSPACE;
+  kvc_status s = upload_items(batch, stream);
+  if (s != KVC_OK) return s;
   char* ws = static_cast<char*>(workspace);
   kvc::LayerFitArgs la;
   std::memset(&la, 0, sizeof(la));
@@ -512,12 +553,11 @@ kvc_status fit_per_layer(const kvc_cache* cache, const kvc_batch* batch, int32_t
   la.eps = reinterpret_cast<double*>(ws + p.off_eps);
   la.vrows = reinterpret_cast<float*>(ws + p.off_vrows);
   la.vsigma = reinterpret_cast<float*>(ws + p.off_vsigma);
-  kvc_status s = KVC_OK;
   for (int32_t i = 0; i < batch->num_items; ++i) {
     const kvc_state& st = batch->items[i].state;
     if (st.rank == 0 || st.num_tokens == 0) continue;
     la.rank = st.rank;
-    la.items = batch->items_dev + i;
+    la.items = device_items(batch) + i;
     la.src_tables = batch->src_tables ? batch->src_tables + static_cast<int64_t>(i) * batch->max_blocks : nullptr;
     la.dst_tables = batch->dst_tables ? batch->dst_tables + static_cast<int64_t>(i) * batch->max_blocks : nullptr;
     for (int32_t l0 = layer_begin; l0 < layer_end; l0 += p.layers_per_group) {
@@ -587,6 +627,8 @@ kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t
   const FitPlan p = plan_fit(cache, batch, layer_begin, layer_end);
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255u) || workspace_bytes < p.total)
     return KVC_ERR_WORKSPACE;
+  s = upload_items(batch, stream);
+  if (s != KVC_OK) return s;
   char* ws = static_cast<char*>(workspace);
 
   kvc::FitArgs fa;
@@ -618,7 +660,7 @@ kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t
     }
     for (int32_t i0 = 0; i0 < batch->num_items; i0 += p.items_per_group) {
       const int32_t n = std::min(p.items_per_group, batch->num_items - i0);
-      fa.items = ea.items = batch->items_dev + i0;
+      fa.items = ea.items = device_items(batch) + i0;
       fa.src_tables = batch->src_tables ? batch->src_tables + static_cast<int64_t>(i0) * batch->max_blocks : nullptr;
       fa.dst_tables = batch->dst_tables ? batch->dst_tables + static_cast<int64_t>(i0) * batch->max_blocks : nullptr;
       ea.num_units = n * fa.num_layers * 2 * cache->num_kv_heads;

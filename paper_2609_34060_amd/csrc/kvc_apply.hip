@@ -132,7 +132,8 @@ __global__ __launch_bounds__(kApplyThreads) void apply_bf16_mfma(ApplyArgs a) {
     const int t = t_begin + (j * kApplyWaves + wave) * 16 + n;
     const bool valid = t < T;
     const int64_t so = valid ? row_offset(a.pv, src_tab, src_off, t, head) : -1;
-    tl.dof = valid ? row_offset(a.pv, dst_tab, dst_off, t, head) : -1;
+    // a row whose source block id is out of range is neither read nor written
+    tl.dof = so >= 0 ? row_offset(a.pv, dst_tab, dst_off, t, head) : -1;
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const u32x4* p = reinterpret_cast<const u32x4*>(src_pool + so + 32 * q + 8 * g);

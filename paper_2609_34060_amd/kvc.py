@@ -24,8 +24,8 @@ KVC_GROUP_HEAD, KVC_GROUP_LAYER = 0, 1
 KVC_MAX_RANK = 128
 KVC_MAX_ANCHORS = 16
 
-EXPORTED = ["kvc_version", "kvc_status_str", "kvc_last_hip_error", "kvc_state_bytes", "kvc_layer_state_bytes",
-            "kvc_dense_bytes",
+EXPORTED = ["kvc_version", "kvc_status_str", "kvc_last_hip_error", "kvc_item_scratch_bytes", "kvc_state_bytes",
+            "kvc_layer_state_bytes", "kvc_dense_bytes",
             "kvc_apply", "kvc_fit_workspace_bytes", "kvc_fit_state", "kvc_chain_workspace_bytes", "kvc_chain",
             "kvc_anchor_weights", "kvc_apply_anchored", "kvc_gate_workspace_bytes", "kvc_gate_distances",
             "kvc_gate_decide", "kvc_pool_create", "kvc_pool_destroy", "kvc_pool_insert", "kvc_pool_record_use",
@@ -62,7 +62,7 @@ class kvc_item(ctypes.Structure):
 
 class kvc_batch(ctypes.Structure):
     _fields_ = [("num_items", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
-                ("items", ctypes.POINTER(kvc_item)), ("items_dev", ctypes.c_void_p),
+                ("items", ctypes.POINTER(kvc_item)), ("item_scratch", ctypes.c_void_p),
                 ("src_tables", ctypes.c_void_p), ("dst_tables", ctypes.c_void_p)]
 
 
@@ -87,6 +87,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.kvc_status_str.restype = ctypes.c_char_p
     lib.kvc_status_str.argtypes = [ctypes.c_int]
     lib.kvc_last_hip_error.restype = i32
+    lib.kvc_item_scratch_bytes.restype = sz
+    lib.kvc_item_scratch_bytes.argtypes = [i32]
     lib.kvc_state_bytes.restype = sz
     lib.kvc_state_bytes.argtypes = [i32, i32, i32, i32, i32, ctypes.c_int]
     lib.kvc_layer_state_bytes.restype = sz
@@ -153,6 +155,22 @@ def _stream_handle(stream) -> ctypes.c_void_p:
     if stream is None:
         stream = torch.cuda.current_stream()
     return ctypes.c_void_p(stream.cuda_stream)
+
+
+# The library copies a batch's host items (pinned memory) into its device scratch on the call's stream, so the copy
+# reads the host bytes only when the stream reaches it.  A Batch passed as a temporary would be freed on return and its
+# pinned block handed to the next allocation before that; calls that use the item scratch therefore keep their batch
+# alive until an event recorded after the call has completed.
+_inflight: list = []
+
+
+def _hold_until_done(stream, batch: "Batch") -> None:
+    if batch._host is None:
+        return
+    ev = torch.cuda.Event()
+    ev.record(torch.cuda.current_stream() if stream is None else stream)
+    _inflight[:] = [x for x in _inflight if not x[0].query()]
+    _inflight.append((ev, batch))
 
 
 # ------------------------------------------------------------------------------------------------------------------
@@ -234,7 +252,9 @@ class State:
 
 
 class Batch:
-    """kvc_batch: host items, their device copy and the block tables (device int32 [n, max_blocks] or None)."""
+    """kvc_batch: host items, the device scratch the library copies them into, and the block tables (device int32
+    [n, max_blocks] or None).  The host items sit in pinned memory when a GPU is present, so the library's copy runs
+    asynchronously on the call's stream; a Batch is not modified after construction."""
 
     def __init__(self, num_tokens: Sequence[int], src_offsets: Sequence[int], dst_offsets: Sequence[int],
                  states: Sequence[State], src_tables: Optional[torch.Tensor] = None,
@@ -242,7 +262,13 @@ class Batch:
                  src_positions: Optional[Sequence[int]] = None, dst_positions: Optional[Sequence[int]] = None):
         n = len(num_tokens)
         self.states = list(states)
-        arr = (kvc_item * max(n, 1))()
+        nbytes = ctypes.sizeof(kvc_item) * max(n, 1)
+        self._host = None
+        if torch.cuda.is_available():
+            self._host = torch.zeros(nbytes, dtype=torch.uint8, pin_memory=True)
+            arr = (kvc_item * max(n, 1)).from_address(self._host.data_ptr())
+        else:
+            arr = (kvc_item * max(n, 1))()
         for i in range(n):
             arr[i].num_tokens = int(num_tokens[i])
             arr[i].src_offset = int(src_offsets[i])
@@ -253,8 +279,7 @@ class Batch:
             arr[i].state = states[i].s
         self._items = arr
         device = device if device is not None else (states[0].basis.device if n else "cuda")
-        raw = bytes(memoryview(arr).cast("B"))[: n * ctypes.sizeof(kvc_item)]
-        self.items_dev = torch.frombuffer(bytearray(raw), dtype=torch.uint8).to(device) if n else None
+        self.item_scratch = torch.empty(kvc_item_scratch_bytes(n), dtype=torch.uint8, device=device) if n else None
         self.src_tables = None if src_tables is None else src_tables.to(torch.int32).contiguous()
         self.dst_tables = None if dst_tables is None else dst_tables.to(torch.int32).contiguous()
         max_blocks = 0
@@ -265,7 +290,7 @@ class Batch:
         if self.src_tables is not None and self.dst_tables is not None:
             assert self.src_tables.shape[1] == self.dst_tables.shape[1]
         self.b = kvc_batch(n, max_blocks, ctypes.cast(arr, ctypes.POINTER(kvc_item)),
-                           self.items_dev.data_ptr() if n else None,
+                           self.item_scratch.data_ptr() if n else None,
                            None if self.src_tables is None else self.src_tables.data_ptr(),
                            None if self.dst_tables is None else self.dst_tables.data_ptr())
 
@@ -276,6 +301,10 @@ class Batch:
 
 def kvc_version() -> int:
     return load().kvc_version()
+
+
+def kvc_item_scratch_bytes(num_items: int) -> int:
+    return load().kvc_item_scratch_bytes(num_items)
 
 
 def kvc_state_bytes(L: int, H: int, d: int, T: int, rank: int, coef_dtype: int) -> int:
@@ -296,6 +325,7 @@ def kvc_apply(cache: Cache, batch: Batch, layer_begin: int = 0, layer_end: Optio
     st = load().kvc_apply(ctypes.byref(cache.c), ctypes.byref(batch.b), layer_begin, layer_end,
                           _stream_handle(stream))
     _check(st, "kvc_apply")
+    _hold_until_done(stream, batch)
 
 
 def kvc_fit_workspace_bytes(cache: Cache, batch: Batch, layer_begin: int = 0, layer_end: Optional[int] = None) -> int:
@@ -312,6 +342,7 @@ def kvc_fit_state(cache: Cache, batch: Batch, layer_begin: int = 0, layer_end: O
     st = load().kvc_fit_state(ctypes.byref(cache.c), ctypes.byref(batch.b), layer_begin, layer_end, mode,
                               ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream_handle(stream))
     _check(st, "kvc_fit_state")
+    _hold_until_done(stream, batch)
 
 
 def kvc_chain_workspace_bytes(first: State, second: State, out: State, layer_begin: int = 0,

@@ -151,9 +151,24 @@ def _cases():
         f.items[0].dst_offset = 50
         return f.apply(), kvc.KVC_ERR_ALIAS
 
-    def null_items_dev(f):
-        f.batch.items_dev = None
+    def null_item_scratch(f):
+        f.batch.item_scratch = None
         return f.apply(), kvc.KVC_ERR_NULL_ARG
+
+    def item_scratch_align(f):
+        f.batch.item_scratch = FAKE + 8
+        return f.apply(), kvc.KVC_ERR_ALIGN
+
+    def overlap_across_items(f):
+        # item 1's destination rows [100, 200) are item 0's source rows [100, 200): a race inside one launch
+        f.items[0].src_offset, f.items[0].dst_offset = 100, 300
+        f.items[1].src_offset, f.items[1].dst_offset = 500, 100
+        return f.apply(), kvc.KVC_ERR_ALIAS
+
+    def overlap_destinations(f):
+        f.items[0].src_offset, f.items[0].dst_offset = 0, 300
+        f.items[1].src_offset, f.items[1].dst_offset = 120, 350
+        return f.apply(), kvc.KVC_ERR_ALIAS
 
     def reserved(f):
         f.items[0].reserved = 1
@@ -201,14 +216,15 @@ def _cases():
 
     return [null_cache, null_batch, head_dim, dtype, layer_range, stride_align, layer_ptr_align, null_layer,
             rank_gt_d, rank_gt_max, state_tokens, state_shape, coef_dtype, coef_align, null_coef, beyond_pool,
-            beyond_table, same_tables, overlap_rows, null_items_dev, reserved, negative_offset, negative_position,
+            beyond_table, same_tables, overlap_rows, null_item_scratch, item_scratch_align, overlap_across_items,
+            overlap_destinations, reserved, negative_offset, negative_position,
             rope_style, rope_reserved, rope_null_freq, rope_nonfinite_freq, grouping_value, state_reserved,
             layer_rank_gt_max]
 
 
 @pytest.mark.parametrize("case", _cases(), ids=lambda c: c.__name__)
 def test_apply_rejects_bad_arguments_before_launch(case):
-    got, expected = case(Fixture())
+    got, expected = case(Fixture(n=2) if case.__name__.startswith("overlap_") else Fixture())
     assert got == expected, (kvc.status_str(got), kvc.status_str(expected))
 
 

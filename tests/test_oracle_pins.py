@@ -437,10 +437,21 @@ def test_memory_example_is_fifty_gib():
     assert got == g["expected_bytes"] == g["expected_gib"] * 2 ** 30
 
 
-def test_lowrank_state_bytes_closed_form():
-    # Section 3.3: O(VNr(L+D)) per pool; per unit r (T + d) numbers plus sigma
-    assert O.lowrank_state_bytes(1, 1, 128, 4096, 32, 2, with_sigma=False) == 2 * (32 * 4096 * 2 + 32 * 128 * 4)
-    assert O.lowrank_state_bytes(32, 8, 128, 32768, 32, 2) == 512 * (32768 * 32 * 2 + 32 * 128 * 4 + 32 * 4)
+@pytest.mark.parametrize("dtype,coef_bytes", [("bf16", 2), ("f32", 4)])
+def test_lowrank_state_bytes_counts_the_arrays_fit_returns(dtype, coef_bytes):
+    """Section 3.3's O(N r (L + D)) state size, pinned to the storage numpy actually holds for the states the oracle's
+    fit produces (coefficients in the cache dtype, float32 basis and sigma), not to a restated formula."""
+    L, H, d, bs, T, r = 2, 3, 16, 8, 40, 5
+    rng = np.random.default_rng(7)
+    nb = 2 * (T // bs)
+    pools = [[O.to_storage(rng.standard_normal((nb, bs, H, d)), dtype) for _ in range(L)] for _ in range(2)]
+    cache = O.Cache(dtype, bs, pools[0], pools[1])
+    states, _ = O.fit(cache, [O.Item(T, 0, T, None, None)], r)
+    st = states[0]
+    assert O.lowrank_state_bytes(L, H, d, T, r, coef_bytes) == st.coef.nbytes + st.basis.nbytes + st.sigma.nbytes
+    assert O.lowrank_state_bytes(L, H, d, T, r, coef_bytes, with_sigma=False) == st.coef.nbytes + st.basis.nbytes
+    # with r << min(T, d) the state is far smaller than the dense segment it replaces (Section 3.1 vs 3.3)
+    assert O.lowrank_state_bytes(L, H, d, T, r, coef_bytes) < O.dense_segment_bytes(L, H, d, T, coef_bytes)
 
 
 def test_effective_rank_and_error_metric():
