@@ -33,8 +33,8 @@
  *   coef  [L][2][H][T_s][r]  (coef_dtype)      basis [L][2][H][r][d] (float32)      sigma [L][2][H][r] (float32)
  *
  * Ownership.  The caller allocates every buffer (pools, tables, states, workspaces, the item scratch); the library
- * allocates no device memory, keeps no pointer after a call returns, holds no global state and may be called from
- * several threads.  Source rows are only read.  The one host-side object is the anchor-pool bookkeeping
+ * allocates no device memory, keeps no pointer after a call returns, holds no global state (except the static
+ * scratch of kvc_gate_distances_noalloc) and may be called from several threads.  Source rows are only read.  The one host-side object is the anchor-pool bookkeeping
  * of kvc_pool_create, owned by the caller until kvc_pool_destroy (not thread-safe per pool).
  *
  * Errors.  Every argument check runs on the host before anything is enqueued; on an error nothing is enqueued and
@@ -59,6 +59,8 @@ extern "C" {
 #define KVC_VERSION 1
 #define KVC_MAX_RANK 128   /* largest r of a state */
 #define KVC_MAX_ANCHORS 16 /* largest V of an anchor set in one call */
+/* Bytes of the static device scratch of kvc_gate_distances_noalloc (one copy per GPU the library runs on). */
+#define KVC_NOALLOC_SCRATCH_BYTES (2u << 20)
 
 typedef enum kvc_status {
   KVC_OK = 0,
@@ -70,7 +72,8 @@ typedef enum kvc_status {
   KVC_ERR_WORKSPACE = 6,   /* workspace missing, misaligned or smaller than the query says */
   KVC_ERR_UNSUPPORTED = 7, /* head_dim other than 64 or 128, or a state grouping or rotary setting the entry point
                               does not take (stated at each entry point) */
-  KVC_ERR_HIP = 8          /* the HIP runtime refused a launch */
+  KVC_ERR_HIP = 8,         /* the HIP runtime refused a launch */
+  KVC_ERR_TOO_LARGE = 9    /* the call needs more than the static scratch of an allocation-free entry point */
 } kvc_status;
 
 typedef enum kvc_dtype { KVC_F32 = 0, KVC_BF16 = 1 } kvc_dtype;
@@ -266,6 +269,17 @@ size_t kvc_gate_workspace_bytes(const kvc_cache* cache, const kvc_anchors* ancho
 kvc_status kvc_gate_distances(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
                               int32_t prefix, int32_t layer_begin, int32_t layer_end, float* distances,
                               void* workspace, size_t workspace_bytes, hipStream_t stream);
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving loops that forbid
+ * hipMalloc): kvc_gate_distances without a workspace argument.  The partial sums live in a static device array of
+ * KVC_NOALLOC_SCRATCH_BYTES bytes that the library holds on every GPU it runs on until the process ends; a call that
+ * needs more than that (kvc_gate_workspace_bytes) returns KVC_ERR_TOO_LARGE before anything is enqueued.  Nothing is
+ * allocated and no allocating routine is called.  Every call on one GPU shares that GPU's array: the kernels write
+ * each partial before it is read, so no contents carry over between calls, but calls that overlap in time on one GPU
+ * (other streams, other threads) race and must be serialised by the caller.  Arguments, results and errors otherwise
+ * as kvc_gate_distances. */
+kvc_status kvc_gate_distances_noalloc(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
+                                      int32_t prefix, int32_t layer_begin, int32_t layer_end, float* distances,
+                                      hipStream_t stream);
 /* Eq. 10-11 on the host: g_v = softmax(-d_v / temperature) over the n compatible anchors (HOST arrays), normalised
  * entropy H = -sum g log2 g / log2 n; returns 1 (accept the correction) when n >= 2 and H <= tau, else 0 (dense
  * prefill).  gate_weights may be NULL; with n < 2 *entropy is set to 1. */

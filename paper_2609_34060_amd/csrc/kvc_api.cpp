@@ -4,6 +4,7 @@
 #include <cstdint>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -416,6 +417,42 @@ struct PoolSlot {
 
 }  // namespace
 
+// Allocation-free gate: the partial sums live in this static array instead of a caller workspace.  Host code never
+// passes the array's name to a kernel (in host code it is only a stand-in for the symbol); it uses the device address
+// that hipGetSymbolAddress returns, taken once per device with that device current.
+static __device__ __align__(256) float scratch[KVC_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of `scratch` on the device of `stream` (the null stream: the current device).
+kvc_status scratch_address(hipStream_t stream, float** out) {
+  int dev = -1;
+  kvc_status s = hip_status(hipStreamGetDevice(stream, &dev));
+  if (s != KVC_OK) return s;
+  if (dev < 0 || dev >= kMaxScratchDevices) return KVC_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = -1;
+    s = hip_status(hipGetDevice(&cur));
+    if (s != KVC_OK) return s;
+    if (cur != dev && (s = hip_status(hipSetDevice(dev))) != KVC_OK) return s;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if ((s = hip_status(e)) != KVC_OK) return s;
+    if (!p) return KVC_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = static_cast<float*>(g_scratch_ptr[dev]);
+  return KVC_OK;
+}
+
+}  // namespace
+
 struct kvc_pool {
   std::vector<PoolSlot> slots;
   int64_t clock = 0;
@@ -439,6 +476,7 @@ const char* kvc_status_str(kvc_status s) {
     case KVC_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case KVC_ERR_UNSUPPORTED: return "head_dim other than 64 or 128, or a grouping or rotary setting the call does not take";
     case KVC_ERR_HIP: return "HIP runtime error";
+    case KVC_ERR_TOO_LARGE: return "the call needs more than the static scratch of the allocation-free entry point";
   }
   return "unknown status";
 }
@@ -782,6 +820,29 @@ kvc_status kvc_gate_distances(const kvc_cache* cache, const kvc_batch* batch, co
   const int chunk = cache->dtype == KVC_BF16 ? kvc::anchor_chunk_tokens() : 64;
   a.gate_chunks = (prefix + chunk - 1) / chunk;
   a.gate_partials = static_cast<float*>(workspace);
+  a.distances = distances;
+  return hip_status(kvc::launch_gate_distances(a, cache->dtype, stream));
+}
+
+kvc_status kvc_gate_distances_noalloc(const kvc_cache* cache, const kvc_batch* batch, const kvc_anchors* anchors,
+                                      int32_t prefix, int32_t layer_begin, int32_t layer_end, float* distances,
+                                      hipStream_t stream) {
+  kvc_status s = check_anchor_call(cache, batch, anchors, layer_begin, layer_end, false, false);
+  if (s != KVC_OK) return s;
+  if (!distances) return KVC_ERR_NULL_ARG;
+  if (prefix < 1 || prefix > anchors->num_tokens) return KVC_ERR_SHAPE;
+  if (layer_end - layer_begin > kvc::kMaxLayersPerLaunch || layer_end == layer_begin) return KVC_ERR_SHAPE;
+  if (kvc_gate_workspace_bytes(cache, anchors, prefix, layer_begin, layer_end) > KVC_NOALLOC_SCRATCH_BYTES)
+    return KVC_ERR_TOO_LARGE;
+  float* partials = nullptr;
+  s = scratch_address(stream, &partials);
+  if (s != KVC_OK) return s;
+  kvc::AnchorArgs a;
+  fill_anchor_args(cache, batch, anchors, layer_begin, layer_end, a);
+  a.num_weighted = prefix;
+  const int chunk = cache->dtype == KVC_BF16 ? kvc::anchor_chunk_tokens() : 64;
+  a.gate_chunks = (prefix + chunk - 1) / chunk;
+  a.gate_partials = partials;
   a.distances = distances;
   return hip_status(kvc::launch_gate_distances(a, cache->dtype, stream));
 }

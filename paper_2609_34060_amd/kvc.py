@@ -16,7 +16,8 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvc.so")
 
 KVC_OK, KVC_ERR_NULL_ARG, KVC_ERR_SHAPE, KVC_ERR_DTYPE, KVC_ERR_ALIGN = 0, 1, 2, 3, 4
-KVC_ERR_ALIAS, KVC_ERR_WORKSPACE, KVC_ERR_UNSUPPORTED, KVC_ERR_HIP = 5, 6, 7, 8
+KVC_ERR_ALIAS, KVC_ERR_WORKSPACE, KVC_ERR_UNSUPPORTED, KVC_ERR_HIP, KVC_ERR_TOO_LARGE = 5, 6, 7, 8, 9
+KVC_NOALLOC_SCRATCH_BYTES = 2 << 20
 KVC_F32, KVC_BF16 = 0, 1
 KVC_FIT_DELTA, KVC_FIT_BASE = 0, 1
 KVC_ROPE_NONE, KVC_ROPE_HALF, KVC_ROPE_PAIRS = 0, 1, 2
@@ -28,6 +29,7 @@ EXPORTED = ["kvc_version", "kvc_status_str", "kvc_last_hip_error", "kvc_item_scr
             "kvc_layer_state_bytes", "kvc_dense_bytes",
             "kvc_apply", "kvc_fit_workspace_bytes", "kvc_fit_state", "kvc_chain_workspace_bytes", "kvc_chain",
             "kvc_anchor_weights", "kvc_apply_anchored", "kvc_gate_workspace_bytes", "kvc_gate_distances",
+            "kvc_gate_distances_noalloc",
             "kvc_gate_decide", "kvc_pool_create", "kvc_pool_destroy", "kvc_pool_insert", "kvc_pool_record_use",
             "kvc_pool_eligible", "kvc_pool_slot"]
 
@@ -116,6 +118,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.kvc_gate_workspace_bytes.argtypes = [pc, pa, i32, i32, i32]
     lib.kvc_gate_distances.restype = ctypes.c_int
     lib.kvc_gate_distances.argtypes = [pc, pb, pa, i32, i32, i32, vp, vp, sz, vp]
+    lib.kvc_gate_distances_noalloc.restype = ctypes.c_int
+    lib.kvc_gate_distances_noalloc.argtypes = [pc, pb, pa, i32, i32, i32, vp, vp]
     lib.kvc_gate_decide.restype = i32
     lib.kvc_gate_decide.argtypes = [ctypes.POINTER(f32), i32, f32, f32, ctypes.POINTER(f32), ctypes.POINTER(f32)]
     lib.kvc_pool_create.restype = vp
@@ -426,6 +430,21 @@ def kvc_gate_distances(cache: Cache, batch: Batch, anchors: Anchors, prefix: int
                                    layer_begin, layer_end, ctypes.c_void_p(distances.data_ptr()),
                                    ctypes.c_void_p(workspace.data_ptr()), workspace.numel(), _stream_handle(stream))
     _check(st, "kvc_gate_distances")
+    return distances
+
+
+def kvc_gate_distances_noalloc(cache: Cache, batch: Batch, anchors: Anchors, prefix: int, layer_begin: int = 0,
+                               layer_end: Optional[int] = None, distances: Optional[torch.Tensor] = None,
+                               stream=None) -> torch.Tensor:
+    """kvc_gate_distances with the library's static scratch instead of a workspace: `distances` (float32 [V], on the
+    device) must be passed by a caller that cannot allocate; it is allocated here only when omitted."""
+    layer_end = cache.num_layers if layer_end is None else layer_end
+    if distances is None:
+        distances = torch.empty(len(anchors.states), dtype=torch.float32, device=cache.k_pools[0].device)
+    st = load().kvc_gate_distances_noalloc(ctypes.byref(cache.c), ctypes.byref(batch.b), ctypes.byref(anchors.a),
+                                           prefix, layer_begin, layer_end, ctypes.c_void_p(distances.data_ptr()),
+                                           _stream_handle(stream))
+    _check(st, "kvc_gate_distances_noalloc")
     return distances
 
 

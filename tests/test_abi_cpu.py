@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for st in range(9):
+    for st in range(10):
         assert kvc.status_str(st)
     assert kvc.status_str(0) == "ok"
 
@@ -379,3 +379,29 @@ def test_per_layer_states_are_refused_where_unsupported():
     f.cache.rope_style = kvc.KVC_ROPE_HALF
     f.cache.rope_inv_freq = ctypes.cast(inv, ctypes.POINTER(ctypes.c_double))
     assert fit() == kvc.KVC_ERR_UNSUPPORTED
+
+
+def test_gate_noalloc_rejects_before_launch():
+    """The allocation-free gate takes the same checks as kvc_gate_distances, and a call whose partial sums would not
+    fit the static scratch is refused with KVC_ERR_TOO_LARGE before anything is enqueued."""
+    lib = kvc.load()
+
+    def call(f, prefix, dist=FAKE + 0x200000):
+        return lib.kvc_gate_distances_noalloc(ctypes.byref(f.cache), ctypes.byref(f.batch), ctypes.byref(f.anchors),
+                                              prefix, 0, f.cache.num_layers, dist, None)
+
+    f = AnchorFixture()
+    assert call(f, 81) == kvc.KVC_ERR_SHAPE
+    assert call(f, 50, dist=None) == kvc.KVC_ERR_NULL_ARG
+    f.states[0].num_kv_heads = 5
+    assert call(f, 50) == kvc.KVC_ERR_SHAPE
+    # 128 layers x 64 KV heads x 16 anchors: 4 partials of 4 bytes per (layer, head, anchor) fill 2 MiB exactly
+    # (2048 tokens = four 512-token chunks), one more chunk does not fit
+    f = AnchorFixture(V=16, Ts=4000, L=128, H=64, T=4096, nb=300)
+    for v in range(16):
+        f.states[v].num_tokens = 4096
+    need = lib.kvc_gate_workspace_bytes(ctypes.byref(f.cache), ctypes.byref(f.anchors), 2048, 0, 128)
+    assert need == kvc.KVC_NOALLOC_SCRATCH_BYTES
+    assert lib.kvc_gate_workspace_bytes(ctypes.byref(f.cache), ctypes.byref(f.anchors), 2049, 0, 128) > need
+    assert call(f, 2049) == kvc.KVC_ERR_TOO_LARGE
+    assert "static scratch" in kvc.status_str(kvc.KVC_ERR_TOO_LARGE)
