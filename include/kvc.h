@@ -210,8 +210,10 @@ size_t kvc_fit_workspace_bytes(const kvc_cache* cache, const kvc_batch* batch, i
  * Z = R(-dst_position) C_dst - R(-src_position) C_src (KVC_FIT_BASE: Z = R(-dst_position) C_dst), so the state is in
  * canonical coordinates.  Per-layer states (KVC_GROUP_LAYER, every item of the call): Z = [Z_0 ... Z_{H-1}] with the
  * heads side by side, D = H d <= 1024, rank <= 112, no rotary keys (KVC_ERR_UNSUPPORTED otherwise; float32 caches
- * also need rank * D * 4 <= 160 KiB); the SVD is reached by a fixed number of subspace iterations on Z^T Z followed
- * by a Rayleigh-Ritz step, exact up to (sigma_{k+1} / sigma_r)^16 with k = 64 (rank <= 48) or 128. */
+ * also need rank * D * 4 <= 160 KiB); the SVD is reached by subspace iteration on Z^T Z (k = 64 columns for
+ * rank <= 48, else 128) with a Rayleigh-Ritz step after 4 iterations and every 4 more, stopping per layer unit once
+ * every top-r Ritz pair (theta, y) has ||Z^T Z y - theta y|| <= 1e-6 theta_1, or after 48 iterations (a spectrum with
+ * no gap between sigma_r and sigma_{k+1}); the kernels of a stopped unit return at once. */
 kvc_status kvc_fit_state(const kvc_cache* cache, const kvc_batch* batch, int32_t layer_begin, int32_t layer_end,
                          kvc_fit_mode mode, void* workspace, size_t workspace_bytes, hipStream_t stream);
 

@@ -179,7 +179,8 @@ FitPlan plan_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int32_t le)
 struct LayerPlan {
   int32_t layers_per_group = 1, part_tokens = 256, max_parts = 1, k = 64;
   size_t units = 0, off_partials = 0, off_gram = 0, off_x = 0, off_y = 0, off_h = 0, off_spart = 0, off_eps = 0,
-         off_vrows = 0, off_vsigma = 0, off_reflect = 0, off_beta = 0, off_vecs = 0, total = 0;
+         off_vrows = 0, off_vsigma = 0, off_reflect = 0, off_beta = 0, off_vecs = 0, off_resid = 0, off_conv = 0,
+         off_iters = 0, total = 0;
 };
 
 // Which calls the per-layer path takes (every item per layer, no rotary keys, D = H d <= 1024, rank + 16 <= k).
@@ -240,6 +241,12 @@ LayerPlan plan_layer_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int
   off = align256(off + U * k * sizeof(double));
   p.off_vecs = off;
   off = align256(off + U * KVC_MAX_RANK * k * sizeof(double));
+  p.off_resid = off;
+  off = align256(off + U * KVC_MAX_RANK * sizeof(double));
+  p.off_conv = off;
+  off = align256(off + U * sizeof(int32_t));
+  p.off_iters = off;
+  off = align256(off + U * sizeof(int32_t));
   p.total = off;
   return p;
 }
@@ -591,6 +598,9 @@ kvc_status fit_per_layer(const kvc_cache* cache, const kvc_batch* batch, int32_t
   la.eps = reinterpret_cast<double*>(ws + p.off_eps);
   la.vrows = reinterpret_cast<float*>(ws + p.off_vrows);
   la.vsigma = reinterpret_cast<float*>(ws + p.off_vsigma);
+  la.resid = reinterpret_cast<double*>(ws + p.off_resid);
+  la.conv = reinterpret_cast<int32_t*>(ws + p.off_conv);
+  la.iters = reinterpret_cast<int32_t*>(ws + p.off_iters);
   for (int32_t i = 0; i < batch->num_items; ++i) {
     const kvc_state& st = batch->items[i].state;
     if (st.rank == 0 || st.num_tokens == 0) continue;

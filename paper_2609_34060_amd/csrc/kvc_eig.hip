@@ -324,6 +324,7 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   float* s_rbeta = s_rb + kReflChunk * N;
 
   const int u = blockIdx.x;
+  if (a.skip && a.skip[u]) return;  // whole workgroup
   const UnitTarget tg = eig_target(a, u);
   const int r = tg.rank;
   if (r <= 0) return;

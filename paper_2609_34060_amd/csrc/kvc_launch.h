@@ -67,8 +67,15 @@ struct LayerFitArgs {
   double* eps;                 // [unit] perturbation size of the Cholesky QR
   float* vrows;                // [unit][rank][k] eigenvectors of hmat (rows)
   float* vsigma;               // [unit][rank]
+  double* resid;               // [unit][KVC_MAX_RANK] residual norms of the Ritz pairs of the last check
+  int32_t* conv;               // [unit] 0 while iterating, 1 once the top-r Ritz pairs met the tolerance, 2 at the cap
+  int32_t* iters;              // [unit] subspace iterations done when the unit stopped
 };
-constexpr int kLayerIters = 8;  // subspace iterations before the Rayleigh-Ritz step
+// Subspace iteration with Rayleigh-Ritz checks: the first check after kLayerFirstIters iterations, then every
+// kLayerCheckEvery, until every top-r Ritz pair (theta, y) has ||G y - theta y|| <= kLayerTol * theta_1 or
+// kLayerMaxIters iterations are done.  A unit that has stopped skips the remaining launches.
+constexpr int kLayerFirstIters = 4, kLayerCheckEvery = 4, kLayerMaxIters = 48;
+constexpr double kLayerTol = 1e-6;
 struct EigArgs;
 hipError_t launch_layer_gram(const LayerFitArgs& a, kvc_dtype dtype, hipStream_t stream);
 hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipStream_t stream);
@@ -92,6 +99,7 @@ struct EigArgs {
   double* reflect_beta;       // workspace [unit][n]
   double* vecs;               // workspace [unit][KVC_MAX_RANK][n]
   uint32_t seed;
+  const int32_t* skip;        // [unit] nonzero: leave the unit's outputs as they are (null: every unit)
 };
 size_t eig_lds_bytes(int n);
 hipError_t launch_eig(const EigArgs& a, hipStream_t stream);

@@ -566,6 +566,10 @@ __global__ __launch_bounds__(kLayerThreads) void sub_init(LayerFitArgs a) {
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
   const int u = blockIdx.y;
   const int e = blockIdx.x * kLayerThreads + threadIdx.x;
+  if (e == 0) {
+    a.conv[u] = 0;
+    a.iters[u] = 0;
+  }
   if (e >= a.k * DL) return;
   a.y[(size_t)u * a.k * DL + e] = hash_uniform((uint32_t)u, (uint32_t)(e / DL), (uint32_t)(e % DL));
 }
@@ -579,6 +583,7 @@ __global__ __launch_bounds__(kLayerThreads) void sub_gemm(LayerFitArgs a) {
   __shared__ double s_g[TR][KB + 1], s_x[KB][TC + 1];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
   const int f0 = blockIdx.x * TR, c0 = blockIdx.y * TC, u = blockIdx.z;
+  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
   const double* G = a.gram + (size_t)u * DL * DL;
   const double* X = a.x + (size_t)u * a.k * DL;
   double* Y = a.y + (size_t)u * a.k * DL;
@@ -670,6 +675,7 @@ __global__ __launch_bounds__(kScaleThreads) void cqr_scale(LayerFitArgs a) {
   constexpr int NB = 8;
   __shared__ double red[kScaleThreads / kWave];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim, u = blockIdx.x;
+  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
   const size_t n = (size_t)a.k * DL;
   const double* Y = a.y + (size_t)u * n;
   double ss[NB];
@@ -697,6 +703,7 @@ __global__ __launch_bounds__(kCqrThreads) void cqr_syrk(LayerFitArgs a, const do
   __shared__ double tile[K][kCqrSub + 1];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
   const int chunk = blockIdx.x, u = blockIdx.y, tid = threadIdx.x, bi = tid / 16, bj = tid % 16;
+  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
   const int f_begin = chunk * kCqrChunk, f_end = min(DL, f_begin + kCqrChunk);
   const double* Y = src + (size_t)u * K * DL;
   const double eps = perturb ? a.eps[u] : 0.0;
@@ -744,6 +751,7 @@ __global__ __launch_bounds__(kWave) void cqr_factor(LayerFitArgs a, int shifted)
   extern __shared__ double fs[];     // [K][K + 1]
   const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
   const int u = blockIdx.x, tid = threadIdx.x;
+  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
   const double* P = a.spart + (size_t)u * nch * K * K;
   for (int e0 = tid; e0 < K * K; e0 += NB * kWave) {
     double s[NB];
@@ -845,6 +853,7 @@ __global__ __launch_bounds__(kWave) void cqr_factor_reg64(LayerFitArgs a, int sh
   constexpr int K = 64;
   const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
   const int u = blockIdx.x, lane = threadIdx.x;
+  if (a.conv[u]) return;  // whole wave: the unit has stopped
   const double* P = a.spart + (size_t)u * nch * K * K;
   double col[K];
 #pragma unroll
@@ -906,6 +915,7 @@ __global__ __launch_bounds__(kCqrThreads) void cqr_apply(LayerFitArgs a, const d
   double* tw = as_ + K * (kCqrRows + 1);     // [kCqrWChunk][K]
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
   const int f0 = blockIdx.x * kCqrRows, u = blockIdx.y, tid = threadIdx.x, ti = tid / 16, tj = tid % 16;
+  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
   const double* Y = src + (size_t)u * K * DL;
   const double* W = a.hmat + (size_t)u * K * K;
   const double eps = perturb ? a.eps[u] : 0.0;
@@ -952,6 +962,7 @@ __global__ __launch_bounds__(kCqrThreads) void sub_rayleigh(LayerFitArgs a) {
   __shared__ double tx[K][kCqrTile + 1], ty[K][kCqrTile + 1];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
   const int u = blockIdx.x, tid = threadIdx.x, bi = tid / 16, bj = tid % 16;
+  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
   const double* X = a.x + (size_t)u * K * DL;
   const double* Y = a.y + (size_t)u * K * DL;
   double* Hm = a.hmat + (size_t)u * K * K;
@@ -982,8 +993,9 @@ __global__ __launch_bounds__(kCqrThreads) void sub_rayleigh(LayerFitArgs a) {
     }
     __syncthreads();
   }
-  // X^T Y into the unit's Y area (no longer read), then the symmetric part
-  double* raw = a.y + (size_t)u * K * DL;
+  // X^T Y into the unit's Cholesky QR partials (idle until the next iteration; Y = G X is kept for the residual
+  // check), then the symmetric part
+  double* raw = a.spart + (size_t)u * ((DL + kCqrChunk - 1) / kCqrChunk) * K * K;
 #pragma unroll
   for (int i = 0; i < B; ++i)
 #pragma unroll
@@ -992,6 +1004,67 @@ __global__ __launch_bounds__(kCqrThreads) void sub_rayleigh(LayerFitArgs a) {
   for (int e = tid; e < K * K; e += kCqrThreads) {
     const int i = e / K, j = e - i * K;
     Hm[e] = 0.5 * (raw[i * K + j] + raw[j * K + i]);
+  }
+}
+
+// Residual of Ritz pair j of unit u: with w = X v_j (v_j from the eigensolver) and z = Y v_j = G w, the Rayleigh
+// quotient theta = w.z / w.w and ||z - theta w|| / ||w||, both in fp64 (the float32 Ritz vector puts the floor of this
+// residual near 1e-7 theta_1).  One workgroup per (j, unit); thread t owns features t + 256 q.
+__global__ __launch_bounds__(kLayerThreads) void sub_check(LayerFitArgs a) {
+  constexpr int MAXF = 1024 / kLayerThreads;
+  __shared__ double s_red[kLayerWaves];
+  __shared__ double s_v[128];
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, k = a.k;
+  const int j = blockIdx.x, u = blockIdx.y;
+  if (a.conv[u]) return;  // whole workgroup
+  const float* v = a.vrows + ((size_t)u * a.rank + j) * k;
+  for (int c = threadIdx.x; c < k; c += kLayerThreads) s_v[c] = (double)v[c];
+  __syncthreads();
+  const double* X = a.x + (size_t)u * k * DL;
+  const double* Y = a.y + (size_t)u * k * DL;
+  double w[MAXF], z[MAXF], ww = 0.0, wz = 0.0;
+#pragma unroll
+  for (int q = 0; q < MAXF; ++q) {
+    const int f = threadIdx.x + q * kLayerThreads;
+    w[q] = z[q] = 0.0;
+    if (f < DL) {
+      for (int c = 0; c < k; ++c) {
+        w[q] = fma(s_v[c], X[(size_t)c * DL + f], w[q]);
+        z[q] = fma(s_v[c], Y[(size_t)c * DL + f], z[q]);
+      }
+    }
+    ww = fma(w[q], w[q], ww);
+    wz = fma(w[q], z[q], wz);
+  }
+  ww = block_sum<kLayerWaves>(ww, s_red);
+  wz = block_sum<kLayerWaves>(wz, s_red);
+  const double theta = ww > 0.0 ? wz / ww : 0.0;
+  double rr = 0.0;
+#pragma unroll
+  for (int q = 0; q < MAXF; ++q) {
+    const double e = fma(-theta, w[q], z[q]);
+    rr = fma(e, e, rr);
+  }
+  rr = block_sum<kLayerWaves>(rr, s_red);
+  if (threadIdx.x == 0) a.resid[(size_t)u * KVC_MAX_RANK + j] = ww > 0.0 ? sqrt(rr / ww) : 0.0;
+}
+
+// Stop a unit once every top-r residual is at most kLayerTol * theta_1 (theta_1 = sigma_1^2 of the Ritz step), or at
+// the iteration cap; `done` is the number of subspace iterations so far.
+__global__ __launch_bounds__(kWave) void sub_decide(LayerFitArgs a, int done, int last) {
+  const int u = blockIdx.x, lane = threadIdx.x;
+  if (a.conv[u]) return;  // whole wave
+  double m = 0.0;
+  for (int j = lane; j < a.rank; j += kWave) m = fmax(m, a.resid[(size_t)u * KVC_MAX_RANK + j]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) m = fmax(m, __shfl_xor(m, o, kWave));
+  if (lane == 0) {
+    const double s1 = (double)a.vsigma[(size_t)u * a.rank];
+    const bool ok = m <= kLayerTol * s1 * s1;
+    if (ok || last) {
+      a.conv[u] = ok ? 1 : 2;
+      a.iters[u] = done;
+    }
   }
 }
 
@@ -1298,16 +1371,25 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
   };
   orth(0u);
   const dim3 ggrid((DL + kGemmRows - 1) / kGemmRows, a.k / 64, a.num_units);
-  for (int it = 0; it < kLayerIters; ++it) {
+  EigArgs es = ea;
+  es.skip = a.conv;  // units that have stopped keep the Ritz pairs of their last check
+  int done = 0;
+  while (done < kLayerMaxIters) {
+    const int n = done == 0 ? kLayerFirstIters : kLayerCheckEvery;
+    for (int it = 0; it < n; ++it) {
+      hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
+      orth((uint32_t)(++done));
+    }
+    // Rayleigh-Ritz on span(X) and the residuals of its top-r pairs (Y = G X is kept by the Ritz step)
     hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
-    orth((uint32_t)(it + 1));
+    if (a.k == 64) hipLaunchKernelGGL(sub_rayleigh<64>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
+    else hipLaunchKernelGGL(sub_rayleigh<128>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if ((e = launch_eig(es, stream)) != hipSuccess) return e;
+    hipLaunchKernelGGL(sub_check, dim3(a.rank, a.num_units), dim3(kLayerThreads), 0, stream, a);
+    hipLaunchKernelGGL(sub_decide, dim3(a.num_units), dim3(kWave), 0, stream, a, done, done >= kLayerMaxIters);
   }
-  hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
-  if (a.k == 64) hipLaunchKernelGGL(sub_rayleigh<64>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
-  else hipLaunchKernelGGL(sub_rayleigh<128>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if ((e = launch_eig(ea, stream)) != hipSuccess) return e;
   hipLaunchKernelGGL(sub_basis, dim3(a.rank, a.num_units), dim3(kLayerThreads), 0, stream, a);
   return hipGetLastError();
 }
