@@ -11,7 +11,10 @@ Printed: one JSON line.  `value` is the corrected-KV throughput of kvc_apply in 
 destination rows, coefficients at their stored width, bases) measured with HIP events on the launch stream; fit
 throughput is token*layers/s.  `roofline` is kvc_apply against the 8 TB/s HBM peak; `cpu_baseline` is the CPU
 oracle timed on a bounded sample of the same workload on this host.  `copy_ceiling` gives, on the same GPU, the
-rate of a pure bit copy through the same block tables (kvc_apply with a rank-0 state) and of a contiguous copy.
+rate of a pure bit copy through the same block tables (kvc_apply with a rank-0 state) and of hand-written copy
+kernels (contiguous, read-only, write-only, paged whole blocks in several work orders, paged per-head rows).
+`verify_last_apply` checks the output of the last timed apply against the oracle on a sampled layer and KV head;
+`configs` times the apply on the 8B/4K, VLM (rotated data sets) and serving-batch shapes.
 """
 import argparse
 import hashlib
@@ -70,14 +73,22 @@ def _weights_bytes(L, H, d, T, V, r, elem=2, coef_elem=2):
     return rows * (d * elem + V * r * coef_elem) + L * 2 * T * V * 4 + V * L * 2 * H * r * d * 4
 
 
-def anchor_pool_measurement(args, kvc, synth, torch):
+def anchor_pool_measurement(args, kvc, synth, torch, rope=False):
     """The anchor-pool path of one transfer at the paper's anchor setting (V anchors of rank r on a shared segment):
-    token-wise weights from the anchors' bases, the anchored apply of Eq. 8, and the gate distances of Eq. 9."""
+    token-wise weights from the anchors' bases, the anchored apply of Eq. 8, and the gate distances of Eq. 9.  With
+    rope the keys carry a rotary encoding (rotate-half, theta 5e5) and the segment sits at position 2048 in the source
+    agent and 6144 in the target, so the weights compare canonical keys and the apply rotates every key row."""
+    import numpy as np
     w = synth.WORKLOADS[args.anchor_workload].with_(num_agents=1)
     L, H, d, T, r, V = w.num_layers, w.num_kv_heads, w.head_dim, w.seq_tokens[0], w.rank, args.anchors
     r = args.anchor_rank
     pc = synth.build_paged(w, device="cuda", num_output_agents=1)
-    cache = kvc.Cache(pc.k_pools, pc.v_pools)
+    if rope:
+        inv = 500000.0 ** (-np.arange(0, d, 2, dtype=np.float64) / d)
+        cache = kvc.Cache(pc.k_pools, pc.v_pools, rope_style=kvc.KVC_ROPE_HALF, rope_inv_freq=inv)
+    else:
+        cache = kvc.Cache(pc.k_pools, pc.v_pools)
+    ps, pd = (2048, 6144) if rope else (0, 0)
     src, dst = pc.seqs[(0, 0)], pc.seqs[(0, 100)]
     tab = lambda s: pc.tables[[s.table_row]]
     sdt = torch.bfloat16
@@ -94,8 +105,10 @@ def anchor_pool_measurement(args, kvc, synth, torch):
     anchors = kvc.Anchors(bases, T, L)
     anchors_d = anchors.with_states(deltas)
     empty = kvc.State.empty(L, H, d, 0, 0, sdt, "cuda")
-    bw = kvc.Batch([T], [src.offset], [src.offset], [empty], tab(src), tab(src))
-    ba = kvc.Batch([T], [src.offset], [dst.offset], [empty], tab(src), tab(dst))
+    bw = kvc.Batch([T], [src.offset], [src.offset], [empty], tab(src), tab(src), src_positions=[ps],
+                   dst_positions=[ps])
+    ba = kvc.Batch([T], [src.offset], [dst.offset], [empty], tab(src), tab(dst), src_positions=[ps],
+                   dst_positions=[pd])
     prefix = T
     gws = torch.empty(max(1, kvc.kvc_gate_workspace_bytes(cache, anchors, prefix)), dtype=torch.uint8, device="cuda")
     dist = torch.empty(V, dtype=torch.float32, device="cuda")
@@ -120,8 +133,10 @@ def anchor_pool_measurement(args, kvc, synth, torch):
     ab, wb = _anchored_bytes(L, H, d, T, V, r), _weights_bytes(L, H, d, T, V, r)
     del pc, cache, bases, deltas, anchors, anchors_d
     torch.cuda.empty_cache()
+    where = (f"; rotary keys (rotate-half, theta 5e5), segment at position {ps} in the source and {pd} in the target"
+             if rope else "")
     return {"workload": f"{w.name}: {L} layers x {H} KV heads x head_dim {d}, {T} shared tokens, {V} anchors of "
-                        f"rank {r} (bf16 paged); gate prefix {prefix}",
+                        f"rank {r} (bf16 paged); gate prefix {prefix}{where}",
             "gate_ms": round(gate_ms, 4), "weights_ms": round(weights_ms, 4), "apply_anchored_ms": round(apply_ms, 4),
             "apply_anchored_gbps": round(ab / (apply_ms * 1e-3) / 1e9, 2),
             "apply_anchored_frac": round(ab / (apply_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
@@ -157,11 +172,16 @@ def copy_ceiling(args, kvc, torch, cache, w, batch):
     del src, dst
     torch.cuda.empty_cache()
     pg, cg = 2 * row_bytes / (paged_ms * 1e-3) / 1e9, 2 * row_bytes / (contig_ms * 1e-3) / 1e9
-    return {"bytes": 2 * row_bytes,
-            "paged_rank0_apply_ms": round(paged_ms, 4), "paged_rank0_apply_gbps": round(pg, 2),
-            "paged_rank0_apply_frac": round(pg / HBM_PEAK_GBPS, 4),
-            "contiguous_copy_ms": round(contig_ms, 4), "contiguous_copy_gbps": round(cg, 2),
-            "contiguous_copy_frac": round(cg / HBM_PEAK_GBPS, 4)}
+    out = {"bytes": 2 * row_bytes,
+           "paged_rank0_apply_ms": round(paged_ms, 4), "paged_rank0_apply_gbps": round(pg, 2),
+           "paged_rank0_apply_frac": round(pg / HBM_PEAK_GBPS, 4),
+           "torch_copy_ms": round(contig_ms, 4), "torch_copy_gbps": round(cg, 2),
+           "torch_copy_frac": round(cg / HBM_PEAK_GBPS, 4)}
+    # the hand-written copies of csrc/kvc_copybench.hip: 4 GiB read + 4 GiB written (read-only / write-only 4 GiB)
+    from paper_2609_34060_amd import copybench
+    out["kernels"] = copybench.ceilings("cuda", gib=4.0, reps=max(5, args.steps // 2))
+    torch.cuda.empty_cache()
+    return out
 
 
 def rope_measurement(args, kvc, torch, pc, w, state, batch):
@@ -288,6 +308,135 @@ def chain_study(args, kvc, synth, torch):
     return res
 
 
+def _progress(msg):
+    """One line on stderr as each measurement ends (the JSON line alone goes to stdout)."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
+
+
+def _timed_calls(torch, fns, steps, warmup):
+    """Mean, p10/p50/p90 milliseconds of fns[k % len(fns)]() over `steps` calls (HIP events on the current stream)."""
+    import numpy as np
+    for k in range(warmup):
+        fns[k % len(fns)]()
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+    for k in range(steps):
+        ev[k][0].record()
+        fns[k % len(fns)]()
+        ev[k][1].record()
+    torch.cuda.synchronize()
+    ms = [e[0].elapsed_time(e[1]) for e in ev]
+    return sum(ms) / steps, [round(float(v), 4) for v in np.percentile(np.asarray(ms), [10, 50, 90])]
+
+
+def secondary_apply(args, kvc, synth, torch, name, rotate):
+    """kvc_apply alone on another configuration's shapes: one edge's state is fitted (untimed), then the apply is timed.
+    With rotate > 1 that many independent data sets (caches, tables, states) are cycled, so that a working set smaller
+    than the 256 MB MALL cannot stay cached between iterations."""
+    w = synth.WORKLOADS[name].with_(num_agents=2)
+    L, H, d, T, r = w.num_layers, w.num_kv_heads, w.head_dim, w.seq_tokens[0], w.rank
+    sets, calls = [], []
+    for s_ in range(rotate):
+        pc = synth.build_paged(w.with_(seed=w.seed + 7919 * s_), device="cuda", num_output_agents=1)
+        cache = kvc.Cache(pc.k_pools, pc.v_pools)
+        st = kvc.State.empty(L, H, d, T, r, torch.bfloat16, "cuda")
+        src, dst, out = pc.seqs[(0, 0)], pc.seqs[(0, 1)], pc.seqs[(0, 100)]
+        tab = lambda q, pc=pc: pc.tables[[q.table_row]]
+        kvc.kvc_fit_state(cache, kvc.Batch([T], [src.offset], [dst.offset], [st], tab(src), tab(dst)))
+        ab = kvc.Batch([T], [src.offset], [out.offset], [st], tab(src), tab(out))
+        sets.append((pc, cache, st, ab))
+        calls.append(lambda cache=cache, ab=ab: kvc.kvc_apply(cache, ab))
+    torch.cuda.synchronize()
+    ms, q = _timed_calls(torch, calls, args.steps, min(args.warmup, 10))
+    b = _apply_bytes(L, H, d, T, r)
+    gbps = b / (ms * 1e-3) / 1e9
+    del sets, calls
+    torch.cuda.empty_cache()
+    return {"workload": f"{w.name}: {L} layers x {H} KV heads x head_dim {d}, {T} shared tokens, rank {r}, bf16 paged "
+                        f"(block {w.block_size}, shuffled table); {rotate} data set(s) rotated",
+            "apply_ms": round(ms, 4), "apply_ms_p10_p50_p90": q, "apply_bytes": b, "apply_gbps": round(gbps, 2),
+            "apply_frac": round(gbps / HBM_PEAK_GBPS, 4)}
+
+
+def serving_measurement(args, kvc, synth, torch, window=2):
+    """The concurrent serving batch: 64 requests (lengths ~ U[1024, 16384]) sharing one block pool, rank 64, one hop.
+    The whole cache (32 layers, about 292 GB over four agents) does not fit in HBM, so a window of `window` layers is
+    generated; per layer the batched fit of all 64 requests and one kvc_apply launch over all 64 requests are timed,
+    and the full-model figures are the per-layer times x 32."""
+    w = synth.WORKLOADS["serving"]
+    full_layers = w.num_layers
+    w = w.with_(num_layers=window, num_agents=2)
+    H, d, r, Q = w.num_kv_heads, w.head_dim, w.rank, w.num_requests
+    pc = synth.build_paged(w, device="cuda", num_output_agents=1)
+    cache = kvc.Cache(pc.k_pools, pc.v_pools)
+    rows = lambda seqs: pc.tables[[pc.seqs[s_].table_row for s_ in seqs]]
+    src, dst, out = [(q, 0) for q in range(Q)], [(q, 1) for q in range(Q)], [(q, 100) for q in range(Q)]
+    lens = list(w.seq_tokens)
+    st = [kvc.State.empty(window, H, d, lens[q], r, torch.bfloat16, "cuda") for q in range(Q)]
+    fb = kvc.Batch(lens, [pc.seqs[s_].offset for s_ in src], [pc.seqs[s_].offset for s_ in dst], st, rows(src),
+                   rows(dst))
+    ab = kvc.Batch(lens, [pc.seqs[s_].offset for s_ in src], [pc.seqs[s_].offset for s_ in out], st, rows(src),
+                   rows(out))
+    ws = torch.empty(kvc.kvc_fit_workspace_bytes(cache, fb, 0, 1), dtype=torch.uint8, device="cuda")
+    fit_calls = [lambda l=l: kvc.kvc_fit_state(cache, fb, l, l + 1, workspace=ws) for l in range(window)]
+    apply_calls = [lambda l=l: kvc.kvc_apply(cache, ab, l, l + 1) for l in range(window)]
+    n = max(window, args.steps // 2)
+    fit_ms, fq = _timed_calls(torch, fit_calls, n, window)
+    apply_ms, aq = _timed_calls(torch, apply_calls, max(window, args.steps), window)
+    tok = sum(lens)
+    b = tok * 2 * H * (2 * d * 2 + r * 2) + Q * 2 * H * r * d * 4
+    gbps = b / (apply_ms * 1e-3) / 1e9
+    del ws, st, fb, ab, pc, cache
+    torch.cuda.empty_cache()
+    return {"workload": f"serving: {Q} requests (sum of lengths {tok}, ~U[1024, 16384]) x 8 KV heads x head_dim {d}, "
+                        f"rank {r}, bf16 paged shared pool; one hop; {window} of {full_layers} layers generated",
+            "apply_ms_per_layer_launch": round(apply_ms, 4), "apply_ms_p10_p50_p90": aq,
+            "apply_bytes_per_launch": b, "apply_gbps": round(gbps, 2), "apply_frac": round(gbps / HBM_PEAK_GBPS, 4),
+            "fit_ms_per_layer": round(fit_ms, 4), "fit_ms_p10_p50_p90": fq,
+            "fit_token_layers_per_s": round(tok / (fit_ms * 1e-3), 1),
+            "full_model_ms": {"fit": round(fit_ms * full_layers, 3), "apply": round(apply_ms * full_layers, 3)}}
+
+
+def verify_last_apply(pc, w, edge, out_seq, layer, head):
+    """The output of the last timed apply against the oracle on one sampled (layer, KV head): the oracle fits every
+    edge 1 .. `edge` from the ground-truth caches, composes them as the benchmark does (T_1 = S_1, T_i = chain(T_{i-1},
+    S_i) at the same rank) and applies the result to the first agent's rows."""
+    import numpy as np
+    import torch
+    from oracle import kvc_oracle as O
+
+    def np_storage(t):
+        return t.detach().to("cpu").contiguous().view(torch.int16).numpy().view(np.uint16).copy()
+
+    t0 = time.perf_counter()
+    k = np_storage(pc.k_pools[layer][:, :, head:head + 1, :])
+    v = np_storage(pc.v_pools[layer][:, :, head:head + 1, :])
+    cache = O.Cache("bf16", w.block_size, [k], [v])
+    tabs = pc.tables.cpu().numpy().astype(np.int64)
+    T, r = w.seq_tokens[0], w.rank
+
+    def item(a, b, st=None):
+        return O.Item(T, pc.seqs[a].offset, pc.seqs[b].offset, tabs[pc.seqs[a].table_row],
+                      tabs[pc.seqs[b].table_row], st)
+
+    comp = None
+    for i in range(1, edge + 1):
+        s_i = O.fit(cache, [item((0, i - 1), (0, i))], r)[0][0]
+        comp = s_i if comp is None else O.chain(comp, s_i, r)[0]
+    ref = O.apply(cache, [item((0, 0), out_seq, comp)])
+    it = item((0, 0), out_seq)
+    worst = teeth = 0.0
+    for kv in range(2):
+        g = O.to_f64(O.read_rows(cache, 0, kv, 0, it.dst_table, it.dst_offset, T), "bf16")
+        e = O.to_f64(O.read_rows(ref, 0, kv, 0, it.dst_table, it.dst_offset, T), "bf16")
+        s_ = O.to_f64(O.read_rows(cache, 0, kv, 0, it.src_table, it.src_offset, T), "bf16")
+        worst = max(worst, O.max_relative_error(g, e))
+        teeth = max(teeth, O.max_relative_error(s_, e))
+    return {"layer": layer, "head": head, "edge": edge, "max_rel_err": float(f"{worst:.3e}"), "bar": 1e-2,
+            "uncorrected_rel_err": float(f"{teeth:.3e}"), "ok": bool(worst <= 1e-2),
+            "oracle_seconds": round(time.perf_counter() - t0, 2)}
+
+
 def cpu_baseline(pc, w, sample_layers=(0, 1)):
     """The oracle as it stands on a bounded sample of the same workload: `sample_layers` (every K/V head) of the
     first two edges -- fit S_1 and S_2, compose T_2 = chain(S_1, S_2), apply T_2 to the first agent's cache."""
@@ -323,8 +472,16 @@ def cpu_baseline(pc, w, sample_layers=(0, 1)):
     nl = len(ls)
     apply_gbps = _apply_bytes(nl, w.num_kv_heads, w.head_dim, T, w.rank) / (t4 - t3) / 1e9
     fit_s = (t2 - t0) / 2
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
     return {
         "value": round(apply_gbps, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+        "host_cpus": os.cpu_count(), "cpu_model": model,
+        "cores_note": "cores = BLAS threads the oracle's linear algebra used; host_cpus = os.cpu_count()",
         "sample": f"layers {ls} of {w.num_layers} (all K/V heads), edges 1-2: fit {fit_s:.2f} s per edge, "
                   f"chain {t3 - t2:.2f} s, apply {t4 - t3:.2f} s (value = apply GB/s on the sample)",
         "fit_token_layers_per_s": round(T * nl / fit_s, 1),
@@ -347,6 +504,10 @@ def main():
     ap.add_argument("--no-rope", action="store_true", help="skip the rotary re-alignment measurement")
     ap.add_argument("--no-layer-fit", action="store_true", help="skip the per-layer factorisation measurement")
     ap.add_argument("--no-chain-study", action="store_true", help="skip the chained / non-chained error study")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the apply timings on the 8B/4K, VLM and serving-batch shapes")
+    ap.add_argument("--no-verify", action="store_true",
+                    help="skip the oracle check of the last timed apply's output on a sampled layer and head")
     ap.add_argument("--no-copy-ceiling", action="store_true",
                     help="skip the same-GPU copy ceilings (rank-0 apply through the tables, contiguous copy)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -423,6 +584,7 @@ def main():
         step(args.warmup + k, evs[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    _progress(f"{args.steps} timed steps done")
     fit_all = [e[0].elapsed_time(e[1]) for e in evs]
     chain_all = [e[1].elapsed_time(e[2]) for e in evs]
     apply_all = [e[2].elapsed_time(e[3]) for e in evs]
@@ -470,20 +632,47 @@ def main():
         "generation_s": round(t_gen, 2),
         "source_hash": src_hash,
     }
+    last_edge = edges[(args.warmup + args.steps - 1) % len(edges)]
+    if not args.no_verify:
+        out["verify_last_apply"] = verify_last_apply(pc, w, last_edge, (0, 100 + last_edge - 1), L - 1, H // 2)
+        _progress("verify_last_apply done")
     if not args.no_copy_ceiling:
         out["copy_ceiling"] = copy_ceiling(args, kvc, torch, cache, w, batch)
+        _progress("copy_ceiling done")
+        cc = out["copy_ceiling"]["kernels"]
+        blocks = {k_: v_["gbps"] for k_, v_ in cc.items() if k_.startswith("paged_blocks")}
+        out["copy_ceiling"]["apply_vs_paged_block_copy_logical"] = round(apply_gbps / cc["paged_blocks_logical_x1"]["gbps"], 4)
+        out["copy_ceiling"]["apply_vs_best_paged_block_copy"] = round(apply_gbps / max(blocks.values()), 4)
+        out["copy_ceiling"]["apply_vs_best_contiguous_copy"] = round(
+            apply_gbps / max(cc["contiguous_xcd"]["gbps"], cc["contiguous_chunked"]["gbps"]), 4)
     if not args.no_rope:
         out["rope"] = rope_measurement(args, kvc, torch, pc, w, Tc[0], batch)
+        _progress("rope done")
     if not args.no_layer_fit:
         out["layer_fit"] = layer_fit_measurement(args, kvc, torch, pc, w)
+        _progress("layer_fit done")
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(pc, w)
+        _progress("cpu_baseline done")
     if not args.no_anchor_pool:
         del cache, S, Tc, fit_batches, apply_batches, ws_fit, ws_chain, pc
         torch.cuda.empty_cache()
         out["anchor_pool"] = anchor_pool_measurement(args, kvc, synth, torch)
+        _progress("anchor_pool done")
+        if not args.no_rope:
+            out["anchor_pool_rope"] = anchor_pool_measurement(args, kvc, synth, torch, rope=True)
+            _progress("anchor_pool_rope done")
     if not args.no_chain_study:
         out["chain_study"] = chain_study(args, kvc, synth, torch)
+        _progress("chain_study done")
+    if not args.no_configs:
+        out["configs"] = {}
+        out["configs"]["llama8b_4k"] = secondary_apply(args, kvc, synth, torch, "llama8b_4k", 1)
+        _progress("configs.llama8b_4k done")
+        out["configs"]["vlm"] = secondary_apply(args, kvc, synth, torch, "vlm", 3)
+        _progress("configs.vlm done")
+        out["configs"]["serving"] = serving_measurement(args, kvc, synth, torch)
+        _progress("configs.serving done")
     print(json.dumps(out), flush=True)
     return 0
 
