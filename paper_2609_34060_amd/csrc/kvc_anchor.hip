@@ -572,11 +572,106 @@ __device__ __forceinline__ bf16x8 res_frag(const uint16_t* s, int kpt, int f, in
   return as_bf16x8(*reinterpret_cast<const u32x4*>(s + f * kpt + 8 * (4 * c + (g ^ res_swz(f)))));
 }
 
-// Every chunk of unit `unit` into LDS: a thread takes (feature f, eight ranks of one chunk); the lanes of a wave
-// take 64 consecutive features, so each of the eight 4-byte loads is one coalesced 256-byte row segment.
+// The resident kernels fill the LDS with bases, so per-workgroup tables live in registers and are read with lane
+// shuffles (no global load, hence no wait on the wave's earlier stores, inside the tile loop).
+//
+// Block ids of the chunk's logical blocks lb0 .. lb0 + 127: lane k holds those of lb0 + k (e0) and lb0 + 64 + k (e1).
+// A chunk spanning more blocks (block sizes below 9 at 1024 tokens) reads the table from global memory instead.
+struct LaneTable {
+  int32_t e0, e1;
+  int lb0;
+  bool regs;
+};
+__device__ __forceinline__ int lane_lblock(const PoolView& pv, int p) {
+  return pv.block_shift >= 0 ? p >> pv.block_shift : p / pv.block_size;
+}
+__device__ __forceinline__ LaneTable lane_table(const PoolView& pv, const int32_t* __restrict__ table, int off,
+                                                int t_begin, int t_end, int lane) {
+  LaneTable lt;
+  lt.lb0 = lane_lblock(pv, off + t_begin);
+  const int nb = lane_lblock(pv, off + t_end - 1) - lt.lb0 + 1;  // the host checked these lie in the table row
+  lt.regs = nb <= 2 * kWave;
+  const int i0 = lane, i1 = lane + kWave;
+  lt.e0 = lt.regs && i0 < nb ? (table ? table[lt.lb0 + i0] : lt.lb0 + i0) : -1;
+  lt.e1 = lt.regs && i1 < nb ? (table ? table[lt.lb0 + i1] : lt.lb0 + i1) : -1;
+  return lt;
+}
+// Row offset of token t (-1 when absent or out of range).  Call from converged control flow (lane shuffles).
+__device__ __forceinline__ int64_t lane_row_offset(const PoolView& pv, const LaneTable& lt,
+                                                   const int32_t* __restrict__ table, int off, int t, bool valid,
+                                                   int head) {
+  const int p = off + t, lb = lane_lblock(pv, p), k = lb - lt.lb0;
+  const int a0 = __shfl(lt.e0, k & (kWave - 1), kWave), a1 = __shfl(lt.e1, k & (kWave - 1), kWave);
+  if (!valid) return -1;
+  const int32_t blk = lt.regs ? (k < kWave ? a0 : a1) : (table ? table[lb] : lb);
+  if (blk < 0 || blk >= pv.num_blocks) return -1;
+  return (int64_t)blk * pv.block_stride + (int64_t)(p - lb * pv.block_size) * pv.token_stride +
+         (int64_t)head * pv.head_stride;
+}
+
+// Rotary angle table of one wave: lane L holds cos / sin of pair rope_wave_pair(L) at angle p * inv_freq[pair]; the
+// lanes of token group g (the MFMA row layout: features 32 q + 8 g + e) need D / 8 pairs, lanes g D / 8 .. of the
+// table, in the order rope_rotate_rows visits them.
 template <int D>
-__device__ __forceinline__ void stage_stacked(const AnchorArgs& a, int64_t unit, uint16_t* s_hi, uint16_t* s_lo) {
+__device__ __forceinline__ int rope_wave_pair(int style, int lane) {
+  constexpr int NP = D / 8;
+  const int gg = (lane / NP) & 3, k = lane % NP;
+  return style == KVC_ROPE_HALF ? 32 * (k / 8) + 8 * gg + k % 8 : 16 * (k / 4) + 4 * gg + k % 4;
+}
+template <int D>
+__device__ __forceinline__ void rope_wave_table(const RopeView& rp, double p, int lane, float& c, float& s) {
+  double sn, cs;
+  sincos(p * rp.inv_freq[rope_wave_pair<D>(rp.style, lane)], &sn, &cs);
+  c = (float)cs;
+  s = (float)sn;
+}
+// rope_rotate_rows with the angles of a wave table (converged control flow: lane shuffles).
+template <int D>
+__device__ __forceinline__ void rope_rotate_rows_wave(f32x4* v, int style, int g, float tc, float ts) {
+  constexpr int NQ = D / 32, NP = D / 8;
+  if (style == KVC_ROPE_HALF) {
+#pragma unroll
+    for (int q = 0; q < NQ / 2; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int src = g * NP + 8 * q + e, ja = 2 * q + (e >> 2), jb = 2 * (q + NQ / 2) + (e >> 2);
+        const float cc = __shfl(tc, src, kWave), ss = __shfl(ts, src, kWave);
+        const float a = v[ja][e & 3], b = v[jb][e & 3];
+        v[ja][e & 3] = a * cc - b * ss;
+        v[jb][e & 3] = a * ss + b * cc;
+      }
+  } else {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const int src = g * NP + 4 * q + (e >> 1), j = 2 * q + (e >> 2);
+        const float cc = __shfl(tc, src, kWave), ss = __shfl(ts, src, kWave);
+        const float a = v[j][e & 3], b = v[j][(e & 3) + 1];
+        v[j][e & 3] = a * cc - b * ss;
+        v[j][(e & 3) + 1] = a * ss + b * cc;
+      }
+  }
+}
+
+// Every chunk of unit `unit` into LDS: a thread takes (feature f, eight ranks of one chunk); the lanes of a wave
+// take 64 consecutive features, so each of the eight 4-byte loads is one coalesced 256-byte row segment.  A thread
+// always takes the same feature (kResThreads is a multiple of D).  ROPE with `rot`: each basis row is rotated like a
+// key row at position `pos` (B R(pos)^T), from the partner feature's values and one angle per thread.
+template <int D, bool ROPE = false>
+__device__ __forceinline__ void stage_stacked(const AnchorArgs& a, int64_t unit, uint16_t* s_hi, uint16_t* s_lo,
+                                              bool rot = false, double pos = 0.0) {
+  static_assert(kResThreads % D == 0, "one feature per thread");
   const int NC = a.num_chunks, kpt = 32 * NC, items = D * 4 * NC;
+  const int style = a.pv.rope.style;
+  const int fth = (int)threadIdx.x % D;
+  float rc = 1.0f, rs = 0.0f;
+  if (ROPE && rot) {
+    double sn, cs;
+    sincos(pos * a.pv.rope.inv_freq[rope_pair(style, D, fth)], &sn, &cs);
+    rc = (float)cs;
+    rs = (float)sn;
+  }
   for (int base = 0; base < items; base += kResThreads) {
     const int idx = base + (int)threadIdx.x;
     if (idx >= items) break;  // whole waves: items is a multiple of 64
@@ -587,6 +682,13 @@ __device__ __forceinline__ void stage_stacked(const AnchorArgs& a, int64_t unit,
     float x[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) x[e] = k0 + e < r ? b[(int64_t)(k0 + e) * D] : 0.0f;
+    if (ROPE && rot) {
+      const float* bp = a.basis[v] + unit * (int64_t)r * D + rope_partner(style, D, f);
+      const bool first = rope_first(style, D, f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        x[e] = rope_rotated(first, x[e], k0 + e < r ? bp[(int64_t)(k0 + e) * D] : 0.0f, rc, rs);
+    }
     u32x4 hi, lo;
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
@@ -605,7 +707,9 @@ __device__ __forceinline__ void stage_stacked(const AnchorArgs& a, int64_t unit,
 // takes w_v[t] (A_v[t, chunk c] B_v[chunk c]) over all chunks (the bf16 coefficients are exact MFMA operands against
 // the basis hi/lo, two MFMAs per fragment, and the product is scaled by the token's weight in fp32), then one
 // rounding.
-template <int D>
+// ROPE: keys of a rotary cache, C_dst = R(pd - ps) C_src + sum_v w_v A_v (B_v R(pd)^T) (bases staged rotated, the
+// source rotated in the accumulator; rows past T_s get the rotated source).
+template <int D, bool ROPE>
 __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArgs a) {
   constexpr int MT = D / 16, NQ = D / 32, NCM = kResMaxChunks;
   extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
@@ -624,10 +728,18 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
   const uint16_t* src_pool = static_cast<const uint16_t*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
   uint16_t* dst_pool = static_cast<uint16_t*>(const_cast<void*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]));
   const float* wrow = a.weights + (int64_t)(lrel * 2 + kv) * Ts * V;
+  const bool rope = ROPE && kv == 0;  // uniform over the workgroup
+  const int style = a.pv.rope.style;
+  const bool shift = rope && a.dst_position != a.src_position;
+  float tc = 1.0f, ts = 0.0f;  // this lane's entry of the wave's angle table for pd - ps
+  if (shift) rope_wave_table<D>(a.pv.rope, (double)a.dst_position - (double)a.src_position, lane, tc, ts);
   if (t_begin < Ts) {  // whole workgroup
-    stage_stacked<D>(a, unit, s_hi, s_lo);
+    stage_stacked<D, ROPE>(a, unit, s_hi, s_lo, rope, (double)a.dst_position);
     __syncthreads();
   }
+  const int t_end = min(T, t_begin + kResChunk);
+  const LaneTable lts = lane_table(a.pv, a.src_table, a.src_offset, t_begin, t_end, lane);
+  const LaneTable ltd = lane_table(a.pv, a.dst_table, a.dst_offset, t_begin, t_end, lane);
 
   struct Tile {
     u32x4 raw[NQ];
@@ -638,9 +750,10 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
   auto load_tile = [&](int j, Tile& tl) __attribute__((always_inline)) {
     const int t = t_begin + (j * kResWaves + wave) * 16 + n;
     const bool valid = t < T, crow = t < Ts;
-    const int64_t so = valid ? row_offset(a.pv, a.src_table, a.src_offset, t, head) : -1;
+    const int64_t so = lane_row_offset(a.pv, lts, a.src_table, a.src_offset, t, valid, head);
     // a row whose source block id is out of range is neither read nor written
-    tl.dof = so >= 0 ? row_offset(a.pv, a.dst_table, a.dst_offset, t, head) : -1;
+    const int64_t dof = lane_row_offset(a.pv, ltd, a.dst_table, a.dst_offset, t, valid, head);
+    tl.dof = so >= 0 ? dof : -1;
     load_row_segments<NQ>(src_pool, so, g, tl.raw);
 #pragma unroll
     for (int c = 0; c < NCM; ++c) {
@@ -654,10 +767,10 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
       }
     }
   };
-  auto finish_tile = [&](int j, const Tile& tl) __attribute__((always_inline)) {
+  // the corrected (or copied) rows of tile j, ready to store
+  auto finish_tile = [&](int j, const Tile& tl, u32x4* outw) __attribute__((always_inline)) {
     const int t0 = t_begin + (j * kResWaves + wave) * 16, t = t0 + n;
-    u32x4 outw[NQ];
-    if (t0 < Ts) {  // uniform over the wave
+    if (t0 < Ts || shift) {  // uniform over the wave
       f32x4 acc[MT];
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
@@ -666,8 +779,10 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
         acc[2 * q + 1] = f32x4{bf16_lo_to_f32(tl.raw[q][2]), bf16_hi_to_f32(tl.raw[q][2]),
                                bf16_lo_to_f32(tl.raw[q][3]), bf16_hi_to_f32(tl.raw[q][3])};
       }
+      if (ROPE && shift) rope_rotate_rows_wave<D>(acc, style, g, tc, ts);
 #pragma unroll
       for (int c = 0; c < NCM; ++c) {
+        if (t0 >= Ts) break;  // uniform: a tile past the coverage takes the rotated source only
         if (c >= NC) break;
         int kc = kpt;
         asm volatile("" : "+s"(kc));  // keeps the fragment reads in this chunk's step (not hoisted out of the tiles)
@@ -685,7 +800,8 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
           for (int e = 0; e < 4; ++e) acc[mt][e] = fmaf(wc, p[e], acc[mt][e]);
         }
       }
-      const bool crow = t < Ts;
+      // rows past T_s have a zero correction: the rotated source with a shift, else bit copies
+      const bool crow = t < Ts || shift;
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         const f32x4 x = acc[2 * q], y = acc[2 * q + 1];
@@ -697,18 +813,23 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
 #pragma unroll
       for (int q = 0; q < NQ; ++q) outw[q] = tl.raw[q];
     }
-    if (tl.dof >= 0) {
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) *reinterpret_cast<u32x4*>(dst_pool + tl.dof + 32 * q + 8 * g) = outw[q];
-    }
   };
 
-  // no software prefetch: eight waves per CU keep enough tiles in flight (as in kvc_apply)
+  // the next tile's loads are issued before this tile's stores, so waiting for them never waits for the stores
+  if (t_begin + wave * 16 >= T) return;  // whole wave
+  Tile cur;
+  load_tile(0, cur);
   for (int j = 0; j < kResTiles; ++j) {
-    if (t_begin + (j * kResWaves + wave) * 16 >= T) break;  // uniform over the wave
-    Tile cur;
-    load_tile(j, cur);
-    finish_tile(j, cur);
+    u32x4 outw[NQ];
+    finish_tile(j, cur, outw);
+    const int64_t dof = cur.dof;
+    const bool more = j + 1 < kResTiles && t_begin + ((j + 1) * kResWaves + wave) * 16 < T;  // uniform
+    if (more) load_tile(j + 1, cur);
+    if (dof >= 0) {
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) *reinterpret_cast<u32x4*>(dst_pool + dof + 32 * q + 8 * g) = outw[q];
+    }
+    if (!more) break;
   }
 }
 
@@ -717,7 +838,8 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
 // anchor's chunks (bf16 coefficients are exact MFMA operands, B as hi/lo), then |x - recon| (weights) or
 // (x - recon)^2 (gate) is summed over the row.  Lane (g, n) keeps the sums of anchors v = 4u + g of its tiles'
 // token n in registers across heads.
-template <int D, bool GATE>
+// ROPE (weights): keys of a rotary cache are compared in canonical coordinates, R(-ps) C_src (the bases are canonical).
+template <int D, bool GATE, bool ROPE>
 __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a) {
   constexpr int MT = D / 16, NQ = D / 32, NCM = kResMaxChunks, TPW = kResTiles;
   static_assert(KVC_MAX_ANCHORS <= 16, "four anchors per lane group");
@@ -743,6 +865,11 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
   for (int j = 0; j < TPW; ++j)
 #pragma unroll
     for (int u = 0; u < 4; ++u) dist[j][u] = 0.0f;
+  const bool rot = ROPE && !GATE && kv == 0;  // uniform over the workgroup
+  const int style = a.pv.rope.style;
+  float tc = 1.0f, ts = 0.0f;  // this lane's entry of the wave's angle table for -ps
+  if (rot) rope_wave_table<D>(a.pv.rope, -(double)a.src_position, lane, tc, ts);
+  const LaneTable lts = lane_table(a.pv, a.src_table, a.src_offset, t_begin, min(Tl, t_begin + kResChunk), lane);
 
   struct Tile {
     u32x4 raw[NQ];
@@ -756,7 +883,7 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
     auto load_tile = [&](int j, Tile& tl) __attribute__((always_inline)) {
       const int t = t_begin + (j * kResWaves + wave) * 16 + n;
       const bool valid = t < Tl;
-      load_row_segments<NQ>(pool, valid ? row_offset(a.pv, a.src_table, a.src_offset, t, h) : -1, g, tl.raw);
+      load_row_segments<NQ>(pool, lane_row_offset(a.pv, lts, a.src_table, a.src_offset, t, valid, h), g, tl.raw);
 #pragma unroll
       for (int c = 0; c < NCM; ++c) {
         tl.cw[c] = u32x4{0u, 0u, 0u, 0u};
@@ -776,6 +903,18 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
         Tile cur;
         load_tile(j, cur);
         const bool valid = t0 + n < Tl;
+        // ROPE: the canonical source rows R(-ps) C_src in fp32 (the rotary instantiation only)
+        f32x4 xv[ROPE ? MT : 1];
+        if constexpr (ROPE) {
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) {
+            xv[2 * q] = f32x4{bf16_lo_to_f32(cur.raw[q][0]), bf16_hi_to_f32(cur.raw[q][0]),
+                              bf16_lo_to_f32(cur.raw[q][1]), bf16_hi_to_f32(cur.raw[q][1])};
+            xv[2 * q + 1] = f32x4{bf16_lo_to_f32(cur.raw[q][2]), bf16_hi_to_f32(cur.raw[q][2]),
+                                  bf16_lo_to_f32(cur.raw[q][3]), bf16_hi_to_f32(cur.raw[q][3])};
+          }
+          if (rot) rope_rotate_rows_wave<D>(xv, style, g, tc, ts);
+        }
         f32x4 acc[MT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -798,7 +937,8 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
 #pragma unroll
               for (int e = 0; e < 8; ++e) {
                 const uint32_t w = cur.raw[q][e >> 1];
-                const float x = (e & 1) ? bf16_hi_to_f32(w) : bf16_lo_to_f32(w);
+                const float x = ROPE ? xv[ROPE ? 2 * q + (e >> 2) : 0][e & 3]
+                                     : ((e & 1) ? bf16_hi_to_f32(w) : bf16_lo_to_f32(w));
                 const float diff = x - acc[2 * q + (e >> 2)][e & 3];
                 s += GATE ? diff * diff : fabsf(diff);
               }
@@ -896,9 +1036,8 @@ static hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, const AnchorA
   return hipGetLastError();
 }
 
-// The chunk map of the resident-basis kernels (bf16, no rotary keys); false when they do not apply.
+// The chunk map of the resident-basis kernels (bf16); false when the anchors' chunks do not fit.
 static bool plan_resident(AnchorArgs& a) {
-  if (a.pv.rope.style != KVC_ROPE_NONE) return false;
   int nc = 0;
   for (int v = 0; v < a.num_anchors; ++v) {
     const int ks = std::max(1, (a.rank[v] + 31) / 32);
@@ -952,8 +1091,8 @@ static hipError_t launch_weights_variant(const AnchorArgs& a, kvc_dtype dtype, h
     if (plan_resident(r)) {
       dim3 grid((a.num_weighted + kResChunk - 1) / kResChunk, 2, a.num_layers);
       const size_t rl = res_lds_bytes(r, 0);
-      return D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, false>, grid, rl, r, stream, kResThreads)
-                     : launch_with_lds(anchor_dist_res_bf16<128, false>, grid, rl, r, stream, kResThreads);
+      return D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, false, ROPE>, grid, rl, r, stream, kResThreads)
+                     : launch_with_lds(anchor_dist_res_bf16<128, false, ROPE>, grid, rl, r, stream, kResThreads);
     }
     dim3 grid((a.num_weighted + kAnchorChunk - 1) / kAnchorChunk, 2, a.num_layers);
     return D == 64 ? launch_dist_bf16<64, false, ROPE>(a, grid, lds, stream)
@@ -984,8 +1123,8 @@ hipError_t launch_gate_distances(const AnchorArgs& args, kvc_dtype dtype, hipStr
     grid.y = a.pv.num_kv_heads;
     a.gate_chunks = (int)(grid.x * grid.y);
     const size_t rl = res_lds_bytes(a, 2);
-    e = D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, true>, grid, rl, a, stream, kResThreads)
-                : launch_with_lds(anchor_dist_res_bf16<128, true>, grid, rl, a, stream, kResThreads);
+    e = D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, true, false>, grid, rl, a, stream, kResThreads)
+                : launch_with_lds(anchor_dist_res_bf16<128, true, false>, grid, rl, a, stream, kResThreads);
   } else if (dtype == KVC_BF16) {
     // one partial per (layer, 512-token chunk, KV head), as the workspace query sizes
     grid.y = a.pv.num_kv_heads;
@@ -1010,8 +1149,8 @@ static hipError_t launch_anchored_variant(const AnchorArgs& a, kvc_dtype dtype, 
     if (plan_resident(r)) {
       dim3 grid((a.num_tokens + kResChunk - 1) / kResChunk, 2 * a.pv.num_kv_heads, a.num_layers);
       const size_t rl = res_lds_bytes(r, 1);
-      return D == 64 ? launch_with_lds(apply_anchored_res_bf16<64>, grid, rl, r, stream, kResThreads)
-                     : launch_with_lds(apply_anchored_res_bf16<128>, grid, rl, r, stream, kResThreads);
+      return D == 64 ? launch_with_lds(apply_anchored_res_bf16<64, ROPE>, grid, rl, r, stream, kResThreads)
+                     : launch_with_lds(apply_anchored_res_bf16<128, ROPE>, grid, rl, r, stream, kResThreads);
     }
     dim3 grid((a.num_tokens + kAnchoredChunk - 1) / kAnchoredChunk, 2 * a.pv.num_kv_heads, a.num_layers);
     return D == 64 ? launch_anchored_bf16<64, ROPE>(a, grid, lds, stream)

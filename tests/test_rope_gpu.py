@@ -21,8 +21,8 @@ TOL = {"f32": 1e-5, "bf16": 1e-2}
 HALF, PAIRS = kvc.KVC_ROPE_HALF, kvc.KVC_ROPE_PAIRS
 
 
-def _case(name, layers):
-    w = synth.WORKLOADS[name].with_(num_layers=layers)
+def _case(name, layers, **over):
+    w = synth.WORKLOADS[name].with_(num_layers=layers, **over)
     pc = synth.build_paged(w, device="cuda", num_output_agents=1)
     src, dst = pc.seqs[(0, 0)], pc.seqs[(0, 100)]
     tab = (lambda s: None) if pc.tables is None else (lambda s: pc.tables[[s.table_row]])
@@ -155,15 +155,23 @@ def test_fit_with_rope_matches_oracle(name, layers, style, ps, pd, rank):
     assert worst <= TOL[dt], worst
 
 
-@pytest.mark.parametrize("name,layers,style,ps,pd,ranks,Ts", [
-    ("tiny", 2, HALF, 300, 4000, [8, 4, 8], 200),
-    ("llama8b_4k", 1, PAIRS, 0, 0, [32, 16, 32], 2000),
-    ("llama8b_4k", 1, HALF, 2048, 100, [32, 64, 96], 4096),
+# bf16 sets of at most ten 32-rank chunks run through the resident-basis kernels (ten chunks of rank 32, the paper's
+# pool of V = 10, fill the LDS), larger sets through the one-anchor-at-a-time kernels (the [64, 96, 64, 96] case)
+@pytest.mark.parametrize("name,layers,style,ps,pd,ranks,Ts,over", [
+    ("tiny", 2, HALF, 300, 4000, [8, 4, 8], 200, {}),
+    ("llama8b_4k", 1, PAIRS, 0, 0, [32, 16, 32], 2000, {}),
+    ("llama8b_4k", 1, HALF, 2048, 100, [32, 64, 96], 4096, {}),
+    ("llama8b_4k", 2, HALF, 2048, 6144, [32] * 10, 4096, {}),
+    ("llama8b_4k", 1, PAIRS, 5000, 77, [32] * 10, 3001, {}),
+    ("llama8b_4k", 1, HALF, 1000, 3000, [64, 96, 64, 96], 2500, {}),
+    ("llama8b_4k", 1, HALF, 900, 900, [32, 32, 48], 1000, {"head_dim": 64, "num_kv_heads": 3,
+                                                           "seq_tokens": (1100,)}),
+    ("llama8b_4k", 1, PAIRS, 0, 4096, [16, 32, 32, 8], 1100, {"head_dim": 64, "seq_tokens": (1300,)}),
 ])
-def test_anchor_weights_and_anchored_apply_with_rope(name, layers, style, ps, pd, ranks, Ts):
+def test_anchor_weights_and_anchored_apply_with_rope(name, layers, style, ps, pd, ranks, Ts, over):
     """Key distances in canonical coordinates (R(-ps) C_src against the canonical anchor bases) and the anchored
     correction rotated to the target positions."""
-    w, pc, src, dst, tab = _case(name, layers)
+    w, pc, src, dst, tab = _case(name, layers, **over)
     T, H, d = w.seq_tokens[0], w.num_kv_heads, w.head_dim
     Ts = min(Ts, T)
     inv = Hp.rope_inv_freq(d, 1e4 if name == "tiny" else 5e5)
