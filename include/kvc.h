@@ -209,8 +209,9 @@ size_t kvc_fit_workspace_bytes(const kvc_cache* cache, const kvc_batch* batch, i
  * Sigma descending; each basis row has its largest-magnitude entry positive.  Keys of a rotary cache:
  * Z = R(-dst_position) C_dst - R(-src_position) C_src (KVC_FIT_BASE: Z = R(-dst_position) C_dst), so the state is in
  * canonical coordinates.  Per-layer states (KVC_GROUP_LAYER, every item of the call): Z = [Z_0 ... Z_{H-1}] with the
- * heads side by side, D = H d <= 1024, rank <= 112, no rotary keys (KVC_ERR_UNSUPPORTED otherwise; float32 caches
- * also need rank * D * 4 <= 160 KiB); the SVD is reached by subspace iteration on Z^T Z (k = 64 columns for
+ * heads side by side (each head's key rows in canonical coordinates for a rotary cache), D = H d <= 1024, rank <= 112
+ * (KVC_ERR_UNSUPPORTED otherwise; float32 caches also need rank * D * 4 + 1024 <= 160 KiB, and rotary keys in a
+ * bf16 cache a power-of-two block size of at least 8 with every head of a row within 2 GiB); the SVD is reached by subspace iteration on Z^T Z (k = 64 columns for
  * rank <= 48, else 128) with a Rayleigh-Ritz step after 4 iterations and every 4 more, stopping per layer unit once
  * every top-r Ritz pair (theta, y) has ||Z^T Z y - theta y|| <= 1e-6 theta_1, or after 48 iterations (a spectrum with
  * no gap between sigma_r and sigma_{k+1}); the kernels of a stopped unit return at once. */

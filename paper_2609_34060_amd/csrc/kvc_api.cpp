@@ -183,16 +183,25 @@ struct LayerPlan {
          off_iters = 0, total = 0;
 };
 
-// Which calls the per-layer path takes (every item per layer, no rotary keys, D = H d <= 1024, rank + 16 <= k).
+// Which calls the per-layer path takes (every item per layer, D = H d <= 1024, rank + 16 <= k; rotary keys with bf16
+// caches need the LDS Gram: a power-of-two block size of at least 8 and every head of a row within 2 GiB).
 kvc_status check_layer_fit(const kvc_cache* c, const kvc_batch* b) {
   const int32_t DL = c->num_kv_heads * c->head_dim;
-  if (c->rope_style != KVC_ROPE_NONE || DL > 1024) return KVC_ERR_UNSUPPORTED;
+  if (DL > 1024) return KVC_ERR_UNSUPPORTED;
+  if (c->rope_style != KVC_ROPE_NONE && c->dtype == KVC_BF16) {
+    bool pow2 = false;
+    for (int32_t sh = 3; sh < 31; ++sh) pow2 = pow2 || (int32_t{1} << sh) == c->block_size;
+    const bool small_rows = 2 * (static_cast<int64_t>(c->num_kv_heads - 1) * c->head_stride + c->head_dim) <
+                            (int64_t{1} << 31);
+    if (!pow2 || !small_rows) return KVC_ERR_UNSUPPORTED;
+  }
   for (int32_t i = 0; i < b->num_items; ++i) {
     const kvc_state& st = b->items[i].state;
     if (st.grouping != KVC_GROUP_LAYER) return KVC_ERR_UNSUPPORTED;
     const int32_t k = st.rank + 16 <= 64 ? 64 : 128;
     if (st.rank + 16 > 128 || k > DL) return KVC_ERR_UNSUPPORTED;
-    if (c->dtype == KVC_F32 && static_cast<size_t>(st.rank) * DL * 4 > 160 * 1024) return KVC_ERR_UNSUPPORTED;
+    // float32: the projection holds the basis and the rotary angle tables (1 KiB) in LDS
+    if (c->dtype == KVC_F32 && static_cast<size_t>(st.rank) * DL * 4 + 1024 > 160 * 1024) return KVC_ERR_UNSUPPORTED;
   }
   return KVC_OK;
 }

@@ -146,6 +146,51 @@ __device__ __forceinline__ void rope_rotate_rows(f32x4* v, int style, int g, con
   }
 }
 
+// Rotary angle table of one wave: lane L holds cos / sin of pair rope_wave_pair(L) at angle p * inv_freq[pair]; the
+// lanes of token group g (the MFMA row layout: features 32 q + 8 g + e) need D / 8 pairs, lanes g D / 8 .. of the
+// table, in the order rope_rotate_rows visits them.
+template <int D>
+__device__ __forceinline__ int rope_wave_pair(int style, int lane) {
+  constexpr int NP = D / 8;
+  const int gg = (lane / NP) & 3, k = lane % NP;
+  return style == KVC_ROPE_HALF ? 32 * (k / 8) + 8 * gg + k % 8 : 16 * (k / 4) + 4 * gg + k % 4;
+}
+template <int D>
+__device__ __forceinline__ void rope_wave_table(const RopeView& rp, double p, int lane, float& c, float& s) {
+  double sn, cs;
+  sincos(p * rp.inv_freq[rope_wave_pair<D>(rp.style, lane)], &sn, &cs);
+  c = (float)cs;
+  s = (float)sn;
+}
+// rope_rotate_rows with the angles of a wave table (converged control flow: lane shuffles).
+template <int D>
+__device__ __forceinline__ void rope_rotate_rows_wave(f32x4* v, int style, int g, float tc, float ts) {
+  constexpr int NQ = D / 32, NP = D / 8;
+  if (style == KVC_ROPE_HALF) {
+#pragma unroll
+    for (int q = 0; q < NQ / 2; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int src = g * NP + 8 * q + e, ja = 2 * q + (e >> 2), jb = 2 * (q + NQ / 2) + (e >> 2);
+        const float cc = __shfl(tc, src, kWave), ss = __shfl(ts, src, kWave);
+        const float a = v[ja][e & 3], b = v[jb][e & 3];
+        v[ja][e & 3] = a * cc - b * ss;
+        v[jb][e & 3] = a * ss + b * cc;
+      }
+  } else {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        const int src = g * NP + 4 * q + (e >> 1), j = 2 * q + (e >> 2);
+        const float cc = __shfl(tc, src, kWave), ss = __shfl(ts, src, kWave);
+        const float a = v[j][e & 3], b = v[j][(e & 3) + 1];
+        v[j][e & 3] = a * cc - b * ss;
+        v[j][(e & 3) + 1] = a * ss + b * cc;
+      }
+  }
+}
+
 // Offset of unit (layer, kv, head) in a state's per-unit arrays.
 __device__ __forceinline__ int64_t unit_index(int32_t layer, int32_t kv, int32_t head, int32_t num_kv_heads) {
   return ((int64_t)layer * 2 + kv) * num_kv_heads + head;

@@ -217,7 +217,11 @@ __device__ __forceinline__ GLRows gl_rows(const GLPaging& pg, int2 b, int32_t of
 constexpr int kGLZeroBytes = 65536;
 __device__ __attribute__((aligned(256))) uint32_t gl_zero_page[kGLZeroBytes / 4];
 
-template <int D, bool DELTA, bool FULL>
+// ROPE: the key rows of a rotary cache enter Z in canonical coordinates, Z = R(-pd) C_dst - R(-ps) C_src (Eq. 12 with
+// Align): a producer lane holds 4 consecutive features of one head, the partner of a rotate-half pair lies in the lane
+// D / 8 away (one xor shuffle per row dword) and the partner of an adjacent pair inside the lane; the lane's 4 angles
+// per side are formed once.
+template <int D, bool DELTA, bool FULL, bool ROPE>
 __global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, int num_pairs, int num_groups) {
   extern __shared__ __attribute__((aligned(16))) u32x4 gl_lds[];
   const int H = a.pv.num_kv_heads, DL = H * D, NB = (DL + 127) / 128;
@@ -260,6 +264,30 @@ __global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, in
   const bool inrange = pact && fglob < DL;
   // byte offset of the lane's 4 features within a token's row (the launcher checks it fits 32 bits)
   const uint32_t fbytes = inrange ? 2u * (uint32_t)((fglob / D) * a.pv.head_stride + fglob % D) : 0u;
+  // rotary keys: cos / sin of the lane's 4 features' pairs at -pd (dst) and -ps (src), and whether each feature is
+  // the first of its pair
+  const bool rot = ROPE && lu.kv == 0;  // uniform over the workgroup
+  const int style = a.pv.rope.style;
+  float rcd[ROPE ? 4 : 1], rsd[ROPE ? 4 : 1], rcs[ROPE ? 4 : 1], rss[ROPE ? 4 : 1];
+  bool rfirst = true;
+  if constexpr (ROPE) {
+    const int f0 = fglob % D;
+    rfirst = rope_first(style, D, f0);  // the same for the lane's 4 features (pairs never straddle a lane's quad)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      rcd[e] = 1.0f, rsd[e] = 0.0f, rcs[e] = 1.0f, rss[e] = 0.0f;
+      if (rot) {
+        const double th = a.pv.rope.inv_freq[rope_pair(style, D, f0 + e)];
+        double sn, cs;
+        sincos(-(double)itp->dst_position * th, &sn, &cs);
+        rcd[e] = (float)cs;
+        rsd[e] = (float)sn;
+        sincos(-(double)itp->src_position * th, &sn, &cs);
+        rcs[e] = (float)cs;
+        rss[e] = (float)sn;
+      }
+    }
+  }
 
   // consumer: wave = 2 x block pair (i1, i2) + row half
   const int bp = wave >> 1, half = wave & 1, i1 = bp >> 1, i2 = bp & 1;
@@ -327,10 +355,37 @@ __global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, in
         sx = ps ? sx : 0u;
         sy = ps ? sy : 0u;
       }
-      split_bf16x2(bf16_lo_to_f32(dx) - bf16_lo_to_f32(sx), bf16_hi_to_f32(dx) - bf16_hi_to_f32(sx), hi[j][0],
-                   lo[j][0]);
-      split_bf16x2(bf16_lo_to_f32(dy) - bf16_lo_to_f32(sy), bf16_hi_to_f32(dy) - bf16_hi_to_f32(sy), hi[j][1],
-                   lo[j][1]);
+      float d4[4] = {bf16_lo_to_f32(dx), bf16_hi_to_f32(dx), bf16_lo_to_f32(dy), bf16_hi_to_f32(dy)};
+      float s4[4] = {bf16_lo_to_f32(sx), bf16_hi_to_f32(sx), bf16_lo_to_f32(sy), bf16_hi_to_f32(sy)};
+      if constexpr (ROPE) {
+        if (rot) {  // uniform: every lane of the wave takes part in the shuffles
+          float pd4[4], ps4[4];
+          if (style == KVC_ROPE_HALF) {
+            const uint32_t qdx = __shfl_xor(dx, D / 8, kWave), qdy = __shfl_xor(dy, D / 8, kWave);
+            const uint32_t qsx = __shfl_xor(sx, D / 8, kWave), qsy = __shfl_xor(sy, D / 8, kWave);
+            pd4[0] = bf16_lo_to_f32(qdx), pd4[1] = bf16_hi_to_f32(qdx);
+            pd4[2] = bf16_lo_to_f32(qdy), pd4[3] = bf16_hi_to_f32(qdy);
+            ps4[0] = bf16_lo_to_f32(qsx), ps4[1] = bf16_hi_to_f32(qsx);
+            ps4[2] = bf16_lo_to_f32(qsy), ps4[3] = bf16_hi_to_f32(qsy);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              pd4[e] = d4[e ^ 1];
+              ps4[e] = s4[e ^ 1];
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool first = style == KVC_ROPE_HALF ? rfirst : (e & 1) == 0;
+            const float dn = rope_rotated(first, d4[e], pd4[e], rcd[e], rsd[e]);
+            const float sn = rope_rotated(first, s4[e], ps4[e], rcs[e], rss[e]);
+            d4[e] = dn;
+            s4[e] = sn;
+          }
+        }
+      }
+      split_bf16x2(d4[0] - s4[0], d4[1] - s4[1], hi[j][0], lo[j][0]);
+      split_bf16x2(d4[2] - s4[2], d4[3] - s4[3], hi[j][1], lo[j][1]);
     }
 #pragma unroll
     for (int f = 0; f < 4; ++f) {
@@ -456,9 +511,24 @@ __global__ __launch_bounds__(kGLThreads) void gram_layer_bf16(LayerFitArgs a, in
 
 constexpr int kF32Block = 64, kF32Step = 16;
 
+// Rotary angle tables of the float32 per-layer kernels in LDS: cos / sin at -pd, then at -ps, D / 2 each.
+constexpr size_t kLayerRopeTableBytes = 4 * 64 * sizeof(float);
+template <int D>
+__device__ __forceinline__ void layer_rope_tables(const LayerFitArgs& a, const kvc_item* itp, float* t) {
+  rope_table(a.pv.rope, D, -(double)itp->dst_position, t, t + D / 2);
+  rope_table(a.pv.rope, D, -(double)itp->src_position, t + D, t + 3 * D / 2);
+}
+// Feature f of a key row in canonical coordinates, from the row at `row` (f32 pool) and the tables of one side.
+template <int D>
+__device__ __forceinline__ float layer_rope_value(const float* row, int f, int style, const float* c, const float* s) {
+  const int i = rope_pair(style, D, f);
+  return rope_rotated(rope_first(style, D, f), row[f], row[rope_partner(style, D, f)], c[i], s[i]);
+}
+
 template <int D>
 __global__ __launch_bounds__(kLayerThreads) void gram_block_f32(LayerFitArgs a) {
   __shared__ float s_a[kF32Step][kF32Block + 1], s_b[kF32Step][kF32Block + 1];
+  __shared__ float s_rope[4 * (D / 2)];
   const int H = a.pv.num_kv_heads, DL = H * D, nb = DL / kF32Block;
   const int bi = blockIdx.x / nb, bj = blockIdx.x - bi * nb;
   const int part = blockIdx.y, u = blockIdx.z;
@@ -474,17 +544,22 @@ __global__ __launch_bounds__(kLayerThreads) void gram_block_f32(LayerFitArgs a) 
   const bool delta = a.mode == KVC_FIT_DELTA;
   const int tid = threadIdx.x, ti = tid / 16, tj = tid % 16;
   float acc[4][4] = {};
+  // keys of a rotary cache in canonical coordinates: Z = R(-pd) C_dst - R(-ps) C_src (tables read after a barrier)
+  const bool rot = a.pv.rope.style != KVC_ROPE_NONE && lu.kv == 0;
+  const int style = a.pv.rope.style;
+  if (rot) layer_rope_tables<D>(a, itp, s_rope);
   // every 64-feature block lies inside one head (64 divides d)
   auto z_of = [&](int t, int F) {
     const int h = F / D, f = F - h * D;
     const int64_t od = row_offset(a.pv, dst_tab, itp->dst_offset, t, h);
-    float z = od >= 0 ? pool[od + f] : 0.0f;
+    float z = od >= 0 ? (rot ? layer_rope_value<D>(pool + od, f, style, s_rope, s_rope + D / 2) : pool[od + f]) : 0.0f;
     if (delta) {
       const int64_t os = row_offset(a.pv, src_tab, itp->src_offset, t, h);
-      if (os >= 0) z -= pool[os + f];
+      if (os >= 0) z -= rot ? layer_rope_value<D>(pool + os, f, style, s_rope + D, s_rope + 3 * D / 2) : pool[os + f];
     }
     return z;
   };
+  __syncthreads();
   for (int t0 = t_begin; t0 < t_end; t0 += kF32Step) {
     for (int e = tid; e < kF32Step * kF32Block; e += kLayerThreads) {
       const int tk = e / kF32Block, c = e - tk * kF32Block, t = t0 + tk;
@@ -1145,7 +1220,9 @@ constexpr int kPLChunk = kPLWaves * kPLTiles * 16;        // tokens per workgrou
 
 // bf16: per head h the d columns of B (rank rows padded to RP = 16 MTR) are staged hi/lo in LDS (two buffers), the
 // rows of h are read in MFMA B-operand layout and Z split hi/lo; the coefficient tiles accumulate over the heads.
-template <int D, int MTR>
+// ROPE: key rows of a rotary cache enter Z in canonical coordinates (R(-pd) C_dst - R(-ps) C_src); the pairs of both
+// styles lie inside a lane in this layout, and the angles come from two wave tables.
+template <int D, int MTR, bool ROPE>
 __global__ __launch_bounds__(kPLThreads) void proj_layer_bf16(LayerFitArgs a) {
   constexpr int KS = D / 32, RP = MTR * 16;
   extern __shared__ __attribute__((aligned(16))) unsigned char layer_lds[];
@@ -1166,6 +1243,13 @@ __global__ __launch_bounds__(kPLThreads) void proj_layer_bf16(LayerFitArgs a) {
   const float* basis = st.basis + lunit * r * DL;
   uint16_t* coef = static_cast<uint16_t*>(st.coef) + lunit * (int64_t)Ts * r;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, n = lane & 15;
+  const bool rot = ROPE && lu.kv == 0;  // uniform over the workgroup
+  const int style = a.pv.rope.style;
+  float tcd = 1.0f, tsd = 0.0f, tcs = 1.0f, tss = 0.0f;  // wave tables for -pd (dst) and -ps (src)
+  if (rot) {
+    rope_wave_table<D>(a.pv.rope, -(double)itp->dst_position, lane, tcd, tsd);
+    rope_wave_table<D>(a.pv.rope, -(double)itp->src_position, lane, tcs, tss);
+  }
 
   f32x4 acc[kPLTiles][MTR];
 #pragma unroll
@@ -1194,21 +1278,51 @@ __global__ __launch_bounds__(kPLThreads) void proj_layer_bf16(LayerFitArgs a) {
       const int64_t od = valid ? row_offset(a.pv, dst_tab, itp->dst_offset, t, h) : -1;
       const int64_t os = (valid && delta) ? row_offset(a.pv, src_tab, itp->src_offset, t, h) : -1;
       bf16x8 zh[KS], zl[KS];
+      if (ROPE && rot) {  // uniform: the rotation reads the wave tables with shuffles
+        f32x4 dv[2 * KS], sv[2 * KS];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const u32x4 d = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
-        const u32x4 s = os >= 0 ? *reinterpret_cast<const u32x4*>(pool + os + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
-        u32x4 hw, lw;
-#pragma unroll
-        for (int w = 0; w < 4; ++w) {
-          uint32_t hh, ll;
-          split_bf16x2(bf16_lo_to_f32(d[w]) - bf16_lo_to_f32(s[w]), bf16_hi_to_f32(d[w]) - bf16_hi_to_f32(s[w]), hh,
-                       ll);
-          hw[w] = hh;
-          lw[w] = ll;
+        for (int ks = 0; ks < KS; ++ks) {
+          const u32x4 d = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+          const u32x4 s = os >= 0 ? *reinterpret_cast<const u32x4*>(pool + os + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+          dv[2 * ks] = f32x4{bf16_lo_to_f32(d[0]), bf16_hi_to_f32(d[0]), bf16_lo_to_f32(d[1]), bf16_hi_to_f32(d[1])};
+          dv[2 * ks + 1] = f32x4{bf16_lo_to_f32(d[2]), bf16_hi_to_f32(d[2]), bf16_lo_to_f32(d[3]), bf16_hi_to_f32(d[3])};
+          sv[2 * ks] = f32x4{bf16_lo_to_f32(s[0]), bf16_hi_to_f32(s[0]), bf16_lo_to_f32(s[1]), bf16_hi_to_f32(s[1])};
+          sv[2 * ks + 1] = f32x4{bf16_lo_to_f32(s[2]), bf16_hi_to_f32(s[2]), bf16_lo_to_f32(s[3]), bf16_hi_to_f32(s[3])};
         }
-        zh[ks] = as_bf16x8(hw);
-        zl[ks] = as_bf16x8(lw);
+        rope_rotate_rows_wave<D>(dv, style, g, tcd, tsd);
+        rope_rotate_rows_wave<D>(sv, style, g, tcs, tss);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          u32x4 hw, lw;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const f32x4& dd = dv[2 * ks + (w >> 1)];
+            const f32x4& ss = sv[2 * ks + (w >> 1)];
+            uint32_t hh, ll;
+            split_bf16x2(dd[2 * (w & 1)] - ss[2 * (w & 1)], dd[2 * (w & 1) + 1] - ss[2 * (w & 1) + 1], hh, ll);
+            hw[w] = hh;
+            lw[w] = ll;
+          }
+          zh[ks] = as_bf16x8(hw);
+          zl[ks] = as_bf16x8(lw);
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const u32x4 d = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+          const u32x4 s = os >= 0 ? *reinterpret_cast<const u32x4*>(pool + os + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
+          u32x4 hw, lw;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            uint32_t hh, ll;
+            split_bf16x2(bf16_lo_to_f32(d[w]) - bf16_lo_to_f32(s[w]), bf16_hi_to_f32(d[w]) - bf16_hi_to_f32(s[w]),
+                         hh, ll);
+            hw[w] = hh;
+            lw[w] = ll;
+          }
+          zh[ks] = as_bf16x8(hw);
+          zl[ks] = as_bf16x8(lw);
+        }
       }
 #pragma unroll
       for (int mt = 0; mt < MTR; ++mt) {
@@ -1268,6 +1382,10 @@ __global__ __launch_bounds__(kLayerThreads) void proj_layer_f32(LayerFitArgs a) 
   const int64_t lunit = (int64_t)lu.layer * 2 + lu.kv;
   const float* basis = st.basis + lunit * r * DL;
   float* coef = static_cast<float*>(st.coef) + lunit * (int64_t)Ts * r;
+  float* s_rope = s_b + r * DL;  // keys of a rotary cache: the tables of -pd and -ps
+  const bool rot = a.pv.rope.style != KVC_ROPE_NONE && lu.kv == 0;
+  const int style = a.pv.rope.style;
+  if (rot) layer_rope_tables<D>(a, itp, s_rope);
   for (int e = threadIdx.x; e < r * DL; e += kLayerThreads) s_b[e] = basis[e];
   __syncthreads();
   const int64_t total = (int64_t)(t_end - t_begin) * r;
@@ -1278,8 +1396,8 @@ __global__ __launch_bounds__(kLayerThreads) void proj_layer_f32(LayerFitArgs a) 
       const int64_t od = row_offset(a.pv, dst_tab, itp->dst_offset, t, h);
       const int64_t os = delta ? row_offset(a.pv, src_tab, itp->src_offset, t, h) : -1;
       for (int f = 0; f < D; ++f) {
-        float z = od >= 0 ? pool[od + f] : 0.f;
-        if (os >= 0) z -= pool[os + f];
+        float z = od >= 0 ? (rot ? layer_rope_value<D>(pool + od, f, style, s_rope, s_rope + D / 2) : pool[od + f]) : 0.f;
+        if (os >= 0) z -= rot ? layer_rope_value<D>(pool + os, f, style, s_rope + D, s_rope + 3 * D / 2) : pool[os + f];
         s = fmaf(z, s_b[kk * DL + h * D + f], s);
       }
     }
@@ -1290,6 +1408,23 @@ __global__ __launch_bounds__(kLayerThreads) void proj_layer_f32(LayerFitArgs a) 
 // ---------------------------------------------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------------------------------------------
+
+template <int D, bool DELTA, bool FULL, bool ROPE>
+static hipError_t launch_gl_one(const LayerFitArgs& a, dim3 grid, dim3 block, int pairs, int ng, hipStream_t stream) {
+  hipError_t e = hipFuncSetAttribute((const void*)gram_layer_bf16<D, DELTA, FULL, ROPE>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGLLdsBytes);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((gram_layer_bf16<D, DELTA, FULL, ROPE>), grid, block, kGLLdsBytes, stream, a, pairs, ng);
+  return hipGetLastError();
+}
+template <int D, bool ROPE>
+static hipError_t launch_gl(const LayerFitArgs& a, bool delta, bool full, dim3 grid, dim3 block, int pairs, int ng,
+                            hipStream_t stream) {
+  if (delta) return full ? launch_gl_one<D, true, true, ROPE>(a, grid, block, pairs, ng, stream)
+                         : launch_gl_one<D, true, false, ROPE>(a, grid, block, pairs, ng, stream);
+  return full ? launch_gl_one<D, false, true, ROPE>(a, grid, block, pairs, ng, stream)
+              : launch_gl_one<D, false, false, ROPE>(a, grid, block, pairs, ng, stream);
+}
 
 hipError_t launch_layer_gram(const LayerFitArgs& a, kvc_dtype dtype, hipStream_t stream) {
   const int D = a.pv.head_dim, H = a.pv.num_kv_heads, DL = H * D;
@@ -1302,24 +1437,14 @@ hipError_t launch_layer_gram(const LayerFitArgs& a, kvc_dtype dtype, hipStream_t
     const bool delta = a.mode == KVC_FIT_DELTA;
     // straight-line variant: every producing lane inside D and a row's lane offsets inside the zero page
     const bool full = DL % 256 == 0 && 2 * ((int64_t)(H - 1) * a.pv.head_stride + D) <= kGLZeroBytes;
-    const int variant = (D == 64 ? 0 : 4) + (delta ? 2 : 0) + (full ? 1 : 0);
-    const void* fns[8] = {(const void*)gram_layer_bf16<64, false, false>, (const void*)gram_layer_bf16<64, false, true>,
-                          (const void*)gram_layer_bf16<64, true, false>,  (const void*)gram_layer_bf16<64, true, true>,
-                          (const void*)gram_layer_bf16<128, false, false>, (const void*)gram_layer_bf16<128, false, true>,
-                          (const void*)gram_layer_bf16<128, true, false>,  (const void*)gram_layer_bf16<128, true, true>};
-    hipError_t e = hipFuncSetAttribute(fns[variant], hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGLLdsBytes);
-    if (e != hipSuccess) return e;
+    const bool rope = a.pv.rope.style != KVC_ROPE_NONE;
     const dim3 grid(nwork), block(kGLThreads);
-    switch (variant) {
-      case 0: hipLaunchKernelGGL((gram_layer_bf16<64, false, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
-      case 1: hipLaunchKernelGGL((gram_layer_bf16<64, false, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
-      case 2: hipLaunchKernelGGL((gram_layer_bf16<64, true, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
-      case 3: hipLaunchKernelGGL((gram_layer_bf16<64, true, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
-      case 4: hipLaunchKernelGGL((gram_layer_bf16<128, false, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
-      case 5: hipLaunchKernelGGL((gram_layer_bf16<128, false, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
-      case 6: hipLaunchKernelGGL((gram_layer_bf16<128, true, false>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
-      default: hipLaunchKernelGGL((gram_layer_bf16<128, true, true>), grid, block, kGLLdsBytes, stream, a, pairs, NG); break;
-    }
+    hipError_t e;
+    if (D == 64) e = rope ? launch_gl<64, true>(a, delta, full, grid, block, pairs, NG, stream)
+                          : launch_gl<64, false>(a, delta, full, grid, block, pairs, NG, stream);
+    else e = rope ? launch_gl<128, true>(a, delta, full, grid, block, pairs, NG, stream)
+                  : launch_gl<128, false>(a, delta, full, grid, block, pairs, NG, stream);
+    if (e != hipSuccess) return e;
     upper_only = 1;
   } else if (dtype == KVC_BF16) {
     dim3 grid((a.max_parts + kLayerWaves / 2 - 1) / (kLayerWaves / 2), H * (H + 1) / 2, a.num_units);
@@ -1394,30 +1519,30 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
   return hipGetLastError();
 }
 
+// float32: the basis [rank][H d], then the rotary angle tables (cos / sin at -pd and -ps, D / 2 each)
 size_t layer_proj_lds_bytes(int D, int H, int rank, kvc_dtype dtype) {
   if (dtype == KVC_BF16) return (size_t)2 * 2 * ((rank + 15) / 16 * 16) * D * sizeof(uint16_t);
-  return (size_t)rank * H * D * sizeof(float);
+  return (size_t)rank * H * D * sizeof(float) + kLayerRopeTableBytes;
 }
 
-template <int D>
+template <int D, int MTR, bool ROPE>
+static hipError_t launch_pl_one(const LayerFitArgs& a, dim3 grid, size_t lds, hipStream_t stream) {
+  hipError_t e = hipFuncSetAttribute((const void*)proj_layer_bf16<D, MTR, ROPE>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((proj_layer_bf16<D, MTR, ROPE>), grid, dim3(kPLThreads), lds, stream, a);
+  return hipGetLastError();
+}
+
+template <int D, bool ROPE>
 static hipError_t launch_proj_layer_bf16(const LayerFitArgs& a, dim3 grid, size_t lds, hipStream_t stream) {
   const int mtr = (a.rank + 15) / 16;
-  const void* fn;
   switch (mtr <= 1 ? 1 : mtr <= 2 ? 2 : mtr <= 4 ? 4 : 8) {
-    case 1: fn = (const void*)proj_layer_bf16<D, 1>; break;
-    case 2: fn = (const void*)proj_layer_bf16<D, 2>; break;
-    case 4: fn = (const void*)proj_layer_bf16<D, 4>; break;
-    default: fn = (const void*)proj_layer_bf16<D, 8>; break;
+    case 1: return launch_pl_one<D, 1, ROPE>(a, grid, lds, stream);
+    case 2: return launch_pl_one<D, 2, ROPE>(a, grid, lds, stream);
+    case 4: return launch_pl_one<D, 4, ROPE>(a, grid, lds, stream);
+    default: return launch_pl_one<D, 8, ROPE>(a, grid, lds, stream);
   }
-  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  switch (mtr <= 1 ? 1 : mtr <= 2 ? 2 : mtr <= 4 ? 4 : 8) {
-    case 1: hipLaunchKernelGGL((proj_layer_bf16<D, 1>), grid, dim3(kPLThreads), lds, stream, a); break;
-    case 2: hipLaunchKernelGGL((proj_layer_bf16<D, 2>), grid, dim3(kPLThreads), lds, stream, a); break;
-    case 4: hipLaunchKernelGGL((proj_layer_bf16<D, 4>), grid, dim3(kPLThreads), lds, stream, a); break;
-    default: hipLaunchKernelGGL((proj_layer_bf16<D, 8>), grid, dim3(kPLThreads), lds, stream, a); break;
-  }
-  return hipGetLastError();
 }
 
 hipError_t launch_layer_proj(const LayerFitArgs& a, kvc_dtype dtype, int max_tokens, hipStream_t stream) {
@@ -1426,8 +1551,13 @@ hipError_t launch_layer_proj(const LayerFitArgs& a, kvc_dtype dtype, int max_tok
   // the bf16 kernel stages RP = 16 MTR rank rows (MTR in 1, 2, 4, 8) of one head, hi and lo, in two buffers
   const int mtr = (a.rank + 15) / 16, mtr_inst = mtr <= 1 ? 1 : mtr <= 2 ? 2 : mtr <= 4 ? 4 : 8;
   const size_t lds = (size_t)2 * 2 * 16 * mtr_inst * D * sizeof(uint16_t);
-  if (dtype == KVC_BF16)
-    return D == 64 ? launch_proj_layer_bf16<64>(a, grid, lds, stream) : launch_proj_layer_bf16<128>(a, grid, lds, stream);
+  if (dtype == KVC_BF16) {
+    if (a.pv.rope.style != KVC_ROPE_NONE)
+      return D == 64 ? launch_proj_layer_bf16<64, true>(a, grid, lds, stream)
+                     : launch_proj_layer_bf16<128, true>(a, grid, lds, stream);
+    return D == 64 ? launch_proj_layer_bf16<64, false>(a, grid, lds, stream)
+                   : launch_proj_layer_bf16<128, false>(a, grid, lds, stream);
+  }
   const size_t flds = layer_proj_lds_bytes(D, H, a.rank, dtype);
   const void* fn = D == 64 ? (const void*)proj_layer_f32<64> : (const void*)proj_layer_f32<128>;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)flds);

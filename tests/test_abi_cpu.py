@@ -350,8 +350,8 @@ def test_gate_workspace_query():
 
 
 def test_per_layer_states_are_refused_where_unsupported():
-    """Chain and anchors take per-head states; the per-layer fit takes no rotary keys and D = H d <= 1024 with
-    rank + 16 <= 128 (the Rayleigh-Ritz subspace)."""
+    """Chain and anchors take per-head states; the per-layer fit takes D = H d <= 1024 with rank + 16 <= 128 (the
+    Rayleigh-Ritz subspace), and rotary keys in a bf16 cache only with power-of-two blocks of at least 8."""
     lib = kvc.load()
     f = Fixture(T=300)
     L, H, d = f.cache.num_layers, f.cache.num_kv_heads, f.cache.head_dim
@@ -378,7 +378,11 @@ def test_per_layer_states_are_refused_where_unsupported():
     inv = (ctypes.c_double * 64)(*([1e-3] * 64))
     f.cache.rope_style = kvc.KVC_ROPE_HALF
     f.cache.rope_inv_freq = ctypes.cast(inv, ctypes.POINTER(ctypes.c_double))
-    assert fit() == kvc.KVC_ERR_UNSUPPORTED
+    assert ws() > 0                    # rotary keys with a power-of-two block size of at least 8
+    f.cache.block_size = 12            # bf16 rotary keys need the LDS Gram (power-of-two blocks of at least 8)
+    f.cache.block_stride = 12 * H * d
+    f.cache.num_blocks = 128
+    assert ws() == 0 and fit() == kvc.KVC_ERR_UNSUPPORTED
 
 
 def test_gate_noalloc_rejects_before_launch():

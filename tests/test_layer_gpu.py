@@ -250,3 +250,85 @@ def test_layer_fit_tie_at_truncation():
         print(f"kv {kv}: EY residual {resid:.6e} vs optimal {optimal:.6e}, coverage {coverage:.1e}, "
               f"leakage {leakage:.1e}")
         assert coverage <= 1e-3 and leakage <= 1e-3
+
+
+def _rotate(x, pos, inv, style):
+    """Rows x (float64 [..., d]) rotated by the angles pos * inv[i] of their feature pairs (rotate-half pairs
+    (i, i + d/2) or adjacent pairs (2i, 2i + 1)): the rotary encoding of a key at position pos."""
+    d = x.shape[-1]
+    ang = pos * torch.as_tensor(inv, dtype=torch.float64)
+    c, s = ang.cos(), ang.sin()
+    if style == kvc.KVC_ROPE_HALF:
+        a, b = x[..., : d // 2], x[..., d // 2:]
+        return torch.cat([a * c - b * s, a * s + b * c], -1)
+    a, b = x[..., 0::2], x[..., 1::2]
+    out = torch.empty_like(x)
+    out[..., 0::2] = a * c - b * s
+    out[..., 1::2] = a * s + b * c
+    return out
+
+
+# Per-layer factorisation with rotary keys (Section 3.3 granularity, Eq. 12 with Align): the key deviation is planted in
+# canonical coordinates, C_dst = R(pd) (R(-ps) C_src + D) with D of exact rank r per layer plus N(0, 1e-3^2) noise
+# (values: C_dst = C_src + D'), so the truncation is well defined for any pair of positions.
+@pytest.mark.parametrize("H,d,T,rank,style,ps,pd,dt", [
+    (8, 128, 900, 32, kvc.KVC_ROPE_HALF, 1000, 1000, "bf16"),
+    (8, 128, 1100, 32, kvc.KVC_ROPE_HALF, 300, 5000, "bf16"),
+    (4, 128, 700, 16, kvc.KVC_ROPE_PAIRS, 0, 4096, "bf16"),
+    (5, 64, 600, 24, kvc.KVC_ROPE_HALF, 4096, 17, "bf16"),
+    (2, 64, 300, 8, kvc.KVC_ROPE_PAIRS, 77, 900, "f32"),
+])
+def test_layer_fit_with_rope(H, d, T, rank, style, ps, pd, dt):
+    base = synth.WORKLOADS["llama8b_4k"] if dt == "bf16" else synth.WORKLOADS["tiny"]
+    w = base.with_(num_layers=1, num_kv_heads=H, head_dim=d, seq_tokens=(T,), num_agents=2)
+    pc = synth.build_paged(w, device="cuda", num_output_agents=1)
+    src, dst, out = pc.seqs[(0, 0)], pc.seqs[(0, 1)], pc.seqs[(0, 100)]
+    inv = Hp.rope_inv_freq(d, 5e5)
+    g = torch.Generator().manual_seed(211 + rank)
+    for kv, pool in ((0, pc.k_pools[0]), (1, pc.v_pools[0])):
+        bs, ss = _rows(pc, src, pool)
+        bd, sd = _rows(pc, dst, pool)
+        x = pool[bs, ss].to("cpu", torch.float64)                          # [T, H, d]
+        u = torch.linalg.qr(torch.randn(T, rank, generator=g, dtype=torch.float64))[0]
+        v = torch.linalg.qr(torch.randn(H * d, rank, generator=g, dtype=torch.float64))[0]
+        sv = torch.sort(0.5 + 0.5 * torch.rand(rank, generator=g, dtype=torch.float64), descending=True)[0]
+        dev = (u * sv) @ v.T
+        dev *= 0.25 / dev.square().mean().sqrt()
+        dev = (dev + 1e-3 * torch.randn(T, H * d, generator=g, dtype=torch.float64)).reshape(T, H, d)
+        y = _rotate(_rotate(x, -ps, inv, style) + dev, pd, inv, style) if kv == 0 else x + dev
+        pool[bd, sd] = y.to(pool.dtype).to(pool.device)
+    tab = (lambda s: None) if pc.tables is None else (lambda s: pc.tables[[s.table_row]])
+    sdt = synth.storage_dtype(w)
+    st = kvc.State.empty_layer(1, H, d, T, rank, sdt, "cuda")
+    cache = kvc.Cache(pc.k_pools, pc.v_pools, rope_style=style, rope_inv_freq=inv)
+    kvc.kvc_fit_state(cache, kvc.Batch([T], [src.offset], [dst.offset], [st], tab(src), tab(dst),
+                                       src_positions=[ps], dst_positions=[pd]))
+    # materialise agent 1's cache from agent 0's through the fitted per-layer state (rotary apply)
+    kvc.kvc_apply(cache, kvc.Batch([T], [src.offset], [out.offset], [st], tab(src), tab(out), src_positions=[ps],
+                                   dst_positions=[pd]))
+    torch.cuda.synchronize()
+    rope = O.Rope(inv, Hp.ROPE_STYLE_NAME[style])
+    cnp = Hp.oracle_cache(pc.k_pools, pc.v_pools, w.block_size, rope)
+    item = O.Item(T, src.offset, dst.offset, Hp.table_np(tab(src), 0), Hp.table_np(tab(dst), 0), None, ps, pd)
+    ost, raw = O.fit(cnp, [item], rank, grouping=O.GROUP_LAYER)
+    coef, basis, sigma = raw[0]
+    gc = O.to_f64(Hp.to_np_storage(st.coef), dt)
+    gb = st.basis.cpu().numpy().astype(np.float64).reshape(1, 2, rank, H * d)
+    gs = st.sigma.cpu().numpy().astype(np.float64)
+    worst_p = worst_s = 0.0
+    for idx in np.ndindex(1, 2):
+        b = gb[idx]
+        assert np.allclose(b @ b.T, np.eye(rank), atol=2e-6), idx
+        worst_p = max(worst_p, O.max_relative_error(gc[idx] @ b, coef[idx] @ basis[idx]))
+        worst_s = max(worst_s, np.max(np.abs(gs[idx] - sigma[idx])) / sigma[idx][0])
+    oitem = O.Item(T, src.offset, out.offset, item.src_table, Hp.table_np(tab(out), 0), ost[0], ps, pd)
+    ref = O.apply(cnp, [oitem])
+    worst_c = 0.0
+    for kv in range(2):
+        for h in range(H):
+            gr = O.read_rows(cnp, 0, kv, h, oitem.dst_table, out.offset, T)
+            e = O.read_rows(ref, 0, kv, h, oitem.dst_table, out.offset, T)
+            worst_c = max(worst_c, O.max_relative_error(O.to_f64(gr, dt), O.to_f64(e, dt)))
+    print(f"rope {style} {ps}->{pd} H {H} d {d} rank {rank} {dt}: product err {worst_p:.2e}, sigma err "
+          f"{worst_s:.2e}, materialised err {worst_c:.2e}")
+    assert worst_p <= TOL_PROD[dt] and worst_s <= 1e-4 and worst_c <= TOL_CACHE[dt]
