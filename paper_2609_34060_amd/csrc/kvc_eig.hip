@@ -22,6 +22,7 @@ constexpr int kEigThreads = 1024;
 constexpr int kEigWaves = kEigThreads / kWave;
 constexpr int kReflChunk = 16;  // reflectors staged in LDS per back-transformation chunk
 constexpr int kInvBatch = 32;   // eigenvectors per inverse-iteration batch (one lane each)
+constexpr int kBisShifts = 2;   // Sturm counts per lane and bisection step
 
 // fp64 cross-lane moves by DPP (two 32-bit halves); lanes whose row is masked off receive 0.
 template <int CTRL, int ROW_MASK = 0xF>
@@ -140,151 +141,192 @@ __device__ __forceinline__ void reflector_scalars(double x0, double s, double* o
   out[2] = nrm == 0.0 ? 0.0 : recip(nrm * (nrm + fabs(x0)));
 }
 
-// Number of eigenvalues of T below x (ratio form of the Sturm sequence; pivots smaller than pivmin are replaced
-// by -pivmin, so that b^2 / q stays finite).
-template <int N>
-__device__ __forceinline__ int sturm_count(const double* sa, const double* sb2, double x, double pivmin) {
-  double q = sa[0] - x;
-  if (fabs(q) < pivmin) q = -pivmin;
-  int c = q < 0.0;
+// Numbers of eigenvalues of T below each of the M shifts x[m] (ratio form of the Sturm sequence; pivots smaller
+// than pivmin are replaced by -pivmin, so that b^2 / q stays finite).  The M recurrences are independent, so their
+// latencies overlap, and they share the loads of T.
+template <int N, int M>
+__device__ __forceinline__ void sturm_counts(const double* sa, const double* sb2, const double* x, double pivmin,
+                                             int* cnt) {
+  double q[M];
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    q[m] = sa[0] - x[m];
+    if (fabs(q[m]) < pivmin) q[m] = -pivmin;
+    cnt[m] = q[m] < 0.0;
+  }
 #pragma unroll 4
   for (int i = 1; i < N; ++i) {
-    q = (sa[i] - x) - sb2[i - 1] * recip(q);
-    if (fabs(q) < pivmin) q = -pivmin;
-    c += q < 0.0;
+    const double ai = sa[i], bi = sb2[i - 1];
+#pragma unroll
+    for (int m = 0; m < M; ++m) {
+      q[m] = (ai - x[m]) - bi * recip(q[m]);
+      if (fabs(q[m]) < pivmin) q[m] = -pivmin;
+      cnt[m] += q[m] < 0.0;
+    }
   }
-  return c;
 }
 
-// ---- Householder tridiagonalisation steps ----------------------------------------------------------------------
+// ---- Householder tridiagonalisation ----------------------------------------------------------------------------
 // Step k reflects x = row k beyond the diagonal (the matrix is symmetric) onto alpha e_1 with H_k = I - beta v v^T,
-// v = x - alpha e_1; with p = beta A22 v, K = beta v^T p / 2 and w = p - K v, A22 <- A22 - v w^T - w v^T.
+// v = x - alpha e_1; with p = A22 v, K = (beta^2 / 2) v^T p and w = beta p - K v, A22 <- A22 - v w^T - w v^T.
 // The matrix lives in LDS as fp32 [N][N]; the rank-2 update is two fp32 fmas per entry (v and w rounded to fp32),
-// everything else (p, K, w, the scalars, the reflectors) is fp64.  Per step:
-//   pivot (wave 0): p of step k from the row-group partials, K, w; row k + 1 under step k (the next x); the scalars
-//       of step k + 1; {v_C, w_C, x'_C} of every column to s_vw; the reflector to the workspace.
-//   sweep (all threads): rows C > k + 1 under step k; from the updated entries, the row-group partial sums of the
-//       next step's A22 v' (no scaling by beta yet).  Thread (g, R) owns column R of rows g, g + RG, ...; a row
-//       group is whole waves, so row skips are uniform; partial[g][R] goes to LDS, summed by the next pivot.
-// Step k's scalars {alpha, v_0, beta} are in s_ab + 4 (k & 1).
+// everything else (p, K, w, the scalars, the reflectors) is fp64.
+//
+// kTriWaves waves (one per SIMD) run the reduction with one workgroup barrier per step.  Lane l of every wave owns
+// the CPL = N / 64 consecutive columns CPL l ..; row R belongs to wave R mod kTriWaves.  The update of step k - 1 is
+// applied lazily: step k
+//   1. brings row k up to date in registers (every wave, from the same LDS row), forms the reflector (every wave
+//      the same scalars; wave 0 writes the reflector, alpha and the diagonal entry),
+//   2. sweeps the wave's rows R > k: applies the pending update to them and accumulates the wave's share of A22 v
+//      (fp32 fmas of the fp32 entries and the fp32 copy of v over the wave's rows; the shares are summed in fp64),
+//   3. after the barrier, sums the shares in a fixed order, so K and w, the next pending update, come out
+//      identical in every wave.
+// s_vw[R] = {v_R, w_R} of the pending update and v'_R of the current step; every wave writes the same values to
+// it, each before reading them (LDS operations of one wave complete in issue order; the fences below stop the
+// compiler from moving LDS accesses across the points where other lanes' values are read).  The shares are double
+// buffered by step parity: a wave writes step k + 1's share only after the barrier that follows every wave's reads
+// of step k - 1's.
+constexpr int kTriWaves = 4;
 
-// Wave 0.  Before the first step (k = -1) only the scalars of step 0 and s_vw are formed.  Every LDS load is issued
-// up front (indices stay in range), so the pivot waits for LDS once.
-template <int N>
-__device__ __forceinline__ void tri_pivot(float* A, const double* partial, const double* s_kp, float4* s_vw,
-                                          double* s_ab, double* s_b, double* refl, double* refl_beta, int k, int lane) {
-  constexpr int RG = kEigThreads / N;  // row groups of the sweep
-  constexpr int Q = N / kWave;         // columns per lane
-  const int kn = k + 1;
-  const int kr = k < 0 ? 0 : k;
-  const double* ab = s_ab + 4 * (kr & 1);
-  const double alpha = ab[0], v0 = k < 0 ? 0.0 : ab[1], beta = k < 0 ? 0.0 : ab[2];
-  double psum[Q];
-  float xk[Q], xn[Q];
-#pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int C = lane + kWave * q;
-    xk[q] = A[kr * N + C];
-    xn[q] = A[kn * N + C];
-    double sum = 0.0;
-#pragma unroll
-    for (int gi = 0; gi < RG; ++gi) sum += partial[gi * N + C];
-    psum[q] = k < 0 ? 0.0 : sum;  // (before the first step the partials hold nothing yet)
-  }
-  // K = (beta / 2) v^T p = (beta^2 / 2) sum of the sweep's per-wave shares
-  double kk = 0.0;
-#pragma unroll
-  for (int i = 0; i < kEigWaves; ++i) kk += s_kp[i];
-  const double K = k < 0 ? 0.0 : 0.5 * beta * beta * kk;
-  double vq[Q], wq[Q];
-#pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int C = lane + kWave * q;
-    vq[q] = k < 0 ? 0.0 : (C > kn ? (double)xk[q] : (C == kn ? v0 : 0.0));
-    wq[q] = C >= kn ? beta * psum[q] - K * vq[q] : 0.0;
-  }
-  const double wR = k < 0 ? 0.0 : lane_value(wq[kn / kWave], kn % kWave);  // w of row k + 1 (its v is v_0)
-  // row k + 1 under step k (same arithmetic as the sweep; columns below k + 1 do not change), its norm beyond the
-  // diagonal, the next scalars; s_vw[C] = {v_C, w_C, v'_C} with v' the next step's v
-  const float v0f = (float)v0, wRf = (float)wR;
-  double s = 0.0;
-#pragma unroll
-  for (int q = 0; q < Q; ++q) {
-    const int C = lane + kWave * q;
-    xn[q] = fmaf(-v0f, (float)wq[q], fmaf(-wRf, (float)vq[q], xn[q]));
-    A[kn * N + C] = xn[q];
-    s += C > kn ? (double)xn[q] * (double)xn[q] : 0.0;
-    s_vw[C] = make_float4((float)vq[q], (float)wq[q], C > kn + 1 ? xn[q] : 0.0f, 0.0f);
-  }
-  s = wave_sum(s);
-  const double x0 = lane_value((double)xn[((kn + 1) % N) / kWave], (kn + 1) % kWave);
-  if (lane == 0) {
-    double* abn = s_ab + 4 * (kn & 1);
-    reflector_scalars(kn + 1 < N ? x0 : 0.0, s, abn);
-    if (kn + 1 < N) s_vw[kn + 1].z = (float)abn[1];  // v'_{k+2} = v_0 of the next step
-  }
-  if (k >= 0) {
-    double* refl_k = refl + __builtin_amdgcn_readfirstlane(k * N);
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      const int C = lane + kWave * q;
-      if (C >= kn) refl_k[C - kn] = vq[q];
-    }
-    if (lane == 0) {
-      s_b[k] = alpha;
-      refl_beta[k] = beta;
-    }
-  }
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// All threads: rows C > k + 1 under step k (UPD; without UPD, k = -1 and nothing is updated), then the row-group
-// partial sums of A22 v' for step k + 1 and each wave's share of v'^T (A22 v').
-template <int N, bool UPD>
-__device__ __forceinline__ void tri_sweep(float* A, double* partial, double* s_kp, const float4* s_vw, int k,
-                                          int tid, int lane, int wave) {
-  constexpr int RG = kEigThreads / N;
-  constexpr int RPT = N / RG;
-  const int R = tid & (N - 1);
-  const int g = __builtin_amdgcn_readfirstlane(tid / N);  // uniform: a row group is whole waves
-  const int kn = k + 1;
-  const float4 vwR = s_vw[R];
-  // first live row of this thread: g + RG t > k + 1.  Entries of eliminated columns (R <= k + 1) are updated too
-  // (with v_R = w_R = 0 they do not change, and column k + 1 is not read again), so that stores need no mask.
-  const int t0 = kn < g ? 0 : (kn - g) / RG + 1;
-  float acc = 0.0f;
-  // rows in batches of four: every load of a batch is issued before its stores
-  auto rows = [&](int t, auto nb) {
-    constexpr int NB = decltype(nb)::value;
-    float4 vwC[NB];
-    float a[NB];
+// Waves 0 .. kTriWaves - 1 of the workgroup; the other waves meet the same N - 2 barriers.  Writes s_a (the diagonal
+// of T), s_b[0 .. N - 2] (its off-diagonal), the reflectors (v of step k in refl[k N ..]) and their beta.
+template <int N>
+__device__ __forceinline__ void tri_reduce(float* A, float4* s_vw, double* share, double* s_a, double* s_b,
+                                           double* refl, double* refl_beta, int lane, int wave) {
+  constexpr int CPL = N / kWave;
+  constexpr int W = kTriWaves;
+  if (wave >= W) {
+    for (int k = 0; k < N - 2; ++k) __syncthreads();
+    return;
+  }
+  float vpf[CPL], wpf[CPL];  // pending update of the lane's columns (fp32, as applied)
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int C = g + RG * (t + j);
-      vwC[j] = s_vw[C];
-      a[j] = A[C * N + R];
+  for (int c = 0; c < CPL; ++c) {
+    vpf[c] = wpf[c] = 0.0f;
+    *reinterpret_cast<float2*>(&s_vw[CPL * lane + c]) = make_float2(0.0f, 0.0f);
+  }
+  auto upd = [&](float a, const float4& vw, int c) { return fmaf(-vw.x, wpf[c], fmaf(-vw.y, vpf[c], a)); };
+  for (int k = 0; k < N - 2; ++k) {
+    const int k1 = k + 1;
+    wave_lds_sync();
+    // 1. row k under the pending update; its entries beyond the diagonal are x
+    const float4 vwk = s_vw[k];
+    double x[CPL];
+    double ss = 0.0;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int C = CPL * lane + c;
+      const float a = upd(A[k * N + C], vwk, c);
+      if (wave == 0 && C == k) s_a[k] = (double)a;
+      x[c] = C > k ? (double)a : 0.0;
+      ss += x[c] * x[c];
     }
+    ss = wave_sum(ss);
+    const double x0 = lane_value(x[k1 % CPL], k1 / CPL);
+    double ab[3];
+    reflector_scalars(x0, ss, ab);
+    const double beta = ab[2];
+    double v[CPL];
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int C = g + RG * (t + j);
-      if (UPD) {
-        a[j] = fmaf(-vwC[j].x, vwR.y, fmaf(-vwC[j].y, vwR.x, a[j]));
-        A[C * N + R] = a[j];
+    for (int c = 0; c < CPL; ++c) {
+      const int C = CPL * lane + c;
+      v[c] = C > k1 ? x[c] : (C == k1 ? ab[1] : 0.0);
+      s_vw[C].z = (float)v[c];
+    }
+    if (wave == 0) {
+      double* refl_k = refl + __builtin_amdgcn_readfirstlane(k * N);
+#pragma unroll
+      for (int c = 0; c < CPL; ++c)
+        if (CPL * lane + c >= k1) refl_k[CPL * lane + c - k1] = v[c];
+      if (lane == 0) {
+        s_b[k] = ab[0];
+        refl_beta[k] = beta;
       }
-      acc = fmaf(a[j], vwC[j].z, acc);
     }
-  };
-  int t = t0;
-  for (; t + 4 <= RPT; t += 4) rows(t, std::integral_constant<int, 4>());
-  for (; t < RPT; ++t) rows(t, std::integral_constant<int, 1>());
-  partial[g * N + R] = acc;
-  const double kp = group_sum<kWave>((double)acc * (double)vwR.z);
-  if (lane == kWave - 1) s_kp[wave] = kp;
+    wave_lds_sync();
+    // 2. the wave's rows R > k: the pending update, then p += a v'_R
+    float pf[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) pf[c] = 0.0f;
+    const int R0 = k1 + ((wave - k1) % W + W) % W;  // first row > k of this wave
+    int R = R0;
+    for (; R + 3 * W < N; R += 4 * W) {
+      float4 vw[4];
+      float a[4][CPL];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        vw[j] = s_vw[R + j * W];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) a[j][c] = A[(R + j * W) * N + CPL * lane + c];
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          a[j][c] = upd(a[j][c], vw[j], c);
+          A[(R + j * W) * N + CPL * lane + c] = a[j][c];
+          pf[c] = fmaf(a[j][c], vw[j].z, pf[c]);
+        }
+    }
+    for (; R < N; R += W) {
+      const float4 vw = s_vw[R];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        const float a = upd(A[R * N + CPL * lane + c], vw, c);
+        A[R * N + CPL * lane + c] = a;
+        pf[c] = fmaf(a, vw.z, pf[c]);
+      }
+    }
+    double* sh = share + (k & 1) * W * N;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) sh[wave * N + CPL * lane + c] = (double)pf[c];
+    __syncthreads();
+    // 3. p = the sum of the shares; K = (beta^2 / 2) v^T p; w = beta p - K v becomes the pending update
+    double kk = 0.0, p[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      double t = 0.0;
+#pragma unroll
+      for (int w = 0; w < W; ++w) t += sh[w * N + CPL * lane + c];
+      p[c] = t;
+      kk += CPL * lane + c > k ? v[c] * t : 0.0;
+    }
+    const double K = 0.5 * beta * beta * wave_sum(kk);
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      const int C = CPL * lane + c;
+      vpf[c] = (float)v[c];
+      wpf[c] = C > k ? (float)(beta * p[c] - K * v[c]) : 0.0f;
+      *reinterpret_cast<float2*>(&s_vw[C]) = make_float2(vpf[c], wpf[c]);
+    }
+  }
+  // the last pending update on the trailing 2 x 2 block
+  if (wave == 0) {
+    wave_lds_sync();
+#pragma unroll
+    for (int R = N - 2; R < N; ++R) {
+      const float4 vw = s_vw[R];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        const int C = CPL * lane + c;
+        const float a = upd(A[R * N + C], vw, c);
+        if (C == R) s_a[R] = (double)a;
+        if (R == N - 2 && C == N - 1) s_b[N - 2] = (double)a;
+      }
+    }
+  }
 }
 
 // LDS layout (bytes): the matrix region MREG holds, in turn, G / the trailing matrix as fp32 [N][N] (phases 1-2),
 // the inverse-iteration scratch fp64 [N][kInvBatch] x 2 (phase 4), X fp32 [r][N] (MGS, back-transformation); then
-// fp64 scalars and vectors; then the staging region: the sweep's row-group partials fp64 [RG][N] during phase 2, a
-// chunk of reflectors during phase 5.  About 79 KB for N = 128, so two units share a CU.
+// fp64 scalars and vectors; then the staging region: the sweep's per-wave shares of A22 v, fp64 [2][kTriWaves][N],
+// during phase 2, a chunk of reflectors during phase 5.  About 79 KB for N = 128, so two units share a CU.
 template <int N>
 struct EigLds {
   static constexpr size_t kMat = (size_t)N * N * 4;
@@ -292,11 +334,11 @@ struct EigLds {
   static constexpr size_t kX = (size_t)KVC_MAX_RANK * N * 4;
   static constexpr size_t kMreg = ((kMat > kScratch ? (kMat > kX ? kMat : kX) : (kScratch > kX ? kScratch : kX)) +
                                    15) / 16 * 16;
-  // s_a, s_b [N]; s_lam [KVC_MAX_RANK]; s_ab [2][4]; s_kp [kEigWaves]; s_misc [8]; s_vw float4 [N] (later b^2 [N])
-  static constexpr size_t kSmall = (size_t)(2 * N + KVC_MAX_RANK + 8 + kEigWaves + 8) * 8 + (size_t)N * 16;
-  static constexpr size_t kPartial = (size_t)(kEigThreads / N) * N * 8;
+  // s_a, s_b [N]; s_lam [KVC_MAX_RANK]; s_misc [8]; s_vw float4 [N] (later b^2 [N])
+  static constexpr size_t kSmall = (size_t)(2 * N + KVC_MAX_RANK + 8) * 8 + (size_t)N * 16;
+  static constexpr size_t kShare = (size_t)2 * kTriWaves * N * 8;
   static constexpr size_t kReflStage = (size_t)kReflChunk * (N + 1) * 4;
-  static constexpr size_t kStage = kPartial > kReflStage ? kPartial : kReflStage;
+  static constexpr size_t kStage = kShare > kReflStage ? kShare : kReflStage;
   static constexpr size_t kTotal = kMreg + kSmall + kStage;
 };
 
@@ -314,13 +356,11 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   double* s_a = reinterpret_cast<double*>(base + Lay::kMreg);  // diagonal of T
   double* s_b = s_a + N;                    // off-diagonal of T: b[i] couples i and i + 1
   double* s_lam = s_b + N;                  // eigenvalues, descending
-  double* s_ab = s_lam + KVC_MAX_RANK;      // reflector scalars {alpha, v_0, beta, -}, by step parity [2][4]
-  double* s_kp = s_ab + 8;                  // per-wave shares of v^T A22 v from the sweep [kEigWaves]
-  double* s_misc = s_kp + kEigWaves;        // scalars
-  float4* s_vw = reinterpret_cast<float4*>(s_misc + 8);  // {v_C, w_C, x'_C, -} of the current step
+  double* s_misc = s_lam + KVC_MAX_RANK;    // scalars
+  float4* s_vw = reinterpret_cast<float4*>(s_misc + 8);  // {v_C, w_C, v'_C, -} of the tridiagonalisation
   double* s_b2 = reinterpret_cast<double*>(s_vw);        // b^2 (after the tridiagonalisation)
-  double* partial = reinterpret_cast<double*>(base + Lay::kMreg + Lay::kSmall);  // sweep partials [RG][N]
-  float* s_rb = reinterpret_cast<float*>(partial);  // reflector chunk fp32 [kReflChunk][N] (back-transformation)
+  double* share = reinterpret_cast<double*>(base + Lay::kMreg + Lay::kSmall);  // shares of A22 v [2][W][N]
+  float* s_rb = reinterpret_cast<float*>(share);  // reflector chunk fp32 [kReflChunk][N] (back-transformation)
   float* s_rbeta = s_rb + kReflChunk * N;
 
   const int u = blockIdx.x;
@@ -328,7 +368,7 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   const UnitTarget tg = eig_target(a, u);
   const int r = tg.rank;
   if (r <= 0) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   double* refl = a.reflect + (size_t)u * N * N;          // v_k in row k
   double* refl_beta = a.reflect_beta + (size_t)u * N;
   double* gvec = a.vecs + (size_t)u * N * KVC_MAX_RANK;  // eigenvectors of T, vector j in row j
@@ -348,19 +388,8 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   }
   __syncthreads();
 
-  // ---- 2. Householder tridiagonalisation -----------------------------------------------------------------------
-  if (wave == 0) tri_pivot<N>(A, partial, s_kp, s_vw, s_ab, s_b, refl, refl_beta, -1, lane);
-  __syncthreads();
-  tri_sweep<N, false>(A, partial, s_kp, s_vw, -1, tid, lane, wave);
-  __syncthreads();
-  for (int k = 0; k < N - 2; ++k) {
-    if (wave == 0) tri_pivot<N>(A, partial, s_kp, s_vw, s_ab, s_b, refl, refl_beta, k, lane);
-    __syncthreads();
-    tri_sweep<N, true>(A, partial, s_kp, s_vw, k, tid, lane, wave);
-    __syncthreads();
-  }
-  for (int i = tid; i < N; i += kEigThreads) s_a[i] = A[i * LD + i];
-  if (tid == 0) s_b[N - 2] = A[(N - 2) * LD + N - 1];
+  // ---- 2. Householder tridiagonalisation ------------------------------------------------------------------------
+  tri_reduce<N>(A, s_vw, share, s_a, s_b, refl, refl_beta, lane, wave);
   __syncthreads();
   for (int i = tid; i < N - 1; i += kEigThreads) s_b2[i] = s_b[i] * s_b[i];
   if (tid == 0) {
@@ -392,24 +421,36 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
     {
       int rp = 1;
       while (rp < r) rp <<= 1;
-      // lanes per eigenvalue (a power of two dividing 64): 8 lanes and 11 steps of 9-way splitting (88 Sturm counts
-      // per eigenvalue) measured faster than 16 lanes and 8 steps (128 counts) or 4 lanes and 14 steps (56)
+      // P lanes per eigenvalue (a power of two dividing 64), each evaluating kBisShifts shifts: the bracket is cut
+      // into S = P kBisShifts + 1 pieces per step
       const int P = min(8, kEigThreads / rp);
-      // each step shrinks the bracket (P + 1)-fold; stop below 2^-32 of the Gershgorin interval, under the
-      // perturbation that fp32 storage of the matrix already carries
-      const int iters = P >= 16 ? 8 : P >= 8 ? 11 : P >= 4 ? 14 : P >= 2 ? 21 : 32;
+      const int S = P * kBisShifts + 1;
+      // stop below 2^-32 of the Gershgorin interval, under the perturbation that fp32 storage of the matrix
+      // already carries
+      int iters = 0;
+      for (double w = 1.0; w < 4294967296.0; w *= S) ++iters;
       const int grp = tid / P, s = tid - grp * P;
       const int kasc = N - 1 - grp;                  // ascending index of the target eigenvalue
       const double pivmin = s_misc[4];
       double lo = s_misc[1], hi = s_misc[2];
       for (int it = 0; it < iters; ++it) {
-        const double x = lo + (hi - lo) * (double)(s + 1) / (double)(P + 1);
-        const int c = grp < r ? sturm_count<N>(s_a, s_b2, x, pivmin) : 0;
-        const uint64_t mask = __ballot(c <= kasc);
-        const uint64_t gmask = P == kWave ? mask : (mask >> ((lane / P) * P)) & ((1ull << P) - 1ull);
-        const int sstar = __popcll(gmask);
-        const double nlo = sstar == 0 ? lo : lo + (hi - lo) * (double)sstar / (double)(P + 1);
-        const double nhi = sstar == P ? hi : lo + (hi - lo) * (double)(sstar + 1) / (double)(P + 1);
+        double x[kBisShifts];
+        int c[kBisShifts];
+#pragma unroll
+        for (int m = 0; m < kBisShifts; ++m) {
+          x[m] = lo + (hi - lo) * (double)(s * kBisShifts + m + 1) / (double)S;
+          c[m] = 0;
+        }
+        if (grp < r) sturm_counts<N, kBisShifts>(s_a, s_b2, x, pivmin, c);
+        // shifts left of the target form a prefix of the S - 1 cut points; sstar counts them
+        int sstar = 0;
+#pragma unroll
+        for (int m = 0; m < kBisShifts; ++m) {
+          const uint64_t mask = __ballot(c[m] <= kasc);
+          sstar += __popcll(P == kWave ? mask : (mask >> ((lane / P) * P)) & ((1ull << P) - 1ull));
+        }
+        const double nlo = sstar == 0 ? lo : lo + (hi - lo) * (double)sstar / (double)S;
+        const double nhi = sstar == S - 1 ? hi : lo + (hi - lo) * (double)(sstar + 1) / (double)S;
         lo = nlo;
         hi = nhi;
       }
@@ -423,50 +464,54 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
       const int j = j0 + tid;
       if (tid < kInvBatch && j < r) {
         const double lam = s_lam[j];
+        // LDL^T of T - lam I without pivoting (tiny pivots replaced): invd[i] = 1 / d_i; pseudo-random start
         double d = s_a[0] - lam;
         if (fabs(d) < piv) d = copysign(piv, d);
-        invd[tid] = 1.0 / d;
-#pragma unroll 2
+        double id = recip(d);
+        invd[tid] = id;
+#pragma unroll 4
         for (int i = 1; i < N; ++i) {
-          const double l = s_b[i - 1] * invd[(i - 1) * kInvBatch + tid];
-          d = (s_a[i] - lam) - l * s_b[i - 1];
+          const double b = s_b[i - 1];
+          d = (s_a[i] - lam) - b * id * b;
           if (fabs(d) < piv) d = copysign(piv, d);
-          invd[i * kInvBatch + tid] = 1.0 / d;
+          id = recip(d);
+          invd[i * kInvBatch + tid] = id;
         }
-#pragma unroll 2
+#pragma unroll 4
         for (int i = 0; i < N; ++i) {
           const uint32_t h = hash3(a.seed ^ (uint32_t)u, (uint32_t)j, (uint32_t)i);
           xv[i * kInvBatch + tid] = (double)(h >> 11) * (1.0 / 2097152.0) - 1.0;
         }
+        // three solves (T - lam I) x_new = x; each right-hand side is scaled by 1 / max|x| on the way in
+        double sc = 1.0;
         for (int itr = 0; itr < 3; ++itr) {
-          double z = xv[tid];
-#pragma unroll 2
+          double z = xv[tid] * sc;
+          xv[tid] = z;
+#pragma unroll 4
           for (int i = 1; i < N; ++i) {
-            z = xv[i * kInvBatch + tid] - s_b[i - 1] * invd[(i - 1) * kInvBatch + tid] * z;
+            z = xv[i * kInvBatch + tid] * sc - s_b[i - 1] * invd[(i - 1) * kInvBatch + tid] * z;
             xv[i * kInvBatch + tid] = z;
           }
-          double x = xv[(N - 1) * kInvBatch + tid] * invd[(N - 1) * kInvBatch + tid];
+          double x = z * invd[(N - 1) * kInvBatch + tid];
           xv[(N - 1) * kInvBatch + tid] = x;
           double mx = fabs(x);
-#pragma unroll 2
+#pragma unroll 4
           for (int i = N - 2; i >= 0; --i) {
             x = (xv[i * kInvBatch + tid] - s_b[i] * x) * invd[i * kInvBatch + tid];
             xv[i * kInvBatch + tid] = x;
             mx = fmax(mx, fabs(x));
           }
-          const double sc = mx > 0.0 ? 1.0 / mx : 1.0;
-          double ss = 0.0;
-#pragma unroll 2
-          for (int i = 0; i < N; ++i) {
-            const double y = xv[i * kInvBatch + tid] * sc;
-            ss += y * y;
-          }
-          const double f = sc / sqrt(ss);
-#pragma unroll 2
-          for (int i = 0; i < N; ++i) xv[i * kInvBatch + tid] *= f;
+          sc = mx > 0.0 ? 1.0 / mx : 1.0;
         }
-#pragma unroll 2
-        for (int i = 0; i < N; ++i) gvec[(size_t)j * N + i] = xv[i * kInvBatch + tid];
+        double ss = 0.0;
+#pragma unroll 4
+        for (int i = 0; i < N; ++i) {
+          const double y = xv[i * kInvBatch + tid] * sc;
+          ss += y * y;
+        }
+        const double f = sc / sqrt(ss);
+#pragma unroll 4
+        for (int i = 0; i < N; ++i) gvec[(size_t)j * N + i] = xv[i * kInvBatch + tid] * f;
       }
       __syncthreads();
     }

@@ -582,35 +582,58 @@ __global__ __launch_bounds__(kFitThreads) void gram_f32_valu(FitArgs a) {
 // Projection coef = Z R_r, bf16 caches
 // ---------------------------------------------------------------------------------------------------------------
 
-constexpr int kProjTilesPerWave = 16;
-constexpr int kProjChunk = kFitWaves * kProjTilesPerWave * 16;
-constexpr bool kProjRegFrags = false;  // basis fragments held in registers (ranks up to 32) or read from LDS per tile
-constexpr bool kProjPrefetch = false;  // the next tile's rows are loaded before this tile's products
+// Workgroups of kProjWaves waves take kProjChunkTokens tokens of one (item, layer, K/V, head) unit; rotary keys
+// take kProjRopeWaves waves and kProjRopeChunkTokens tokens (every workgroup forms fp64 angle tables, which the
+// longer chunk amortises, and the rotation's registers leave room for fewer waves).  Each wave takes 16-token
+// tiles; the loads of its next tile are issued before this tile's products and coefficient stores (loads and
+// stores leave a wave in order), and row addresses come from the chunk's block-table slices in LDS, so no table
+// read sits between two row loads.
+constexpr int kProjWaves = 8, kProjChunkTokens = 512;
+constexpr int kProjRopeWaves = 4, kProjRopeChunkTokens = 1024;
+constexpr int kProjChunk = 1024;  // tokens per workgroup of the float32 kernel
 
-template <int D, int MTR, bool ROPE>
-__global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
+__host__ __device__ constexpr size_t proj_lds_bytes(int D, int RP, int nblk) {
+  return (size_t)2 * RP * D * 2 + (size_t)2 * nblk * 4;
+}
+
+template <int D, int MTR, int W, bool ROPE>
+__global__ __launch_bounds__(W * kWave) void proj_bf16_mfma(FitArgs a, int tpw, int nblk) {
   constexpr int KS = D / 32;          // K-steps over features
   constexpr int RP = MTR * 16;        // padded rank
-  constexpr bool kRegFrags = kProjRegFrags && MTR <= 2;
-  constexpr int FM = kRegFrags ? MTR : 1, FK = kRegFrags ? KS : 1;
-  __shared__ __attribute__((aligned(16))) uint16_t s_hi[RP * D];
-  __shared__ __attribute__((aligned(16))) uint16_t s_lo[RP * D];
+  extern __shared__ __attribute__((aligned(16))) uint16_t s_dyn[];
+  uint16_t* s_hi = s_dyn;
+  uint16_t* s_lo = s_dyn + RP * D;
+  int32_t* s_tab = reinterpret_cast<int32_t*>(s_dyn + 2 * RP * D);  // [2][nblk]: source, destination
 
   const FitUnit f = fit_unit(a);
   const kvc_item* itp = a.items + f.item;
   const int r = itp->state.rank;
   const int Ts = itp->state.num_tokens;
-  const int t_begin = blockIdx.x * kProjChunk;
-  if (r == 0 || t_begin >= Ts) return;
-  const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
-  const int32_t* dst_tab = a.dst_tables ? a.dst_tables + (int64_t)f.item * a.max_blocks : nullptr;
+  const int chunk = W * 16 * tpw;
+  const int t_begin = blockIdx.x * chunk;
+  if (r == 0 || t_begin >= Ts) return;  // whole workgroup
+  const int t_end = min(Ts, t_begin + chunk);
   const uint16_t* pool = static_cast<const uint16_t*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
   const bool delta = a.mode == KVC_FIT_DELTA;
   const float* basis = itp->state.basis + f.unit * (int64_t)r * D;
   uint16_t* coef = static_cast<uint16_t*>(itp->state.coef) + f.unit * (int64_t)Ts * r;
+  const int src_off = itp->src_offset, dst_off = itp->dst_offset;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, n = lane & 15;
+
+  // block ids of the chunk's logical blocks (the host checked that they lie inside the item's table row)
+  const int bs = a.pv.block_size, bsh = a.pv.block_shift;
+  auto lblock = [&](int p) { return bsh >= 0 ? p >> bsh : p / bs; };
+  const int lb0s = lblock(src_off + t_begin), lb0d = lblock(dst_off + t_begin);
+  {
+    const int ns = delta ? lblock(src_off + t_end - 1) - lb0s + 1 : 0;
+    const int nd = lblock(dst_off + t_end - 1) - lb0d + 1;
+    const int32_t* st = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
+    const int32_t* dt = a.dst_tables ? a.dst_tables + (int64_t)f.item * a.max_blocks : nullptr;
+    for (int i = tid; i < ns; i += W * kWave) s_tab[i] = st ? st[lb0s + i] : lb0s + i;
+    for (int i = tid; i < nd; i += W * kWave) s_tab[nblk + i] = dt ? dt[lb0d + i] : lb0d + i;
+  }
   // rotary keys: Z = R(-pd) C_dst - R(-ps) C_src (angle tables ready at the staging barrier below)
   __shared__ float s_rope[4][ROPE ? D / 2 : 1];
   const bool rope = ROPE && f.kv == 0;  // uniform over the workgroup
@@ -619,8 +642,7 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
     rope_table(a.pv.rope, D, -(double)itp->dst_position, s_rope[0], s_rope[1]);
     rope_table(a.pv.rope, D, -(double)itp->src_position, s_rope[2], s_rope[3]);
   }
-
-  for (int e = tid; e < RP * D; e += kFitThreads) {
+  for (int e = tid; e < RP * D; e += W * kWave) {
     const int k = e / D;
     const float x = k < r ? basis[e] : 0.f;
     uint32_t hb, lb;
@@ -629,27 +651,25 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
     s_lo[e] = (uint16_t)lb;
   }
   __syncthreads();
-  bf16x8 ah[FM][FK], al[FM][FK];
-  if constexpr (kRegFrags) {
-#pragma unroll
-    for (int mt = 0; mt < MTR; ++mt)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int o = (16 * mt + n) * D + 32 * ks + 8 * g;
-        ah[mt][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[o]));
-        al[mt][ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[o]));
-      }
-  }
 
-  // Rows of tile j: the dst (and src) row of token t0 + n, features 32 ks + 8 g .. + 7; lanes past T_s load nothing.
+  // Row offset of token t through a staged table slice (-1 when the block id is out of range: the row reads as 0).
+  auto row_off = [&](int off, int lb0, const int32_t* tab, int t) -> int64_t {
+    const int p = off + t, lb = lblock(p), slot = p - lb * bs;
+    const int32_t blk = tab[lb - lb0];
+    if (blk < 0 || blk >= a.pv.num_blocks) return -1;
+    return (int64_t)blk * a.pv.block_stride + (int64_t)slot * a.pv.token_stride + (int64_t)f.head * a.pv.head_stride;
+  };
+  // Rows of tile j: the dst (and src) row of token t0 + n, features 32 ks + 8 g .. + 7; lanes past the chunk load
+  // nothing.
   struct Rows {
     u32x4 d[KS], s[KS];
   };
-  auto load_rows = [&](int j, Rows& R) {
-    const int t = t_begin + (j * kFitWaves + wave) * 16 + n;
-    const bool valid = t < Ts;
-    const int64_t od = valid ? row_offset(a.pv, dst_tab, itp->dst_offset, t, f.head) : -1;
-    const int64_t os = (valid && delta) ? row_offset(a.pv, src_tab, itp->src_offset, t, f.head) : -1;
+  auto tile_t0 = [&](int j) { return t_begin + (j * W + wave) * 16; };
+  auto load_rows = [&](int j, Rows& R) __attribute__((always_inline)) {
+    const int t = tile_t0(j) + n;
+    const bool valid = t < t_end;
+    const int64_t od = valid ? row_off(dst_off, lb0d, s_tab + nblk, t) : -1;
+    const int64_t os = (valid && delta) ? row_off(src_off, lb0s, s_tab, t) : -1;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       R.d[ks] = od >= 0 ? *reinterpret_cast<const u32x4*>(pool + od + 32 * ks + 8 * g) : u32x4{0, 0, 0, 0};
@@ -657,9 +677,9 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
     }
   };
   // Z hi/lo of tile j, its products with the basis, the coefficient rows.
-  auto finish = [&](int j, const Rows& R) {
-    const int t = t_begin + (j * kFitWaves + wave) * 16 + n;
-    const bool valid = t < Ts;
+  auto finish = [&](int j, const Rows& R) __attribute__((always_inline)) {
+    const int t = tile_t0(j) + n;
+    const bool valid = t < t_end;
     bf16x8 zh[KS], zl[KS];
     if (ROPE && rope) {
       f32x4 dv[2 * KS], sv[2 * KS];
@@ -710,15 +730,9 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 fh, fl;
-        if constexpr (kRegFrags) {
-          fh = ah[mt][ks];
-          fl = al[mt][ks];
-        } else {
-          const int o = (16 * mt + n) * D + 32 * ks + 8 * g;
-          fh = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[o]));
-          fl = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[o]));
-        }
+        const int o = (16 * mt + n) * D + 32 * ks + 8 * g;
+        const bf16x8 fh = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_hi[o]));
+        const bf16x8 fl = as_bf16x8(*reinterpret_cast<const u32x4*>(&s_lo[o]));
         acc = mfma16x16x32(fl, zh[ks], acc);
         acc = mfma16x16x32(fh, zl[ks], acc);
         acc = mfma16x16x32(fh, zh[ks], acc);
@@ -741,23 +755,19 @@ __global__ __launch_bounds__(kFitThreads) void proj_bf16_mfma(FitArgs a) {
     }
   };
 
-  auto tile_start = [&](int j) { return t_begin + (j * kFitWaves + wave) * 16; };
-  if constexpr (kProjPrefetch) {
-    Rows cur, nxt;
-    load_rows(0, cur);
-    for (int j = 0; j < kProjTilesPerWave; ++j) {
-      if (tile_start(j) >= Ts) break;
-      if (j + 1 < kProjTilesPerWave && tile_start(j + 1) < Ts) load_rows(j + 1, nxt);
-      finish(j, cur);
-      cur = nxt;
-    }
-  } else {
-    for (int j = 0; j < kProjTilesPerWave; ++j) {
-      if (tile_start(j) >= Ts) break;
-      Rows cur;
-      load_rows(j, cur);
-      finish(j, cur);
-    }
+  // tiles of this wave in pairs: the loads of the next tile are in flight while this one is finished
+  Rows ra, rb;
+  if (tile_t0(0) >= t_end) return;  // whole wave
+  load_rows(0, ra);
+  for (int j = 0;; j += 2) {
+    const bool m1 = j + 1 < tpw && tile_t0(j + 1) < t_end;
+    if (m1) load_rows(j + 1, rb);
+    finish(j, ra);
+    if (!m1) break;
+    const bool m2 = j + 2 < tpw && tile_t0(j + 2) < t_end;
+    if (m2) load_rows(j + 2, ra);
+    finish(j + 1, rb);
+    if (!m2) break;
   }
 }
 
@@ -814,7 +824,6 @@ __global__ __launch_bounds__(kFitThreads) void proj_f32_valu(FitArgs a) {
 // Launchers
 // ---------------------------------------------------------------------------------------------------------------
 
-int proj_chunk_tokens() { return kProjChunk; }
 
 template <bool ROPE>
 static hipError_t launch_gram_variants(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream) {
@@ -850,27 +859,42 @@ hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hip
                                           : launch_gram_variants<false>(a, dtype, num_items, stream);
 }
 
-template <int D, bool ROPE>
-static hipError_t launch_proj_bf16(const FitArgs& a, int mtr, dim3 grid, hipStream_t stream) {
-  switch (mtr) {
-    case 1: hipLaunchKernelGGL((proj_bf16_mfma<D, 1, ROPE>), grid, dim3(kFitThreads), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((proj_bf16_mfma<D, 2, ROPE>), grid, dim3(kFitThreads), 0, stream, a); break;
-    case 3:
-    case 4: hipLaunchKernelGGL((proj_bf16_mfma<D, 4, ROPE>), grid, dim3(kFitThreads), 0, stream, a); break;
-    default: hipLaunchKernelGGL((proj_bf16_mfma<D, 8, ROPE>), grid, dim3(kFitThreads), 0, stream, a); break;
-  }
+template <int D, int MTR, bool ROPE>
+static hipError_t launch_proj_bf16_m(const FitArgs& a, int max_tokens, int num_items, hipStream_t stream) {
+  constexpr int W = ROPE ? kProjRopeWaves : kProjWaves;
+  const int chunk = ROPE ? kProjRopeChunkTokens : kProjChunkTokens;
+  dim3 grid((max_tokens + chunk - 1) / chunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+  const int nblk = (chunk + a.pv.block_size - 1) / a.pv.block_size + 1;
+  const size_t lds = proj_lds_bytes(D, MTR * 16, nblk);
+  hipError_t e = hipFuncSetAttribute((const void*)proj_bf16_mfma<D, MTR, W, ROPE>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((proj_bf16_mfma<D, MTR, W, ROPE>), grid, dim3(W * kWave), lds, stream, a, chunk / (16 * W),
+                     nblk);
   return hipGetLastError();
+}
+
+template <int D, bool ROPE>
+static hipError_t launch_proj_bf16(const FitArgs& a, int mtr, int max_tokens, int num_items, hipStream_t stream) {
+  switch (mtr) {
+    case 1: return launch_proj_bf16_m<D, 1, ROPE>(a, max_tokens, num_items, stream);
+    case 2: return launch_proj_bf16_m<D, 2, ROPE>(a, max_tokens, num_items, stream);
+    case 3:
+    case 4: return launch_proj_bf16_m<D, 4, ROPE>(a, max_tokens, num_items, stream);
+    default: return launch_proj_bf16_m<D, 8, ROPE>(a, max_tokens, num_items, stream);
+  }
 }
 
 template <bool ROPE>
 static hipError_t launch_proj_variants(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens,
                                        int max_rank, hipStream_t stream) {
-  dim3 grid((max_tokens + kProjChunk - 1) / kProjChunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
   const int D = a.pv.head_dim;
   if (dtype == KVC_BF16) {
     const int mtr = (max_rank + 15) / 16;
-    return D == 64 ? launch_proj_bf16<64, ROPE>(a, mtr, grid, stream) : launch_proj_bf16<128, ROPE>(a, mtr, grid, stream);
+    return D == 64 ? launch_proj_bf16<64, ROPE>(a, mtr, max_tokens, num_items, stream)
+                   : launch_proj_bf16<128, ROPE>(a, mtr, max_tokens, num_items, stream);
   }
+  dim3 grid((max_tokens + kProjChunk - 1) / kProjChunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
   const size_t lds = (size_t)max_rank * D * sizeof(float);
   if (D == 64) hipLaunchKernelGGL((proj_f32_valu<64, ROPE>), grid, dim3(kFitThreads), lds, stream, a);
   else hipLaunchKernelGGL((proj_f32_valu<128, ROPE>), grid, dim3(kFitThreads), lds, stream, a);

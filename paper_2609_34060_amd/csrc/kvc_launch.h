@@ -38,7 +38,6 @@ struct FitArgs {
   int32_t max_parts;
   int32_t part_tokens;
 };
-int proj_chunk_tokens();
 hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream);
 hipError_t launch_fit_proj(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens, int max_rank,
                            hipStream_t stream);
