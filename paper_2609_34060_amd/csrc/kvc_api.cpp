@@ -143,6 +143,8 @@ struct FitPlan {
   size_t units = 0, off_partials = 0, off_reflect = 0, off_beta = 0, off_vecs = 0, total = 0;
 };
 
+constexpr int64_t kGramWaveTarget = 2048;  // Gram waves per fit launch
+
 FitPlan plan_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int32_t le) {
   FitPlan p;
   const int32_t nl = le - lb;
@@ -150,13 +152,20 @@ FitPlan plan_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int32_t le)
   p.layers_per_group = std::min<int32_t>(nl, kvc::kMaxLayersPerLaunch);
   p.items_per_group = std::max<int32_t>(1, std::min<int32_t>(b->num_items, 65535 / p.layers_per_group));
   int32_t tmax = 0;
+  int64_t tsum = 0;
   for (int32_t i = 0; i < b->num_items; ++i)
-    if (b->items[i].state.rank > 0) tmax = std::max(tmax, b->items[i].state.num_tokens);
+    if (b->items[i].state.rank > 0) {
+      tmax = std::max(tmax, b->items[i].state.num_tokens);
+      tsum += b->items[i].state.num_tokens;
+    }
   const int64_t d = c->head_dim;
   p.units = static_cast<size_t>(p.items_per_group) * p.layers_per_group * 2 * c->num_kv_heads;
-  // one partial per Gram wave; about 2048 waves per call (two per SIMD of the chip), a multiple of 4 per unit
-  const int64_t want_parts = std::max<int64_t>(1, (2048 + static_cast<int64_t>(p.units) - 1) / p.units);
-  int64_t part = (std::max<int32_t>(tmax, 1) + want_parts - 1) / want_parts;
+  // one partial per Gram wave: the rows a launch group holds (on average over the groups) cut into about
+  // kGramWaveTarget equal ranges, so ragged batches fill the chip as well as uniform ones; a multiple of 4 partials
+  // per unit
+  const int64_t group_rows =
+      tsum * p.items_per_group / b->num_items * p.layers_per_group * 2 * c->num_kv_heads;
+  int64_t part = (std::max<int64_t>(group_rows, 1) + kGramWaveTarget - 1) / kGramWaveTarget;
   part = std::max<int64_t>(256, (part + 31) / 32 * 32);
   p.part_tokens = static_cast<int32_t>(part);
   p.max_parts = static_cast<int32_t>(std::max<int64_t>(1, (tmax + part - 1) / part));
