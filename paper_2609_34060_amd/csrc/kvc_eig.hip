@@ -519,21 +519,43 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
     for (int e = tid; e < r * N; e += kEigThreads) X[e] = (float)gvec[e];
     __syncthreads();
 
-    // modified Gram-Schmidt
+    // modified Gram-Schmidt, one barrier per vector: the wave that takes vector j + 1 in round j (wave 0) also
+    // normalises it, so vector j is normalised when round j starts
+    constexpr int QN = N / kWave;
+    auto normalise = [&](float* x) {
+      double s = 0.0;
+#pragma unroll
+      for (int q = 0; q < QN; ++q) s += (double)x[q] * x[q];
+      s = wave_sum(s);
+      const double f = 1.0 / sqrt(s);
+#pragma unroll
+      for (int q = 0; q < QN; ++q) x[q] = (float)(x[q] * f);
+    };
+    if (wave == 0) {
+      float x[QN];
+#pragma unroll
+      for (int q = 0; q < QN; ++q) x[q] = X[lane + kWave * q];
+      normalise(x);
+#pragma unroll
+      for (int q = 0; q < QN; ++q) X[lane + kWave * q] = x[q];
+    }
+    __syncthreads();
     for (int j = 0; j < r; ++j) {
-      if (wave == 0) {
-        double s = 0.0;
-        for (int i = lane; i < N; i += kWave) s += (double)X[j * N + i] * X[j * N + i];
-        s = wave_sum(s);
-        const double f = 1.0 / sqrt(s);
-        for (int i = lane; i < N; i += kWave) X[j * N + i] = (float)(X[j * N + i] * f);
-      }
-      __syncthreads();
       for (int k = j + 1 + wave; k < r; k += kEigWaves) {
+        float xj[QN], xk[QN];
         double s = 0.0;
-        for (int i = lane; i < N; i += kWave) s += (double)X[j * N + i] * X[k * N + i];
+#pragma unroll
+        for (int q = 0; q < QN; ++q) {
+          xj[q] = X[j * N + lane + kWave * q];
+          xk[q] = X[k * N + lane + kWave * q];
+          s += (double)xj[q] * xk[q];
+        }
         s = wave_sum(s);
-        for (int i = lane; i < N; i += kWave) X[k * N + i] = (float)(X[k * N + i] - s * X[j * N + i]);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) xk[q] = (float)(xk[q] - s * xj[q]);
+        if (k == j + 1) normalise(xk);
+#pragma unroll
+        for (int q = 0; q < QN; ++q) X[k * N + lane + kWave * q] = xk[q];
       }
       __syncthreads();
     }
