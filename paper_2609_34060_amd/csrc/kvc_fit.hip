@@ -582,13 +582,14 @@ __global__ __launch_bounds__(kFitThreads) void gram_f32_valu(FitArgs a) {
 // Projection coef = Z R_r, bf16 caches
 // ---------------------------------------------------------------------------------------------------------------
 
-// Workgroups of kProjWaves waves take kProjChunkTokens tokens of one (item, layer, K/V, head) unit; rotary keys
-// take kProjRopeWaves waves and kProjRopeChunkTokens tokens (every workgroup forms fp64 angle tables, which the
-// longer chunk amortises, and the rotation's registers leave room for fewer waves).  Each wave takes 16-token
+// Workgroups of kProjWaves waves take kProjChunkTokens tokens of one (item, layer, K/V, head) unit (ranks above 32:
+// kProjLongChunkTokens, which amortises staging the larger basis); rotary keys take kProjRopeWaves waves and
+// kProjRopeChunkTokens tokens (every workgroup forms fp64 angle tables, which the longer chunk amortises, and the
+// rotation's registers leave room for fewer waves).  Each wave takes 16-token
 // tiles; the loads of its next tile are issued before this tile's products and coefficient stores (loads and
 // stores leave a wave in order), and row addresses come from the chunk's block-table slices in LDS, so no table
 // read sits between two row loads.
-constexpr int kProjWaves = 8, kProjChunkTokens = 512;
+constexpr int kProjWaves = 8, kProjChunkTokens = 512, kProjLongChunkTokens = 1024;
 constexpr int kProjRopeWaves = 4, kProjRopeChunkTokens = 1024;
 constexpr int kProjChunk = 1024;  // tokens per workgroup of the float32 kernel
 
@@ -862,7 +863,7 @@ hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hip
 template <int D, int MTR, bool ROPE>
 static hipError_t launch_proj_bf16_m(const FitArgs& a, int max_tokens, int num_items, hipStream_t stream) {
   constexpr int W = ROPE ? kProjRopeWaves : kProjWaves;
-  const int chunk = ROPE ? kProjRopeChunkTokens : kProjChunkTokens;
+  const int chunk = ROPE ? kProjRopeChunkTokens : (MTR > 2 ? kProjLongChunkTokens : kProjChunkTokens);
   dim3 grid((max_tokens + chunk - 1) / chunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
   const int nblk = (chunk + a.pv.block_size - 1) / a.pv.block_size + 1;
   const size_t lds = proj_lds_bytes(D, MTR * 16, nblk);
