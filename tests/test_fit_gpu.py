@@ -231,3 +231,15 @@ def test_fit_is_deterministic():
         outs.append(b"".join(t.cpu().numpy().tobytes() for t in (states[0].coef.view(torch.int16),
                                                                   states[0].basis, states[0].sigma)))
     assert outs[0] == outs[1]
+
+
+def test_fit_ragged_batch_partials_sized_by_rows():
+    """A ragged batch whose rows (not its longest item) decide the partial length: sum of rows x 2 layers x 16
+    units above 2048 x 256, so partials are longer than the 256-row minimum and short items span one partial."""
+    lens = (5000, 300, 2500, 64, 4100, 1200, 3300, 900)
+    w = synth.WORKLOADS["serving"].with_(num_layers=2, seq_tokens=lens, num_agents=2, rank=24)
+    assert sum(lens) * 2 * 2 * w.num_kv_heads > 2048 * 256
+    pc = synth.build_paged(w, device="cuda", lead_slots=(0, 3, 11, 7, 1, 5, 2, 9, 4))
+    ranks = [24, 8, 24, 16, 24, 24, 8, 24]
+    states, ostates, raw, *_ = _fit_both(pc, [((q, 0), (q, 1)) for q in range(len(lens))], ranks)
+    _compare_states(states, raw, "bf16")
