@@ -32,8 +32,9 @@ __device__ __forceinline__ FitUnit fit_unit(const FitArgs& a) {
   f.item = blockIdx.z / a.num_layers;
   f.lrel = blockIdx.z - f.item * a.num_layers;
   f.layer = a.layer_begin + f.lrel;
-  f.kv = blockIdx.y / H;
-  f.head = blockIdx.y - f.kv * H;
+  const int y = blockIdx.y;
+  f.kv = a.kv_begin + y / H;
+  f.head = y % H;
   f.unit = unit_index(f.layer, f.kv, f.head, H);
   return f;
 }
@@ -304,8 +305,8 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_ring(FitArgs a) {
   f.item = blockIdx.z / a.num_layers;
   f.lrel = blockIdx.z - f.item * a.num_layers;
   f.layer = a.layer_begin + f.lrel;
-  f.kv = blockIdx.y / HG;
-  f.head = (blockIdx.y - f.kv * HG) * kFitWaves + wave;
+  f.kv = a.kv_begin + (int)blockIdx.y / HG;
+  f.head = ((int)blockIdx.y % HG) * kFitWaves + wave;
   if (f.head >= H) return;
   f.unit = unit_index(f.layer, f.kv, f.head, H);
   const kvc_item* itp = a.items + f.item;
@@ -826,15 +827,19 @@ __global__ __launch_bounds__(kFitThreads) void proj_f32_valu(FitArgs a) {
 // ---------------------------------------------------------------------------------------------------------------
 
 
+// Gram launches of K/V sides kv_begin .. kv_begin + nkv - 1.
 template <bool ROPE>
-static hipError_t launch_gram_variants(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream) {
+static hipError_t launch_gram_variants(const FitArgs& a0, kvc_dtype dtype, int num_items, int kv_begin, int nkv,
+                                       hipStream_t stream) {
+  FitArgs a = a0;
+  a.kv_begin = kv_begin;
   const int D = a.pv.head_dim;
   if (dtype == KVC_BF16) {
-    dim3 grid((a.max_parts + kFitWaves - 1) / kFitWaves, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+    dim3 grid((a.max_parts + kFitWaves - 1) / kFitWaves, nkv * a.pv.num_kv_heads, num_items * a.num_layers);
     if (!ROPE && D == 128 && a.pv.block_shift >= 4 && a.part_tokens / a.pv.block_size + 3 <= kGramTabMax) {
       // LDS-staged rows (block sizes of at least 16 tokens, a partial's table fits the wave's LDS copy)
       const bool delta = a.mode == KVC_FIT_DELTA;
-      grid = dim3(a.max_parts, 2 * ((a.pv.num_kv_heads + kFitWaves - 1) / kFitWaves), num_items * a.num_layers);
+      grid = dim3(a.max_parts, nkv * ((a.pv.num_kv_heads + kFitWaves - 1) / kFitWaves), num_items * a.num_layers);
       const void* fn = delta ? (const void*)gram_bf16_ring<true> : (const void*)gram_bf16_ring<false>;
       hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGramLdsBytes);
       if (e != hipSuccess) return e;
@@ -846,25 +851,26 @@ static hipError_t launch_gram_variants(const FitArgs& a, kvc_dtype dtype, int nu
       hipLaunchKernelGGL((gram_bf16_mfma<128, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
     }
   } else {
-    dim3 grid(a.max_parts, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+    dim3 grid(a.max_parts, nkv * a.pv.num_kv_heads, num_items * a.num_layers);
     if (D == 64) hipLaunchKernelGGL((gram_f32_valu<64, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
     else hipLaunchKernelGGL((gram_f32_valu<128, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
   }
   return hipGetLastError();
 }
 
-// A rotary cache takes the register-pipelined Gram (the rotation needs each feature's partner, which that layout
-// reaches with one row rotation).
+// The keys of a rotary cache take the register-pipelined Gram (the rotation needs each feature's partner, which that
+// layout reaches with one row rotation); its values, which carry no rotation, take the plain kernels.
 hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream) {
-  return a.pv.rope.style != KVC_ROPE_NONE ? launch_gram_variants<true>(a, dtype, num_items, stream)
-                                          : launch_gram_variants<false>(a, dtype, num_items, stream);
+  if (a.pv.rope.style == KVC_ROPE_NONE) return launch_gram_variants<false>(a, dtype, num_items, 0, 2, stream);
+  const hipError_t e = launch_gram_variants<true>(a, dtype, num_items, 0, 1, stream);
+  return e != hipSuccess ? e : launch_gram_variants<false>(a, dtype, num_items, 1, 1, stream);
 }
 
 template <int D, int MTR, bool ROPE>
-static hipError_t launch_proj_bf16_m(const FitArgs& a, int max_tokens, int num_items, hipStream_t stream) {
+static hipError_t launch_proj_bf16_m(const FitArgs& a, int nkv, int max_tokens, int num_items, hipStream_t stream) {
   constexpr int W = ROPE ? kProjRopeWaves : kProjWaves;
   const int chunk = ROPE ? kProjRopeChunkTokens : (MTR > 2 ? kProjLongChunkTokens : kProjChunkTokens);
-  dim3 grid((max_tokens + chunk - 1) / chunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+  dim3 grid((max_tokens + chunk - 1) / chunk, nkv * a.pv.num_kv_heads, num_items * a.num_layers);
   const int nblk = (chunk + a.pv.block_size - 1) / a.pv.block_size + 1;
   const size_t lds = proj_lds_bytes(D, MTR * 16, nblk);
   hipError_t e = hipFuncSetAttribute((const void*)proj_bf16_mfma<D, MTR, W, ROPE>,
@@ -876,26 +882,30 @@ static hipError_t launch_proj_bf16_m(const FitArgs& a, int max_tokens, int num_i
 }
 
 template <int D, bool ROPE>
-static hipError_t launch_proj_bf16(const FitArgs& a, int mtr, int max_tokens, int num_items, hipStream_t stream) {
+static hipError_t launch_proj_bf16(const FitArgs& a, int mtr, int nkv, int max_tokens, int num_items,
+                                   hipStream_t stream) {
   switch (mtr) {
-    case 1: return launch_proj_bf16_m<D, 1, ROPE>(a, max_tokens, num_items, stream);
-    case 2: return launch_proj_bf16_m<D, 2, ROPE>(a, max_tokens, num_items, stream);
+    case 1: return launch_proj_bf16_m<D, 1, ROPE>(a, nkv, max_tokens, num_items, stream);
+    case 2: return launch_proj_bf16_m<D, 2, ROPE>(a, nkv, max_tokens, num_items, stream);
     case 3:
-    case 4: return launch_proj_bf16_m<D, 4, ROPE>(a, max_tokens, num_items, stream);
-    default: return launch_proj_bf16_m<D, 8, ROPE>(a, max_tokens, num_items, stream);
+    case 4: return launch_proj_bf16_m<D, 4, ROPE>(a, nkv, max_tokens, num_items, stream);
+    default: return launch_proj_bf16_m<D, 8, ROPE>(a, nkv, max_tokens, num_items, stream);
   }
 }
 
+// Projection launches of K/V sides kv_begin .. kv_begin + nkv - 1.
 template <bool ROPE>
-static hipError_t launch_proj_variants(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens,
-                                       int max_rank, hipStream_t stream) {
+static hipError_t launch_proj_variants(const FitArgs& a0, kvc_dtype dtype, int num_items, int max_tokens,
+                                       int max_rank, int kv_begin, int nkv, hipStream_t stream) {
+  FitArgs a = a0;
+  a.kv_begin = kv_begin;
   const int D = a.pv.head_dim;
   if (dtype == KVC_BF16) {
     const int mtr = (max_rank + 15) / 16;
-    return D == 64 ? launch_proj_bf16<64, ROPE>(a, mtr, max_tokens, num_items, stream)
-                   : launch_proj_bf16<128, ROPE>(a, mtr, max_tokens, num_items, stream);
+    return D == 64 ? launch_proj_bf16<64, ROPE>(a, mtr, nkv, max_tokens, num_items, stream)
+                   : launch_proj_bf16<128, ROPE>(a, mtr, nkv, max_tokens, num_items, stream);
   }
-  dim3 grid((max_tokens + kProjChunk - 1) / kProjChunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+  dim3 grid((max_tokens + kProjChunk - 1) / kProjChunk, nkv * a.pv.num_kv_heads, num_items * a.num_layers);
   const size_t lds = (size_t)max_rank * D * sizeof(float);
   if (D == 64) hipLaunchKernelGGL((proj_f32_valu<64, ROPE>), grid, dim3(kFitThreads), lds, stream, a);
   else hipLaunchKernelGGL((proj_f32_valu<128, ROPE>), grid, dim3(kFitThreads), lds, stream, a);
@@ -905,9 +915,11 @@ static hipError_t launch_proj_variants(const FitArgs& a, kvc_dtype dtype, int nu
 hipError_t launch_fit_proj(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens, int max_rank,
                            hipStream_t stream) {
   if (max_rank == 0 || max_tokens == 0) return hipSuccess;
-  return a.pv.rope.style != KVC_ROPE_NONE
-             ? launch_proj_variants<true>(a, dtype, num_items, max_tokens, max_rank, stream)
-             : launch_proj_variants<false>(a, dtype, num_items, max_tokens, max_rank, stream);
+  // a rotary cache's values carry no rotation: they take the plain kernels
+  if (a.pv.rope.style == KVC_ROPE_NONE)
+    return launch_proj_variants<false>(a, dtype, num_items, max_tokens, max_rank, 0, 2, stream);
+  const hipError_t e = launch_proj_variants<true>(a, dtype, num_items, max_tokens, max_rank, 0, 1, stream);
+  return e != hipSuccess ? e : launch_proj_variants<false>(a, dtype, num_items, max_tokens, max_rank, 1, 1, stream);
 }
 
 }  // namespace kvc

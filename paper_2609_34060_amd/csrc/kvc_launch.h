@@ -37,6 +37,7 @@ struct FitArgs {
   float* partials;             // workspace [unit][max_parts][d][d]
   int32_t max_parts;
   int32_t part_tokens;
+  int32_t kv_begin;            // the launch covers K/V sides kv_begin .. (grid y: one or both sides' heads)
 };
 hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hipStream_t stream);
 hipError_t launch_fit_proj(const FitArgs& a, kvc_dtype dtype, int num_items, int max_tokens, int max_rank,
