@@ -56,8 +56,8 @@ __global__ __launch_bounds__(W * kWave) void apply_bf16_mfma(ApplyArgs a, int tp
   const int lrel = blockIdx.z - item_id * nl;
   const int layer = a.layer_begin + lrel;
   const int H = a.pv.num_kv_heads;
-  const int kv = blockIdx.y / H;
-  const int head = blockIdx.y - kv * H;
+  const int kv = a.kv_begin + (int)blockIdx.y / H;
+  const int head = (int)blockIdx.y % H;
 
   const kvc_item* itp = a.items + item_id;
   const int T = itp->num_tokens;
@@ -273,8 +273,8 @@ __global__ __launch_bounds__(kApplyThreads) void apply_f32_valu(ApplyArgs a) {
   const int lrel = blockIdx.z - item_id * nl;
   const int layer = a.layer_begin + lrel;
   const int H = a.pv.num_kv_heads;
-  const int kv = blockIdx.y / H;
-  const int head = blockIdx.y - kv * H;
+  const int kv = a.kv_begin + (int)blockIdx.y / H;
+  const int head = (int)blockIdx.y % H;
 
   const kvc_item* itp = a.items + item_id;
   const int T = itp->num_tokens;
@@ -366,17 +366,28 @@ static hipError_t launch_bf16_w(const ApplyArgs& a, dim3 grid, int tpw, int nblk
 // Waves per workgroup for a rank of KS 32-rank chunks.
 constexpr int apply_waves(int ks) { return ks == 1 ? 8 : 4; }
 
+// Keys of a rotary cache: every workgroup forms fp64 angle tables and stages a rotated basis, which a 1024-token chunk
+// (4 waves of 16 tiles) amortises; values (and every unit of a plain cache) take 256-token chunks.
 template <int D, int KS>
-static hipError_t launch_bf16(const ApplyArgs& a, int max_tokens, int num_items, hipStream_t stream) {
-  // rotary keys: every workgroup forms fp64 angle tables and stages a rotated basis, which a 1024-token chunk
-  // (4 waves of 16 tiles) amortises; otherwise 256-token chunks
-  const bool rope = a.pv.rope.style != KVC_ROPE_NONE;
-  const int chunk = rope ? kApplyRopeChunkTokens : kApplyChunkTokens;
-  dim3 grid((max_tokens + chunk - 1) / chunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
-  const int nblk = (chunk + a.pv.block_size - 1) / a.pv.block_size + 1;
-  if (rope) return launch_bf16_w<D, KS, 4, true>(a, grid, chunk / 64, nblk, stream);
+static hipError_t launch_bf16(const ApplyArgs& a0, int max_tokens, int num_items, hipStream_t stream) {
+  ApplyArgs a = a0;
+  const int H = a.pv.num_kv_heads;
+  int nkv = 2;
+  if (a.pv.rope.style != KVC_ROPE_NONE) {
+    const int chunk = kApplyRopeChunkTokens;
+    a.kv_begin = 0;
+    const dim3 grid((max_tokens + chunk - 1) / chunk, H, num_items * a.num_layers);
+    const hipError_t e = launch_bf16_w<D, KS, 4, true>(a, grid, chunk / 64,
+                                                       (chunk + a.pv.block_size - 1) / a.pv.block_size + 1, stream);
+    if (e != hipSuccess) return e;
+    a.kv_begin = 1;
+    nkv = 1;
+  }
+  const int chunk = kApplyChunkTokens;
   constexpr int W = apply_waves(KS);
-  return launch_bf16_w<D, KS, W, false>(a, grid, chunk / (16 * W), nblk, stream);
+  const dim3 grid((max_tokens + chunk - 1) / chunk, nkv * H, num_items * a.num_layers);
+  return launch_bf16_w<D, KS, W, false>(a, grid, chunk / (16 * W), (chunk + a.pv.block_size - 1) / a.pv.block_size + 1,
+                                        stream);
 }
 
 template <int D>

@@ -17,6 +17,7 @@ struct ApplyArgs {
   int32_t max_blocks;
   int32_t layer_begin;
   int32_t num_layers;
+  int32_t kv_begin;            // the launch covers K/V sides kv_begin .. (grid y: one or both sides' heads)
 };
 
 int apply_chunk_tokens();
