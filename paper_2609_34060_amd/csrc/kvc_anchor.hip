@@ -558,9 +558,12 @@ __global__ __launch_bounds__(kAnchorThreads) void apply_anchored_f32(AnchorArgs 
 
 constexpr int kResWaves = 8;
 constexpr int kResThreads = kResWaves * kWave;
-constexpr int kResTiles = 8;                            // 16-token tiles per wave
-constexpr int kResChunk = kResWaves * kResTiles * 16;  // 1024 tokens per workgroup
-int anchor_resident_chunk_tokens() { return kResChunk; }
+// 16-token tiles per wave: 16 for the anchored apply and the gate (2048 tokens per workgroup), 8 for the weights,
+// whose per-tile distances stay in registers (1024 tokens)
+constexpr int kResTiles = 16, kResDistTiles = 8;
+constexpr int kResChunk = kResWaves * kResTiles * 16;
+constexpr int kResDistChunk = kResWaves * kResDistTiles * 16;
+int anchor_resident_chunk_tokens() { return kResDistChunk; }  // the shorter chunk (more partials)
 constexpr size_t kResMaxLds = 160 * 1024;
 
 // LDS holds hi [D][32 NC] then lo; the 16-byte granule (8 ranks) q of feature row f sits at q ^ res_swz(f), a
@@ -796,7 +799,8 @@ __global__ __launch_bounds__(kResThreads) void apply_anchored_res_bf16(AnchorArg
 // ROPE (weights): keys of a rotary cache are compared in canonical coordinates, R(-ps) C_src (the bases are canonical).
 template <int D, bool GATE, bool ROPE>
 __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a) {
-  constexpr int MT = D / 16, NQ = D / 32, NCM = kResMaxChunks, TPW = kResTiles;
+  constexpr int MT = D / 16, NQ = D / 32, NCM = kResMaxChunks, TPW = GATE ? kResTiles : kResDistTiles;
+  constexpr int CH = kResWaves * TPW * 16;  // tokens per workgroup
   static_assert(KVC_MAX_ANCHORS <= 16, "four anchors per lane group");
   extern __shared__ __attribute__((aligned(16))) unsigned char anchor_lds[];
   const int NC = a.num_chunks, kpt = 32 * NC;
@@ -810,7 +814,7 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
   // weights need every head of a token in one workgroup (the mean runs over the whole layer row)
   const int h_lo = GATE ? (int)blockIdx.y : 0, h_hi = GATE ? h_lo + 1 : H;
   const int Tl = a.num_weighted;
-  const int t_begin = blockIdx.x * kResChunk;
+  const int t_begin = blockIdx.x * CH;
   if (t_begin >= Tl) return;  // whole workgroup
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave, g = lane >> 4, n = lane & 15;
   const uint16_t* pool = static_cast<const uint16_t*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
@@ -824,7 +828,7 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
   const int style = a.pv.rope.style;
   float tc = 1.0f, ts = 0.0f;  // this lane's entry of the wave's angle table for -ps
   if (rot) rope_wave_table<D>(a.pv.rope, -(double)a.src_position, lane, tc, ts);
-  const LaneTable lts = lane_table(a.pv, a.src_table, a.src_offset, t_begin, min(Tl, t_begin + kResChunk), lane);
+  const LaneTable lts = lane_table(a.pv, a.src_table, a.src_offset, t_begin, min(Tl, t_begin + CH), lane);
 
   struct Tile {
     u32x4 raw[NQ];
@@ -948,7 +952,7 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
     }
     __syncthreads();
     const float inv_feat = 1.0f / (float)(H * D);
-    for (int tok = threadIdx.x; tok < kResChunk; tok += kResThreads) {
+    for (int tok = threadIdx.x; tok < CH; tok += kResThreads) {
       const int t = t_begin + tok;
       if (t >= Tl) break;
       float dmin = INFINITY;
@@ -1011,7 +1015,7 @@ static bool plan_resident(AnchorArgs& a) {
 // which: 0 weights, 1 apply, 2 gate
 static size_t res_lds_bytes(const AnchorArgs& a, int which) {
   const size_t basis = (size_t)a.pv.head_dim * 32 * a.num_chunks * 2 * sizeof(uint16_t);
-  const size_t sums = which == 0   ? (size_t)kResChunk * a.num_anchors * sizeof(float)
+  const size_t sums = which == 0   ? (size_t)kResDistChunk * a.num_anchors * sizeof(float)
                       : which == 2 ? (size_t)kResWaves * a.num_anchors * sizeof(float)
                                    : 0;
   return std::max(basis, sums);
@@ -1044,7 +1048,7 @@ static hipError_t launch_weights_variant(const AnchorArgs& a, kvc_dtype dtype, h
   if (dtype == KVC_BF16) {
     AnchorArgs r = a;
     if (plan_resident(r)) {
-      dim3 grid((a.num_weighted + kResChunk - 1) / kResChunk, 2, a.num_layers);
+      dim3 grid((a.num_weighted + kResDistChunk - 1) / kResDistChunk, 2, a.num_layers);
       const size_t rl = res_lds_bytes(r, 0);
       return D == 64 ? launch_with_lds(anchor_dist_res_bf16<64, false, ROPE>, grid, rl, r, stream, kResThreads)
                      : launch_with_lds(anchor_dist_res_bf16<128, false, ROPE>, grid, rl, r, stream, kResThreads);
@@ -1073,7 +1077,7 @@ hipError_t launch_gate_distances(const AnchorArgs& args, kvc_dtype dtype, hipStr
   hipError_t e;
   dim3 grid(a.gate_chunks, 1, a.num_layers);
   if (dtype == KVC_BF16 && plan_resident(a)) {
-    // one partial per (layer, 1024-token chunk, KV head): the workspace query sizes for this count as well
+    // one partial per (layer, 2048-token chunk, KV head): within what the workspace query sizes (1024-token chunks)
     grid.x = (a.num_weighted + kResChunk - 1) / kResChunk;
     grid.y = a.pv.num_kv_heads;
     a.gate_chunks = (int)(grid.x * grid.y);

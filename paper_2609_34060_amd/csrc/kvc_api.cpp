@@ -824,7 +824,7 @@ size_t kvc_gate_workspace_bytes(const kvc_cache* cache, const kvc_anchors* ancho
   if (anchors->num_anchors < 1 || anchors->num_anchors > KVC_MAX_ANCHORS) return 0;
   const int chunk = cache->dtype == KVC_BF16 ? kvc::anchor_chunk_tokens() : 64;
   size_t chunks = static_cast<size_t>((prefix + chunk - 1) / chunk);
-  if (cache->dtype == KVC_BF16) {  // bf16 kernels keep one partial per chunk and KV head (512 or 1024-token chunks)
+  if (cache->dtype == KVC_BF16) {  // bf16 kernels keep one partial per chunk and KV head (512 tokens and up)
     const int res = kvc::anchor_resident_chunk_tokens();
     chunks = std::max(chunks, static_cast<size_t>((prefix + res - 1) / res)) * static_cast<size_t>(cache->num_kv_heads);
   }
