@@ -374,17 +374,45 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   double* gvec = a.vecs + (size_t)u * N * KVC_MAX_RANK;  // eigenvectors of T, vector j in row j
 
   // ---- 1. load G ------------------------------------------------------------------------------------------
+  // Each thread takes Q groups of 4 consecutive entries; every load of a partial (or of the dense matrix) is issued
+  // before its values are added, and the partials are added in order c = 0, 1, ... in fp64.
+  static_assert(LD == N && (N * N) % (4 * kEigThreads) == 0, "whole float4 groups per thread");
+  constexpr int Q = N * N / (4 * kEigThreads);
   if (a.partials) {
     const int parts = (tg.tokens + a.part_tokens - 1) / a.part_tokens;
-    const float* P = a.partials + (size_t)u * a.max_parts * N * N;
-    for (int e = tid; e < N * N; e += kEigThreads) {
-      double s = 0.0;
-      for (int c = 0; c < parts; ++c) s += (double)P[(size_t)c * N * N + e];
-      A[(e / N) * LD + (e % N)] = (float)s;
+    const float4* P4 = reinterpret_cast<const float4*>(a.partials + (size_t)u * a.max_parts * N * N);
+    double acc[Q][4];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) acc[q][0] = acc[q][1] = acc[q][2] = acc[q][3] = 0.0;
+#pragma unroll 2
+    for (int c = 0; c < parts; ++c) {
+      float4 v[Q];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) v[q] = P4[(size_t)c * (N * N / 4) + tid + q * kEigThreads];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        acc[q][0] += (double)v[q].x;
+        acc[q][1] += (double)v[q].y;
+        acc[q][2] += (double)v[q].z;
+        acc[q][3] += (double)v[q].w;
+      }
     }
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+      reinterpret_cast<float4*>(A)[tid + q * kEigThreads] =
+          make_float4((float)acc[q][0], (float)acc[q][1], (float)acc[q][2], (float)acc[q][3]);
   } else {
-    const double* Dm = a.dense + (size_t)u * N * N;
-    for (int e = tid; e < N * N; e += kEigThreads) A[(e / N) * LD + (e % N)] = (float)Dm[e];
+    const double2* D2 = reinterpret_cast<const double2*>(a.dense + (size_t)u * N * N);
+    double2 v[2 * Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      v[2 * q] = D2[2 * (tid + q * kEigThreads)];
+      v[2 * q + 1] = D2[2 * (tid + q * kEigThreads) + 1];
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+      reinterpret_cast<float4*>(A)[tid + q * kEigThreads] =
+          make_float4((float)v[2 * q].x, (float)v[2 * q].y, (float)v[2 * q + 1].x, (float)v[2 * q + 1].y);
   }
   __syncthreads();
 
