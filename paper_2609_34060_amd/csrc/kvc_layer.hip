@@ -6,7 +6,8 @@
 //                Block sizes below 8 or not a power of two: gram_pair, the d x d block Z_h1^T Z_h2 of a head pair with
 //                its mirror, rows read straight into registers.  float32 caches: 64 x 64 blocks on VALU.
 //   gram_reduce  the partials of a unit summed in a fixed order in fp64.
-//   subspace     k = 64 or 128 columns: X <- orth(G X) (fp64 GEMM, Cholesky QR twice), then the
+//   subspace     k = 64 or 128 columns: X <- orth(G X) (fp64 GEMM, shifted Cholesky QR; a second, exact pass
+//                before each Rayleigh-Ritz step), then the
 //                Rayleigh-Ritz matrix X^T G X goes to the per-head eigensolver as a dense k x k input; its top r
 //                eigenvectors V give the basis rows (X V^T)^T and sigma = sqrt(Ritz value).  The top-r subspace
 //                converges like (lambda_{k+1} / lambda_r)^iterations.
@@ -623,7 +624,7 @@ __global__ __launch_bounds__(kLayerThreads) void gram_reduce(LayerFitArgs a, int
 }
 
 // ---------------------------------------------------------------------------------------------------------------
-// Subspace iteration on G (fp64)
+// Subspace iteration on G (fp64 arithmetic)
 // ---------------------------------------------------------------------------------------------------------------
 
 __device__ __forceinline__ double hash_uniform(uint32_t a, uint32_t b, uint32_t c) {
@@ -652,9 +653,14 @@ __global__ __launch_bounds__(kLayerThreads) void sub_init(LayerFitArgs a) {
 // Y = G X for every unit: a 128 x 64 tile (features x columns) per workgroup; thread (ti, tj) owns features
 // 8 ti .. 8 ti + 7 and columns tj + 16 j.  The next 32-wide slices of G and X are loaded into registers while the
 // current ones are used.
-constexpr int kGemmRows = 128;
-__global__ __launch_bounds__(kLayerThreads) void sub_gemm(LayerFitArgs a) {
-  constexpr int TR = kGemmRows, TC = 64, KB = 32, NG = TR * KB / kLayerThreads, NX = TC * KB / kLayerThreads;
+// Y = G X (fp64): a kGemmRows x 64 tile of Y per workgroup of 128 threads; thread (ti, tj) accumulates the
+// entries of rows ti + 16 i and columns tj + 8 j (each LDS read of X feeds kGemmRows / 16 fmas, each read of G
+// eight; interleaved rows and columns keep the reads of a wave on distinct banks).  The next k-step's tiles are loaded into registers while this one
+// is multiplied.
+constexpr int kGemmRows = 64, kGemmCols = 64, kGemmK = 16, kGemmThreads = 128;
+__global__ __launch_bounds__(kGemmThreads) void sub_gemm(LayerFitArgs a) {
+  constexpr int TR = kGemmRows, TC = kGemmCols, KB = kGemmK, RB = TR / 16;
+  constexpr int NG = TR * KB / kGemmThreads, NX = TC * KB / kGemmThreads;
   __shared__ double s_g[TR][KB + 1], s_x[KB][TC + 1];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
   const int f0 = blockIdx.x * TR, c0 = blockIdx.y * TC, u = blockIdx.z;
@@ -662,54 +668,58 @@ __global__ __launch_bounds__(kLayerThreads) void sub_gemm(LayerFitArgs a) {
   const double* G = a.gram + (size_t)u * DL * DL;
   const double* X = a.x + (size_t)u * a.k * DL;
   double* Y = a.y + (size_t)u * a.k * DL;
-  const int tid = threadIdx.x, ti = tid / 16, tj = tid % 16;
+  const int tid = threadIdx.x, ti = tid / 8, tj = tid % 8;
   double pg[NG], px[NX];
   auto load = [&](int k0) {
 #pragma unroll
     for (int q = 0; q < NG; ++q) {
-      const int e = tid + q * kLayerThreads, i = e / KB, kk = e - i * KB;
+      const int e = tid + q * kGemmThreads, i = e / KB, kk = e - i * KB;
       pg[q] = f0 + i < DL ? G[(size_t)(f0 + i) * DL + k0 + kk] : 0.0;
     }
 #pragma unroll
     for (int q = 0; q < NX; ++q) {
-      const int e = tid + q * kLayerThreads, i = e / KB, kk = e - i * KB;
+      const int e = tid + q * kGemmThreads, i = e / KB, kk = e - i * KB;
       px[q] = X[(size_t)(c0 + i) * DL + k0 + kk];
     }
   };
-  double acc[8][4] = {};
+  double acc[RB][8];
+#pragma unroll
+  for (int i = 0; i < RB; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = 0.0;
   load(0);
   for (int k0 = 0; k0 < DL; k0 += KB) {
 #pragma unroll
     for (int q = 0; q < NG; ++q) {
-      const int e = tid + q * kLayerThreads, i = e / KB, kk = e - i * KB;
+      const int e = tid + q * kGemmThreads, i = e / KB, kk = e - i * KB;
       s_g[i][kk] = pg[q];
     }
 #pragma unroll
     for (int q = 0; q < NX; ++q) {
-      const int e = tid + q * kLayerThreads, i = e / KB, kk = e - i * KB;
+      const int e = tid + q * kGemmThreads, i = e / KB, kk = e - i * KB;
       s_x[kk][i] = px[q];
     }
     __syncthreads();
     if (k0 + KB < DL) load(k0 + KB);
-#pragma unroll 4
+#pragma unroll 2
     for (int kk = 0; kk < KB; ++kk) {
-      double g8[8], x4[4];
+      double g8[RB], x8[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) g8[i] = s_g[8 * ti + i][kk];
+      for (int i = 0; i < RB; ++i) g8[i] = s_g[ti + 16 * i][kk];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) x4[j] = s_x[kk][tj + 16 * j];
+      for (int j = 0; j < 8; ++j) x8[j] = s_x[kk][tj + 8 * j];
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
+      for (int i = 0; i < RB; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fma(g8[i], x4[j], acc[i][j]);
+        for (int j = 0; j < 8; ++j) acc[i][j] = fma(g8[i], x8[j], acc[i][j]);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int j = 0; j < 8; ++j)
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if (f0 + 8 * ti + i < DL) Y[(size_t)(c0 + tj + 16 * j) * DL + f0 + 8 * ti + i] = acc[i][j];
+    for (int i = 0; i < RB; ++i)
+      if (f0 + ti + 16 * i < DL) Y[(size_t)(c0 + tj + 8 * j) * DL + f0 + ti + 16 * i] = acc[i][j];
 }
 
 // Whole-workgroup sum (fixed order: waves in order), result in every thread.
@@ -1488,25 +1498,27 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
       hipLaunchKernelGGL(cqr_apply<128>, agrid, dim3(kCqrThreads), alds, stream, a, src, dst, first, round);
     }
   };
-  // X = orth(Y): the perturbed, shifted pass from Y into X, then the exact pass on X in place
-  auto orth = [&](uint32_t round) {
+  // X = orth(Y): the perturbed, shifted pass from Y into X, then (`exact`) the exact pass on X in place.  Between two
+  // Rayleigh-Ritz steps X only has to keep full rank (the iteration depends on span(X) alone), so the exact pass runs
+  // before each Rayleigh-Ritz step only.
+  auto orth = [&](uint32_t round, bool exact) {
     hipLaunchKernelGGL(cqr_scale, dim3(a.num_units), dim3(kScaleThreads), 0, stream, a);
     pass(a.y, a.x, 1, round);
-    pass(a.x, a.x, 0, round);
+    if (exact) pass(a.x, a.x, 0, round);
   };
-  orth(0u);
-  const dim3 ggrid((DL + kGemmRows - 1) / kGemmRows, a.k / 64, a.num_units);
+  orth(0u, true);
+  const dim3 ggrid((DL + kGemmRows - 1) / kGemmRows, a.k / kGemmCols, a.num_units);
   EigArgs es = ea;
   es.skip = a.conv;  // units that have stopped keep the Ritz pairs of their last check
   int done = 0;
   while (done < kLayerMaxIters) {
     const int n = done == 0 ? kLayerFirstIters : kLayerCheckEvery;
     for (int it = 0; it < n; ++it) {
-      hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
-      orth((uint32_t)(++done));
+      hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kGemmThreads), 0, stream, a);
+      orth((uint32_t)(++done), it + 1 == n);
     }
     // Rayleigh-Ritz on span(X) and the residuals of its top-r pairs (Y = G X is kept by the Ritz step)
-    hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kLayerThreads), 0, stream, a);
+    hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kGemmThreads), 0, stream, a);
     if (a.k == 64) hipLaunchKernelGGL(sub_rayleigh<64>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
     else hipLaunchKernelGGL(sub_rayleigh<128>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
     hipError_t e = hipGetLastError();
