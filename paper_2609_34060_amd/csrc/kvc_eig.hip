@@ -4,7 +4,7 @@
 //   2. Householder tridiagonalisation G = Q T Q^T in fp64 arithmetic; the trailing matrix is kept in LDS in fp32
 //      (the Gram itself carries fp32 accuracy), which lets two units share a CU; the reflectors go to the workspace.
 //   3. Multisection bisection with Sturm counts for the r largest eigenvalues of T (groups of lanes per
-//      eigenvalue, one ballot per step).
+//      eigenvalue, kBisShifts shifts per lane, one ballot per shift).
 //   4. Inverse iteration on T (LDL^T without pivoting, tiny pivots replaced) from pseudo-random starts, one lane
 //      per eigenvector; then modified Gram-Schmidt over the r vectors.  Vectors of tightly clustered eigenvalues
 //      come out as an orthonormal basis of the cluster's invariant subspace (where the SVD itself is not unique).
