@@ -23,6 +23,10 @@ constexpr int kEigWaves = kEigThreads / kWave;
 constexpr int kReflChunk = 16;  // reflectors staged in LDS per back-transformation chunk
 constexpr int kInvBatch = 32;   // eigenvectors per inverse-iteration batch (one lane each)
 constexpr int kBisShifts = 2;   // Sturm counts per lane and bisection step
+// Inverse-iteration solves per eigenvector: with lambda within 2^-32 of the spectrum's width, each solve shrinks the
+// other eigenvectors' components by that error over their gap, so two solves leave a residual at the rounding level
+// (a third does not lower it).
+constexpr int kInvSolves = 2;
 
 // fp64 cross-lane moves by DPP (two 32-bit halves); lanes whose row is masked off receive 0.
 template <int CTRL, int ROW_MASK = 0xF>
@@ -510,9 +514,9 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
           const uint32_t h = hash3(a.seed ^ (uint32_t)u, (uint32_t)j, (uint32_t)i);
           xv[i * kInvBatch + tid] = (double)(h >> 11) * (1.0 / 2097152.0) - 1.0;
         }
-        // three solves (T - lam I) x_new = x; each right-hand side is scaled by 1 / max|x| on the way in
+        // kInvSolves solves (T - lam I) x_new = x; each right-hand side is scaled by 1 / max|x| on the way in
         double sc = 1.0;
-        for (int itr = 0; itr < 3; ++itr) {
+        for (int itr = 0; itr < kInvSolves; ++itr) {
           double z = xv[tid] * sc;
           xv[tid] = z;
 #pragma unroll 4
