@@ -174,7 +174,8 @@ __device__ __forceinline__ void sturm_counts(const double* sa, const double* sb2
 // Step k reflects x = row k beyond the diagonal (the matrix is symmetric) onto alpha e_1 with H_k = I - beta v v^T,
 // v = x - alpha e_1; with p = A22 v, K = (beta^2 / 2) v^T p and w = beta p - K v, A22 <- A22 - v w^T - w v^T.
 // The matrix lives in LDS as fp32 [N][N]; the rank-2 update is two fp32 fmas per entry (v and w rounded to fp32),
-// everything else (p, K, w, the scalars, the reflectors) is fp64.
+// each wave's share of A22 v is an fp32 sum over its rows, and the rest (the shares' total p, K, w, the scalars,
+// the reflectors) is fp64.
 //
 // kTriWaves waves (one per SIMD) run the reduction with one workgroup barrier per step.  Lane l of every wave owns
 // the CPL = N / 64 consecutive columns CPL l ..; row R belongs to wave R mod kTriWaves.  The update of step k - 1 is
