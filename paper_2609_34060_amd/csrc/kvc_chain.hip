@@ -425,7 +425,9 @@ size_t chain_ymat_lds_bytes(int m, int ro, int d) { return (size_t)(m + ro) * (d
 // step).  Y^T is staged in LDS as a bf16 hi/lo pair; the coefficient rows are the B operand.
 // ---------------------------------------------------------------------------------------------------------------
 
-constexpr int kCprojTilesPerWave = 8;
+// 2048 tokens per workgroup: Y^T is staged once per 2048 tokens (0.652 ms at 8B/32K against 0.715 ms with 512 and
+// 0.663 ms with 1024)
+constexpr int kCprojTilesPerWave = 32;
 constexpr int kCprojChunk = kChainWaves * kCprojTilesPerWave * 16;
 
 // VEC (bf16, r1 and r2 multiples of 8, r_out a multiple of 4): 16-byte coefficient loads and 8-byte stores.
