@@ -54,6 +54,9 @@ def _setup(name, layers, num_tokens=None, **over):
     ("llama8b_4k", 1, [64, 48, 64, 40, 64, 56], 2050, {}),
     ("llama8b_4k", 1, [32, 16, 40], 900, {"head_dim": 64, "seq_tokens": (1000,)}),
     ("llama8b_4k", 1, [64, 48, 64, 40, 64, 56], 700, {"head_dim": 64, "num_kv_heads": 3, "seq_tokens": (800,)}),
+    # block size 8: a 2048-token workgroup of the resident kernels spans 256 blocks, more than its register-held
+    # table slice (128), so it reads its block ids from the table in memory
+    ("llama8b_4k", 1, [32, 32, 16], 3000, {"block_size": 8, "seq_tokens": (3100,)}),
 ])
 def test_anchor_weights_and_anchored_apply(name, layers, ranks, Ts, over):
     w, pc, cache, T, src, dst, tab = _setup(name, layers, num_tokens=None, **over)
@@ -130,7 +133,9 @@ def test_anchored_apply_with_one_anchor_matches_kvc_apply():
                                                            ("llama8b_4k", 3, 4096, [32] * 3, {}),
                                                            ("llama8b_4k", 1, 1500, [96, 96, 64, 96], {}),
                                                            ("llama8b_4k", 1, 700, [32, 32, 16],
-                                                            {"head_dim": 64, "seq_tokens": (900,)})])
+                                                            {"head_dim": 64, "seq_tokens": (900,)}),
+                                                           ("llama8b_4k", 1, 3000, [32, 32],
+                                                            {"block_size": 8, "seq_tokens": (3100,)})])
 def test_gate_distances_and_decision(name, layers, prefix, ranks, over):
     w, pc, cache, T, src, dst, tab = _setup(name, layers, num_tokens=None, **over)
     bases = _anchor_states(w, layers, T, ranks, [(0.1 + 0.9 * v) / np.sqrt(r / w.head_dim)
