@@ -181,8 +181,9 @@ __global__ __launch_bounds__(kChainThreads) void chain_gram_wave(ChainArgs a) {
   f32x4 acc[NT];
 #pragma unroll
   for (int q = 0; q < NT; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  Seg seg[8];
-  auto load = [&](int t0) {
+  // rows of two steps ahead in flight (two register sets): step s + 2 is issued before step s is multiplied
+  Seg sa[8], sb[8];
+  auto load = [&](int t0, Seg* seg) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int t = t0 + 8 * g + j;
@@ -197,13 +198,19 @@ __global__ __launch_bounds__(kChainThreads) void chain_gram_wave(ChainArgs a) {
       seg[j] = v;
     }
   };
-  load(t_begin);
-  for (int t0 = t_begin; t0 < t_end; t0 += STEP) {
+  auto step = [&](int t0, Seg* seg) {
     Seg cur[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) cur[j] = seg[j];
-    if (t0 + STEP < t_end) load(t0 + STEP);
+    if (t0 + 2 * STEP < t_end) load(t0 + 2 * STEP, seg);
     cgram_tiles<FT>(acc, cur, std::make_integer_sequence<int, NT>{});
+  };
+  load(t_begin, sa);
+  if (t_begin + STEP < t_end) load(t_begin + STEP, sb);
+  for (int t0 = t_begin; t0 < t_end; t0 += 2 * STEP) {
+    step(t0, sa);
+    if (t0 + STEP >= t_end) break;
+    step(t0 + STEP, sb);
   }
   float* P = a.partials + ((size_t)u * a.max_parts + part) * MP * MP;
 #pragma unroll
