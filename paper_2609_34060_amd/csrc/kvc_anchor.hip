@@ -819,9 +819,11 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave, g = lane >> 4, n = lane & 15;
   const uint16_t* pool = static_cast<const uint16_t*>(kv ? a.layers.v[lrel] : a.layers.k[lrel]);
 
-  float dist[TPW][4];
+  // per-tile distances (the weights need each token's); the gate only needs their sum, so it keeps one set
+  constexpr int ND = GATE ? 1 : TPW;
+  float dist[ND][4];
 #pragma unroll
-  for (int j = 0; j < TPW; ++j)
+  for (int j = 0; j < ND; ++j)
 #pragma unroll
     for (int u = 0; u < 4; ++u) dist[j][u] = 0.0f;
   const bool rot = ROPE && !GATE && kv == 0;  // uniform over the workgroup
@@ -853,8 +855,8 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
         }
       }
     };
-    // dist[0] always belongs to the current tile: the array is rotated by one after every tile (static register
-    // indices with a rolled tile loop), so after TPW tiles dist[j] is tile j's again
+    // dist[0] always belongs to the current tile (the weights): the array is rotated by one after every tile (static
+    // register indices with a rolled tile loop), so after TPW tiles dist[j] is tile j's again
 #pragma unroll 1
     for (int j = 0; j < TPW; ++j) {
       const int t0 = t_begin + (j * kResWaves + wave) * 16;
@@ -914,12 +916,14 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
           }
         }
       }
+      if constexpr (!GATE) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float d0 = dist[0][u];
+        for (int u = 0; u < 4; ++u) {
+          const float d0 = dist[0][u];
 #pragma unroll
-        for (int jj = 0; jj + 1 < TPW; ++jj) dist[jj][u] = dist[jj + 1][u];
-        dist[TPW - 1][u] = d0;
+          for (int jj = 0; jj + 1 < TPW; ++jj) dist[jj][u] = dist[jj + 1][u];
+          dist[TPW - 1][u] = d0;
+        }
       }
     }
   }
@@ -928,9 +932,7 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
   if (GATE) {
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      float p = 0.0f;
-#pragma unroll
-      for (int j = 0; j < TPW; ++j) p += dist[j][u];
+      float p = dist[0][u];
 #pragma unroll
       for (int o = 1; o < 16; o <<= 1) p += __shfl_xor(p, o, kWave);
       if (n == 0 && 4 * u + g < V) s_d[wave * V + 4 * u + g] = p;
@@ -944,7 +946,7 @@ __global__ __launch_bounds__(kResThreads) void anchor_dist_res_bf16(AnchorArgs a
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < TPW; ++j) {
+    for (int j = 0; j < ND; ++j) {
       const int tok = (j * kResWaves + wave) * 16 + n;
 #pragma unroll
       for (int u = 0; u < 4; ++u)
