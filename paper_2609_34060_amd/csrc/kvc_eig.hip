@@ -3,8 +3,9 @@
 //   1. G = sum of the unit's fp32 partial Grams in a fixed order in fp64 (or a dense fp64 matrix), into LDS.
 //   2. Householder tridiagonalisation G = Q T Q^T in fp64 arithmetic; the trailing matrix is kept in LDS in fp32
 //      (the Gram itself carries fp32 accuracy), which lets two units share a CU; the reflectors go to the workspace.
-//   3. Multisection bisection with Sturm counts for the r largest eigenvalues of T (groups of lanes per
-//      eigenvalue, kBisShifts shifts per lane, one ballot per shift).
+//   3. Multisection bisection with Sturm counts for the r largest eigenvalues of T: a first step shared by all
+//      targets (every lane's shifts cut the whole interval), then groups of lanes per eigenvalue, kBisShifts
+//      shifts per lane, one ballot per shift.
 //   4. Inverse iteration on T (LDL^T without pivoting, tiny pivots replaced) from pseudo-random starts, one lane
 //      per eigenvector; then modified Gram-Schmidt over the r vectors.  Vectors of tightly clustered eigenvalues
 //      come out as an orthonormal basis of the cluster's invariant subspace (where the SVD itself is not unique).
@@ -22,49 +23,40 @@ constexpr int kEigThreads = 1024;
 constexpr int kEigWaves = kEigThreads / kWave;
 constexpr int kReflChunk = 16;  // reflectors staged in LDS per back-transformation chunk
 constexpr int kInvBatch = 32;   // eigenvectors per inverse-iteration batch (one lane each)
-constexpr int kBisShifts = 2;   // Sturm counts per lane and bisection step
-// Inverse-iteration solves per eigenvector: with lambda within 2^-32 of the spectrum's width, each solve shrinks the
-// other eigenvectors' components by that error over their gap, so two solves leave a residual at the rounding level
-// (a third does not lower it).
+constexpr int kBisShifts = 2;   // Sturm counts per lane and bisection step (even: whole int2 slices below)
+// Inverse-iteration solves per eigenvector: with lambda within 2^-29 of the spectrum's width, each solve shrinks the
+// other eigenvectors' components by that error over their gap, so two solves leave a residual far below the fp32
+// rounding of the reduced matrix.
 constexpr int kInvSolves = 2;
 
-// fp64 cross-lane moves by DPP (two 32-bit halves); lanes whose row is masked off receive 0.
+// fp64 cross-lane move by DPP (two 32-bit halves).  Lanes whose row is masked off keep an undefined value: the only
+// user reads a lane that every step writes.
 template <int CTRL, int ROW_MASK = 0xF>
 __device__ __forceinline__ double dpp64(double x) {
   const unsigned long long b = __builtin_bit_cast(unsigned long long, x);
-  const int lo = __builtin_amdgcn_update_dpp(0, (int)(unsigned)b, CTRL, ROW_MASK, 0xF, false);
-  const int hi = __builtin_amdgcn_update_dpp(0, (int)(unsigned)(b >> 32), CTRL, ROW_MASK, 0xF, false);
+  const int lo = __builtin_amdgcn_mov_dpp((int)(unsigned)b, CTRL, ROW_MASK, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(unsigned)(b >> 32), CTRL, ROW_MASK, 0xF, false);
   return __builtin_bit_cast(double, ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
 }
 constexpr int kDppRor1 = 0x121, kDppRor2 = 0x122, kDppRor4 = 0x124, kDppRor8 = 0x128;
 constexpr int kDppBcast15 = 0x142, kDppBcast31 = 0x143;
 
-// Sum over each group of G consecutive lanes (G = 16, 32 or 64); the group's last lane holds the total (other lanes
-// hold partial sums).  A fixed order, so the result is deterministic.  Called with the whole wave active.
-template <int G>
-__device__ __forceinline__ double group_sum(double x) {
-  x += dpp64<kDppRor8>(x);
-  x += dpp64<kDppRor4>(x);
-  x += dpp64<kDppRor2>(x);
-  x += dpp64<kDppRor1>(x);
-  if (G >= 32) x += dpp64<kDppBcast15, 0xA>(x);
-  if (G >= 64) x += dpp64<kDppBcast31, 0xC>(x);
-  return x;
-}
 __device__ __forceinline__ double lane_value(double x, int l) {
   const unsigned long long b = __builtin_bit_cast(unsigned long long, x);
   const unsigned lo = __builtin_amdgcn_readlane((int)(unsigned)b, l);
   const unsigned hi = __builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
   return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
 }
-// Whole-wave sum and maximum, returned in every lane.
-__device__ __forceinline__ double wave_sum(double x) { return lane_value(group_sum<64>(x), 63); }
-__device__ __forceinline__ double wave_max(double x) {
-  x = fmax(x, dpp64<kDppRor8>(x));
-  x = fmax(x, dpp64<kDppRor4>(x));
-  x = fmax(x, dpp64<kDppRor2>(x));
-  x = fmax(x, dpp64<kDppRor1>(x));
-  return fmax(fmax(lane_value(x, 0), lane_value(x, 16)), fmax(lane_value(x, 32), lane_value(x, 48)));
+// Whole-wave sum in a fixed order (deterministic), returned in every lane: sums within rows of 16 lanes, then the
+// row broadcasts carry rows 0-2 into row 3, whose last lane holds the total.  Called with the whole wave active.
+__device__ __forceinline__ double wave_sum(double x) {
+  x += dpp64<kDppRor8>(x);
+  x += dpp64<kDppRor4>(x);
+  x += dpp64<kDppRor2>(x);
+  x += dpp64<kDppRor1>(x);
+  x += dpp64<kDppBcast15, 0xA>(x);
+  x += dpp64<kDppBcast31, 0xC>(x);
+  return lane_value(x, 63);
 }
 
 // Reductions over groups of eight consecutive lanes (every lane of the group gets the result; fp32 addition is
@@ -87,6 +79,11 @@ __device__ __forceinline__ float max8(float x) {
   x = fmaxf(x, dpp32<kDppXor1>(x));
   x = fmaxf(x, dpp32<kDppXor2>(x));
   return fmaxf(x, dpp32<kDppHalfMirror>(x));
+}
+__device__ __forceinline__ int sum8i(int x) {
+  x += dpp32i<kDppXor1>(x);
+  x += dpp32i<kDppXor2>(x);
+  return x + dpp32i<kDppHalfMirror>(x);
 }
 __device__ __forceinline__ int min8(int x) {
   x = min(x, dpp32i<kDppXor1>(x));
@@ -222,12 +219,15 @@ __device__ __forceinline__ void tri_reduce(float* A, float4* s_vw, double* share
     wave_lds_sync();
     // 1. row k under the pending update; its entries beyond the diagonal are x
     const float4 vwk = s_vw[k];
+    float ak[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) ak[c] = A[k * N + CPL * lane + c];
     double x[CPL];
     double ss = 0.0;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
       const int C = CPL * lane + c;
-      const float a = upd(A[k * N + C], vwk, c);
+      const float a = upd(ak[c], vwk, c);
       if (wave == 0 && C == k) s_a[k] = (double)a;
       x[c] = C > k ? (double)a : 0.0;
       ss += x[c] * x[c];
@@ -296,9 +296,9 @@ __device__ __forceinline__ void tri_reduce(float* A, float4* s_vw, double* share
     double kk = 0.0, p[CPL];
 #pragma unroll
     for (int c = 0; c < CPL; ++c) {
-      double t = 0.0;
+      double t = sh[CPL * lane + c];
 #pragma unroll
-      for (int w = 0; w < W; ++w) t += sh[w * N + CPL * lane + c];
+      for (int w = 1; w < W; ++w) t += sh[w * N + CPL * lane + c];
       p[c] = t;
       kk += CPL * lane + c > k ? v[c] * t : 0.0;
     }
@@ -454,18 +454,57 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
     {
       int rp = 1;
       while (rp < r) rp <<= 1;
-      // P lanes per eigenvalue (a power of two dividing 64), each evaluating kBisShifts shifts: the bracket is cut
-      // into S = P kBisShifts + 1 pieces per step
-      const int P = min(8, kEigThreads / rp);
-      const int S = P * kBisShifts + 1;
-      // stop below 2^-32 of the Gershgorin interval, under the perturbation that fp32 storage of the matrix
-      // already carries
-      int iters = 0;
-      for (double w = 1.0; w < 4294967296.0; w *= S) ++iters;
-      const int grp = tid / P, s = tid - grp * P;
+      // P lanes per eigenvalue, each evaluating kBisShifts shifts: the bracket is cut into S = P kBisShifts + 1
+      // pieces per step
+      constexpr int P = 8;
+      static_assert(kEigThreads / KVC_MAX_RANK >= P, "P lanes for every eigenvalue");
+      constexpr int S = P * kBisShifts + 1;
+      // (tid passes through an empty asm so that the compiler does not keep tid / P live until the
+      // back-transformation, which takes the same quotient, and spill it)
+      int tidb = tid;
+      asm volatile("" : "+v"(tidb));
+      const int grp = tidb / P, s = tidb - grp * P;
       const int kasc = N - 1 - grp;                  // ascending index of the target eigenvalue
       const double pivmin = s_misc[4];
       double lo = s_misc[1], hi = s_misc[2];
+      // First step, shared by all targets: the rp P lanes cut the Gershgorin interval at M = rp P kBisShifts
+      // points (counts to LDS, in the matrix region, free since the reduction); each target's lanes then count
+      // the cut points left of it, so every bracket starts at 1 / (M + 1) of the interval.
+      const int M = rp * P * kBisShifts;
+      int* s_cnt = reinterpret_cast<int*>(A);
+      if (tid < rp * P) {
+        double x[kBisShifts];
+        int c[kBisShifts];
+#pragma unroll
+        for (int m = 0; m < kBisShifts; ++m) {
+          x[m] = lo + (hi - lo) * (double)(tid * kBisShifts + m + 1) / (double)(M + 1);
+          c[m] = 0;
+        }
+        sturm_counts<N, kBisShifts>(s_a, s_b2, x, pivmin, c);
+#pragma unroll
+        for (int m = 0; m < kBisShifts; ++m) s_cnt[tid * kBisShifts + m] = c[m];
+      }
+      __syncthreads();
+      if (grp < rp) {
+        // counts do not decrease along the cut points, so those left of the target are a prefix; lane s scans
+        // the s-th of P equal slices
+        const int per = M / P;  // rp kBisShifts, even
+        int left = 0;
+#pragma unroll 4
+        for (int j = s * per; j < (s + 1) * per; j += 2) {
+          const int2 c2 = *reinterpret_cast<const int2*>(&s_cnt[j]);
+          left += (c2.x <= kasc) + (c2.y <= kasc);
+        }
+        left = sum8i(left);
+        const double nlo = left == 0 ? lo : lo + (hi - lo) * (double)left / (double)(M + 1);
+        const double nhi = left == M ? hi : lo + (hi - lo) * (double)(left + 1) / (double)(M + 1);
+        lo = nlo;
+        hi = nhi;
+      }
+      // then S-way steps per target until the bracket is below 2^-29 of the Gershgorin interval: 2^-5 of the
+      // perturbation that fp32 storage of the matrix already carries (the reduction runs in fp32 as well)
+      int iters = 0;
+      for (double w = (double)(M + 1); w < 536870912.0; w *= S) ++iters;
       for (int it = 0; it < iters; ++it) {
         double x[kBisShifts];
         int c[kBisShifts];
@@ -480,7 +519,7 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
 #pragma unroll
         for (int m = 0; m < kBisShifts; ++m) {
           const uint64_t mask = __ballot(c[m] <= kasc);
-          sstar += __popcll(P == kWave ? mask : (mask >> ((lane / P) * P)) & ((1ull << P) - 1ull));
+          sstar += __popcll((mask >> ((lane / P) * P)) & ((1ull << P) - 1ull));
         }
         const double nlo = sstar == 0 ? lo : lo + (hi - lo) * (double)sstar / (double)S;
         const double nhi = sstar == S - 1 ? hi : lo + (hi - lo) * (double)(sstar + 1) / (double)S;
@@ -497,18 +536,25 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
       const int j = j0 + tid;
       if (tid < kInvBatch && j < r) {
         const double lam = s_lam[j];
-        // LDL^T of T - lam I without pivoting (tiny pivots replaced): invd[i] = 1 / d_i; pseudo-random start
-        double d = s_a[0] - lam;
-        if (fabs(d) < piv) d = copysign(piv, d);
-        double id = recip(d);
-        invd[tid] = id;
-#pragma unroll 4
-        for (int i = 1; i < N; ++i) {
-          const double b = s_b[i - 1];
-          d = (s_a[i] - lam) - b * id * b;
-          if (fabs(d) < piv) d = copysign(piv, d);
-          id = recip(d);
-          invd[i * kInvBatch + tid] = id;
+        // LDL^T of T - lam I without pivoting (tiny pivots replaced): invd[i] = 1 / d_i; pseudo-random start.
+        // The recurrences below read T and the scratch in chunks loaded ahead of the chunk's stores, so one LDS
+        // round trip serves a chunk instead of each step waiting for its own loads behind the previous store.
+        static_assert(N % 4 == 0, "whole chunks");
+        double id = 0.0;
+        for (int i0 = 0; i0 < N; i0 += 4) {
+          double av[4], bv[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            av[t] = s_a[i0 + t];
+            bv[t] = s_b[i0 + t > 0 ? i0 + t - 1 : 0];
+          }
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            double d = i0 + t > 0 ? (av[t] - lam) - bv[t] * id * bv[t] : av[t] - lam;
+            if (fabs(d) < piv) d = copysign(piv, d);
+            id = recip(d);
+            invd[(i0 + t) * kInvBatch + tid] = id;
+          }
         }
 #pragma unroll 4
         for (int i = 0; i < N; ++i) {
@@ -518,21 +564,38 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
         // kInvSolves solves (T - lam I) x_new = x; each right-hand side is scaled by 1 / max|x| on the way in
         double sc = 1.0;
         for (int itr = 0; itr < kInvSolves; ++itr) {
-          double z = xv[tid] * sc;
-          xv[tid] = z;
-#pragma unroll 4
-          for (int i = 1; i < N; ++i) {
-            z = xv[i * kInvBatch + tid] * sc - s_b[i - 1] * invd[(i - 1) * kInvBatch + tid] * z;
-            xv[i * kInvBatch + tid] = z;
+          double z = 0.0;
+          for (int i0 = 0; i0 < N; i0 += 4) {
+            double xw[4], bw[4], iw[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int i = i0 + t, im = i > 0 ? i - 1 : 0;
+              xw[t] = xv[i * kInvBatch + tid];
+              bw[t] = s_b[im];
+              iw[t] = invd[im * kInvBatch + tid];
+            }
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              z = i0 + t > 0 ? xw[t] * sc - bw[t] * iw[t] * z : xw[t] * sc;
+              xv[(i0 + t) * kInvBatch + tid] = z;
+            }
           }
-          double x = z * invd[(N - 1) * kInvBatch + tid];
-          xv[(N - 1) * kInvBatch + tid] = x;
-          double mx = fabs(x);
-#pragma unroll 4
-          for (int i = N - 2; i >= 0; --i) {
-            x = (xv[i * kInvBatch + tid] - s_b[i] * x) * invd[i * kInvBatch + tid];
-            xv[i * kInvBatch + tid] = x;
-            mx = fmax(mx, fabs(x));
+          double x = 0.0, mx = 0.0;
+          for (int i1 = N - 1; i1 >= 0; i1 -= 4) {
+            double xw[4], bw[4], iw[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const int i = i1 - t;
+              xw[t] = xv[i * kInvBatch + tid];
+              bw[t] = s_b[i < N - 1 ? i : 0];
+              iw[t] = invd[i * kInvBatch + tid];
+            }
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              x = i1 - t == N - 1 ? xw[t] * iw[t] : (xw[t] - bw[t] * x) * iw[t];
+              xv[(i1 - t) * kInvBatch + tid] = x;
+              mx = fmax(mx, fabs(x));
+            }
           }
           sc = mx > 0.0 ? 1.0 / mx : 1.0;
         }
