@@ -47,16 +47,21 @@ __device__ __forceinline__ double lane_value(double x, int l) {
   const unsigned hi = __builtin_amdgcn_readlane((int)(unsigned)(b >> 32), l);
   return __builtin_bit_cast(double, ((unsigned long long)hi << 32) | lo);
 }
-// Whole-wave sum in a fixed order (deterministic), returned in every lane: sums within rows of 16 lanes, then the
-// row broadcasts carry rows 0-2 into row 3, whose last lane holds the total.  Called with the whole wave active.
-__device__ __forceinline__ double wave_sum(double x) {
-  x += dpp64<kDppRor8>(x);
-  x += dpp64<kDppRor4>(x);
-  x += dpp64<kDppRor2>(x);
-  x += dpp64<kDppRor1>(x);
-  x += dpp64<kDppBcast15, 0xA>(x);
-  x += dpp64<kDppBcast31, 0xC>(x);
+// Whole-wave reduction by op in a fixed order (deterministic), returned in every lane: within rows of 16 lanes,
+// then the row broadcasts carry rows 0-2 into row 3, whose last lane holds the result.  Called with the whole wave
+// active.
+template <class Op>
+__device__ __forceinline__ double wave_reduce(double x, Op op) {
+  x = op(x, dpp64<kDppRor8>(x));
+  x = op(x, dpp64<kDppRor4>(x));
+  x = op(x, dpp64<kDppRor2>(x));
+  x = op(x, dpp64<kDppRor1>(x));
+  x = op(x, dpp64<kDppBcast15, 0xA>(x));
+  x = op(x, dpp64<kDppBcast31, 0xC>(x));
   return lane_value(x, 63);
+}
+__device__ __forceinline__ double wave_sum(double x) {
+  return wave_reduce(x, [](double u, double v) { return u + v; });
 }
 
 // Reductions over groups of eight consecutive lanes (every lane of the group gets the result; fp32 addition is
@@ -425,21 +430,29 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   tri_reduce<N>(A, s_vw, share, s_a, s_b, refl, refl_beta, lane, wave);
   __syncthreads();
   for (int i = tid; i < N - 1; i += kEigThreads) s_b2[i] = s_b[i] * s_b[i];
-  if (tid == 0) {
+  if (wave == 0) {
+    // Gershgorin interval of T and the largest b^2 (minima and maxima: any order gives the same result)
     double lo = s_a[0], hi = s_a[0], bmax2 = 0.0;
-    for (int i = 0; i < N; ++i) {
+#pragma unroll
+    for (int q = 0; q < N / kWave; ++q) {
+      const int i = lane + kWave * q;
       const double rad = (i > 0 ? fabs(s_b[i - 1]) : 0.0) + (i < N - 1 ? fabs(s_b[i]) : 0.0);
       lo = fmin(lo, s_a[i] - rad);
       hi = fmax(hi, s_a[i] + rad);
       if (i < N - 1) bmax2 = fmax(bmax2, s_b[i] * s_b[i]);
     }
-    const double tnorm = fmax(fabs(lo), fabs(hi));
-    const double pivmin = 2.2250738585072014e-308 * fmax(1.0, bmax2);
-    const double pad = 2.0 * 2.220446049250313e-16 * tnorm * N + pivmin;
-    s_misc[1] = lo - pad;
-    s_misc[2] = hi + pad;
-    s_misc[3] = tnorm;
-    s_misc[4] = pivmin;
+    lo = wave_reduce(lo, [](double x, double y) { return fmin(x, y); });
+    hi = wave_reduce(hi, [](double x, double y) { return fmax(x, y); });
+    bmax2 = wave_reduce(bmax2, [](double x, double y) { return fmax(x, y); });
+    if (lane == 0) {
+      const double tnorm = fmax(fabs(lo), fabs(hi));
+      const double pivmin = 2.2250738585072014e-308 * fmax(1.0, bmax2);
+      const double pad = 2.0 * 2.220446049250313e-16 * tnorm * N + pivmin;
+      s_misc[1] = lo - pad;
+      s_misc[2] = hi + pad;
+      s_misc[3] = tnorm;
+      s_misc[4] = pivmin;
+    }
   }
   __syncthreads();
   const double tnorm = s_misc[3];
@@ -681,16 +694,38 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
     for (int i = 0; i < PB; ++i) xr[i] = 0.0f;
   }
   if (tnorm != 0.0) {
+    // each chunk's reflectors are read from the workspace into registers one chunk ahead, so that the global
+    // loads run while the previous chunk is applied
+    constexpr int EPT = (kReflChunk * N + kEigThreads - 1) / kEigThreads;
+    static_assert(kReflChunk <= kEigThreads, "one beta per thread");
+    float pre[EPT], preb = 0.0f;
+    auto fetch = [&](int kc) {
+      const int nk = min(kReflChunk, kc + 1);
+#pragma unroll
+      for (int q = 0; q < EPT; ++q) {
+        const int e = tid + q * kEigThreads;
+        float v = 0.0f;
+        if (e < nk * N) {
+          const int c = e / N, pos = e - c * N;
+          const int k = kc - c;
+          if (pos > k) v = (float)refl[k * N + pos - k - 1];
+        }
+        pre[q] = v;
+      }
+      preb = tid < nk ? (float)refl_beta[kc - tid] : 0.0f;
+    };
+    fetch(N - 3);
     for (int kc = N - 3; kc >= 0; kc -= kReflChunk) {
       const int nk = min(kReflChunk, kc + 1);
       __syncthreads();
-      for (int e = tid; e < nk * N; e += kEigThreads) {
-        const int c = e / N, pos = e - c * N;
-        const int k = kc - c;
-        s_rb[c * N + pos] = pos > k ? (float)refl[k * N + pos - k - 1] : 0.0f;
+#pragma unroll
+      for (int q = 0; q < EPT; ++q) {
+        const int e = tid + q * kEigThreads;
+        if (e < nk * N) s_rb[e] = pre[q];
       }
-      for (int c = tid; c < nk; c += kEigThreads) s_rbeta[c] = (float)refl_beta[kc - c];
+      if (tid < nk) s_rbeta[tid] = preb;
       __syncthreads();
+      if (kc >= kReflChunk) fetch(kc - kReflChunk);
       if (wave_act) {
         for (int c = 0; c < nk; ++c) {
           const float beta = s_rbeta[c];
