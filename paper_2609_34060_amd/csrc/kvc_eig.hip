@@ -24,9 +24,10 @@ constexpr int kEigWaves = kEigThreads / kWave;
 constexpr int kReflChunk = 16;  // reflectors staged in LDS per back-transformation chunk
 constexpr int kInvBatch = 32;   // eigenvectors per inverse-iteration batch (one lane each)
 constexpr int kBisShifts = 2;   // Sturm counts per lane and bisection step (even: whole int2 slices below)
-// Inverse-iteration solves per eigenvector: with lambda within 2^-29 of the spectrum's width, each solve shrinks the
-// other eigenvectors' components by that error over their gap, so two solves leave a residual far below the fp32
-// rounding of the reduced matrix.
+// Inverse-iteration solves per eigenvector: with lambda within about 2^-24 of the spectrum's width, each solve
+// shrinks the other eigenvectors' components by that error over their gap, so two solves leave a residual far
+// below the fp32 rounding of the reduced matrix (about 1e-11 of the width in an fp64 simulation of the recurrence
+// on decaying and flat spectra).
 constexpr int kInvSolves = 2;
 
 // fp64 cross-lane move by DPP (two 32-bit halves).  Lanes whose row is masked off keep an undefined value: the only
@@ -147,17 +148,19 @@ __device__ __forceinline__ void reflector_scalars(double x0, double s, double* o
   out[2] = nrm == 0.0 ? 0.0 : recip(nrm * (nrm + fabs(x0)));
 }
 
-// Numbers of eigenvalues of T below each of the M shifts x[m] (ratio form of the Sturm sequence; pivots smaller
-// than pivmin are replaced by -pivmin, so that b^2 / q stays finite).  The M recurrences are independent, so their
-// latencies overlap, and they share the loads of T.
+// Numbers of eigenvalues of T below each of the M shifts x[m]: the ratio form of the Sturm sequence, q_i = (a_i - x)
+// - b_{i-1}^2 / q_{i-1}, with the hardware reciprocal (relative error below 2^-24, measured on random fp64 inputs)
+// and IEEE infinities in place of a pivot guard: a zero pivot makes the next one -inf (counted), and the one after
+// that is plain a - x again, the same count the classical replacement of tiny pivots gives.  b^2 is floored at the
+// smallest normal number so that b^2 times an infinite reciprocal is never 0 * inf.  Each count is exact for T with
+// every b^2 perturbed by at most 2^-24 relative, below the perturbation fp32 storage of the matrix carries.  The M
+// recurrences are independent, so their latencies overlap, and they share the loads of T.
 template <int N, int M>
-__device__ __forceinline__ void sturm_counts(const double* sa, const double* sb2, const double* x, double pivmin,
-                                             int* cnt) {
+__device__ __forceinline__ void sturm_counts(const double* sa, const double* sb2, const double* x, int* cnt) {
   double q[M];
 #pragma unroll
   for (int m = 0; m < M; ++m) {
     q[m] = sa[0] - x[m];
-    if (fabs(q[m]) < pivmin) q[m] = -pivmin;
     cnt[m] = q[m] < 0.0;
   }
 #pragma unroll 4
@@ -165,8 +168,7 @@ __device__ __forceinline__ void sturm_counts(const double* sa, const double* sb2
     const double ai = sa[i], bi = sb2[i - 1];
 #pragma unroll
     for (int m = 0; m < M; ++m) {
-      q[m] = (ai - x[m]) - bi * recip(q[m]);
-      if (fabs(q[m]) < pivmin) q[m] = -pivmin;
+      q[m] = fma(-bi, __builtin_amdgcn_rcp(q[m]), ai - x[m]);
       cnt[m] += q[m] < 0.0;
     }
   }
@@ -219,14 +221,15 @@ __device__ __forceinline__ void tri_reduce(float* A, float4* s_vw, double* share
     *reinterpret_cast<float2*>(&s_vw[CPL * lane + c]) = make_float2(0.0f, 0.0f);
   }
   auto upd = [&](float a, const float4& vw, int c) { return fmaf(-vw.x, wpf[c], fmaf(-vw.y, vpf[c], a)); };
+  // row k as the sweep of step k - 1 left it (loaded right after that step's barrier) and its pending-update
+  // scalars {v_k, w_k} (taken from the lane that holds column k, not through LDS)
+  float ak[CPL];
+  float4 vwk = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) ak[c] = A[CPL * lane + c];
   for (int k = 0; k < N - 2; ++k) {
     const int k1 = k + 1;
-    wave_lds_sync();
     // 1. row k under the pending update; its entries beyond the diagonal are x
-    const float4 vwk = s_vw[k];
-    float ak[CPL];
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) ak[c] = A[k * N + CPL * lane + c];
     double x[CPL];
     double ss = 0.0;
 #pragma unroll
@@ -297,6 +300,8 @@ __device__ __forceinline__ void tri_reduce(float* A, float4* s_vw, double* share
 #pragma unroll
     for (int c = 0; c < CPL; ++c) sh[wave * N + CPL * lane + c] = (double)pf[c];
     __syncthreads();
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) ak[c] = A[k1 * N + CPL * lane + c];
     // 3. p = the sum of the shares; K = (beta^2 / 2) v^T p; w = beta p - K v becomes the pending update
     double kk = 0.0, p[CPL];
 #pragma unroll
@@ -315,6 +320,15 @@ __device__ __forceinline__ void tri_reduce(float* A, float4* s_vw, double* share
       wpf[c] = C > k ? (float)(beta * p[c] - K * v[c]) : 0.0f;
       *reinterpret_cast<float2*>(&s_vw[C]) = make_float2(vpf[c], wpf[c]);
     }
+    float vsel = vpf[0], wsel = wpf[0];
+#pragma unroll
+    for (int c = 1; c < CPL; ++c)
+      if (k1 % CPL == c) {
+        vsel = vpf[c];
+        wsel = wpf[c];
+      }
+    vwk.x = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, vsel), k1 / CPL));
+    vwk.y = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wsel), k1 / CPL));
   }
   // the last pending update on the trailing 2 x 2 block
   if (wave == 0) {
@@ -429,29 +443,25 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
   // ---- 2. Householder tridiagonalisation ------------------------------------------------------------------------
   tri_reduce<N>(A, s_vw, share, s_a, s_b, refl, refl_beta, lane, wave);
   __syncthreads();
-  for (int i = tid; i < N - 1; i += kEigThreads) s_b2[i] = s_b[i] * s_b[i];
+  for (int i = tid; i < N - 1; i += kEigThreads) s_b2[i] = fmax(s_b[i] * s_b[i], 2.2250738585072014e-308);
   if (wave == 0) {
-    // Gershgorin interval of T and the largest b^2 (minima and maxima: any order gives the same result)
-    double lo = s_a[0], hi = s_a[0], bmax2 = 0.0;
+    // Gershgorin interval of T (minima and maxima: any order gives the same result)
+    double lo = s_a[0], hi = s_a[0];
 #pragma unroll
     for (int q = 0; q < N / kWave; ++q) {
       const int i = lane + kWave * q;
       const double rad = (i > 0 ? fabs(s_b[i - 1]) : 0.0) + (i < N - 1 ? fabs(s_b[i]) : 0.0);
       lo = fmin(lo, s_a[i] - rad);
       hi = fmax(hi, s_a[i] + rad);
-      if (i < N - 1) bmax2 = fmax(bmax2, s_b[i] * s_b[i]);
     }
     lo = wave_reduce(lo, [](double x, double y) { return fmin(x, y); });
     hi = wave_reduce(hi, [](double x, double y) { return fmax(x, y); });
-    bmax2 = wave_reduce(bmax2, [](double x, double y) { return fmax(x, y); });
     if (lane == 0) {
       const double tnorm = fmax(fabs(lo), fabs(hi));
-      const double pivmin = 2.2250738585072014e-308 * fmax(1.0, bmax2);
-      const double pad = 2.0 * 2.220446049250313e-16 * tnorm * N + pivmin;
+      const double pad = 2.0 * 2.220446049250313e-16 * tnorm * N + 2.2250738585072014e-308;
       s_misc[1] = lo - pad;
       s_misc[2] = hi + pad;
       s_misc[3] = tnorm;
-      s_misc[4] = pivmin;
     }
   }
   __syncthreads();
@@ -478,7 +488,6 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
       asm volatile("" : "+v"(tidb));
       const int grp = tidb / P, s = tidb - grp * P;
       const int kasc = N - 1 - grp;                  // ascending index of the target eigenvalue
-      const double pivmin = s_misc[4];
       double lo = s_misc[1], hi = s_misc[2];
       // First step, shared by all targets: the rp P lanes cut the Gershgorin interval at M = rp P kBisShifts
       // points (counts to LDS, in the matrix region, free since the reduction); each target's lanes then count
@@ -493,7 +502,7 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
           x[m] = lo + (hi - lo) * (double)(tid * kBisShifts + m + 1) / (double)(M + 1);
           c[m] = 0;
         }
-        sturm_counts<N, kBisShifts>(s_a, s_b2, x, pivmin, c);
+        sturm_counts<N, kBisShifts>(s_a, s_b2, x, c);
 #pragma unroll
         for (int m = 0; m < kBisShifts; ++m) s_cnt[tid * kBisShifts + m] = c[m];
       }
@@ -514,10 +523,10 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
         lo = nlo;
         hi = nhi;
       }
-      // then S-way steps per target until the bracket is below 2^-29 of the Gershgorin interval: 2^-5 of the
-      // perturbation that fp32 storage of the matrix already carries (the reduction runs in fp32 as well)
+      // then S-way steps per target until the bracket is below 2^-25 of the Gershgorin interval, the accuracy of
+      // the counts themselves
       int iters = 0;
-      for (double w = (double)(M + 1); w < 536870912.0; w *= S) ++iters;
+      for (double w = (double)(M + 1); w < 33554432.0; w *= S) ++iters;
       for (int it = 0; it < iters; ++it) {
         double x[kBisShifts];
         int c[kBisShifts];
@@ -526,7 +535,7 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
           x[m] = lo + (hi - lo) * (double)(s * kBisShifts + m + 1) / (double)S;
           c[m] = 0;
         }
-        if (grp < r) sturm_counts<N, kBisShifts>(s_a, s_b2, x, pivmin, c);
+        if (grp < r) sturm_counts<N, kBisShifts>(s_a, s_b2, x, c);
         // shifts left of the target form a prefix of the S - 1 cut points; sstar counts them
         int sstar = 0;
 #pragma unroll
