@@ -52,8 +52,9 @@ __global__ __launch_bounds__(W * kWave) void apply_bf16_mfma(ApplyArgs a, int tp
   int32_t* s_tab = reinterpret_cast<int32_t*>(s_dyn + 2 * D * KP);  // [2][nblk]: source, destination
 
   const int nl = a.num_layers;
-  const int item_id = blockIdx.z / nl;
-  const int lrel = blockIdx.z - item_id * nl;
+  const int il = grid_item_layer(a.chunk_order);
+  const int item_id = il / nl;
+  const int lrel = il - item_id * nl;
   const int layer = a.layer_begin + lrel;
   const int H = a.pv.num_kv_heads;
   const int kv = a.kv_begin + (int)blockIdx.y / H;
@@ -62,7 +63,7 @@ __global__ __launch_bounds__(W * kWave) void apply_bf16_mfma(ApplyArgs a, int tp
   const kvc_item* itp = a.items + item_id;
   const int T = itp->num_tokens;
   const int chunk = W * 16 * tpw;
-  const int t_begin = blockIdx.x * chunk;
+  const int t_begin = grid_chunk(a.chunk_order) * chunk;
   if (t_begin >= T) return;  // whole workgroup
   const int t_end = min(T, t_begin + chunk);
   const int r = itp->state.rank;
@@ -269,8 +270,9 @@ __global__ __launch_bounds__(kApplyThreads) void apply_f32_valu(ApplyArgs a) {
   constexpr int TPP = kApplyThreads / LPT;                     // tokens per pass
 
   const int nl = a.num_layers;
-  const int item_id = blockIdx.z / nl;
-  const int lrel = blockIdx.z - item_id * nl;
+  const int il = grid_item_layer(a.chunk_order);
+  const int item_id = il / nl;
+  const int lrel = il - item_id * nl;
   const int layer = a.layer_begin + lrel;
   const int H = a.pv.num_kv_heads;
   const int kv = a.kv_begin + (int)blockIdx.y / H;
@@ -278,7 +280,7 @@ __global__ __launch_bounds__(kApplyThreads) void apply_f32_valu(ApplyArgs a) {
 
   const kvc_item* itp = a.items + item_id;
   const int T = itp->num_tokens;
-  const int t_begin = blockIdx.x * kApplyChunk;
+  const int t_begin = grid_chunk(a.chunk_order) * kApplyChunk;
   if (t_begin >= T) return;
   const int r = itp->state.rank;
   const int Tdecl = itp->state.num_tokens;
@@ -376,7 +378,9 @@ static hipError_t launch_bf16(const ApplyArgs& a0, int max_tokens, int num_items
   if (a.pv.rope.style != KVC_ROPE_NONE) {
     const int chunk = kApplyRopeChunkTokens;
     a.kv_begin = 0;
-    const dim3 grid((max_tokens + chunk - 1) / chunk, H, num_items * a.num_layers);
+    const int chunks = (max_tokens + chunk - 1) / chunk;
+    a.chunk_order = multi_item_order(num_items, chunks, kChunksRotated);
+    const dim3 grid = chunk_grid(chunks, H, num_items * a.num_layers, a.chunk_order);
     const hipError_t e = launch_bf16_w<D, KS, 4, true>(a, grid, chunk / 64,
                                                        (chunk + a.pv.block_size - 1) / a.pv.block_size + 1, stream);
     if (e != hipSuccess) return e;
@@ -385,7 +389,9 @@ static hipError_t launch_bf16(const ApplyArgs& a0, int max_tokens, int num_items
   }
   const int chunk = kApplyChunkTokens;
   constexpr int W = apply_waves(KS);
-  const dim3 grid((max_tokens + chunk - 1) / chunk, nkv * H, num_items * a.num_layers);
+  const int chunks = (max_tokens + chunk - 1) / chunk;
+  a.chunk_order = multi_item_order(num_items, chunks, kChunksRotated);
+  const dim3 grid = chunk_grid(chunks, nkv * H, num_items * a.num_layers, a.chunk_order);
   return launch_bf16_w<D, KS, W, false>(a, grid, chunk / (16 * W), (chunk + a.pv.block_size - 1) / a.pv.block_size + 1,
                                         stream);
 }
@@ -410,12 +416,15 @@ hipError_t launch_apply(const ApplyArgs& a, kvc_dtype dtype, int max_rank, int m
     return D == 64 ? launch_bf16_ks<64>(a, ks, max_tokens, num_items, stream)
                    : launch_bf16_ks<128>(a, ks, max_tokens, num_items, stream);
   }
-  dim3 grid((max_tokens + kApplyChunk - 1) / kApplyChunk, 2 * a.pv.num_kv_heads, num_items * a.num_layers);
+  ApplyArgs b = a;
+  const int chunks = (max_tokens + kApplyChunk - 1) / kApplyChunk;
+  b.chunk_order = multi_item_order(num_items, chunks, kChunksRotated);
+  const dim3 grid = chunk_grid(chunks, 2 * a.pv.num_kv_heads, num_items * a.num_layers, b.chunk_order);
   const size_t lds = (size_t)max_rank * D * sizeof(float);
   if (D == 64) {
-    hipLaunchKernelGGL(apply_f32_valu<64>, grid, dim3(kApplyThreads), lds, stream, a);
+    hipLaunchKernelGGL(apply_f32_valu<64>, grid, dim3(kApplyThreads), lds, stream, b);
   } else {
-    hipLaunchKernelGGL(apply_f32_valu<128>, grid, dim3(kApplyThreads), lds, stream, a);
+    hipLaunchKernelGGL(apply_f32_valu<128>, grid, dim3(kApplyThreads), lds, stream, b);
   }
   return hipGetLastError();
 }

@@ -192,6 +192,19 @@ __device__ __forceinline__ void rope_rotate_rows_wave(f32x4* v, int style, int g
 }
 
 // Offset of unit (layer, kv, head) in a state's per-unit arrays.
+// Position of a workgroup in a grid over (chunk, unit, item x layer) laid out by chunk_grid: order 0 has the chunks
+// fastest, 1 shifts each row's (y, z) chunks by the row index modulo the row length, 2 has the items fastest (x and
+// z trade places).
+__device__ __forceinline__ int grid_chunk(int order) {
+  if (order == 2) return (int)blockIdx.z;
+  if (order == 1) {
+    const unsigned row = blockIdx.y + gridDim.y * blockIdx.z;
+    return (int)((blockIdx.x + row % gridDim.x) % gridDim.x);
+  }
+  return (int)blockIdx.x;
+}
+__device__ __forceinline__ int grid_item_layer(int order) { return (int)(order == 2 ? blockIdx.x : blockIdx.z); }
+
 __device__ __forceinline__ int64_t unit_index(int32_t layer, int32_t kv, int32_t head, int32_t num_kv_heads) {
   return ((int64_t)layer * 2 + kv) * num_kv_heads + head;
 }

@@ -29,8 +29,9 @@ struct FitUnit {
 __device__ __forceinline__ FitUnit fit_unit(const FitArgs& a) {
   FitUnit f;
   const int H = a.pv.num_kv_heads;
-  f.item = blockIdx.z / a.num_layers;
-  f.lrel = blockIdx.z - f.item * a.num_layers;
+  const int il = grid_item_layer(a.chunk_order);
+  f.item = il / a.num_layers;
+  f.lrel = il - f.item * a.num_layers;
   f.layer = a.layer_begin + f.lrel;
   const int y = blockIdx.y;
   f.kv = a.kv_begin + y / H;
@@ -124,7 +125,7 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_mfma(FitArgs a) {
     rope_table(a.pv.rope, D, -(double)itp->src_position, s_rope[2], s_rope[3]);
     __syncthreads();
   }
-  const int part = blockIdx.x * kFitWaves + wave;
+  const int part = grid_chunk(a.chunk_order) * kFitWaves + wave;
   const int t_begin = part * a.part_tokens;
   if (r == 0 || t_begin >= Ts) return;  // per wave: the kernel has no barrier
   const int t_end = min(Ts, t_begin + a.part_tokens);
@@ -302,8 +303,9 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_ring(FitArgs a) {
   const int H = a.pv.num_kv_heads;
   const int HG = (H + kFitWaves - 1) / kFitWaves;
   FitUnit f;
-  f.item = blockIdx.z / a.num_layers;
-  f.lrel = blockIdx.z - f.item * a.num_layers;
+  const int il = grid_item_layer(a.chunk_order);
+  f.item = il / a.num_layers;
+  f.lrel = il - f.item * a.num_layers;
   f.layer = a.layer_begin + f.lrel;
   f.kv = a.kv_begin + (int)blockIdx.y / HG;
   f.head = ((int)blockIdx.y % HG) * kFitWaves + wave;
@@ -312,7 +314,7 @@ __global__ __launch_bounds__(kFitThreads) void gram_bf16_ring(FitArgs a) {
   const kvc_item* itp = a.items + f.item;
   const int r = itp->state.rank;
   const int Ts = itp->state.num_tokens;
-  const int part = blockIdx.x;
+  const int part = grid_chunk(a.chunk_order);
   const int t_begin = part * a.part_tokens;
   if (r == 0 || t_begin >= Ts) return;  // per wave: the kernel has no barrier
   const int t_end = min(Ts, t_begin + a.part_tokens);
@@ -504,7 +506,7 @@ __global__ __launch_bounds__(kFitThreads) void gram_f32_valu(FitArgs a) {
   const kvc_item* itp = a.items + f.item;
   const int r = itp->state.rank;
   const int Ts = itp->state.num_tokens;
-  const int c = blockIdx.x;
+  const int c = grid_chunk(a.chunk_order);
   const int t_begin = c * a.part_tokens;
   if (r == 0 || t_begin >= Ts) return;
   const int t_end = min(Ts, t_begin + a.part_tokens);
@@ -612,7 +614,7 @@ __global__ __launch_bounds__(W * kWave) void proj_bf16_mfma(FitArgs a, int tpw, 
   const int r = itp->state.rank;
   const int Ts = itp->state.num_tokens;
   const int chunk = W * 16 * tpw;
-  const int t_begin = blockIdx.x * chunk;
+  const int t_begin = grid_chunk(a.chunk_order) * chunk;
   if (r == 0 || t_begin >= Ts) return;  // whole workgroup
   const int t_end = min(Ts, t_begin + chunk);
   const uint16_t* pool = static_cast<const uint16_t*>(f.kv ? a.layers.v[f.lrel] : a.layers.k[f.lrel]);
@@ -781,7 +783,7 @@ __global__ __launch_bounds__(kFitThreads) void proj_f32_valu(FitArgs a) {
   const kvc_item* itp = a.items + f.item;
   const int r = itp->state.rank;
   const int Ts = itp->state.num_tokens;
-  const int t_begin = blockIdx.x * kProjChunk;
+  const int t_begin = grid_chunk(a.chunk_order) * kProjChunk;
   if (r == 0 || t_begin >= Ts) return;
   const int t_end = min(Ts, t_begin + kProjChunk);
   const int32_t* src_tab = a.src_tables ? a.src_tables + (int64_t)f.item * a.max_blocks : nullptr;
@@ -834,12 +836,16 @@ static hipError_t launch_gram_variants(const FitArgs& a0, kvc_dtype dtype, int n
   FitArgs a = a0;
   a.kv_begin = kv_begin;
   const int D = a.pv.head_dim;
+  const int il = num_items * a.num_layers;
   if (dtype == KVC_BF16) {
-    dim3 grid((a.max_parts + kFitWaves - 1) / kFitWaves, nkv * a.pv.num_kv_heads, num_items * a.num_layers);
+    const int pchunks = (a.max_parts + kFitWaves - 1) / kFitWaves;
+    a.chunk_order = multi_item_order(num_items, pchunks, kItemsFast);
+    dim3 grid = chunk_grid(pchunks, nkv * a.pv.num_kv_heads, il, a.chunk_order);
     if (!ROPE && D == 128 && a.pv.block_shift >= 4 && a.part_tokens / a.pv.block_size + 3 <= kGramTabMax) {
       // LDS-staged rows (block sizes of at least 16 tokens, a partial's table fits the wave's LDS copy)
       const bool delta = a.mode == KVC_FIT_DELTA;
-      grid = dim3(a.max_parts, nkv * ((a.pv.num_kv_heads + kFitWaves - 1) / kFitWaves), num_items * a.num_layers);
+      a.chunk_order = multi_item_order(num_items, a.max_parts, kItemsFast);
+      grid = chunk_grid(a.max_parts, nkv * ((a.pv.num_kv_heads + kFitWaves - 1) / kFitWaves), il, a.chunk_order);
       const void* fn = delta ? (const void*)gram_bf16_ring<true> : (const void*)gram_bf16_ring<false>;
       hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kGramLdsBytes);
       if (e != hipSuccess) return e;
@@ -851,7 +857,8 @@ static hipError_t launch_gram_variants(const FitArgs& a0, kvc_dtype dtype, int n
       hipLaunchKernelGGL((gram_bf16_mfma<128, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
     }
   } else {
-    dim3 grid(a.max_parts, nkv * a.pv.num_kv_heads, num_items * a.num_layers);
+    a.chunk_order = multi_item_order(num_items, a.max_parts, kItemsFast);
+    const dim3 grid = chunk_grid(a.max_parts, nkv * a.pv.num_kv_heads, il, a.chunk_order);
     if (D == 64) hipLaunchKernelGGL((gram_f32_valu<64, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
     else hipLaunchKernelGGL((gram_f32_valu<128, ROPE>), grid, dim3(kFitThreads), 0, stream, a);
   }
@@ -867,10 +874,13 @@ hipError_t launch_fit_gram(const FitArgs& a, kvc_dtype dtype, int num_items, hip
 }
 
 template <int D, int MTR, bool ROPE>
-static hipError_t launch_proj_bf16_m(const FitArgs& a, int nkv, int max_tokens, int num_items, hipStream_t stream) {
+static hipError_t launch_proj_bf16_m(const FitArgs& a0, int nkv, int max_tokens, int num_items, hipStream_t stream) {
   constexpr int W = ROPE ? kProjRopeWaves : kProjWaves;
   const int chunk = ROPE ? kProjRopeChunkTokens : (MTR > 2 ? kProjLongChunkTokens : kProjChunkTokens);
-  dim3 grid((max_tokens + chunk - 1) / chunk, nkv * a.pv.num_kv_heads, num_items * a.num_layers);
+  FitArgs a = a0;
+  const int chunks = (max_tokens + chunk - 1) / chunk;
+  a.chunk_order = multi_item_order(num_items, chunks, kChunksRotated);
+  const dim3 grid = chunk_grid(chunks, nkv * a.pv.num_kv_heads, num_items * a.num_layers, a.chunk_order);
   const int nblk = (chunk + a.pv.block_size - 1) / a.pv.block_size + 1;
   const size_t lds = proj_lds_bytes(D, MTR * 16, nblk);
   hipError_t e = hipFuncSetAttribute((const void*)proj_bf16_mfma<D, MTR, W, ROPE>,
@@ -905,7 +915,9 @@ static hipError_t launch_proj_variants(const FitArgs& a0, kvc_dtype dtype, int n
     return D == 64 ? launch_proj_bf16<64, ROPE>(a, mtr, nkv, max_tokens, num_items, stream)
                    : launch_proj_bf16<128, ROPE>(a, mtr, nkv, max_tokens, num_items, stream);
   }
-  dim3 grid((max_tokens + kProjChunk - 1) / kProjChunk, nkv * a.pv.num_kv_heads, num_items * a.num_layers);
+  const int chunks = (max_tokens + kProjChunk - 1) / kProjChunk;
+  a.chunk_order = multi_item_order(num_items, chunks, kChunksRotated);
+  const dim3 grid = chunk_grid(chunks, nkv * a.pv.num_kv_heads, num_items * a.num_layers, a.chunk_order);
   const size_t lds = (size_t)max_rank * D * sizeof(float);
   if (D == 64) hipLaunchKernelGGL((proj_f32_valu<64, ROPE>), grid, dim3(kFitThreads), lds, stream, a);
   else hipLaunchKernelGGL((proj_f32_valu<128, ROPE>), grid, dim3(kFitThreads), lds, stream, a);
