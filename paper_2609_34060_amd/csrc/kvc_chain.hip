@@ -232,7 +232,8 @@ __global__ __launch_bounds__(kChainThreads) void chain_gram_wave(ChainArgs a) {
 // LDS version for m <= 128: H (fp64 sum of the partials, kept as fp32) and K^T = [B1; B2] staged in LDS (H needs
 // M8 x M8 floats, more than P's M8 x d when the rank sum exceeds the head dimension); P = H K^T
 // with fp64 accumulation in registers (8 x 4 tiles), written back over H; G = K P in 8 x 8 tiles on or above the
-// diagonal, each stored with its mirror.
+// diagonal, staged in LDS as fp32 (the precision the eigensolver keeps) with each tile's mirror, then written out in
+// whole rows.
 __global__ __launch_bounds__(kChainThreads) void chain_assemble_lds(ChainArgs a) {
   extern __shared__ __attribute__((aligned(16))) float s_asm[];
   const int u = blockIdx.x;
@@ -246,16 +247,46 @@ __global__ __launch_bounds__(kChainThreads) void chain_assemble_lds(ChainArgs a)
   float* R = s_asm;
   float* Bs = s_asm + M8 * RW;     // K^T [M8][d]
   const int tid = threadIdx.x;
-  for (int e = tid; e < M8 * M8; e += kChainThreads) {
-    const int i = e / M8, j = e - i * M8;
-    double s = 0.0;
-    if (i < m && j < m)
-      for (int c = 0; c < parts; ++c) s += (double)PP[(size_t)c * MP * MP + i * MP + j];
-    R[e] = (float)s;
+  // H: the partials summed in fp64 in order c = 0, 1, ...; a batch of entries per thread has all its loads of one
+  // partial in flight together
+  constexpr int HB = 16;
+  for (int e0 = 0; e0 < M8 * M8; e0 += HB * kChainThreads) {
+    double s[HB];
+    int off[HB];
+#pragma unroll
+    for (int q = 0; q < HB; ++q) {
+      const int e = e0 + tid + q * kChainThreads;
+      const int i = e / M8, j = e - i * M8;
+      s[q] = 0.0;
+      off[q] = e < M8 * M8 && i < m && j < m ? i * MP + j : -1;
+    }
+    for (int c = 0; c < parts; ++c) {
+      float v[HB];
+#pragma unroll
+      for (int q = 0; q < HB; ++q) v[q] = off[q] >= 0 ? PP[(size_t)c * MP * MP + off[q]] : 0.0f;
+#pragma unroll
+      for (int q = 0; q < HB; ++q) s[q] += (double)v[q];
+    }
+#pragma unroll
+    for (int q = 0; q < HB; ++q) {
+      const int e = e0 + tid + q * kChainThreads;
+      if (e < M8 * M8) R[e] = (float)s[q];
+    }
   }
-  for (int e = tid; e < M8 * d; e += kChainThreads) {
-    const int l = e / d, f = e - l * d;
-    Bs[e] = l < m ? cat_basis(a, cu.idx, l, f) : 0.f;
+  constexpr int BB = 32;
+  for (int e0 = 0; e0 < M8 * d; e0 += BB * kChainThreads) {
+    float v[BB];
+#pragma unroll
+    for (int q = 0; q < BB; ++q) {
+      const int e = e0 + tid + q * kChainThreads;
+      const int l = e / d, f = e - l * d;
+      v[q] = e < M8 * d && l < m ? cat_basis(a, cu.idx, l, f) : 0.f;
+    }
+#pragma unroll
+    for (int q = 0; q < BB; ++q) {
+      const int e = e0 + tid + q * kChainThreads;
+      if (e < M8 * d) Bs[e] = v[q];
+    }
   }
   __syncthreads();
   // P = H K^T: tile (8 rows l, 4 columns f); at most two tiles per thread (M8 <= 128)
@@ -296,21 +327,26 @@ __global__ __launch_bounds__(kChainThreads) void chain_assemble_lds(ChainArgs a)
     }
   }
   __syncthreads();
-  // G = K P: tiles (8 rows i, 8 columns j) with i0 <= j0
-  double* G = a.gram + (size_t)u * d * d;
+  // G = K P: tiles (8 rows i, 8 columns j) with i0 <= j0, one per thread (at most 136 for d <= 128); staged in LDS
+  // over H and K^T (whose reads end at the barrier) as the fp32 values the eigensolver takes, with their mirrors, then
+  // written out in whole rows
   const int nb = d / 8;
-  for (int tile = tid; tile < nb * (nb + 1) / 2; tile += kChainThreads) {
+  const int tile = tid;
+  const bool has_tile = tile < nb * (nb + 1) / 2;
+  int i0 = 0, j0 = 0;
+  double g[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) g[i][j] = 0.0;
+  if (has_tile) {
     int bi = 0, rem = tile;
     while (rem >= nb - bi) {
       rem -= nb - bi;
       ++bi;
     }
-    const int i0 = 8 * bi, j0 = 8 * (bi + rem);
-    double g[8][8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) g[i][j] = 0.0;
+    i0 = 8 * bi;
+    j0 = 8 * (bi + rem);
     for (int l = 0; l < m; ++l) {
       const float4 b0 = *reinterpret_cast<const float4*>(&Bs[l * d + i0]);
       const float4 b1 = *reinterpret_cast<const float4*>(&Bs[l * d + i0 + 4]);
@@ -323,6 +359,10 @@ __global__ __launch_bounds__(kChainThreads) void chain_assemble_lds(ChainArgs a)
 #pragma unroll
         for (int j = 0; j < 8; ++j) g[i][j] += bi8[i] * pj8[j];
     }
+  }
+  __syncthreads();
+  float* Gs = s_asm;  // [d][d]
+  if (has_tile) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
 #pragma unroll
@@ -330,15 +370,23 @@ __global__ __launch_bounds__(kChainThreads) void chain_assemble_lds(ChainArgs a)
         // the diagonal tiles are computed twice (i, j) and (j, i) with different rounding; keep the upper value
         // and mirror it so that G is exactly symmetric
         if (i0 == j0 && j < i) continue;
-        G[(i0 + i) * d + j0 + j] = g[i][j];
-        G[(j0 + j) * d + i0 + i] = g[i][j];
+        const float v = (float)g[i][j];
+        Gs[(i0 + i) * d + j0 + j] = v;
+        Gs[(j0 + j) * d + i0 + i] = v;
       }
+  }
+  __syncthreads();
+  double* G = a.gram + (size_t)u * d * d;
+  for (int e = tid; e < d * d / 2; e += kChainThreads) {
+    const float2 v = *reinterpret_cast<const float2*>(&Gs[2 * e]);
+    *reinterpret_cast<double2*>(&G[2 * e]) = make_double2((double)v.x, (double)v.y);
   }
 }
 
 size_t chain_assemble_lds_bytes(int m, int d) {
   const size_t m8 = (size_t)(m + 7) / 8 * 8;
-  return (m8 * (m8 > (size_t)d ? m8 : (size_t)d) + m8 * d) * sizeof(float);
+  const size_t hk = m8 * (m8 > (size_t)d ? m8 : (size_t)d) + m8 * d;  // H (later P) and K^T
+  return (hk > (size_t)d * d ? hk : (size_t)d * d) * sizeof(float);  // then G
 }
 
 __global__ __launch_bounds__(kChainThreads) void chain_assemble(ChainArgs a) {
