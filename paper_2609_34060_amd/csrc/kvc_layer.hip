@@ -650,25 +650,24 @@ __global__ __launch_bounds__(kLayerThreads) void sub_init(LayerFitArgs a) {
   a.y[(size_t)u * a.k * DL + e] = hash_uniform((uint32_t)u, (uint32_t)(e / DL), (uint32_t)(e % DL));
 }
 
-// Y = G X for every unit: a 128 x 64 tile (features x columns) per workgroup; thread (ti, tj) owns features
-// 8 ti .. 8 ti + 7 and columns tj + 16 j.  The next 32-wide slices of G and X are loaded into registers while the
-// current ones are used.
-// Y = G X (fp64): a kGemmRows x 64 tile of Y per workgroup of 128 threads; thread (ti, tj) accumulates the
-// entries of rows ti + 16 i and columns tj + 8 j (each LDS read of X feeds kGemmRows / 16 fmas, each read of G
-// eight; interleaved rows and columns keep the reads of a wave on distinct banks).  The next k-step's tiles are loaded into registers while this one
-// is multiplied.
-constexpr int kGemmRows = 64, kGemmCols = 64, kGemmK = 16, kGemmThreads = 128;
+// Y = G X (fp64) for every unit on the matrix cores: a 64 x 64 tile of Y (features x columns) per workgroup of four
+// waves, each wave a 32 x 32 quarter as 2 x 2 products v_mfma_f64_16x16x4_f64 (operands: lane l holds A[l % 16][l / 16]
+// and B[l / 16][l % 16]; result element v of lane l is D[l / 16 + 4 v][l % 16]).  16-wide slices of G and X are
+// staged in LDS, the next slices loaded into registers while the current ones are multiplied.
+constexpr int kGemmRows = 64, kGemmCols = 64, kGemmK = 16, kGemmThreads = 256;
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(kGemmThreads) void sub_gemm(LayerFitArgs a) {
-  constexpr int TR = kGemmRows, TC = kGemmCols, KB = kGemmK, RB = TR / 16;
+  constexpr int TR = kGemmRows, TC = kGemmCols, KB = kGemmK;
   constexpr int NG = TR * KB / kGemmThreads, NX = TC * KB / kGemmThreads;
-  __shared__ double s_g[TR][KB + 1], s_x[KB][TC + 1];
+  __shared__ double s_g[TR][KB + 1], s_x[TC][KB + 1];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
   const int f0 = blockIdx.x * TR, c0 = blockIdx.y * TC, u = blockIdx.z;
   if (a.conv[u]) return;  // whole workgroup: the unit has stopped
   const double* G = a.gram + (size_t)u * DL * DL;
   const double* X = a.x + (size_t)u * a.k * DL;
   double* Y = a.y + (size_t)u * a.k * DL;
-  const int tid = threadIdx.x, ti = tid / 8, tj = tid % 8;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1, li = lane & 15, lk = lane >> 4;
   double pg[NG], px[NX];
   auto load = [&](int k0) {
 #pragma unroll
@@ -682,11 +681,11 @@ __global__ __launch_bounds__(kGemmThreads) void sub_gemm(LayerFitArgs a) {
       px[q] = X[(size_t)(c0 + i) * DL + k0 + kk];
     }
   };
-  double acc[RB][8];
+  f64x4 acc[2][2];
 #pragma unroll
-  for (int i = 0; i < RB; ++i)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = 0.0;
+    for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
   load(0);
   for (int k0 = 0; k0 < DL; k0 += KB) {
 #pragma unroll
@@ -697,29 +696,36 @@ __global__ __launch_bounds__(kGemmThreads) void sub_gemm(LayerFitArgs a) {
 #pragma unroll
     for (int q = 0; q < NX; ++q) {
       const int e = tid + q * kGemmThreads, i = e / KB, kk = e - i * KB;
-      s_x[kk][i] = px[q];
+      s_x[i][kk] = px[q];
     }
     __syncthreads();
     if (k0 + KB < DL) load(k0 + KB);
-#pragma unroll 2
-    for (int kk = 0; kk < KB; ++kk) {
-      double g8[RB], x8[8];
 #pragma unroll
-      for (int i = 0; i < RB; ++i) g8[i] = s_g[ti + 16 * i][kk];
+    for (int kk = 0; kk < KB; kk += 4) {
+      double ga[2], xb[2];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) x8[j] = s_x[kk][tj + 8 * j];
+      for (int t = 0; t < 2; ++t) {
+        ga[t] = s_g[32 * wr + 16 * t + li][kk + lk];
+        xb[t] = s_x[32 * wc + 16 * t + li][kk + lk];
+      }
 #pragma unroll
-      for (int i = 0; i < RB; ++i)
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = fma(g8[i], x8[j], acc[i][j]);
+        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ga[i], xb[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int i = 0; i < RB; ++i)
-      if (f0 + ti + 16 * i < DL) Y[(size_t)(c0 + tj + 8 * j) * DL + f0 + ti + 16 * i] = acc[i][j];
+    for (int j = 0; j < 2; ++j) {
+      const int c = c0 + 32 * wc + 16 * j + li;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int f = f0 + 32 * wr + 16 * i + lk + 4 * v;
+        if (f < DL) Y[(size_t)c * DL + f] = acc[i][j][v];
+      }
+    }
 }
 
 // Whole-workgroup sum (fixed order: waves in order), result in every thread.
