@@ -654,11 +654,13 @@ __global__ __launch_bounds__(kLayerThreads) void sub_init(LayerFitArgs a) {
 // waves, each wave a 32 x 32 quarter as 2 x 2 products v_mfma_f64_16x16x4_f64 (operands: lane l holds A[l % 16][l / 16]
 // and B[l / 16][l % 16]; result element v of lane l is D[l / 16 + 4 v][l % 16]).  16-wide slices of G and X are
 // staged in LDS, the next slices loaded into registers while the current ones are multiplied.
-constexpr int kGemmRows = 64, kGemmCols = 64, kGemmK = 16, kGemmThreads = 256;
+constexpr int kGemmRows = 128, kGemmCols = 64, kGemmK = 16, kGemmMI = 2, kGemmNJ = 2;
+constexpr int kGemmThreads = kGemmRows / (16 * kGemmMI) * (kGemmCols / (16 * kGemmNJ)) * kWave;
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(kGemmThreads) void sub_gemm(LayerFitArgs a) {
-  constexpr int TR = kGemmRows, TC = kGemmCols, KB = kGemmK;
+  constexpr int TR = kGemmRows, TC = kGemmCols, KB = kGemmK, MI = kGemmMI, NJ = kGemmNJ;
   constexpr int NG = TR * KB / kGemmThreads, NX = TC * KB / kGemmThreads;
+  static_assert(NG * kGemmThreads == TR * KB && NX * kGemmThreads == TC * KB, "whole slices per thread");
   __shared__ double s_g[TR][KB + 1], s_x[TC][KB + 1];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
   const int f0 = blockIdx.x * TR, c0 = blockIdx.y * TC, u = blockIdx.z;
@@ -667,7 +669,8 @@ __global__ __launch_bounds__(kGemmThreads) void sub_gemm(LayerFitArgs a) {
   const double* X = a.x + (size_t)u * a.k * DL;
   double* Y = a.y + (size_t)u * a.k * DL;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave >> 1, wc = wave & 1, li = lane & 15, lk = lane >> 4;
+  constexpr int WC = TC / (16 * NJ);  // waves across the columns
+  const int wr = wave / WC, wc = wave % WC, li = lane & 15, lk = lane >> 4;
   double pg[NG], px[NX];
   auto load = [&](int k0) {
 #pragma unroll
@@ -681,11 +684,11 @@ __global__ __launch_bounds__(kGemmThreads) void sub_gemm(LayerFitArgs a) {
       px[q] = X[(size_t)(c0 + i) * DL + k0 + kk];
     }
   };
-  f64x4 acc[2][2];
+  f64x4 acc[MI][NJ];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+    for (int j = 0; j < NJ; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
   load(0);
   for (int k0 = 0; k0 < DL; k0 += KB) {
 #pragma unroll
@@ -702,27 +705,26 @@ __global__ __launch_bounds__(kGemmThreads) void sub_gemm(LayerFitArgs a) {
     if (k0 + KB < DL) load(k0 + KB);
 #pragma unroll
     for (int kk = 0; kk < KB; kk += 4) {
-      double ga[2], xb[2];
+      double ga[MI], xb[NJ];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        ga[t] = s_g[32 * wr + 16 * t + li][kk + lk];
-        xb[t] = s_x[32 * wc + 16 * t + li][kk + lk];
-      }
+      for (int t = 0; t < MI; ++t) ga[t] = s_g[16 * (MI * wr + t) + li][kk + lk];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int t = 0; t < NJ; ++t) xb[t] = s_x[16 * (NJ * wc + t) + li][kk + lk];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ga[i], xb[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ga[i], xb[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int c = c0 + 32 * wc + 16 * j + li;
+    for (int j = 0; j < NJ; ++j) {
+      const int c = c0 + 16 * (NJ * wc + j) + li;
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int f = f0 + 32 * wr + 16 * i + lk + 4 * v;
+        const int f = f0 + 16 * (MI * wr + i) + lk + 4 * v;
         if (f < DL) Y[(size_t)c * DL + f] = acc[i][j][v];
       }
     }
