@@ -933,9 +933,16 @@ __global__ __launch_bounds__(kWave) void cqr_factor(LayerFitArgs a, int shifted)
   }
 }
 
-// k = 64 with every value in registers: lane c holds column c of S (entries k <= c are used), the pivots and the
-// entries of row j of R come from their lanes by readlane, and lane i forms row i of R^{-1} from
-// W[i][j] = -(sum_{i <= l < j} W[i][l] R[l][j]) / R[j][j].  Same arithmetic as cqr_factor, no LDS round trips.
+// k = 64, one wave: lane c holds column c of S in registers (entries k <= c are used).  Step j takes the pivot from
+// lane j, every lane forms its entry R[j][c] and writes it to row j of R in LDS, and the trailing update reads that
+// row back as broadcast loads (two entries per load) instead of one readlane pair per entry.  Lane i then forms
+// row i of R^{-1} from W[i][j] = -(sum_{i <= l < j} W[i][l] R[l][j]) / R[j][j], the column of R read from LDS.
+// Orders one wave's LDS accesses around points where lanes read values other lanes wrote.
+__device__ __forceinline__ void wave_lds_sync_layer() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 __device__ __forceinline__ double readlane_f64(double v, int lane) {
   const uint64_t b = __builtin_bit_cast(uint64_t, v);
   const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)b, lane), hi = __builtin_amdgcn_readlane((uint32_t)(b >> 32), lane);
@@ -943,7 +950,8 @@ __device__ __forceinline__ double readlane_f64(double v, int lane) {
 }
 
 __global__ __launch_bounds__(kWave) void cqr_factor_reg64(LayerFitArgs a, int shifted) {
-  constexpr int K = 64;
+  constexpr int K = 64, KP = K + 2;  // row stride: even, so that 16-byte loads stay aligned
+  __shared__ __attribute__((aligned(16))) double s_r[K * KP];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
   const int u = blockIdx.x, lane = threadIdx.x;
   if (a.conv[u]) return;  // whole wave: the unit has stopped
@@ -971,25 +979,43 @@ __global__ __launch_bounds__(kWave) void cqr_factor_reg64(LayerFitArgs a, int sh
     const double d = readlane_f64(col[j], j);
     const double rjj = sqrt(d > 1e-300 ? d : 1e-300);
     col[j] = lane == j ? rjj : col[j] / rjj;
+    s_r[j * KP + lane] = col[j];
+    wave_lds_sync_layer();
 #pragma unroll
-    for (int k = j + 1; k < K; ++k) col[k] -= readlane_f64(col[j], k) * col[j];
+    for (int k = j + 1; k < K; k += 2) {
+      if (k + 1 < K) {
+        const double2 rk = *reinterpret_cast<const double2*>(&s_r[j * KP + k]);
+        col[k] -= rk.x * col[j];
+        col[k + 1] -= rk.y * col[j];
+      } else {
+        col[k] -= s_r[j * KP + k] * col[j];
+      }
+    }
   }
-  // terms with l < lane are skipped (selected, so an overflowed entry of R cannot turn 0 * inf into NaN)
+  // W = R^{-1} by columns: lane c solves R w = e_c upwards, w_i = (delta_ic - sum_{i < m <= c} R[i][m] w_m) / R[i][i]
+  // for i <= c (0 below the diagonal), with row i of R read from LDS
   double w[K];
 #pragma unroll
-  for (int j = 0; j < K; ++j) {
-    const double rjj = readlane_f64(col[j], j);
+  for (int i = K - 1; i >= 0; --i) {
     double s = 0.0;
 #pragma unroll
-    for (int l = 0; l < j; ++l) {
-      const double x = w[l] * readlane_f64(col[l], j);
-      s += lane <= l ? x : 0.0;
+    for (int m = i + 1; m < K; m += 2) {
+      // terms with m > c (where w_m = 0) are dropped by selecting the entry of R, so that an overflowed entry of
+      // R cannot turn 0 * inf into NaN
+      if (m + 1 < K) {
+        const double2 rm = *reinterpret_cast<const double2*>(&s_r[i * KP + m]);
+        s = fma(m <= lane ? rm.x : 0.0, w[m], s);
+        s = fma(m + 1 <= lane ? rm.y : 0.0, w[m + 1], s);
+      } else {
+        s = fma(m <= lane ? s_r[i * KP + m] : 0.0, w[m], s);
+      }
     }
-    w[j] = lane == j ? 1.0 / rjj : (lane < j ? -s / rjj : 0.0);
+    w[i] = i <= lane ? ((lane == i ? 1.0 : 0.0) - s) / s_r[i * KP + i] : 0.0;
   }
-  double* W = a.hmat + (size_t)u * K * K + (size_t)lane * K;
+  // row-major W[i][c]: one row per store instruction
+  double* W = a.hmat + (size_t)u * K * K;
 #pragma unroll
-  for (int j = 0; j < K; ++j) W[j] = w[j];
+  for (int i = 0; i < K; ++i) W[(size_t)i * K + lane] = w[i];
 }
 
 size_t cqr_factor_lds(int k) { return (size_t)k * (k + 1) * sizeof(double); }
