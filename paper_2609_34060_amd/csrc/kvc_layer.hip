@@ -792,19 +792,24 @@ __global__ __launch_bounds__(kScaleThreads) void cqr_scale(LayerFitArgs a) {
 template <int K>
 __global__ __launch_bounds__(kCqrThreads) void cqr_syrk(LayerFitArgs a, const double* __restrict__ src, int perturb,
                                                          uint32_t round) {
-  constexpr int B = K / 16;
+  // the partial S = Y_c Y_c^T of 256 features on the matrix cores: each of the four waves takes a K/2 x K/2 quadrant
+  // as (K/32)^2 products v_mfma_f64_16x16x4_f64 (lane layouts as in sub_gemm), both operands read from the staged
+  // slice of Y
+  constexpr int T = K / 32;
+  static_assert(kCqrThreads == 4 * kWave, "four waves, one quadrant each");
   __shared__ double tile[K][kCqrSub + 1];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
-  const int chunk = blockIdx.x, u = blockIdx.y, tid = threadIdx.x, bi = tid / 16, bj = tid % 16;
+  const int chunk = blockIdx.x, u = blockIdx.y, tid = threadIdx.x;
   if (a.conv[u]) return;  // whole workgroup: the unit has stopped
+  const int lane = tid & 63, wave = tid >> 6, qi = wave >> 1, qj = wave & 1, li = lane & 15, lk = lane >> 4;
   const int f_begin = chunk * kCqrChunk, f_end = min(DL, f_begin + kCqrChunk);
   const double* Y = src + (size_t)u * K * DL;
   const double eps = perturb ? a.eps[u] : 0.0;
-  double acc[B][B];
+  f64x4 acc[T][T];
 #pragma unroll
-  for (int i = 0; i < B; ++i)
+  for (int i = 0; i < T; ++i)
 #pragma unroll
-    for (int j = 0; j < B; ++j) acc[i][j] = 0.0;
+    for (int j = 0; j < T; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
   for (int f0 = f_begin; f0 < f_end; f0 += kCqrSub) {
     for (int e = tid; e < K * kCqrSub; e += kCqrThreads) {
       const int c = e / kCqrSub, ff = e - c * kCqrSub;
@@ -813,26 +818,29 @@ __global__ __launch_bounds__(kCqrThreads) void cqr_syrk(LayerFitArgs a, const do
       tile[c][ff] = perturb ? cqr_perturbed(y, eps, round, u, idx) : y;
     }
     __syncthreads();
-#pragma unroll 4
-    for (int ff = 0; ff < kCqrSub; ++ff) {
-      double xi[B], xj[B];
 #pragma unroll
-      for (int i = 0; i < B; ++i) {
-        xi[i] = tile[bi * B + i][ff];
-        xj[i] = tile[bj * B + i][ff];
+    for (int kk = 0; kk < kCqrSub; kk += 4) {
+      double ya[T], yb[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        ya[t] = tile[qi * (K / 2) + 16 * t + li][kk + lk];
+        yb[t] = tile[qj * (K / 2) + 16 * t + li][kk + lk];
       }
 #pragma unroll
-      for (int i = 0; i < B; ++i)
+      for (int i = 0; i < T; ++i)
 #pragma unroll
-        for (int j = 0; j < B; ++j) acc[i][j] = fma(xi[i], xj[j], acc[i][j]);
+        for (int j = 0; j < T; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ya[i], yb[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
   double* P = a.spart + ((size_t)u * nch + chunk) * K * K;
 #pragma unroll
-  for (int i = 0; i < B; ++i)
+  for (int i = 0; i < T; ++i)
 #pragma unroll
-    for (int j = 0; j < B; ++j) P[(bi * B + i) * K + bj * B + j] = acc[i][j];
+    for (int j = 0; j < T; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        P[(qi * (K / 2) + 16 * i + lk + 4 * v) * K + qj * (K / 2) + 16 * j + li] = acc[i][j][v];
 }
 
 // One wave per unit; S in LDS with rows padded to K + 1.  Cholesky (upper, S = R^T R; a pivot that is not positive is
@@ -1023,17 +1031,15 @@ size_t cqr_apply_lds(int k) {
   return ((size_t)k * (kCqrRows + 1) + (size_t)kCqrWChunk * k) * sizeof(double);
 }
 
-// dst = (src (+ perturbation)) R^{-1} for 64 features: thread (ti, tj) owns features 4 ti .. 4 ti + 3 and columns
-// tj + 16 n; R^{-1} is streamed through LDS 32 rows at a time.
+// dst = (src (+ perturbation)) R^{-1} for 64 features; R^{-1} is streamed through LDS 32 rows at a time.
 template <int K>
 __global__ __launch_bounds__(kCqrThreads) void cqr_apply(LayerFitArgs a, const double* src, double* dst, int perturb,
                                                           uint32_t round) {
-  constexpr int NJ = K / 16;
   extern __shared__ double as_[];
   double* ty = as_;                          // [K][kCqrRows + 1]
   double* tw = as_ + K * (kCqrRows + 1);     // [kCqrWChunk][K]
   const int DL = a.pv.num_kv_heads * a.pv.head_dim;
-  const int f0 = blockIdx.x * kCqrRows, u = blockIdx.y, tid = threadIdx.x, ti = tid / 16, tj = tid % 16;
+  const int f0 = blockIdx.x * kCqrRows, u = blockIdx.y, tid = threadIdx.x;
   if (a.conv[u]) return;  // whole workgroup: the unit has stopped
   const double* Y = src + (size_t)u * K * DL;
   const double* W = a.hmat + (size_t)u * K * K;
@@ -1044,33 +1050,40 @@ __global__ __launch_bounds__(kCqrThreads) void cqr_apply(LayerFitArgs a, const d
     const double y = Y[idx];
     ty[c * (kCqrRows + 1) + ff] = perturb ? cqr_perturbed(y, eps, round, u, idx) : y;
   }
-  double acc[4][NJ];
+  // on the matrix cores: wave (qi, qj) takes features 32 qi .. 32 qi + 31 and columns (K / 2) qj .. as 2 x K / 32
+  // products v_mfma_f64_16x16x4_f64 (lane layouts as in sub_gemm)
+  constexpr int NT = K / 32;
+  const int lane = tid & 63, wave = tid >> 6, qi = wave >> 1, qj = wave & 1, li = lane & 15, lk = lane >> 4;
+  f64x4 acc[2][NT];
 #pragma unroll
-  for (int f = 0; f < 4; ++f)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int n = 0; n < NJ; ++n) acc[f][n] = 0.0;
+    for (int j = 0; j < NT; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
   for (int i0 = 0; i0 < K; i0 += kCqrWChunk) {
     __syncthreads();
     for (int e = tid; e < kCqrWChunk * K; e += kCqrThreads) tw[e] = W[(size_t)i0 * K + e];
     __syncthreads();
-#pragma unroll 4
-    for (int ii = 0; ii < kCqrWChunk; ++ii) {
-      double y4[4], w[NJ];
 #pragma unroll
-      for (int f = 0; f < 4; ++f) y4[f] = ty[(i0 + ii) * (kCqrRows + 1) + 4 * ti + f];
+    for (int kk = 0; kk < kCqrWChunk; kk += 4) {
+      double ya[2], wb[NT];
 #pragma unroll
-      for (int n = 0; n < NJ; ++n) w[n] = tw[ii * K + tj + 16 * n];
+      for (int t = 0; t < 2; ++t) ya[t] = ty[(i0 + kk + lk) * (kCqrRows + 1) + 32 * qi + 16 * t + li];
 #pragma unroll
-      for (int f = 0; f < 4; ++f)
+      for (int t = 0; t < NT; ++t) wb[t] = tw[(kk + lk) * K + (K / 2) * qj + 16 * t + li];
 #pragma unroll
-        for (int n = 0; n < NJ; ++n) acc[f][n] = fma(y4[f], w[n], acc[f][n]);
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ya[i], wb[j], acc[i][j], 0, 0, 0);
     }
   }
   double* X = dst + (size_t)u * K * DL;
 #pragma unroll
-  for (int n = 0; n < NJ; ++n)
+  for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int f = 0; f < 4; ++f) X[(size_t)(tj + 16 * n) * DL + f0 + 4 * ti + f] = acc[f][n];
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        X[(size_t)((K / 2) * qj + 16 * j + li) * DL + f0 + 32 * qi + 16 * i + lk + 4 * v] = acc[i][j][v];
 }
 
 // Rayleigh-Ritz matrix H = (X^T Y + Y^T X) / 2 with Y = G X: one 256-thread workgroup per unit, B x B register
