@@ -1086,56 +1086,74 @@ __global__ __launch_bounds__(kCqrThreads) void cqr_apply(LayerFitArgs a, const d
         X[(size_t)((K / 2) * qj + 16 * j + li) * DL + f0 + 32 * qi + 16 * i + lk + 4 * v] = acc[i][j][v];
 }
 
-// Rayleigh-Ritz matrix H = (X^T Y + Y^T X) / 2 with Y = G X: one 256-thread workgroup per unit, B x B register
-// blocks of X^T Y over LDS tiles of the rows of X and Y.
+// Rayleigh-Ritz matrix H = (X^T Y + Y^T X) / 2 with Y = G X, in two steps: the partials X_c^T Y_c of 256 features
+// per workgroup on the matrix cores (the layout of cqr_syrk, with X rows as the A operand and Y rows as B), written
+// over the unit's Cholesky QR partials (idle until the next iteration; Y is kept for the residual check); then one
+// workgroup per unit sums them in chunk order and takes the symmetric part.
 template <int K>
 __global__ __launch_bounds__(kCqrThreads) void sub_rayleigh(LayerFitArgs a) {
-  constexpr int B = K / 16;
-  __shared__ double tx[K][kCqrTile + 1], ty[K][kCqrTile + 1];
-  const int DL = a.pv.num_kv_heads * a.pv.head_dim;
-  const int u = blockIdx.x, tid = threadIdx.x, bi = tid / 16, bj = tid % 16;
+  constexpr int T = K / 32;
+  constexpr int SW = K > 64 ? kCqrSub / 2 : kCqrSub;  // slice width: both slices within 64 KB of LDS
+  __shared__ double tx[K][SW + 1], ty[K][SW + 1];
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
+  const int chunk = blockIdx.x, u = blockIdx.y, tid = threadIdx.x;
   if (a.conv[u]) return;  // whole workgroup: the unit has stopped
+  const int lane = tid & 63, wave = tid >> 6, qi = wave >> 1, qj = wave & 1, li = lane & 15, lk = lane >> 4;
+  const int f_begin = chunk * kCqrChunk, f_end = min(DL, f_begin + kCqrChunk);
   const double* X = a.x + (size_t)u * K * DL;
   const double* Y = a.y + (size_t)u * K * DL;
-  double* Hm = a.hmat + (size_t)u * K * K;
-  double acc[B][B];
+  f64x4 acc[T][T];
 #pragma unroll
-  for (int i = 0; i < B; ++i)
+  for (int i = 0; i < T; ++i)
 #pragma unroll
-    for (int j = 0; j < B; ++j) acc[i][j] = 0.0;
-  for (int f0 = 0; f0 < DL; f0 += kCqrTile) {
-    for (int e = tid; e < K * kCqrTile; e += kCqrThreads) {
-      const int c = e / kCqrTile, ff = e - c * kCqrTile;
+    for (int j = 0; j < T; ++j) acc[i][j] = f64x4{0.0, 0.0, 0.0, 0.0};
+  for (int f0 = f_begin; f0 < f_end; f0 += SW) {
+    for (int e = tid; e < K * SW; e += kCqrThreads) {
+      const int c = e / SW, ff = e - c * SW;
       tx[c][ff] = X[(size_t)c * DL + f0 + ff];
       ty[c][ff] = Y[(size_t)c * DL + f0 + ff];
     }
     __syncthreads();
-#pragma unroll 4
-    for (int ff = 0; ff < kCqrTile; ++ff) {
-      double xi[B], yj[B];
 #pragma unroll
-      for (int i = 0; i < B; ++i) {
-        xi[i] = tx[bi * B + i][ff];
-        yj[i] = ty[bj * B + i][ff];
+    for (int kk = 0; kk < SW; kk += 4) {
+      double xa[T], yb[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        xa[t] = tx[qi * (K / 2) + 16 * t + li][kk + lk];
+        yb[t] = ty[qj * (K / 2) + 16 * t + li][kk + lk];
       }
 #pragma unroll
-      for (int i = 0; i < B; ++i)
+      for (int i = 0; i < T; ++i)
 #pragma unroll
-        for (int j = 0; j < B; ++j) acc[i][j] = fma(xi[i], yj[j], acc[i][j]);
+        for (int j = 0; j < T; ++j) acc[i][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(xa[i], yb[j], acc[i][j], 0, 0, 0);
     }
     __syncthreads();
   }
-  // X^T Y into the unit's Cholesky QR partials (idle until the next iteration; Y = G X is kept for the residual
-  // check), then the symmetric part
-  double* raw = a.spart + (size_t)u * ((DL + kCqrChunk - 1) / kCqrChunk) * K * K;
+  double* P = a.spart + ((size_t)u * nch + chunk) * K * K;
 #pragma unroll
-  for (int i = 0; i < B; ++i)
+  for (int i = 0; i < T; ++i)
 #pragma unroll
-    for (int j = 0; j < B; ++j) raw[(bi * B + i) * K + bj * B + j] = acc[i][j];
-  __syncthreads();
-  for (int e = tid; e < K * K; e += kCqrThreads) {
+    for (int j = 0; j < T; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        P[(qi * (K / 2) + 16 * i + lk + 4 * v) * K + qj * (K / 2) + 16 * j + li] = acc[i][j][v];
+}
+
+template <int K>
+__global__ __launch_bounds__(kCqrThreads) void sub_rayleigh_sum(LayerFitArgs a) {
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
+  const int u = blockIdx.x;
+  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
+  const double* P = a.spart + (size_t)u * nch * K * K;
+  double* Hm = a.hmat + (size_t)u * K * K;
+  for (int e = threadIdx.x; e < K * K; e += kCqrThreads) {
     const int i = e / K, j = e - i * K;
-    Hm[e] = 0.5 * (raw[i * K + j] + raw[j * K + i]);
+    double sij = 0.0, sji = 0.0;
+    for (int c = 0; c < nch; ++c) {
+      sij += P[(size_t)c * K * K + i * K + j];
+      sji += P[(size_t)c * K * K + j * K + i];
+    }
+    Hm[e] = 0.5 * (sij + sji);
   }
 }
 
@@ -1566,8 +1584,13 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
     }
     // Rayleigh-Ritz on span(X) and the residuals of its top-r pairs (Y = G X is kept by the Ritz step)
     hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kGemmThreads), 0, stream, a);
-    if (a.k == 64) hipLaunchKernelGGL(sub_rayleigh<64>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
-    else hipLaunchKernelGGL(sub_rayleigh<128>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
+    if (a.k == 64) {
+      hipLaunchKernelGGL(sub_rayleigh<64>, sgrid, dim3(kCqrThreads), 0, stream, a);
+      hipLaunchKernelGGL(sub_rayleigh_sum<64>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
+    } else {
+      hipLaunchKernelGGL(sub_rayleigh<128>, sgrid, dim3(kCqrThreads), 0, stream, a);
+      hipLaunchKernelGGL(sub_rayleigh_sum<128>, dim3(a.num_units), dim3(kCqrThreads), 0, stream, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((e = launch_eig(es, stream)) != hipSuccess) return e;
