@@ -7,8 +7,9 @@
 //      targets (every lane's shifts cut the whole interval), then groups of lanes per eigenvalue, kBisShifts
 //      shifts per lane, one ballot per shift.
 //   4. Inverse iteration on T (LDL^T without pivoting, tiny pivots replaced) from pseudo-random starts, one lane
-//      per eigenvector; then modified Gram-Schmidt over the r vectors.  Vectors of tightly clustered eigenvalues
-//      come out as an orthonormal basis of the cluster's invariant subspace (where the SVD itself is not unique).
+//      per eigenvector; then modified Gram-Schmidt within each cluster of close eigenvalues.  Vectors of tightly
+//      clustered eigenvalues come out as an orthonormal basis of the cluster's invariant subspace (where the SVD
+//      itself is not unique).
 //   5. Back-transformation by the reflectors, canonical sign (largest-magnitude entry positive, first index on
 //      near-ties), basis rows and sigma = sqrt(lambda) written to the state.
 #include <algorithm>
@@ -141,7 +142,10 @@ __device__ __forceinline__ double recip(double q) {
 // Scalars of one Householder step from x_0 and s = ||x||^2: out = {alpha, v_0, beta} with alpha = -sign(x_0) ||x||,
 // v = x - alpha e_1 and beta = 2 / v^T v = 1 / (||x|| (||x|| + |x_0|)) (0 when x = 0: the step is the identity).
 __device__ __forceinline__ void reflector_scalars(double x0, double s, double* out) {
-  const double nrm = sqrt(s);
+  // ||x|| from the hardware reciprocal square root and one Newton step (s is 0 or a normal number)
+  const double y0 = __builtin_amdgcn_rsq(s);
+  const double g0 = s * y0, h0 = 0.5 * y0;
+  const double nrm = s == 0.0 ? 0.0 : fma(g0, fma(-g0, h0, 0.5), g0);
   const double alpha = nrm == 0.0 ? 0.0 : -copysign(nrm, x0);
   out[0] = alpha;
   out[1] = x0 - alpha;
@@ -287,13 +291,28 @@ __device__ __forceinline__ void tri_reduce(float* A, float4* s_vw, double* share
           pf[c] = fmaf(a[j][c], vw[j].z, pf[c]);
         }
     }
-    for (; R < N; R += W) {
-      const float4 vw = s_vw[R];
+    if (R < N) {
+      // the last 1 - 3 rows, loaded together (a missing row re-reads row R and is neither stored nor counted)
+      const int m = (N - 1 - R) / W + 1;
+      float4 vw[3];
+      float a[3][CPL];
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        const float a = upd(A[R * N + CPL * lane + c], vw, c);
-        A[R * N + CPL * lane + c] = a;
-        pf[c] = fmaf(a, vw.z, pf[c]);
+      for (int j = 0; j < 3; ++j) {
+        const int Rj = j < m ? R + j * W : R;
+        vw[j] = s_vw[Rj];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) a[j][c] = A[Rj * N + CPL * lane + c];
+      }
+#pragma unroll
+      for (int j = 0; j < 3; ++j) {
+        if (j < m) {
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) {
+            a[j][c] = upd(a[j][c], vw[j], c);
+            A[(R + j * W) * N + CPL * lane + c] = a[j][c];
+            pf[c] = fmaf(a[j][c], vw[j].z, pf[c]);
+          }
+        }
       }
     }
     double* sh = share + (k & 1) * W * N;
@@ -637,29 +656,40 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
     for (int e = tid; e < r * N; e += kEigThreads) X[e] = (float)gvec[e];
     __syncthreads();
 
-    // modified Gram-Schmidt, one barrier per vector: the wave that takes vector j + 1 in round j (wave 0) also
-    // normalises it, so vector j is normalised when round j starts
+    // modified Gram-Schmidt within clusters, one barrier per vector that has a later cluster member: the wave that
+    // takes vector j + 1 in round j (wave 0) also normalises it, so vector j is normalised when round j starts
     constexpr int QN = N / kWave;
     auto normalise = [&](float* x) {
       double s = 0.0;
 #pragma unroll
       for (int q = 0; q < QN; ++q) s += (double)x[q] * x[q];
       s = wave_sum(s);
-      const double f = 1.0 / sqrt(s);
+      // 1 / sqrt(s) from the hardware reciprocal square root and one Newton step
+      const double y0 = __builtin_amdgcn_rsq(s);
+      const double f = y0 * fma(-0.5 * s * y0, y0, 1.5);
 #pragma unroll
       for (int q = 0; q < QN; ++q) x[q] = (float)(x[q] * f);
     };
-    if (wave == 0) {
-      float x[QN];
-#pragma unroll
-      for (int q = 0; q < QN; ++q) x[q] = X[lane + kWave * q];
-      normalise(x);
-#pragma unroll
-      for (int q = 0; q < QN; ++q) X[lane + kWave * q] = x[q];
-    }
-    __syncthreads();
+    // Clusters: runs of eigenvalues whose consecutive gaps are at most 1e-3 of the norm of T (the reorthogonalisation
+    // criterion of LAPACK's inverse iteration, stein).  A vector is orthogonalised against the earlier vectors of its
+    // cluster only: the bisection's eigenvalues lie within about 2^-24 of the norm of T of the exact ones, so each
+    // inverse-iteration solve scales a vector's components along eigenvectors at least 1e-3 away by at most
+    // 2^-24 / 1e-3 relative to its own, and the two solves leave vectors of different clusters orthogonal to about
+    // 4e-9 of the start's components.  The first vector of a cluster keeps the inverse iteration's normalisation.
+    // Bit j of the mask: vectors j and j + 1 share a cluster.
+    const double ctol = 1e-3 * tnorm;
+    static_assert(KVC_MAX_RANK <= 2 * kWave, "two mask words");
+    const uint64_t m0 = __ballot(lane + 1 < r && s_lam[lane] - s_lam[lane + 1] <= ctol);
+    const uint64_t m1 = __ballot(lane + kWave + 1 < r && s_lam[lane + kWave] - s_lam[lane + kWave + 1] <= ctol);
+    auto joined = [&](int j) { return ((j < kWave ? m0 >> j : m1 >> (j - kWave)) & 1ull) != 0; };
+    int cend = 0;  // last index of the cluster of vector j (uniform)
     for (int j = 0; j < r; ++j) {
-      for (int k = j + 1 + wave; k < r; k += kEigWaves) {
+      if (!joined(j)) continue;
+      if (cend <= j) {
+        cend = j + 1;
+        while (joined(cend)) ++cend;
+      }
+      for (int k = j + 1 + wave; k <= cend; k += kEigWaves) {
         float xj[QN], xk[QN];
         double s = 0.0;
 #pragma unroll

@@ -222,6 +222,38 @@ def test_fit_batched_items_different_ranks_and_lengths():
     _compare_states(states, raw, "bf16")
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_fit_clustered_eigenvalues_fp32(d):
+    """Gram spectra with an exact triple and pairs of eigenvalues 4e-4 to 6e-3 of the largest apart, on both sides of
+    the eigensolver's cluster tolerance (consecutive eigenvalues within 1e-3 of the norm of T are orthogonalised
+    together; the others rely on inverse iteration alone), and a clear gap at the truncation so that the rank-r
+    product is unique: the basis rows must be orthonormal to 2e-6 and the fit must match the oracle at the fp32
+    bars."""
+    H, T, r = 2, 512, 16
+    w = synth.WORKLOADS["tiny"].with_(num_layers=1, num_kv_heads=H, head_dim=d, seq_tokens=(T,), rank=r)
+    pc = synth.build_paged(w, device="cuda", num_output_agents=1)
+    src, dst = pc.seqs[(0, 0)], pc.seqs[(0, 1)]
+    lam = torch.tensor([1.0, 1.0, 1.0, 0.95, 0.95 - 4e-4, 0.9, 0.9 - 1.5e-3, 0.85, 0.85 - 3e-3, 0.8, 0.8 - 6e-3,
+                        0.75, 0.7, 0.7 - 8e-4, 0.65, 0.6, 0.3, 0.3, 0.25, 0.2], dtype=torch.float64)
+    assert len(lam) > r and lam[r - 1] > 1.5 * lam[r]
+    g = torch.Generator().manual_seed(211)
+    t = torch.arange(T) + src.offset
+    td = torch.arange(T) + dst.offset
+    for pools in (pc.k_pools, pc.v_pools):
+        pool = pools[0]
+        for h in range(H):
+            u = torch.linalg.qr(torch.randn(T, len(lam), generator=g, dtype=torch.float64))[0]
+            v = torch.linalg.qr(torch.randn(d, len(lam), generator=g, dtype=torch.float64))[0]
+            z = (u * (10.0 * lam.sqrt())) @ v.T
+            x = pool[t // w.block_size, t % w.block_size, h].to("cpu", torch.float64)
+            pool[td // w.block_size, td % w.block_size, h] = (x + z).to(pool.dtype).to(pool.device)
+    states, ostates, raw, cnp, items, tabs = _fit_both(pc, [((0, 0), (0, 1))], [r])
+    wp, ws = _compare_states(states, raw, "f32")
+    worst, teeth = _apply_compare(pc, states, ostates, items, tabs, (0, 100))
+    print(f"clustered d {d}: prod {wp:.2e} sigma {ws:.2e} cache {worst:.2e} (uncorrected {teeth:.2e})")
+    assert teeth > 10 * TOL_CACHE["f32"]
+
+
 def test_fit_is_deterministic():
     w = synth.WORKLOADS["llama8b_4k"].with_(num_layers=1, num_kv_heads=2, seq_tokens=(2000,), num_agents=2)
     pc = synth.build_paged(w, device="cuda")
