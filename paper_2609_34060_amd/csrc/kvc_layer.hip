@@ -941,10 +941,12 @@ __global__ __launch_bounds__(kWave) void cqr_factor(LayerFitArgs a, int shifted)
   }
 }
 
-// k = 64, one wave: lane c holds column c of S in registers (entries k <= c are used).  Step j takes the pivot from
-// lane j, every lane forms its entry R[j][c] and writes it to row j of R in LDS, and the trailing update reads that
-// row back as broadcast loads (two entries per load) instead of one readlane pair per entry.  Lane i then forms
-// row i of R^{-1} from W[i][j] = -(sum_{i <= l < j} W[i][l] R[l][j]) / R[j][j], the column of R read from LDS.
+// k = 64: wave 0 factorises, lane c holding column c of S in registers (entries k <= c are used).  Step j takes the
+// pivot from lane j, every lane forms its entry R[j][c] and writes it to row j of R in LDS, and the trailing update
+// reads that row back as broadcast loads (two entries per load) instead of one readlane pair per entry.  All four
+// waves then form R^{-1} by back substitution, four lanes per column: with one lane per column the 64 accumulators
+// of a lane left no registers to batch the inverse's LDS loads, which the compiler then waited on one at a time
+// (67 us per launch at 8B/32K against 35 us now).
 // Orders one wave's LDS accesses around points where lanes read values other lanes wrote.
 __device__ __forceinline__ void wave_lds_sync_layer() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -957,73 +959,111 @@ __device__ __forceinline__ double readlane_f64(double v, int lane) {
   return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 
-__global__ __launch_bounds__(kWave) void cqr_factor_reg64(LayerFitArgs a, int shifted) {
+// 64-bit broadcast of lane SEL of every quad (DPP quad_perm [SEL, SEL, SEL, SEL]; all lanes active).
+template <int SEL>
+__device__ __forceinline__ double quad_bcast_f64(double x) {
+  constexpr int ctrl = SEL * 0x55;
+  const unsigned long long b = __builtin_bit_cast(unsigned long long, x);
+  const int lo = __builtin_amdgcn_mov_dpp((int)(unsigned)b, ctrl, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(unsigned)(b >> 32), ctrl, 0xF, 0xF, false);
+  return __builtin_bit_cast(double, ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
+}
+
+constexpr int kCqrFactorThreads = 256;
+
+__global__ __launch_bounds__(kCqrFactorThreads) void cqr_factor_reg64(LayerFitArgs a, int shifted) {
   constexpr int K = 64, KP = K + 2;  // row stride: even, so that 16-byte loads stay aligned
-  __shared__ __attribute__((aligned(16))) double s_r[K * KP];
+  __shared__ __attribute__((aligned(16))) double s_r[K * KP];  // rows of R (the factorisation)
+  __shared__ __attribute__((aligned(16))) double s_c[K * KP];  // columns of R above the diagonal, 0 on and below it
+  __shared__ double s_ri[K];                                   // 1 / R[j][j]
   const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
-  const int u = blockIdx.x, lane = threadIdx.x;
-  if (a.conv[u]) return;  // whole wave: the unit has stopped
-  const double* P = a.spart + (size_t)u * nch * K * K;
-  double col[K];
+  const int u = blockIdx.x, tid = threadIdx.x;
+  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
+  if (tid < kWave) {
+    // the factorisation, by wave 0: lane c holds column c of S
+    const int lane = tid;
+    const double* P = a.spart + (size_t)u * nch * K * K;
+    double col[K];
+    double myinv = 0.0;  // 1 / R[lane][lane]
 #pragma unroll
-  for (int k = 0; k < K; ++k) col[k] = 0.0;
-  for (int p = 0; p < nch; ++p)
+    for (int k = 0; k < K; ++k) col[k] = 0.0;
+    for (int p = 0; p < nch; ++p)
 #pragma unroll
-    for (int k = 0; k < K; ++k) col[k] += P[(size_t)p * K * K + k * K + lane];
-  if (shifted) {
-    double d = 0.0;
+      for (int k = 0; k < K; ++k) col[k] += P[(size_t)p * K * K + k * K + lane];
+    if (shifted) {
+      double d = 0.0;
 #pragma unroll
-    for (int k = 0; k < K; ++k) d = k == lane ? col[k] : d;
-    double tr = 0.0;
+      for (int k = 0; k < K; ++k) d = k == lane ? col[k] : d;
+      double tr = 0.0;
 #pragma unroll
-    for (int c = 0; c < K; ++c) tr += readlane_f64(d, c);
-    const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
+      for (int c = 0; c < K; ++c) tr += readlane_f64(d, c);
+      const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
 #pragma unroll
-    for (int k = 0; k < K; ++k) col[k] += k == lane ? shift : 0.0;
-  }
-  // entries below the diagonal of a lane's column are updated too but never read
+      for (int k = 0; k < K; ++k) col[k] += k == lane ? shift : 0.0;
+    }
+    // entries below the diagonal of a lane's column are updated too but never read.  Pivots: 1 / sqrt from the
+    // hardware reciprocal square root and one Newton step (relative error about 2^-47), R[j][j] = d / sqrt(d) and
+    // row j of R = the column entries times 1 / sqrt(d).
 #pragma unroll
-  for (int j = 0; j < K; ++j) {
-    const double d = readlane_f64(col[j], j);
-    const double rjj = sqrt(d > 1e-300 ? d : 1e-300);
-    col[j] = lane == j ? rjj : col[j] / rjj;
-    s_r[j * KP + lane] = col[j];
-    wave_lds_sync_layer();
+    for (int j = 0; j < K; ++j) {
+      const double d0 = readlane_f64(col[j], j);
+      const double d = d0 > 1e-300 ? d0 : 1e-300;
+      const double y0 = __builtin_amdgcn_rsq(d);
+      const double inv = y0 * fma(-0.5 * d * y0, y0, 1.5);
+      col[j] = lane == j ? d * inv : col[j] * inv;
+      myinv = lane == j ? inv : myinv;
+      s_r[j * KP + lane] = col[j];
+      wave_lds_sync_layer();
 #pragma unroll
-    for (int k = j + 1; k < K; k += 2) {
-      if (k + 1 < K) {
-        const double2 rk = *reinterpret_cast<const double2*>(&s_r[j * KP + k]);
-        col[k] -= rk.x * col[j];
-        col[k + 1] -= rk.y * col[j];
-      } else {
-        col[k] -= s_r[j * KP + k] * col[j];
+      for (int k = j + 1; k < K; k += 2) {
+        if (k + 1 < K) {
+          const double2 rk = *reinterpret_cast<const double2*>(&s_r[j * KP + k]);
+          col[k] -= rk.x * col[j];
+          col[k + 1] -= rk.y * col[j];
+        } else {
+          col[k] -= s_r[j * KP + k] * col[j];
+        }
       }
     }
+    // column c of R (lane c) for the inverse, clamped to finite values so that a zero never meets an infinity
+#pragma unroll
+    for (int i = 0; i < K; ++i)
+      s_c[lane * KP + i] = i < lane ? fmin(fmax(col[i], -1.7976931348623157e308), 1.7976931348623157e308) : 0.0;
+    s_ri[lane] = myinv;
   }
-  // W = R^{-1} by columns: lane c solves R w = e_c upwards, w_i = (delta_ic - sum_{i < m <= c} R[i][m] w_m) / R[i][i]
-  // for i <= c (0 below the diagonal), with row i of R read from LDS
-  double w[K];
+  __syncthreads();
+  // W = R^{-1} by column-oriented back substitution (R w = e_c): for j = K - 1 .. 0, w_j = acc_j / R[j][j], then
+  // acc_i -= R[i][j] w_j for i < j.  Column c = tid / 4 is taken by the four lanes of a quad, lane s of the quad
+  // holding rows 4 q + s (q = 0 .. 15, so that the triangle's work is spread evenly); w_j comes from the lane that
+  // holds row j by a quad broadcast.  Every step updates all 16 rows of a lane: rows i >= j read the zeros of s_c
+  // and stay unchanged (they are final by then).  For columns c < j, acc_j stays 0 and so w_j = 0 (W is upper
+  // triangular).  Steps go in blocks of four (rows 4 J .. 4 J + 3), so that the broadcast's source lane is a
+  // constant; cur follows row 4 J + s through the block.
+  const int c = tid >> 2, sq = tid & 3;
+  constexpr int QR = K / 4;
+  double acc[QR];
 #pragma unroll
-  for (int i = K - 1; i >= 0; --i) {
-    double s = 0.0;
+  for (int q = 0; q < QR; ++q) acc[q] = 4 * q + sq == c ? 1.0 : 0.0;
+  double* W = a.hmat + (size_t)u * K * K + c;
+  for (int J = QR - 1; J >= 0; --J) {
+    double cur = acc[0];
 #pragma unroll
-    for (int m = i + 1; m < K; m += 2) {
-      // terms with m > c (where w_m = 0) are dropped by selecting the entry of R, so that an overflowed entry of
-      // R cannot turn 0 * inf into NaN
-      if (m + 1 < K) {
-        const double2 rm = *reinterpret_cast<const double2*>(&s_r[i * KP + m]);
-        s = fma(m <= lane ? rm.x : 0.0, w[m], s);
-        s = fma(m + 1 <= lane ? rm.y : 0.0, w[m + 1], s);
-      } else {
-        s = fma(m <= lane ? s_r[i * KP + m] : 0.0, w[m], s);
-      }
-    }
-    w[i] = i <= lane ? ((lane == i ? 1.0 : 0.0) - s) / s_r[i * KP + i] : 0.0;
+    for (int q = 1; q < QR; ++q) cur = q == J ? acc[q] : cur;
+    auto step = [&](auto tc) {
+      constexpr int t = decltype(tc)::value;
+      const int j = 4 * J + t;
+      const double wj = quad_bcast_f64<t>(cur * s_ri[j]);
+      W[(size_t)j * K] = wj;  // row j of W (the quad's four lanes store the same value: no branch in the loop)
+      const double* cj = s_c + j * KP + sq;
+#pragma unroll
+      for (int q = 0; q < QR; ++q) acc[q] = fma(-cj[4 * q], wj, acc[q]);
+      cur = fma(-cj[4 * J], wj, cur);
+    };
+    step(std::integral_constant<int, 3>{});
+    step(std::integral_constant<int, 2>{});
+    step(std::integral_constant<int, 1>{});
+    step(std::integral_constant<int, 0>{});
   }
-  // row-major W[i][c]: one row per store instruction
-  double* W = a.hmat + (size_t)u * K * K;
-#pragma unroll
-  for (int i = 0; i < K; ++i) W[(size_t)i * K + lane] = w[i];
 }
 
 size_t cqr_factor_lds(int k) { return (size_t)k * (k + 1) * sizeof(double); }
@@ -1555,7 +1595,7 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
   auto pass = [&](const double* src, double* dst, int first, uint32_t round) {
     if (a.k == 64) {
       hipLaunchKernelGGL(cqr_syrk<64>, sgrid, dim3(kCqrThreads), 0, stream, a, src, first, round);
-      hipLaunchKernelGGL(cqr_factor_reg64, dim3(a.num_units), dim3(kWave), 0, stream, a, first);
+      hipLaunchKernelGGL(cqr_factor_reg64, dim3(a.num_units), dim3(kCqrFactorThreads), 0, stream, a, first);
       hipLaunchKernelGGL(cqr_apply<64>, agrid, dim3(kCqrThreads), alds, stream, a, src, dst, first, round);
     } else {
       hipLaunchKernelGGL(cqr_syrk<128>, sgrid, dim3(kCqrThreads), 0, stream, a, src, first, round);
