@@ -752,8 +752,8 @@ __device__ __forceinline__ double block_sum(double v, double* s_red) {
 // kernels per pass, each spread over the unit's features except the k x k factorisation:
 //   cqr_scale   the perturbation size of each unit (first pass)
 //   cqr_syrk    partial S over 256 features per workgroup (register blocks over LDS tiles of 32 features)
-//   cqr_factor  one wave per unit: the partials summed in order, the shift, Cholesky and the inverse of R (k = 64
-//               in registers, k = 128 in LDS)
+//   cqr_factor  one workgroup per unit: the partials summed in order, the shift, Cholesky and the inverse of R
+//               (k = 64: the factorisation in one wave's registers, the inverse by four waves; k = 128: one wave, LDS)
 //   cqr_apply   X = Y R^{-1} for 64 features per workgroup (the tile is read whole before it is written, so the
 //               second pass runs in place)
 constexpr int kCqrThreads = 256, kCqrTile = 16, kCqrChunk = 256, kCqrSub = 32, kCqrRows = 64, kCqrWChunk = 32;
@@ -1197,46 +1197,87 @@ __global__ __launch_bounds__(kCqrThreads) void sub_rayleigh_sum(LayerFitArgs a) 
   }
 }
 
-// Residual of Ritz pair j of unit u: with w = X v_j (v_j from the eigensolver) and z = Y v_j = G w, the Rayleigh
-// quotient theta = w.z / w.w and ||z - theta w|| / ||w||, both in fp64 (the float32 Ritz vector puts the floor of this
-// residual near 1e-7 theta_1).  One workgroup per (j, unit); thread t owns features t + 256 q.
+// Residual check of the top-r Ritz pairs: w_j = X v_j, z_j = Y v_j = G w_j (Y = G X of the last product), theta_j =
+// w^T z / w^T w and resid_j = ||z - theta_j w|| / ||w|| = sqrt(z^T z - (w^T z)^2 / w^T w) / ||w||.  Each workgroup takes
+// 256 features of a unit and all r pairs (kCheckBatch at a time), so X and Y are read once per unit; it writes its
+// sums of w^T w, w^T z and z^T z over those features (in the syrk partials, free between the Rayleigh-Ritz sum and the
+// next Cholesky QR pass), and sub_check_sum adds the feature chunks in order.  The expanded form of the squared
+// residual carries the rounding of the sums, a few 1e-15 of z^T z; near the stopping tolerance (1e-6 of theta_1) the
+// squared residual is at least 1e-12 of z^T z, so the decision moves by well under 1 % of the tolerance.  (The float32
+// Ritz vectors put the residual's floor near 1e-7 theta_1.)
+constexpr int kCheckBatch = 16;
 __global__ __launch_bounds__(kLayerThreads) void sub_check(LayerFitArgs a) {
-  constexpr int MAXF = 1024 / kLayerThreads;
-  __shared__ double s_red[kLayerWaves];
-  __shared__ double s_v[128];
-  const int DL = a.pv.num_kv_heads * a.pv.head_dim, k = a.k;
-  const int j = blockIdx.x, u = blockIdx.y;
+  constexpr int B = kCheckBatch, NV = 3 * B;
+  __shared__ float s_v[B * 128];
+  __shared__ double s_red[kLayerWaves][NV];
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, k = a.k, r = a.rank;
+  const int chunk = blockIdx.x, u = blockIdx.y, tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   if (a.conv[u]) return;  // whole workgroup
-  const float* v = a.vrows + ((size_t)u * a.rank + j) * k;
-  for (int c = threadIdx.x; c < k; c += kLayerThreads) s_v[c] = (double)v[c];
-  __syncthreads();
+  const int nch = (DL + kLayerThreads - 1) / kLayerThreads;
+  const int f = chunk * kLayerThreads + tid;
   const double* X = a.x + (size_t)u * k * DL;
   const double* Y = a.y + (size_t)u * k * DL;
-  double w[MAXF], z[MAXF], ww = 0.0, wz = 0.0;
+  double* part = a.spart + ((size_t)u * nch + chunk) * r * 3;
+  for (int j0 = 0; j0 < r; j0 += B) {
+    const int nb = min(B, r - j0);
+    __syncthreads();
+    for (int e = tid; e < B * k; e += kLayerThreads)
+      s_v[e] = e < nb * k ? a.vrows[((size_t)u * r + j0) * k + e] : 0.0f;
+    __syncthreads();
+    double w[B], z[B];
 #pragma unroll
-  for (int q = 0; q < MAXF; ++q) {
-    const int f = threadIdx.x + q * kLayerThreads;
-    w[q] = z[q] = 0.0;
+    for (int jj = 0; jj < B; ++jj) w[jj] = z[jj] = 0.0;
     if (f < DL) {
       for (int c = 0; c < k; ++c) {
-        w[q] = fma(s_v[c], X[(size_t)c * DL + f], w[q]);
-        z[q] = fma(s_v[c], Y[(size_t)c * DL + f], z[q]);
+        const double x = X[(size_t)c * DL + f], y = Y[(size_t)c * DL + f];
+#pragma unroll
+        for (int jj = 0; jj < B; ++jj) {
+          const double v = (double)s_v[jj * k + c];
+          w[jj] = fma(v, x, w[jj]);
+          z[jj] = fma(v, y, z[jj]);
+        }
       }
     }
-    ww = fma(w[q], w[q], ww);
-    wz = fma(w[q], z[q], wz);
-  }
-  ww = block_sum<kLayerWaves>(ww, s_red);
-  wz = block_sum<kLayerWaves>(wz, s_red);
-  const double theta = ww > 0.0 ? wz / ww : 0.0;
-  double rr = 0.0;
+    // per-lane terms, summed over the wave by a fixed butterfly, then over the four waves in order
+    double t[NV];
 #pragma unroll
-  for (int q = 0; q < MAXF; ++q) {
-    const double e = fma(-theta, w[q], z[q]);
-    rr = fma(e, e, rr);
+    for (int jj = 0; jj < B; ++jj) {
+      t[3 * jj] = w[jj] * w[jj];
+      t[3 * jj + 1] = w[jj] * z[jj];
+      t[3 * jj + 2] = z[jj] * z[jj];
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1)
+#pragma unroll
+      for (int i = 0; i < NV; ++i) t[i] += __shfl_xor(t[i], o, kWave);
+    if (lane == 0)
+#pragma unroll
+      for (int i = 0; i < NV; ++i) s_red[wave][i] = t[i];
+    __syncthreads();
+    if (tid < 3 * nb) {
+      double sum = 0.0;
+#pragma unroll
+      for (int wv = 0; wv < kLayerWaves; ++wv) sum += s_red[wv][tid];
+      part[(size_t)j0 * 3 + tid] = sum;
+    }
   }
-  rr = block_sum<kLayerWaves>(rr, s_red);
-  if (threadIdx.x == 0) a.resid[(size_t)u * KVC_MAX_RANK + j] = ww > 0.0 ? sqrt(rr / ww) : 0.0;
+}
+
+// resid_j of unit u from the feature chunks' sums (in chunk order).
+__global__ __launch_bounds__(KVC_MAX_RANK) void sub_check_sum(LayerFitArgs a) {
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, r = a.rank;
+  const int u = blockIdx.x, j = threadIdx.x;
+  if (a.conv[u] || j >= r) return;
+  const int nch = (DL + kLayerThreads - 1) / kLayerThreads;
+  const double* part = a.spart + (size_t)u * nch * r * 3;
+  double ww = 0.0, wz = 0.0, zz = 0.0;
+  for (int ch = 0; ch < nch; ++ch) {
+    const double* p = part + ((size_t)ch * r + j) * 3;
+    ww += p[0];
+    wz += p[1];
+    zz += p[2];
+  }
+  a.resid[(size_t)u * KVC_MAX_RANK + j] = ww > 0.0 ? sqrt(fmax(zz - wz * (wz / ww), 0.0) / ww) : 0.0;
 }
 
 // Stop a unit once every top-r residual is at most kLayerTol * theta_1 (theta_1 = sigma_1^2 of the Ritz step), or at
@@ -1634,7 +1675,9 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((e = launch_eig(es, stream)) != hipSuccess) return e;
-    hipLaunchKernelGGL(sub_check, dim3(a.rank, a.num_units), dim3(kLayerThreads), 0, stream, a);
+    hipLaunchKernelGGL(sub_check, dim3((DL + kLayerThreads - 1) / kLayerThreads, a.num_units), dim3(kLayerThreads), 0,
+                       stream, a);
+    hipLaunchKernelGGL(sub_check_sum, dim3(a.num_units), dim3(KVC_MAX_RANK), 0, stream, a);
     hipLaunchKernelGGL(sub_decide, dim3(a.num_units), dim3(kWave), 0, stream, a, done, done >= kLayerMaxIters);
   }
   hipLaunchKernelGGL(sub_basis, dim3(a.rank, a.num_units), dim3(kLayerThreads), 0, stream, a);
