@@ -1025,10 +1025,14 @@ __global__ __launch_bounds__(kCqrFactorThreads) void cqr_factor_reg64(LayerFitAr
         }
       }
     }
-    // column c of R (lane c) for the inverse, clamped to finite values so that a zero never meets an infinity
+    // column c of R (lane c) for the inverse, infinities clamped to the largest finite values so that a zero never
+    // meets an infinity (a NaN from NaN input stays NaN)
 #pragma unroll
-    for (int i = 0; i < K; ++i)
-      s_c[lane * KP + i] = i < lane ? fmin(fmax(col[i], -1.7976931348623157e308), 1.7976931348623157e308) : 0.0;
+    for (int i = 0; i < K; ++i) {
+      constexpr double kMax = 1.7976931348623157e308;
+      const double x = col[i];
+      s_c[lane * KP + i] = i < lane ? (x == x ? fmin(fmax(x, -kMax), kMax) : x) : 0.0;
+    }
     s_ri[lane] = myinv;
   }
   __syncthreads();
