@@ -756,7 +756,7 @@ __device__ __forceinline__ double block_sum(double v, double* s_red) {
 //               (k = 64: the factorisation in one wave's registers, the inverse by four waves; k = 128: one wave, LDS)
 //   cqr_apply   X = Y R^{-1} for 64 features per workgroup (the tile is read whole before it is written, so the
 //               second pass runs in place)
-constexpr int kCqrThreads = 256, kCqrTile = 16, kCqrChunk = 256, kCqrSub = 32, kCqrRows = 64, kCqrWChunk = 32;
+constexpr int kCqrThreads = 256, kCqrChunk = 256, kCqrSub = 32, kCqrRows = 64, kCqrWChunk = 32;
 
 // The perturbed entry e of unit u's Y (every kernel of a pass forms it the same way).
 __device__ __forceinline__ double cqr_perturbed(double y, double eps, uint32_t round, int u, size_t e) {
