@@ -254,6 +254,52 @@ def test_fit_clustered_eigenvalues_fp32(d):
     assert teeth > 10 * TOL_CACHE["f32"]
 
 
+def test_fit_one_cluster_across_the_truncation_fp32():
+    """Z with 40 equal singular values and rank 16: the Gram's top eigenvalue has multiplicity 40, so all 16 computed
+    eigenvectors form one cluster of the eigensolver (orthogonalised together) and the rank-16 truncation is not
+    unique.  Checked is what every correct truncation shares (Eq. 7, Eckart-Young): sigma, orthonormal basis rows
+    inside the 40-dimensional singular subspace, A^T A = diag(sigma^2) and the optimal residual."""
+    H, T, r, p, d = 2, 512, 16, 40, 128
+    w = synth.WORKLOADS["tiny"].with_(num_layers=1, num_kv_heads=H, head_dim=d, seq_tokens=(T,), rank=r)
+    pc = synth.build_paged(w, device="cuda", num_output_agents=1)
+    src, dst = pc.seqs[(0, 0)], pc.seqs[(0, 1)]
+    g = torch.Generator().manual_seed(223)
+    t = torch.arange(T) + src.offset
+    td = torch.arange(T) + dst.offset
+    for pools in (pc.k_pools, pc.v_pools):
+        pool = pools[0]
+        for h in range(H):
+            u = torch.linalg.qr(torch.randn(T, p, generator=g, dtype=torch.float64))[0]
+            v = torch.linalg.qr(torch.randn(d, p, generator=g, dtype=torch.float64))[0]
+            x = pool[t // w.block_size, t % w.block_size, h].to("cpu", torch.float64)
+            pool[td // w.block_size, td % w.block_size, h] = (x + 3.0 * (u @ v.T)).to(pool.dtype).to(pool.device)
+    st = kvc.State.empty(1, H, d, T, r, torch.float32, "cuda")
+    tab = lambda s: None if pc.tables is None else pc.tables[[s.table_row]]
+    kvc.kvc_fit_state(kvc.Cache(pc.k_pools, pc.v_pools),
+                      kvc.Batch([T], [src.offset], [dst.offset], [st], tab(src), tab(dst)))
+    torch.cuda.synchronize()
+    cnp = Hp.oracle_cache(pc.k_pools, pc.v_pools, w.block_size)
+    gc = Hp.rows_f64(Hp.to_np_storage(st.coef), "f32")
+    gb = st.basis.cpu().numpy().astype(np.float64)
+    gs = st.sigma.cpu().numpy().astype(np.float64)
+    for kv in range(2):
+        for h in range(H):
+            z = (O.to_f64(O.read_rows(cnp, 0, kv, h, Hp.table_np(tab(dst), 0), dst.offset, T), "f32") -
+                 O.to_f64(O.read_rows(cnp, 0, kv, h, Hp.table_np(tab(src), 0), src.offset, T), "f32"))
+            _, sv, vt = np.linalg.svd(z, full_matrices=False)
+            assert sv[p - 1] - sv[p] > 0.5 * sv[0] and sv[0] - sv[p - 1] < 1e-4 * sv[0]  # one cluster of p
+            a, b, sig = gc[0, kv, h], gb[0, kv, h], gs[0, kv, h]
+            assert np.max(np.abs(sig - sv[:r])) <= 1e-4 * sv[0]
+            assert np.allclose(b @ b.T, np.eye(r), atol=2e-6)
+            span = vt[:p]
+            assert np.linalg.norm(b - (b @ span.T) @ span) <= 1e-4  # basis inside the singular subspace
+            ata = a.T @ a
+            assert np.max(np.abs(ata - np.diag(sig ** 2))) <= 1e-4 * sv[0] ** 2
+            resid = np.sum((z - a @ b) ** 2)
+            optimal = np.sum(sv[r:] ** 2)
+            assert abs(resid - optimal) <= 1e-4 * optimal, (kv, h, resid, optimal)
+
+
 def test_fit_is_deterministic():
     w = synth.WORKLOADS["llama8b_4k"].with_(num_layers=1, num_kv_heads=2, seq_tokens=(2000,), num_agents=2)
     pc = synth.build_paged(w, device="cuda")
