@@ -753,7 +753,8 @@ __device__ __forceinline__ double block_sum(double v, double* s_red) {
 //   cqr_scale   the perturbation size of each unit (first pass)
 //   cqr_syrk    partial S over 256 features per workgroup (register blocks over LDS tiles of 32 features)
 //   cqr_factor  one workgroup per unit: the partials summed in order, the shift, Cholesky and the inverse of R
-//               (k = 64: the factorisation in one wave's registers, the inverse by four waves; k = 128: one wave, LDS)
+//               (k = 64: the factorisation in one wave's registers, the inverse by four waves; k = 128: eight waves
+//               on the matrix in LDS)
 //   cqr_apply   X = Y R^{-1} for 64 features per workgroup (the tile is read whole before it is written, so the
 //               second pass runs in place)
 constexpr int kCqrThreads = 256, kCqrChunk = 256, kCqrSub = 32, kCqrRows = 64, kCqrWChunk = 32;
@@ -841,104 +842,6 @@ __global__ __launch_bounds__(kCqrThreads) void cqr_syrk(LayerFitArgs a, const do
 #pragma unroll
       for (int v = 0; v < 4; ++v)
         P[(qi * (K / 2) + 16 * i + lk + 4 * v) * K + qj * (K / 2) + 16 * j + li] = acc[i][j][v];
-}
-
-// One wave per unit; S in LDS with rows padded to K + 1.  Cholesky (upper, S = R^T R; a pivot that is not positive is
-// replaced by a tiny one), then R^{-1} in place column by column: column j of the inverse needs only the inverted
-// leading block and column j of R.  R^{-1} goes to hmat with zeros below the diagonal.
-template <int K>
-__global__ __launch_bounds__(kWave) void cqr_factor(LayerFitArgs a, int shifted) {
-  constexpr int KP = K + 1, NB = 8;  // LDS row pitch; loads issued in batches of NB ahead of their stores
-  extern __shared__ double fs[];     // [K][K + 1]
-  const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
-  const int u = blockIdx.x, tid = threadIdx.x;
-  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
-  const double* P = a.spart + (size_t)u * nch * K * K;
-  for (int e0 = tid; e0 < K * K; e0 += NB * kWave) {
-    double s[NB];
-#pragma unroll
-    for (int q = 0; q < NB; ++q) s[q] = 0.0;
-    for (int p = 0; p < nch; ++p)
-#pragma unroll
-      for (int q = 0; q < NB; ++q) s[q] += P[(size_t)p * K * K + e0 + q * kWave];
-#pragma unroll
-    for (int q = 0; q < NB; ++q) {
-      const int e = e0 + q * kWave;
-      fs[(e / K) * KP + e % K] = s[q];
-    }
-  }
-  __syncthreads();
-  if (shifted) {
-    double tr = 0.0;
-    for (int c = 0; c < K; ++c) tr += fs[c * KP + c];
-    const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
-    __syncthreads();
-    for (int c = tid; c < K; c += kWave) fs[c * KP + c] += shift;
-    __syncthreads();
-  }
-  // Cholesky: row j scaled by the pivot, then the trailing upper triangle updated column by column (one column per
-  // lane), NB rows at a time with every load of the batch before its stores
-  for (int j = 0; j < K; ++j) {
-    const double d = fs[j * KP + j];
-    const double rjj = sqrt(d > 1e-300 ? d : 1e-300);
-    __syncthreads();
-    for (int c = j + 1 + tid; c < K; c += kWave) fs[j * KP + c] /= rjj;
-    if (tid == 0) fs[j * KP + j] = rjj;
-    __syncthreads();
-    for (int c = j + 1 + tid; c < K; c += kWave) {
-      const double rjc = fs[j * KP + c];
-      for (int k0 = j + 1; k0 <= c; k0 += NB) {
-        double rj[NB], v[NB];
-#pragma unroll
-        for (int q = 0; q < NB; ++q) {
-          const int k = min(k0 + q, c);
-          rj[q] = fs[j * KP + k];
-          v[q] = fs[k * KP + c];
-        }
-#pragma unroll
-        for (int q = 0; q < NB; ++q)
-          if (k0 + q <= c) fs[(k0 + q) * KP + c] = v[q] - rj[q] * rjc;
-      }
-    }
-    __syncthreads();
-  }
-  // R^{-1} in place, column by column: V[r][j] = -(sum_{r <= l < j} V[r][l] R[l][j]) / R[j][j]
-  for (int j = 0; j < K; ++j) {
-    const double inv_jj = 1.0 / fs[j * KP + j];
-    double t[K / kWave];
-#pragma unroll
-    for (int m = 0; m < K / kWave; ++m) {
-      const int r = tid + m * kWave;
-      double acc[NB];
-#pragma unroll
-      for (int q = 0; q < NB; ++q) acc[q] = 0.0;
-      for (int l0 = r; l0 < j; l0 += NB) {
-#pragma unroll
-        for (int q = 0; q < NB; ++q) {
-          const int l = min(l0 + q, j - 1);
-          const double x = fs[r * KP + l] * fs[l * KP + j];
-          acc[q] += l0 + q < j ? x : 0.0;
-        }
-      }
-      double sum = 0.0;
-#pragma unroll
-      for (int q = 0; q < NB; ++q) sum += acc[q];
-      t[m] = sum;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int m = 0; m < K / kWave; ++m) {
-      const int r = tid + m * kWave;
-      if (r < j) fs[r * KP + j] = -t[m] * inv_jj;
-      if (r == j) fs[j * KP + j] = inv_jj;
-    }
-    __syncthreads();
-  }
-  double* W = a.hmat + (size_t)u * K * K;
-  for (int e = tid; e < K * K; e += kWave) {
-    const int i = e / K, j = e - i * K;
-    W[e] = i <= j ? fs[i * KP + j] : 0.0;
-  }
 }
 
 // k = 64: wave 0 factorises, lane c holding column c of S in registers (entries k <= c are used).  Step j takes the
@@ -1059,6 +962,113 @@ __global__ __launch_bounds__(kCqrFactorThreads) void cqr_factor_reg64(LayerFitAr
       const double wj = quad_bcast_f64<t>(cur * s_ri[j]);
       W[(size_t)j * K] = wj;  // row j of W (the quad's four lanes store the same value: no branch in the loop)
       const double* cj = s_c + j * KP + sq;
+#pragma unroll
+      for (int q = 0; q < QR; ++q) acc[q] = fma(-cj[4 * q], wj, acc[q]);
+      cur = fma(-cj[4 * J], wj, cur);
+    };
+    step(std::integral_constant<int, 3>{});
+    step(std::integral_constant<int, 2>{});
+    step(std::integral_constant<int, 1>{});
+    step(std::integral_constant<int, 0>{});
+  }
+}
+
+// k = 128 (ranks above 48): S in LDS with rows padded to K + 1, eight waves.  The right-looking Cholesky (upper,
+// S = R^T R; a pivot that is not positive is replaced by a tiny one) spreads each step's trailing update over 128
+// columns x 4 row groups and reads the pivot row unscaled, so a step needs one barrier: row j is scaled after it,
+// while the next step works on the rows below.  R^{-1} then comes by column-oriented back substitution as for k = 64
+// (four lanes per column, 32 rows per lane), with the columns of R copied into the lower triangle of the LDS matrix
+// so that each is contiguous.  (One wave for the whole factorisation took about 1 ms per launch at rank 64.)
+constexpr int kCqrFactor128Threads = 512;
+
+template <int K>
+__global__ __launch_bounds__(kCqrFactor128Threads) void cqr_factor(LayerFitArgs a, int shifted) {
+  constexpr int KP = K + 1, NB = 8, NT = kCqrFactor128Threads;
+  static_assert(NT == 4 * K && (K * K) % (NB * NT) == 0, "four lanes per column; whole load batches");
+  extern __shared__ double fs[];  // [K][K + 1]
+  __shared__ double s_ri[K];      // 1 / R[j][j]
+  const int DL = a.pv.num_kv_heads * a.pv.head_dim, nch = (DL + kCqrChunk - 1) / kCqrChunk;
+  const int u = blockIdx.x, tid = threadIdx.x;
+  if (a.conv[u]) return;  // whole workgroup: the unit has stopped
+  const double* P = a.spart + (size_t)u * nch * K * K;
+  for (int e0 = tid; e0 < K * K; e0 += NB * NT) {
+    double s[NB];
+#pragma unroll
+    for (int q = 0; q < NB; ++q) s[q] = 0.0;
+    for (int p = 0; p < nch; ++p)
+#pragma unroll
+      for (int q = 0; q < NB; ++q) s[q] += P[(size_t)p * K * K + e0 + q * NT];
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+      const int e = e0 + q * NT;
+      fs[(e / K) * KP + e % K] = s[q];
+    }
+  }
+  __syncthreads();
+  if (shifted) {
+    double tr = 0.0;
+    for (int c = 0; c < K; ++c) tr += fs[c * KP + c];
+    const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
+    __syncthreads();
+    for (int c = tid; c < K; c += NT) fs[c * KP + c] += shift;
+    __syncthreads();
+  }
+  // Cholesky: thread (column cc, row group hg) updates S[k][cc] -= S[j][k] S[j][cc] / d for j < k <= cc, k = hg mod 4,
+  // NB rows at a time with every load of the batch before its stores
+  const int cc = tid & (K - 1), hg = tid / K;
+  for (int j = 0; j < K; ++j) {
+    const double d0 = fs[j * KP + j];
+    const double d = d0 > 1e-300 ? d0 : 1e-300;
+    const double y0 = __builtin_amdgcn_rsq(d);
+    const double inv = y0 * fma(-0.5 * d * y0, y0, 1.5);  // 1 / sqrt(d), relative error about 2^-47
+    if (cc > j) {
+      const double sjc = fs[j * KP + cc] * (inv * inv);
+      for (int k0 = j + 1 + ((hg - j - 1) & 3); k0 <= cc; k0 += 4 * NB) {
+        double rj[NB], v[NB];
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+          const int k = k0 + 4 * q <= cc ? k0 + 4 * q : k0;
+          rj[q] = fs[j * KP + k];
+          v[q] = fs[k * KP + cc];
+        }
+#pragma unroll
+        for (int q = 0; q < NB; ++q)
+          if (k0 + 4 * q <= cc) fs[(k0 + 4 * q) * KP + cc] = v[q] - rj[q] * sjc;
+      }
+    }
+    __syncthreads();
+    if (tid == 0) s_ri[j] = inv;
+    if (j + tid < K) fs[j * KP + j + tid] = tid == 0 ? d * inv : fs[j * KP + j + tid] * inv;
+  }
+  __syncthreads();
+  // column j of R into row j left of the diagonal: fs[j KP + i] = R[i][j] for i < j
+  for (int e = tid; e < K * K; e += NT) {
+    const int j = e / K, i = e - j * K;
+    if (i < j) fs[j * KP + i] = fs[i * KP + j];
+  }
+  __syncthreads();
+  // W = R^{-1}, R w = e_c: for j = K - 1 .. 0, w_j = acc_j / R[j][j], then acc_i -= R[i][j] w_j for i < j.  Column
+  // c = tid / 4 by the four lanes of a quad, lane s holding rows 4 q + s (q < 32); w_j by a quad broadcast from the
+  // lane that holds row j.  Row j of the LDS matrix holds R[i][j] for i < j, then R[j][j] and row j of R: rows i >= j
+  // take those values too, but they are final by then and the updates are never used.  For columns c < j, acc_j
+  // stays 0 and so w_j = 0 (W is upper triangular).  Steps go in blocks of four so that the broadcast's source lane
+  // is a constant; cur follows row 4 J + s through the block.
+  const int c = tid >> 2, sq = tid & 3;
+  constexpr int QR = K / 4;
+  double acc[QR];
+#pragma unroll
+  for (int q = 0; q < QR; ++q) acc[q] = 4 * q + sq == c ? 1.0 : 0.0;
+  double* W = a.hmat + (size_t)u * K * K + c;
+  for (int J = QR - 1; J >= 0; --J) {
+    double cur = acc[0];
+#pragma unroll
+    for (int q = 1; q < QR; ++q) cur = q == J ? acc[q] : cur;
+    auto step = [&](auto tc) {
+      constexpr int t = decltype(tc)::value;
+      const int j = 4 * J + t;
+      const double wj = quad_bcast_f64<t>(cur * s_ri[j]);
+      W[(size_t)j * K] = wj;  // row j of W (the quad's four lanes store the same value: no branch in the loop)
+      const double* cj = fs + j * KP + sq;
 #pragma unroll
       for (int q = 0; q < QR; ++q) acc[q] = fma(-cj[4 * q], wj, acc[q]);
       cur = fma(-cj[4 * J], wj, cur);
@@ -1644,7 +1654,7 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
       hipLaunchKernelGGL(cqr_apply<64>, agrid, dim3(kCqrThreads), alds, stream, a, src, dst, first, round);
     } else {
       hipLaunchKernelGGL(cqr_syrk<128>, sgrid, dim3(kCqrThreads), 0, stream, a, src, first, round);
-      hipLaunchKernelGGL(cqr_factor<128>, dim3(a.num_units), dim3(kWave), flds, stream, a, first);
+      hipLaunchKernelGGL(cqr_factor<128>, dim3(a.num_units), dim3(kCqrFactor128Threads), flds, stream, a, first);
       hipLaunchKernelGGL(cqr_apply<128>, agrid, dim3(kCqrThreads), alds, stream, a, src, dst, first, round);
     }
   };
