@@ -650,8 +650,8 @@ __global__ __launch_bounds__(kLayerThreads) void sub_init(LayerFitArgs a) {
   a.y[(size_t)u * a.k * DL + e] = hash_uniform((uint32_t)u, (uint32_t)(e / DL), (uint32_t)(e % DL));
 }
 
-// Y = G X (fp64) for every unit on the matrix cores: a 64 x 64 tile of Y (features x columns) per workgroup of four
-// waves, each wave a 32 x 32 quarter as 2 x 2 products v_mfma_f64_16x16x4_f64 (operands: lane l holds A[l % 16][l / 16]
+// Y = G X (fp64) for every unit on the matrix cores: a 128 x 64 tile of Y (features x columns) per workgroup of eight
+// waves, each wave a 32 x 32 block as 2 x 2 products v_mfma_f64_16x16x4_f64 (operands: lane l holds A[l % 16][l / 16]
 // and B[l / 16][l % 16]; result element v of lane l is D[l / 16 + 4 v][l % 16]).  16-wide slices of G and X are
 // staged in LDS, the next slices loaded into registers while the current ones are multiplied.
 constexpr int kGemmRows = 128, kGemmCols = 64, kGemmK = 16, kGemmMI = 2, kGemmNJ = 2;
