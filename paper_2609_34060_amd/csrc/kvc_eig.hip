@@ -577,36 +577,42 @@ __global__ __launch_bounds__(kEigThreads) __attribute__((amdgpu_waves_per_eu(8))
       const int j = j0 + tid;
       if (tid < kInvBatch && j < r) {
         const double lam = s_lam[j];
-        // LDL^T of T - lam I without pivoting (tiny pivots replaced): invd[i] = 1 / d_i; pseudo-random start.
-        // The recurrences below read T and the scratch in chunks loaded ahead of the chunk's stores, so one LDS
-        // round trip serves a chunk instead of each step waiting for its own loads behind the previous store.
+        // LDL^T of T - lam I without pivoting (tiny pivots replaced): invd[i] = 1 / d_i, in one pass with the
+        // pseudo-random start x and the first solve's forward substitution z_i = x_i - b_{i-1} z_{i-1} / d_{i-1}
+        // (which needs 1 / d_{i-1} only), so the start is never stored and the forward chain and the start's hash
+        // run beside the reciprocals.  The recurrences read T and the scratch in chunks loaded ahead of the chunk's
+        // stores, so one LDS round trip serves a chunk instead of each step waiting for its own loads behind the
+        // previous store.
         static_assert(N % 4 == 0, "whole chunks");
-        double id = 0.0;
-        for (int i0 = 0; i0 < N; i0 += 4) {
-          double av[4], bv[4];
+        {
+          double id = 0.0, z = 0.0;
+          for (int i0 = 0; i0 < N; i0 += 4) {
+            double av[4], bv[4];
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            av[t] = s_a[i0 + t];
-            bv[t] = s_b[i0 + t > 0 ? i0 + t - 1 : 0];
-          }
+            for (int t = 0; t < 4; ++t) {
+              av[t] = s_a[i0 + t];
+              bv[t] = s_b[i0 + t > 0 ? i0 + t - 1 : 0];
+            }
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            double d = i0 + t > 0 ? (av[t] - lam) - bv[t] * id * bv[t] : av[t] - lam;
-            if (fabs(d) < piv) d = copysign(piv, d);
-            id = recip(d);
-            invd[(i0 + t) * kInvBatch + tid] = id;
+            for (int t = 0; t < 4; ++t) {
+              const int i = i0 + t;
+              const uint32_t h = hash3(a.seed ^ (uint32_t)u, (uint32_t)j, (uint32_t)i);
+              const double x0 = (double)(h >> 11) * (1.0 / 2097152.0) - 1.0;
+              z = i > 0 ? x0 - bv[t] * id * z : x0;
+              xv[i * kInvBatch + tid] = z;
+              double d = i > 0 ? (av[t] - lam) - bv[t] * id * bv[t] : av[t] - lam;
+              if (fabs(d) < piv) d = copysign(piv, d);
+              id = recip(d);
+              invd[i * kInvBatch + tid] = id;
+            }
           }
         }
-#pragma unroll 4
-        for (int i = 0; i < N; ++i) {
-          const uint32_t h = hash3(a.seed ^ (uint32_t)u, (uint32_t)j, (uint32_t)i);
-          xv[i * kInvBatch + tid] = (double)(h >> 11) * (1.0 / 2097152.0) - 1.0;
-        }
-        // kInvSolves solves (T - lam I) x_new = x; each right-hand side is scaled by 1 / max|x| on the way in
+        // kInvSolves solves (T - lam I) x_new = x; each right-hand side is scaled by 1 / max|x| on the way in (the
+        // first solve's forward substitution is done above, with scale 1)
         double sc = 1.0;
         for (int itr = 0; itr < kInvSolves; ++itr) {
           double z = 0.0;
-          for (int i0 = 0; i0 < N; i0 += 4) {
+          for (int i0 = 0; itr > 0 && i0 < N; i0 += 4) {
             double xw[4], bw[4], iw[4];
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
