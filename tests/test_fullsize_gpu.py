@@ -219,13 +219,15 @@ def test_fullsize_rotary_fit_and_apply_32k():
     assert worst <= TOL["bf16"], worst
 
 
-def test_fullsize_per_layer_fit_and_apply_32k():
-    """The per-layer factorisation at the 8B/32K shapes (D = 1024, rank 32) as the benchmark times it, on a planted
-    per-layer deviation of rank 32 (orthonormal factors over all heads, RMS 0.25, N(0, 1e-3^2) noise) so that the
-    truncation is well defined; the oracle refits a sampled layer (32768 x 1024 SVD per K/V)."""
+@pytest.mark.parametrize("r", [32, 64])
+def test_fullsize_per_layer_fit_and_apply_32k(r):
+    """The per-layer factorisation at the 8B/32K shapes (D = 1024) as the benchmark times it (rank 32: 64 subspace
+    columns) and at rank 64 (128 columns, the eight-wave Cholesky factor), on a planted per-layer deviation of rank r
+    (orthonormal factors over all heads, RMS 0.25, N(0, 1e-3^2) noise) so that the truncation is well defined; the
+    oracle refits a sampled layer (32768 x 1024 SVD per K/V)."""
     w = synth.WORKLOADS["llama8b_32k"].with_(num_agents=2)
     pc = synth.build_paged(w, device="cuda", num_output_agents=1)
-    L, H, d, T, r = w.num_layers, w.num_kv_heads, w.head_dim, w.seq_tokens[0], 32
+    L, H, d, T = w.num_layers, w.num_kv_heads, w.head_dim, w.seq_tokens[0]
     src, dst, out = pc.seqs[(0, 0)], pc.seqs[(0, 1)], pc.seqs[(0, 100)]
     g = torch.Generator(device="cuda").manual_seed(81)
     for pools in (pc.k_pools, pc.v_pools):
@@ -265,5 +267,5 @@ def test_fullsize_per_layer_fit_and_apply_32k():
             gr = O.to_f64(O.read_rows(got, 0, kv, h, Hp.table_np(tab(out), 0), out.offset, T), "bf16")
             e = O.to_f64(O.read_rows(ref, 0, kv, h, Hp.table_np(tab(out), 0), out.offset, T), "bf16")
             worst = max(worst, O.max_relative_error(gr, e))
-    print(f"llama8b_32k per-layer: sigma err {es:.2e}, cache err {worst:.2e}")
+    print(f"llama8b_32k per-layer rank {r}: sigma err {es:.2e}, cache err {worst:.2e}")
     assert es <= 1e-4 and worst <= TOL["bf16"], (es, worst)
