@@ -1674,7 +1674,9 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
   while (done < kLayerMaxIters) {
     const int n = done == 0 ? kLayerFirstIters : kLayerCheckEvery;
     for (int it = 0; it < n; ++it) {
-      hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kGemmThreads), 0, stream, a);
+      // after a Rayleigh-Ritz step Y already holds G X for this X (the Ritz step, the residual check and the
+      // decision read X and Y and write neither), so the first product of every later round is that one
+      if (done == 0 || it > 0) hipLaunchKernelGGL(sub_gemm, ggrid, dim3(kGemmThreads), 0, stream, a);
       orth((uint32_t)(++done), it + 1 == n);
     }
     // Rayleigh-Ritz on span(X) and the residuals of its top-r pairs (Y = G X is kept by the Ritz step)
