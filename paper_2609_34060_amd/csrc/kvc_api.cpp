@@ -228,7 +228,10 @@ LayerPlan plan_layer_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int
   p.k = rmax + 16 <= 64 ? 64 : 128;
   const size_t DL = static_cast<size_t>(c->num_kv_heads) * c->head_dim, k = p.k;
   p.units = static_cast<size_t>(p.layers_per_group) * 2;
-  int64_t part = (std::max<int32_t>(tmax, 1) + 7) / 8;
+  // four token ranges per unit (at least 256 tokens each): fewer fp32 partials to write and to reduce (8192-token
+  // ranges at 32K tokens), while the LDS Gram still runs one workgroup per unit, token range and pair of 256-feature
+  // groups (40 per unit at D = 1024)
+  int64_t part = (std::max<int32_t>(tmax, 1) + 3) / 4;
   part = std::max<int64_t>(256, (part + 31) / 32 * 32);
   p.part_tokens = static_cast<int32_t>(part);
   p.max_parts = static_cast<int32_t>(std::max<int64_t>(1, (tmax + part - 1) / part));
