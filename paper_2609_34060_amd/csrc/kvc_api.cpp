@@ -228,10 +228,13 @@ LayerPlan plan_layer_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int
   p.k = rmax + 16 <= 64 ? 64 : 128;
   const size_t DL = static_cast<size_t>(c->num_kv_heads) * c->head_dim, k = p.k;
   p.units = static_cast<size_t>(p.layers_per_group) * 2;
-  // four token ranges per unit (at least 256 tokens each): fewer fp32 partials to write and to reduce (8192-token
-  // ranges at 32K tokens), while the LDS Gram still runs one workgroup per unit, token range and pair of 256-feature
-  // groups (40 per unit at D = 1024)
-  int64_t part = (std::max<int32_t>(tmax, 1) + 3) / 4;
+  // token ranges per unit: enough for about 1024 workgroups of the LDS Gram (one per unit, token range and pair of
+  // 256-feature groups), at least two and at least 256 tokens each; more ranges than that only add fp32 partials to
+  // write and to reduce (8B/32K, 64 units: two 16384-token ranges, 1280 workgroups)
+  const int64_t ng = static_cast<int64_t>((DL + 255) / 256);
+  const int64_t per_range = static_cast<int64_t>(p.units) * ng * (ng + 1) / 2;
+  const int64_t nranges = std::max<int64_t>(2, (1024 + per_range - 1) / per_range);
+  int64_t part = (std::max<int32_t>(tmax, 1) + nranges - 1) / nranges;
   part = std::max<int64_t>(256, (part + 31) / 32 * 32);
   p.part_tokens = static_cast<int32_t>(part);
   p.max_parts = static_cast<int32_t>(std::max<int64_t>(1, (tmax + part - 1) / part));
