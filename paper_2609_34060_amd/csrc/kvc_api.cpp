@@ -254,7 +254,7 @@ LayerPlan plan_layer_fit(const kvc_cache* c, const kvc_batch* b, int32_t lb, int
   p.off_spart = off;
   off = align256(off + U * ((DL + 255) / 256) * k * k * sizeof(double));
   p.off_eps = off;
-  off = align256(off + U * sizeof(double));
+  off = align256(off + 2 * U * sizeof(double));
   p.off_vrows = off;
   off = align256(off + U * KVC_MAX_RANK * k * sizeof(float));
   p.off_vsigma = off;

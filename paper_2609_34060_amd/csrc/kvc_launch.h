@@ -87,7 +87,7 @@ struct LayerFitArgs {
   double* y;                   // [unit][k][D]
   double* hmat;                // [unit][k][k]; during the iteration R^{-1} of the Cholesky QR
   double* spart;               // [unit][ceil(D / 256)][k][k] partial Y^T Y of the Cholesky QR
-  double* eps;                 // [unit] perturbation size of the Cholesky QR
+  double* eps;                 // [2][unit] perturbation size of the Cholesky QR, by round parity
   float* vrows;                // [unit][rank][k] eigenvectors of hmat (rows)
   float* vsigma;               // [unit][rank]
   double* resid;               // [unit][KVC_MAX_RANK] residual norms of the Ritz pairs of the last check

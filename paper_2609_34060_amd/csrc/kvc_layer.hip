@@ -765,7 +765,7 @@ __device__ __forceinline__ double cqr_perturbed(double y, double eps, uint32_t r
 }
 
 constexpr int kScaleThreads = 1024;
-__global__ __launch_bounds__(kScaleThreads) void cqr_scale(LayerFitArgs a) {
+__global__ __launch_bounds__(kScaleThreads) void cqr_scale(LayerFitArgs a, uint32_t round) {
   constexpr int NB = 8;
   __shared__ double red[kScaleThreads / kWave];
   const int DL = a.pv.num_kv_heads * a.pv.head_dim, u = blockIdx.x;
@@ -787,7 +787,7 @@ __global__ __launch_bounds__(kScaleThreads) void cqr_scale(LayerFitArgs a) {
   for (int q = 0; q < NB; ++q) s += ss[q];
   s = block_sum<kScaleThreads / kWave>(s, red);
   const double rms = sqrt(s / (double)n);
-  if (threadIdx.x == 0) a.eps[u] = rms > 0.0 ? 1e-12 * rms : 1.0;
+  if (threadIdx.x == 0) a.eps[(round & 1u) * a.num_units + u] = rms > 0.0 ? 1e-12 * rms : 1.0;
 }
 
 template <int K>
@@ -805,7 +805,7 @@ __global__ __launch_bounds__(kCqrThreads) void cqr_syrk(LayerFitArgs a, const do
   const int lane = tid & 63, wave = tid >> 6, qi = wave >> 1, qj = wave & 1, li = lane & 15, lk = lane >> 4;
   const int f_begin = chunk * kCqrChunk, f_end = min(DL, f_begin + kCqrChunk);
   const double* Y = src + (size_t)u * K * DL;
-  const double eps = perturb ? a.eps[u] : 0.0;
+  const double eps = perturb ? a.eps[(round & 1u) * a.num_units + u] : 0.0;
   f64x4 acc[T][T];
 #pragma unroll
   for (int i = 0; i < T; ++i)
@@ -874,7 +874,16 @@ __device__ __forceinline__ double quad_bcast_f64(double x) {
 
 constexpr int kCqrFactorThreads = 256;
 
-__global__ __launch_bounds__(kCqrFactorThreads) void cqr_factor_reg64(LayerFitArgs a, int shifted) {
+// The perturbation size of the next round's shifted pass, 1e-12 of the RMS of Y, from this shifted pass's trace of
+// S = ||Y||_F^2: from the third round on, Y = G X in consecutive rounds with X of full rank and columns of about unit
+// norm, so consecutive products have the same scale (the first two rounds measure Y itself: the random start, then
+// the first product).  Slot (round + 1) mod 2 of eps; this round's passes read slot round mod 2.
+__device__ __forceinline__ void cqr_next_eps(const LayerFitArgs& a, int u, uint32_t round, double tr, int DL, int K) {
+  const double rms = sqrt(fmax(tr, 0.0) / ((double)DL * K));
+  a.eps[((round + 1u) & 1u) * a.num_units + u] = rms > 0.0 ? 1e-12 * rms : 1.0;
+}
+
+__global__ __launch_bounds__(kCqrFactorThreads) void cqr_factor_reg64(LayerFitArgs a, int shifted, uint32_t round) {
   constexpr int K = 64, KP = K + 2;  // row stride: even, so that 16-byte loads stay aligned
   __shared__ __attribute__((aligned(16))) double s_r[K * KP];  // rows of R (the factorisation)
   __shared__ __attribute__((aligned(16))) double s_c[K * KP];  // columns of R above the diagonal, 0 on and below it
@@ -900,6 +909,7 @@ __global__ __launch_bounds__(kCqrFactorThreads) void cqr_factor_reg64(LayerFitAr
       double tr = 0.0;
 #pragma unroll
       for (int c = 0; c < K; ++c) tr += readlane_f64(d, c);
+      if (round >= 1u && lane == 0) cqr_next_eps(a, u, round, tr, DL, K);
       const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
 #pragma unroll
       for (int k = 0; k < K; ++k) col[k] += k == lane ? shift : 0.0;
@@ -982,7 +992,7 @@ __global__ __launch_bounds__(kCqrFactorThreads) void cqr_factor_reg64(LayerFitAr
 constexpr int kCqrFactor128Threads = 512;
 
 template <int K>
-__global__ __launch_bounds__(kCqrFactor128Threads) void cqr_factor(LayerFitArgs a, int shifted) {
+__global__ __launch_bounds__(kCqrFactor128Threads) void cqr_factor(LayerFitArgs a, int shifted, uint32_t round) {
   constexpr int KP = K + 1, NB = 8, NT = kCqrFactor128Threads;
   static_assert(NT == 4 * K && (K * K) % (NB * NT) == 0, "four lanes per column; whole load batches");
   extern __shared__ double fs[];  // [K][K + 1]
@@ -1008,6 +1018,7 @@ __global__ __launch_bounds__(kCqrFactor128Threads) void cqr_factor(LayerFitArgs 
   if (shifted) {
     double tr = 0.0;
     for (int c = 0; c < K; ++c) tr += fs[c * KP + c];
+    if (round >= 1u && tid == 0) cqr_next_eps(a, u, round, tr, DL, K);
     const double shift = 11.0 * ((double)DL * K + (double)K * (K + 1)) * 1.1102230246251565e-16 * tr;
     __syncthreads();
     for (int c = tid; c < K; c += NT) fs[c * KP + c] += shift;
@@ -1097,7 +1108,7 @@ __global__ __launch_bounds__(kCqrThreads) void cqr_apply(LayerFitArgs a, const d
   if (a.conv[u]) return;  // whole workgroup: the unit has stopped
   const double* Y = src + (size_t)u * K * DL;
   const double* W = a.hmat + (size_t)u * K * K;
-  const double eps = perturb ? a.eps[u] : 0.0;
+  const double eps = perturb ? a.eps[(round & 1u) * a.num_units + u] : 0.0;
   for (int e = tid; e < K * kCqrRows; e += kCqrThreads) {
     const int c = e / kCqrRows, ff = e - c * kCqrRows;
     const size_t idx = (size_t)c * DL + f0 + ff;
@@ -1650,11 +1661,12 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
   auto pass = [&](const double* src, double* dst, int first, uint32_t round) {
     if (a.k == 64) {
       hipLaunchKernelGGL(cqr_syrk<64>, sgrid, dim3(kCqrThreads), 0, stream, a, src, first, round);
-      hipLaunchKernelGGL(cqr_factor_reg64, dim3(a.num_units), dim3(kCqrFactorThreads), 0, stream, a, first);
+      hipLaunchKernelGGL(cqr_factor_reg64, dim3(a.num_units), dim3(kCqrFactorThreads), 0, stream, a, first, round);
       hipLaunchKernelGGL(cqr_apply<64>, agrid, dim3(kCqrThreads), alds, stream, a, src, dst, first, round);
     } else {
       hipLaunchKernelGGL(cqr_syrk<128>, sgrid, dim3(kCqrThreads), 0, stream, a, src, first, round);
-      hipLaunchKernelGGL(cqr_factor<128>, dim3(a.num_units), dim3(kCqrFactor128Threads), flds, stream, a, first);
+      hipLaunchKernelGGL(cqr_factor<128>, dim3(a.num_units), dim3(kCqrFactor128Threads), flds, stream, a, first,
+                         round);
       hipLaunchKernelGGL(cqr_apply<128>, agrid, dim3(kCqrThreads), alds, stream, a, src, dst, first, round);
     }
   };
@@ -1662,7 +1674,8 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
   // Rayleigh-Ritz steps X only has to keep full rank (the iteration depends on span(X) alone), so the exact pass runs
   // before each Rayleigh-Ritz step only.
   auto orth = [&](uint32_t round, bool exact) {
-    hipLaunchKernelGGL(cqr_scale, dim3(a.num_units), dim3(kScaleThreads), 0, stream, a);
+    // the perturbation size: measured on Y in the first two rounds, then set by the previous round's factorisation
+    if (round <= 1u) hipLaunchKernelGGL(cqr_scale, dim3(a.num_units), dim3(kScaleThreads), 0, stream, a, round);
     pass(a.y, a.x, 1, round);
     if (exact) pass(a.x, a.x, 0, round);
   };
