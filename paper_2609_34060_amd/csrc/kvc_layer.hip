@@ -1679,7 +1679,7 @@ hipError_t launch_layer_subspace(const LayerFitArgs& a, const EigArgs& ea, hipSt
     pass(a.y, a.x, 1, round);
     if (exact) pass(a.x, a.x, 0, round);
   };
-  orth(0u, true);
+  orth(0u, false);  // the random start is well conditioned, and X only has to keep full rank until the first check
   const dim3 ggrid((DL + kGemmRows - 1) / kGemmRows, a.k / kGemmCols, a.num_units);
   EigArgs es = ea;
   es.skip = a.conv;  // units that have stopped keep the Ritz pairs of their last check
